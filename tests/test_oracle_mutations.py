@@ -1,0 +1,180 @@
+"""Planted mistakes: each deliberately broken copy of an oracle routine must
+fail at least one pin.  The mistakes are planted in the oracle, on the CPU,
+through pytest's monkeypatch; nothing here touches the GPU library."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle.lapsum_oracle as O
+import pins
+
+_F64 = np.float64
+
+
+def _bad_cdf_sign(u):
+    u = np.asarray(u, dtype=_F64)
+    out = np.empty_like(u)
+    neg = u <= 0.0
+    out[neg] = 0.5 * np.exp(-u[neg])          # wrong exponent sign
+    out[~neg] = 1.0 - 0.5 * np.exp(u[~neg])
+    return out
+
+
+def _bad_cdf_branch(u):
+    u = np.asarray(u, dtype=_F64)
+    out = np.empty_like(u)
+    neg = u < -0.5                            # wrong branch point
+    out[neg] = 0.5 * np.exp(u[neg])
+    out[~neg] = 1.0 - 0.5 * np.exp(-u[~neg])
+    return out
+
+
+_orig_node_curve = O._node_curve
+_orig_gap_root = O._gap_root
+_orig_bracket_ranks = O.bracket_ranks
+_orig_partition = O.partition
+_orig_vjp = O.vjp
+
+
+def _bad_node_full_E(s, t, n_above, above, below):
+    logP, logQ, N = _orig_node_curve(s, t, n_above, above, below)
+    i = np.arange(1, s.size + 1, dtype=_F64)
+    E = 2.0 * (N - n_above - i + 0.5 * np.exp(logP))
+    return logP, logQ, n_above + i - 0.5 * np.exp(logP) + E     # dropped the 1/2 on E
+
+
+def _bad_node_inclusive_E(s, t, n_above, above, below):
+    logP, logQ, N = _orig_node_curve(s, t, n_above, above, below)
+    i = np.arange(1, s.size + 1, dtype=_F64)
+    return logP, logQ, n_above + i - 0.5 * np.exp(logP) + 0.5 * np.exp(logQ)  # inclusive suffix
+
+
+def _bad_node_rank(s, t, n_above, above, below):
+    logP, logQ, N = _orig_node_curve(s, t, n_above, above, below)
+    return logP, logQ, N - 1.0                # 0-based rank
+
+
+def _bad_gap_sign(k, t, c_up, up, down):
+    return _orig_gap_root(2.0 * c_up - k if up is not None and down is not None else k, t, c_up, up, down)
+
+
+def _bad_vjp_unnormalised(r, b, alpha, g):
+    t = -float(alpha)
+    r = np.asarray(r, _F64).ravel()
+    g = np.asarray(g, _F64).ravel()
+    f = np.exp(-np.abs(b - r) / t) / (2.0 * t)
+    return f * (g - math.fsum(g * f))         # q = f, not f / sum f
+
+
+def _bad_vjp_scale(r, b, alpha, g):
+    return 2.0 * _orig_vjp(r, b, alpha, g)    # f without the 1/(2t)... off by 2
+
+
+def _bad_ranks_sd(n, k, K, z):
+    q = (n - k) / n
+    sd = math.sqrt(K * q)                     # dropped (1 - q)
+    return math.floor(K * q - z * sd), math.ceil(K * q + z * sd), q
+
+
+def _bad_ranks_q(n, k, K, z):
+    q = k / n                                 # transposed quantile
+    sd = math.sqrt(K * q * (1.0 - q))
+    return math.floor(K * q - z * sd), math.ceil(K * q + z * sd), q
+
+
+def _bad_partition_closed(r32, a_L, a_R, t):
+    r32 = np.asarray(r32, np.float32).ravel()
+    p = _orig_partition(r32, a_L, a_R, t)
+    inL = r32 <= np.float32(a_L)              # wrong boundary side
+    p.n_L = int(inL.sum())
+    p.m_idx = np.nonzero(~inL & (r32 < np.float32(a_R)))[0]
+    p.n_M = int(p.m_idx.size)
+    return p
+
+
+def _bad_partition_tail_sign(r32, a_L, a_R, t):
+    p = _orig_partition(r32, a_L, a_R, t)
+    r = np.asarray(r32, np.float32).ravel().astype(_F64)
+    inR = r >= np.float32(a_R)
+    p.T_R = math.fsum(np.exp(-(r[inR] - a_R) / t) * 0.5)  # halved tail
+    return p
+
+
+def _bad_widen(a_L, a_R, side):
+    aL, aR = float(np.float32(a_L)), float(np.float32(a_R))
+    if side == "right":
+        aL = aR
+        aR = aR + 2.0 * (aR - aL)             # uses the updated a_L
+    else:
+        aR = aL
+        aL = aL - 2.0 * (aR - aL)
+    return float(np.float32(aL)), float(np.float32(aR))
+
+
+def _bad_order_stat(y32, j):
+    K = y32.size
+    if j < 0:
+        return -math.inf
+    if j >= K:
+        return math.inf
+    return float(np.sort(np.asarray(y32, np.float32))[j])   # 0-based
+
+
+def _bad_sampler(r32, noise32):
+    r32 = np.asarray(r32, np.float32).ravel()
+    eps = np.asarray(noise32, np.float32).ravel()
+    stride = -(-r32.size // eps.size)         # ceil instead of floor
+    idx = np.minimum(np.arange(eps.size) * stride, r32.size - 1)
+    return (r32[idx] + eps).astype(np.float32)
+
+
+MUTANTS = {
+    "cdf_sign": ("laplace_cdf", _bad_cdf_sign),
+    "cdf_branch": ("laplace_cdf", _bad_cdf_branch),
+    "node_E_half_dropped": ("_node_curve", _bad_node_full_E),
+    "node_E_inclusive": ("_node_curve", _bad_node_inclusive_E),
+    "node_rank_off_by_one": ("_node_curve", _bad_node_rank),
+    "gap_root_sign": ("_gap_root", _bad_gap_sign),
+    "vjp_unnormalised_q": ("vjp", _bad_vjp_unnormalised),
+    "vjp_scale": ("vjp", _bad_vjp_scale),
+    "ranks_sd": ("bracket_ranks", _bad_ranks_sd),
+    "ranks_q": ("bracket_ranks", _bad_ranks_q),
+    "partition_boundary": ("partition", _bad_partition_closed),
+    "partition_tail": ("partition", _bad_partition_tail_sign),
+    "widen_sequential": ("widen", _bad_widen),
+    "order_stat_0based": ("order_statistic", _bad_order_stat),
+    "sampler_stride": ("systematic_sample", _bad_sampler),
+}
+
+CHECKS = [
+    pins.check_n1_closed_form, pins.check_all_equal_closed_form,
+    pins.check_symmetric_half_budget, pins.check_invariants,
+    lambda: pins.check_bisect_matches_scan(6),
+    pins.check_decimal_bruteforce,
+    lambda: pins.check_vjp_fd(((1, 16, 4, -1.0),), tol=1e-8),
+    pins.check_vjp_invariants,
+    pins.check_bracket_ranks, pins.check_partition_definition,
+    pins.check_sampler_and_order_statistic, pins.check_widen_rule,
+    pins.check_bracket_equals_full, pins.check_forced_widening,
+]
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name, monkeypatch):
+    attr, bad = MUTANTS[name]
+    monkeypatch.setattr(O, attr, bad)
+    failed = []
+    for chk in CHECKS:
+        try:
+            with np.errstate(all="ignore"):
+                chk()
+        except (AssertionError, ValueError, ZeroDivisionError, IndexError, FloatingPointError):
+            failed.append(getattr(chk, "__name__", "lambda"))
+            break
+    assert failed, f"mutant {name} passed every pin"
+
+
+def test_unmutated_oracle_passes_the_same_checks():
+    for chk in CHECKS:
+        chk()
