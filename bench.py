@@ -1,0 +1,202 @@
+"""Benchmark: the extreme-scale workload, bracketed forward + backward.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+A step is one pass of the whole hot path over one row of n = 1e8 float32
+scores (s + e, s ~ N(0,1), e ~ Laplace(0, 0.05)), k = 20000, alpha = -0.01,
+K = 1e5 sample, z = 5.16: sample + order statistics, the streaming partition,
+the middle-band sort, the bracketed scan / certificate / root, the Laplace-CDF
+emit, then the Eq. (5) backward for an upstream gradient ~ N(0,1).  Inputs are
+resident in HBM before timing starts.  One JSON line is printed.
+
+Roofline: the dominant kernel's algorithmic bytes per launch divided by its
+average duration, timed live with HIP events (the library's event profiler,
+on the launch stream) over a second run of the same K steps.  The whole path
+is also reported against the 32 bytes/score required-traffic model (read r
+twice, write p, read p and g twice, write grad_r).
+
+CPU baseline: the float64 oracle (bracketed model + Eq. (5)) on the first
+2e7 scores of the same row (k and K scaled with n), timed on the host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=20_000_000)
+    return ap.parse_args()
+
+
+def kernel_bytes(name: str, n: int, active: int, m: int) -> float | None:
+    """Algorithmic HBM bytes one launch of a kernel must move."""
+    if name == "partition":
+        return 4.0 * n                       # read r
+    if name == "emit":
+        return 8.0 * n                       # read r, write p
+    if name == "vjp_reduce":
+        return 4.0 * n + 4.0 * active        # read p, g where f != 0
+    if name == "vjp_emit":
+        return 8.0 * n + 4.0 * active        # read p, write grad, g where f != 0
+    return None
+
+
+def cpu_baseline(r_full, noise_full, w, n_s: int):
+    import numpy as np
+
+    import oracle.lapsum_oracle as O
+    import workloads as W
+
+    n = w.n
+    scale = n_s / n
+    k_s = w.k * scale
+    K_s = max(2, int(round(w.sample_size * scale)))
+    r = np.ascontiguousarray(r_full[:n_s])
+    noise = np.ascontiguousarray(noise_full[:K_s])
+    g = W.upstream_grad("n1e8")[0, :n_s]
+    t0 = time.perf_counter()
+    p, b, info, _ = O.bracketed_forward(r, k_s, w.alpha, noise, z=w.z)
+    grad = O.vjp(r, b, w.alpha, g)
+    dt = time.perf_counter() - t0
+    del p, grad
+    return {
+        "value": n_s / dt, "unit": "scores/s", "cores": 1, "kind": "oracle",
+        "sample": f"first {n_s:.0e} scores of the row, k={k_s:g}, K={K_s} (k/n and K/n as in the "
+                  f"workload), float64 bracketed model + Eq. (5) VJP, {dt:.1f} s "
+                  f"(NumPy, single-threaded; host cores available: {len(os.sched_getaffinity(0))})",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2608_06912_amd as L
+    import workloads as W
+
+    L.load()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    w = W.get("n1e8")
+    print(f"[bench] generating n1e8 inputs", file=sys.stderr, flush=True)
+    r_np = W.scores("n1e8")
+    g_np = W.upstream_grad("n1e8")
+    noise_np = W.bracket_noise("n1e8")
+    r = torch.from_numpy(r_np).to(dev)
+    g = torch.from_numpy(g_np).to(dev)
+    noise = torch.from_numpy(noise_np).to(dev)
+    n, K = w.n, w.sample_size
+    mcap = L.default_m_capacity(n, K)
+    ws_f = torch.empty(L.lapsum_forward_bracketed_workspace_size(1, n, K, mcap), dtype=torch.uint8,
+                       device=dev)
+    ws_b = torch.empty(max(1, L.lapsum_backward_workspace_size(1, n)), dtype=torch.uint8, device=dev)
+    grad = torch.empty_like(r)
+
+    def step():
+        p, b, infos, _ = L.lapsum_forward_bracketed(r, w.k, w.alpha, noise, z=w.z, m_capacity=mcap,
+                                                    workspace=ws_f)
+        L.lapsum_backward(g, p, b, w.alpha, workspace=ws_b, out=grad)
+        return p, b, infos
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        p, b, infos = step()
+    torch.cuda.synchronize()
+
+    # timed region: K whole steps
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        p, b, infos = step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    # forward and backward separately (same K)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        p, b, infos = L.lapsum_forward_bracketed(r, w.k, w.alpha, noise, z=w.z, m_capacity=mcap,
+                                                 workspace=ws_f)[:3]
+    torch.cuda.synchronize()
+    ms_fwd = (time.perf_counter() - t0) * 1e3 / args.steps
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        L.lapsum_backward(g, p, b, w.alpha, workspace=ws_b, out=grad)
+    torch.cuda.synchronize()
+    ms_bwd = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    # per-kernel durations with HIP events over the same K steps
+    L.lapsum_profile_start()
+    for _ in range(args.steps):
+        p, b, infos = step()
+    prof = L.lapsum_profile_stop()
+    active = int(((p > 0) & (p < 1)).sum().item())
+    m = int(infos[0]["n_M"])
+    dom = max((kname for kname in prof if kernel_bytes(kname, n, active, m) is not None),
+              key=lambda kname: prof[kname][1])
+    launches, total_ms = prof[dom]
+    avg_s = total_ms / launches / 1e3
+    achieved = kernel_bytes(dom, n, active, m) / avg_s / 1e9
+    kernels = {kname: {"launches": c, "avg_us": 1e3 * ms / c} for kname, (c, ms) in sorted(prof.items())}
+
+    model_bytes = 32.0 * n
+    path_frac = model_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS
+
+    out = {
+        "metric": METRIC,
+        "value": n / (ms_step / 1e3),
+        "unit": "scores/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "n1e8 bracketed forward+backward: one row n=1e8, r=s+e with "
+                               "s~N(0,1), e~Laplace(0,0.05); k=20000, alpha=-0.01, K=1e5, z=5.16",
+                   "batch": 1, "n": n, "k": w.k, "alpha": w.alpha, "K": K, "z": w.z,
+                   "m_capacity": mcap},
+        "ms_fwd": ms_fwd,
+        "ms_bwd": ms_bwd,
+        "path_roofline": {"model_bytes_per_score": 32, "frac": path_frac,
+                          "note": "32 B/score required-traffic model at 8 TB/s"},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+        "kernels": kernels,
+        "bracket": {key: infos[0][key] for key in ("attempts", "fell_back", "n_M", "n_L", "n_R")},
+        "active_scores": active,
+    }
+    if not args.no_cpu_baseline:
+        print(f"[bench] cpu baseline on {args.cpu_sample:.0e} scores", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(r_np[0], noise_np, w, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

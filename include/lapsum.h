@@ -1,0 +1,213 @@
+/*
+ * lapsum.h - exact-budget LapSum soft top-k ("Fast LapSum") on AMD Instinct
+ * MI355X (gfx950).  C ABI of liblapsum.so.
+ *
+ * The operator (paper: "Fast LapSum: Exact Differentiable Top-k at Million
+ * Scale", Eq. (1) and Suppl. A): given scores r in R^n, a budget k in (0, n)
+ * and a temperature alpha < 0 (t = -alpha), find the threshold b with
+ *
+ *     LapSum(b) = sum_i sigma((b - r_i) / alpha) = k,
+ *
+ * sigma being the Laplace CDF (sigma(u) = e^u / 2 for u <= 0, 1 - e^{-u} / 2
+ * for u > 0, Eq. (3)), and return p_i = sigma((b - r_i) / alpha).  LapSum is
+ * strictly decreasing in b, so b is unique.  Larger scores get larger p, and
+ * sum_i p_i = k exactly up to rounding.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers are DEVICE pointers (memory of the current HIP device) unless a
+ *    comment says otherwise.  The caller owns all memory; the library never
+ *    allocates device memory and keeps no state across calls.
+ *  - Arrays are row-major [batch, n] and contiguous; k and alpha are shared
+ *    by all rows.  Indices are int32 and count within a row.
+ *  - Each call validates its scalar arguments on the host, then enqueues
+ *    kernels on `stream` and returns.  Results are valid once the stream has
+ *    synchronised.  lapsum_forward_bracketed additionally waits on `stream`
+ *    once per row to read the bracket certificate (see there).
+ *  - Errors are returned as lapsum_status codes; no call aborts or throws.
+ *    On an error nothing has been enqueued, except LAPSUM_ERR_HIP, which can
+ *    follow earlier launches of the same call.
+ *  - Scores must be finite; NaN or infinite scores give unspecified outputs
+ *    (they are not scanned for).
+ *  - workspace: caller-owned scratch of at least the size the matching
+ *    *_workspace_size function returns, aligned to 256 bytes.  Its content
+ *    on entry does not matter.  Two calls that overlap in time (different
+ *    streams) must use different workspaces.
+ *  - Only gfx950 devices are accepted (LAPSUM_ERR_DEVICE otherwise).
+ */
+#ifndef LAPSUM_H
+#define LAPSUM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum lapsum_status {
+    LAPSUM_OK = 0,
+    LAPSUM_ERR_INVALID_ARG = 1, /* null required pointer; batch < 1; n < 1 or
+                                   n > 2^31 - 1; k not in (0, n); alpha not a
+                                   finite negative number; bracketed: K < 2 or
+                                   K > n, z not finite and > 0, m_capacity < 1,
+                                   unknown flag bits */
+    LAPSUM_ERR_WORKSPACE = 2,   /* workspace NULL, too small, or not 256-byte
+                                   aligned */
+    LAPSUM_ERR_HIP = 3,         /* a HIP runtime call or kernel launch failed */
+    LAPSUM_ERR_DEVICE = 4       /* the current device is not gfx950 */
+} lapsum_status;
+
+/* Static description of a status code (host memory, never freed). */
+const char* lapsum_status_string(int status);
+
+/* ------------------------------------------------------------------------
+ * Full-sort forward (paper §1, §3, Suppl. A): sort each row descending, one
+ * prefix/suffix exponential scan gives the node curve LapSum(r_(i)), an index
+ * lookup finds the interval holding b and the two-exponential equation on it
+ * is solved in closed form; then the Laplace CDF is evaluated for every score
+ * in the original order.
+ *
+ *   scores   [batch, n] float32, input.
+ *   k        budget, 0 < k < n (real; the same for every row).
+ *   alpha    temperature, alpha < 0.
+ *   p        [batch, n] float32, output p_i = sigma((b - r_i) / alpha).
+ *   b        [batch] float64, output threshold per row.
+ *   perm_out NULL, or [batch, n] int32 output: perm_out[row][i] = original
+ *            index of the i-th largest score of the row.  Ties in value are
+ *            ordered by the order-preserving uint32 key of the float (so
+ *            +0.0 precedes -0.0) and then by ascending original index.
+ *            Asking for it makes the sort carry indices (slower).
+ * Rows with n <= 32768 are solved by one workgroup per row entirely on chip;
+ * longer rows use the device-wide sort and scan, one row after another.
+ * ------------------------------------------------------------------------ */
+size_t lapsum_forward_workspace_size(int64_t batch, int64_t n, int with_perm);
+
+int lapsum_forward(const float* scores, int64_t batch, int64_t n, double k,
+                   double alpha, float* p, double* b, int32_t* perm_out,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Backward: the analytical vector-Jacobian product of Eq. (5),
+ *
+ *   grad_r = f * (g - <g, q>),  q = f / sum_j f_j,
+ *   f_i = exp(-|b - r_i| / t) / (2 t) = min(p_i, 1 - p_i) / t,
+ *
+ * evaluated from the forward's p (the two forms of f are equal for the
+ * Laplace CDF).  One reduction of (sum f, sum f g) per row, then one
+ * element-wise pass.  When sum f is zero in floating point (every p is
+ * exactly 0 or 1) grad_r is zero.
+ *
+ *   grad_p  [batch, n] float32, upstream gradient dL/dp.
+ *   p       [batch, n] float32, the forward output for the same k, alpha.
+ *   b       [batch] float64 or NULL; not read by this p-form (accepted so
+ *           that callers can pass the forward's outputs unchanged).
+ *   alpha   the forward's temperature.
+ *   grad_r  [batch, n] float32, output dL/dr.
+ * ------------------------------------------------------------------------ */
+size_t lapsum_backward_workspace_size(int64_t batch, int64_t n);
+
+int lapsum_backward(const float* grad_p, const float* p, const double* b,
+                    int64_t batch, int64_t n, double alpha, float* grad_r,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Bracketed forward for very long rows (paper §4, Suppl. B, Suppl. C,
+ * Algorithm 1, validated path of Suppl. D):
+ *
+ *  1. systematic sample of K kernel-noised scores,
+ *     y_s = fl32(r[s * floor(n / K)] + noise[s]), s = 0..K-1;
+ *  2. ranks of Eq. (8) in IEEE float64: q = (n - k) / n,
+ *     j = floor(K q - z sqrt(K q (1 - q))), l = ceil(K q + z sqrt(K q (1 - q)));
+ *     a_L = y_(j), a_R = y_(l) (1-based order statistics; j < 1 gives
+ *     a_L = -inf, l > K gives a_R = +inf);
+ *  3. one pass over r: L = {r < a_L}, M = {a_L <= r < a_R}, R = {r >= a_R},
+ *     the tail sums of Eq. (7) S_L = sum_L e^{-(a_L - r)/t},
+ *     S_R = sum_R e^{-(r - a_R)/t}, the counts, and M gathered in index order;
+ *  4. M sorted descending; the scan of Suppl. A on sorted M with the tails as
+ *     carries gives LapSum(a_L) and LapSum(a_R); the bracket is certified when
+ *     LapSum(a_R) <= k <= LapSum(a_L);
+ *  5. certified: b by the closed-form root on sorted M (Suppl. B).  Not
+ *     certified: the failing side is widened by one-sided doubling
+ *     (LapSum(a_R) > k: a_L <- a_R, a_R <- a_R + 2 (a_R - a_L); LapSum(a_L) < k:
+ *     a_R <- a_L, a_L <- a_L - 2 (a_R - a_L); float64 arithmetic on the
+ *     float32 endpoints, rounded to float32) and steps 3-5 repeat.  After 3
+ *     brackets, or when |M| > m_capacity, the row is solved by the full-sort
+ *     path instead;
+ *  6. p_i = sigma((b - r_i) / alpha) in the original order.
+ *
+ * The result is the same b as lapsum_forward (the bracket only locates it).
+ * The host waits on `stream` once per bracket attempt to read the
+ * certificate, so this call returns after the row's threshold is known (the
+ * final emit is still asynchronous).
+ *
+ *   K           sample size, 2 <= K <= n.
+ *   z           bracket half-width in standard deviations (the paper uses
+ *               5.16), finite and > 0.
+ *   noise       [K] float32 Laplace(0, |alpha|) draws, shared by all rows
+ *               (the cached kernel noise); required.
+ *   m_capacity  largest |M| the workspace holds, >= 1.
+ *   flags       0, or LAPSUM_FLAG_FULL_SORT to skip the bracket and solve
+ *               by the full-sort path (same outputs; info->fell_back = 1).
+ *   p, b        as in lapsum_forward.
+ *   info        NULL, or [batch] lapsum_bracket_info in HOST memory, filled
+ *               with the last attempt's record.
+ *   m_idx_out   NULL, or [batch, m_capacity] int32: the original indices of
+ *               the final M in descending order (ties by ascending index),
+ *               -1 after the first n_M entries.  Rows that fell back to the
+ *               full sort get all -1.  Asking for it makes the M sort carry
+ *               indices.
+ * ------------------------------------------------------------------------ */
+#define LAPSUM_FLAG_FULL_SORT 1u
+
+typedef struct lapsum_bracket_info {
+    float a_L, a_R;        /* final bracket, +-INFINITY when unbounded */
+    int64_t j, l;          /* 1-based ranks of the first bracket (Eq. (8)) */
+    int64_t n_L, n_M, n_R; /* set sizes of the last attempt */
+    double T_L, T_R;       /* tail sums S_L, S_R of the last attempt */
+    double lap_aL, lap_aR; /* certificate values LapSum(a_L), LapSum(a_R) */
+    int32_t attempts;      /* brackets tried, 1..3 (0 with the flag) */
+    int32_t fell_back;     /* 1 if the row was solved by the full sort */
+    int32_t m_overflow;    /* 1 if |M| exceeded m_capacity */
+    int32_t reserved;
+} lapsum_bracket_info;
+
+size_t lapsum_forward_bracketed_workspace_size(int64_t batch, int64_t n,
+                                               int64_t K, int64_t m_capacity,
+                                               int with_m_idx);
+
+int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n,
+                             double k, double alpha, int64_t K, double z,
+                             const float* noise, int64_t m_capacity,
+                             uint32_t flags, float* p, double* b,
+                             lapsum_bracket_info* info, int32_t* m_idx_out,
+                             void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Diagnostics: per-kernel timing with HIP events.  Off by default.  While
+ * on, every kernel the library launches is bracketed by two events recorded
+ * on the launch stream (this adds a little host work per launch).  Not
+ * thread-safe: start, run, stop from one host thread.
+ *
+ *   lapsum_profile_start()   clears previous records and turns recording on
+ *   lapsum_profile_stop()    turns it off, waits for the recorded events and
+ *                            aggregates them by kernel name; returns the
+ *                            number of distinct kernels (or -LAPSUM_ERR_HIP)
+ *   lapsum_profile_entry(i, name, name_len, launches, total_ms)
+ *                            the i-th aggregate: name (NUL-terminated, host
+ *                            buffer of name_len bytes), launch count and
+ *                            summed duration in milliseconds
+ * ------------------------------------------------------------------------ */
+int lapsum_profile_start(void);
+int lapsum_profile_stop(void);
+int lapsum_profile_entry(int i, char* name, size_t name_len, int64_t* launches,
+                         double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LAPSUM_H */

@@ -524,10 +524,11 @@ def bracketed_forward(r32, k: float, alpha: float, noise32, z: float = 5.16,
     1. K = len(noise) kernel-noised samples by the systematic sampler;
     2. ranks j, l of Eq. (8); a_L = y_(j), a_R = y_(l);
     3. one pass: tails, counts, the middle set M;
-    4. certificate LapSum(a_R) <= k <= LapSum(a_L) (plain sums here);
-       on failure widen the failing side (one-sided doubling) and go to 3;
-       after `max_attempts` brackets, or when |M| exceeds m_capacity (no
-       room to hold M; widening only grows it), solve by the full sort;
+    4. when |M| exceeds m_capacity (no room to hold M; widening only grows
+       it) stop and solve by the full sort; otherwise the certificate
+       LapSum(a_R) <= k <= LapSum(a_L) (plain sums here); on failure widen
+       the failing side (one-sided doubling) and go to 3; after
+       `max_attempts` brackets solve by the full sort;
     5. exact solve on the sorted M with the tails (Suppl. B);
     6. p_i = sigma((b - r_i)/alpha).
     Returns (p, b, info, sorted M indices or None after a fallback).
@@ -548,13 +549,16 @@ def bracketed_forward(r32, k: float, alpha: float, noise32, z: float = 5.16,
     info = BracketInfo(a_L, a_R, j, l, 0, 0, 0, 0.0, 0.0, 0.0, 0.0, 0, 0, 0)
     for attempt in range(1, max_attempts + 1):
         part = partition(r32, a_L, a_R, t)
-        lap_R = 0.0 if math.isinf(a_R) and a_R > 0 else lapsum(r, a_R, t)
-        lap_L = float(n) if math.isinf(a_L) and a_L < 0 else lapsum(r, a_L, t)
         info = BracketInfo(part.a_L, part.a_R, j, l, part.n_L, part.n_M, part.n_R,
-                           part.T_L, part.T_R, lap_L, lap_R, attempt, 0, 0)
+                           part.T_L, part.T_R, math.nan, math.nan, attempt, 0, 0)
         if part.n_M > m_capacity:
+            # the certificate is read off the scan of the gathered M; an
+            # attempt whose M does not fit is not certified at all
             info.m_overflow = 1
             break
+        lap_R = 0.0 if math.isinf(a_R) and a_R > 0 else lapsum(r, a_R, t)
+        lap_L = float(n) if math.isinf(a_L) and a_L < 0 else lapsum(r, a_L, t)
+        info.lap_aL, info.lap_aR = lap_L, lap_R
         if lap_R <= k <= lap_L:
             b, m_sorted = solve_in_bracket(r32, part, k, t)
             return probs(r, b, alpha), b, info, m_sorted

@@ -1,0 +1,246 @@
+"""Exact-budget LapSum soft top-k ("Fast LapSum") on AMD Instinct MI355X.
+
+Thin Python binding over the C ABI of liblapsum.so (include/lapsum.h).  The
+functions carry the C names and only marshal arguments: torch supplies
+device memory and the current HIP stream, every step of the computation runs
+in the library's HIP kernels.  There is no CPU fallback: if the library is
+not built, or the tensors are not on a gfx950 device, the calls raise.
+
+    p, b = lapsum_forward(scores, k, alpha)                 # full sort
+    grad_r = lapsum_backward(grad_p, p, b, alpha)           # Eq. (5) VJP
+    p, b, info, m_idx = lapsum_forward_bracketed(scores, k, alpha, noise)
+
+`scores` is a float32 CUDA tensor of shape [n] or [batch, n]; k and alpha
+are Python floats with 0 < k < n and alpha < 0.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "load", "LapsumError", "BracketInfo", "lapsum_status_string",
+    "lapsum_forward_workspace_size", "lapsum_forward",
+    "lapsum_backward_workspace_size", "lapsum_backward",
+    "lapsum_forward_bracketed_workspace_size", "lapsum_forward_bracketed",
+    "LAPSUM_FLAG_FULL_SORT", "LIB_PATH", "lapsum_profile_start", "lapsum_profile_stop",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapsum.so")
+LAPSUM_FLAG_FULL_SORT = 1
+
+_lib = None
+
+
+class LapsumError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {lapsum_status_string(status)} (status {status})")
+
+
+class BracketInfo(ctypes.Structure):
+    """Mirror of lapsum_bracket_info."""
+    _fields_ = [
+        ("a_L", ctypes.c_float), ("a_R", ctypes.c_float),
+        ("j", ctypes.c_int64), ("l", ctypes.c_int64),
+        ("n_L", ctypes.c_int64), ("n_M", ctypes.c_int64), ("n_R", ctypes.c_int64),
+        ("T_L", ctypes.c_double), ("T_R", ctypes.c_double),
+        ("lap_aL", ctypes.c_double), ("lap_aR", ctypes.c_double),
+        ("attempts", ctypes.c_int32), ("fell_back", ctypes.c_int32),
+        ("m_overflow", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    ]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+
+
+def load():
+    """Load liblapsum.so (built in-tree) and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_06912_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, f64, sz, u32, i32 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_double,
+                                  ctypes.c_size_t, ctypes.c_uint32, ctypes.c_int)
+    lib.lapsum_status_string.argtypes = [i32]
+    lib.lapsum_status_string.restype = ctypes.c_char_p
+    lib.lapsum_forward_workspace_size.argtypes = [i64, i64, i32]
+    lib.lapsum_forward_workspace_size.restype = sz
+    lib.lapsum_forward.argtypes = [vp, i64, i64, f64, f64, vp, vp, vp, vp, sz, vp]
+    lib.lapsum_forward.restype = i32
+    lib.lapsum_backward_workspace_size.argtypes = [i64, i64]
+    lib.lapsum_backward_workspace_size.restype = sz
+    lib.lapsum_backward.argtypes = [vp, vp, vp, i64, i64, f64, vp, vp, sz, vp]
+    lib.lapsum_backward.restype = i32
+    lib.lapsum_forward_bracketed_workspace_size.argtypes = [i64, i64, i64, i64, i32]
+    lib.lapsum_forward_bracketed_workspace_size.restype = sz
+    lib.lapsum_forward_bracketed.argtypes = [vp, i64, i64, f64, f64, i64, f64, vp, i64, u32,
+                                             vp, vp, vp, vp, vp, sz, vp]
+    lib.lapsum_forward_bracketed.restype = i32
+    lib.lapsum_profile_start.argtypes = []
+    lib.lapsum_profile_start.restype = i32
+    lib.lapsum_profile_stop.argtypes = []
+    lib.lapsum_profile_stop.restype = i32
+    lib.lapsum_profile_entry.argtypes = [i32, ctypes.c_char_p, sz, ctypes.POINTER(ctypes.c_int64),
+                                         ctypes.POINTER(ctypes.c_double)]
+    lib.lapsum_profile_entry.restype = i32
+    _lib = lib
+    return lib
+
+
+def lapsum_status_string(status: int) -> str:
+    return load().lapsum_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise LapsumError(status, where)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _rows(x, name):
+    torch = _torch()
+    if not isinstance(x, torch.Tensor) or x.device.type != "cuda":
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if x.dtype != torch.float32:
+        raise ValueError(f"{name} must be float32")
+    if x.dim() not in (1, 2):
+        raise ValueError(f"{name} must have shape [n] or [batch, n]")
+    if not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    batch, n = (1, x.shape[0]) if x.dim() == 1 else (x.shape[0], x.shape[1])
+    return int(batch), int(n)
+
+
+def _stream(device):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _workspace(nbytes, device, workspace):
+    torch = _torch()
+    if nbytes == 0:
+        return None, 0
+    if workspace is not None and workspace.numel() * workspace.element_size() >= nbytes:
+        ws = workspace
+    else:
+        ws = torch.empty(int(nbytes), dtype=torch.uint8, device=device)
+    if ws.data_ptr() % 256:
+        raise ValueError("workspace must be 256-byte aligned")
+    return ws, ws.numel() * ws.element_size()
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def lapsum_forward_workspace_size(batch: int, n: int, with_perm: bool = False) -> int:
+    return int(load().lapsum_forward_workspace_size(batch, n, int(bool(with_perm))))
+
+
+def lapsum_forward(scores, k: float, alpha: float, *, perm: bool = False, workspace=None):
+    """Full-sort forward.  Returns (p, b) or (p, b, perm) with perm=True;
+    p has the shape of scores, b is float64 of shape [batch]."""
+    torch = _torch()
+    lib = load()
+    batch, n = _rows(scores, "scores")
+    dev = scores.device
+    p = torch.empty_like(scores)
+    b = torch.empty(batch, dtype=torch.float64, device=dev)
+    pm = torch.empty(scores.shape, dtype=torch.int32, device=dev) if perm else None
+    ws, nbytes = _workspace(lib.lapsum_forward_workspace_size(batch, n, int(perm)), dev, workspace)
+    with torch.cuda.device(dev):
+        _check(lib.lapsum_forward(_ptr(scores), batch, n, float(k), float(alpha), _ptr(p), _ptr(b),
+                                  _ptr(pm), _ptr(ws), nbytes, _stream(dev)), "lapsum_forward")
+    return (p, b, pm) if perm else (p, b)
+
+
+def lapsum_backward_workspace_size(batch: int, n: int) -> int:
+    return int(load().lapsum_backward_workspace_size(batch, n))
+
+
+def lapsum_backward(grad_p, p, b, alpha: float, *, workspace=None, out=None):
+    """VJP of Eq. (5): grad_r = f * (g - <g, q>) with f from p."""
+    torch = _torch()
+    lib = load()
+    batch, n = _rows(p, "p")
+    if grad_p.shape != p.shape:
+        raise ValueError("grad_p and p must have the same shape")
+    _rows(grad_p, "grad_p")
+    dev = p.device
+    grad = out if out is not None else torch.empty_like(p)
+    ws, nbytes = _workspace(lib.lapsum_backward_workspace_size(batch, n), dev, workspace)
+    with torch.cuda.device(dev):
+        _check(lib.lapsum_backward(_ptr(grad_p), _ptr(p), _ptr(b), batch, n, float(alpha),
+                                   _ptr(grad), _ptr(ws), nbytes, _stream(dev)), "lapsum_backward")
+    return grad
+
+
+def lapsum_forward_bracketed_workspace_size(batch: int, n: int, K: int, m_capacity: int,
+                                            with_m_idx: bool = False) -> int:
+    return int(load().lapsum_forward_bracketed_workspace_size(batch, n, K, m_capacity,
+                                                              int(bool(with_m_idx))))
+
+
+def default_m_capacity(n: int, K: int) -> int:
+    """A middle-set capacity comfortably above the expected band of a z = 5.16
+    bracket (rank width ~ 2 z n / sqrt(K)) and its widenings."""
+    return int(min(n, max(1 << 16, 64 * (n // max(1, int(K ** 0.5))))))
+
+
+def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float = 5.16,
+                             m_capacity: int | None = None, flags: int = 0,
+                             m_idx: bool = False, workspace=None):
+    """Bracketed forward.  noise: float32 CUDA tensor [K] of Laplace(0, |alpha|)
+    draws.  Returns (p, b, infos, m_idx or None) with infos a list of dicts."""
+    torch = _torch()
+    lib = load()
+    batch, n = _rows(scores, "scores")
+    if noise.dim() != 1:
+        raise ValueError("noise must be 1-D [K]")
+    _rows(noise, "noise")
+    K = int(noise.shape[0])
+    if m_capacity is None:
+        m_capacity = default_m_capacity(n, K)
+    dev = scores.device
+    p = torch.empty_like(scores)
+    b = torch.empty(batch, dtype=torch.float64, device=dev)
+    mi = torch.empty((batch, m_capacity), dtype=torch.int32, device=dev) if m_idx else None
+    infos = (BracketInfo * batch)()
+    ws, nbytes = _workspace(lib.lapsum_forward_bracketed_workspace_size(batch, n, K, m_capacity,
+                                                                        int(m_idx)), dev, workspace)
+    with torch.cuda.device(dev):
+        _check(lib.lapsum_forward_bracketed(_ptr(scores), batch, n, float(k), float(alpha), K,
+                                            float(z), _ptr(noise), int(m_capacity), int(flags),
+                                            _ptr(p), _ptr(b), ctypes.cast(infos, ctypes.c_void_p),
+                                            _ptr(mi), _ptr(ws), nbytes, _stream(dev)),
+               "lapsum_forward_bracketed")
+    return p, b, [infos[i].as_dict() for i in range(batch)], mi
+
+
+def lapsum_profile_start() -> None:
+    """Record HIP events around every kernel the library launches."""
+    _check(load().lapsum_profile_start(), "lapsum_profile_start")
+
+
+def lapsum_profile_stop() -> dict:
+    """Stop recording; returns {kernel: (launches, total_ms)}."""
+    lib = load()
+    cnt = lib.lapsum_profile_stop()
+    if cnt < 0:
+        raise LapsumError(-cnt, "lapsum_profile_stop")
+    out = {}
+    buf = ctypes.create_string_buffer(128)
+    for i in range(cnt):
+        launches = ctypes.c_int64(0)
+        ms = ctypes.c_double(0.0)
+        _check(lib.lapsum_profile_entry(i, buf, 128, ctypes.byref(launches), ctypes.byref(ms)),
+               "lapsum_profile_entry")
+        out[buf.value.decode()] = (int(launches.value), float(ms.value))
+    return out

@@ -1,0 +1,131 @@
+// Stable LSD radix sort of uint32 keys (optionally with int32 values) held by
+// one workgroup in registers, 8-bit digits, scattered through LDS.
+//
+// Arrangement ("wave-striped"): item i of lane `lane` in wave `w` sits at
+// position w*(64*ITEMS) + i*64 + lane.  That position order is the order the
+// sort keeps among equal keys, so loading element `pos` of a row into that
+// slot makes the sort stable by original index.
+//
+// Digit ranking per pass: the lanes of a wave holding the same digit are
+// found with eight ballots (one per digit bit), giving each lane the number
+// of earlier same-digit lanes; a per-wave LDS counter per digit carries the
+// count across the ITEMS rounds.  An exclusive scan over the counters laid
+// out digit-major, wave-minor then gives every (wave, digit) its first output
+// position, which keeps the order position-stable.
+#pragma once
+
+#include "common.hpp"
+
+namespace lapsum {
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
+// Lanes of this wave whose 8-bit digit equals mine (all 64 lanes active).
+__device__ __forceinline__ uint64_t match_digit8(uint32_t d) {
+  uint64_t peers = ~0ull;
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const bool bit = (d >> b) & 1u;
+    const uint64_t bal = __ballot(bit);
+    peers &= bit ? bal : ~bal;
+  }
+  return peers;
+}
+
+// In-place exclusive scan of `count` u32 values in LDS, count = 4 * BLOCK.
+template <int BLOCK>
+__device__ void block_excl_scan_u32x4(uint32_t* a, uint32_t* wave_tot) {
+  constexpr int WAVES = BLOCK / kWave;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  uint32_t v0 = a[4 * tid + 0], v1 = a[4 * tid + 1], v2 = a[4 * tid + 2], v3 = a[4 * tid + 3];
+  uint32_t sum = v0 + v1 + v2 + v3;
+  uint32_t incl = sum;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    uint32_t o = __shfl_up(incl, d, kWave);
+    if (lane >= d) incl += o;
+  }
+  if (lane == kWave - 1) wave_tot[wid] = incl;
+  __syncthreads();
+  uint32_t wbase = 0;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w)
+    if (w < wid) wbase += wave_tot[w];
+  uint32_t ex = wbase + incl - sum;
+  a[4 * tid + 0] = ex;
+  a[4 * tid + 1] = ex + v0;
+  a[4 * tid + 2] = ex + v0 + v1;
+  a[4 * tid + 3] = ex + v0 + v1 + v2;
+  __syncthreads();
+}
+
+template <int BLOCK>
+struct SortSmem {
+  uint32_t cnt[256 * (BLOCK / kWave)];
+  uint32_t wave_tot[BLOCK / kWave];
+};
+
+// One LSD pass on bits [shift, shift+8).  On return the keys (and values)
+// are back in registers: wave-striped, or blocked (thread tid holds positions
+// tid*ITEMS .. tid*ITEMS+ITEMS-1) when `blocked_out`.  `buf` holds
+// BLOCK*ITEMS u32.
+template <int BLOCK, int ITEMS, bool PAIRS>
+__device__ void block_sort_pass(uint32_t (&key)[ITEMS], int32_t (&val)[ITEMS], int shift,
+                                uint32_t* buf, SortSmem<BLOCK>& sm, bool blocked_out) {
+  constexpr int WAVES = BLOCK / kWave;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  for (int e = tid; e < 256 * WAVES; e += BLOCK) sm.cnt[e] = 0u;
+  __syncthreads();
+
+  uint32_t pos[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const uint32_t d = (key[i] >> shift) & 255u;
+    const uint64_t peers = match_digit8(d);
+    const uint32_t below = lanes_below(peers);
+    uint32_t* slot = &sm.cnt[d * WAVES + wid];
+    const uint32_t c = *slot;
+    pos[i] = c + below;
+    if (below == 0u) *slot = c + static_cast<uint32_t>(__popcll(peers));
+  }
+  __syncthreads();
+  block_excl_scan_u32x4<BLOCK>(sm.cnt, sm.wave_tot);
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) pos[i] += sm.cnt[((key[i] >> shift) & 255u) * WAVES + wid];
+
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) buf[pos[i]] = key[i];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i)
+    key[i] = buf[blocked_out ? tid * ITEMS + i : wid * (kWave * ITEMS) + i * kWave + lane];
+  __syncthreads();
+  if constexpr (PAIRS) {
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) buf[pos[i]] = static_cast<uint32_t>(val[i]);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i)
+      val[i] = static_cast<int32_t>(buf[blocked_out ? tid * ITEMS + i : wid * (kWave * ITEMS) + i * kWave + lane]);
+    __syncthreads();
+  }
+}
+
+// Full 32-bit sort; the result is left in blocked arrangement.
+template <int BLOCK, int ITEMS, bool PAIRS>
+__device__ void block_sort_u32(uint32_t (&key)[ITEMS], int32_t (&val)[ITEMS], uint32_t* buf,
+                               SortSmem<BLOCK>& sm) {
+  block_sort_pass<BLOCK, ITEMS, PAIRS>(key, val, 0, buf, sm, false);
+  block_sort_pass<BLOCK, ITEMS, PAIRS>(key, val, 8, buf, sm, false);
+  block_sort_pass<BLOCK, ITEMS, PAIRS>(key, val, 16, buf, sm, false);
+  block_sort_pass<BLOCK, ITEMS, PAIRS>(key, val, 24, buf, sm, true);
+}
+
+}  // namespace lapsum

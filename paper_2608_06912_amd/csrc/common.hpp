@@ -1,0 +1,360 @@
+// Device helpers shared by the LapSum kernels (gfx950, wave64).
+//
+// Notation follows the paper: scores r, temperature t = -alpha > 0, threshold
+// b with LapSum(b) = sum_i sigma((r_i - b)/t) = k (Eq. (1), Suppl. A).  After
+// a descending sort s_1 >= ... >= s_n the node curve
+//     N_i = LapSum(s_i) = i - P_i / 2 + E_i / 2,
+//     P_i = sum_{j <= i} e^{-(s_j - s_i)/t},   E_i = sum_{j > i} e^{-(s_i - s_j)/t}
+// is non-decreasing in i (the three-group split of Suppl. A), and inside the
+// interval [s_{m+1}, s_m] holding b the budget equation has two exponentials
+// and a closed-form root.
+//
+// Both sums are scanned in "shift-carrying" form: a group of sorted scores is
+// summarised by (anchor, sum) where every term is an exponential of a
+// non-positive exponent relative to the anchor, so nothing overflows and no
+// sum is ever formed by subtracting two large numbers.
+//   Pre (anchor u = the group's smallest score):  S = sum e^{-(r - u)/t}
+//   Suf (anchor v = the group's largest score):   T = sum e^{-(v - r)/t}
+// Combining an earlier (larger) group A with a later group B:
+//   Pre(A then B) = (u_B, S_B + e^{-(u_A - u_B)/t} S_A)
+//   Suf(A then B) = (v_A, T_A + e^{-(v_A - v_B)/t} T_B)
+// This is the associative form of the affine recurrence x_i = w_i x_{i-1} + 1
+// of Suppl. A (the 2x2 matrix [[w,1],[0,1]]), with each weight formed from
+// the anchors directly rather than as a product of per-step weights.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lapsum {
+
+constexpr int kWave = 64;
+constexpr double kLog2e = 1.4426950408889634074;
+
+// ---------------------------------------------------------------- keys ----
+// uint32 key whose ascending order is the descending order of the float.
+// Ascending map: non-negative floats get the sign bit set, negative floats
+// are inverted; the descending key is the complement of that.
+__device__ __forceinline__ uint32_t desc_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ~asc;
+}
+
+__device__ __forceinline__ float key_float(uint32_t dk) {
+  uint32_t asc = ~dk;
+  uint32_t u = (asc & 0x80000000u) ? (asc & 0x7fffffffu) : ~asc;
+  return __uint_as_float(u);
+}
+
+// ----------------------------------------------------------- exponentials --
+// 2^x on the hardware transcendental unit (results below the normal range
+// flush to zero, which only drops terms under 1e-38).
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// e^{-d/t} for d >= 0 with the exponent formed in float64 (d may be the
+// difference of two float32 scores of very different size) and the
+// exponential in float32; c2 = log2(e)/t.  For per-score terms summed in
+// float64: each term carries one float32 rounding, never a product of them.
+__device__ __forceinline__ double wexp_f32(double d, double c2) {
+  return static_cast<double>(exp2_fast(static_cast<float>(-d * c2)));
+}
+
+// e^{-d/t} in float64, for scan combines and the root.
+__device__ __forceinline__ double wexp_f64(double d, double inv_t) { return exp(-d * inv_t); }
+
+// ----------------------------------------------------------- pair algebra --
+struct Pre {   // sum_j e^{-(r_j - u)/t}; S == 0 means "no scores"
+  float u;
+  double S;
+};
+struct Suf {   // sum_j e^{-(v - r_j)/t}; T == 0 means "no scores"
+  float v;
+  double T;
+};
+
+__device__ __forceinline__ Pre pre_empty() { return Pre{0.0f, 0.0}; }
+__device__ __forceinline__ Suf suf_empty() { return Suf{0.0f, 0.0}; }
+
+// a is the earlier group (larger scores), b the later one.
+__device__ __forceinline__ Pre pre_combine(Pre a, Pre b, double inv_t) {
+  if (a.S == 0.0) return b;
+  if (b.S == 0.0) return a;
+  double w = wexp_f64(static_cast<double>(a.u) - static_cast<double>(b.u), inv_t);
+  return Pre{b.u, b.S + w * a.S};
+}
+
+__device__ __forceinline__ Suf suf_combine(Suf a, Suf b, double inv_t) {
+  if (a.T == 0.0) return b;
+  if (b.T == 0.0) return a;
+  double w = wexp_f64(static_cast<double>(a.v) - static_cast<double>(b.v), inv_t);
+  return Suf{a.v, a.T + w * b.T};
+}
+
+// ------------------------------------------------------------ wave scans ---
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// inclusive, left to right: lane l gets x_0 (+) ... (+) x_l
+__device__ __forceinline__ Pre wave_incl_pre(Pre x, double inv_t) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    float ou = __shfl_up(x.u, d, kWave);
+    double oS = __shfl_up(x.S, d, kWave);
+    if (lane >= d) x = pre_combine(Pre{ou, oS}, x, inv_t);
+  }
+  return x;
+}
+
+// inclusive, right to left: lane l gets x_l (+) ... (+) x_63
+__device__ __forceinline__ Suf wave_incl_suf(Suf x, double inv_t) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    float ov = __shfl_down(x.v, d, kWave);
+    double oT = __shfl_down(x.T, d, kWave);
+    if (lane + d < kWave) x = suf_combine(x, Suf{ov, oT}, inv_t);
+  }
+  return x;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int d = kWave / 2; d >= 1; d >>= 1) v += __shfl_xor(v, d, kWave);
+  return v;
+}
+
+// Scratch for the block-level scans and the crossing search.
+template <int WAVES>
+struct ScanSmem {
+  Pre pre[WAVES + 1];
+  Suf suf[WAVES + 1];
+  int cnt[WAVES];
+  double b;
+  double P[64];   // crossing refinement (at most 64 items per thread)
+  double Q[64];
+  float sv[64];
+};
+
+// Exclusive block scan of Pre, seeded with carry (groups before the block).
+// Returns this thread's exclusive prefix; *total gets carry (+) all.
+template <int WAVES>
+__device__ Pre block_excl_pre(Pre x, Pre carry, double inv_t, ScanSmem<WAVES>& sm, Pre* total) {
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  Pre incl = wave_incl_pre(x, inv_t);
+  float eu = __shfl_up(incl.u, 1, kWave);
+  double eS = __shfl_up(incl.S, 1, kWave);
+  Pre lane_excl = (lane == 0) ? pre_empty() : Pre{eu, eS};
+  if (lane == kWave - 1) sm.pre[wid] = incl;
+  __syncthreads();
+  if (wid == 0) {
+    Pre wv = (lane < WAVES) ? sm.pre[lane] : pre_empty();
+    Pre wi = wave_incl_pre(wv, inv_t);
+    float pu = __shfl_up(wi.u, 1, kWave);
+    double pS = __shfl_up(wi.S, 1, kWave);
+    Pre we = (lane == 0) ? pre_empty() : Pre{pu, pS};
+    if (lane < WAVES) sm.pre[lane] = pre_combine(carry, we, inv_t);
+    if (lane == WAVES - 1) sm.pre[WAVES] = pre_combine(carry, wi, inv_t);
+  }
+  __syncthreads();
+  Pre r = pre_combine(sm.pre[wid], lane_excl, inv_t);
+  *total = sm.pre[WAVES];
+  __syncthreads();
+  return r;
+}
+
+// Exclusive block scan of Suf from the right, seeded with carry (groups
+// after the block).  *total gets all (+) carry.
+template <int WAVES>
+__device__ Suf block_excl_suf(Suf x, Suf carry, double inv_t, ScanSmem<WAVES>& sm, Suf* total) {
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  Suf incl = wave_incl_suf(x, inv_t);
+  float ev = __shfl_down(incl.v, 1, kWave);
+  double eT = __shfl_down(incl.T, 1, kWave);
+  Suf lane_excl = (lane == kWave - 1) ? suf_empty() : Suf{ev, eT};
+  if (lane == 0) sm.suf[wid] = incl;
+  __syncthreads();
+  if (wid == 0) {
+    Suf wv = (lane < WAVES) ? sm.suf[lane] : suf_empty();
+    Suf wi = wave_incl_suf(wv, inv_t);
+    float nv = __shfl_down(wi.v, 1, kWave);
+    double nT = __shfl_down(wi.T, 1, kWave);
+    Suf we = (lane == kWave - 1) ? suf_empty() : Suf{nv, nT};
+    if (lane < WAVES) sm.suf[lane] = suf_combine(we, carry, inv_t);
+    if (lane == 0) sm.suf[WAVES] = suf_combine(wi, carry, inv_t);
+  }
+  __syncthreads();
+  Suf r = suf_combine(lane_excl, sm.suf[wid], inv_t);
+  *total = sm.suf[WAVES];
+  __syncthreads();
+  return r;
+}
+
+// Number of threads in the block with flag set.
+template <int WAVES>
+__device__ int block_count(bool flag, ScanSmem<WAVES>& sm) {
+  const int wid = threadIdx.x / kWave;
+  uint64_t m = __ballot(flag);
+  if (lane_id() == 0) sm.cnt[wid] = __popcll(m);
+  __syncthreads();
+  int c = 0;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) c += sm.cnt[w];
+  __syncthreads();
+  return c;
+}
+
+// ------------------------------------------------------------- the root ----
+// For v <= b <= u let the c_up scores above the interval be summarised at u
+// (A = sum e^{-(r-u)/t}) and the scores below at v (B = sum e^{-(v-r)/t}).
+// Then LapSum(b) = c_up - (A/2) e^{-(u-b)/t} + (B/2) e^{-(b-v)/t}, and with
+// y = e^{(u-b)/t}, E = B e^{-(u-v)/t}, c = k - c_up the budget equation is the
+// quadratic E y^2 - 2 c y - A = 0 whose positive root is
+//     y = (c + D) / E = A / (D - c),   D = sqrt(c^2 + A E).
+// The form without cancellation is used for each sign of c, in logarithms
+// because E underflows when the interval is many temperatures wide.  A group
+// whose sum is zero (no scores, or all saturated) drops out: then
+// b = v + t ln(B / (2(k - c_up))) or b = u - t ln(A / (2(c_up - k))).
+__device__ inline double gap_root(double k, double t, double c_up, bool has_up, double u,
+                                  double lnA, bool has_dn, double v, double lnB) {
+  if (!has_up) return v + t * (lnB - log(2.0 * (k - c_up)));
+  if (!has_dn) return u - t * (lnA - log(2.0 * (c_up - k)));
+  const double g = (u - v) / t;
+  const double lnE = lnB - g;
+  const double c = k - c_up;
+  double lny;
+  if (c == 0.0) {
+    lny = 0.5 * (lnA - lnE);
+  } else {
+    const double D = sqrt(c * c + exp(lnA + lnE));   // A E <= n^2, never overflows
+    lny = (c > 0.0) ? log(c + D) - lnE : lnA - log(D - c);
+  }
+  lny = fmin(fmax(lny, 0.0), g);
+  return u - t * lny;
+}
+
+// ------------------------------------------------------ block-level solve ---
+// A block holds a run of sorted scores, thread tid owning the consecutive
+// positions tid*ITEMS .. tid*ITEMS+cnt-1 (blocked arrangement, descending).
+// ext_pre summarises every score ranked before the block (rank0 of them,
+// rank0 counted from 0), ext_suf every score ranked after it.  The block is
+// known to hold the crossing, or b lies between the block's first score and
+// whatever precedes it.  Returns b (the same value in every thread) and the
+// block totals ext_pre (+) block, block (+) ext_suf.
+template <int BLOCK, int ITEMS>
+__device__ double block_solve(const float (&s)[ITEMS], int cnt, double rank0, Pre ext_pre,
+                              Suf ext_suf, double k, double t, ScanSmem<BLOCK / kWave>& sm,
+                              Pre* pre_total, Suf* suf_total) {
+  static_assert(ITEMS <= 64, "crossing refinement scratch");
+  constexpr int WAVES = BLOCK / kWave;
+  const int tid = threadIdx.x;
+  const double inv_t = 1.0 / t;
+  const double c2 = kLog2e / t;
+
+  // 1. this thread's group summaries (direct terms relative to the anchors)
+  Pre mine_pre = pre_empty();
+  Suf mine_suf = suf_empty();
+  double suf_x = 0.0;   // sum over positions after the first
+  float lastf = s[0];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i)
+    if (i == cnt - 1) lastf = s[i];
+  if (cnt > 0) {
+    const double last = lastf;
+    const double first = s[0];
+    double sp = 0.0;
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      if (i < cnt) {
+        sp += wexp_f32(static_cast<double>(s[i]) - last, c2);
+        if (i > 0) suf_x += wexp_f32(first - static_cast<double>(s[i]), c2);
+      }
+    }
+    mine_pre = Pre{lastf, sp};
+    mine_suf = Suf{s[0], 1.0 + suf_x};
+  }
+
+  // 2. carries into this thread from both sides
+  Pre pre_in = block_excl_pre<WAVES>(mine_pre, ext_pre, inv_t, sm, pre_total);
+  Suf suf_in = block_excl_suf<WAVES>(mine_suf, ext_suf, inv_t, sm, suf_total);
+
+  // 3. node value at this thread's first position
+  bool below_k = false;
+  if (cnt > 0) {
+    const double first = s[0];
+    double P0 = 1.0;
+    if (pre_in.S != 0.0) P0 += wexp_f64(static_cast<double>(pre_in.u) - first, inv_t) * pre_in.S;
+    double E0 = suf_x;
+    if (suf_in.T != 0.0) E0 += wexp_f64(first - static_cast<double>(suf_in.v), inv_t) * suf_in.T;
+    const double N0 = rank0 + static_cast<double>(tid) * ITEMS + 1.0 - 0.5 * P0 + 0.5 * E0;
+    below_k = (N0 <= k);
+  }
+  const int nthr = block_count<WAVES>(below_k, sm);
+
+  // 4. the thread holding the crossing refines it position by position
+  if (nthr == 0) {
+    if (tid == 0) {
+      // b lies above every score of the block
+      Suf all = *suf_total;
+      sm.b = gap_root(k, t, rank0, ext_pre.S != 0.0, ext_pre.u, log(ext_pre.S > 0 ? ext_pre.S : 1.0),
+                      true, all.v, log(all.T));
+    }
+  } else if (tid == nthr - 1) {
+    double* P = sm.P;
+    double* Q = sm.Q;
+    float* sv = sm.sv;   // LDS copy: the serial loops below index it at run time
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i)
+      if (i < cnt) sv[i] = s[i];
+    const double first = s[0];
+    double Pi = 1.0;
+    if (pre_in.S != 0.0) Pi += wexp_f64(static_cast<double>(pre_in.u) - first, inv_t) * pre_in.S;
+    P[0] = Pi;
+    for (int i = 1; i < cnt; ++i) {
+      Pi = 1.0 + wexp_f64(static_cast<double>(sv[i - 1]) - static_cast<double>(sv[i]), inv_t) * Pi;
+      P[i] = Pi;
+    }
+    // Q_i = 1 + E_i (inclusive suffix at s_i); E_i kept separately
+    double Enext = (suf_in.T != 0.0)
+                       ? wexp_f64(static_cast<double>(sv[cnt - 1]) - static_cast<double>(suf_in.v), inv_t) * suf_in.T
+                       : 0.0;
+    int m = 0;
+    const double base = rank0 + static_cast<double>(tid) * ITEMS;
+    for (int i = cnt - 1; i >= 0; --i) {
+      const double Ei = Enext;
+      Q[i] = 1.0 + Ei;
+      const double Ni = base + static_cast<double>(i) + 1.0 - 0.5 * P[i] + 0.5 * Ei;
+      if (Ni <= k) m = (m == 0) ? i + 1 : m;   // node values are non-decreasing
+      if (i > 0) Enext = wexp_f64(static_cast<double>(sv[i - 1]) - static_cast<double>(sv[i]), inv_t) * Q[i];
+    }
+    if (m == 0) m = 1;   // the first position was found at or below k above
+    const double c_up = base + m;
+    double bb;
+    if (m < cnt) {
+      bb = gap_root(k, t, c_up, true, sv[m - 1], log(P[m - 1]), true, sv[m], log(Q[m]));
+    } else {
+      const bool has_dn = suf_in.T != 0.0;
+      bb = gap_root(k, t, c_up, true, sv[cnt - 1], log(P[cnt - 1]), has_dn, suf_in.v,
+                    has_dn ? log(suf_in.T) : 0.0);
+    }
+    sm.b = bb;
+  }
+  __syncthreads();
+  const double b = sm.b;
+  __syncthreads();
+  return b;
+}
+
+// ---------------------------------------------------------------- emit -----
+// p = sigma((r - b)/t) with the difference taken in float64 (b is float64)
+// and the exponential in float32.
+__device__ __forceinline__ float laplace_p(float r, double b, double inv_t) {
+  const float u = static_cast<float>((static_cast<double>(r) - b) * inv_t);
+  const float e = exp2_fast(-fabsf(u) * static_cast<float>(kLog2e));
+  return (u <= 0.0f) ? 0.5f * e : 1.0f - 0.5f * e;
+}
+
+}  // namespace lapsum

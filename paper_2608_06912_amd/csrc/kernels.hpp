@@ -1,0 +1,146 @@
+// Internal interface between the host orchestration (lapsum_api.cpp) and the
+// HIP kernels.  Every launcher enqueues on `stream` and returns the launch
+// status; none synchronises.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace lapsum {
+
+// Largest row solved entirely on chip by one workgroup (keys in LDS).
+constexpr int64_t kRowOnChipMax = 32768;
+// Tile of the device-wide sort and of the device-wide solve.
+constexpr int kTileThreads = 256;
+constexpr int kTileItems = 16;
+constexpr int64_t kTile = kTileThreads * kTileItems;   // 4096
+// Bracketed pass: blocks of the streaming partition and their staging.
+constexpr int kPartThreads = 256;
+constexpr int kPartStageCap = 2048;    // M entries a partition block keeps
+constexpr int kSelectBins = 2048;      // 11-bit digits of the order-statistic select
+
+// Threshold record written by the device-wide solve (one per row).
+struct SolveRec {
+  double b;
+  double lap_aL;   // LapSum(a_L) from the scan totals (bracketed only)
+  double lap_aR;   // LapSum(a_R)
+  int32_t ok;      // bracket certified (always 1 for a full sort)
+  int32_t side;    // 0 certified, +1 b >= a_R (LapSum(a_R) > k), -1 b < a_L
+};
+
+// Per-block record of the streaming partition.
+struct PartBlock {
+  int64_t nL, nM, nR;
+  double TL, TR;
+  int32_t overflow;   // this block's M did not fit its staging
+  int32_t pad;
+};
+
+// Totals of the streaming partition (one per attempt).
+struct PartTotals {
+  int64_t nL, nM, nR;
+  double TL, TR;
+  float aL, aR;       // the bracket that was partitioned
+  int32_t any_block_overflow;
+  int32_t pad;
+};
+
+// Order statistics of the noised sample.
+struct SelectRec {
+  float aL, aR;
+  uint32_t keyL, keyR;
+};
+
+// Optional per-kernel event timing (lapsum_profile_*): a no-op unless on.
+void prof_begin(const char* name, hipStream_t s);
+void prof_end(hipStream_t s);
+struct ProfScope {
+  hipStream_t s;
+  ProfScope(const char* name, hipStream_t st) : s(st) { prof_begin(name, st); }
+  ~ProfScope() { prof_end(s); }
+};
+
+// -------------------------------------------------------------- launchers --
+hipError_t launch_fill_u32(uint32_t* dst, int64_t count, uint32_t value, hipStream_t s);
+
+// Full-sort forward for rows with n <= kRowOnChipMax (one workgroup per row).
+hipError_t launch_row_forward(const float* scores, int64_t batch, int64_t n, double k, double t,
+                              float* p, double* b, int32_t* perm, hipStream_t s);
+// Backward for rows with n <= kRowOnChipMax.
+hipError_t launch_row_backward(const float* grad_p, const float* p, int64_t batch, int64_t n,
+                               double t, float* grad_r, hipStream_t s);
+
+// Laplace-CDF emit p = sigma((r - b)/t) for one row, b read from device.
+hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t, float* p,
+                       hipStream_t s);
+
+// Device-wide backward for one row: partial (sum f, sum f g) per block, then
+// the emit (each emit block re-reduces the partials in a fixed order).
+int vjp_reduce_blocks(int64_t n);
+hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
+                             int nblocks, hipStream_t s);
+hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* partials,
+                           int nblocks, double t, float* grad, hipStream_t s);
+
+// Device-wide stable LSD radix sort (descending float order) of one array.
+// Source: floats (converted to keys) or keys; values: none, the source
+// position, or an int32 array.  len_dev (nullable) overrides len with a
+// device-side length <= len.
+struct SortBuffers {
+  uint32_t* keys[2];
+  int32_t* vals[2];
+  uint32_t* hist;      // [256][max_tiles]
+  uint32_t* totals;    // [256]
+  int64_t max_tiles;
+};
+size_t sort_hist_words(int64_t len);
+// Returns the index (0/1) of the buffer holding the sorted result.
+hipError_t launch_sort(const float* src_f, const uint32_t* src_k, const int32_t* src_v,
+                       bool with_vals, int64_t len, const int64_t* len_dev, SortBuffers& sb,
+                       int* out_buf, hipStream_t s);
+
+// Device-wide threshold solve on a sorted (descending keys) array with the
+// bracket tails as carries.  nR/aR/TR: scores ranked before the array; aL/TL:
+// after it (T == 0 or +-inf anchors mean none).  n_total: row length.
+struct SolveArgs {
+  const uint32_t* keys;
+  int64_t len;
+  const int64_t* len_dev;   // nullable
+  double k, t;
+  int64_t n_total;
+  // tails (bracketed); full sort passes zeros / infinities
+  const PartTotals* tails;  // nullable => no tails
+  double* tile_buf;         // kSolveTileDoubles per tile
+  int64_t max_tiles;
+  SolveRec* out;
+  double* b_out;            // nullable: also store b here
+};
+constexpr int kSolveTileDoubles = 8;
+hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s);
+
+// Bracketed pipeline.
+hipError_t launch_sample(const float* r, int64_t n, const float* noise, int64_t K,
+                         uint32_t* ykeys, uint32_t* hist, hipStream_t s);
+hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* hist, int64_t j,
+                         int64_t l, SelectRec* out, hipStream_t s);
+int partition_blocks(int64_t n, int64_t* chunk);
+hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
+                            float aR, double t, int nblocks, int64_t chunk, float* stage_v,
+                            int32_t* stage_i, PartBlock* blk, hipStream_t s);
+hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const SelectRec* sel,
+                                   int use_sel, float aL, float aR, int64_t* offsets,
+                                   PartTotals* tot, hipStream_t s);
+hipError_t launch_gather(const float* r, int64_t n, const PartTotals* tot, const PartBlock* blk,
+                         const int64_t* offsets, int nblocks, int64_t chunk, const float* stage_v,
+                         const int32_t* stage_i, int64_t m_capacity, uint32_t* m_keys,
+                         int32_t* m_idx, hipStream_t s);
+// |M| <= kRowOnChipMax: sort M on chip, certify and solve in one workgroup.
+hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, int64_t m_len,
+                                bool with_idx, const PartTotals* tot, double k, double t,
+                                int64_t n_total, SolveRec* out, int32_t* m_idx_sorted,
+                                hipStream_t s);
+// Copy sorted M indices to the caller's [m_capacity] row, -1 padded.
+hipError_t launch_write_m_idx(const int32_t* sorted_idx, int64_t m_len, int64_t m_capacity,
+                              int32_t* out, hipStream_t s);
+
+}  // namespace lapsum

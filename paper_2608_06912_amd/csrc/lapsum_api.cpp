@@ -1,0 +1,512 @@
+// Host side of liblapsum.so: argument validation, workspace carving, path
+// selection and launch order.  Compiled without floating-point contraction
+// so that the bracket ranks of Eq. (8) are evaluated exactly as written.
+#include <math.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/lapsum.h"
+#include "kernels.hpp"
+
+using namespace lapsum;
+
+// ------------------------------------------------------- kernel timing ----
+namespace {
+struct ProfRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+struct ProfAgg {
+  std::string name;
+  int64_t launches;
+  double total_ms;
+};
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof_recs;
+std::vector<hipEvent_t> g_prof_pool;
+size_t g_prof_pool_used = 0;
+std::vector<ProfAgg> g_prof_aggs;
+
+hipEvent_t prof_event() {
+  if (g_prof_pool_used == g_prof_pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    g_prof_pool.push_back(e);
+  }
+  return g_prof_pool[g_prof_pool_used++];
+}
+}  // namespace
+
+namespace lapsum {
+void prof_begin(const char* name, hipStream_t s) {
+  if (!g_prof_on) return;
+  ProfRec r{name, prof_event(), prof_event()};
+  if (r.a && r.b && hipEventRecord(r.a, s) == hipSuccess) g_prof_recs.push_back(r);
+}
+void prof_end(hipStream_t s) {
+  if (!g_prof_on || g_prof_recs.empty()) return;
+  hipEventRecord(g_prof_recs.back().b, s);
+}
+}  // namespace lapsum
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+// Bump allocator over the caller's workspace; a null base only measures.
+struct Carve {
+  char* base;
+  size_t off = 0;
+  explicit Carve(void* b) : base(static_cast<char*>(b)) {}
+  template <typename T>
+  T* take(size_t count) {
+    off = (off + kAlign - 1) / kAlign * kAlign;
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+  size_t size() const { return (off + kAlign - 1) / kAlign * kAlign; }
+};
+
+int64_t tiles_of(int64_t len) { return (len + kTile - 1) / kTile; }
+
+// ------------------------------------------------------------ device check --
+int check_device() {
+  static std::mutex mu;
+  static int known[64] = {0};   // 0 unknown, 1 gfx950, 2 other
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return LAPSUM_ERR_HIP;
+  if (dev < 0 || dev >= 64) return LAPSUM_ERR_DEVICE;
+  std::lock_guard<std::mutex> g(mu);
+  if (known[dev] == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return LAPSUM_ERR_HIP;
+    known[dev] = (strncmp(prop.gcnArchName, "gfx950", 6) == 0) ? 1 : 2;
+  }
+  return known[dev] == 1 ? LAPSUM_OK : LAPSUM_ERR_DEVICE;
+}
+
+bool valid_common(int64_t batch, int64_t n, double k, double alpha) {
+  if (batch < 1 || n < 1 || n > 2147483647LL) return false;
+  if (!isfinite(k) || !(k > 0.0) || !(k < static_cast<double>(n))) return false;
+  if (!isfinite(alpha) || !(alpha < 0.0)) return false;
+  return true;
+}
+
+int check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return LAPSUM_OK;
+  if (ws == nullptr || have < need) return LAPSUM_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return LAPSUM_ERR_WORKSPACE;
+  return LAPSUM_OK;
+}
+
+#define LAPSUM_TRY(expr)                         \
+  do {                                           \
+    if ((expr) != hipSuccess) return LAPSUM_ERR_HIP; \
+  } while (0)
+
+// --------------------------------------------------- full-sort long rows --
+struct FullWs {
+  SortBuffers sb;
+  double* tile_buf;
+  SolveRec* rec;
+};
+
+FullWs carve_full(Carve& c, int64_t n, bool with_vals) {
+  FullWs w{};
+  const int64_t tiles = tiles_of(n) < 1 ? 1 : tiles_of(n);
+  w.sb.keys[0] = c.take<uint32_t>(n);
+  w.sb.keys[1] = c.take<uint32_t>(n);
+  w.sb.vals[0] = with_vals ? c.take<int32_t>(n) : nullptr;
+  w.sb.vals[1] = with_vals ? c.take<int32_t>(n) : nullptr;
+  w.sb.hist = c.take<uint32_t>(sort_hist_words(n));
+  w.sb.totals = c.take<uint32_t>(256);
+  w.sb.max_tiles = tiles;
+  w.tile_buf = c.take<double>(static_cast<size_t>(tiles) * kSolveTileDoubles);
+  w.rec = c.take<SolveRec>(1);
+  return w;
+}
+
+// Sort one long row, solve for b (written to b_row), optionally copy the
+// permutation.  Does not emit.
+int full_row_solve(const float* r, int64_t n, double k, double t, double* b_row, int32_t* perm_row,
+                   FullWs& w, hipStream_t s) {
+  int which = 0;
+  LAPSUM_TRY(launch_sort(r, nullptr, nullptr, perm_row != nullptr, n, nullptr, w.sb, &which, s));
+  SolveArgs a{};
+  a.keys = w.sb.keys[which];
+  a.len = n;
+  a.len_dev = nullptr;
+  a.k = k;
+  a.t = t;
+  a.n_total = n;
+  a.tails = nullptr;
+  a.tile_buf = w.tile_buf;
+  a.max_tiles = w.sb.max_tiles;
+  a.out = w.rec;
+  a.b_out = b_row;
+  LAPSUM_TRY(launch_sorted_solve(a, s));
+  if (perm_row)
+    LAPSUM_TRY(hipMemcpyAsync(perm_row, w.sb.vals[which], static_cast<size_t>(n) * sizeof(int32_t),
+                              hipMemcpyDeviceToDevice, s));
+  return LAPSUM_OK;
+}
+
+size_t forward_ws(int64_t n, bool with_perm) {
+  if (n <= kRowOnChipMax) return 0;
+  Carve c(nullptr);
+  carve_full(c, n, with_perm);
+  return c.size();
+}
+
+// --------------------------------------------------------------- bracket --
+struct BracketWs {
+  uint32_t* ykeys;
+  uint32_t* hist;
+  SelectRec* sel;
+  PartBlock* blk;
+  int64_t* offsets;
+  PartTotals* tot;
+  float* stage_v;
+  int32_t* stage_i;
+  uint32_t* m_keys;
+  int32_t* m_idx;
+  int32_t* m_idx_sorted;
+  SortBuffers msb;     // device-wide sort of M (|M| > on-chip limit)
+  double* m_tile_buf;
+  SolveRec* rec;
+  FullWs fall;         // full-sort fallback
+  int nblocks;
+  int64_t chunk;
+};
+
+BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_idx) {
+  BracketWs w{};
+  w.nblocks = partition_blocks(n, &w.chunk);
+  w.ykeys = c.take<uint32_t>(K);
+  w.hist = c.take<uint32_t>(kSelectBins);
+  w.sel = c.take<SelectRec>(1);
+  w.blk = c.take<PartBlock>(w.nblocks);
+  w.offsets = c.take<int64_t>(w.nblocks);
+  w.tot = c.take<PartTotals>(1);
+  w.stage_v = c.take<float>(static_cast<size_t>(w.nblocks) * kPartStageCap);
+  w.stage_i = c.take<int32_t>(static_cast<size_t>(w.nblocks) * kPartStageCap);
+  w.m_keys = c.take<uint32_t>(mcap);
+  w.m_idx = c.take<int32_t>(mcap);
+  w.m_idx_sorted = with_idx ? c.take<int32_t>(mcap < kRowOnChipMax ? mcap : kRowOnChipMax) : nullptr;
+  if (mcap > kRowOnChipMax) {
+    const int64_t mt = tiles_of(mcap);
+    w.msb.keys[0] = c.take<uint32_t>(mcap);
+    w.msb.keys[1] = c.take<uint32_t>(mcap);
+    w.msb.vals[0] = with_idx ? c.take<int32_t>(mcap) : nullptr;
+    w.msb.vals[1] = with_idx ? c.take<int32_t>(mcap) : nullptr;
+    w.msb.hist = c.take<uint32_t>(sort_hist_words(mcap));
+    w.msb.totals = c.take<uint32_t>(256);
+    w.msb.max_tiles = mt;
+    w.m_tile_buf = c.take<double>(static_cast<size_t>(mt) * kSolveTileDoubles);
+  }
+  w.rec = c.take<SolveRec>(1);
+  if (n > kRowOnChipMax) w.fall = carve_full(c, n, false);
+  return w;
+}
+
+size_t bracketed_ws(int64_t n, int64_t K, int64_t mcap, bool with_idx) {
+  Carve c(nullptr);
+  carve_bracket(c, n, K, mcap, with_idx);
+  return c.size();
+}
+
+// Eq. (8) in IEEE float64, left to right, no contraction.
+void bracket_ranks(int64_t n, double k, int64_t K, double z, int64_t* j, int64_t* l) {
+  const double q = (static_cast<double>(n) - k) / static_cast<double>(n);
+  const double Kq = static_cast<double>(K) * q;
+  const double var = Kq * (1.0 - q);
+  const double sd = sqrt(var);
+  const double zs = z * sd;
+  *j = static_cast<int64_t>(floor(Kq - zs));
+  *l = static_cast<int64_t>(ceil(Kq + zs));
+}
+
+// One-sided doubling, float64 on the float32 endpoints, rounded to float32.
+void widen(float* aL, float* aR, int side) {
+  const double L = *aL, R = *aR;
+  const double w = R - L;
+  if (side > 0) {
+    *aL = static_cast<float>(R);
+    *aR = static_cast<float>(R + 2.0 * w);
+  } else {
+    *aL = static_cast<float>(L - 2.0 * w);
+    *aR = static_cast<float>(L);
+  }
+}
+
+template <typename T>
+int read_back(T* host, const T* dev, hipStream_t s) {
+  if (hipMemcpyAsync(host, dev, sizeof(T), hipMemcpyDeviceToHost, s) != hipSuccess) return LAPSUM_ERR_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return LAPSUM_ERR_HIP;
+  return LAPSUM_OK;
+}
+
+int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, double z,
+                  const float* noise, int64_t mcap, int64_t out_cap, uint32_t flags, float* p_row,
+                  double* b_row,
+                  lapsum_bracket_info* info, int32_t* midx_row, BracketWs& w, hipStream_t s) {
+  const double t = -alpha;
+  lapsum_bracket_info rec_info;
+  memset(&rec_info, 0, sizeof(rec_info));
+  int64_t j = 0, l = 0;
+  bracket_ranks(n, k, K, z, &j, &l);
+  rec_info.j = j;
+  rec_info.l = l;
+  bool solved = false;
+  bool wrote_midx = false;
+
+  if (!(flags & LAPSUM_FLAG_FULL_SORT)) {
+    LAPSUM_TRY(launch_fill_u32(w.hist, kSelectBins, 0u, s));
+    LAPSUM_TRY(launch_sample(r, n, noise, K, w.ykeys, w.hist, s));
+    LAPSUM_TRY(launch_select(w.ykeys, K, w.hist, j, l, w.sel, s));
+    float aL = 0.0f, aR = 0.0f;
+    for (int attempt = 1; attempt <= 3 && !solved; ++attempt) {
+      const int use_sel = attempt == 1 ? 1 : 0;
+      LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR, t, w.nblocks, w.chunk, w.stage_v,
+                                  w.stage_i, w.blk, s));
+      LAPSUM_TRY(launch_partition_totals(w.blk, w.nblocks, w.sel, use_sel, aL, aR, w.offsets, w.tot, s));
+      LAPSUM_TRY(launch_gather(r, n, w.tot, w.blk, w.offsets, w.nblocks, w.chunk, w.stage_v,
+                               w.stage_i, mcap, w.m_keys, w.m_idx, s));
+      PartTotals tot;
+      int st = read_back(&tot, w.tot, s);
+      if (st != LAPSUM_OK) return st;
+      aL = tot.aL;
+      aR = tot.aR;
+      rec_info.attempts = attempt;
+      rec_info.a_L = tot.aL;
+      rec_info.a_R = tot.aR;
+      rec_info.n_L = tot.nL;
+      rec_info.n_M = tot.nM;
+      rec_info.n_R = tot.nR;
+      rec_info.T_L = tot.TL;
+      rec_info.T_R = tot.TR;
+      if (tot.nM > mcap) {
+        // no room for M: the certificate is never evaluated
+        rec_info.m_overflow = 1;
+        rec_info.lap_aL = NAN;
+        rec_info.lap_aR = NAN;
+        break;
+      }
+      const bool want_idx = midx_row != nullptr;
+      const int32_t* sorted_idx = nullptr;
+      if (tot.nM <= kRowOnChipMax) {
+        LAPSUM_TRY(launch_small_m_solve(w.m_keys, w.m_idx, tot.nM, want_idx, w.tot, k, t, n, w.rec,
+                                        w.m_idx_sorted, s));
+        sorted_idx = w.m_idx_sorted;
+      } else {
+        int which = 0;
+        LAPSUM_TRY(launch_sort(nullptr, w.m_keys, w.m_idx, want_idx, tot.nM, nullptr, w.msb, &which, s));
+        SolveArgs a{};
+        a.keys = w.msb.keys[which];
+        a.len = tot.nM;
+        a.len_dev = nullptr;
+        a.k = k;
+        a.t = t;
+        a.n_total = n;
+        a.tails = w.tot;
+        a.tile_buf = w.m_tile_buf;
+        a.max_tiles = w.msb.max_tiles;
+        a.out = w.rec;
+        a.b_out = nullptr;
+        LAPSUM_TRY(launch_sorted_solve(a, s));
+        sorted_idx = want_idx ? w.msb.vals[which] : nullptr;
+      }
+      SolveRec rec;
+      st = read_back(&rec, w.rec, s);
+      if (st != LAPSUM_OK) return st;
+      rec_info.lap_aL = rec.lap_aL;
+      rec_info.lap_aR = rec.lap_aR;
+      if (rec.ok) {
+        LAPSUM_TRY(hipMemcpyAsync(b_row, &w.rec->b, sizeof(double), hipMemcpyDeviceToDevice, s));
+        if (want_idx) {
+          LAPSUM_TRY(launch_write_m_idx(sorted_idx, tot.nM, out_cap, midx_row, s));
+          wrote_midx = true;
+        }
+        solved = true;
+        break;
+      }
+      if (attempt < 3) widen(&aL, &aR, rec.side);
+    }
+  }
+  if (!solved) {
+    rec_info.fell_back = 1;
+    if (n <= kRowOnChipMax) {
+      // the on-chip kernel also emits p
+      LAPSUM_TRY(launch_row_forward(r, 1, n, k, t, p_row, b_row, nullptr, s));
+    } else {
+      int st = full_row_solve(r, n, k, t, b_row, nullptr, w.fall, s);
+      if (st != LAPSUM_OK) return st;
+      LAPSUM_TRY(launch_emit(r, n, b_row, t, p_row, s));
+    }
+  } else {
+    LAPSUM_TRY(launch_emit(r, n, b_row, t, p_row, s));
+  }
+  if (midx_row && !wrote_midx) LAPSUM_TRY(launch_write_m_idx(nullptr, 0, out_cap, midx_row, s));
+  if (info) *info = rec_info;
+  return LAPSUM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int lapsum_profile_start(void) {
+  g_prof_recs.clear();
+  g_prof_aggs.clear();
+  g_prof_pool_used = 0;
+  g_prof_on = true;
+  return LAPSUM_OK;
+}
+
+int lapsum_profile_stop(void) {
+  g_prof_on = false;
+  std::map<std::string, size_t> where;
+  for (const ProfRec& r : g_prof_recs) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return -LAPSUM_ERR_HIP;
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return -LAPSUM_ERR_HIP;
+    auto it = where.find(r.name);
+    if (it == where.end()) {
+      where[r.name] = g_prof_aggs.size();
+      g_prof_aggs.push_back(ProfAgg{r.name, 1, static_cast<double>(ms)});
+    } else {
+      g_prof_aggs[it->second].launches += 1;
+      g_prof_aggs[it->second].total_ms += ms;
+    }
+  }
+  g_prof_recs.clear();
+  g_prof_pool_used = 0;
+  return static_cast<int>(g_prof_aggs.size());
+}
+
+int lapsum_profile_entry(int i, char* name, size_t name_len, int64_t* launches, double* total_ms) {
+  if (i < 0 || static_cast<size_t>(i) >= g_prof_aggs.size() || !name || name_len == 0)
+    return LAPSUM_ERR_INVALID_ARG;
+  const ProfAgg& a = g_prof_aggs[static_cast<size_t>(i)];
+  strncpy(name, a.name.c_str(), name_len - 1);
+  name[name_len - 1] = '\0';
+  if (launches) *launches = a.launches;
+  if (total_ms) *total_ms = a.total_ms;
+  return LAPSUM_OK;
+}
+
+const char* lapsum_status_string(int status) {
+  switch (status) {
+    case LAPSUM_OK: return "ok";
+    case LAPSUM_ERR_INVALID_ARG: return "invalid argument";
+    case LAPSUM_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+    case LAPSUM_ERR_HIP: return "HIP runtime or launch error";
+    case LAPSUM_ERR_DEVICE: return "current device is not gfx950";
+    default: return "unknown status";
+  }
+}
+
+size_t lapsum_forward_workspace_size(int64_t batch, int64_t n, int with_perm) {
+  (void)batch;
+  if (n < 1) return 0;
+  return forward_ws(n, with_perm != 0);
+}
+
+int lapsum_forward(const float* scores, int64_t batch, int64_t n, double k, double alpha, float* p,
+                   double* b, int32_t* perm_out, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream) {
+  if (!scores || !p || !b || !valid_common(batch, n, k, alpha)) return LAPSUM_ERR_INVALID_ARG;
+  const int wst = check_ws(workspace, workspace_bytes, forward_ws(n, perm_out != nullptr));
+  if (wst != LAPSUM_OK) return wst;
+  const int dst = check_device();
+  if (dst != LAPSUM_OK) return dst;
+  const double t = -alpha;
+  if (n <= kRowOnChipMax) {
+    LAPSUM_TRY(launch_row_forward(scores, batch, n, k, t, p, b, perm_out, stream));
+    return LAPSUM_OK;
+  }
+  Carve c(workspace);
+  FullWs w = carve_full(c, n, perm_out != nullptr);
+  for (int64_t row = 0; row < batch; ++row) {
+    const float* r = scores + row * n;
+    int st = full_row_solve(r, n, k, t, b + row, perm_out ? perm_out + row * n : nullptr, w, stream);
+    if (st != LAPSUM_OK) return st;
+    LAPSUM_TRY(launch_emit(r, n, b + row, t, p + row * n, stream));
+  }
+  return LAPSUM_OK;
+}
+
+size_t lapsum_backward_workspace_size(int64_t batch, int64_t n) {
+  (void)batch;
+  if (n <= kRowOnChipMax) return 0;
+  Carve c(nullptr);
+  c.take<double>(2 * static_cast<size_t>(vjp_reduce_blocks(n)));
+  return c.size();
+}
+
+int lapsum_backward(const float* grad_p, const float* p, const double* b, int64_t batch, int64_t n,
+                    double alpha, float* grad_r, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+  (void)b;
+  if (!grad_p || !p || !grad_r) return LAPSUM_ERR_INVALID_ARG;
+  if (batch < 1 || n < 1 || n > 2147483647LL || !isfinite(alpha) || !(alpha < 0.0))
+    return LAPSUM_ERR_INVALID_ARG;
+  const int wst = check_ws(workspace, workspace_bytes, lapsum_backward_workspace_size(batch, n));
+  if (wst != LAPSUM_OK) return wst;
+  const int dst = check_device();
+  if (dst != LAPSUM_OK) return dst;
+  const double t = -alpha;
+  if (n <= kRowOnChipMax) {
+    LAPSUM_TRY(launch_row_backward(grad_p, p, batch, n, t, grad_r, stream));
+    return LAPSUM_OK;
+  }
+  Carve c(workspace);
+  const int nb = vjp_reduce_blocks(n);
+  double* partials = c.take<double>(2 * static_cast<size_t>(nb));
+  for (int64_t row = 0; row < batch; ++row) {
+    const int64_t o = row * n;
+    LAPSUM_TRY(launch_vjp_reduce(grad_p + o, p + o, n, partials, nb, stream));
+    LAPSUM_TRY(launch_vjp_emit(grad_p + o, p + o, n, partials, nb, t, grad_r + o, stream));
+  }
+  return LAPSUM_OK;
+}
+
+size_t lapsum_forward_bracketed_workspace_size(int64_t batch, int64_t n, int64_t K,
+                                               int64_t m_capacity, int with_m_idx) {
+  (void)batch;
+  if (n < 1 || K < 1 || m_capacity < 1) return 0;
+  return bracketed_ws(n, K, m_capacity < n ? m_capacity : n, with_m_idx != 0);
+}
+
+int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n, double k, double alpha,
+                             int64_t K, double z, const float* noise, int64_t m_capacity,
+                             uint32_t flags, float* p, double* b, lapsum_bracket_info* info,
+                             int32_t* m_idx_out, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+  if (!scores || !p || !b || !noise || !valid_common(batch, n, k, alpha)) return LAPSUM_ERR_INVALID_ARG;
+  if (K < 2 || K > n || !isfinite(z) || !(z > 0.0) || m_capacity < 1 || (flags & ~LAPSUM_FLAG_FULL_SORT))
+    return LAPSUM_ERR_INVALID_ARG;
+  // |M| <= n always, so capacity beyond n is never used internally; the
+  // caller's m_idx_out rows keep their m_capacity stride.
+  const int64_t mcap = m_capacity < n ? m_capacity : n;
+  const int wst = check_ws(workspace, workspace_bytes, bracketed_ws(n, K, mcap, m_idx_out != nullptr));
+  if (wst != LAPSUM_OK) return wst;
+  const int dst = check_device();
+  if (dst != LAPSUM_OK) return dst;
+  Carve c(workspace);
+  BracketWs w = carve_bracket(c, n, K, mcap, m_idx_out != nullptr);
+  for (int64_t row = 0; row < batch; ++row) {
+    int st = bracketed_row(scores + row * n, n, k, alpha, K, z, noise, mcap, m_capacity, flags,
+                           p + row * n, b + row, info ? info + row : nullptr,
+                           m_idx_out ? m_idx_out + row * m_capacity : nullptr, w, stream);
+    if (st != LAPSUM_OK) return st;
+  }
+  return LAPSUM_OK;
+}
+
+}  // extern "C"

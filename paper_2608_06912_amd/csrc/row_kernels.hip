@@ -1,0 +1,187 @@
+// One workgroup per row, the whole row on chip (n <= 32768): the full-sort
+// forward of §1/§3/Suppl. A and the VJP of Eq. (5).
+//
+// Forward: the row's keys are sorted in LDS (block_sort.hpp), the sorted run
+// is solved by block_solve (scan, lookup, closed-form root, common.hpp), and
+// p is written in the original order.  HBM traffic: read r, write p (the
+// second read of r for the emit hits L2).  Backward: p and g stay in
+// registers between the reduction and the emit, so read g, p and write
+// grad_r once each.
+#include "block_sort.hpp"
+#include "kernels.hpp"
+
+namespace lapsum {
+
+template <int BLOCK, int ITEMS, bool PAIRS>
+__global__ __launch_bounds__(BLOCK) void row_forward_kernel(const float* __restrict__ scores,
+                                                            int n, double k, double t,
+                                                            float* __restrict__ p,
+                                                            double* __restrict__ b_out,
+                                                            int32_t* __restrict__ perm) {
+  constexpr int WAVES = BLOCK / kWave;
+  __shared__ uint32_t buf[BLOCK * ITEMS];
+  __shared__ SortSmem<BLOCK> ssm;
+  __shared__ ScanSmem<WAVES> csm;
+
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  const int64_t row = blockIdx.x;
+  const float* r = scores + row * n;
+
+  uint32_t key[ITEMS];
+  int32_t val[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int pos = wid * (kWave * ITEMS) + i * kWave + lane;
+    if (pos < n) {
+      key[i] = desc_key(r[pos]);
+      val[i] = pos;
+    } else {
+      key[i] = 0xffffffffu;   // after every finite score
+      val[i] = -1;
+    }
+  }
+  block_sort_u32<BLOCK, ITEMS, PAIRS>(key, val, buf, ssm);
+
+  float s[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) s[i] = key_float(key[i]);
+  int cnt = n - tid * ITEMS;
+  cnt = cnt < 0 ? 0 : (cnt > ITEMS ? ITEMS : cnt);
+  Pre pt;
+  Suf st;
+  const double b = block_solve<BLOCK, ITEMS>(s, cnt, 0.0, pre_empty(), suf_empty(), k, t, csm, &pt, &st);
+  if (tid == 0) b_out[row] = b;
+
+  if constexpr (PAIRS) {
+    int32_t* pr = perm + row * n;
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i)
+      if (i < cnt) pr[tid * ITEMS + i] = val[i];
+  }
+
+  const double inv_t = 1.0 / t;
+  float* pr = p + row * n;
+  if ((n & 3) == 0) {
+    const float4* r4 = reinterpret_cast<const float4*>(r);
+    float4* p4 = reinterpret_cast<float4*>(pr);
+    for (int j = tid; j < n / 4; j += BLOCK) {
+      const float4 v = r4[j];
+      float4 o;
+      o.x = laplace_p(v.x, b, inv_t);
+      o.y = laplace_p(v.y, b, inv_t);
+      o.z = laplace_p(v.z, b, inv_t);
+      o.w = laplace_p(v.w, b, inv_t);
+      p4[j] = o;
+    }
+  } else {
+    for (int j = tid; j < n; j += BLOCK) pr[j] = laplace_p(r[j], b, inv_t);
+  }
+}
+
+template <int BLOCK, int ITEMS>
+__global__ __launch_bounds__(BLOCK) void row_backward_kernel(const float* __restrict__ g,
+                                                             const float* __restrict__ p, int n,
+                                                             double t, float* __restrict__ grad) {
+  constexpr int WAVES = BLOCK / kWave;
+  __shared__ double red[2 * WAVES];
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const float* pr = p + row * n;
+  const float* gr = g + row * n;
+  double F = 0.0, G = 0.0;
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int j = i * BLOCK + tid;
+    if (j < n) {
+      const float pp = pr[j];
+      const float f = fminf(pp, 1.0f - pp);   // e^{-|b-r|/t} / 2, exact from p
+      F += static_cast<double>(f);
+      if (f != 0.0f) G += static_cast<double>(f) * static_cast<double>(gr[j]);
+    }
+  }
+  F = wave_sum(F);
+  G = wave_sum(G);
+  const int wid = tid / kWave;
+  if (lane_id() == 0) {
+    red[wid] = F;
+    red[WAVES + wid] = G;
+  }
+  __syncthreads();
+  F = 0.0;
+  G = 0.0;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    F += red[w];
+    G += red[WAVES + w];
+  }
+  // grad_r = (f/t) (g - <g, q>), q = f / sum f; zero when sum f == 0.  The
+  // second read of p and g hits L2 (the row is at most 256 KB).
+  const double coef = (F > 0.0) ? G / F : 0.0;
+  const double scale = (F > 0.0) ? 1.0 / t : 0.0;
+  float* out = grad + row * n;
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int j = i * BLOCK + tid;
+    if (j < n) {
+      const float pp = pr[j];
+      const float f = fminf(pp, 1.0f - pp);
+      out[j] = (f != 0.0f)
+                   ? static_cast<float>(static_cast<double>(f) * scale * (static_cast<double>(gr[j]) - coef))
+                   : 0.0f;
+    }
+  }
+}
+
+namespace {
+
+template <int BLOCK, int ITEMS>
+hipError_t fwd_items(const float* scores, int64_t batch, int64_t n, double k, double t, float* p,
+                     double* b, int32_t* perm, hipStream_t s) {
+  if (perm)
+    { ProfScope ps_("row_forward", s);
+    hipLaunchKernelGGL((row_forward_kernel<BLOCK, ITEMS, true>), dim3(batch), dim3(BLOCK), 0, s,
+                       scores, static_cast<int>(n), k, t, p, b, perm); }
+  else
+    { ProfScope ps_("row_forward", s);
+    hipLaunchKernelGGL((row_forward_kernel<BLOCK, ITEMS, false>), dim3(batch), dim3(BLOCK), 0, s,
+                       scores, static_cast<int>(n), k, t, p, b, perm); }
+  return hipGetLastError();
+}
+
+template <int BLOCK, int ITEMS>
+hipError_t bwd_items(const float* g, const float* p, int64_t batch, int64_t n, double t,
+                     float* grad, hipStream_t s) {
+  { ProfScope ps_("row_backward", s);
+  hipLaunchKernelGGL((row_backward_kernel<BLOCK, ITEMS>), dim3(batch), dim3(BLOCK), 0, s, g, p,
+                     static_cast<int>(n), t, grad); }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_row_forward(const float* scores, int64_t batch, int64_t n, double k, double t,
+                              float* p, double* b, int32_t* perm, hipStream_t s) {
+  if (n <= 256) return fwd_items<256, 1>(scores, batch, n, k, t, p, b, perm, s);
+  if (n <= 512) return fwd_items<256, 2>(scores, batch, n, k, t, p, b, perm, s);
+  if (n <= 1024) return fwd_items<256, 4>(scores, batch, n, k, t, p, b, perm, s);
+  if (n <= 2048) return fwd_items<256, 8>(scores, batch, n, k, t, p, b, perm, s);
+  if (n <= 4096) return fwd_items<1024, 4>(scores, batch, n, k, t, p, b, perm, s);
+  if (n <= 8192) return fwd_items<1024, 8>(scores, batch, n, k, t, p, b, perm, s);
+  if (n <= 16384) return fwd_items<1024, 16>(scores, batch, n, k, t, p, b, perm, s);
+  if (n <= kRowOnChipMax) return fwd_items<1024, 32>(scores, batch, n, k, t, p, b, perm, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_row_backward(const float* grad_p, const float* p, int64_t batch, int64_t n,
+                               double t, float* grad_r, hipStream_t s) {
+  if (n <= 1024) return bwd_items<256, 4>(grad_p, p, batch, n, t, grad_r, s);
+  if (n <= 4096) return bwd_items<1024, 4>(grad_p, p, batch, n, t, grad_r, s);
+  if (n <= 8192) return bwd_items<1024, 8>(grad_p, p, batch, n, t, grad_r, s);
+  if (n <= 16384) return bwd_items<1024, 16>(grad_p, p, batch, n, t, grad_r, s);
+  if (n <= kRowOnChipMax) return bwd_items<1024, 32>(grad_p, p, batch, n, t, grad_r, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace lapsum

@@ -1,0 +1,378 @@
+// Threshold solve on a sorted array (descending keys), device-wide.
+//
+// The node curve N_i = LapSum(s_i) is non-decreasing, so the interval that
+// holds b lies in exactly one tile: only that tile needs per-position node
+// values.  Two kernels:
+//   solve_tiles     one block per 4096-key tile: the tile's summaries
+//                   Pre = (last, sum e^{-(s-last)/t}) and
+//                   Suf = (first, 1 + sum_{after first} e^{-(first-s)/t}),
+//                   every term relative to the tile's own anchor
+//   solve_finalize  one block: shift-carrying scans over the tile summaries
+//                   from both ends (seeded with the bracket tails), the node
+//                   value at each tile's first score, the crossing tile, and
+//                   block_solve on that tile; for a bracket also the
+//                   certificate LapSum(a_R) <= k <= LapSum(a_L) from the totals
+//                   (Suppl. B / Suppl. C)
+// Reads the sorted keys once plus one tile: 4 bytes per score.
+//
+// For |M| <= 32768 one workgroup sorts M on chip and solves it in a single
+// launch (small_m_solve).
+#include <math.h>
+
+#include "block_sort.hpp"
+#include "kernels.hpp"
+
+namespace lapsum {
+
+namespace {
+constexpr int TT = kTileThreads;
+constexpr int TI = kTileItems;
+constexpr int64_t TILE = kTile;
+constexpr int kTileRec = 8;   // doubles per tile: S, X, first, last, suffix after (v, T), prefix before (u, S)
+
+__device__ __forceinline__ int64_t eff_len(int64_t len, const int64_t* len_dev) {
+  if (len_dev == nullptr) return len;
+  const int64_t d = *len_dev;
+  return d < len ? (d < 0 ? 0 : d) : len;
+}
+
+struct Tails {
+  double nR, nL;
+  float aR, aL;
+  Pre pre;   // R tail at a_R
+  Suf suf;   // L tail at a_L
+  bool bracketed;
+};
+
+__device__ Tails load_tails(const PartTotals* tot) {
+  Tails x;
+  if (tot == nullptr) {
+    x.nR = x.nL = 0.0;
+    x.aR = INFINITY;
+    x.aL = -INFINITY;
+    x.pre = pre_empty();
+    x.suf = suf_empty();
+    x.bracketed = false;
+    return x;
+  }
+  x.nR = static_cast<double>(tot->nR);
+  x.nL = static_cast<double>(tot->nL);
+  x.aR = tot->aR;
+  x.aL = tot->aL;
+  x.pre = (tot->nR > 0 && tot->TR > 0.0) ? Pre{tot->aR, tot->TR} : pre_empty();
+  x.suf = (tot->nL > 0 && tot->TL > 0.0) ? Suf{tot->aL, tot->TL} : suf_empty();
+  x.bracketed = true;
+  return x;
+}
+
+// Certificate values from the scan totals.  pre_all = R tail (+) M (anchor:
+// last of M, or a_R when M is empty); suf_all = M (+) L tail.
+__device__ void certify(const Tails& x, double m_len, double n_total, double k, double t,
+                        Pre pre_all, Suf suf_all, SolveRec& rec) {
+  const double inv_t = 1.0 / t;
+  double lap_aR = 0.0, lap_aL = n_total;
+  if (isfinite(x.aR)) {
+    // scores >= a_R contribute 1 - e^{-(r-a_R)/t}/2, the others e^{-(a_R-r)/t}/2
+    const double TR = x.pre.S;
+    lap_aR = x.nR - 0.5 * TR;
+    if (suf_all.T != 0.0)
+      lap_aR += 0.5 * wexp_f64(static_cast<double>(x.aR) - static_cast<double>(suf_all.v), inv_t) * suf_all.T;
+  }
+  if (isfinite(x.aL)) {
+    lap_aL = x.nR + m_len + 0.5 * x.suf.T;
+    if (pre_all.S != 0.0)
+      lap_aL -= 0.5 * wexp_f64(static_cast<double>(pre_all.u) - static_cast<double>(x.aL), inv_t) * pre_all.S;
+  }
+  rec.lap_aL = lap_aL;
+  rec.lap_aR = lap_aR;
+  const bool okR = lap_aR <= k;
+  const bool okL = k <= lap_aL;
+  rec.ok = (okR && okL) ? 1 : 0;
+  rec.side = okR ? (okL ? 0 : -1) : 1;
+}
+
+// b when the array is empty, or when b lies above its first score:
+// the c_up = n_R scores above are the R tail, the rest summarised by `below`.
+__device__ double root_above(const Tails& x, Suf below, double k, double t) {
+  const bool has_up = x.pre.S != 0.0;
+  const bool has_dn = below.T != 0.0;
+  return gap_root(k, t, x.nR, has_up, x.pre.u, has_up ? log(x.pre.S) : 0.0, has_dn, below.v,
+                  has_dn ? log(below.T) : 0.0);
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(TT) void solve_tiles_kernel(const uint32_t* __restrict__ keys,
+                                                         int64_t len, const int64_t* len_dev,
+                                                         double t, double* __restrict__ tiles) {
+  const int64_t m = eff_len(len, len_dev);
+  const int64_t ntiles = (m + TILE - 1) / TILE;
+  const int64_t tile = blockIdx.x;
+  if (tile >= ntiles) return;
+  __shared__ double red[2][TT / kWave];
+  const int tid = threadIdx.x;
+  const int64_t base = tile * TILE;
+  const int64_t nv = (m - base) < TILE ? (m - base) : TILE;
+  const double first = key_float(keys[base]);
+  const double last = key_float(keys[base + nv - 1]);
+  const double c2 = kLog2e / t;
+  double S = 0.0, X = 0.0;
+  const int64_t p0 = base + static_cast<int64_t>(tid) * TI;
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    if (static_cast<int64_t>(tid) * TI + i < nv) {
+      const double s = key_float(keys[p0 + i]);
+      S += wexp_f32(s - last, c2);
+      if (tid * TI + i > 0) X += wexp_f32(first - s, c2);
+    }
+  }
+  S = wave_sum(S);
+  X = wave_sum(X);
+  const int wid = tid / kWave;
+  if (lane_id() == 0) {
+    red[0][wid] = S;
+    red[1][wid] = X;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double s = 0.0, x = 0.0;
+#pragma unroll
+    for (int w = 0; w < TT / kWave; ++w) {
+      s += red[0][w];
+      x += red[1][w];
+    }
+    double* rec = tiles + tile * kTileRec;
+    rec[0] = s;
+    rec[1] = x;
+    rec[2] = first;
+    rec[3] = last;
+  }
+}
+
+__global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double* b_out) {
+  constexpr int WAVES = TT / kWave;
+  __shared__ ScanSmem<WAVES> sm;
+  __shared__ int64_t cnt_s[WAVES];
+  __shared__ Pre tile_pre_s;
+  __shared__ Suf tile_suf_s;
+  const int tid = threadIdx.x;
+  const double t = a.t;
+  const double inv_t = 1.0 / t;
+  const double k = a.k;
+  const int64_t m = eff_len(a.len, a.len_dev);
+  const int64_t ntiles = (m + TILE - 1) / TILE;
+  const Tails x = load_tails(a.tails);
+  double* tb = a.tile_buf;
+
+  // 1. this thread's run of tiles
+  const int64_t per = (ntiles + TT - 1) / TT;
+  const int64_t t0 = static_cast<int64_t>(tid) * per;
+  const int64_t t1 = (t0 + per < ntiles) ? t0 + per : ntiles;
+  Pre mp = pre_empty();
+  Suf ms = suf_empty();
+  for (int64_t q = t0; q < t1; ++q) {
+    const double* r = tb + q * kTileRec;
+    mp = pre_combine(mp, Pre{static_cast<float>(r[3]), r[0]}, inv_t);
+  }
+  for (int64_t q = t1 - 1; q >= t0; --q) {
+    const double* r = tb + q * kTileRec;
+    ms = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, ms, inv_t);
+  }
+  Pre pre_all;
+  Suf suf_all;
+  const Pre pre_in = block_excl_pre<WAVES>(mp, x.pre, inv_t, sm, &pre_all);
+  const Suf suf_in = block_excl_suf<WAVES>(ms, x.suf, inv_t, sm, &suf_all);
+
+  // 2. suffix carried into each tile from the right (stored), then the node
+  //    value at each tile's first score walking left to right
+  {
+    Suf after = suf_in;
+    for (int64_t q = t1 - 1; q >= t0; --q) {
+      double* r = tb + q * kTileRec;
+      r[4] = after.v;
+      r[5] = after.T;
+      after = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, after, inv_t);
+    }
+  }
+  int64_t below = 0;
+  {
+    Pre before = pre_in;
+    for (int64_t q = t0; q < t1; ++q) {
+      double* r = tb + q * kTileRec;
+      r[6] = before.u;
+      r[7] = before.S;
+      const double first = r[2];
+      double P = 1.0;
+      if (before.S != 0.0) P += wexp_f64(static_cast<double>(before.u) - first, inv_t) * before.S;
+      double E = r[1];
+      if (r[5] != 0.0) E += wexp_f64(first - r[4], inv_t) * r[5];
+      const double N = x.nR + static_cast<double>(q * TILE) + 1.0 - 0.5 * P + 0.5 * E;
+      if (N <= k) below = q + 1;   // non-decreasing: the last such tile
+      before = pre_combine(before, Pre{static_cast<float>(r[3]), r[0]}, inv_t);
+    }
+  }
+  // crossing tile = max over threads of `below`
+  {
+    int64_t v = below;
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) {
+      const int64_t w = __shfl_xor(v, o, kWave);
+      v = w > v ? w : v;
+    }
+    if (lane_id() == 0) cnt_s[tid / kWave] = v;
+    __syncthreads();
+    v = 0;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) v = cnt_s[w] > v ? cnt_s[w] : v;
+    below = v;
+    __syncthreads();
+  }
+
+  SolveRec rec;
+  rec.ok = 1;
+  rec.side = 0;
+  rec.lap_aL = 0.0;
+  rec.lap_aR = 0.0;
+  if (x.bracketed) {
+    // pre_all / suf_all already include the tails
+    certify(x, static_cast<double>(m), static_cast<double>(a.n_total), k, t, pre_all, suf_all, rec);
+  }
+
+  double b;
+  if (m == 0 || below == 0) {
+    b = root_above(x, suf_all, k, t);
+  } else {
+    const int64_t ct = below - 1;
+    if (tid == 0) {
+      const double* r = tb + ct * kTileRec;
+      tile_pre_s = Pre{static_cast<float>(r[6]), r[7]};
+      tile_suf_s = Suf{static_cast<float>(r[4]), r[5]};
+    }
+    __syncthreads();
+    const Pre tp = tile_pre_s;
+    const Suf ts = tile_suf_s;
+    const int64_t base = ct * TILE;
+    const int64_t nv = (m - base) < TILE ? (m - base) : TILE;
+    float s[TI];
+    int cnt = static_cast<int>(nv - static_cast<int64_t>(tid) * TI);
+    cnt = cnt < 0 ? 0 : (cnt > TI ? TI : cnt);
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+      s[i] = (i < cnt) ? key_float(a.keys[base + static_cast<int64_t>(tid) * TI + i]) : 0.0f;
+    Pre pt;
+    Suf st;
+    b = block_solve<TT, TI>(s, cnt, x.nR + static_cast<double>(base), tp, ts, k, t, sm, &pt, &st);
+  }
+  if (tid == 0) {
+    rec.b = b;
+    *a.out = rec;
+    if (b_out) *b_out = b;
+  }
+}
+
+hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s) {
+  const int64_t tiles = (a.len + TILE - 1) / TILE;
+  if (tiles > a.max_tiles) return hipErrorInvalidValue;
+  if (tiles > 0)
+    { ProfScope ps_("solve_tiles", s);
+    hipLaunchKernelGGL(solve_tiles_kernel, dim3(static_cast<unsigned>(tiles)), dim3(TT), 0, s,
+                       a.keys, a.len, a.len_dev, a.t, a.tile_buf); }
+  { ProfScope ps_("solve_finalize", s);
+  hipLaunchKernelGGL(solve_finalize_kernel, dim3(1), dim3(TT), 0, s, a, a.b_out); }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------- small middle set ----
+template <bool PAIRS>
+__global__ __launch_bounds__(1024) void small_m_solve_kernel(const uint32_t* __restrict__ m_keys,
+                                                             const int32_t* __restrict__ m_idx,
+                                                             const PartTotals* __restrict__ tot,
+                                                             double k, double t, int64_t n_total,
+                                                             SolveRec* __restrict__ out,
+                                                             int32_t* __restrict__ idx_sorted) {
+  constexpr int BLOCK = 1024;
+  constexpr int ITEMS = 32;
+  constexpr int WAVES = BLOCK / kWave;
+  __shared__ uint32_t buf[BLOCK * ITEMS];
+  __shared__ SortSmem<BLOCK> ssm;
+  __shared__ ScanSmem<WAVES> csm;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  const Tails x = load_tails(tot);
+  const int m = static_cast<int>(tot->nM);
+
+  uint32_t key[ITEMS];
+  int32_t val[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int pos = wid * (kWave * ITEMS) + i * kWave + lane;
+    key[i] = (pos < m) ? m_keys[pos] : 0xffffffffu;
+    val[i] = (pos < m) ? m_idx[pos] : -1;
+  }
+  if (m > 0) block_sort_u32<BLOCK, ITEMS, PAIRS>(key, val, buf, ssm);
+  float s[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) s[i] = key_float(key[i]);
+  int cnt = m - tid * ITEMS;
+  cnt = cnt < 0 ? 0 : (cnt > ITEMS ? ITEMS : cnt);
+
+  SolveRec rec;
+  rec.ok = 1;
+  rec.side = 0;
+  double b;
+  if (m == 0) {
+    certify(x, 0.0, static_cast<double>(n_total), k, t, x.pre, x.suf, rec);
+    b = root_above(x, x.suf, k, t);
+  } else {
+    Pre pt;
+    Suf st;
+    b = block_solve<BLOCK, ITEMS>(s, cnt, x.nR, x.pre, x.suf, k, t, csm, &pt, &st);
+    certify(x, static_cast<double>(m), static_cast<double>(n_total), k, t, pt, st, rec);
+  }
+  if constexpr (PAIRS) {
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i)
+      if (i < cnt) idx_sorted[tid * ITEMS + i] = val[i];
+  }
+  if (tid == 0) {
+    rec.b = b;
+    *out = rec;
+  }
+}
+
+hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, int64_t m_len,
+                                bool with_idx, const PartTotals* tot, double k, double t,
+                                int64_t n_total, SolveRec* out, int32_t* m_idx_sorted,
+                                hipStream_t s) {
+  if (m_len > kRowOnChipMax) return hipErrorInvalidValue;
+  if (with_idx)
+    { ProfScope ps_("small_m_solve", s);
+    hipLaunchKernelGGL(small_m_solve_kernel<true>, dim3(1), dim3(1024), 0, s, m_keys, m_idx, tot, k,
+                       t, n_total, out, m_idx_sorted); }
+  else
+    { ProfScope ps_("small_m_solve", s);
+    hipLaunchKernelGGL(small_m_solve_kernel<false>, dim3(1), dim3(1024), 0, s, m_keys, m_idx, tot,
+                       k, t, n_total, out, m_idx_sorted); }
+  return hipGetLastError();
+}
+
+__global__ void write_m_idx_kernel(const int32_t* __restrict__ src, int64_t m, int64_t cap,
+                                   int32_t* __restrict__ out) {
+  int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (; i < cap; i += stride) out[i] = (i < m) ? src[i] : -1;
+}
+
+hipError_t launch_write_m_idx(const int32_t* sorted_idx, int64_t m_len, int64_t m_capacity,
+                              int32_t* out, hipStream_t s) {
+  int64_t blocks = (m_capacity + 255) / 256;
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  { ProfScope ps_("write_m_idx", s);
+  hipLaunchKernelGGL(write_m_idx_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                     sorted_idx, m_len, m_capacity, out); }
+  return hipGetLastError();
+}
+
+}  // namespace lapsum

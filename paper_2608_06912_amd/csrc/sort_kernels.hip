@@ -1,0 +1,264 @@
+// Device-wide stable LSD radix sort of one array into descending float order
+// (the sort step of the full-sort solver, §1/§3, and of the middle band M,
+// Suppl. B).  Four passes of 8-bit digits; each pass is
+//   upsweep    per-tile digit counts (tiles of 4096 keys)          read keys
+//   scan       per digit, exclusive prefix of the counts over tiles
+//   downsweep  stable rank inside the tile (ballot digit matching),
+//              staged through LDS so that each digit run leaves the tile as
+//              a contiguous burst                                  read + write
+// Ties keep their input order (tile order, then position inside the tile),
+// which for the first pass is the original index: the sort is stable.
+#include "block_sort.hpp"
+#include "kernels.hpp"
+
+namespace lapsum {
+
+namespace {
+
+constexpr int TT = kTileThreads;           // 256
+constexpr int TI = kTileItems;             // 16
+constexpr int TW = TT / kWave;             // 4 waves
+constexpr int64_t TILE = kTile;            // 4096
+
+struct PassArgs {
+  const float* src_f;      // pass 0 from floats, else null
+  const uint32_t* src_k;
+  const int32_t* src_v;    // null => values are source positions (mode 1)
+  uint32_t* dst_k;
+  int32_t* dst_v;          // null => keys only
+  int64_t len;
+  const int64_t* len_dev;
+  uint32_t* hist;          // [256][max_tiles]
+  uint32_t* totals;        // [256]
+  int64_t max_tiles;
+  int shift;
+};
+
+__device__ __forceinline__ int64_t eff_len(const PassArgs& a) {
+  if (a.len_dev == nullptr) return a.len;
+  const int64_t d = *a.len_dev;
+  return d < a.len ? (d < 0 ? 0 : d) : a.len;
+}
+
+__device__ __forceinline__ uint32_t load_key(const PassArgs& a, int64_t i) {
+  return a.src_f ? desc_key(a.src_f[i]) : a.src_k[i];
+}
+
+// position of item i of this thread inside the tile (wave-striped)
+__device__ __forceinline__ int tile_pos(int i) {
+  return (threadIdx.x / kWave) * (kWave * TI) + i * kWave + lane_id();
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
+  const int64_t len = eff_len(a);
+  const int64_t ntiles = (len + TILE - 1) / TILE;
+  const int64_t tile = blockIdx.x;
+  if (tile >= ntiles) return;
+  __shared__ uint32_t cnt[256 * TW];
+  const int tid = threadIdx.x;
+  const int wid = tid / kWave;
+  for (int e = tid; e < 256 * TW; e += TT) cnt[e] = 0u;
+  __syncthreads();
+  const int64_t base = tile * TILE;
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const int64_t pos = base + tile_pos(i);
+    const bool valid = pos < len;
+    const uint32_t d = valid ? (load_key(a, pos) >> a.shift) & 255u : 0u;
+    const uint64_t peers = match_digit8(d) & __ballot(valid);
+    if (valid && lanes_below(peers) == 0u) cnt[d * TW + wid] += static_cast<uint32_t>(__popcll(peers));
+  }
+  __syncthreads();
+  uint32_t sum = 0;
+#pragma unroll
+  for (int w = 0; w < TW; ++w) sum += cnt[tid * TW + w];
+  a.hist[static_cast<int64_t>(tid) * a.max_tiles + tile] = sum;
+}
+
+// One block per digit: exclusive prefix of hist[d][0..ntiles) in place.
+__global__ __launch_bounds__(TT) void sort_scan_kernel(PassArgs a) {
+  const int64_t len = eff_len(a);
+  const int64_t ntiles = (len + TILE - 1) / TILE;
+  const int d = blockIdx.x;
+  __shared__ uint32_t wtot[TW];
+  uint32_t* h = a.hist + static_cast<int64_t>(d) * a.max_tiles;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  uint32_t carry = 0;
+  for (int64_t c0 = 0; c0 < ntiles; c0 += 4 * TT) {
+    uint32_t v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t idx = c0 + 4 * tid + q;
+      v[q] = idx < ntiles ? h[idx] : 0u;
+    }
+    const uint32_t sum = v[0] + v[1] + v[2] + v[3];
+    uint32_t incl = sum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t x = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += x;
+    }
+    if (lane == kWave - 1) wtot[wid] = incl;
+    __syncthreads();
+    uint32_t wbase = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < TW; ++w) {
+      if (w < wid) wbase += wtot[w];
+      all += wtot[w];
+    }
+    uint32_t ex = carry + wbase + incl - sum;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t idx = c0 + 4 * tid + q;
+      if (idx < ntiles) h[idx] = ex;
+      ex += v[q];
+    }
+    carry += all;
+    __syncthreads();
+  }
+  if (tid == 0) a.totals[d] = carry;
+}
+
+template <bool PAIRS>
+__global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
+  const int64_t len = eff_len(a);
+  const int64_t ntiles = (len + TILE - 1) / TILE;
+  const int64_t tile = blockIdx.x;
+  if (tile >= ntiles) return;
+  __shared__ uint32_t cnt[256 * TW];
+  __shared__ uint32_t wave_tot[TW];
+  __shared__ uint32_t gbase[256];    // first output position of each digit for this tile
+  __shared__ uint32_t dstart[256];   // first tile-local position of each digit
+  __shared__ uint32_t buf[TILE];
+  __shared__ uint8_t dg[PAIRS ? TILE : 1];   // digit of each tile-local position
+  const int tid = threadIdx.x;
+  const int wid = tid / kWave;
+  const int lane = lane_id();
+
+  // digit base over the whole array: exclusive prefix of totals over digits
+  {
+    const uint32_t tot = a.totals[tid];
+    uint32_t incl = tot;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t x = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += x;
+    }
+    if (lane == kWave - 1) wave_tot[wid] = incl;
+    __syncthreads();
+    uint32_t wbase = 0;
+#pragma unroll
+    for (int w = 0; w < TW; ++w)
+      if (w < wid) wbase += wave_tot[w];
+    gbase[tid] = wbase + incl - tot + a.hist[static_cast<int64_t>(tid) * a.max_tiles + tile];
+  }
+  for (int e = tid; e < 256 * TW; e += TT) cnt[e] = 0u;
+  __syncthreads();
+
+  const int64_t base = tile * TILE;
+  uint32_t key[TI];
+  int32_t val[TI];
+  uint32_t pos[TI];
+  uint64_t validm[TI];
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const int64_t gp = base + tile_pos(i);
+    const bool valid = gp < len;
+    key[i] = valid ? load_key(a, gp) : 0xffffffffu;
+    if constexpr (PAIRS) val[i] = valid ? (a.src_v ? a.src_v[gp] : static_cast<int32_t>(gp)) : -1;
+    validm[i] = __ballot(valid);
+  }
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const uint32_t d = (key[i] >> a.shift) & 255u;
+    const uint64_t peers = match_digit8(d) & validm[i];
+    const uint32_t below = lanes_below(peers);
+    uint32_t* slot = &cnt[d * TW + wid];
+    const uint32_t c = *slot;
+    pos[i] = c + below;
+    const bool valid = (validm[i] >> lane) & 1ull;
+    if (valid && below == 0u) *slot = c + static_cast<uint32_t>(__popcll(peers));
+  }
+  __syncthreads();
+  block_excl_scan_u32x4<TT>(cnt, wave_tot);
+  dstart[tid] = cnt[tid * TW];
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    pos[i] += cnt[((key[i] >> a.shift) & 255u) * TW + wid];
+    if ((validm[i] >> lane) & 1ull) buf[pos[i]] = key[i];
+  }
+  __syncthreads();
+  const int nvalid = static_cast<int>((len - base) < TILE ? (len - base) : TILE);
+  for (int q = tid; q < nvalid; q += TT) {
+    const uint32_t k = buf[q];
+    const uint32_t d = (k >> a.shift) & 255u;
+    a.dst_k[gbase[d] + (q - dstart[d])] = k;
+    if constexpr (PAIRS) dg[q] = static_cast<uint8_t>(d);
+  }
+  if constexpr (PAIRS) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+      if ((validm[i] >> lane) & 1ull) buf[pos[i]] = static_cast<uint32_t>(val[i]);
+    __syncthreads();
+    for (int q = tid; q < nvalid; q += TT) {
+      const uint32_t d = dg[q];
+      a.dst_v[gbase[d] + (q - dstart[d])] = static_cast<int32_t>(buf[q]);
+    }
+  }
+}
+
+size_t sort_hist_words(int64_t len) {
+  const int64_t tiles = (len + TILE - 1) / TILE;
+  return static_cast<size_t>(256) * static_cast<size_t>(tiles < 1 ? 1 : tiles);
+}
+
+hipError_t launch_sort(const float* src_f, const uint32_t* src_k, const int32_t* src_v,
+                       bool with_vals, int64_t len, const int64_t* len_dev, SortBuffers& sb,
+                       int* out_buf, hipStream_t s) {
+  const int64_t tiles = (len + TILE - 1) / TILE;
+  if (tiles > sb.max_tiles) return hipErrorInvalidValue;
+  const unsigned grid = static_cast<unsigned>(tiles < 1 ? 1 : tiles);
+  int cur = -1;
+  for (int pass = 0; pass < 4; ++pass) {
+    PassArgs a{};
+    a.len = len;
+    a.len_dev = len_dev;
+    a.hist = sb.hist;
+    a.totals = sb.totals;
+    a.max_tiles = sb.max_tiles;
+    a.shift = 8 * pass;
+    if (pass == 0) {
+      a.src_f = src_f;
+      a.src_k = src_k;
+      a.src_v = src_v;
+    } else {
+      a.src_k = sb.keys[cur];
+      a.src_v = sb.vals[cur];
+    }
+    const int nxt = (cur == 0) ? 1 : 0;
+    a.dst_k = sb.keys[nxt];
+    a.dst_v = with_vals ? sb.vals[nxt] : nullptr;
+    { ProfScope ps_("sort_upsweep", s);
+    hipLaunchKernelGGL(sort_upsweep_kernel, dim3(grid), dim3(TT), 0, s, a); }
+    { ProfScope ps_("sort_scan", s);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(256), dim3(TT), 0, s, a); }
+    if (with_vals)
+      { ProfScope ps_("sort_downsweep", s);
+      hipLaunchKernelGGL((sort_downsweep_kernel<true>), dim3(grid), dim3(TT), 0, s, a); }
+    else
+      { ProfScope ps_("sort_downsweep", s);
+      hipLaunchKernelGGL((sort_downsweep_kernel<false>), dim3(grid), dim3(TT), 0, s, a); }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    cur = nxt;
+  }
+  *out_buf = cur;
+  return hipSuccess;
+}
+
+}  // namespace lapsum

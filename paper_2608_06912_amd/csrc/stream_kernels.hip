@@ -1,0 +1,225 @@
+// Streaming passes over one long row: the Laplace-CDF emit (the fused CDF
+// evaluation of Suppl. D) and the two passes of the Eq. (5) backward.
+//
+// All three are HBM-bound.  Algorithmic bytes per score:
+//   emit        read r, write p                          8 B
+//   vjp reduce  read p, read g where f != 0              4 B + 4 B x (active share)
+//   vjp emit    read p, read g where f != 0, write grad  8 B + 4 B x (active share)
+// f = min(p, 1 - p) is exactly zero for scores whose p rounded to 0 or 1 in
+// float32; their g is never read.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace lapsum {
+
+namespace {
+constexpr int kStreamThreads = 256;
+constexpr int kStreamVec = 4;   // float4 per thread per block
+constexpr int64_t kStreamTile = static_cast<int64_t>(kStreamThreads) * kStreamVec * 4;   // scores
+}  // namespace
+
+__global__ void fill_u32_kernel(uint32_t* __restrict__ dst, int64_t count, uint32_t value) {
+  int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (; i < count; i += stride) dst[i] = value;
+}
+
+hipError_t launch_fill_u32(uint32_t* dst, int64_t count, uint32_t value, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  int64_t blocks = (count + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  { ProfScope ps_("fill_u32", s);
+  hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, dst,
+                     count, value); }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ emit ---
+__global__ __launch_bounds__(kStreamThreads) void emit_kernel(const float* __restrict__ r,
+                                                              int64_t n,
+                                                              const double* __restrict__ b_dev,
+                                                              double inv_t,
+                                                              float* __restrict__ p) {
+  const double b = *b_dev;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kStreamTile;
+  const int tid = threadIdx.x;
+  const bool vec = ((reinterpret_cast<uintptr_t>(r) | reinterpret_cast<uintptr_t>(p)) & 15) == 0;
+  if (vec && base + kStreamTile <= n) {
+    const float4* r4 = reinterpret_cast<const float4*>(r + base);
+    float4* p4 = reinterpret_cast<float4*>(p + base);
+    float4 v[kStreamVec];
+#pragma unroll
+    for (int j = 0; j < kStreamVec; ++j) v[j] = r4[j * kStreamThreads + tid];
+#pragma unroll
+    for (int j = 0; j < kStreamVec; ++j) {
+      float4 o;
+      o.x = laplace_p(v[j].x, b, inv_t);
+      o.y = laplace_p(v[j].y, b, inv_t);
+      o.z = laplace_p(v[j].z, b, inv_t);
+      o.w = laplace_p(v[j].w, b, inv_t);
+      p4[j * kStreamThreads + tid] = o;
+    }
+  } else {
+    for (int64_t i = base + tid; i < n; i += kStreamThreads) p[i] = laplace_p(r[i], b, inv_t);
+  }
+}
+
+hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t, float* p,
+                       hipStream_t s) {
+  const int64_t blocks = (n + kStreamTile - 1) / kStreamTile;
+  { ProfScope ps_("emit", s);
+  hipLaunchKernelGGL(emit_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kStreamThreads), 0, s,
+                     r, n, b_dev, 1.0 / t, p); }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ vjp reduce ---
+int vjp_reduce_blocks(int64_t n) {
+  int64_t b = (n + kStreamTile - 1) / kStreamTile;
+  return static_cast<int>(b < 1024 ? (b < 1 ? 1 : b) : 1024);
+}
+
+// Block-level sums of f = min(p, 1-p) and f g over a contiguous chunk,
+// float32 within one float4, float64 across float4s, then a fixed-order
+// reduction (butterfly within a wave, waves in order).
+__global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float* __restrict__ g,
+                                                                    const float* __restrict__ p,
+                                                                    int64_t n,
+                                                                    double* __restrict__ partials) {
+  __shared__ double red[2][kStreamThreads / kWave];
+  const int tid = threadIdx.x;
+  const bool vec = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(p)) & 15) == 0;
+  const int64_t n4 = vec ? n / 4 : 0;
+  const int64_t per = (n4 + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = static_cast<int64_t>(blockIdx.x) * per;
+  const int64_t hi = (lo + per < n4) ? lo + per : n4;
+  const float4* p4 = reinterpret_cast<const float4*>(p);
+  const float4* g4 = reinterpret_cast<const float4*>(g);
+  double F = 0.0, G = 0.0;
+  for (int64_t i = lo + tid; i < hi; i += kStreamThreads) {
+    const float4 pv = p4[i];
+    const float fx = fminf(pv.x, 1.0f - pv.x), fy = fminf(pv.y, 1.0f - pv.y);
+    const float fz = fminf(pv.z, 1.0f - pv.z), fw = fminf(pv.w, 1.0f - pv.w);
+    const float fs = (fx + fy) + (fz + fw);
+    if (fs != 0.0f) {
+      const float4 gv = g4[i];
+      F += static_cast<double>(fs);
+      G += static_cast<double>((fx * gv.x + fy * gv.y) + (fz * gv.z + fw * gv.w));
+    }
+  }
+  if (blockIdx.x == gridDim.x - 1) {   // scalar tail
+    for (int64_t i = n4 * 4 + tid; i < n; i += kStreamThreads) {
+      const float pp = p[i];
+      const float f = fminf(pp, 1.0f - pp);
+      if (f != 0.0f) {
+        F += static_cast<double>(f);
+        G += static_cast<double>(f) * static_cast<double>(g[i]);
+      }
+    }
+  }
+  F = wave_sum(F);
+  G = wave_sum(G);
+  const int wid = tid / kWave;
+  if (lane_id() == 0) {
+    red[0][wid] = F;
+    red[1][wid] = G;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double f = 0.0, gg = 0.0;
+#pragma unroll
+    for (int w = 0; w < kStreamThreads / kWave; ++w) {
+      f += red[0][w];
+      gg += red[1][w];
+    }
+    partials[2 * blockIdx.x] = f;
+    partials[2 * blockIdx.x + 1] = gg;
+  }
+}
+
+hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
+                             int nblocks, hipStream_t s) {
+  { ProfScope ps_("vjp_reduce", s);
+  hipLaunchKernelGGL(vjp_reduce_kernel, dim3(nblocks), dim3(kStreamThreads), 0, s, g, p, n,
+                     partials); }
+  return hipGetLastError();
+}
+
+// -------------------------------------------------------------- vjp emit ---
+// Every block first re-reduces the per-block partials in the same fixed
+// order, so each block holds the identical (sum f, sum f g).
+__global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* __restrict__ g,
+                                                                  const float* __restrict__ p,
+                                                                  int64_t n,
+                                                                  const double* __restrict__ partials,
+                                                                  int nparts, double inv_t,
+                                                                  float* __restrict__ grad) {
+  __shared__ double red[2][kStreamThreads / kWave];
+  const int tid = threadIdx.x;
+  double F = 0.0, G = 0.0;
+  for (int j = tid; j < nparts; j += kStreamThreads) {
+    F += partials[2 * j];
+    G += partials[2 * j + 1];
+  }
+  F = wave_sum(F);
+  G = wave_sum(G);
+  const int wid = tid / kWave;
+  if (lane_id() == 0) {
+    red[0][wid] = F;
+    red[1][wid] = G;
+  }
+  __syncthreads();
+  F = 0.0;
+  G = 0.0;
+#pragma unroll
+  for (int w = 0; w < kStreamThreads / kWave; ++w) {
+    F += red[0][w];
+    G += red[1][w];
+  }
+  // grad_r = (f/t)(g - <g,q>), q = f / sum f; zero when sum f == 0
+  const float coef = static_cast<float>((F > 0.0) ? G / F : 0.0);
+  const float scale = static_cast<float>((F > 0.0) ? inv_t : 0.0);
+
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kStreamTile;
+  const bool vec =
+      ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(grad)) & 15) == 0;
+  if (vec && base + kStreamTile <= n) {
+    const float4* p4 = reinterpret_cast<const float4*>(p + base);
+    const float4* g4 = reinterpret_cast<const float4*>(g + base);
+    float4* o4 = reinterpret_cast<float4*>(grad + base);
+    float4 pv[kStreamVec];
+#pragma unroll
+    for (int j = 0; j < kStreamVec; ++j) pv[j] = p4[j * kStreamThreads + tid];
+#pragma unroll
+    for (int j = 0; j < kStreamVec; ++j) {
+      const float fx = fminf(pv[j].x, 1.0f - pv[j].x), fy = fminf(pv[j].y, 1.0f - pv[j].y);
+      const float fz = fminf(pv[j].z, 1.0f - pv[j].z), fw = fminf(pv[j].w, 1.0f - pv[j].w);
+      float4 o = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if ((fx + fy) + (fz + fw) != 0.0f) {
+        const float4 gv = g4[j * kStreamThreads + tid];
+        o.x = fx * scale * (gv.x - coef);
+        o.y = fy * scale * (gv.y - coef);
+        o.z = fz * scale * (gv.z - coef);
+        o.w = fw * scale * (gv.w - coef);
+      }
+      o4[j * kStreamThreads + tid] = o;
+    }
+  } else {
+    for (int64_t i = base + tid; i < n; i += kStreamThreads) {
+      const float pp = p[i];
+      const float f = fminf(pp, 1.0f - pp);
+      grad[i] = (f != 0.0f) ? f * scale * (g[i] - coef) : 0.0f;
+    }
+  }
+}
+
+hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* partials,
+                           int nblocks, double t, float* grad, hipStream_t s) {
+  const int64_t blocks = (n + kStreamTile - 1) / kStreamTile;
+  { ProfScope ps_("vjp_emit", s);
+  hipLaunchKernelGGL(vjp_emit_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kStreamThreads), 0,
+                     s, g, p, n, partials, nblocks, 1.0 / t, grad); }
+  return hipGetLastError();
+}
+
+}  // namespace lapsum

@@ -1,0 +1,111 @@
+"""The C-ABI library on the CPU: it loads, exports every entry point the
+header declares, and its host-only paths (status strings, workspace sizes,
+argument validation, which return before any HIP call) behave as documented.
+No compute call is made here."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_06912_amd as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lapsum.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH), reason="library not built")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lapsum_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for want in ("lapsum_forward", "lapsum_backward", "lapsum_forward_bracketed",
+                 "lapsum_forward_workspace_size", "lapsum_backward_workspace_size",
+                 "lapsum_forward_bracketed_workspace_size", "lapsum_status_string"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    assert L.lapsum_status_string(0) == "ok"
+    assert "invalid" in L.lapsum_status_string(1)
+    assert "workspace" in L.lapsum_status_string(2)
+    assert "HIP" in L.lapsum_status_string(3)
+    assert "gfx950" in L.lapsum_status_string(4)
+    assert "unknown" in L.lapsum_status_string(99)
+
+
+def test_workspace_sizes():
+    # rows that fit on chip need no workspace
+    assert L.lapsum_forward_workspace_size(256, 32768) == 0
+    assert L.lapsum_backward_workspace_size(256, 32768) == 0
+    a = L.lapsum_forward_workspace_size(1, 10**6, False)
+    b = L.lapsum_forward_workspace_size(1, 10**6, True)
+    assert a >= 2 * 4 * 10**6 and b >= a + 2 * 4 * 10**6
+    assert a % 256 == 0 and b % 256 == 0
+    assert L.lapsum_backward_workspace_size(1, 10**7) > 0
+    w1 = L.lapsum_forward_bracketed_workspace_size(1, 10**7, 46416, 1 << 16, False)
+    w2 = L.lapsum_forward_bracketed_workspace_size(1, 10**7, 46416, 1 << 20, False)
+    w3 = L.lapsum_forward_bracketed_workspace_size(1, 10**7, 46416, 1 << 20, True)
+    assert 0 < w1 < w2 < w3
+    # capacity beyond n is clamped
+    assert (L.lapsum_forward_bracketed_workspace_size(1, 1000, 100, 10**6, False)
+            == L.lapsum_forward_bracketed_workspace_size(1, 1000, 100, 1000, False))
+
+
+def _fwd(lib, scores=1, batch=1, n=8, k=2.0, alpha=-1.0, p=1, b=1):
+    v = ctypes.c_void_p
+    return lib.lapsum_forward(v(scores), batch, n, k, alpha, v(p), v(b), v(0), v(0), 0, v(0))
+
+
+@pytest.mark.parametrize("kw", [
+    dict(scores=0), dict(p=0), dict(b=0), dict(batch=0), dict(n=0), dict(n=2**31),
+    dict(k=0.0), dict(k=8.0), dict(k=-1.0), dict(k=float("nan")), dict(k=float("inf")),
+    dict(alpha=0.0), dict(alpha=1.0), dict(alpha=float("-inf")), dict(alpha=float("nan")),
+])
+def test_forward_rejects_invalid_arguments(kw):
+    assert _fwd(L.load(), **kw) == 1
+
+
+def test_forward_rejects_missing_workspace():
+    lib = L.load()
+    v = ctypes.c_void_p
+    # a long row needs a workspace: null, too small, misaligned
+    assert lib.lapsum_forward(v(1), 1, 10**6, 5.0, -1.0, v(1), v(1), v(0), v(0), 0, v(0)) == 2
+    need = L.lapsum_forward_workspace_size(1, 10**6)
+    assert lib.lapsum_forward(v(1), 1, 10**6, 5.0, -1.0, v(1), v(1), v(0), v(256), need - 1, v(0)) == 2
+    assert lib.lapsum_forward(v(1), 1, 10**6, 5.0, -1.0, v(1), v(1), v(0), v(128), need, v(0)) == 2
+
+
+def test_backward_rejects_invalid_arguments():
+    lib = L.load()
+    v = ctypes.c_void_p
+    assert lib.lapsum_backward(v(0), v(1), v(0), 1, 8, -1.0, v(1), v(0), 0, v(0)) == 1
+    assert lib.lapsum_backward(v(1), v(1), v(0), 1, 8, 0.5, v(1), v(0), 0, v(0)) == 1
+    assert lib.lapsum_backward(v(1), v(1), v(0), 0, 8, -1.0, v(1), v(0), 0, v(0)) == 1
+    assert lib.lapsum_backward(v(1), v(1), v(0), 1, 10**6, -1.0, v(1), v(0), 0, v(0)) == 2
+
+
+@pytest.mark.parametrize("kw", [
+    dict(noise=0), dict(K=1), dict(K=1001), dict(z=0.0), dict(z=float("nan")),
+    dict(m_capacity=0), dict(flags=2), dict(k=1000.0),
+])
+def test_bracketed_rejects_invalid_arguments(kw):
+    lib = L.load()
+    v = ctypes.c_void_p
+    a = dict(noise=1, K=100, z=5.16, m_capacity=64, flags=0, k=10.0)
+    a.update(kw)
+    st = lib.lapsum_forward_bracketed(v(1), 1, 1000, a["k"], -1.0, a["K"], a["z"], v(a["noise"]),
+                                      a["m_capacity"], a["flags"], v(1), v(1), v(0), v(0), v(0),
+                                      0, v(0))
+    assert st == 1

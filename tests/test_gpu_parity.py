@@ -1,0 +1,297 @@
+"""HIP path vs the float64 oracle, element by element (GPU only).
+
+Tolerances (applied in float32):
+  p       max |p - p_oracle| <= 1e-5
+  sum p   |sum p - k| <= 1e-6 max(1, k) + 1e-3        (sum taken in float64)
+  b       |b - b_oracle| <= 2e-6 t   (keeps the p error below 1e-6)
+  grad_r  ||grad - grad_oracle||_2 / ||grad_oracle||_2 <= 1e-4
+  permutation, bracket endpoints, set sizes and M membership: bit-exact
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle.lapsum_oracle as O
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+P_TOL = 1e-5
+G_TOL = 1e-4
+
+
+def _t(x):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def _np(x):
+    return x.detach().cpu().numpy()
+
+
+def sum_tol(k):
+    return 1e-6 * max(1.0, k) + 1e-3
+
+
+def check_row(r32, k, alpha, p_gpu, b_gpu, label=""):
+    t = -alpha
+    b_ref = O.solve_sorted_scan(r32, k, alpha)
+    assert abs(b_gpu - b_ref) <= 2e-6 * t, (label, b_gpu, b_ref)
+    p_ref = O.probs(r32, b_ref, alpha)
+    err = float(np.max(np.abs(p_gpu.astype(np.float64) - p_ref)))
+    assert err <= P_TOL, (label, err)
+    assert O.budget_error(p_gpu, k) <= sum_tol(k), (label, O.budget_error(p_gpu, k))
+    return b_ref
+
+
+def grad_rel(g_gpu, g_ref):
+    num = np.linalg.norm(g_gpu.astype(np.float64) - g_ref)
+    den = np.linalg.norm(g_ref)
+    return num / den if den > 0 else num
+
+
+# ------------------------------------------------------------ on-chip rows --
+ROW_CASES = [
+    (1, "normal", 0.3, -0.5), (2, "normal", 1.5, -0.1), (3, "levels16", 1.0, -1.0),
+    (63, "normal", 5.0, -0.2), (64, "cauchy", 32.0, -1.0), (65, "normal", 64.9, -0.01),
+    (255, "clusters3", 100.0, -0.3), (256, "normal", 0.01, -0.05), (257, "laplace_abs", 200.0, -2.0),
+    (1000, "normal", 62.5, -1.0), (2048, "levels16", 128.0, -0.25), (2049, "normal", 7.0, -0.001),
+    (4096, "normal", 16.0, -0.5), (5000, "student2", 4999.5, -0.1), (16384, "normal", 1024.0, -1.0),
+    (20000, "lognormal", 3.0, -0.02), (32768, "normal", 256.0, -0.1), (32768, "constant", 100.0, -1.0),
+]
+
+
+@pytest.mark.parametrize("n,dist,k,alpha", ROW_CASES)
+def test_row_forward_matches_oracle(lib, n, dist, k, alpha):
+    r = W.random_case(n, n, dist=dist, ties=0.05)[0]
+    p, b, perm = lib.lapsum_forward(_t(r), k, alpha, perm=True)
+    check_row(r, k, alpha, _np(p), float(_np(b)[0]), f"n={n} {dist}")
+    assert np.array_equal(_np(perm), O.desc_order(r)), "permutation"
+
+
+def test_row_forward_single4k(lib):
+    w = W.get("single4k")
+    r = W.scores("single4k")
+    p, b, perm = lib.lapsum_forward(_t(r), w.k, w.alpha, perm=True)
+    check_row(r[0], w.k, w.alpha, _np(p)[0], float(_np(b)[0]), "single4k")
+    assert np.array_equal(_np(perm)[0], O.desc_order(r[0]))
+
+
+def test_row_forward_batch256_with_duplicates(lib):
+    w = W.get("batch256")
+    r = W.scores("batch256")
+    p, b, perm = lib.lapsum_forward(_t(r), w.k, w.alpha, perm=True)
+    p, b, perm = _np(p), _np(b), _np(perm)
+    for row in range(w.batch):
+        check_row(r[row], w.k, w.alpha, p[row], float(b[row]), f"row {row}")
+        assert np.array_equal(perm[row], O.desc_order(r[row])), f"perm row {row}"
+
+
+@pytest.mark.parametrize("n,alpha", [(1, -1.0), (100, -0.5), (4096, -0.5), (5000, -0.1),
+                                     (32768, -0.1), (32768, -0.002)])
+def test_row_backward_matches_oracle(lib, n, alpha):
+    rg = np.random.default_rng([7, n])
+    r = rg.standard_normal((3, n)).astype(np.float32)
+    g = rg.standard_normal((3, n)).astype(np.float32)
+    k = max(0.5, n / 16.0) if n > 1 else 0.25
+    p, b = lib.lapsum_forward(_t(r), k, alpha)
+    grad = _np(lib.lapsum_backward(_t(g), p, b, alpha))
+    for row in range(3):
+        b_ref = O.solve_sorted_scan(r[row], k, alpha)
+        ref = O.vjp(r[row], b_ref, alpha, g[row])
+        assert grad_rel(grad[row], ref) <= G_TOL, (n, row, grad_rel(grad[row], ref))
+
+
+def test_forward_is_deterministic(lib):
+    r = W.random_case(3, 32768, dist="normal", ties=0.01, batch=4)
+    x = _t(r)
+    p1, b1 = lib.lapsum_forward(x, 100.0, -0.1)
+    p2, b2 = lib.lapsum_forward(x, 100.0, -0.1)
+    assert np.array_equal(_np(p1), _np(p2)) and np.array_equal(_np(b1), _np(b2))
+
+
+# ------------------------------------------------------- device-wide rows --
+@pytest.mark.parametrize("n,dist,k,alpha", [
+    (32769, "normal", 100.0, -0.1), (100003, "levels16", 5000.0, -1.0),
+    (250000, "laplace_abs", 3.0, -0.01), (262144, "normal", 131072.0, -0.5),
+])
+def test_devicewide_forward_matches_oracle(lib, n, dist, k, alpha):
+    r = W.random_case(n % 97, n, dist=dist, ties=0.02)[0]
+    p, b, perm = lib.lapsum_forward(_t(r), k, alpha, perm=True)
+    check_row(r, k, alpha, _np(p), float(_np(b)[0]), f"n={n}")
+    assert np.array_equal(_np(perm), O.desc_order(r))
+
+
+def test_devicewide_n1e6(lib):
+    w = W.get("n1e6")
+    r = W.scores("n1e6")
+    x = _t(r)
+    p, b, perm = lib.lapsum_forward(x, w.k, w.alpha, perm=True)
+    check_row(r[0], w.k, w.alpha, _np(p)[0], float(_np(b)[0]), "n1e6")
+    assert np.array_equal(_np(perm)[0], O.desc_order(r[0]))
+    p2, b2 = lib.lapsum_forward(x, w.k, w.alpha)            # keys-only sort
+    assert float(_np(b2)[0]) == float(_np(b)[0])
+    g = W.upstream_grad("n1e6")
+    grad = _np(lib.lapsum_backward(_t(g), p2, b2, w.alpha))[0]
+    ref = O.vjp(r[0], O.solve_sorted_scan(r[0], w.k, w.alpha), w.alpha, g[0])
+    assert grad_rel(grad, ref) <= G_TOL
+
+
+@pytest.mark.parametrize("n,alpha", [(40000, -0.1), (1_000_003, -0.05)])
+def test_devicewide_backward(lib, n, alpha):
+    rg = np.random.default_rng([9, n])
+    r = rg.standard_normal((1, n)).astype(np.float32)
+    g = rg.standard_normal((1, n)).astype(np.float32)
+    k = n / 100.0
+    p, b = lib.lapsum_forward(_t(r), k, alpha)
+    grad = _np(lib.lapsum_backward(_t(g), p, b, alpha))[0]
+    ref = O.vjp(r[0], O.solve_sorted_scan(r[0], k, alpha), alpha, g[0])
+    assert grad_rel(grad, ref) <= G_TOL
+
+
+# -------------------------------------------------------------- bracketed --
+def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label=""):
+    import torch
+    p, b, infos, midx = lib.lapsum_forward_bracketed(_t(r32[None, :]), k, alpha, _t(noise), z=z,
+                                                     m_capacity=m_capacity, m_idx=True)
+    info = infos[0]
+    po, bo, oinfo, oms = O.bracketed_forward(r32, k, alpha, noise, z=z,
+                                             m_capacity=m_capacity or len(r32))
+    assert (info["j"], info["l"]) == (oinfo.j, oinfo.l), (label, info, oinfo)
+    assert (info["attempts"], info["fell_back"], info["m_overflow"]) == \
+        (oinfo.attempts, oinfo.fell_back, oinfo.m_overflow), (label, info, oinfo)
+    assert np.float32(info["a_L"]) == np.float32(oinfo.a_L) and np.float32(info["a_R"]) == np.float32(oinfo.a_R)
+    assert (info["n_L"], info["n_M"], info["n_R"]) == (oinfo.n_L, oinfo.n_M, oinfo.n_R)
+    # The tail sums add float32 exponentials in float64: each term is
+    # e^{-u} with u formed in float32 (error <= u e^{-u} 6e-8 <= 2.2e-8
+    # absolute) and rounded once more (6e-8 relative), so a sum is within
+    # 1e-6 relative.  LapSum(a_L), LapSum(a_R) carry those sums with weight
+    # 1/2 plus the middle set's terms (computed the same way).
+    for f in ("T_L", "T_R"):
+        ref = getattr(oinfo, f)
+        assert abs(info[f] - ref) <= 1e-6 * ref + 1e-30, (label, f, info[f], ref)
+    scale = 1.0 + oinfo.T_L + oinfo.T_R + oinfo.n_M
+    for f in ("lap_aL", "lap_aR"):
+        ref = getattr(oinfo, f)
+        if oinfo.m_overflow:
+            assert math.isnan(info[f]) and math.isnan(ref)
+        else:
+            assert abs(info[f] - ref) <= 1e-6 * scale, (label, f, info[f], ref)
+    t = -alpha
+    b_gpu = float(_np(b)[0])
+    assert abs(b_gpu - bo) <= 2e-6 * t, (label, b_gpu, bo)
+    m = _np(midx)[0]
+    if not oinfo.fell_back:
+        nm = oinfo.n_M
+        assert np.array_equal(m[:nm], oms), label
+        assert np.all(m[nm:] == -1)
+    else:
+        assert np.all(m == -1)
+    return _np(p)[0], b_gpu, bo, info
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_bracketed_small_matches_oracle(lib, case):
+    dists = ["normal", "student2", "lognormal", "cauchy", "clusters3", "levels16"]
+    n = 200_000
+    r = W.random_case(case, n, dist=dists[case])[0]
+    k, alpha, K = n / 16.0, -1.0, W.default_sample_size(n)
+    noise = W.laplace_noise([77, case], K, 1.0)
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=dists[case])
+    p_ref = O.probs(r, bo, alpha)
+    assert np.max(np.abs(p.astype(np.float64) - p_ref)) <= P_TOL
+    assert O.budget_error(p, k) <= sum_tol(k)
+
+
+@pytest.mark.parametrize("shift", [3.0, -3.0, 30.0])
+def test_bracketed_forced_widening_and_fallback(lib, shift):
+    n, k, alpha, K = 20000, 1250.0, -0.5, 737
+    r = W.random_case(4, n, dist="normal")[0]
+    noise = W.laplace_noise([56], K, 0.5) + np.float32(shift)
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=f"shift {shift}")
+    assert info["attempts"] == 3
+
+
+def test_bracketed_overflow_and_flag(lib):
+    n, k, alpha, K = 20000, 1250.0, -0.5, 737
+    r = W.random_case(4, n, dist="normal")[0]
+    noise = W.laplace_noise([56], K, 0.5)
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, m_capacity=10, label="overflow")
+    assert info["m_overflow"] == 1 and info["fell_back"] == 1
+    p2, b2, infos, _ = lib.lapsum_forward_bracketed(_t(r[None, :]), k, alpha, _t(noise),
+                                                    flags=lib.LAPSUM_FLAG_FULL_SORT)
+    assert infos[0]["fell_back"] == 1 and infos[0]["attempts"] == 0
+    assert abs(float(_np(b2)[0]) - bo) <= 2e-6 * 0.5
+
+
+def test_bracketed_large_middle_set(lib):
+    # |M| above the on-chip limit: the middle band goes through the
+    # device-wide sort
+    n = 3_000_000
+    r = W.random_case(11, n, dist="normal", ties=0.01)[0]
+    k, alpha = n / 2.0, -0.3
+    K = 2000
+    noise = W.laplace_noise([78], K, 0.3)
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label="large M")
+    assert info["n_M"] > 32768 and not info["fell_back"]
+    idx = np.random.default_rng(0).integers(0, n, 20000)
+    assert np.max(np.abs(p[idx].astype(np.float64) - O.probs(r[idx], bo, alpha))) <= P_TOL
+
+
+# ----------------------------------------------- the named workloads, full size
+def _sampled_p_check(p_gpu, r, b_ref, alpha, count=200000, seed=0):
+    idx = np.random.default_rng(seed).integers(0, r.size, count)
+    err = np.max(np.abs(p_gpu[idx].astype(np.float64) - O.probs(r[idx], b_ref, alpha)))
+    assert err <= P_TOL, err
+
+
+@pytest.mark.timeout(600)
+def test_workload_n1e7_full_sort(lib):
+    w = W.get("n1e7")
+    r = W.scores("n1e7")
+    x = _t(r)
+    p, b = lib.lapsum_forward(x, w.k, w.alpha)
+    b_ref = O.solve_sorted_scan(r[0], w.k, w.alpha)
+    assert O.certify_root(r[0], w.k, w.alpha, b_ref, 1e-7 * w.t)
+    bg = float(_np(b)[0])
+    assert abs(bg - b_ref) <= 2e-6 * w.t, (bg, b_ref)
+    pg = _np(p)[0]
+    _sampled_p_check(pg, r[0], b_ref, w.alpha)
+    assert O.budget_error(pg, w.k) <= sum_tol(w.k)
+    g = W.upstream_grad("n1e7")
+    grad = _np(lib.lapsum_backward(_t(g), p, b, w.alpha))[0]
+    assert grad_rel(grad, O.vjp(r[0], b_ref, w.alpha, g[0])) <= G_TOL
+
+
+@pytest.mark.timeout(600)
+def test_workload_n1e7_bracketed(lib):
+    w = W.get("n1e7")
+    r = W.scores("n1e7")
+    noise = W.bracket_noise("n1e7")
+    p, bg, bo, info = _check_bracketed(lib, r[0], w.k, w.alpha, noise, z=w.z, label="n1e7")
+    assert O.certify_root(r[0], w.k, w.alpha, bo, 1e-7 * w.t)
+    assert info["attempts"] == 1 and not info["fell_back"]
+    _sampled_p_check(p, r[0], bo, w.alpha)
+    assert O.budget_error(p, w.k) <= sum_tol(w.k)
+
+
+@pytest.mark.timeout(900)
+def test_workload_n1e8_bracketed(lib):
+    """The extreme-scale workload at full size, in the configuration the
+    benchmark times: b, the bracket, M and sampled p against the oracle's
+    bracketed model (itself certified against the plain sum), sum p over
+    all 1e8 outputs, and the backward against Eq. (5)."""
+    import torch
+    w = W.get("n1e8")
+    r = W.scores("n1e8")
+    noise = W.bracket_noise("n1e8")
+    p, bg, bo, info = _check_bracketed(lib, r[0], w.k, w.alpha, noise, z=w.z, label="n1e8")
+    assert O.certify_root(r[0], w.k, w.alpha, bo, 1e-7 * w.t)
+    _sampled_p_check(p, r[0], bo, w.alpha)
+    assert O.budget_error(p, w.k) <= sum_tol(w.k)
+    g = W.upstream_grad("n1e8")
+    pt = _t(p[None, :])
+    bt = torch.tensor([bg], dtype=torch.float64, device="cuda")
+    grad = _np(lib.lapsum_backward(_t(g), pt, bt, w.alpha))[0]
+    assert grad_rel(grad, O.vjp(r[0], bo, w.alpha, g[0])) <= G_TOL
