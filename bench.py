@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=20_000_000)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 4e8-byte device copy (outside the timed region) so a "
+                         "counter profile can calibrate its byte counters")
     return ap.parse_args()
 
 
@@ -122,6 +125,10 @@ def main():
         L.lapsum_backward(g, p, b, w.alpha, workspace=ws_b, out=grad)
         return p, b, infos
 
+    if args.copy_probe:
+        for _ in range(3):
+            grad.copy_(r)
+        torch.cuda.synchronize()
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
         p, b, infos = step()

@@ -27,7 +27,6 @@ constexpr int kSampleThreads = 256;
 constexpr int kSelThreads = 1024;
 constexpr int PT = kPartThreads;               // 256
 constexpr int PW = PT / kWave;                 // 4 waves
-constexpr int kWaveStage = kPartStageCap / PW; // 512 M entries staged per wave
 
 }  // namespace
 
@@ -100,60 +99,111 @@ __device__ void find_bin(const uint32_t* h, int nb, uint32_t rank, uint32_t* wsu
 
 }  // namespace
 
+namespace {
+constexpr int kCand = 4096;   // candidates per target kept in LDS
+
+// Histogram (into h, nb bins) of (key >> lo) & mask over the keys whose
+// bits above `hi` equal `prefix`.
+__device__ void prefix_hist(const uint32_t* keys, int64_t count, int hi, uint32_t prefix, int lo,
+                            uint32_t mask, int nb, uint32_t* h) {
+  for (int e = threadIdx.x; e < nb; e += kSelThreads) h[e] = 0u;
+  __syncthreads();
+  for (int64_t i = threadIdx.x; i < count; i += kSelThreads) {
+    const uint32_t key = keys[i];
+    if ((key >> hi) == prefix) atomicAdd(&h[(key >> lo) & mask], 1u);
+  }
+  __syncthreads();
+}
+}  // namespace
+
 // One workgroup.  Targets are 1-based ranks among the K sample keys; a rank
-// outside 1..K gives -inf (below) or +inf (above).
+// outside 1..K gives -inf (below) or +inf (above).  Level 1 (top 11 bits)
+// comes from the sample kernel's histogram; one vectorized pass then copies
+// each target's bin into LDS, where bits 10..20 and 0..9 are resolved.  A
+// bin too large for LDS is resolved by passes over the keys in memory.
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __restrict__ ykeys,
                                                              int64_t K,
                                                              const uint32_t* __restrict__ hist,
                                                              int64_t j, int64_t l,
                                                              SelectRec* __restrict__ out) {
-  __shared__ uint32_t h[2][kSelectBins];
+  __shared__ uint32_t h[kSelectBins];
   __shared__ uint32_t wsum[kSelThreads / kWave];
-  __shared__ int bin_s[2];
-  __shared__ uint32_t rank_s[2];
+  __shared__ int bin_s;
+  __shared__ uint32_t rank_s;
+  __shared__ uint32_t cand[2][kCand];
+  __shared__ uint32_t ccnt[2];
   const int tid = threadIdx.x;
   const int64_t tgt[2] = {j, l};
   bool live[2];
-  uint32_t prefix[2] = {0u, 0u};
+  uint32_t pre[2] = {0u, 0u}, rk[2] = {0u, 0u}, key_out[2] = {0u, 0u};
   for (int q = 0; q < 2; ++q) live[q] = (tgt[q] >= 1 && tgt[q] <= K);
 
-  // pass 0: top 11 bits, histogram built by the sample kernel
   for (int q = 0; q < 2; ++q) {
     if (!live[q]) continue;
-    for (int e = tid; e < kSelectBins; e += kSelThreads) h[0][e] = hist[e];
+    for (int e = tid; e < kSelectBins; e += kSelThreads) h[e] = hist[e];
     __syncthreads();
-    find_bin(h[0], kSelectBins, static_cast<uint32_t>(tgt[q]), wsum, &bin_s[q], &rank_s[q]);
+    find_bin(h, kSelectBins, static_cast<uint32_t>(tgt[q]), wsum, &bin_s, &rank_s);
+    pre[q] = static_cast<uint32_t>(bin_s);
+    rk[q] = rank_s;
     __syncthreads();
   }
-  for (int q = 0; q < 2; ++q) prefix[q] = static_cast<uint32_t>(bin_s[q]);
-  // passes 1 and 2: bits 10..20 (11 bits), then bits 0..9 (10 bits)
-  for (int pass = 1; pass <= 2; ++pass) {
-    const int hi_shift = (pass == 1) ? 21 : 10;   // bits already fixed
-    const int lo_shift = (pass == 1) ? 10 : 0;
-    const uint32_t mask = (pass == 1) ? 2047u : 1023u;
-    const int nb = (pass == 1) ? 2048 : 1024;
-    for (int e = tid; e < 2 * kSelectBins; e += kSelThreads) (&h[0][0])[e] = 0u;
-    __syncthreads();
-    for (int64_t i = tid; i < K; i += kSelThreads) {
-      const uint32_t key = ykeys[i];
-      for (int q = 0; q < 2; ++q)
-        if (live[q] && (key >> hi_shift) == prefix[q]) atomicAdd(&h[q][(key >> lo_shift) & mask], 1u);
-    }
-    __syncthreads();
+  if (tid < 2) ccnt[tid] = 0u;
+  __syncthreads();
+  auto collect = [&](uint32_t key) {
+#pragma unroll
     for (int q = 0; q < 2; ++q) {
-      if (!live[q]) continue;
-      find_bin(h[q], nb, rank_s[q], wsum, &bin_s[q], &rank_s[q]);
-      __syncthreads();
-      prefix[q] = (prefix[q] << (pass == 1 ? 11 : 10)) | static_cast<uint32_t>(bin_s[q]);
+      if (live[q] && (key >> 21) == pre[q]) {
+        const uint32_t c = atomicAdd(&ccnt[q], 1u);
+        if (c < static_cast<uint32_t>(kCand)) cand[q][c] = key;
+      }
     }
+  };
+  const int64_t K4 = K / 4;
+  const uint4* y4 = reinterpret_cast<const uint4*>(ykeys);
+  int64_t i4 = tid;
+  for (; i4 + 3 * kSelThreads < K4; i4 += 4 * kSelThreads) {   // four loads in flight
+    uint4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = y4[i4 + u * kSelThreads];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      collect(v[u].x);
+      collect(v[u].y);
+      collect(v[u].z);
+      collect(v[u].w);
+    }
+  }
+  for (; i4 < K4; i4 += kSelThreads) {
+    const uint4 v = y4[i4];
+    collect(v.x);
+    collect(v.y);
+    collect(v.z);
+    collect(v.w);
+  }
+  for (int64_t i = K4 * 4 + tid; i < K; i += kSelThreads) collect(ykeys[i]);
+  __syncthreads();
+
+  for (int q = 0; q < 2; ++q) {
+    if (!live[q]) continue;
+    const bool in_lds = ccnt[q] <= static_cast<uint32_t>(kCand);
+    const uint32_t* src = in_lds ? cand[q] : ykeys;
+    const int64_t count = in_lds ? static_cast<int64_t>(ccnt[q]) : K;
+    prefix_hist(src, count, 21, pre[q], 10, 2047u, 2048, h);
+    find_bin(h, 2048, rk[q], wsum, &bin_s, &rank_s);
+    const uint32_t pre2 = (pre[q] << 11) | static_cast<uint32_t>(bin_s);
+    const uint32_t rk2 = rank_s;
+    __syncthreads();
+    prefix_hist(src, count, 10, pre2, 0, 1023u, 1024, h);
+    find_bin(h, 1024, rk2, wsum, &bin_s, &rank_s);
+    key_out[q] = (pre2 << 10) | static_cast<uint32_t>(bin_s);
+    __syncthreads();
   }
   if (tid == 0) {
     SelectRec rec;
-    rec.keyL = live[0] ? prefix[0] : 0u;
-    rec.keyR = live[1] ? prefix[1] : 0u;
-    rec.aL = live[0] ? asc_key_float(prefix[0]) : -INFINITY;
-    rec.aR = live[1] ? asc_key_float(prefix[1]) : (tgt[1] < 1 ? -INFINITY : INFINITY);
-    if (!live[0] && tgt[0] > K) rec.aL = INFINITY;
+    rec.keyL = key_out[0];
+    rec.keyR = key_out[1];
+    rec.aL = live[0] ? asc_key_float(key_out[0]) : (tgt[0] < 1 ? -INFINITY : INFINITY);
+    rec.aR = live[1] ? asc_key_float(key_out[1]) : (tgt[1] < 1 ? -INFINITY : INFINITY);
     *out = rec;
   }
 }
@@ -167,9 +217,9 @@ hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* hist,
 
 // -------------------------------------------------------------- partition --
 int partition_blocks(int64_t n, int64_t* chunk) {
-  // ~2048 blocks; each block's chunk is a multiple of 1024 scores so that
-  // every wave owns a contiguous, float4-aligned quarter of it
-  int64_t c = (n + 2047) / 2048;
+  // up to 4096 blocks; a block's chunk is a multiple of 1024 scores so that
+  // each wave owns a contiguous, float4-aligned quarter of it
+  int64_t c = (n + kPartMaxBlocks - 1) / kPartMaxBlocks;
   c = (c + 1023) / 1024 * 1024;
   if (c < 1024) c = 1024;
   *chunk = c;
@@ -182,103 +232,113 @@ struct PartState {
   double TL, TR;
   int64_t nL, nR;
   int64_t nM;   // M count of this wave (uniform across the wave)
+  float mmin, mmax;
 };
 
-// Classify 4 consecutive scores of one lane; tails accumulate in float32
-// over the four and in float64 across calls.  M members are reported by
-// the callback in index order within the wave (lane-major, then element).
+// Classify 4 consecutive scores of one lane (the slow path of the gather);
+// M members are reported in index order within the wave (lane-major, then
+// element).
 template <typename Emit>
 __device__ __forceinline__ void classify4(const float (&v)[4], const bool (&ok)[4], int64_t i0,
-                                          float aL, float aR, float c2f, PartState& st,
-                                          Emit&& emit) {
-  float tl = 0.0f, tr = 0.0f;
-  int cl = 0, cr = 0;
+                                          float aL, float aR, PartState& st, Emit&& emit) {
   bool inM[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const bool L = ok[e] && v[e] < aL;
-    const bool R = ok[e] && v[e] >= aR;
-    inM[e] = ok[e] && !L && !R;
-    // e^{-(a_L - r)/t} for L, e^{-(r - a_R)/t} for R (exponent <= 0)
-    const float x = L ? (v[e] - aL) : (aR - v[e]);
-    const float term = exp2_fast(x * c2f);
-    tl += L ? term : 0.0f;
-    tr += R ? term : 0.0f;
-    cl += L;
-    cr += R;
-  }
-  st.TL += static_cast<double>(tl);
-  st.TR += static_cast<double>(tr);
-  st.nL += cl;
-  st.nR += cr;
-  uint64_t bal[4];
+  for (int e = 0; e < 4; ++e) inM[e] = ok[e] && !(v[e] < aL) && !(v[e] >= aR);
   uint32_t before = 0;
   uint32_t total = 0;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    bal[e] = __ballot(inM[e]);
-    before += lanes_below(bal[e]);
-    total += static_cast<uint32_t>(__popcll(bal[e]));
+    const uint64_t bal = __ballot(inM[e]);
+    before += lanes_below(bal);
+    total += static_cast<uint32_t>(__popcll(bal));
   }
-  if (total) {
-    uint32_t idx = before;
+  uint32_t idx = before;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (inM[e]) {
-        emit(st.nM + idx, v[e], i0 + e);
-        ++idx;
-      }
+  for (int e = 0; e < 4; ++e) {
+    if (inM[e]) {
+      emit(st.nM + idx, v[e], i0 + e);
+      ++idx;
     }
   }
   st.nM += total;
 }
 
-}  // namespace
+constexpr int kWaveStage = kPartStageCap / PW;   // M entries staged per wave
 
-// Each block owns [b*chunk, (b+1)*chunk); wave w the w-th contiguous quarter
-// of it, walked 256 scores (one float4 per lane) at a time, so the wave sees
-// its scores in index order.  M members are staged per wave in LDS, then
-// written to the block's slot of the global staging area in index order.
-__global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__ r, int64_t n,
-                                                       const SelectRec* __restrict__ sel,
-                                                       int use_sel, float aL_arg, float aR_arg,
-                                                       float c2f, int64_t chunk,
-                                                       float* __restrict__ stage_v,
-                                                       int32_t* __restrict__ stage_i,
-                                                       PartBlock* __restrict__ blk) {
-  __shared__ float sv[PW][kWaveStage];
-  __shared__ int32_t si[PW][kWaveStage];
-  __shared__ double red_d[2][PW];
-  __shared__ int64_t red_i[3][PW];
-  const float aL = use_sel ? sel->aL : aL_arg;
-  const float aR = use_sel ? sel->aR : aR_arg;
-  const int tid = threadIdx.x;
+// Per-wave pass over [w0, w1): tails in float32 over one float4 and float64
+// across, R counted only when a_R is finite (HAS_R), M members staged in
+// index order.  L is not counted: n_L = scores - n_M - n_R.
+template <bool HAS_R>
+__device__ __forceinline__ void partition_range(const float* __restrict__ r, int64_t w0, int64_t w1,
+                                                bool vec, float aL, float aR, float c2f,
+                                                float* sv, int32_t* si, PartState& st) {
   const int lane = lane_id();
-  const int wid = tid / kWave;
-  const int64_t b0 = static_cast<int64_t>(blockIdx.x) * chunk;
-  const int64_t wq = chunk / PW;
-  const int64_t w0 = b0 + wid * wq;
-  int64_t w1 = w0 + wq;
-  if (w1 > n) w1 = n;
-  PartState st{0.0, 0.0, 0, 0, 0};
-  auto stage = [&](int64_t slot, float v, int64_t gi) {
-    if (slot < kWaveStage) {
-      sv[wid][slot] = v;
-      si[wid][slot] = static_cast<int32_t>(gi);
+  auto one = [&](const float (&v)[4], const bool (&ok)[4], int64_t i0) {
+    float tl = 0.0f, tr = 0.0f;
+    uint32_t mb = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool L = v[e] < aL;
+      tl += (ok[e] && L) ? exp2_fast((v[e] - aL) * c2f) : 0.0f;
+      if constexpr (HAS_R) {
+        const bool R = v[e] >= aR;
+        tr += (ok[e] && R) ? exp2_fast((aR - v[e]) * c2f) : 0.0f;
+        st.nR += (ok[e] && R) ? 1 : 0;
+        if (ok[e] && !L && !R) mb |= 1u << e;
+      } else {
+        if (ok[e] && !L) mb |= 1u << e;
+      }
+    }
+    st.TL += static_cast<double>(tl);
+    if constexpr (HAS_R) st.TR += static_cast<double>(tr);
+    if (__ballot(mb != 0u)) {   // rare: some lane holds an M member
+      uint32_t before = 0, total = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint64_t bal = __ballot((mb >> e) & 1u);
+        before += lanes_below(bal);
+        total += static_cast<uint32_t>(__popcll(bal));
+      }
+      uint32_t idx = static_cast<uint32_t>(st.nM) + before;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if ((mb >> e) & 1u) {
+          st.mmin = fminf(st.mmin, v[e]);
+          st.mmax = fmaxf(st.mmax, v[e]);
+          if (idx < static_cast<uint32_t>(kWaveStage)) {
+            sv[idx] = v[e];
+            si[idx] = static_cast<int32_t>(i0 + e);
+          }
+          ++idx;
+        }
+      }
+      st.nM += total;
     }
   };
-  constexpr int U = 4;   // float4 loads in flight per lane
-  const bool vec = (reinterpret_cast<uintptr_t>(r) & 15) == 0;
+  constexpr int U = 4;   // float4 loads per lane per batch, two batches in flight
   int64_t it = w0;
-  for (; vec && it + U * 256 <= w1; it += U * 256) {
+  if (vec && it + U * 256 <= w1) {
     float4 q[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) q[u] = *reinterpret_cast<const float4*>(r + it + u * 256 + 4 * lane);
+    while (true) {
+      const int64_t cur = it;
+      it += U * 256;
+      const bool more = it + U * 256 <= w1;
+      float4 qn[U];
+      if (more) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float v[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
-      const bool ok[4] = {true, true, true, true};
-      classify4(v, ok, it + u * 256 + 4 * lane, aL, aR, c2f, st, stage);
+        for (int u = 0; u < U; ++u) qn[u] = *reinterpret_cast<const float4*>(r + it + u * 256 + 4 * lane);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float v[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+        const bool ok[4] = {true, true, true, true};
+        one(v, ok, cur + u * 256 + 4 * lane);
+      }
+      if (!more) break;
+#pragma unroll
+      for (int u = 0; u < U; ++u) q[u] = qn[u];
     }
   }
   for (; it < w1; it += 256) {
@@ -290,30 +350,72 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
       ok[e] = (i0 + e) < w1;
       v[e] = ok[e] ? r[i0 + e] : 0.0f;
     }
-    classify4(v, ok, i0, aL, aR, c2f, st, stage);
+    one(v, ok, i0);
   }
-  // block totals in a fixed order
+}
+
+}  // namespace
+
+// Block b owns [b*chunk, (b+1)*chunk) and wave w the w-th contiguous
+// quarter of it, so each wave sees its scores in index order and stages its
+// M members in LDS with a wave-private counter; the block then writes them
+// to its slot of the global staging area (wave 0's first) and one record of
+// tails and counts.
+__global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__ r, int64_t n,
+                                                       const SelectRec* __restrict__ sel,
+                                                       int use_sel, float aL_arg, float aR_arg,
+                                                       float c2f, int64_t chunk,
+                                                       float* __restrict__ stage_v,
+                                                       int32_t* __restrict__ stage_i,
+                                                       PartBlock* __restrict__ blk) {
+  __shared__ float sv[PW][kWaveStage];
+  __shared__ int32_t si[PW][kWaveStage];
+  __shared__ double red_d[2][PW];
+  __shared__ int64_t red_i[2][PW];
+  __shared__ float red_f[2][PW];
+  const float aL = use_sel ? sel->aL : aL_arg;
+  const float aR = use_sel ? sel->aR : aR_arg;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  const int64_t b0 = static_cast<int64_t>(blockIdx.x) * chunk;
+  const int64_t wq = chunk / PW;
+  const int64_t w0 = b0 + wid * wq < n ? b0 + wid * wq : n;
+  const int64_t w1 = w0 + wq < n ? w0 + wq : n;
+  const bool vec = (reinterpret_cast<uintptr_t>(r) & 15) == 0;
+  PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY};
+  if (aR < INFINITY)
+    partition_range<true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], st);
+  else
+    partition_range<false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], st);
+
   const double TL = wave_sum(st.TL);
   const double TR = wave_sum(st.TR);
-  const int64_t nL = wave_sum(st.nL);
   const int64_t nR = wave_sum(st.nR);
+  float mn = st.mmin, mx = st.mmax;
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    mn = fminf(mn, __shfl_xor(mn, o, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+  }
   if (lane == 0) {
     red_d[0][wid] = TL;
     red_d[1][wid] = TR;
-    red_i[0][wid] = nL;
-    red_i[1][wid] = nR;
-    red_i[2][wid] = st.nM;
+    red_i[0][wid] = nR;
+    red_i[1][wid] = st.nM;
+    red_f[0][wid] = mn;
+    red_f[1][wid] = mx;
   }
   __syncthreads();
   int64_t off = 0, mtot = 0;
   bool over = false;
 #pragma unroll
   for (int w = 0; w < PW; ++w) {
-    if (w < wid) off += red_i[2][w];
-    mtot += red_i[2][w];
-    over |= red_i[2][w] > kWaveStage;
+    if (w < wid) off += red_i[1][w];
+    mtot += red_i[1][w];
+    over |= red_i[1][w] > kWaveStage;
   }
-  if (!over) {
+  if (!over && st.nM > 0) {
     float* ov = stage_v + static_cast<int64_t>(blockIdx.x) * kPartStageCap;
     int32_t* oi = stage_i + static_cast<int64_t>(blockIdx.x) * kPartStageCap;
     for (int64_t q = lane; q < st.nM; q += kWave) {
@@ -324,19 +426,27 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   if (tid == 0) {
     PartBlock rec;
     double tl = 0.0, tr = 0.0;
-    int64_t cl = 0, cr = 0;
+    int64_t nr = 0;
 #pragma unroll
     for (int w = 0; w < PW; ++w) {
       tl += red_d[0][w];
       tr += red_d[1][w];
-      cl += red_i[0][w];
-      cr += red_i[1][w];
+      nr += red_i[0][w];
     }
+    const int64_t b1 = b0 + chunk < n ? b0 + chunk : n;
     rec.TL = tl;
     rec.TR = tr;
-    rec.nL = cl;
-    rec.nR = cr;
+    rec.nR = nr;
     rec.nM = mtot;
+    rec.nL = (b1 - b0) - mtot - nr;
+    float mn2 = INFINITY, mx2 = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < PW; ++w) {
+      mn2 = fminf(mn2, red_f[0][w]);
+      mx2 = fmaxf(mx2, red_f[1][w]);
+    }
+    rec.mmin = mn2;
+    rec.mmax = mx2;
     rec.overflow = over ? 1 : 0;
     rec.pad = 0;
     blk[blockIdx.x] = rec;
@@ -354,72 +464,82 @@ hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int
 }
 
 // One workgroup: totals over the partition blocks in a fixed order, and the
-// exclusive prefix of their M counts (each block's offset into M).
-__global__ __launch_bounds__(1024) void partition_totals_kernel(const PartBlock* __restrict__ blk,
+// exclusive prefix of their M counts (each block's offset into M).  Thread
+// tid owns a contiguous run of block records.
+__global__ __launch_bounds__(256) void partition_totals_kernel(const PartBlock* __restrict__ blk,
                                                                 int nblocks,
                                                                 const SelectRec* __restrict__ sel,
                                                                 int use_sel, float aL_arg,
                                                                 float aR_arg,
                                                                 int64_t* __restrict__ offsets,
                                                                 PartTotals* __restrict__ tot) {
-  constexpr int T = 1024;
+  constexpr int T = 256;
   constexpr int W = T / kWave;
   __shared__ double rd[2][W];
   __shared__ int64_t ri[4][W];
-  __shared__ int64_t carry_s;
+  __shared__ float rf[2][W];
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
+  const int per = (nblocks + T - 1) / T;
+  const int b0 = tid * per;
+  const int b1 = (b0 + per < nblocks) ? b0 + per : nblocks;
   double TL = 0.0, TR = 0.0;
-  int64_t nL = 0, nR = 0, ov = 0;
-  for (int b = tid; b < nblocks; b += T) {
-    TL += blk[b].TL;
-    TR += blk[b].TR;
-    nL += blk[b].nL;
-    nR += blk[b].nR;
-    ov += blk[b].overflow;
+  int64_t nL = 0, nR = 0, nM = 0, ov = 0;
+  float mn = INFINITY, mx = -INFINITY;
+  for (int b = b0; b < b1; ++b) {
+    const PartBlock rec = blk[b];
+    TL += rec.TL;
+    TR += rec.TR;
+    nL += rec.nL;
+    nR += rec.nR;
+    nM += rec.nM;
+    ov += rec.overflow;
+    mn = fminf(mn, rec.mmin);
+    mx = fmaxf(mx, rec.mmax);
+  }
+  // exclusive prefix of nM over threads (each thread's run is contiguous)
+  int64_t incl = nM;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int64_t x = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += x;
   }
   TL = wave_sum(TL);
   TR = wave_sum(TR);
-  nL = wave_sum(nL);
-  nR = wave_sum(nR);
-  ov = wave_sum(ov);
+  const int64_t sL = wave_sum(nL), sR = wave_sum(nR), sO = wave_sum(ov);
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    mn = fminf(mn, __shfl_xor(mn, o, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+  }
+  if (lane == kWave - 1) ri[3][wid] = incl;
   if (lane == 0) {
     rd[0][wid] = TL;
     rd[1][wid] = TR;
-    ri[0][wid] = nL;
-    ri[1][wid] = nR;
-    ri[2][wid] = ov;
+    ri[0][wid] = sL;
+    ri[1][wid] = sR;
+    ri[2][wid] = sO;
+    rf[0][wid] = mn;
+    rf[1][wid] = mx;
   }
-  if (tid == 0) carry_s = 0;
   __syncthreads();
-  // exclusive scan of nM over blocks, T at a time
-  for (int c0 = 0; c0 < nblocks; c0 += T) {
-    const int b = c0 + tid;
-    const int64_t v = (b < nblocks) ? blk[b].nM : 0;
-    int64_t incl = v;
+  int64_t base = 0, allm = 0;
 #pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int64_t x = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += x;
-    }
-    if (lane == kWave - 1) ri[3][wid] = incl;
-    __syncthreads();
-    int64_t base = carry_s, all = 0;
-#pragma unroll
-    for (int w = 0; w < W; ++w) {
-      if (w < wid) base += ri[3][w];
-      all += ri[3][w];
-    }
-    if (b < nblocks) offsets[b] = base + incl - v;
-    __syncthreads();
-    if (tid == 0) carry_s += all;
-    __syncthreads();
+  for (int w = 0; w < W; ++w) {
+    if (w < wid) base += ri[3][w];
+    allm += ri[3][w];
+  }
+  int64_t off = base + incl - nM;
+  for (int b = b0; b < b1; ++b) {
+    offsets[b] = off;
+    off += blk[b].nM;
   }
   if (tid == 0) {
     PartTotals x;
     double tl = 0.0, tr = 0.0;
     int64_t cl = 0, cr = 0, co = 0;
+    float fmn = INFINITY, fmx = -INFINITY;
 #pragma unroll
     for (int w = 0; w < W; ++w) {
       tl += rd[0][w];
@@ -427,14 +547,18 @@ __global__ __launch_bounds__(1024) void partition_totals_kernel(const PartBlock*
       cl += ri[0][w];
       cr += ri[1][w];
       co += ri[2][w];
+      fmn = fminf(fmn, rf[0][w]);
+      fmx = fmaxf(fmx, rf[1][w]);
     }
     x.TL = tl;
     x.TR = tr;
     x.nL = cl;
     x.nR = cr;
-    x.nM = carry_s;
+    x.nM = allm;
     x.aL = use_sel ? sel->aL : aL_arg;
     x.aR = use_sel ? sel->aR : aR_arg;
+    x.mmin = fmn;
+    x.mmax = fmx;
     x.any_block_overflow = co > 0 ? 1 : 0;
     x.pad = 0;
     *tot = x;
@@ -445,7 +569,7 @@ hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const Sele
                                    int use_sel, float aL, float aR, int64_t* offsets,
                                    PartTotals* tot, hipStream_t s) {
   { ProfScope ps_("partition_totals", s);
-  hipLaunchKernelGGL(partition_totals_kernel, dim3(1), dim3(1024), 0, s, blk, nblocks, sel, use_sel,
+  hipLaunchKernelGGL(partition_totals_kernel, dim3(1), dim3(256), 0, s, blk, nblocks, sel, use_sel,
                      aL, aR, offsets, tot); }
   return hipGetLastError();
 }
@@ -483,11 +607,12 @@ __global__ __launch_bounds__(PT) void gather_kernel(const float* __restrict__ r,
   const int64_t b0 = static_cast<int64_t>(b) * chunk;
   int64_t b1 = b0 + chunk;
   if (b1 > n) b1 = n;
-  PartState st{0.0, 0.0, 0, 0, 0};
+  PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY};
   auto put = [&](int64_t slot, float v, int64_t gi) {
     m_keys[off + slot] = desc_key(v);
     m_idx[off + slot] = static_cast<int32_t>(gi);
   };
+  // walk the chunk in index order with one wave, 256 scores at a time
   for (int64_t it = b0; it < b1; it += 256) {
     const int64_t i0 = it + 4 * lane;
     float v[4];
@@ -497,7 +622,7 @@ __global__ __launch_bounds__(PT) void gather_kernel(const float* __restrict__ r,
       ok[e] = (i0 + e) < b1;
       v[e] = ok[e] ? r[i0 + e] : 0.0f;
     }
-    classify4(v, ok, i0, aL, aR, 0.0f, st, put);
+    classify4(v, ok, i0, aL, aR, st, put);
   }
 }
 

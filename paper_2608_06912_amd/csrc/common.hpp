@@ -135,6 +135,9 @@ struct ScanSmem {
   double P[64];   // crossing refinement (at most 64 items per thread)
   double Q[64];
   float sv[64];
+  Pre pre_c;
+  Suf suf_c;
+  int cnt_c;
 };
 
 // Exclusive block scan of Pre, seeded with carry (groups before the block).
@@ -294,7 +297,9 @@ __device__ double block_solve(const float (&s)[ITEMS], int cnt, double rank0, Pr
   }
   const int nthr = block_count<WAVES>(below_k, sm);
 
-  // 4. the thread holding the crossing refines it position by position
+  // 4. the run holding the crossing is refined position by position: its
+  //    owner publishes the scores and carries, then one thread per position
+  //    forms P_i and E_i directly (independent terms, no serial chain)
   if (nthr == 0) {
     if (tid == 0) {
       // b lies above every score of the block
@@ -302,47 +307,54 @@ __device__ double block_solve(const float (&s)[ITEMS], int cnt, double rank0, Pr
       sm.b = gap_root(k, t, rank0, ext_pre.S != 0.0, ext_pre.u, log(ext_pre.S > 0 ? ext_pre.S : 1.0),
                       true, all.v, log(all.T));
     }
-  } else if (tid == nthr - 1) {
-    double* P = sm.P;
-    double* Q = sm.Q;
-    float* sv = sm.sv;   // LDS copy: the serial loops below index it at run time
+    __syncthreads();
+  } else {
+    const int owner = nthr - 1;
+    if (tid == owner) {
 #pragma unroll
-    for (int i = 0; i < ITEMS; ++i)
-      if (i < cnt) sv[i] = s[i];
-    const double first = s[0];
-    double Pi = 1.0;
-    if (pre_in.S != 0.0) Pi += wexp_f64(static_cast<double>(pre_in.u) - first, inv_t) * pre_in.S;
-    P[0] = Pi;
-    for (int i = 1; i < cnt; ++i) {
-      Pi = 1.0 + wexp_f64(static_cast<double>(sv[i - 1]) - static_cast<double>(sv[i]), inv_t) * Pi;
-      P[i] = Pi;
+      for (int i = 0; i < ITEMS; ++i)
+        if (i < cnt) sm.sv[i] = s[i];
+      sm.pre_c = pre_in;
+      sm.suf_c = suf_in;
+      sm.cnt_c = cnt;
     }
-    // Q_i = 1 + E_i (inclusive suffix at s_i); E_i kept separately
-    double Enext = (suf_in.T != 0.0)
-                       ? wexp_f64(static_cast<double>(sv[cnt - 1]) - static_cast<double>(suf_in.v), inv_t) * suf_in.T
-                       : 0.0;
-    int m = 0;
-    const double base = rank0 + static_cast<double>(tid) * ITEMS;
-    for (int i = cnt - 1; i >= 0; --i) {
-      const double Ei = Enext;
-      Q[i] = 1.0 + Ei;
-      const double Ni = base + static_cast<double>(i) + 1.0 - 0.5 * P[i] + 0.5 * Ei;
-      if (Ni <= k) m = (m == 0) ? i + 1 : m;   // node values are non-decreasing
-      if (i > 0) Enext = wexp_f64(static_cast<double>(sv[i - 1]) - static_cast<double>(sv[i]), inv_t) * Q[i];
+    __syncthreads();
+    const int oc = sm.cnt_c;
+    const Pre pc = sm.pre_c;
+    const Suf sc = sm.suf_c;
+    const double base = rank0 + static_cast<double>(owner) * ITEMS;
+    bool le = false;
+    if (tid < oc) {
+      const double si = sm.sv[tid];
+      double P = 1.0, E = 0.0;
+      if (pc.S != 0.0) P += wexp_f64(static_cast<double>(pc.u) - si, inv_t) * pc.S;
+      if (sc.T != 0.0) E += wexp_f64(si - static_cast<double>(sc.v), inv_t) * sc.T;
+      for (int j = 0; j < oc; ++j) {
+        const double sj = sm.sv[j];
+        if (j < tid) P += wexp_f64(sj - si, inv_t);
+        else if (j > tid) E += wexp_f64(si - sj, inv_t);
+      }
+      sm.P[tid] = P;
+      sm.Q[tid] = 1.0 + E;
+      le = (base + static_cast<double>(tid) + 1.0 - 0.5 * P + 0.5 * E) <= k;
     }
-    if (m == 0) m = 1;   // the first position was found at or below k above
-    const double c_up = base + m;
-    double bb;
-    if (m < cnt) {
-      bb = gap_root(k, t, c_up, true, sv[m - 1], log(P[m - 1]), true, sv[m], log(Q[m]));
-    } else {
-      const bool has_dn = suf_in.T != 0.0;
-      bb = gap_root(k, t, c_up, true, sv[cnt - 1], log(P[cnt - 1]), has_dn, suf_in.v,
-                    has_dn ? log(suf_in.T) : 0.0);
+    int m = block_count<WAVES>(le, sm);   // node values are non-decreasing
+    if (m == 0) m = 1;                    // the first position was found at or below k
+    if (tid == 0) {
+      const double c_up = base + m;
+      const double u = sm.sv[m - 1];
+      const double lnA = log(sm.P[m - 1]);
+      double bb;
+      if (m < oc) {
+        bb = gap_root(k, t, c_up, true, u, lnA, true, sm.sv[m], log(sm.Q[m]));
+      } else {
+        const bool has_dn = sc.T != 0.0;
+        bb = gap_root(k, t, c_up, true, u, lnA, has_dn, sc.v, has_dn ? log(sc.T) : 0.0);
+      }
+      sm.b = bb;
     }
-    sm.b = bb;
+    __syncthreads();
   }
-  __syncthreads();
   const double b = sm.b;
   __syncthreads();
   return b;

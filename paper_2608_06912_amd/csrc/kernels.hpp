@@ -16,7 +16,8 @@ constexpr int kTileItems = 16;
 constexpr int64_t kTile = kTileThreads * kTileItems;   // 4096
 // Bracketed pass: blocks of the streaming partition and their staging.
 constexpr int kPartThreads = 256;
-constexpr int kPartStageCap = 2048;    // M entries a partition block keeps
+constexpr int kPartMaxBlocks = 4096;   // blocks of the streaming partition
+constexpr int kPartStageCap = 2048;    // M entries a partition block stages
 constexpr int kSelectBins = 2048;      // 11-bit digits of the order-statistic select
 
 // Threshold record written by the device-wide solve (one per row).
@@ -32,6 +33,7 @@ struct SolveRec {
 struct PartBlock {
   int64_t nL, nM, nR;
   double TL, TR;
+  float mmin, mmax;   // smallest / largest member of M (+inf / -inf if none)
   int32_t overflow;   // this block's M did not fit its staging
   int32_t pad;
 };
@@ -41,6 +43,7 @@ struct PartTotals {
   int64_t nL, nM, nR;
   double TL, TR;
   float aL, aR;       // the bracket that was partitioned
+  float mmin, mmax;   // range of M (+inf / -inf when M is empty)
   int32_t any_block_overflow;
   int32_t pad;
 };
@@ -74,13 +77,14 @@ hipError_t launch_row_backward(const float* grad_p, const float* p, int64_t batc
 hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t, float* p,
                        hipStream_t s);
 
-// Device-wide backward for one row: partial (sum f, sum f g) per block, then
-// the emit (each emit block re-reduces the partials in a fixed order).
+// Device-wide backward for one row: partial (sum f, sum f g) per 4096-score
+// tile, one block reducing them in a fixed order to coef[0] = <g, q> and
+// coef[1] = 1/t (0 when sum f == 0), then the emit.
 int vjp_reduce_blocks(int64_t n);
 hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
-                             int nblocks, hipStream_t s);
-hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* partials,
-                           int nblocks, double t, float* grad, hipStream_t s);
+                             int nblocks, double t, double* coef, hipStream_t s);
+hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* coef,
+                           float* grad, hipStream_t s);
 
 // Device-wide stable LSD radix sort (descending float order) of one array.
 // Source: floats (converted to keys) or keys; values: none, the source
@@ -94,10 +98,15 @@ struct SortBuffers {
   int64_t max_tiles;
 };
 size_t sort_hist_words(int64_t len);
-// Returns the index (0/1) of the buffer holding the sorted result.
+int64_t sort_max_tiles(int64_t len);
+// pass_mask: bit p set when pass p (bits 8p..8p+7) must run; a pass whose
+// digit every key shares may be left out (a float source always runs its
+// first requested pass).  *keys_out / *vals_out point at the sorted result
+// (the source itself when no pass ran).
 hipError_t launch_sort(const float* src_f, const uint32_t* src_k, const int32_t* src_v,
                        bool with_vals, int64_t len, const int64_t* len_dev, SortBuffers& sb,
-                       int* out_buf, hipStream_t s);
+                       unsigned pass_mask, const uint32_t** keys_out, const int32_t** vals_out,
+                       hipStream_t s);
 
 // Device-wide threshold solve on a sorted (descending keys) array with the
 // bracket tails as carries.  nR/aR/TR: scores ranked before the array; aL/TL:

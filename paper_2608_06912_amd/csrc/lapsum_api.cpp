@@ -112,6 +112,7 @@ int check_ws(void* ws, size_t have, size_t need) {
 // --------------------------------------------------- full-sort long rows --
 struct FullWs {
   SortBuffers sb;
+  int64_t solve_tiles;
   double* tile_buf;
   SolveRec* rec;
 };
@@ -125,7 +126,8 @@ FullWs carve_full(Carve& c, int64_t n, bool with_vals) {
   w.sb.vals[1] = with_vals ? c.take<int32_t>(n) : nullptr;
   w.sb.hist = c.take<uint32_t>(sort_hist_words(n));
   w.sb.totals = c.take<uint32_t>(256);
-  w.sb.max_tiles = tiles;
+  w.sb.max_tiles = sort_max_tiles(n);
+  w.solve_tiles = tiles;
   w.tile_buf = c.take<double>(static_cast<size_t>(tiles) * kSolveTileDoubles);
   w.rec = c.take<SolveRec>(1);
   return w;
@@ -135,10 +137,12 @@ FullWs carve_full(Carve& c, int64_t n, bool with_vals) {
 // permutation.  Does not emit.
 int full_row_solve(const float* r, int64_t n, double k, double t, double* b_row, int32_t* perm_row,
                    FullWs& w, hipStream_t s) {
-  int which = 0;
-  LAPSUM_TRY(launch_sort(r, nullptr, nullptr, perm_row != nullptr, n, nullptr, w.sb, &which, s));
+  const uint32_t* keys = nullptr;
+  const int32_t* vals = nullptr;
+  LAPSUM_TRY(launch_sort(r, nullptr, nullptr, perm_row != nullptr, n, nullptr, w.sb, 0xfu, &keys,
+                         &vals, s));
   SolveArgs a{};
-  a.keys = w.sb.keys[which];
+  a.keys = keys;
   a.len = n;
   a.len_dev = nullptr;
   a.k = k;
@@ -146,12 +150,12 @@ int full_row_solve(const float* r, int64_t n, double k, double t, double* b_row,
   a.n_total = n;
   a.tails = nullptr;
   a.tile_buf = w.tile_buf;
-  a.max_tiles = w.sb.max_tiles;
+  a.max_tiles = w.solve_tiles;
   a.out = w.rec;
   a.b_out = b_row;
   LAPSUM_TRY(launch_sorted_solve(a, s));
   if (perm_row)
-    LAPSUM_TRY(hipMemcpyAsync(perm_row, w.sb.vals[which], static_cast<size_t>(n) * sizeof(int32_t),
+    LAPSUM_TRY(hipMemcpyAsync(perm_row, vals, static_cast<size_t>(n) * sizeof(int32_t),
                               hipMemcpyDeviceToDevice, s));
   return LAPSUM_OK;
 }
@@ -177,6 +181,7 @@ struct BracketWs {
   int32_t* m_idx;
   int32_t* m_idx_sorted;
   SortBuffers msb;     // device-wide sort of M (|M| > on-chip limit)
+  int64_t m_solve_tiles;
   double* m_tile_buf;
   SolveRec* rec;
   FullWs fall;         // full-sort fallback
@@ -206,7 +211,8 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
     w.msb.vals[1] = with_idx ? c.take<int32_t>(mcap) : nullptr;
     w.msb.hist = c.take<uint32_t>(sort_hist_words(mcap));
     w.msb.totals = c.take<uint32_t>(256);
-    w.msb.max_tiles = mt;
+    w.msb.max_tiles = sort_max_tiles(mcap);
+    w.m_solve_tiles = mt;
     w.m_tile_buf = c.take<double>(static_cast<size_t>(mt) * kSolveTileDoubles);
   }
   w.rec = c.take<SolveRec>(1);
@@ -218,6 +224,27 @@ size_t bracketed_ws(int64_t n, int64_t K, int64_t mcap, bool with_idx) {
   Carve c(nullptr);
   carve_bracket(c, n, K, mcap, with_idx);
   return c.size();
+}
+
+// Descending uint32 key of a float (the device's order-preserving map).
+uint32_t host_desc_key(float f) {
+  uint32_t u;
+  memcpy(&u, &f, sizeof(u));
+  const uint32_t asc = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ~asc;
+}
+
+// LSD passes a sort of keys within [key(mmax), key(mmin)] needs: the leading
+// bytes both ends share are shared by every key in between.
+unsigned sort_pass_mask(float mmin, float mmax) {
+  if (!(mmin <= mmax)) return 0xfu;
+  const uint32_t lo = host_desc_key(mmax), hi = host_desc_key(mmin);
+  unsigned mask = 0xfu;
+  for (int p = 3; p >= 0; --p) {
+    if (((lo >> (8 * p)) & 255u) != ((hi >> (8 * p)) & 255u)) break;
+    mask &= ~(1u << p);
+  }
+  return mask;
 }
 
 // Eq. (8) in IEEE float64, left to right, no contraction.
@@ -304,10 +331,12 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
                                         w.m_idx_sorted, s));
         sorted_idx = w.m_idx_sorted;
       } else {
-        int which = 0;
-        LAPSUM_TRY(launch_sort(nullptr, w.m_keys, w.m_idx, want_idx, tot.nM, nullptr, w.msb, &which, s));
+        const uint32_t* mk = nullptr;
+        const int32_t* mv = nullptr;
+        LAPSUM_TRY(launch_sort(nullptr, w.m_keys, w.m_idx, want_idx, tot.nM, nullptr, w.msb,
+                               sort_pass_mask(tot.mmin, tot.mmax), &mk, &mv, s));
         SolveArgs a{};
-        a.keys = w.msb.keys[which];
+        a.keys = mk;
         a.len = tot.nM;
         a.len_dev = nullptr;
         a.k = k;
@@ -315,11 +344,11 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
         a.n_total = n;
         a.tails = w.tot;
         a.tile_buf = w.m_tile_buf;
-        a.max_tiles = w.msb.max_tiles;
+        a.max_tiles = w.m_solve_tiles;
         a.out = w.rec;
         a.b_out = nullptr;
         LAPSUM_TRY(launch_sorted_solve(a, s));
-        sorted_idx = want_idx ? w.msb.vals[which] : nullptr;
+        sorted_idx = want_idx ? mv : nullptr;
       }
       SolveRec rec;
       st = read_back(&rec, w.rec, s);
@@ -446,6 +475,7 @@ size_t lapsum_backward_workspace_size(int64_t batch, int64_t n) {
   if (n <= kRowOnChipMax) return 0;
   Carve c(nullptr);
   c.take<double>(2 * static_cast<size_t>(vjp_reduce_blocks(n)));
+  c.take<double>(2);
   return c.size();
 }
 
@@ -468,10 +498,11 @@ int lapsum_backward(const float* grad_p, const float* p, const double* b, int64_
   Carve c(workspace);
   const int nb = vjp_reduce_blocks(n);
   double* partials = c.take<double>(2 * static_cast<size_t>(nb));
+  double* coef = c.take<double>(2);
   for (int64_t row = 0; row < batch; ++row) {
     const int64_t o = row * n;
-    LAPSUM_TRY(launch_vjp_reduce(grad_p + o, p + o, n, partials, nb, stream));
-    LAPSUM_TRY(launch_vjp_emit(grad_p + o, p + o, n, partials, nb, t, grad_r + o, stream));
+    LAPSUM_TRY(launch_vjp_reduce(grad_p + o, p + o, n, partials, nb, t, coef, stream));
+    LAPSUM_TRY(launch_vjp_emit(grad_p + o, p + o, n, coef, grad_r + o, stream));
   }
   return LAPSUM_OK;
 }

@@ -100,6 +100,22 @@ __device__ double root_above(const Tails& x, Suf below, double k, double t) {
                   has_dn ? log(below.T) : 0.0);
 }
 
+template <int WAVES>
+__device__ int64_t block_max_i64(int64_t v, int64_t* scratch) {
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    const int64_t w = __shfl_xor(v, o, kWave);
+    v = w > v ? w : v;
+  }
+  if (lane_id() == 0) scratch[threadIdx.x / kWave] = v;
+  __syncthreads();
+  v = 0;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) v = scratch[w] > v ? scratch[w] : v;
+  __syncthreads();
+  return v;
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(TT) void solve_tiles_kernel(const uint32_t* __restrict__ keys,
@@ -118,10 +134,26 @@ __global__ __launch_bounds__(TT) void solve_tiles_kernel(const uint32_t* __restr
   const double c2 = kLog2e / t;
   double S = 0.0, X = 0.0;
   const int64_t p0 = base + static_cast<int64_t>(tid) * TI;
+  uint32_t kv[TI];
+  if (nv == TILE && ((reinterpret_cast<uintptr_t>(keys) & 15) == 0)) {
+    const uint4* k4 = reinterpret_cast<const uint4*>(keys + p0);
+#pragma unroll
+    for (int q = 0; q < TI / 4; ++q) {
+      const uint4 v = k4[q];
+      kv[4 * q + 0] = v.x;
+      kv[4 * q + 1] = v.y;
+      kv[4 * q + 2] = v.z;
+      kv[4 * q + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+      kv[i] = (static_cast<int64_t>(tid) * TI + i < nv) ? keys[p0 + i] : 0u;
+  }
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
     if (static_cast<int64_t>(tid) * TI + i < nv) {
-      const double s = key_float(keys[p0 + i]);
+      const double s = key_float(kv[i]);
       S += wexp_f32(s - last, c2);
       if (tid * TI + i > 0) X += wexp_f32(first - s, c2);
     }
@@ -164,67 +196,89 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
   const Tails x = load_tails(a.tails);
   double* tb = a.tile_buf;
 
-  // 1. this thread's run of tiles
-  const int64_t per = (ntiles + TT - 1) / TT;
-  const int64_t t0 = static_cast<int64_t>(tid) * per;
-  const int64_t t1 = (t0 + per < ntiles) ? t0 + per : ntiles;
-  Pre mp = pre_empty();
-  Suf ms = suf_empty();
-  for (int64_t q = t0; q < t1; ++q) {
-    const double* r = tb + q * kTileRec;
-    mp = pre_combine(mp, Pre{static_cast<float>(r[3]), r[0]}, inv_t);
-  }
-  for (int64_t q = t1 - 1; q >= t0; --q) {
-    const double* r = tb + q * kTileRec;
-    ms = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, ms, inv_t);
-  }
   Pre pre_all;
   Suf suf_all;
-  const Pre pre_in = block_excl_pre<WAVES>(mp, x.pre, inv_t, sm, &pre_all);
-  const Suf suf_in = block_excl_suf<WAVES>(ms, x.suf, inv_t, sm, &suf_all);
-
-  // 2. suffix carried into each tile from the right (stored), then the node
-  //    value at each tile's first score walking left to right
-  {
-    Suf after = suf_in;
-    for (int64_t q = t1 - 1; q >= t0; --q) {
-      double* r = tb + q * kTileRec;
-      r[4] = after.v;
-      r[5] = after.T;
-      after = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, after, inv_t);
-    }
-  }
   int64_t below = 0;
-  {
-    Pre before = pre_in;
-    for (int64_t q = t0; q < t1; ++q) {
-      double* r = tb + q * kTileRec;
-      r[6] = before.u;
-      r[7] = before.S;
-      const double first = r[2];
+  if (ntiles <= TT) {
+    // at most one tile per thread: its record stays in registers
+    const bool has = tid < ntiles;
+    double S = 0.0, X = 0.0, first = 0.0, last = 0.0;
+    if (has) {
+      const double* r = tb + static_cast<int64_t>(tid) * kTileRec;
+      S = r[0];
+      X = r[1];
+      first = r[2];
+      last = r[3];
+    }
+    const Pre mp = has ? Pre{static_cast<float>(last), S} : pre_empty();
+    const Suf ms = has ? Suf{static_cast<float>(first), 1.0 + X} : suf_empty();
+    const Pre pre_in = block_excl_pre<WAVES>(mp, x.pre, inv_t, sm, &pre_all);
+    const Suf suf_in = block_excl_suf<WAVES>(ms, x.suf, inv_t, sm, &suf_all);
+    if (has) {
       double P = 1.0;
-      if (before.S != 0.0) P += wexp_f64(static_cast<double>(before.u) - first, inv_t) * before.S;
-      double E = r[1];
-      if (r[5] != 0.0) E += wexp_f64(first - r[4], inv_t) * r[5];
-      const double N = x.nR + static_cast<double>(q * TILE) + 1.0 - 0.5 * P + 0.5 * E;
-      if (N <= k) below = q + 1;   // non-decreasing: the last such tile
-      before = pre_combine(before, Pre{static_cast<float>(r[3]), r[0]}, inv_t);
+      if (pre_in.S != 0.0) P += wexp_f64(static_cast<double>(pre_in.u) - first, inv_t) * pre_in.S;
+      double E = X;
+      if (suf_in.T != 0.0) E += wexp_f64(first - static_cast<double>(suf_in.v), inv_t) * suf_in.T;
+      const double N = x.nR + static_cast<double>(tid) * TILE + 1.0 - 0.5 * P + 0.5 * E;
+      if (N <= k) below = tid + 1;
     }
-  }
-  // crossing tile = max over threads of `below`
-  {
-    int64_t v = below;
-#pragma unroll
-    for (int o = kWave / 2; o >= 1; o >>= 1) {
-      const int64_t w = __shfl_xor(v, o, kWave);
-      v = w > v ? w : v;
+    below = block_max_i64<WAVES>(below, cnt_s);
+    if (below > 0 && tid == below - 1) {
+      tile_pre_s = pre_in;
+      tile_suf_s = suf_in;
     }
-    if (lane_id() == 0) cnt_s[tid / kWave] = v;
     __syncthreads();
-    v = 0;
-#pragma unroll
-    for (int w = 0; w < WAVES; ++w) v = cnt_s[w] > v ? cnt_s[w] : v;
-    below = v;
+  } else {
+    // 1. this thread's run of tiles
+    const int64_t per = (ntiles + TT - 1) / TT;
+    const int64_t t0 = static_cast<int64_t>(tid) * per;
+    const int64_t t1 = (t0 + per < ntiles) ? t0 + per : ntiles;
+    Pre mp = pre_empty();
+    Suf ms = suf_empty();
+    for (int64_t q = t0; q < t1; ++q) {
+      const double* r = tb + q * kTileRec;
+      mp = pre_combine(mp, Pre{static_cast<float>(r[3]), r[0]}, inv_t);
+    }
+    for (int64_t q = t1 - 1; q >= t0; --q) {
+      const double* r = tb + q * kTileRec;
+      ms = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, ms, inv_t);
+    }
+    const Pre pre_in = block_excl_pre<WAVES>(mp, x.pre, inv_t, sm, &pre_all);
+    const Suf suf_in = block_excl_suf<WAVES>(ms, x.suf, inv_t, sm, &suf_all);
+
+    // 2. suffix carried into each tile from the right (stored), then the
+    //    node value at each tile's first score walking left to right
+    {
+      Suf after = suf_in;
+      for (int64_t q = t1 - 1; q >= t0; --q) {
+        double* r = tb + q * kTileRec;
+        r[4] = after.v;
+        r[5] = after.T;
+        after = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, after, inv_t);
+      }
+    }
+    {
+      Pre before = pre_in;
+      for (int64_t q = t0; q < t1; ++q) {
+        double* r = tb + q * kTileRec;
+        r[6] = before.u;
+        r[7] = before.S;
+        const double first = r[2];
+        double P = 1.0;
+        if (before.S != 0.0) P += wexp_f64(static_cast<double>(before.u) - first, inv_t) * before.S;
+        double E = r[1];
+        if (r[5] != 0.0) E += wexp_f64(first - r[4], inv_t) * r[5];
+        const double N = x.nR + static_cast<double>(q * TILE) + 1.0 - 0.5 * P + 0.5 * E;
+        if (N <= k) below = q + 1;   // non-decreasing: the last such tile
+        before = pre_combine(before, Pre{static_cast<float>(r[3]), r[0]}, inv_t);
+      }
+    }
+    below = block_max_i64<WAVES>(below, cnt_s);
+    if (below > 0 && tid == 0) {
+      const double* r = tb + (below - 1) * kTileRec;
+      tile_pre_s = Pre{static_cast<float>(r[6]), r[7]};
+      tile_suf_s = Suf{static_cast<float>(r[4]), r[5]};
+    }
     __syncthreads();
   }
 
@@ -243,11 +297,6 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
     b = root_above(x, suf_all, k, t);
   } else {
     const int64_t ct = below - 1;
-    if (tid == 0) {
-      const double* r = tb + ct * kTileRec;
-      tile_pre_s = Pre{static_cast<float>(r[6]), r[7]};
-      tile_suf_s = Suf{static_cast<float>(r[4]), r[5]};
-    }
     __syncthreads();
     const Pre tp = tile_pre_s;
     const Suf ts = tile_suf_s;
@@ -283,15 +332,13 @@ hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s) {
 }
 
 // ---------------------------------------------------- small middle set ----
-template <bool PAIRS>
-__global__ __launch_bounds__(1024) void small_m_solve_kernel(const uint32_t* __restrict__ m_keys,
-                                                             const int32_t* __restrict__ m_idx,
-                                                             const PartTotals* __restrict__ tot,
-                                                             double k, double t, int64_t n_total,
-                                                             SolveRec* __restrict__ out,
-                                                             int32_t* __restrict__ idx_sorted) {
-  constexpr int BLOCK = 1024;
-  constexpr int ITEMS = 32;
+template <int BLOCK, int ITEMS, bool PAIRS>
+__global__ __launch_bounds__(BLOCK) void small_m_solve_kernel(const uint32_t* __restrict__ m_keys,
+                                                              const int32_t* __restrict__ m_idx,
+                                                              const PartTotals* __restrict__ tot,
+                                                              double k, double t, int64_t n_total,
+                                                              SolveRec* __restrict__ out,
+                                                              int32_t* __restrict__ idx_sorted) {
   constexpr int WAVES = BLOCK / kWave;
   __shared__ uint32_t buf[BLOCK * ITEMS];
   __shared__ SortSmem<BLOCK> ssm;
@@ -341,20 +388,33 @@ __global__ __launch_bounds__(1024) void small_m_solve_kernel(const uint32_t* __r
   }
 }
 
+namespace {
+template <int BLOCK, int ITEMS>
+hipError_t small_m_items(const uint32_t* m_keys, const int32_t* m_idx, bool with_idx,
+                         const PartTotals* tot, double k, double t, int64_t n_total, SolveRec* out,
+                         int32_t* m_idx_sorted, hipStream_t s) {
+  ProfScope ps_("small_m_solve", s);
+  if (with_idx)
+    hipLaunchKernelGGL((small_m_solve_kernel<BLOCK, ITEMS, true>), dim3(1), dim3(BLOCK), 0, s,
+                       m_keys, m_idx, tot, k, t, n_total, out, m_idx_sorted);
+  else
+    hipLaunchKernelGGL((small_m_solve_kernel<BLOCK, ITEMS, false>), dim3(1), dim3(BLOCK), 0, s,
+                       m_keys, m_idx, tot, k, t, n_total, out, m_idx_sorted);
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, int64_t m_len,
                                 bool with_idx, const PartTotals* tot, double k, double t,
                                 int64_t n_total, SolveRec* out, int32_t* m_idx_sorted,
                                 hipStream_t s) {
-  if (m_len > kRowOnChipMax) return hipErrorInvalidValue;
-  if (with_idx)
-    { ProfScope ps_("small_m_solve", s);
-    hipLaunchKernelGGL(small_m_solve_kernel<true>, dim3(1), dim3(1024), 0, s, m_keys, m_idx, tot, k,
-                       t, n_total, out, m_idx_sorted); }
-  else
-    { ProfScope ps_("small_m_solve", s);
-    hipLaunchKernelGGL(small_m_solve_kernel<false>, dim3(1), dim3(1024), 0, s, m_keys, m_idx, tot,
-                       k, t, n_total, out, m_idx_sorted); }
-  return hipGetLastError();
+  // the on-chip capacity follows |M| (known to the host after the partition)
+  if (m_len <= 1024) return small_m_items<256, 4>(m_keys, m_idx, with_idx, tot, k, t, n_total, out, m_idx_sorted, s);
+  if (m_len <= 4096) return small_m_items<256, 16>(m_keys, m_idx, with_idx, tot, k, t, n_total, out, m_idx_sorted, s);
+  if (m_len <= 8192) return small_m_items<1024, 8>(m_keys, m_idx, with_idx, tot, k, t, n_total, out, m_idx_sorted, s);
+  if (m_len <= 16384) return small_m_items<1024, 16>(m_keys, m_idx, with_idx, tot, k, t, n_total, out, m_idx_sorted, s);
+  if (m_len <= kRowOnChipMax) return small_m_items<1024, 32>(m_keys, m_idx, with_idx, tot, k, t, n_total, out, m_idx_sorted, s);
+  return hipErrorInvalidValue;
 }
 
 __global__ void write_m_idx_kernel(const int32_t* __restrict__ src, int64_t m, int64_t cap,

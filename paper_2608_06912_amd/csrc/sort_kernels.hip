@@ -1,13 +1,17 @@
 // Device-wide stable LSD radix sort of one array into descending float order
 // (the sort step of the full-sort solver, §1/§3, and of the middle band M,
-// Suppl. B).  Four passes of 8-bit digits; each pass is
-//   upsweep    per-tile digit counts (tiles of 4096 keys)          read keys
-//   scan       per digit, exclusive prefix of the counts over tiles
+// Suppl. B).  Up to four passes of 8-bit digits; each pass is
+//   upsweep    per-tile digit counts                               read keys
+//   scan       per digit, exclusive prefix of the counts over tiles (folded
+//              into the downsweep when there are at most 64 tiles)
 //   downsweep  stable rank inside the tile (ballot digit matching),
 //              staged through LDS so that each digit run leaves the tile as
 //              a contiguous burst                                  read + write
-// Ties keep their input order (tile order, then position inside the tile),
-// which for the first pass is the original index: the sort is stable.
+// Tiles hold 1024 keys for inputs up to 2^20 keys (shorter serial ranking per
+// block), 4096 above.  Passes whose digit is the same for every key are
+// skipped (the caller knows the leading bytes all keys share).  Ties keep
+// their input order (tile order, then position inside the tile), which for
+// the first pass is the original index: the sort is stable.
 #include "block_sort.hpp"
 #include "kernels.hpp"
 
@@ -16,9 +20,8 @@ namespace lapsum {
 namespace {
 
 constexpr int TT = kTileThreads;           // 256
-constexpr int TI = kTileItems;             // 16
 constexpr int TW = TT / kWave;             // 4 waves
-constexpr int64_t TILE = kTile;            // 4096
+constexpr int kFusedScanTiles = 64;
 
 struct PassArgs {
   const float* src_f;      // pass 0 from floats, else null
@@ -45,13 +48,16 @@ __device__ __forceinline__ uint32_t load_key(const PassArgs& a, int64_t i) {
 }
 
 // position of item i of this thread inside the tile (wave-striped)
+template <int TI>
 __device__ __forceinline__ int tile_pos(int i) {
   return (threadIdx.x / kWave) * (kWave * TI) + i * kWave + lane_id();
 }
 
 }  // namespace
 
+template <int TI>
 __global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
+  constexpr int64_t TILE = static_cast<int64_t>(TT) * TI;
   const int64_t len = eff_len(a);
   const int64_t ntiles = (len + TILE - 1) / TILE;
   const int64_t tile = blockIdx.x;
@@ -64,7 +70,7 @@ __global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
   const int64_t base = tile * TILE;
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
-    const int64_t pos = base + tile_pos(i);
+    const int64_t pos = base + tile_pos<TI>(i);
     const bool valid = pos < len;
     const uint32_t d = valid ? (load_key(a, pos) >> a.shift) & 255u : 0u;
     const uint64_t peers = match_digit8(d) & __ballot(valid);
@@ -78,7 +84,9 @@ __global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
 }
 
 // One block per digit: exclusive prefix of hist[d][0..ntiles) in place.
+template <int TI>
 __global__ __launch_bounds__(TT) void sort_scan_kernel(PassArgs a) {
+  constexpr int64_t TILE = static_cast<int64_t>(TT) * TI;
   const int64_t len = eff_len(a);
   const int64_t ntiles = (len + TILE - 1) / TILE;
   const int d = blockIdx.x;
@@ -123,8 +131,9 @@ __global__ __launch_bounds__(TT) void sort_scan_kernel(PassArgs a) {
   if (tid == 0) a.totals[d] = carry;
 }
 
-template <bool PAIRS>
+template <int TI, bool PAIRS, bool FUSED>
 __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
+  constexpr int64_t TILE = static_cast<int64_t>(TT) * TI;
   const int64_t len = eff_len(a);
   const int64_t ntiles = (len + TILE - 1) / TILE;
   const int64_t tile = blockIdx.x;
@@ -141,7 +150,26 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
 
   // digit base over the whole array: exclusive prefix of totals over digits
   {
-    const uint32_t tot = a.totals[tid];
+    uint32_t tot, before_tile;
+    if constexpr (FUSED) {
+      // few tiles: this digit's total and its count in earlier tiles
+      const uint32_t* h = a.hist + static_cast<int64_t>(tid) * a.max_tiles;
+      tot = 0;
+      before_tile = 0;
+      for (int64_t q0 = 0; q0 < ntiles; q0 += 8) {   // eight independent loads in flight
+        uint32_t c[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) c[u] = (q0 + u < ntiles) ? h[q0 + u] : 0u;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (q0 + u < tile) before_tile += c[u];
+          tot += c[u];
+        }
+      }
+    } else {
+      tot = a.totals[tid];
+      before_tile = a.hist[static_cast<int64_t>(tid) * a.max_tiles + tile];
+    }
     uint32_t incl = tot;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
@@ -154,7 +182,7 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
 #pragma unroll
     for (int w = 0; w < TW; ++w)
       if (w < wid) wbase += wave_tot[w];
-    gbase[tid] = wbase + incl - tot + a.hist[static_cast<int64_t>(tid) * a.max_tiles + tile];
+    gbase[tid] = wbase + incl - tot + before_tile;
   }
   for (int e = tid; e < 256 * TW; e += TT) cnt[e] = 0u;
   __syncthreads();
@@ -166,7 +194,7 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
   uint64_t validm[TI];
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
-    const int64_t gp = base + tile_pos(i);
+    const int64_t gp = base + tile_pos<TI>(i);
     const bool valid = gp < len;
     key[i] = valid ? load_key(a, gp) : 0xffffffffu;
     if constexpr (PAIRS) val[i] = valid ? (a.src_v ? a.src_v[gp] : static_cast<int32_t>(gp)) : -1;
@@ -213,18 +241,33 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
 }
 
 size_t sort_hist_words(int64_t len) {
-  const int64_t tiles = (len + TILE - 1) / TILE;
+  // sized for the smaller tile
+  const int64_t tiles = (len + 1023) / 1024;
   return static_cast<size_t>(256) * static_cast<size_t>(tiles < 1 ? 1 : tiles);
 }
 
-hipError_t launch_sort(const float* src_f, const uint32_t* src_k, const int32_t* src_v,
+int64_t sort_max_tiles(int64_t len) {
+  const int64_t tiles = (len + 1023) / 1024;
+  return tiles < 1 ? 1 : tiles;
+}
+
+namespace {
+template <int TI>
+hipError_t sort_passes(const float* src_f, const uint32_t* src_k, const int32_t* src_v,
                        bool with_vals, int64_t len, const int64_t* len_dev, SortBuffers& sb,
-                       int* out_buf, hipStream_t s) {
+                       unsigned pass_mask, const uint32_t** keys_out, const int32_t** vals_out,
+                       hipStream_t s) {
+  constexpr int64_t TILE = static_cast<int64_t>(TT) * TI;
   const int64_t tiles = (len + TILE - 1) / TILE;
   if (tiles > sb.max_tiles) return hipErrorInvalidValue;
   const unsigned grid = static_cast<unsigned>(tiles < 1 ? 1 : tiles);
-  int cur = -1;
+  const bool fused = tiles <= kFusedScanTiles && len_dev == nullptr;
+  const uint32_t* cur_k = src_k;
+  const int32_t* cur_v = src_v;
+  const float* cur_f = src_f;
+  int nxt = 0;
   for (int pass = 0; pass < 4; ++pass) {
+    if (!(pass_mask & (1u << pass)) && cur_f == nullptr) continue;   // digit shared by all keys
     PassArgs a{};
     a.len = len;
     a.len_dev = len_dev;
@@ -232,33 +275,49 @@ hipError_t launch_sort(const float* src_f, const uint32_t* src_k, const int32_t*
     a.totals = sb.totals;
     a.max_tiles = sb.max_tiles;
     a.shift = 8 * pass;
-    if (pass == 0) {
-      a.src_f = src_f;
-      a.src_k = src_k;
-      a.src_v = src_v;
-    } else {
-      a.src_k = sb.keys[cur];
-      a.src_v = sb.vals[cur];
-    }
-    const int nxt = (cur == 0) ? 1 : 0;
+    a.src_f = cur_f;
+    a.src_k = cur_k;
+    a.src_v = cur_v;
     a.dst_k = sb.keys[nxt];
     a.dst_v = with_vals ? sb.vals[nxt] : nullptr;
     { ProfScope ps_("sort_upsweep", s);
-    hipLaunchKernelGGL(sort_upsweep_kernel, dim3(grid), dim3(TT), 0, s, a); }
-    { ProfScope ps_("sort_scan", s);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(256), dim3(TT), 0, s, a); }
-    if (with_vals)
-      { ProfScope ps_("sort_downsweep", s);
-      hipLaunchKernelGGL((sort_downsweep_kernel<true>), dim3(grid), dim3(TT), 0, s, a); }
-    else
-      { ProfScope ps_("sort_downsweep", s);
-      hipLaunchKernelGGL((sort_downsweep_kernel<false>), dim3(grid), dim3(TT), 0, s, a); }
+    hipLaunchKernelGGL((sort_upsweep_kernel<TI>), dim3(grid), dim3(TT), 0, s, a); }
+    if (!fused) {
+      ProfScope ps_("sort_scan", s);
+      hipLaunchKernelGGL((sort_scan_kernel<TI>), dim3(256), dim3(TT), 0, s, a);
+    }
+    {
+      ProfScope ps_("sort_downsweep", s);
+      if (with_vals) {
+        if (fused) hipLaunchKernelGGL((sort_downsweep_kernel<TI, true, true>), dim3(grid), dim3(TT), 0, s, a);
+        else hipLaunchKernelGGL((sort_downsweep_kernel<TI, true, false>), dim3(grid), dim3(TT), 0, s, a);
+      } else {
+        if (fused) hipLaunchKernelGGL((sort_downsweep_kernel<TI, false, true>), dim3(grid), dim3(TT), 0, s, a);
+        else hipLaunchKernelGGL((sort_downsweep_kernel<TI, false, false>), dim3(grid), dim3(TT), 0, s, a);
+      }
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    cur = nxt;
+    cur_f = nullptr;
+    cur_k = sb.keys[nxt];
+    cur_v = with_vals ? sb.vals[nxt] : nullptr;
+    nxt ^= 1;
   }
-  *out_buf = cur;
+  *keys_out = cur_k;
+  if (vals_out) *vals_out = cur_v;
   return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_sort(const float* src_f, const uint32_t* src_k, const int32_t* src_v,
+                       bool with_vals, int64_t len, const int64_t* len_dev, SortBuffers& sb,
+                       unsigned pass_mask, const uint32_t** keys_out, const int32_t** vals_out,
+                       hipStream_t s) {
+  if (len <= (int64_t(1) << 20))
+    return sort_passes<4>(src_f, src_k, src_v, with_vals, len, len_dev, sb, pass_mask, keys_out,
+                          vals_out, s);
+  return sort_passes<16>(src_f, src_k, src_v, with_vals, len, len_dev, sb, pass_mask, keys_out,
+                         vals_out, s);
 }
 
 }  // namespace lapsum

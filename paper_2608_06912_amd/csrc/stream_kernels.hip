@@ -60,7 +60,8 @@ __global__ __launch_bounds__(kStreamThreads) void emit_kernel(const float* __res
       p4[j * kStreamThreads + tid] = o;
     }
   } else {
-    for (int64_t i = base + tid; i < n; i += kStreamThreads) p[i] = laplace_p(r[i], b, inv_t);
+    for (int64_t i = base + tid; i < n && i < base + kStreamTile; i += kStreamThreads)
+      p[i] = laplace_p(r[i], b, inv_t);
   }
 }
 
@@ -75,12 +76,13 @@ hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t,
 
 // ------------------------------------------------------------ vjp reduce ---
 int vjp_reduce_blocks(int64_t n) {
-  int64_t b = (n + kStreamTile - 1) / kStreamTile;
-  return static_cast<int>(b < 1024 ? (b < 1 ? 1 : b) : 1024);
+  const int64_t b = (n + kStreamTile - 1) / kStreamTile;
+  return static_cast<int>(b < 1 ? 1 : (b > 4096 ? 4096 : b));
 }
 
-// Block-level sums of f = min(p, 1-p) and f g over a contiguous chunk,
-// float32 within one float4, float64 across float4s, then a fixed-order
+// Block b sums f = min(p, 1-p) and f g over a contiguous range of float4s,
+// four per lane in flight; g is read only for float4s with some f != 0.
+// float32 within a float4, float64 across, then a fixed-order block
 // reduction (butterfly within a wave, waves in order).
 __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float* __restrict__ g,
                                                                     const float* __restrict__ p,
@@ -96,24 +98,69 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float*
   const float4* p4 = reinterpret_cast<const float4*>(p);
   const float4* g4 = reinterpret_cast<const float4*>(g);
   double F = 0.0, G = 0.0;
-  for (int64_t i = lo + tid; i < hi; i += kStreamThreads) {
+  constexpr int U = 4;   // float4 of p per lane per batch, two batches in flight
+  int64_t i = lo + tid;
+  auto batch = [&](const float4 (&pv)[U], int64_t at) {
+    float f[U][4];
+    bool need[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      f[u][0] = fminf(pv[u].x, 1.0f - pv[u].x);
+      f[u][1] = fminf(pv[u].y, 1.0f - pv[u].y);
+      f[u][2] = fminf(pv[u].z, 1.0f - pv[u].z);
+      f[u][3] = fminf(pv[u].w, 1.0f - pv[u].w);
+      need[u] = ((f[u][0] + f[u][1]) + (f[u][2] + f[u][3])) != 0.0f;
+    }
+    float4 gv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      gv[u] = need[u] ? g4[at + u * kStreamThreads] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (need[u]) {
+        F += static_cast<double>((f[u][0] + f[u][1]) + (f[u][2] + f[u][3]));
+        G += static_cast<double>((f[u][0] * gv[u].x + f[u][1] * gv[u].y) +
+                                 (f[u][2] * gv[u].z + f[u][3] * gv[u].w));
+      }
+    }
+  };
+  if (i + (U - 1) * kStreamThreads < hi) {
+    float4 pv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) pv[u] = p4[i + u * kStreamThreads];
+    while (true) {
+      const int64_t cur = i;
+      i += U * kStreamThreads;
+      const bool more = i + (U - 1) * kStreamThreads < hi;
+      float4 pn[U];
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) pn[u] = p4[i + u * kStreamThreads];
+      }
+      batch(pv, cur);
+      if (!more) break;
+#pragma unroll
+      for (int u = 0; u < U; ++u) pv[u] = pn[u];
+    }
+  }
+  for (; i < hi; i += kStreamThreads) {
     const float4 pv = p4[i];
     const float fx = fminf(pv.x, 1.0f - pv.x), fy = fminf(pv.y, 1.0f - pv.y);
     const float fz = fminf(pv.z, 1.0f - pv.z), fw = fminf(pv.w, 1.0f - pv.w);
     const float fs = (fx + fy) + (fz + fw);
     if (fs != 0.0f) {
-      const float4 gv = g4[i];
+      const float4 gq = g4[i];
       F += static_cast<double>(fs);
-      G += static_cast<double>((fx * gv.x + fy * gv.y) + (fz * gv.z + fw * gv.w));
+      G += static_cast<double>((fx * gq.x + fy * gq.y) + (fz * gq.z + fw * gq.w));
     }
   }
-  if (blockIdx.x == gridDim.x - 1) {   // scalar tail
-    for (int64_t i = n4 * 4 + tid; i < n; i += kStreamThreads) {
-      const float pp = p[i];
-      const float f = fminf(pp, 1.0f - pp);
-      if (f != 0.0f) {
-        F += static_cast<double>(f);
-        G += static_cast<double>(f) * static_cast<double>(g[i]);
+  if (blockIdx.x == gridDim.x - 1) {   // scalar tail (all of it when unaligned)
+    for (int64_t j = n4 * 4 + tid; j < n; j += kStreamThreads) {
+      const float pp = p[j];
+      const float f1 = fminf(pp, 1.0f - pp);
+      if (f1 != 0.0f) {
+        F += static_cast<double>(f1);
+        G += static_cast<double>(f1) * static_cast<double>(g[j]);
       }
     }
   }
@@ -126,38 +173,27 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float*
   }
   __syncthreads();
   if (tid == 0) {
-    double f = 0.0, gg = 0.0;
+    double fsum = 0.0, gsum = 0.0;
 #pragma unroll
     for (int w = 0; w < kStreamThreads / kWave; ++w) {
-      f += red[0][w];
-      gg += red[1][w];
+      fsum += red[0][w];
+      gsum += red[1][w];
     }
-    partials[2 * blockIdx.x] = f;
-    partials[2 * blockIdx.x + 1] = gg;
+    partials[2 * blockIdx.x] = fsum;
+    partials[2 * blockIdx.x + 1] = gsum;
   }
 }
 
-hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
-                             int nblocks, hipStream_t s) {
-  { ProfScope ps_("vjp_reduce", s);
-  hipLaunchKernelGGL(vjp_reduce_kernel, dim3(nblocks), dim3(kStreamThreads), 0, s, g, p, n,
-                     partials); }
-  return hipGetLastError();
-}
-
-// -------------------------------------------------------------- vjp emit ---
-// Every block first re-reduces the per-block partials in the same fixed
-// order, so each block holds the identical (sum f, sum f g).
-__global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* __restrict__ g,
-                                                                  const float* __restrict__ p,
-                                                                  int64_t n,
-                                                                  const double* __restrict__ partials,
-                                                                  int nparts, double inv_t,
-                                                                  float* __restrict__ grad) {
-  __shared__ double red[2][kStreamThreads / kWave];
+// One block: sum the partials in a fixed order and store
+// coef = <g, q> = sum f g / sum f and scale = 1/t (both 0 when sum f == 0).
+__global__ __launch_bounds__(1024) void vjp_finalize_kernel(const double* __restrict__ partials,
+                                                            int nparts, double inv_t,
+                                                            double* __restrict__ coef) {
+  constexpr int T = 1024;
+  __shared__ double red[2][T / kWave];
   const int tid = threadIdx.x;
   double F = 0.0, G = 0.0;
-  for (int j = tid; j < nparts; j += kStreamThreads) {
+  for (int j = tid; j < nparts; j += T) {
     F += partials[2 * j];
     G += partials[2 * j + 1];
   }
@@ -169,17 +205,39 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* _
     red[1][wid] = G;
   }
   __syncthreads();
-  F = 0.0;
-  G = 0.0;
+  if (tid == 0) {
+    double f = 0.0, gg = 0.0;
 #pragma unroll
-  for (int w = 0; w < kStreamThreads / kWave; ++w) {
-    F += red[0][w];
-    G += red[1][w];
+    for (int w = 0; w < T / kWave; ++w) {
+      f += red[0][w];
+      gg += red[1][w];
+    }
+    coef[0] = (f > 0.0) ? gg / f : 0.0;
+    coef[1] = (f > 0.0) ? inv_t : 0.0;
   }
-  // grad_r = (f/t)(g - <g,q>), q = f / sum f; zero when sum f == 0
-  const float coef = static_cast<float>((F > 0.0) ? G / F : 0.0);
-  const float scale = static_cast<float>((F > 0.0) ? inv_t : 0.0);
+}
 
+hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
+                             int nblocks, double t, double* coef, hipStream_t s) {
+  { ProfScope ps_("vjp_reduce", s);
+  hipLaunchKernelGGL(vjp_reduce_kernel, dim3(nblocks), dim3(kStreamThreads), 0, s, g, p, n,
+                     partials); }
+  { ProfScope ps_("vjp_finalize", s);
+  hipLaunchKernelGGL(vjp_finalize_kernel, dim3(1), dim3(1024), 0, s, partials, nblocks, 1.0 / t,
+                     coef); }
+  return hipGetLastError();
+}
+
+// -------------------------------------------------------------- vjp emit ---
+// grad_r = (f/t)(g - <g,q>), q = f / sum f; zero where f == 0
+__global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* __restrict__ g,
+                                                                  const float* __restrict__ p,
+                                                                  int64_t n,
+                                                                  const double* __restrict__ coef2,
+                                                                  float* __restrict__ grad) {
+  const float coef = static_cast<float>(coef2[0]);
+  const float scale = static_cast<float>(coef2[1]);
+  const int tid = threadIdx.x;
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kStreamTile;
   const bool vec =
       ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(grad)) & 15) == 0;
@@ -205,7 +263,7 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* _
       o4[j * kStreamThreads + tid] = o;
     }
   } else {
-    for (int64_t i = base + tid; i < n; i += kStreamThreads) {
+    for (int64_t i = base + tid; i < n && i < base + kStreamTile; i += kStreamThreads) {
       const float pp = p[i];
       const float f = fminf(pp, 1.0f - pp);
       grad[i] = (f != 0.0f) ? f * scale * (g[i] - coef) : 0.0f;
@@ -213,12 +271,12 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* _
   }
 }
 
-hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* partials,
-                           int nblocks, double t, float* grad, hipStream_t s) {
+hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* coef,
+                           float* grad, hipStream_t s) {
   const int64_t blocks = (n + kStreamTile - 1) / kStreamTile;
   { ProfScope ps_("vjp_emit", s);
   hipLaunchKernelGGL(vjp_emit_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kStreamThreads), 0,
-                     s, g, p, n, partials, nblocks, 1.0 / t, grad); }
+                     s, g, p, n, coef, grad); }
   return hipGetLastError();
 }
 
