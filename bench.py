@@ -4,10 +4,11 @@
 
 A step is one pass of the whole hot path over one row of n = 1e8 float32
 scores (s + e, s ~ N(0,1), e ~ Laplace(0, 0.05)), k = 20000, alpha = -0.01,
-K = 1e5 sample, z = 5.16: sample + order statistics, the streaming partition,
-the middle-band sort, the bracketed scan / certificate / root, the Laplace-CDF
-emit, then the Eq. (5) backward for an upstream gradient ~ N(0,1).  Inputs are
-resident in HBM before timing starts.  One JSON line is printed.
+K = 1e5 sample, z = 5.16: sample + order statistics, the streaming partition
+(which also keeps the band of scores whose p depends on b), the middle-band
+sort, the bracketed scan / certificate / root, the Laplace-CDF emit, then the
+Eq. (5) backward for an upstream gradient ~ N(0,1) from the saved band.
+Inputs are resident in HBM before timing starts.  One JSON line is printed.
 
 Roofline: the dominant kernel's algorithmic bytes per launch divided by its
 average duration, timed live with HIP events (the library's event profiler,
@@ -51,7 +52,7 @@ METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=20_000_000)
@@ -61,10 +62,17 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_bytes(name: str, n: int, active: int, m: int) -> float | None:
-    """Algorithmic HBM bytes one launch of a kernel must move."""
+def kernel_bytes(name: str, n: int, active: int, band: int) -> float | None:
+    """Algorithmic HBM bytes one launch of a streaming kernel must move
+    (band: scores in the bracket's band; active: scores with 0 < p < 1)."""
     if name == "partition":
-        return 4.0 * n                       # read r
+        return 4.0 * n + 8.0 * band          # read r, stage the band
+    if name == "band_emit":
+        return 4.0 * n + 12.0 * band         # write p; read the band, write its p
+    if name == "band_vjp_reduce":
+        return 8.0 * band + 8.0 * active     # read the band; g and its copy where f != 0
+    if name == "band_vjp_emit":
+        return 4.0 * n + 8.0 * band + 4.0 * active   # write grad; read the band and g copies
     if name == "emit":
         return 8.0 * n                       # read r, write p
     if name == "vjp_reduce":
@@ -145,13 +153,21 @@ def main():
     mcap = L.default_m_capacity(n, K)
     ws_f = torch.empty(L.lapsum_forward_bracketed_workspace_size(1, n, K, mcap), dtype=torch.uint8,
                        device=dev)
-    ws_b = torch.empty(max(1, L.lapsum_backward_workspace_size(1, n)), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(max(1, L.lapsum_backward_band_workspace_size(1, n)), dtype=torch.uint8,
+                       device=dev)
+    band = L.new_band(1, n, dev)
     grad = torch.empty_like(r)
 
+    def forward():
+        return L.lapsum_forward_bracketed(r, w.k, w.alpha, noise, z=w.z, m_capacity=mcap,
+                                          band=band, workspace=ws_f)[:3]
+
+    def backward(p):
+        L.lapsum_backward_band(g, p, band, w.alpha, workspace=ws_b, out=grad)
+
     def step():
-        p, b, infos, _ = L.lapsum_forward_bracketed(r, w.k, w.alpha, noise, z=w.z, m_capacity=mcap,
-                                                    workspace=ws_f)
-        L.lapsum_backward(g, p, b, w.alpha, workspace=ws_b, out=grad)
+        p, b, infos = forward()
+        backward(p)
         return p, b, infos
 
     if args.copy_probe:
@@ -174,13 +190,12 @@ def main():
     # forward and backward separately (same K)
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        p, b, infos = L.lapsum_forward_bracketed(r, w.k, w.alpha, noise, z=w.z, m_capacity=mcap,
-                                                 workspace=ws_f)[:3]
+        p, b, infos = forward()
     torch.cuda.synchronize()
     ms_fwd = (time.perf_counter() - t0) * 1e3 / args.steps
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        L.lapsum_backward(g, p, b, w.alpha, workspace=ws_b, out=grad)
+        backward(p)
     torch.cuda.synchronize()
     ms_bwd = (time.perf_counter() - t0) * 1e3 / args.steps
 
@@ -190,12 +205,15 @@ def main():
         p, b, infos = step()
     prof = L.lapsum_profile_stop()
     active = int(((p > 0) & (p < 1)).sum().item())
-    m = int(infos[0]["n_M"])
-    dom = max((kname for kname in prof if kernel_bytes(kname, n, active, m) is not None),
+    inf0 = infos[0]
+    lo = np.float32(inf0["a_L"]) - np.float64(105.0 * w.t)
+    hi = np.float32(inf0["a_R"]) + np.float64(18.0 * w.t)
+    band_n = int(((r >= float(lo)) & (r < float(hi))).sum().item())
+    dom = max((kname for kname in prof if kernel_bytes(kname, n, active, band_n) is not None),
               key=lambda kname: prof[kname][1])
     launches, total_ms = prof[dom]
     avg_s = total_ms / launches / 1e3
-    achieved = kernel_bytes(dom, n, active, m) / avg_s / 1e9
+    achieved = kernel_bytes(dom, n, active, band_n) / avg_s / 1e9
     kernels = {kname: {"launches": c, "avg_us": 1e3 * ms / c} for kname, (c, ms) in sorted(prof.items())}
 
     model_bytes = 32.0 * n
@@ -225,10 +243,11 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(dom),
-                     "algorithmic_bytes": kernel_bytes(dom, n, active, m)},
+                     "algorithmic_bytes": kernel_bytes(dom, n, active, band_n)},
         "kernels": kernels,
         "bracket": {key: infos[0][key] for key in ("attempts", "fell_back", "n_M", "n_L", "n_R")},
         "active_scores": active,
+        "band_scores": band_n,
     }
     if not args.no_cpu_baseline:
         print(f"[bench] cpu baseline on {args.cpu_sample:.0e} scores", file=sys.stderr, flush=True)

@@ -17,7 +17,8 @@
  * ---------------------------------------
  *  - Pointers are DEVICE pointers (memory of the current HIP device) unless a
  *    comment says otherwise.  The caller owns all memory; the library never
- *    allocates device memory and keeps no state across calls.
+ *    allocates device memory and keeps no state across calls (beyond a
+ *    small pinned host buffer per host thread, see the bracketed forward).
  *  - Arrays are row-major [batch, n] and contiguous; k and alpha are shared
  *    by all rows.  Indices are int32 and count within a row.
  *  - Each call validates its scalar arguments on the host, then enqueues
@@ -136,12 +137,18 @@ int lapsum_backward(const float* grad_p, const float* p, const double* b,
  *     float32 endpoints, rounded to float32) and steps 3-5 repeat.  After 3
  *     brackets, or when |M| > m_capacity, the row is solved by the full-sort
  *     path instead;
- *  6. p_i = sigma((b - r_i) / alpha) in the original order.
+ *  6. p_i = sigma((b - r_i) / alpha) in the original order.  The pass of
+ *     step 3 also keeps the band lo <= r < hi, lo = a_L - 105 t and
+ *     hi = a_R + 18 t (rounded outwards to float32): for any b in a certified
+ *     bracket, p is exactly 0 below the band and exactly 1 above it in
+ *     float32, so step 6 writes p from the band and one bit per score
+ *     without reading r again.
  *
  * The result is the same b as lapsum_forward (the bracket only locates it).
- * The host waits on `stream` once per bracket attempt to read the
- * certificate, so this call returns after the row's threshold is known (the
- * final emit is still asynchronous).
+ * The host waits on `stream` twice per bracket attempt to read the set sizes
+ * and the certificate, so this call returns after the row's threshold is
+ * known (the emit of step 6 may still be running).  The first call on a
+ * host thread allocates a small pinned host buffer that the library keeps.
  *
  *   K           sample size, 2 <= K <= n.
  *   z           bracket half-width in standard deviations (the paper uses
@@ -159,6 +166,11 @@ int lapsum_backward(const float* grad_p, const float* p, const double* b,
  *               -1 after the first n_M entries.  Rows that fell back to the
  *               full sort get all -1.  Asking for it makes the M sort carry
  *               indices.
+ *   band        NULL, or device memory of at least lapsum_band_size(batch, n)
+ *               bytes, 256-byte aligned (band_bytes its size): receives the
+ *               band of each row with its p, for lapsum_backward_band.  Its
+ *               content is private to the library; it stays valid until the
+ *               caller reuses the memory.
  * ------------------------------------------------------------------------ */
 #define LAPSUM_FLAG_FULL_SORT 1u
 
@@ -178,13 +190,39 @@ size_t lapsum_forward_bracketed_workspace_size(int64_t batch, int64_t n,
                                                int64_t K, int64_t m_capacity,
                                                int with_m_idx);
 
+size_t lapsum_band_size(int64_t batch, int64_t n);
+
 int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n,
                              double k, double alpha, int64_t K, double z,
                              const float* noise, int64_t m_capacity,
                              uint32_t flags, float* p, double* b,
                              lapsum_bracket_info* info, int32_t* m_idx_out,
+                             void* band, size_t band_bytes,
                              void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Backward from a saved band: the same vector-Jacobian product as
+ * lapsum_backward (Eq. (5)), for the p of a lapsum_forward_bracketed call
+ * that was given `band`.  f = min(p, 1 - p) / t is zero outside the band, so
+ * the sums of f and f g visit the band only (g is read where f != 0) and
+ * grad_r is written densely, zero outside the band, without reading p.
+ * Blocks of the row whose band did not fit the library's lists, and rows
+ * that fell back to the full sort, are computed from p and grad_p directly.
+ *
+ *   grad_p, p, alpha, grad_r   as in lapsum_backward (p: the forward's output)
+ *   band, band_bytes           the forward's band, unchanged since; a band
+ *                              saved for another row length is detected and
+ *                              the dense form used instead
+ * INVALID_ARG also when band is NULL, smaller than lapsum_band_size(batch, n)
+ * or not 256-byte aligned.
+ * ------------------------------------------------------------------------ */
+size_t lapsum_backward_band_workspace_size(int64_t batch, int64_t n);
+
+int lapsum_backward_band(const float* grad_p, const float* p, const void* band,
+                         size_t band_bytes, int64_t batch, int64_t n,
+                         double alpha, float* grad_r, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Diagnostics: per-kernel timing with HIP events.  Off by default.  While

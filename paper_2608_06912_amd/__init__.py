@@ -24,6 +24,7 @@ __all__ = [
     "lapsum_backward_workspace_size", "lapsum_backward",
     "lapsum_forward_bracketed_workspace_size", "lapsum_forward_bracketed",
     "LAPSUM_FLAG_FULL_SORT", "LIB_PATH", "lapsum_profile_start", "lapsum_profile_stop",
+    "lapsum_band_size", "new_band", "lapsum_backward_band_workspace_size", "lapsum_backward_band",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapsum.so")
@@ -77,8 +78,14 @@ def load():
     lib.lapsum_forward_bracketed_workspace_size.argtypes = [i64, i64, i64, i64, i32]
     lib.lapsum_forward_bracketed_workspace_size.restype = sz
     lib.lapsum_forward_bracketed.argtypes = [vp, i64, i64, f64, f64, i64, f64, vp, i64, u32,
-                                             vp, vp, vp, vp, vp, sz, vp]
+                                             vp, vp, vp, vp, vp, sz, vp, sz, vp]
     lib.lapsum_forward_bracketed.restype = i32
+    lib.lapsum_band_size.argtypes = [i64, i64]
+    lib.lapsum_band_size.restype = sz
+    lib.lapsum_backward_band_workspace_size.argtypes = [i64, i64]
+    lib.lapsum_backward_band_workspace_size.restype = sz
+    lib.lapsum_backward_band.argtypes = [vp, vp, vp, sz, i64, i64, f64, vp, vp, sz, vp]
+    lib.lapsum_backward_band.restype = i32
     lib.lapsum_profile_start.argtypes = []
     lib.lapsum_profile_start.restype = i32
     lib.lapsum_profile_stop.argtypes = []
@@ -194,11 +201,32 @@ def default_m_capacity(n: int, K: int) -> int:
     return int(min(n, max(1 << 16, 64 * (n // max(1, int(K ** 0.5))))))
 
 
+def lapsum_band_size(batch: int, n: int) -> int:
+    return int(load().lapsum_band_size(batch, n))
+
+
+def new_band(batch: int, n: int, device):
+    """Device buffer for the band a bracketed forward saves for its backward."""
+    torch = _torch()
+    return torch.empty(max(1, lapsum_band_size(batch, n)), dtype=torch.uint8, device=device)
+
+
+def _band_arg(band, batch, n):
+    torch = _torch()
+    if band is None:
+        return ctypes.c_void_p(0), 0
+    if not isinstance(band, torch.Tensor) or band.device.type != "cuda" or not band.is_contiguous():
+        raise ValueError("band must be a contiguous CUDA tensor (see new_band)")
+    return ctypes.c_void_p(band.data_ptr()), band.numel() * band.element_size()
+
+
 def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float = 5.16,
                              m_capacity: int | None = None, flags: int = 0,
-                             m_idx: bool = False, workspace=None):
+                             m_idx: bool = False, band=None, workspace=None):
     """Bracketed forward.  noise: float32 CUDA tensor [K] of Laplace(0, |alpha|)
-    draws.  Returns (p, b, infos, m_idx or None) with infos a list of dicts."""
+    draws.  band: None, or a buffer from new_band() that receives the band for
+    lapsum_backward_band.  Returns (p, b, infos, m_idx or None) with infos a
+    list of dicts."""
     torch = _torch()
     lib = load()
     batch, n = _rows(scores, "scores")
@@ -215,13 +243,39 @@ def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float 
     infos = (BracketInfo * batch)()
     ws, nbytes = _workspace(lib.lapsum_forward_bracketed_workspace_size(batch, n, K, m_capacity,
                                                                         int(m_idx)), dev, workspace)
+    bp, bbytes = _band_arg(band, batch, n)
     with torch.cuda.device(dev):
         _check(lib.lapsum_forward_bracketed(_ptr(scores), batch, n, float(k), float(alpha), K,
                                             float(z), _ptr(noise), int(m_capacity), int(flags),
                                             _ptr(p), _ptr(b), ctypes.cast(infos, ctypes.c_void_p),
-                                            _ptr(mi), _ptr(ws), nbytes, _stream(dev)),
+                                            _ptr(mi), bp, bbytes, _ptr(ws), nbytes, _stream(dev)),
                "lapsum_forward_bracketed")
     return p, b, [infos[i].as_dict() for i in range(batch)], mi
+
+
+def lapsum_backward_band_workspace_size(batch: int, n: int) -> int:
+    return int(load().lapsum_backward_band_workspace_size(batch, n))
+
+
+def lapsum_backward_band(grad_p, p, band, alpha: float, *, workspace=None, out=None):
+    """Eq. (5) VJP from the band a bracketed forward saved (see new_band)."""
+    torch = _torch()
+    lib = load()
+    batch, n = _rows(p, "p")
+    if grad_p.shape != p.shape:
+        raise ValueError("grad_p and p must have the same shape")
+    _rows(grad_p, "grad_p")
+    if band is None:
+        raise ValueError("band is required")
+    dev = p.device
+    grad = out if out is not None else torch.empty_like(p)
+    ws, nbytes = _workspace(lib.lapsum_backward_band_workspace_size(batch, n), dev, workspace)
+    bp, bbytes = _band_arg(band, batch, n)
+    with torch.cuda.device(dev):
+        _check(lib.lapsum_backward_band(_ptr(grad_p), _ptr(p), bp, bbytes, batch, n, float(alpha),
+                                        _ptr(grad), _ptr(ws), nbytes, _stream(dev)),
+               "lapsum_backward_band")
+    return grad
 
 
 def lapsum_profile_start() -> None:

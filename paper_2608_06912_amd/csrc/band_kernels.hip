@@ -1,0 +1,358 @@
+// Passes over the band a bracket's partition staged (the scores whose p is
+// strictly between 0 and 1 can only lie there; see BandEntry):
+//   band_emit      p for one partition block's range: band members from
+//                  their staged score and b, every other score 0 or 1 from
+//                  the side it lies on (one bit per score when a_R is
+//                  finite).  Writes p densely without reading r: 4 B/score
+//                  plus 8 B per band member.  The entries then hold p, the
+//                  forward's context for the backward.
+//   band_vjp       Eq. (5) from the context: sums of f = min(p, 1 - p) and
+//                  f g over the band (g read only where f != 0), the
+//                  fixed-order finalize, and grad_r written densely (zero
+//                  outside the band): 4 B/score plus the band.
+// A block whose lists overflowed (or whose range is too long for the LDS
+// map) takes the dense form of each pass over its own range.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace lapsum {
+
+namespace {
+
+constexpr int BT = 256;
+constexpr int BW = BT / kWave;   // one list segment per wave of the partition
+static_assert(BW == 4, "the partition stages one list per wave of four");
+constexpr int kMaxWords = static_cast<int>(kBandMaxChunk / 32);
+constexpr int kMaxEnt = 4 * kBandWaveCapMax;
+constexpr int kWordsPerThread = kMaxWords / BT;
+
+// LDS map from a block-local offset to the rank of its band member.
+struct BandLds {
+  uint32_t bits[kMaxWords];
+  uint32_t pre[kMaxWords];   // members in the words before
+  float vals[kMaxEnt];       // value of the member of each rank
+  int seg[BW + 1];           // rank of each wave segment's first entry
+  uint32_t wtot[BW];
+};
+
+struct BlockRange {
+  int64_t b0, b1;
+};
+
+__device__ __forceinline__ BlockRange block_range(int64_t n, int64_t chunk) {
+  BlockRange br;
+  br.b0 = static_cast<int64_t>(blockIdx.x) * chunk;
+  br.b1 = br.b0 + chunk < n ? br.b0 + chunk : n;
+  return br;
+}
+
+// This block's lists are complete and consistent with the layout.
+__device__ __forceinline__ bool lists_usable(const BandCtx& c) {
+  const BandBlock& bb = c.blk[blockIdx.x];
+  bool ok = bb.dense == 0 && c.chunk <= kBandMaxChunk && c.cap <= kBandWaveCapMax;
+#pragma unroll
+  for (int w = 0; w < BW; ++w) ok = ok && bb.cnt[w] >= 0 && bb.cnt[w] <= c.cap;
+  return ok;
+}
+
+// Backward: the saved header must describe this row (a band saved for
+// another length, or a forward that fell back to the full sort, makes every
+// pass dense).
+__device__ __forceinline__ bool block_dense(const BandCtx& c, int64_t n) {
+  const CtxHeader h = *c.hdr;
+  if (h.mode != 0 || h.n != n || h.nblocks != c.nblocks || h.chunk != c.chunk || h.cap != c.cap)
+    return true;
+  return !lists_usable(c);
+}
+
+// Build the map of this block's band.  value(rank, entry, slot) gives the
+// float stored for each member.  Ends with a barrier.
+template <typename Value>
+__device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L, Value&& value) {
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    int acc = 0;
+    const BandBlock& bb = c.blk[blockIdx.x];
+#pragma unroll
+    for (int w = 0; w < BW; ++w) {
+      L.seg[w] = acc;
+      acc += bb.cnt[w];
+    }
+    L.seg[BW] = acc;
+  }
+  const int nwords = static_cast<int>((len + 31) / 32);
+  for (int w = tid; w < nwords; w += BT) L.bits[w] = 0u;
+  __syncthreads();
+  const int total = L.seg[BW];
+  for (int e = tid; e < total; e += BT) {
+    int w = 0;
+#pragma unroll
+    for (int q = 1; q < BW; ++q) w += (e >= L.seg[q]) ? 1 : 0;
+    const int64_t slot = (static_cast<int64_t>(blockIdx.x) * BW + w) * c.cap + (e - L.seg[w]);
+    const BandEntry en = c.ent[slot];
+    const int64_t o = static_cast<int64_t>(en.idx) - b0;
+    if (o >= 0 && o < len) atomicOr(&L.bits[o >> 5], 1u << (o & 31));
+    L.vals[e] = value(e, en, slot);
+  }
+  __syncthreads();
+  // exclusive prefix of the members per word: each thread owns a run of words
+  const int w0 = tid * kWordsPerThread;
+  uint32_t loc = 0;
+#pragma unroll
+  for (int q = 0; q < kWordsPerThread; ++q)
+    loc += (w0 + q < nwords) ? static_cast<uint32_t>(__popc(L.bits[w0 + q])) : 0u;
+  uint32_t incl = loc;
+  const int lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t x = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += x;
+  }
+  const int wid = tid / kWave;
+  if (lane == kWave - 1) L.wtot[wid] = incl;
+  __syncthreads();
+  uint32_t run = incl - loc;
+#pragma unroll
+  for (int w = 0; w < BW; ++w)
+    if (w < wid) run += L.wtot[w];
+#pragma unroll
+  for (int q = 0; q < kWordsPerThread; ++q) {
+    if (w0 + q < nwords) {
+      L.pre[w0 + q] = run;
+      run += static_cast<uint32_t>(__popc(L.bits[w0 + q]));
+    }
+  }
+  __syncthreads();
+}
+
+// Write out[b0 .. b1) from the map: members take their value, other scores
+// 0, or 1 where their bit in `ones` is set (ones may be null).
+__device__ void write_dense(int64_t b0, int64_t b1, const BandLds& L, const uint32_t* ones,
+                            float* __restrict__ out) {
+  const int tid = threadIdx.x;
+  const int64_t len = b1 - b0;
+  auto value = [&](int64_t o) -> float {   // o: block-local offset
+    const uint32_t word = L.bits[o >> 5];
+    const uint32_t bit = 1u << (o & 31);
+    if (word & bit) return L.vals[L.pre[o >> 5] + __popc(word & (bit - 1u))];
+    return (ones && ((ones[(b0 + o) >> 5] >> ((b0 + o) & 31)) & 1u)) ? 1.0f : 0.0f;
+  };
+  if ((reinterpret_cast<uintptr_t>(out + b0) & 15) == 0) {
+    const int64_t n4 = len / 4;
+    float4* o4 = reinterpret_cast<float4*>(out + b0);
+    for (int64_t q = tid; q < n4; q += BT) {
+      const uint32_t word = L.bits[q >> 3];
+      const int sh = static_cast<int>(q & 7) * 4;
+      const uint32_t nib = (word >> sh) & 15u;
+      const uint32_t onib = ones ? (ones[(b0 >> 5) + (q >> 3)] >> sh) & 15u : 0u;
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = ((onib >> e) & 1u) ? 1.0f : 0.0f;
+      if (nib) {
+        uint32_t rk = L.pre[q >> 3] + static_cast<uint32_t>(__popc(word & ((1u << sh) - 1u)));
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if ((nib >> e) & 1u) v[e] = L.vals[rk++];
+      }
+      o4[q] = make_float4(v[0], v[1], v[2], v[3]);
+    }
+    for (int64_t o = n4 * 4 + tid; o < len; o += BT) out[b0 + o] = value(o);
+  } else {
+    for (int64_t o = tid; o < len; o += BT) out[b0 + o] = value(o);
+  }
+}
+
+// Dense emit of one block's range.
+__device__ void dense_emit(const float* __restrict__ r, int64_t b0, int64_t b1, double b,
+                           double inv_t, float* __restrict__ p) {
+  const int tid = threadIdx.x;
+  const bool vec = ((reinterpret_cast<uintptr_t>(r + b0) | reinterpret_cast<uintptr_t>(p + b0)) & 15) == 0;
+  int64_t i = b0 + tid;
+  if (vec) {
+    const int64_t n4 = (b1 - b0) / 4;
+    const float4* r4 = reinterpret_cast<const float4*>(r + b0);
+    float4* p4 = reinterpret_cast<float4*>(p + b0);
+    for (int64_t q = tid; q < n4; q += BT) {
+      const float4 v = r4[q];
+      p4[q] = make_float4(laplace_p(v.x, b, inv_t), laplace_p(v.y, b, inv_t),
+                          laplace_p(v.z, b, inv_t), laplace_p(v.w, b, inv_t));
+    }
+    i = b0 + n4 * 4 + tid;
+  }
+  for (; i < b1; i += BT) p[i] = laplace_p(r[i], b, inv_t);
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__ r, int64_t n,
+                                                       const SolveRec* __restrict__ rec,
+                                                       double inv_t, BandCtx c,
+                                                       const uint32_t* __restrict__ ones,
+                                                       float* __restrict__ p,
+                                                       double* __restrict__ b_out) {
+  __shared__ BandLds L;
+  if (!rec->ok) return;
+  const double b = rec->b;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    b_out[0] = b;
+    CtxHeader h;
+    h.mode = 0;
+    h.nblocks = c.nblocks;
+    h.chunk = c.chunk;
+    h.cap = c.cap;
+    h.pad = 0;
+    h.n = n;
+    *c.hdr = h;
+  }
+  const BlockRange br = block_range(n, c.chunk);
+  if (!lists_usable(c)) {
+    dense_emit(r, br.b0, br.b1, b, inv_t, p);
+    return;
+  }
+  build_map(c, br.b0, br.b1 - br.b0, L, [&](int, const BandEntry& en, int64_t slot) {
+    const float pv = laplace_p(__uint_as_float(en.bits), b, inv_t);
+    BandEntry o;
+    o.idx = en.idx;
+    o.bits = __float_as_uint(pv);
+    c.ent[slot] = o;
+    return pv;
+  });
+  write_dense(br.b0, br.b1, L, ones, p);
+}
+
+hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, double t,
+                            const BandCtx& band, const uint32_t* ones, int has_ones, float* p,
+                            double* b_out, hipStream_t s) {
+  { ProfScope ps_("band_emit", s);
+  hipLaunchKernelGGL(band_emit_kernel, dim3(band.nblocks), dim3(BT), 0, s, r, n, rec, 1.0 / t, band,
+                     has_ones ? ones : nullptr, p, b_out); }
+  return hipGetLastError();
+}
+
+__global__ void ctx_dense_kernel(BandCtx c, int64_t n) {
+  CtxHeader h;
+  h.mode = 1;
+  h.nblocks = c.nblocks;
+  h.chunk = c.chunk;
+  h.cap = c.cap;
+  h.pad = 0;
+  h.n = n;
+  *c.hdr = h;
+}
+
+hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s) {
+  { ProfScope ps_("ctx_dense", s);
+  hipLaunchKernelGGL(ctx_dense_kernel, dim3(1), dim3(1), 0, s, band, n); }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- backward --
+__global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __restrict__ g,
+                                                             const float* __restrict__ p,
+                                                             int64_t n, BandCtx c,
+                                                             float* __restrict__ gstash,
+                                                             double* __restrict__ partials) {
+  __shared__ double red[2][BW];
+  __shared__ int seg[BW + 1];
+  const int tid = threadIdx.x;
+  const BlockRange br = block_range(n, c.chunk);
+  double F = 0.0, G = 0.0;
+  if (block_dense(c, n)) {
+    for (int64_t i = br.b0 + tid; i < br.b1; i += BT) {
+      const float pv = p[i];
+      const float f = fminf(pv, 1.0f - pv);
+      if (f != 0.0f) {
+        F += static_cast<double>(f);
+        G += static_cast<double>(f) * static_cast<double>(g[i]);
+      }
+    }
+  } else {
+    if (tid == 0) {
+      int acc = 0;
+      const BandBlock& bb = c.blk[blockIdx.x];
+#pragma unroll
+      for (int w = 0; w < BW; ++w) {
+        seg[w] = acc;
+        acc += bb.cnt[w];
+      }
+      seg[BW] = acc;
+    }
+    __syncthreads();
+    const int total = seg[BW];
+    for (int e = tid; e < total; e += BT) {
+      int w = 0;
+#pragma unroll
+      for (int q = 1; q < BW; ++q) w += (e >= seg[q]) ? 1 : 0;
+      const int64_t slot = (static_cast<int64_t>(blockIdx.x) * BW + w) * c.cap + (e - seg[w]);
+      const BandEntry en = c.ent[slot];
+      const float pv = __uint_as_float(en.bits);
+      const float f = fminf(pv, 1.0f - pv);
+      if (f != 0.0f && en.idx >= br.b0 && en.idx < br.b1) {
+        const float gv = g[en.idx];
+        gstash[slot] = gv;
+        F += static_cast<double>(f);
+        G += static_cast<double>(f) * static_cast<double>(gv);
+      }
+    }
+  }
+  F = wave_sum(F);
+  G = wave_sum(G);
+  const int wid = tid / kWave;
+  if (lane_id() == 0) {
+    red[0][wid] = F;
+    red[1][wid] = G;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double fs = 0.0, gs = 0.0;
+#pragma unroll
+    for (int w = 0; w < BW; ++w) {
+      fs += red[0][w];
+      gs += red[1][w];
+    }
+    partials[2 * blockIdx.x] = fs;
+    partials[2 * blockIdx.x + 1] = gs;
+  }
+}
+
+__global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restrict__ g,
+                                                           const float* __restrict__ p,
+                                                           int64_t n, BandCtx c,
+                                                           const float* __restrict__ gstash,
+                                                           const double* __restrict__ coef2,
+                                                           float* __restrict__ grad) {
+  __shared__ BandLds L;
+  const float coef = static_cast<float>(coef2[0]);
+  const float scale = static_cast<float>(coef2[1]);
+  const BlockRange br = block_range(n, c.chunk);
+  if (block_dense(c, n)) {
+    for (int64_t i = br.b0 + threadIdx.x; i < br.b1; i += BT) {
+      const float pv = p[i];
+      const float f = fminf(pv, 1.0f - pv);
+      grad[i] = (f != 0.0f) ? f * scale * (g[i] - coef) : 0.0f;
+    }
+    return;
+  }
+  build_map(c, br.b0, br.b1 - br.b0, L, [&](int, const BandEntry& en, int64_t slot) {
+    const float pv = __uint_as_float(en.bits);
+    const float f = fminf(pv, 1.0f - pv);
+    return (f != 0.0f) ? f * scale * (gstash[slot] - coef) : 0.0f;
+  });
+  write_dense(br.b0, br.b1, L, nullptr, grad);
+}
+
+hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const BandCtx& band,
+                           float* gstash, double* partials, double* coef, double t, float* grad,
+                           hipStream_t s) {
+  { ProfScope ps_("band_vjp_reduce", s);
+  hipLaunchKernelGGL(band_vjp_reduce_kernel, dim3(band.nblocks), dim3(BT), 0, s, g, p, n, band,
+                     gstash, partials); }
+  hipError_t e = launch_vjp_finalize(partials, band.nblocks, t, coef, s);
+  if (e != hipSuccess) return e;
+  { ProfScope ps_("band_vjp_emit", s);
+  hipLaunchKernelGGL(band_vjp_emit_kernel, dim3(band.nblocks), dim3(BT), 0, s, g, p, n, band,
+                     gstash, coef, grad); }
+  return hipGetLastError();
+}
+
+}  // namespace lapsum

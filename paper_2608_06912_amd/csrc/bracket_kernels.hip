@@ -233,6 +233,15 @@ struct PartState {
   int64_t nL, nR;
   int64_t nM;   // M count of this wave (uniform across the wave)
   float mmin, mmax;
+  int64_t nB;   // band count of this wave (uniform across the wave)
+};
+
+// Where a wave stages its band members.
+struct BandWave {
+  BandEntry* out;    // this wave's segment
+  int cap;
+  float lo, hi;      // band: lo <= r < hi
+  uint32_t* ones;    // bit set where r >= hi (used when a_R is finite)
 };
 
 // Classify 4 consecutive scores of one lane (the slow path of the gather);
@@ -266,16 +275,21 @@ __device__ __forceinline__ void classify4(const float (&v)[4], const bool (&ok)[
 constexpr int kWaveStage = kPartStageCap / PW;   // M entries staged per wave
 
 // Per-wave pass over [w0, w1): tails in float32 over one float4 and float64
-// across, R counted only when a_R is finite (HAS_R), M members staged in
-// index order.  L is not counted: n_L = scores - n_M - n_R.
+// across, R counted only when a_R is finite (HAS_R), band members and M
+// members (a subset of the band) staged in index order, and with a finite
+// a_R one bit per score for r >= hi.  L is not counted:
+// n_L = scores - n_M - n_R.
 template <bool HAS_R>
 __device__ __forceinline__ void partition_range(const float* __restrict__ r, int64_t w0, int64_t w1,
                                                 bool vec, float aL, float aR, float c2f,
-                                                float* sv, int32_t* si, PartState& st) {
+                                                float* sv, int32_t* si, const BandWave& bw,
+                                                PartState& st) {
   const int lane = lane_id();
-  auto one = [&](const float (&v)[4], const bool (&ok)[4], int64_t i0) {
+  // it: first score of this wave's 256-score step (a multiple of 256)
+  auto one = [&](const float (&v)[4], const bool (&ok)[4], int64_t it) {
+    const int64_t i0 = it + 4 * lane;
     float tl = 0.0f, tr = 0.0f;
-    uint32_t mb = 0;
+    uint32_t mb = 0, bb = 0, ob = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const bool L = v[e] < aL;
@@ -285,12 +299,47 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
         tr += (ok[e] && R) ? exp2_fast((aR - v[e]) * c2f) : 0.0f;
         st.nR += (ok[e] && R) ? 1 : 0;
         if (ok[e] && !L && !R) mb |= 1u << e;
+        if (ok[e] && v[e] >= bw.hi) ob |= 1u << e;
+        if (ok[e] && !(v[e] < bw.lo) && !(v[e] >= bw.hi)) bb |= 1u << e;
       } else {
         if (ok[e] && !L) mb |= 1u << e;
+        if (ok[e] && !(v[e] < bw.lo)) bb |= 1u << e;
       }
     }
     st.TL += static_cast<double>(tl);
-    if constexpr (HAS_R) st.TR += static_cast<double>(tr);
+    if constexpr (HAS_R) {
+      st.TR += static_cast<double>(tr);
+      // 8 lanes hold the 32 bits of one word
+      uint32_t x = ob << (4 * (lane & 7));
+      x |= __shfl_xor(x, 1, kWave);
+      x |= __shfl_xor(x, 2, kWave);
+      x |= __shfl_xor(x, 4, kWave);
+      if ((lane & 7) == 0 && it + 32 * (lane >> 3) < w1) bw.ones[(it >> 5) + (lane >> 3)] = x;
+    }
+    if (!__ballot(bb != 0u)) return;   // no lane holds a band member
+    {
+      uint32_t before = 0, total = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint64_t bal = __ballot((bb >> e) & 1u);
+        before += lanes_below(bal);
+        total += static_cast<uint32_t>(__popcll(bal));
+      }
+      int64_t slot = st.nB + before;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if ((bb >> e) & 1u) {
+          if (slot < bw.cap) {
+            BandEntry en;
+            en.idx = static_cast<int32_t>(i0 + e);
+            en.bits = __float_as_uint(v[e]);
+            bw.out[slot] = en;
+          }
+          ++slot;
+        }
+      }
+      st.nB += total;
+    }
     if (__ballot(mb != 0u)) {   // rare: some lane holds an M member
       uint32_t before = 0, total = 0;
 #pragma unroll
@@ -334,7 +383,7 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       for (int u = 0; u < U; ++u) {
         const float v[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
         const bool ok[4] = {true, true, true, true};
-        one(v, ok, cur + u * 256 + 4 * lane);
+        one(v, ok, cur + u * 256);
       }
       if (!more) break;
 #pragma unroll
@@ -350,7 +399,7 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       ok[e] = (i0 + e) < w1;
       v[e] = ok[e] ? r[i0 + e] : 0.0f;
     }
-    one(v, ok, i0);
+    one(v, ok, it);
   }
 }
 
@@ -367,12 +416,16 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
                                                        float c2f, int64_t chunk,
                                                        float* __restrict__ stage_v,
                                                        int32_t* __restrict__ stage_i,
-                                                       PartBlock* __restrict__ blk) {
+                                                       PartBlock* __restrict__ blk, double t,
+                                                       BandEntry* __restrict__ bent,
+                                                       BandBlock* __restrict__ bblk, int bcap,
+                                                       uint32_t* __restrict__ ones) {
   __shared__ float sv[PW][kWaveStage];
   __shared__ int32_t si[PW][kWaveStage];
   __shared__ double red_d[2][PW];
   __shared__ int64_t red_i[2][PW];
   __shared__ float red_f[2][PW];
+  __shared__ int64_t red_b[PW];
   const float aL = use_sel ? sel->aL : aL_arg;
   const float aR = use_sel ? sel->aR : aR_arg;
   const int tid = threadIdx.x;
@@ -383,11 +436,22 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   const int64_t w0 = b0 + wid * wq < n ? b0 + wid * wq : n;
   const int64_t w1 = w0 + wq < n ? w0 + wq : n;
   const bool vec = (reinterpret_cast<uintptr_t>(r) & 15) == 0;
-  PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY};
+  BandWave bw;
+  bw.out = bent + (static_cast<int64_t>(blockIdx.x) * PW + wid) * bcap;
+  bw.cap = bcap;
+  // rounded outwards so that the float comparisons imply the float64 bounds
+  bw.lo = __double2float_rd(static_cast<double>(aL) - kBandLowT * t);
+  bw.hi = __double2float_ru(static_cast<double>(aR) + kBandHighT * t);
+  bw.ones = ones;
+  PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY, 0};
   if (aR < INFINITY)
-    partition_range<true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], st);
+    partition_range<true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
   else
-    partition_range<false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], st);
+    partition_range<false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
+  if (lane == 0) {
+    bblk[blockIdx.x].cnt[wid] = static_cast<int32_t>(st.nB);
+    red_b[wid] = st.nB;
+  }
 
   const double TL = wave_sum(st.TL);
   const double TR = wave_sum(st.TR);
@@ -450,17 +514,63 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
     rec.overflow = over ? 1 : 0;
     rec.pad = 0;
     blk[blockIdx.x] = rec;
+    bool bover = b1 - b0 > kBandMaxChunk;
+#pragma unroll
+    for (int w = 0; w < PW; ++w) bover |= red_b[w] > bcap;
+    bblk[blockIdx.x].dense = bover ? 1 : 0;
   }
 }
 
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
                             float aR, double t, int nblocks, int64_t chunk, float* stage_v,
-                            int32_t* stage_i, PartBlock* blk, hipStream_t s) {
+                            int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
+                            hipStream_t s) {
+  if (band.nblocks != nblocks || band.chunk != chunk) return hipErrorInvalidValue;
   const float c2f = static_cast<float>(kLog2e / t);
   { ProfScope ps_("partition", s);
   hipLaunchKernelGGL(partition_kernel, dim3(nblocks), dim3(PT), 0, s, r, n, sel, use_sel, aL, aR,
-                     c2f, chunk, stage_v, stage_i, blk); }
+                     c2f, chunk, stage_v, stage_i, blk, t, band.ent, band.blk, band.cap, ones); }
   return hipGetLastError();
+}
+
+int band_wave_cap(int64_t chunk) {
+  const int64_t q = chunk / PW;
+  return static_cast<int>(q < kBandWaveCapMax ? q : kBandWaveCapMax);
+}
+
+namespace {
+// Layout of one row's context: header, block records, entries.
+struct CtxLayout {
+  int nblocks;
+  int64_t chunk;
+  int cap;
+  size_t blk_off, ent_off, bytes;
+};
+CtxLayout ctx_layout(int64_t n) {
+  CtxLayout L{};
+  L.nblocks = partition_blocks(n, &L.chunk);
+  L.cap = band_wave_cap(L.chunk);
+  L.blk_off = 256;
+  L.ent_off = L.blk_off + (static_cast<size_t>(L.nblocks) * sizeof(BandBlock) + 255) / 256 * 256;
+  L.bytes = (L.ent_off + static_cast<size_t>(L.nblocks) * PW * L.cap * sizeof(BandEntry) + 255) /
+            256 * 256;
+  return L;
+}
+}  // namespace
+
+size_t band_ctx_bytes(int64_t n) { return ctx_layout(n).bytes; }
+
+BandCtx band_ctx_view(void* base, int64_t n) {
+  const CtxLayout L = ctx_layout(n);
+  BandCtx v{};
+  v.nblocks = L.nblocks;
+  v.chunk = L.chunk;
+  v.cap = L.cap;
+  char* b = static_cast<char*>(base);
+  v.hdr = reinterpret_cast<CtxHeader*>(b);
+  v.blk = b ? reinterpret_cast<BandBlock*>(b + L.blk_off) : nullptr;
+  v.ent = b ? reinterpret_cast<BandEntry*>(b + L.ent_off) : nullptr;
+  return v;
 }
 
 // One workgroup: totals over the partition blocks in a fixed order, and the
@@ -607,7 +717,7 @@ __global__ __launch_bounds__(PT) void gather_kernel(const float* __restrict__ r,
   const int64_t b0 = static_cast<int64_t>(b) * chunk;
   int64_t b1 = b0 + chunk;
   if (b1 > n) b1 = n;
-  PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY};
+  PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY, 0};
   auto put = [&](int64_t slot, float v, int64_t gi) {
     m_keys[off + slot] = desc_key(v);
     m_idx[off + slot] = static_cast<int32_t>(gi);

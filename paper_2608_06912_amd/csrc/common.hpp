@@ -365,6 +365,10 @@ __device__ double block_solve(const float (&s)[ITEMS], int cnt, double rank0, Pr
 // and the exponential in float32.
 __device__ __forceinline__ float laplace_p(float r, double b, double inv_t) {
   const float u = static_cast<float>((static_cast<double>(r) - b) * inv_t);
+  // beyond these the float32 result is exactly 0 or 1 anyway; stating it
+  // makes the band bounds of a bracket exact by construction
+  if (u < -104.0f) return 0.0f;
+  if (u > 17.0f) return 1.0f;
   const float e = exp2_fast(-fabsf(u) * static_cast<float>(kLog2e));
   return (u <= 0.0f) ? 0.5f * e : 1.0f - 0.5f * e;
 }

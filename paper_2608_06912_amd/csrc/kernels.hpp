@@ -48,6 +48,49 @@ struct PartTotals {
   int32_t pad;
 };
 
+// Band of a bracket: the scores whose p depends on where b falls inside a
+// certified bracket [a_L, a_R].  With lo = a_L - 105 t (rounded down to
+// float32) and hi = a_R + 18 t (rounded up), every score below lo has
+// (r - b)/t < -104 and p exactly 0 in float32, and every score at or above
+// hi has (r - b)/t > 17 and p exactly 1, for any b in the bracket.  The
+// partition stages the band in index order, the emit then writes p without
+// re-reading r, and the backward visits only the band.
+constexpr double kBandLowT = 105.0;
+constexpr double kBandHighT = 18.0;
+constexpr int kBandWaveCapMax = 512;        // band entries a partition wave stages
+constexpr int64_t kBandMaxChunk = 65536;    // longer block ranges take the dense passes
+
+struct alignas(8) BandEntry {
+  int32_t idx;     // index in the row
+  uint32_t bits;   // float32 score after the partition, p after the emit
+};
+
+// Per partition block.
+struct BandBlock {
+  int32_t cnt[4];   // band members met by each wave (can exceed the capacity)
+  int32_t dense;    // 1: the lists of this block are incomplete; passes read it densely
+  int32_t pad[3];
+};
+
+// Saved band of one row (the forward's context for the backward).
+struct CtxHeader {
+  int32_t mode;     // 0: band lists valid; 1: no lists, every pass is dense
+  int32_t nblocks;
+  int64_t chunk;
+  int32_t cap;      // entries per wave segment
+  int32_t pad;
+  int64_t n;
+};
+
+struct BandCtx {
+  CtxHeader* hdr;
+  BandBlock* blk;    // [nblocks]
+  BandEntry* ent;    // [nblocks][4][cap]
+  int nblocks;
+  int64_t chunk;
+  int cap;
+};
+
 // Order statistics of the noised sample.
 struct SelectRec {
   float aL, aR;
@@ -83,6 +126,10 @@ hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t,
 int vjp_reduce_blocks(int64_t n);
 hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
                              int nblocks, double t, double* coef, hipStream_t s);
+// coef[0] = sum f g / sum f, coef[1] = 1/t (both 0 when sum f == 0) from
+// nparts (sum f, sum f g) pairs, summed in a fixed order.
+hipError_t launch_vjp_finalize(const double* partials, int nparts, double t, double* coef,
+                               hipStream_t s);
 hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* coef,
                            float* grad, hipStream_t s);
 
@@ -133,9 +180,28 @@ hipError_t launch_sample(const float* r, int64_t n, const float* noise, int64_t 
 hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* hist, int64_t j,
                          int64_t l, SelectRec* out, hipStream_t s);
 int partition_blocks(int64_t n, int64_t* chunk);
+int band_wave_cap(int64_t chunk);
+// Bytes of one row's context and its layout at `base` (null base: sizes only).
+size_t band_ctx_bytes(int64_t n);
+BandCtx band_ctx_view(void* base, int64_t n);
+// ones: [ceil(n/32)] bit set where r >= hi (written only when a_R is finite).
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
                             float aR, double t, int nblocks, int64_t chunk, float* stage_v,
-                            int32_t* stage_i, PartBlock* blk, hipStream_t s);
+                            int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
+                            hipStream_t s);
+// Emit after a certified bracket (skipped when rec->ok == 0): p from the band
+// lists and the ones bits, dense from r for blocks without usable lists; the
+// band entries get p in place; b_out[0] = rec->b; the context header is set.
+hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, double t,
+                            const BandCtx& band, const uint32_t* ones, int has_ones, float* p,
+                            double* b_out, hipStream_t s);
+// Mark a context as dense (rows solved by the full sort).
+hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s);
+// Backward from a saved band: partial (sum f, sum f g) per block, the
+// fixed-order finalize, then grad_r written densely (zero outside the band).
+hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const BandCtx& band,
+                           float* gstash, double* partials, double* coef, double t, float* grad,
+                           hipStream_t s);
 hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const SelectRec* sel,
                                    int use_sel, float aL, float aR, int64_t* offsets,
                                    PartTotals* tot, hipStream_t s);

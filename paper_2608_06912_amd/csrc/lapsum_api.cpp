@@ -185,6 +185,8 @@ struct BracketWs {
   double* m_tile_buf;
   SolveRec* rec;
   FullWs fall;         // full-sort fallback
+  uint32_t* ones;      // [ceil(n/32)] scores at or above the band (finite a_R)
+  void* band;          // one row's band when the caller keeps none
   int nblocks;
   int64_t chunk;
 };
@@ -217,6 +219,8 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
   }
   w.rec = c.take<SolveRec>(1);
   if (n > kRowOnChipMax) w.fall = carve_full(c, n, false);
+  w.ones = c.take<uint32_t>(static_cast<size_t>((n + 31) / 32));
+  w.band = c.take<char>(band_ctx_bytes(n));
   return w;
 }
 
@@ -271,17 +275,52 @@ void widen(float* aL, float* aR, int side) {
   }
 }
 
-template <typename T>
-int read_back(T* host, const T* dev, hipStream_t s) {
-  if (hipMemcpyAsync(host, dev, sizeof(T), hipMemcpyDeviceToHost, s) != hipSuccess) return LAPSUM_ERR_HIP;
-  if (hipStreamSynchronize(s) != hipSuccess) return LAPSUM_ERR_HIP;
+// Pinned host records the bracketed path reads back (one set per host
+// thread, allocated on its first use and kept), and the event that tells
+// the host a copy has landed while later work proceeds on the stream.
+struct HostStage {
+  PartTotals tot;
+  SolveRec rec;
+};
+struct ThreadStage {
+  HostStage* h = nullptr;
+  hipEvent_t ev = nullptr;
+};
+thread_local ThreadStage t_stage;
+
+int host_stage(HostStage** h, hipEvent_t* ev) {
+  if (!t_stage.h) {
+    void* ptr = nullptr;
+    if (hipHostMalloc(&ptr, sizeof(HostStage), hipHostMallocPortable) != hipSuccess)
+      return LAPSUM_ERR_HIP;
+    t_stage.h = static_cast<HostStage*>(ptr);
+  }
+  if (!t_stage.ev) {
+    if (hipEventCreateWithFlags(&t_stage.ev, hipEventDisableTiming) != hipSuccess)
+      return LAPSUM_ERR_HIP;
+  }
+  *h = t_stage.h;
+  *ev = t_stage.ev;
   return LAPSUM_OK;
+}
+
+// Copy one record to pinned host memory and mark it with the event; the
+// caller may enqueue more work before waiting.
+template <typename T>
+int copy_back(T* host, const T* dev, hipEvent_t ev, hipStream_t s) {
+  if (hipMemcpyAsync(host, dev, sizeof(T), hipMemcpyDeviceToHost, s) != hipSuccess) return LAPSUM_ERR_HIP;
+  if (hipEventRecord(ev, s) != hipSuccess) return LAPSUM_ERR_HIP;
+  return LAPSUM_OK;
+}
+
+int wait_back(hipEvent_t ev) {
+  return hipEventSynchronize(ev) == hipSuccess ? LAPSUM_OK : LAPSUM_ERR_HIP;
 }
 
 int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, double z,
                   const float* noise, int64_t mcap, int64_t out_cap, uint32_t flags, float* p_row,
-                  double* b_row,
-                  lapsum_bracket_info* info, int32_t* midx_row, BracketWs& w, hipStream_t s) {
+                  double* b_row, lapsum_bracket_info* info, int32_t* midx_row, void* band_row,
+                  BracketWs& w, hipStream_t s) {
   const double t = -alpha;
   lapsum_bracket_info rec_info;
   memset(&rec_info, 0, sizeof(rec_info));
@@ -291,6 +330,11 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
   rec_info.l = l;
   bool solved = false;
   bool wrote_midx = false;
+  const BandCtx band = band_ctx_view(band_row ? band_row : w.band, n);
+  HostStage* hs = nullptr;
+  hipEvent_t ev = nullptr;
+  int st = host_stage(&hs, &ev);
+  if (st != LAPSUM_OK) return st;
 
   if (!(flags & LAPSUM_FLAG_FULL_SORT)) {
     LAPSUM_TRY(launch_fill_u32(w.hist, kSelectBins, 0u, s));
@@ -300,13 +344,14 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
     for (int attempt = 1; attempt <= 3 && !solved; ++attempt) {
       const int use_sel = attempt == 1 ? 1 : 0;
       LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR, t, w.nblocks, w.chunk, w.stage_v,
-                                  w.stage_i, w.blk, s));
+                                  w.stage_i, w.blk, band, w.ones, s));
       LAPSUM_TRY(launch_partition_totals(w.blk, w.nblocks, w.sel, use_sel, aL, aR, w.offsets, w.tot, s));
       LAPSUM_TRY(launch_gather(r, n, w.tot, w.blk, w.offsets, w.nblocks, w.chunk, w.stage_v,
                                w.stage_i, mcap, w.m_keys, w.m_idx, s));
-      PartTotals tot;
-      int st = read_back(&tot, w.tot, s);
+      st = copy_back(&hs->tot, w.tot, ev, s);
+      if (st == LAPSUM_OK) st = wait_back(ev);
       if (st != LAPSUM_OK) return st;
+      const PartTotals tot = hs->tot;
       aL = tot.aL;
       aR = tot.aR;
       rec_info.attempts = attempt;
@@ -350,13 +395,18 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
         LAPSUM_TRY(launch_sorted_solve(a, s));
         sorted_idx = want_idx ? mv : nullptr;
       }
-      SolveRec rec;
-      st = read_back(&rec, w.rec, s);
+      // the record goes back to the host while the emit runs; the emit (and
+      // its write of b) happens only if this bracket was certified
+      st = copy_back(&hs->rec, w.rec, ev, s);
       if (st != LAPSUM_OK) return st;
+      LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, tot.aR < INFINITY ? 1 : 0, p_row,
+                                  b_row, s));
+      st = wait_back(ev);
+      if (st != LAPSUM_OK) return st;
+      const SolveRec rec = hs->rec;
       rec_info.lap_aL = rec.lap_aL;
       rec_info.lap_aR = rec.lap_aR;
       if (rec.ok) {
-        LAPSUM_TRY(hipMemcpyAsync(b_row, &w.rec->b, sizeof(double), hipMemcpyDeviceToDevice, s));
         if (want_idx) {
           LAPSUM_TRY(launch_write_m_idx(sorted_idx, tot.nM, out_cap, midx_row, s));
           wrote_midx = true;
@@ -373,12 +423,11 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
       // the on-chip kernel also emits p
       LAPSUM_TRY(launch_row_forward(r, 1, n, k, t, p_row, b_row, nullptr, s));
     } else {
-      int st = full_row_solve(r, n, k, t, b_row, nullptr, w.fall, s);
+      st = full_row_solve(r, n, k, t, b_row, nullptr, w.fall, s);
       if (st != LAPSUM_OK) return st;
       LAPSUM_TRY(launch_emit(r, n, b_row, t, p_row, s));
     }
-  } else {
-    LAPSUM_TRY(launch_emit(r, n, b_row, t, p_row, s));
+    LAPSUM_TRY(launch_ctx_dense(band, n, s));
   }
   if (midx_row && !wrote_midx) LAPSUM_TRY(launch_write_m_idx(nullptr, 0, out_cap, midx_row, s));
   if (info) *info = rec_info;
@@ -514,13 +563,20 @@ size_t lapsum_forward_bracketed_workspace_size(int64_t batch, int64_t n, int64_t
   return bracketed_ws(n, K, m_capacity < n ? m_capacity : n, with_m_idx != 0);
 }
 
+size_t lapsum_band_size(int64_t batch, int64_t n) {
+  if (batch < 1 || n < 1 || n > 2147483647LL) return 0;
+  return static_cast<size_t>(batch) * band_ctx_bytes(n);
+}
+
 int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n, double k, double alpha,
                              int64_t K, double z, const float* noise, int64_t m_capacity,
                              uint32_t flags, float* p, double* b, lapsum_bracket_info* info,
-                             int32_t* m_idx_out, void* workspace, size_t workspace_bytes,
-                             hipStream_t stream) {
+                             int32_t* m_idx_out, void* band, size_t band_bytes, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
   if (!scores || !p || !b || !noise || !valid_common(batch, n, k, alpha)) return LAPSUM_ERR_INVALID_ARG;
   if (K < 2 || K > n || !isfinite(z) || !(z > 0.0) || m_capacity < 1 || (flags & ~LAPSUM_FLAG_FULL_SORT))
+    return LAPSUM_ERR_INVALID_ARG;
+  if (band && (band_bytes < lapsum_band_size(batch, n) || reinterpret_cast<uintptr_t>(band) % kAlign))
     return LAPSUM_ERR_INVALID_ARG;
   // |M| <= n always, so capacity beyond n is never used internally; the
   // caller's m_idx_out rows keep their m_capacity stride.
@@ -531,11 +587,54 @@ int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n, doub
   if (dst != LAPSUM_OK) return dst;
   Carve c(workspace);
   BracketWs w = carve_bracket(c, n, K, mcap, m_idx_out != nullptr);
+  const size_t band_row_bytes = band_ctx_bytes(n);
   for (int64_t row = 0; row < batch; ++row) {
+    void* band_row = band ? static_cast<char*>(band) + row * band_row_bytes : nullptr;
     int st = bracketed_row(scores + row * n, n, k, alpha, K, z, noise, mcap, m_capacity, flags,
                            p + row * n, b + row, info ? info + row : nullptr,
-                           m_idx_out ? m_idx_out + row * m_capacity : nullptr, w, stream);
+                           m_idx_out ? m_idx_out + row * m_capacity : nullptr, band_row, w, stream);
     if (st != LAPSUM_OK) return st;
+  }
+  return LAPSUM_OK;
+}
+
+size_t lapsum_backward_band_workspace_size(int64_t batch, int64_t n) {
+  (void)batch;
+  if (n < 1 || n > 2147483647LL) return 0;
+  const BandCtx v = band_ctx_view(nullptr, n);
+  Carve c(nullptr);
+  c.take<double>(2 * static_cast<size_t>(v.nblocks));
+  c.take<double>(2);
+  c.take<float>(static_cast<size_t>(v.nblocks) * 4 * v.cap);
+  return c.size();
+}
+
+int lapsum_backward_band(const float* grad_p, const float* p, const void* band, size_t band_bytes,
+                         int64_t batch, int64_t n, double alpha, float* grad_r, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+  if (!grad_p || !p || !band || !grad_r) return LAPSUM_ERR_INVALID_ARG;
+  if (batch < 1 || n < 1 || n > 2147483647LL || !isfinite(alpha) || !(alpha < 0.0))
+    return LAPSUM_ERR_INVALID_ARG;
+  if (band_bytes < lapsum_band_size(batch, n) || reinterpret_cast<uintptr_t>(band) % kAlign)
+    return LAPSUM_ERR_INVALID_ARG;
+  const int wst = check_ws(workspace, workspace_bytes, lapsum_backward_band_workspace_size(batch, n));
+  if (wst != LAPSUM_OK) return wst;
+  const int dst = check_device();
+  if (dst != LAPSUM_OK) return dst;
+  const double t = -alpha;
+  const BandCtx v0 = band_ctx_view(nullptr, n);
+  Carve c(workspace);
+  double* partials = c.take<double>(2 * static_cast<size_t>(v0.nblocks));
+  double* coef = c.take<double>(2);
+  float* gstash = c.take<float>(static_cast<size_t>(v0.nblocks) * 4 * v0.cap);
+  const size_t band_row_bytes = band_ctx_bytes(n);
+  for (int64_t row = 0; row < batch; ++row) {
+    const int64_t o = row * n;
+    // the kernels only read the band
+    void* band_row = const_cast<char*>(static_cast<const char*>(band)) + row * band_row_bytes;
+    const BandCtx v = band_ctx_view(band_row, n);
+    LAPSUM_TRY(launch_band_vjp(grad_p + o, p + o, n, v, gstash, partials, coef, t, grad_r + o,
+                               stream));
   }
   return LAPSUM_OK;
 }

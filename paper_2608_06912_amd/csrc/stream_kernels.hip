@@ -217,15 +217,22 @@ __global__ __launch_bounds__(1024) void vjp_finalize_kernel(const double* __rest
   }
 }
 
+hipError_t launch_vjp_finalize(const double* partials, int nparts, double t, double* coef,
+                               hipStream_t s) {
+  { ProfScope ps_("vjp_finalize", s);
+  hipLaunchKernelGGL(vjp_finalize_kernel, dim3(1), dim3(1024), 0, s, partials, nparts, 1.0 / t,
+                     coef); }
+  return hipGetLastError();
+}
+
 hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
                              int nblocks, double t, double* coef, hipStream_t s) {
   { ProfScope ps_("vjp_reduce", s);
   hipLaunchKernelGGL(vjp_reduce_kernel, dim3(nblocks), dim3(kStreamThreads), 0, s, g, p, n,
                      partials); }
-  { ProfScope ps_("vjp_finalize", s);
-  hipLaunchKernelGGL(vjp_finalize_kernel, dim3(1), dim3(1024), 0, s, partials, nblocks, 1.0 / t,
-                     coef); }
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_vjp_finalize(partials, nblocks, t, coef, s);
 }
 
 // -------------------------------------------------------------- vjp emit ---

@@ -26,7 +26,8 @@ def test_header_declares_the_entry_points():
     names = _declared()
     for want in ("lapsum_forward", "lapsum_backward", "lapsum_forward_bracketed",
                  "lapsum_forward_workspace_size", "lapsum_backward_workspace_size",
-                 "lapsum_forward_bracketed_workspace_size", "lapsum_status_string"):
+                 "lapsum_forward_bracketed_workspace_size", "lapsum_status_string",
+                 "lapsum_band_size", "lapsum_backward_band", "lapsum_backward_band_workspace_size"):
         assert want in names
 
 
@@ -107,5 +108,42 @@ def test_bracketed_rejects_invalid_arguments(kw):
     a.update(kw)
     st = lib.lapsum_forward_bracketed(v(1), 1, 1000, a["k"], -1.0, a["K"], a["z"], v(a["noise"]),
                                       a["m_capacity"], a["flags"], v(1), v(1), v(0), v(0), v(0),
-                                      0, v(0))
+                                      0, v(0), 0, v(0))
     assert st == 1
+
+
+def test_bracketed_rejects_a_short_or_misaligned_band():
+    lib = L.load()
+    v = ctypes.c_void_p
+    need = L.lapsum_band_size(1, 1000)
+    for ptr, size in ((256, need - 1), (128, need)):
+        st = lib.lapsum_forward_bracketed(v(1), 1, 1000, 10.0, -1.0, 100, 5.16, v(1), 64, 0, v(1),
+                                          v(1), v(0), v(0), v(ptr), size, v(0), 0, v(0))
+        assert st == 1
+
+
+def test_band_sizes():
+    # header + block records + four lists of at most 512 entries per block
+    one = L.lapsum_band_size(1, 10**8)
+    assert 8 * 10**8 * 0.08 < one < 8 * 10**8 * 0.09
+    assert L.lapsum_band_size(3, 10**6) == 3 * L.lapsum_band_size(1, 10**6)
+    assert L.lapsum_band_size(1, 1000) % 256 == 0
+    assert L.lapsum_band_size(0, 1000) == 0
+    # lists never hold more entries than the row has scores (small rows)
+    assert L.lapsum_band_size(1, 4096) < 8 * 4096 + 4096
+    assert L.lapsum_backward_band_workspace_size(1, 10**8) > 0
+
+
+def test_backward_band_rejects_invalid_arguments():
+    lib = L.load()
+    v = ctypes.c_void_p
+    need = L.lapsum_band_size(1, 1000)
+    ws = L.lapsum_backward_band_workspace_size(1, 1000)
+    args = lambda band, bb, alpha=-1.0, wsp=256, wsb=ws: lib.lapsum_backward_band(
+        v(1), v(1), v(band), bb, 1, 1000, alpha, v(1), v(wsp), wsb, v(0))
+    assert args(0, need) == 1            # no band
+    assert args(256, need - 1) == 1      # band too small
+    assert args(128, need) == 1          # misaligned
+    assert args(256, need, alpha=1.0) == 1
+    assert args(256, need, wsp=0) == 2   # workspace missing
+    assert args(256, need, wsb=ws - 1) == 2

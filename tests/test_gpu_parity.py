@@ -151,10 +151,14 @@ def test_devicewide_backward(lib, n, alpha):
 
 
 # -------------------------------------------------------------- bracketed --
-def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label=""):
+def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label="", g=None):
+    """Bracketed forward (with a saved band) against the oracle's bracketed
+    model; with an upstream gradient g also the backward from the band,
+    against Eq. (5) and against the p-form backward."""
     import torch
+    band = lib.new_band(1, len(r32), "cuda")
     p, b, infos, midx = lib.lapsum_forward_bracketed(_t(r32[None, :]), k, alpha, _t(noise), z=z,
-                                                     m_capacity=m_capacity, m_idx=True)
+                                                     m_capacity=m_capacity, m_idx=True, band=band)
     info = infos[0]
     po, bo, oinfo, oms = O.bracketed_forward(r32, k, alpha, noise, z=z,
                                              m_capacity=m_capacity or len(r32))
@@ -188,6 +192,14 @@ def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label="
         assert np.all(m[nm:] == -1)
     else:
         assert np.all(m == -1)
+    if g is not None:
+        gt = _t(g[None, :])
+        gb = _np(lib.lapsum_backward_band(gt, p, band, alpha))[0]
+        gp = _np(lib.lapsum_backward(gt, p, b, alpha))[0]
+        assert grad_rel(gb, O.vjp(r32, bo, alpha, g)) <= G_TOL, (label, "band backward")
+        # same f from the same p; only the summation order differs
+        assert grad_rel(gb, gp.astype(np.float64)) <= 1e-6, (label, "band vs p-form")
+        assert np.all(gb[gp == 0.0] == 0.0), label
     return _np(p)[0], b_gpu, bo, info
 
 
@@ -198,7 +210,8 @@ def test_bracketed_small_matches_oracle(lib, case):
     r = W.random_case(case, n, dist=dists[case])[0]
     k, alpha, K = n / 16.0, -1.0, W.default_sample_size(n)
     noise = W.laplace_noise([77, case], K, 1.0)
-    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=dists[case])
+    g = W.random_case(100 + case, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=dists[case], g=g)
     p_ref = O.probs(r, bo, alpha)
     assert np.max(np.abs(p.astype(np.float64) - p_ref)) <= P_TOL
     assert O.budget_error(p, k) <= sum_tol(k)
@@ -209,7 +222,8 @@ def test_bracketed_forced_widening_and_fallback(lib, shift):
     n, k, alpha, K = 20000, 1250.0, -0.5, 737
     r = W.random_case(4, n, dist="normal")[0]
     noise = W.laplace_noise([56], K, 0.5) + np.float32(shift)
-    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=f"shift {shift}")
+    g = W.random_case(57, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=f"shift {shift}", g=g)
     assert info["attempts"] == 3
 
 
@@ -217,7 +231,8 @@ def test_bracketed_overflow_and_flag(lib):
     n, k, alpha, K = 20000, 1250.0, -0.5, 737
     r = W.random_case(4, n, dist="normal")[0]
     noise = W.laplace_noise([56], K, 0.5)
-    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, m_capacity=10, label="overflow")
+    g = W.random_case(58, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, m_capacity=10, label="overflow", g=g)
     assert info["m_overflow"] == 1 and info["fell_back"] == 1
     p2, b2, infos, _ = lib.lapsum_forward_bracketed(_t(r[None, :]), k, alpha, _t(noise),
                                                     flags=lib.LAPSUM_FLAG_FULL_SORT)
@@ -237,6 +252,59 @@ def test_bracketed_large_middle_set(lib):
     assert info["n_M"] > 32768 and not info["fell_back"]
     idx = np.random.default_rng(0).integers(0, n, 20000)
     assert np.max(np.abs(p[idx].astype(np.float64) - O.probs(r[idx], bo, alpha))) <= P_TOL
+
+
+def test_bracketed_band_with_scores_above_it(lib):
+    # k = n/3 puts a_R inside the sample, so scores at or above a_R + 18 t
+    # are written as 1 from their bits; a ragged length exercises the last
+    # partial word and the scalar tail of the last block
+    n = 300_007
+    r = W.random_case(21, n, dist="normal", ties=0.01)[0]
+    k, alpha = n / 3.0, -0.002
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([79], K, 0.002)
+    g = W.random_case(22, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label="ones", g=g)
+    assert math.isfinite(info["a_R"]) and info["n_R"] > 0 and not info["fell_back"]
+    p_ref = O.probs(r, bo, alpha)
+    assert np.max(np.abs(p.astype(np.float64) - p_ref)) <= P_TOL
+    assert np.count_nonzero(p == 1.0) > n // 4
+    assert O.budget_error(p, k) <= sum_tol(k)
+
+
+@pytest.mark.timeout(300)
+def test_bracketed_band_too_wide_for_the_lists(lib):
+    # a temperature wide compared with the score spread puts every score in
+    # the band: every block overflows its lists and takes the dense passes
+    # (lists hold 512 entries per wave; rows above 4096 x 2048 scores give a
+    # wave more scores than that)
+    n = 9_000_011
+    r = W.random_case(23, n, dist="normal")[0]
+    k, alpha = n / 4.0, -2.0
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([80], K, 2.0)
+    g = W.random_case(24, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label="wide band", g=g)
+    assert not info["fell_back"]
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
+
+
+def test_backward_band_saved_for_another_length(lib):
+    # a band whose header names another row length is not used: the
+    # backward takes the dense form from p
+    n1, n2 = 120_000, 100_000
+    r1 = W.random_case(25, n1, dist="normal")[0]
+    r2 = W.random_case(26, n2, dist="normal")[0]
+    alpha = -0.05
+    band = lib.new_band(1, n1, "cuda")
+    lib.lapsum_forward_bracketed(_t(r1[None, :]), 100.0, alpha,
+                                 _t(W.laplace_noise([81], 2000, 0.05)), band=band)
+    p2, b2, _, _ = lib.lapsum_forward_bracketed(_t(r2[None, :]), 50.0, alpha,
+                                                _t(W.laplace_noise([82], 2000, 0.05)))
+    g = W.random_case(27, n2, dist="normal")[0]
+    gb = _np(lib.lapsum_backward_band(_t(g[None, :]), p2, band, alpha))[0]
+    assert lib.lapsum_band_size(1, n2) <= band.numel()
+    assert grad_rel(gb, O.vjp(r2, float(_np(b2)[0]), alpha, g)) <= G_TOL
 
 
 # ----------------------------------------------- the named workloads, full size
@@ -269,7 +337,8 @@ def test_workload_n1e7_bracketed(lib):
     w = W.get("n1e7")
     r = W.scores("n1e7")
     noise = W.bracket_noise("n1e7")
-    p, bg, bo, info = _check_bracketed(lib, r[0], w.k, w.alpha, noise, z=w.z, label="n1e7")
+    g = W.upstream_grad("n1e7")
+    p, bg, bo, info = _check_bracketed(lib, r[0], w.k, w.alpha, noise, z=w.z, label="n1e7", g=g[0])
     assert O.certify_root(r[0], w.k, w.alpha, bo, 1e-7 * w.t)
     assert info["attempts"] == 1 and not info["fell_back"]
     _sampled_p_check(p, r[0], bo, w.alpha)
@@ -286,12 +355,11 @@ def test_workload_n1e8_bracketed(lib):
     w = W.get("n1e8")
     r = W.scores("n1e8")
     noise = W.bracket_noise("n1e8")
-    p, bg, bo, info = _check_bracketed(lib, r[0], w.k, w.alpha, noise, z=w.z, label="n1e8")
+    g = W.upstream_grad("n1e8")
+    # forward with a saved band, then both backwards (from the band, as the
+    # benchmark runs it, and from p)
+    p, bg, bo, info = _check_bracketed(lib, r[0], w.k, w.alpha, noise, z=w.z, label="n1e8",
+                                       g=g[0])
     assert O.certify_root(r[0], w.k, w.alpha, bo, 1e-7 * w.t)
     _sampled_p_check(p, r[0], bo, w.alpha)
     assert O.budget_error(p, w.k) <= sum_tol(w.k)
-    g = W.upstream_grad("n1e8")
-    pt = _t(p[None, :])
-    bt = torch.tensor([bg], dtype=torch.float64, device="cuda")
-    grad = _np(lib.lapsum_backward(_t(g), pt, bt, w.alpha))[0]
-    assert grad_rel(grad, O.vjp(r[0], bo, w.alpha, g[0])) <= G_TOL
