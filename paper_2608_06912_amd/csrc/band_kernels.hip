@@ -139,7 +139,6 @@ __device__ void write_dense(int64_t b0, int64_t b1, const BandLds& L, const uint
   };
   if ((reinterpret_cast<uintptr_t>(out + b0) & 15) == 0) {
     const int64_t n4 = len / 4;
-    float4* o4 = reinterpret_cast<float4*>(out + b0);
     for (int64_t q = tid; q < n4; q += BT) {
       const uint32_t word = L.bits[q >> 3];
       const int sh = static_cast<int>(q & 7) * 4;
@@ -154,7 +153,7 @@ __device__ void write_dense(int64_t b0, int64_t b1, const BandLds& L, const uint
         for (int e = 0; e < 4; ++e)
           if ((nib >> e) & 1u) v[e] = L.vals[rk++];
       }
-      o4[q] = make_float4(v[0], v[1], v[2], v[3]);
+      store_stream4(out + b0 + 4 * q, make_float4(v[0], v[1], v[2], v[3]));
     }
     for (int64_t o = n4 * 4 + tid; o < len; o += BT) out[b0 + o] = value(o);
   } else {
@@ -170,12 +169,10 @@ __device__ void dense_emit(const float* __restrict__ r, int64_t b0, int64_t b1, 
   int64_t i = b0 + tid;
   if (vec) {
     const int64_t n4 = (b1 - b0) / 4;
-    const float4* r4 = reinterpret_cast<const float4*>(r + b0);
-    float4* p4 = reinterpret_cast<float4*>(p + b0);
     for (int64_t q = tid; q < n4; q += BT) {
-      const float4 v = r4[q];
-      p4[q] = make_float4(laplace_p(v.x, b, inv_t), laplace_p(v.y, b, inv_t),
-                          laplace_p(v.z, b, inv_t), laplace_p(v.w, b, inv_t));
+      const float4 v = load_stream4(r + b0 + 4 * q);
+      store_stream4(p + b0 + 4 * q, make_float4(laplace_p(v.x, b, inv_t), laplace_p(v.y, b, inv_t),
+                                                laplace_p(v.z, b, inv_t), laplace_p(v.w, b, inv_t)));
     }
     i = b0 + n4 * 4 + tid;
   }

@@ -9,9 +9,9 @@
 // Digit ranking per pass: the lanes of a wave holding the same digit are
 // found with eight ballots (one per digit bit), giving each lane the number
 // of earlier same-digit lanes; a per-wave LDS counter per digit carries the
-// count across the ITEMS rounds.  An exclusive scan over the counters laid
-// out digit-major, wave-minor then gives every (wave, digit) its first output
-// position, which keeps the order position-stable.
+// count across the ITEMS rounds.  An exclusive scan over the counters in
+// digit-major, wave-minor order then gives every (wave, digit) its first
+// output position, which keeps the order position-stable.
 #pragma once
 
 #include "common.hpp"
@@ -35,14 +35,32 @@ __device__ __forceinline__ uint64_t match_digit8(uint32_t d) {
   return peers;
 }
 
-// In-place exclusive scan of `count` u32 values in LDS, count = 4 * BLOCK.
+// Per-(digit, wave) counters, digit-major.  Each digit's row is padded to an
+// odd stride so that the 64 lanes of a wave, which touch the counters of 64
+// (mostly different) digits of their own wave at once, spread over all LDS
+// banks; with a power-of-two stride they would share very few banks.
+template <int WAVES>
+__device__ __forceinline__ int cnt_at(uint32_t d, int w) {
+  return static_cast<int>(d) * (WAVES + 1) + w;
+}
+template <int WAVES>
+constexpr int cnt_words() { return 256 * (WAVES + 1); }
+
+// In-place exclusive scan, in (digit, wave) order, of the 256 * WAVES
+// counters laid out by cnt_at (4 per thread, BLOCK = 64 * WAVES threads).
 template <int BLOCK>
 __device__ void block_excl_scan_u32x4(uint32_t* a, uint32_t* wave_tot) {
   constexpr int WAVES = BLOCK / kWave;
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
-  uint32_t v0 = a[4 * tid + 0], v1 = a[4 * tid + 1], v2 = a[4 * tid + 2], v3 = a[4 * tid + 3];
+  int at[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int j = 4 * tid + q;
+    at[q] = cnt_at<WAVES>(static_cast<uint32_t>(j / WAVES), j % WAVES);
+  }
+  uint32_t v0 = a[at[0]], v1 = a[at[1]], v2 = a[at[2]], v3 = a[at[3]];
   uint32_t sum = v0 + v1 + v2 + v3;
   uint32_t incl = sum;
 #pragma unroll
@@ -57,23 +75,29 @@ __device__ void block_excl_scan_u32x4(uint32_t* a, uint32_t* wave_tot) {
   for (int w = 0; w < WAVES; ++w)
     if (w < wid) wbase += wave_tot[w];
   uint32_t ex = wbase + incl - sum;
-  a[4 * tid + 0] = ex;
-  a[4 * tid + 1] = ex + v0;
-  a[4 * tid + 2] = ex + v0 + v1;
-  a[4 * tid + 3] = ex + v0 + v1 + v2;
+  a[at[0]] = ex;
+  a[at[1]] = ex + v0;
+  a[at[2]] = ex + v0 + v1;
+  a[at[3]] = ex + v0 + v1 + v2;
   __syncthreads();
 }
 
+// The scatter buffer skips one word after every 32 so that the blocked read
+// of the last pass (lane stride ITEMS words) does not fall into one bank.
+__device__ __forceinline__ int buf_at(int p) { return p + (p >> 5); }
+template <int BLOCK, int ITEMS>
+constexpr int sort_buf_words() { return BLOCK * ITEMS + (BLOCK * ITEMS) / 32; }
+
 template <int BLOCK>
 struct SortSmem {
-  uint32_t cnt[256 * (BLOCK / kWave)];
+  uint32_t cnt[cnt_words<BLOCK / kWave>()];
   uint32_t wave_tot[BLOCK / kWave];
 };
 
 // One LSD pass on bits [shift, shift+8).  On return the keys (and values)
 // are back in registers: wave-striped, or blocked (thread tid holds positions
 // tid*ITEMS .. tid*ITEMS+ITEMS-1) when `blocked_out`.  `buf` holds
-// BLOCK*ITEMS u32.
+// sort_buf_words<BLOCK, ITEMS>() u32.
 template <int BLOCK, int ITEMS, bool PAIRS>
 __device__ void block_sort_pass(uint32_t (&key)[ITEMS], int32_t (&val)[ITEMS], int shift,
                                 uint32_t* buf, SortSmem<BLOCK>& sm, bool blocked_out) {
@@ -81,7 +105,7 @@ __device__ void block_sort_pass(uint32_t (&key)[ITEMS], int32_t (&val)[ITEMS], i
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
-  for (int e = tid; e < 256 * WAVES; e += BLOCK) sm.cnt[e] = 0u;
+  for (int e = tid; e < cnt_words<WAVES>(); e += BLOCK) sm.cnt[e] = 0u;
   __syncthreads();
 
   uint32_t pos[ITEMS];
@@ -90,7 +114,7 @@ __device__ void block_sort_pass(uint32_t (&key)[ITEMS], int32_t (&val)[ITEMS], i
     const uint32_t d = (key[i] >> shift) & 255u;
     const uint64_t peers = match_digit8(d);
     const uint32_t below = lanes_below(peers);
-    uint32_t* slot = &sm.cnt[d * WAVES + wid];
+    uint32_t* slot = &sm.cnt[cnt_at<WAVES>(d, wid)];
     const uint32_t c = *slot;
     pos[i] = c + below;
     if (below == 0u) *slot = c + static_cast<uint32_t>(__popcll(peers));
@@ -98,22 +122,23 @@ __device__ void block_sort_pass(uint32_t (&key)[ITEMS], int32_t (&val)[ITEMS], i
   __syncthreads();
   block_excl_scan_u32x4<BLOCK>(sm.cnt, sm.wave_tot);
 #pragma unroll
-  for (int i = 0; i < ITEMS; ++i) pos[i] += sm.cnt[((key[i] >> shift) & 255u) * WAVES + wid];
+  for (int i = 0; i < ITEMS; ++i) pos[i] += sm.cnt[cnt_at<WAVES>((key[i] >> shift) & 255u, wid)];
 
 #pragma unroll
-  for (int i = 0; i < ITEMS; ++i) buf[pos[i]] = key[i];
+  for (int i = 0; i < ITEMS; ++i) buf[buf_at(static_cast<int>(pos[i]))] = key[i];
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < ITEMS; ++i)
-    key[i] = buf[blocked_out ? tid * ITEMS + i : wid * (kWave * ITEMS) + i * kWave + lane];
+    key[i] = buf[buf_at(blocked_out ? tid * ITEMS + i : wid * (kWave * ITEMS) + i * kWave + lane)];
   __syncthreads();
   if constexpr (PAIRS) {
 #pragma unroll
-    for (int i = 0; i < ITEMS; ++i) buf[pos[i]] = static_cast<uint32_t>(val[i]);
+    for (int i = 0; i < ITEMS; ++i) buf[buf_at(static_cast<int>(pos[i]))] = static_cast<uint32_t>(val[i]);
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < ITEMS; ++i)
-      val[i] = static_cast<int32_t>(buf[blocked_out ? tid * ITEMS + i : wid * (kWave * ITEMS) + i * kWave + lane]);
+      val[i] = static_cast<int32_t>(
+          buf[buf_at(blocked_out ? tid * ITEMS + i : wid * (kWave * ITEMS) + i * kWave + lane)]);
     __syncthreads();
   }
 }

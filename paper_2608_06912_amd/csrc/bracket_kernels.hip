@@ -236,12 +236,19 @@ struct PartState {
   int64_t nB;   // band count of this wave (uniform across the wave)
 };
 
-// Where a wave stages its band members.
+// Where a wave stages its band members and its bits of r >= hi.  Both go
+// to LDS while the wave streams (a global store inside the loop would make
+// every wait for the next loads also wait for the store) and are copied out
+// once at the end.
+constexpr int kOnesWaveWords = static_cast<int>(kBandMaxChunk / 4 / 32);   // 512
+
 struct BandWave {
-  BandEntry* out;    // this wave's segment
+  BandEntry* sbuf;   // LDS, cap entries
+  uint32_t* sones;   // LDS, kOnesWaveWords words: bit i of the wave's range
   int cap;
+  bool stage;        // false when the block's range is too long for the band passes
   float lo, hi;      // band: lo <= r < hi
-  uint32_t* ones;    // bit set where r >= hi (used when a_R is finite)
+  int64_t w0;        // first score of the wave's range (a multiple of 256)
 };
 
 // Classify 4 consecutive scores of one lane (the slow path of the gather);
@@ -314,7 +321,7 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       x |= __shfl_xor(x, 1, kWave);
       x |= __shfl_xor(x, 2, kWave);
       x |= __shfl_xor(x, 4, kWave);
-      if ((lane & 7) == 0 && it + 32 * (lane >> 3) < w1) bw.ones[(it >> 5) + (lane >> 3)] = x;
+      if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
     }
     if (!__ballot(bb != 0u)) return;   // no lane holds a band member
     {
@@ -333,7 +340,7 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
             BandEntry en;
             en.idx = static_cast<int32_t>(i0 + e);
             en.bits = __float_as_uint(v[e]);
-            bw.out[slot] = en;
+            bw.sbuf[slot] = en;
           }
           ++slot;
         }
@@ -369,7 +376,7 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
   if (vec && it + U * 256 <= w1) {
     float4 q[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) q[u] = *reinterpret_cast<const float4*>(r + it + u * 256 + 4 * lane);
+    for (int u = 0; u < U; ++u) q[u] = load_stream4(r + it + u * 256 + 4 * lane);
     while (true) {
       const int64_t cur = it;
       it += U * 256;
@@ -377,7 +384,7 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       float4 qn[U];
       if (more) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) qn[u] = *reinterpret_cast<const float4*>(r + it + u * 256 + 4 * lane);
+        for (int u = 0; u < U; ++u) qn[u] = load_stream4(r + it + u * 256 + 4 * lane);
       }
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -422,6 +429,8 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
                                                        uint32_t* __restrict__ ones) {
   __shared__ float sv[PW][kWaveStage];
   __shared__ int32_t si[PW][kWaveStage];
+  __shared__ BandEntry sband[PW][kBandWaveCapMax];
+  __shared__ uint32_t sones[PW][kOnesWaveWords];
   __shared__ double red_d[2][PW];
   __shared__ int64_t red_i[2][PW];
   __shared__ float red_f[2][PW];
@@ -437,17 +446,30 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   const int64_t w1 = w0 + wq < n ? w0 + wq : n;
   const bool vec = (reinterpret_cast<uintptr_t>(r) & 15) == 0;
   BandWave bw;
-  bw.out = bent + (static_cast<int64_t>(blockIdx.x) * PW + wid) * bcap;
-  bw.cap = bcap;
+  bw.sbuf = sband[wid];
+  bw.sones = sones[wid];
+  bw.stage = chunk <= kBandMaxChunk;
+  bw.cap = bw.stage ? (bcap < kBandWaveCapMax ? bcap : kBandWaveCapMax) : 0;
   // rounded outwards so that the float comparisons imply the float64 bounds
   bw.lo = __double2float_rd(static_cast<double>(aL) - kBandLowT * t);
   bw.hi = __double2float_ru(static_cast<double>(aR) + kBandHighT * t);
-  bw.ones = ones;
+  bw.w0 = w0;
   PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY, 0};
-  if (aR < INFINITY)
+  const bool has_r = aR < INFINITY;
+  if (has_r)
     partition_range<true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
   else
     partition_range<false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
+  // this wave's band list and bits out of LDS
+  if (bw.stage) {
+    BandEntry* out = bent + (static_cast<int64_t>(blockIdx.x) * PW + wid) * bcap;
+    const int64_t nb = st.nB < bw.cap ? st.nB : bw.cap;
+    for (int64_t q = lane; q < nb; q += kWave) out[q] = bw.sbuf[q];
+    if (has_r) {
+      const int64_t nw = (w1 - w0 + 31) / 32;
+      for (int64_t q = lane; q < nw; q += kWave) ones[(w0 >> 5) + q] = bw.sones[q];
+    }
+  }
   if (lane == 0) {
     bblk[blockIdx.x].cnt[wid] = static_cast<int32_t>(st.nB);
     red_b[wid] = st.nB;
@@ -514,7 +536,7 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
     rec.overflow = over ? 1 : 0;
     rec.pad = 0;
     blk[blockIdx.x] = rec;
-    bool bover = b1 - b0 > kBandMaxChunk;
+    bool bover = chunk > kBandMaxChunk;
 #pragma unroll
     for (int w = 0; w < PW; ++w) bover |= red_b[w] > bcap;
     bblk[blockIdx.x].dense = bover ? 1 : 0;

@@ -52,6 +52,20 @@ __device__ __forceinline__ float key_float(uint32_t dk) {
 // flush to zero, which only drops terms under 1e-38).
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Streams touched once per call (the scores in the partition, p and grad_r
+// written by the band passes) use non-temporal accesses, so that they
+// neither evict nor leave behind dirty lines that the next pass would have
+// to write back.
+typedef float stream_v4f __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 load_stream4(const float* p) {
+  const stream_v4f v = __builtin_nontemporal_load(reinterpret_cast<const stream_v4f*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void store_stream4(float* p, float4 x) {
+  const stream_v4f v = {x.x, x.y, x.z, x.w};
+  __builtin_nontemporal_store(v, reinterpret_cast<stream_v4f*>(p));
+}
+
 // e^{-d/t} for d >= 0 with the exponent formed in float64 (d may be the
 // difference of two float32 scores of very different size) and the
 // exponential in float32; c2 = log2(e)/t.  For per-score terms summed in

@@ -17,7 +17,7 @@ constexpr int64_t kTile = kTileThreads * kTileItems;   // 4096
 // Bracketed pass: blocks of the streaming partition and their staging.
 constexpr int kPartThreads = 256;
 constexpr int kPartMaxBlocks = 4096;   // blocks of the streaming partition
-constexpr int kPartStageCap = 2048;    // M entries a partition block stages
+constexpr int kPartStageCap = 960;     // M entries a partition block stages (LDS: 5 blocks per CU)
 constexpr int kSelectBins = 2048;      // 11-bit digits of the order-statistic select
 
 // Threshold record written by the device-wide solve (one per row).

@@ -19,7 +19,7 @@ __global__ __launch_bounds__(BLOCK) void row_forward_kernel(const float* __restr
                                                             double* __restrict__ b_out,
                                                             int32_t* __restrict__ perm) {
   constexpr int WAVES = BLOCK / kWave;
-  __shared__ uint32_t buf[BLOCK * ITEMS];
+  __shared__ uint32_t buf[sort_buf_words<BLOCK, ITEMS>()];
   __shared__ SortSmem<BLOCK> ssm;
   __shared__ ScanSmem<WAVES> csm;
 

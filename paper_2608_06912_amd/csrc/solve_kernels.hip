@@ -340,7 +340,7 @@ __global__ __launch_bounds__(BLOCK) void small_m_solve_kernel(const uint32_t* __
                                                               SolveRec* __restrict__ out,
                                                               int32_t* __restrict__ idx_sorted) {
   constexpr int WAVES = BLOCK / kWave;
-  __shared__ uint32_t buf[BLOCK * ITEMS];
+  __shared__ uint32_t buf[sort_buf_words<BLOCK, ITEMS>()];
   __shared__ SortSmem<BLOCK> ssm;
   __shared__ ScanSmem<WAVES> csm;
   const int tid = threadIdx.x;

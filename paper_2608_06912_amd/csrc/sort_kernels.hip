@@ -62,10 +62,10 @@ __global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
   const int64_t ntiles = (len + TILE - 1) / TILE;
   const int64_t tile = blockIdx.x;
   if (tile >= ntiles) return;
-  __shared__ uint32_t cnt[256 * TW];
+  __shared__ uint32_t cnt[cnt_words<TW>()];
   const int tid = threadIdx.x;
   const int wid = tid / kWave;
-  for (int e = tid; e < 256 * TW; e += TT) cnt[e] = 0u;
+  for (int e = tid; e < cnt_words<TW>(); e += TT) cnt[e] = 0u;
   __syncthreads();
   const int64_t base = tile * TILE;
 #pragma unroll
@@ -74,12 +74,12 @@ __global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
     const bool valid = pos < len;
     const uint32_t d = valid ? (load_key(a, pos) >> a.shift) & 255u : 0u;
     const uint64_t peers = match_digit8(d) & __ballot(valid);
-    if (valid && lanes_below(peers) == 0u) cnt[d * TW + wid] += static_cast<uint32_t>(__popcll(peers));
+    if (valid && lanes_below(peers) == 0u) cnt[cnt_at<TW>(d, wid)] += static_cast<uint32_t>(__popcll(peers));
   }
   __syncthreads();
   uint32_t sum = 0;
 #pragma unroll
-  for (int w = 0; w < TW; ++w) sum += cnt[tid * TW + w];
+  for (int w = 0; w < TW; ++w) sum += cnt[cnt_at<TW>(tid, w)];
   a.hist[static_cast<int64_t>(tid) * a.max_tiles + tile] = sum;
 }
 
@@ -138,7 +138,7 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
   const int64_t ntiles = (len + TILE - 1) / TILE;
   const int64_t tile = blockIdx.x;
   if (tile >= ntiles) return;
-  __shared__ uint32_t cnt[256 * TW];
+  __shared__ uint32_t cnt[cnt_words<TW>()];
   __shared__ uint32_t wave_tot[TW];
   __shared__ uint32_t gbase[256];    // first output position of each digit for this tile
   __shared__ uint32_t dstart[256];   // first tile-local position of each digit
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
       if (w < wid) wbase += wave_tot[w];
     gbase[tid] = wbase + incl - tot + before_tile;
   }
-  for (int e = tid; e < 256 * TW; e += TT) cnt[e] = 0u;
+  for (int e = tid; e < cnt_words<TW>(); e += TT) cnt[e] = 0u;
   __syncthreads();
 
   const int64_t base = tile * TILE;
@@ -205,7 +205,7 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
     const uint32_t d = (key[i] >> a.shift) & 255u;
     const uint64_t peers = match_digit8(d) & validm[i];
     const uint32_t below = lanes_below(peers);
-    uint32_t* slot = &cnt[d * TW + wid];
+    uint32_t* slot = &cnt[cnt_at<TW>(d, wid)];
     const uint32_t c = *slot;
     pos[i] = c + below;
     const bool valid = (validm[i] >> lane) & 1ull;
@@ -213,10 +213,10 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
   }
   __syncthreads();
   block_excl_scan_u32x4<TT>(cnt, wave_tot);
-  dstart[tid] = cnt[tid * TW];
+  dstart[tid] = cnt[cnt_at<TW>(tid, 0)];
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
-    pos[i] += cnt[((key[i] >> a.shift) & 255u) * TW + wid];
+    pos[i] += cnt[cnt_at<TW>((key[i] >> a.shift) & 255u, wid)];
     if ((validm[i] >> lane) & 1ull) buf[pos[i]] = key[i];
   }
   __syncthreads();
