@@ -161,12 +161,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __r
   const int64_t K4 = K / 4;
   const uint4* y4 = reinterpret_cast<const uint4*>(ykeys);
   int64_t i4 = tid;
-  for (; i4 + 3 * kSelThreads < K4; i4 += 4 * kSelThreads) {   // four loads in flight
-    uint4 v[4];
+  for (; i4 + 7 * kSelThreads < K4; i4 += 8 * kSelThreads) {   // eight loads in flight
+    uint4 v[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = y4[i4 + u * kSelThreads];
+    for (int u = 0; u < 8; ++u) v[u] = y4[i4 + u * kSelThreads];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       collect(v[u].x);
       collect(v[u].y);
       collect(v[u].z);
@@ -412,6 +412,138 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
 
 }  // namespace
 
+// Totals over the partition blocks in a fixed order and the exclusive
+// prefix of their M counts (each block's offset into M), TOT_T threads.
+// Records are read coalesced (all loads of a thread independent), the M
+// counts go through LDS (`nm`, kPartMaxBlocks words) for the prefix.
+constexpr int TOT_T = 1024;   // threads of the totals kernel
+constexpr int TOT_W = TOT_T / kWave;
+
+__device__ void partition_totals_block(const PartBlock* __restrict__ blk, int nblocks, float aL,
+                                       float aR, int64_t* __restrict__ offsets,
+                                       PartTotals* __restrict__ tot, int32_t* nm) {
+  constexpr int Q = kPartMaxBlocks / TOT_T;
+  constexpr int PT = TOT_T;
+  constexpr int PW = TOT_W;
+  __shared__ double rd[2][PW];
+  __shared__ int64_t ri[4][PW];
+  __shared__ float rf[2][PW];
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  double TL = 0.0, TR = 0.0;
+  int64_t nL = 0, nR = 0, ov = 0;
+  float mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int b = tid + PT * q;
+    if (b < nblocks) {
+      const PartBlock rec = blk[b];
+      TL += rec.TL;
+      TR += rec.TR;
+      nL += rec.nL;
+      nR += rec.nR;
+      ov += rec.overflow;
+      mn = fminf(mn, rec.mmin);
+      mx = fmaxf(mx, rec.mmax);
+      nm[b] = static_cast<int32_t>(rec.nM);
+    }
+  }
+  __syncthreads();
+  // prefix of the M counts: thread tid owns blocks [Q tid, Q tid + Q)
+  int64_t loc = 0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int b = Q * tid + q;
+    loc += (b < nblocks) ? nm[b] : 0;
+  }
+  int64_t incl = loc;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int64_t x = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += x;
+  }
+  TL = wave_sum(TL);
+  TR = wave_sum(TR);
+  const int64_t sL = wave_sum(nL), sR = wave_sum(nR), sO = wave_sum(ov);
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    mn = fminf(mn, __shfl_xor(mn, o, kWave));
+    mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+  }
+  if (lane == kWave - 1) ri[3][wid] = incl;
+  if (lane == 0) {
+    rd[0][wid] = TL;
+    rd[1][wid] = TR;
+    ri[0][wid] = sL;
+    ri[1][wid] = sR;
+    ri[2][wid] = sO;
+    rf[0][wid] = mn;
+    rf[1][wid] = mx;
+  }
+  __syncthreads();
+  int64_t base = 0, allm = 0;
+#pragma unroll
+  for (int w = 0; w < PW; ++w) {
+    if (w < wid) base += ri[3][w];
+    allm += ri[3][w];
+  }
+  int64_t off = base + incl - loc;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int b = Q * tid + q;
+    if (b < nblocks) {
+      offsets[b] = off;
+      off += nm[b];
+    }
+  }
+  if (tid == 0) {
+    PartTotals x;
+    double tl = 0.0, tr = 0.0;
+    int64_t cl = 0, cr = 0, co = 0;
+    float fmn = INFINITY, fmx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < PW; ++w) {
+      tl += rd[0][w];
+      tr += rd[1][w];
+      cl += ri[0][w];
+      cr += ri[1][w];
+      co += ri[2][w];
+      fmn = fminf(fmn, rf[0][w]);
+      fmx = fmaxf(fmx, rf[1][w]);
+    }
+    x.TL = tl;
+    x.TR = tr;
+    x.nL = cl;
+    x.nR = cr;
+    x.nM = allm;
+    x.aL = aL;
+    x.aR = aR;
+    x.mmin = fmn;
+    x.mmax = fmx;
+    x.any_block_overflow = co > 0 ? 1 : 0;
+    x.pad = 0;
+    *tot = x;
+  }
+}
+
+// One workgroup: the totals of one partition pass.  (A separate launch
+// rather than the last block of the pass: making the records of every block
+// visible to that block would take a device-scope release per block, which
+// writes back the L2 of its XCD.)
+__global__ __launch_bounds__(TOT_T) void partition_totals_kernel(const PartBlock* __restrict__ blk,
+                                                              int nblocks,
+                                                              const SelectRec* __restrict__ sel,
+                                                              int use_sel, float aL_arg,
+                                                              float aR_arg,
+                                                              int64_t* __restrict__ offsets,
+                                                              PartTotals* __restrict__ tot) {
+  __shared__ int32_t nm[kPartMaxBlocks];
+  const float aL = use_sel ? sel->aL : aL_arg;
+  const float aR = use_sel ? sel->aR : aR_arg;
+  partition_totals_block(blk, nblocks, aL, aR, offsets, tot, nm);
+}
+
 // Block b owns [b*chunk, (b+1)*chunk) and wave w the w-th contiguous
 // quarter of it, so each wave sees its scores in index order and stages its
 // M members in LDS with a wave-private counter; the block then writes them
@@ -546,12 +678,18 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
                             float aR, double t, int nblocks, int64_t chunk, float* stage_v,
                             int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
-                            hipStream_t s) {
-  if (band.nblocks != nblocks || band.chunk != chunk) return hipErrorInvalidValue;
+                            int64_t* offsets, PartTotals* tot, hipStream_t s) {
+  if (band.nblocks != nblocks || band.chunk != chunk || nblocks > kPartMaxBlocks)
+    return hipErrorInvalidValue;
   const float c2f = static_cast<float>(kLog2e / t);
   { ProfScope ps_("partition", s);
   hipLaunchKernelGGL(partition_kernel, dim3(nblocks), dim3(PT), 0, s, r, n, sel, use_sel, aL, aR,
                      c2f, chunk, stage_v, stage_i, blk, t, band.ent, band.blk, band.cap, ones); }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  { ProfScope ps_("partition_totals", s);
+  hipLaunchKernelGGL(partition_totals_kernel, dim3(1), dim3(TOT_T), 0, s, blk, nblocks, sel, use_sel,
+                     aL, aR, offsets, tot); }
   return hipGetLastError();
 }
 
@@ -593,117 +731,6 @@ BandCtx band_ctx_view(void* base, int64_t n) {
   v.blk = b ? reinterpret_cast<BandBlock*>(b + L.blk_off) : nullptr;
   v.ent = b ? reinterpret_cast<BandEntry*>(b + L.ent_off) : nullptr;
   return v;
-}
-
-// One workgroup: totals over the partition blocks in a fixed order, and the
-// exclusive prefix of their M counts (each block's offset into M).  Thread
-// tid owns a contiguous run of block records.
-__global__ __launch_bounds__(256) void partition_totals_kernel(const PartBlock* __restrict__ blk,
-                                                                int nblocks,
-                                                                const SelectRec* __restrict__ sel,
-                                                                int use_sel, float aL_arg,
-                                                                float aR_arg,
-                                                                int64_t* __restrict__ offsets,
-                                                                PartTotals* __restrict__ tot) {
-  constexpr int T = 256;
-  constexpr int W = T / kWave;
-  __shared__ double rd[2][W];
-  __shared__ int64_t ri[4][W];
-  __shared__ float rf[2][W];
-  const int tid = threadIdx.x;
-  const int lane = lane_id();
-  const int wid = tid / kWave;
-  const int per = (nblocks + T - 1) / T;
-  const int b0 = tid * per;
-  const int b1 = (b0 + per < nblocks) ? b0 + per : nblocks;
-  double TL = 0.0, TR = 0.0;
-  int64_t nL = 0, nR = 0, nM = 0, ov = 0;
-  float mn = INFINITY, mx = -INFINITY;
-  for (int b = b0; b < b1; ++b) {
-    const PartBlock rec = blk[b];
-    TL += rec.TL;
-    TR += rec.TR;
-    nL += rec.nL;
-    nR += rec.nR;
-    nM += rec.nM;
-    ov += rec.overflow;
-    mn = fminf(mn, rec.mmin);
-    mx = fmaxf(mx, rec.mmax);
-  }
-  // exclusive prefix of nM over threads (each thread's run is contiguous)
-  int64_t incl = nM;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int64_t x = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += x;
-  }
-  TL = wave_sum(TL);
-  TR = wave_sum(TR);
-  const int64_t sL = wave_sum(nL), sR = wave_sum(nR), sO = wave_sum(ov);
-#pragma unroll
-  for (int o = kWave / 2; o >= 1; o >>= 1) {
-    mn = fminf(mn, __shfl_xor(mn, o, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
-  }
-  if (lane == kWave - 1) ri[3][wid] = incl;
-  if (lane == 0) {
-    rd[0][wid] = TL;
-    rd[1][wid] = TR;
-    ri[0][wid] = sL;
-    ri[1][wid] = sR;
-    ri[2][wid] = sO;
-    rf[0][wid] = mn;
-    rf[1][wid] = mx;
-  }
-  __syncthreads();
-  int64_t base = 0, allm = 0;
-#pragma unroll
-  for (int w = 0; w < W; ++w) {
-    if (w < wid) base += ri[3][w];
-    allm += ri[3][w];
-  }
-  int64_t off = base + incl - nM;
-  for (int b = b0; b < b1; ++b) {
-    offsets[b] = off;
-    off += blk[b].nM;
-  }
-  if (tid == 0) {
-    PartTotals x;
-    double tl = 0.0, tr = 0.0;
-    int64_t cl = 0, cr = 0, co = 0;
-    float fmn = INFINITY, fmx = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < W; ++w) {
-      tl += rd[0][w];
-      tr += rd[1][w];
-      cl += ri[0][w];
-      cr += ri[1][w];
-      co += ri[2][w];
-      fmn = fminf(fmn, rf[0][w]);
-      fmx = fmaxf(fmx, rf[1][w]);
-    }
-    x.TL = tl;
-    x.TR = tr;
-    x.nL = cl;
-    x.nR = cr;
-    x.nM = allm;
-    x.aL = use_sel ? sel->aL : aL_arg;
-    x.aR = use_sel ? sel->aR : aR_arg;
-    x.mmin = fmn;
-    x.mmax = fmx;
-    x.any_block_overflow = co > 0 ? 1 : 0;
-    x.pad = 0;
-    *tot = x;
-  }
-}
-
-hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const SelectRec* sel,
-                                   int use_sel, float aL, float aR, int64_t* offsets,
-                                   PartTotals* tot, hipStream_t s) {
-  { ProfScope ps_("partition_totals", s);
-  hipLaunchKernelGGL(partition_totals_kernel, dim3(1), dim3(256), 0, s, blk, nblocks, sel, use_sel,
-                     aL, aR, offsets, tot); }
-  return hipGetLastError();
 }
 
 // Copy each block's staged M to M[offset..]; a block whose staging

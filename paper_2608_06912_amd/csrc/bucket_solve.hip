@@ -1,0 +1,402 @@
+// Threshold solve on the middle set M of a bracket without sorting all of
+// M (the scan, lookup and closed-form root of Suppl. A / Suppl. B, applied
+// where the root is).
+//
+// M is cut into 2048 buckets of consecutive order-preserving keys (bucket
+// d = (key - key(max M)) >> shift, so bucket 0 holds the largest scores).
+// Bucket d covers the score interval [u_d, v_d] (its lowest and highest
+// possible float, clamped to the range of M) and is summarised by its count
+// and the two sums
+//     D_d = sum_{r in d} e^{-(r - u_d)/t}    (a prefix pair anchored at u_d)
+//     U_d = sum_{r in d} e^{-(v_d - r)/t}    (a suffix pair anchored at v_d).
+// The shift-carrying scans over the buckets, seeded with the bracket tails,
+// give LapSum at every bucket's upper edge,
+//     LapSum(v_d) = n_above - (1/2) e^{-(u - v_d)/t} S_above
+//                   + (1/2) (U_d + e^{-(v_d - v')/t} T_below),
+// which is non-decreasing in d; the root lies in the last bucket d* with
+// LapSum(v_d*) <= k (or above every bucket).  Only bucket d* is then sorted
+// (on chip) and solved by block_solve with the scans as carries; the scan
+// totals give the certificate LapSum(a_R) <= k <= LapSum(a_L) as before.
+//
+// The bucket sums are accumulated in 64-bit fixed point (2^F per unit,
+// F = 62 - bits(|M|), so no sum can overflow): integer additions commute,
+// which keeps the result independent of the order in which the atomics land.
+// A term below 2^-F is dropped, an absolute error of at most |M| 2^-F in a
+// sum that enters LapSum with weight 1/2.
+//
+// Two launches: bucket_count (one block per 4096 keys of M) and
+// bucket_solve (one workgroup).  When bucket d* holds more keys than the
+// workgroup can sort (kBucketSortCap) the record reports side = 2 and the
+// caller solves M by the full sort instead.
+#include <math.h>
+
+#include "block_sort.hpp"
+#include "kernels.hpp"
+#include "solve_common.hpp"
+
+namespace lapsum {
+
+namespace {
+
+constexpr int kBuckets = kBucketCount;
+constexpr int CT = 256;             // bucket_count threads
+constexpr int CI = 16;              // keys per thread
+constexpr int ST = 256;             // bucket_solve threads
+constexpr int SW = ST / kWave;      // 4 waves
+constexpr int BPT = kBuckets / ST;  // buckets per thread
+constexpr int SI = kBucketSortCap / ST;   // keys per thread in the largest on-chip sort
+
+struct BucketGeom {
+  uint32_t kmin, kmax;   // keys of max M and min M
+  int shift;
+  float mmin, mmax;
+};
+
+__device__ __forceinline__ float bucket_hi(const BucketGeom& g, int d) {
+  // highest score bucket d can hold (its smallest key); buckets past the
+  // range of M are empty and anchored at min M, so that anchors never
+  // increase along the bucket order
+  const uint64_t first = static_cast<uint64_t>(g.kmin) + (static_cast<uint64_t>(d) << g.shift);
+  if (first > g.kmax) return g.mmin;
+  return fminf(key_float(static_cast<uint32_t>(first)), g.mmax);
+}
+__device__ __forceinline__ float bucket_lo(const BucketGeom& g, int d) {
+  // lowest score bucket d can hold (its largest key, at most key(min M))
+  const uint64_t last = static_cast<uint64_t>(g.kmin) + ((static_cast<uint64_t>(d) + 1) << g.shift) - 1;
+  const uint32_t key = last < g.kmax ? static_cast<uint32_t>(last) : g.kmax;
+  return fmaxf(key_float(key), g.mmin);
+}
+
+}  // namespace
+
+// acc: [kBuckets] u32 counts, then [kBuckets] u64 U, then [kBuckets] u64 D;
+// zero on entry (bucket_solve clears it again).
+__global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __restrict__ keys,
+                                                          int64_t m, BucketGeom g, double c2,
+                                                          double fscale,
+                                                          uint32_t* __restrict__ acc_n,
+                                                          unsigned long long* __restrict__ acc_u,
+                                                          unsigned long long* __restrict__ acc_d) {
+  __shared__ uint32_t cn[kBuckets];
+  __shared__ unsigned long long cu[kBuckets];
+  __shared__ unsigned long long cd[kBuckets];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < kBuckets; e += CT) {
+    cn[e] = 0u;
+    cu[e] = 0ull;
+    cd[e] = 0ull;
+  }
+  __syncthreads();
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * CT * CI;
+#pragma unroll
+  for (int i = 0; i < CI; ++i) {
+    const int64_t pos = base + i * CT + tid;
+    if (pos < m) {
+      const uint32_t key = keys[pos];
+      const int d = static_cast<int>((key - g.kmin) >> g.shift);
+      const double r = key_float(key);
+      const double up = wexp_f32(static_cast<double>(bucket_hi(g, d)) - r, c2);   // e^{-(v_d - r)/t}
+      const double dn = wexp_f32(r - static_cast<double>(bucket_lo(g, d)), c2);   // e^{-(r - u_d)/t}
+      atomicAdd(&cn[d], 1u);
+      atomicAdd(&cu[d], static_cast<unsigned long long>(__double2ull_rn(up * fscale)));
+      atomicAdd(&cd[d], static_cast<unsigned long long>(__double2ull_rn(dn * fscale)));
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < kBuckets; e += CT) {
+    if (cn[e]) {
+      atomicAdd(&acc_n[e], cn[e]);
+      atomicAdd(&acc_u[e], cu[e]);
+      atomicAdd(&acc_d[e], cd[e]);
+    }
+  }
+}
+
+namespace {
+// Sort c relative keys held in buf (any order) on chip and solve on them.
+template <int ITEMS>
+__device__ double sort_and_solve(uint32_t* buf, int c, const BucketGeom& g, double rank0,
+                                 Pre ext_pre, Suf ext_suf, double k, double t, SortSmem<ST>& ssm,
+                                 ScanSmem<SW>& csm) {
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  uint32_t key[ITEMS];
+  int32_t val[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    const int pos = wid * (kWave * ITEMS) + i * kWave + lane;
+    key[i] = pos < c ? buf[buf_at(pos)] : 0xffffffffu;
+    val[i] = 0;
+  }
+  __syncthreads();
+  // relative keys of one bucket differ only in their low `shift` bits; the
+  // padding (all ones) stays behind every member in each pass
+  const int passes = g.shift <= 8 ? 1 : (g.shift + 7) / 8;
+  for (int pidx = 0; pidx < passes; ++pidx)
+    block_sort_pass<ST, ITEMS, false>(key, val, 8 * pidx, buf, ssm, pidx == passes - 1);
+  float s[ITEMS];
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) s[i] = key_float(key[i] + g.kmin);
+  int cnt = c - tid * ITEMS;
+  cnt = cnt < 0 ? 0 : (cnt > ITEMS ? ITEMS : cnt);
+  Pre pt;
+  Suf st;
+  return block_solve<ST, ITEMS>(s, cnt, rank0, ext_pre, ext_suf, k, t, csm, &pt, &st);
+}
+}  // namespace
+
+// One workgroup.  Thread tid owns buckets BPT tid .. BPT tid + BPT - 1.
+// Inside a thread the pairs chain through every bucket's own anchors (empty
+// buckets carry their geometric anchors and a zero sum), so the in-thread
+// folds need one exponential per bucket and no search for the previous
+// non-empty bucket; the block scans then join the threads.
+__global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __restrict__ keys,
+                                                          int64_t m, BucketGeom g,
+                                                          double inv_fscale,
+                                                          uint32_t* __restrict__ acc_n,
+                                                          unsigned long long* __restrict__ acc_u,
+                                                          unsigned long long* __restrict__ acc_d,
+                                                          const PartTotals* __restrict__ tot,
+                                                          double k, double t, int64_t n_total,
+                                                          SolveRec* __restrict__ out) {
+  __shared__ uint32_t buf[sort_buf_words<ST, SI>()];
+  __shared__ SortSmem<ST> ssm;
+  __shared__ ScanSmem<SW> csm;
+  __shared__ int64_t cw[SW];
+  __shared__ int64_t red_i[SW];
+  __shared__ Pre cpre_s;
+  __shared__ Suf csuf_s;
+  __shared__ int64_t cabove_s;
+  __shared__ uint32_t ccount_s;
+  __shared__ uint32_t gathered_s;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  const double inv_t = 1.0 / t;
+  const Tails x = load_tails(tot);
+  const int d0 = BPT * tid;
+
+  // 1. this thread's buckets, cleared behind us for the next attempt
+  uint32_t cnt[BPT];
+  double U[BPT], D[BPT];
+  float v[BPT], u[BPT];
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    cnt[q] = acc_n[d0 + q];
+    U[q] = static_cast<double>(acc_u[d0 + q]) * inv_fscale;
+    D[q] = static_cast<double>(acc_d[d0 + q]) * inv_fscale;
+    v[q] = bucket_hi(g, d0 + q);
+    u[q] = bucket_lo(g, d0 + q);
+  }
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    acc_n[d0 + q] = 0u;
+    acc_u[d0 + q] = 0ull;
+    acc_d[d0 + q] = 0ull;
+  }
+  // links between consecutive anchors of this thread (all independent)
+  double wu[BPT], wv[BPT];   // wu[q] = e^{-(u_{q-1} - u_q)/t}, wv[q] = e^{-(v_q - v_{q+1})/t}
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    wu[q] = q > 0 ? wexp_f64(static_cast<double>(u[q - 1]) - u[q], inv_t) : 0.0;
+    wv[q] = q + 1 < BPT ? wexp_f64(static_cast<double>(v[q]) - v[q + 1], inv_t) : 0.0;
+  }
+  // The prefix pair may sit at any anchor at or above the root, so it
+  // chains through the geometric anchors of empty buckets.  A suffix pair
+  // is anchored at the upper edge of a non-empty bucket: the root lies above
+  // the upper edge of the first non-empty bucket after the crossing, but can
+  // lie below the edge of an empty bucket in between.
+  double Pm = 0.0;   // prefix pair of the thread, anchored at u[BPT-1]
+  int64_t mine = 0;
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    Pm = fma(wu[q], Pm, D[q]);
+    mine += cnt[q];
+  }
+  double Tl[BPT];    // suffix within the thread from bucket q, anchored at v[q]
+#pragma unroll
+  for (int q = BPT - 1; q >= 0; --q) Tl[q] = fma(wv[q], q + 1 < BPT ? Tl[q + 1] : 0.0, U[q]);
+  Suf mys = suf_empty();   // anchored at the first non-empty bucket of the thread
+#pragma unroll
+  for (int q = BPT - 1; q >= 0; --q)
+    if (cnt[q] && Tl[q] != 0.0) mys = Suf{v[q], Tl[q]};
+
+  // 2. block scans, seeded with the tails
+  Pre pre_all;
+  Suf suf_all;
+  const Pre pre_in = block_excl_pre<SW>(Pre{u[BPT - 1], Pm}, x.pre, inv_t, csm, &pre_all);
+  const Suf suf_in = block_excl_suf<SW>(mys, x.suf, inv_t, csm, &suf_all);
+  int64_t incl = mine;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int64_t y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  if (lane == kWave - 1) cw[wid] = incl;
+  __syncthreads();
+  int64_t above = incl - mine;
+#pragma unroll
+  for (int w = 0; w < SW; ++w)
+    if (w < wid) above += cw[w];
+
+  // 3. suffix sums from each bucket on (anchored at its v), right to left,
+  //    then LapSum at each non-empty bucket's upper edge, left to right:
+  //    LapSum(v_q) = n_R + above_q - (1/2) e^{-(u_prev - v_q)/t} P_before + (1/2) T_q
+  double T[BPT];
+  {
+    double tn = suf_in.T;
+    float vn = suf_in.v;
+#pragma unroll
+    for (int q = BPT - 1; q >= 0; --q) {
+      const double w = (q + 1 < BPT) ? wv[q]
+                       : (tn != 0.0 ? wexp_f64(static_cast<double>(v[q]) - vn, inv_t) : 0.0);
+      T[q] = fma(w, (q + 1 < BPT) ? T[q + 1] : tn, U[q]);
+    }
+  }
+  int64_t below = 0;   // 1 + the last bucket with LapSum(v_d) <= k
+  {
+    double P = pre_in.S;   // prefix before bucket q, anchored at pu
+    float pu = pre_in.u;
+    int64_t ab = above;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q) {
+      if (cnt[q]) {
+        double lap = x.nR + static_cast<double>(ab) + 0.5 * T[q];
+        if (P != 0.0) lap -= 0.5 * wexp_f64(static_cast<double>(pu) - v[q], inv_t) * P;
+        if (lap <= k) below = d0 + q + 1;
+      }
+      const double w = (P != 0.0) ? wexp_f64(static_cast<double>(pu) - u[q], inv_t) : 0.0;
+      P = fma(w, P, D[q]);
+      pu = u[q];
+      ab += cnt[q];
+    }
+  }
+#pragma unroll
+  for (int o = kWave / 2; o >= 1; o >>= 1) {
+    const int64_t y = __shfl_xor(below, o, kWave);
+    below = y > below ? y : below;
+  }
+  if (lane == 0) red_i[wid] = below;
+  if (tid == 0) gathered_s = 0u;
+  __syncthreads();
+  below = 0;
+#pragma unroll
+  for (int w = 0; w < SW; ++w) below = red_i[w] > below ? red_i[w] : below;
+  const int dstar = static_cast<int>(below) - 1;
+  if (dstar >= d0 && dstar < d0 + BPT) {
+    // carries around bucket d*: the prefix of everything before it and the
+    // suffix of everything after it
+    double P = pre_in.S;
+    float pu = pre_in.u;
+    int64_t ab = above;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q) {
+      if (d0 + q == dstar) {
+        cpre_s = (P != 0.0) ? Pre{pu, P} : pre_empty();
+        Suf after = suf_in;   // from the next non-empty bucket on
+#pragma unroll
+        for (int q2 = BPT - 1; q2 > q; --q2)
+          if (cnt[q2] && T[q2] != 0.0) after = Suf{v[q2], T[q2]};
+        csuf_s = after;
+        cabove_s = ab;
+        ccount_s = cnt[q];
+      }
+      const double w = (P != 0.0) ? wexp_f64(static_cast<double>(pu) - u[q], inv_t) : 0.0;
+      P = fma(w, P, D[q]);
+      pu = u[q];
+      ab += cnt[q];
+    }
+  }
+  __syncthreads();
+
+  SolveRec rec;
+  rec.ok = 1;
+  rec.side = 0;
+  rec.lap_aL = 0.0;
+  rec.lap_aR = 0.0;
+  certify(x, static_cast<double>(m), static_cast<double>(n_total), k, t, pre_all, suf_all, rec);
+  double b = 0.0;
+  if (dstar < 0) {
+    b = root_above(x, suf_all, k, t);
+  } else if (ccount_s > static_cast<uint32_t>(kBucketSortCap)) {
+    rec.ok = 0;
+    rec.side = 2;   // the bucket is too large to sort here: solve M by the full sort
+  } else {
+    // 4. gather bucket d* as keys relative to key(max M), whose low `shift`
+    //    bits order the bucket (its order in LDS is irrelevant: sorted next)
+    auto take = [&](uint32_t key) {
+      const uint32_t rel = key - g.kmin;
+      if (static_cast<int>(rel >> g.shift) == dstar) {
+        const uint32_t at = atomicAdd(&gathered_s, 1u);
+        if (at < static_cast<uint32_t>(kBucketSortCap)) buf[buf_at(static_cast<int>(at))] = rel;
+      }
+    };
+    const int64_t m4 = (reinterpret_cast<uintptr_t>(keys) & 15) == 0 ? m / 4 : 0;
+    const uint4* k4 = reinterpret_cast<const uint4*>(keys);
+    for (int64_t q0 = tid; q0 < m4; q0 += 8 * ST) {   // eight loads in flight
+      uint4 vv[8];
+#pragma unroll
+      for (int uu = 0; uu < 8; ++uu) {
+        const int64_t q = q0 + static_cast<int64_t>(uu) * ST;
+        vv[uu] = q < m4 ? k4[q] : make_uint4(g.kmin - 1u, g.kmin - 1u, g.kmin - 1u, g.kmin - 1u);
+      }
+#pragma unroll
+      for (int uu = 0; uu < 8; ++uu) {
+        take(vv[uu].x);
+        take(vv[uu].y);
+        take(vv[uu].z);
+        take(vv[uu].w);
+      }
+    }
+    for (int64_t i = m4 * 4 + tid; i < m; i += ST) take(keys[i]);
+    __syncthreads();
+    const int c = static_cast<int>(ccount_s);
+    const double rank0 = x.nR + static_cast<double>(cabove_s);
+    if (c <= ST)
+      b = sort_and_solve<1>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
+    else if (c <= 4 * ST)
+      b = sort_and_solve<4>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
+    else
+      b = sort_and_solve<SI>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
+  }
+  if (tid == 0) {
+    rec.b = b;
+    *out = rec;
+  }
+}
+
+int bucket_shift(uint32_t kmin, uint32_t kmax) {
+  const uint32_t span = kmax - kmin;
+  int bits = 0;
+  while (bits < 32 && (span >> bits) != 0u) ++bits;
+  return bits > 11 ? bits - 11 : 0;
+}
+
+hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m, float mmin, float mmax,
+                               uint32_t kmin, uint32_t kmax, BucketAcc acc, const PartTotals* tot,
+                               double k, double t, int64_t n_total, SolveRec* out, hipStream_t s) {
+  if (m < 1 || !(mmin <= mmax)) return hipErrorInvalidValue;
+  BucketGeom g;
+  g.kmin = kmin;
+  g.kmax = kmax;
+  g.shift = bucket_shift(kmin, kmax);
+  g.mmin = mmin;
+  g.mmax = mmax;
+  int mbits = 0;
+  while (mbits < 63 && (static_cast<uint64_t>(m) >> mbits) != 0u) ++mbits;
+  const int F = 62 - mbits;   // |M| terms of at most 2^F each fit in 62 bits
+  const double fscale = ldexp(1.0, F);
+  const int64_t blocks = (m + CT * CI - 1) / (CT * CI);
+  { ProfScope ps_("bucket_count", s);
+  hipLaunchKernelGGL(bucket_count_kernel, dim3(static_cast<unsigned>(blocks)), dim3(CT), 0, s,
+                     m_keys, m, g, kLog2e / t, fscale, acc.n, acc.u, acc.d); }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  { ProfScope ps_("bucket_solve", s);
+  hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, m_keys, m, g, 1.0 / fscale,
+                     acc.n, acc.u, acc.d, tot, k, t, n_total, out); }
+  return hipGetLastError();
+}
+
+}  // namespace lapsum

@@ -142,8 +142,9 @@ __device__ __forceinline__ T wave_sum(T v) {
 // Scratch for the block-level scans and the crossing search.
 template <int WAVES>
 struct ScanSmem {
-  Pre pre[WAVES + 1];
-  Suf suf[WAVES + 1];
+  double A[WAVES], B[WAVES];   // per-wave affine maps
+  float au[WAVES];             // per-wave anchor of the last (first) non-empty group
+  int ah[WAVES];
   int cnt[WAVES];
   double b;
   double P[64];   // crossing refinement (at most 64 items per thread)
@@ -154,60 +155,169 @@ struct ScanSmem {
   int cnt_c;
 };
 
-// Exclusive block scan of Pre, seeded with carry (groups before the block).
-// Returns this thread's exclusive prefix; *total gets carry (+) all.
+// Block scans of the pairs.  The combine of two prefix pairs is the affine
+// map P -> w P + S with w = e^{-(u_earlier - u_later)/t}, and likewise for
+// suffix pairs, so a scan over the threads' groups is an affine scan once
+// every group knows the anchor of the nearest non-empty group before it
+// (after it, for suffixes): each thread forms its one exponential, and the
+// scan itself multiplies and adds.  Weights never exceed 1 (anchors are
+// non-increasing along the order), so products only underflow, when the
+// carried terms are negligible.
+
+// Exclusive block scan of Pre in thread order, seeded with carry (groups
+// before the block).  Returns this thread's exclusive prefix; *total gets
+// carry (+) all.  Empty groups (S == 0) are skipped.
 template <int WAVES>
 __device__ Pre block_excl_pre(Pre x, Pre carry, double inv_t, ScanSmem<WAVES>& sm, Pre* total) {
   const int lane = lane_id();
   const int wid = threadIdx.x / kWave;
-  Pre incl = wave_incl_pre(x, inv_t);
-  float eu = __shfl_up(incl.u, 1, kWave);
-  double eS = __shfl_up(incl.S, 1, kWave);
-  Pre lane_excl = (lane == 0) ? pre_empty() : Pre{eu, eS};
-  if (lane == kWave - 1) sm.pre[wid] = incl;
-  __syncthreads();
-  if (wid == 0) {
-    Pre wv = (lane < WAVES) ? sm.pre[lane] : pre_empty();
-    Pre wi = wave_incl_pre(wv, inv_t);
-    float pu = __shfl_up(wi.u, 1, kWave);
-    double pS = __shfl_up(wi.S, 1, kWave);
-    Pre we = (lane == 0) ? pre_empty() : Pre{pu, pS};
-    if (lane < WAVES) sm.pre[lane] = pre_combine(carry, we, inv_t);
-    if (lane == WAVES - 1) sm.pre[WAVES] = pre_combine(carry, wi, inv_t);
+  const bool has = x.S != 0.0;
+  const bool chas = carry.S != 0.0;
+  // 1. anchor of the last non-empty group up to each thread
+  int lh = has ? 1 : 0;
+  float lu = x.u;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int oh = __shfl_up(lh, d, kWave);
+    const float ou = __shfl_up(lu, d, kWave);
+    if (lane >= d && !lh && oh) {
+      lh = 1;
+      lu = ou;
+    }
+  }
+  if (lane == kWave - 1) {
+    sm.ah[wid] = lh;
+    sm.au[wid] = lu;
   }
   __syncthreads();
-  Pre r = pre_combine(sm.pre[wid], lane_excl, inv_t);
-  *total = sm.pre[WAVES];
+  int wh = chas ? 1 : 0;   // the anchor entering this wave
+  float wu = carry.u;
+  for (int w = 0; w < wid; ++w)
+    if (sm.ah[w]) {
+      wh = 1;
+      wu = sm.au[w];
+    }
+  int ph = __shfl_up(lh, 1, kWave);
+  float pu = __shfl_up(lu, 1, kWave);
+  if (lane == 0 || !ph) {
+    ph = wh;
+    pu = wu;
+  }
+  // 2. P_i = A_i P_{i-1} + B_i
+  double A = has ? (ph ? wexp_f64(static_cast<double>(pu) - static_cast<double>(x.u), inv_t) : 0.0) : 1.0;
+  double B = has ? x.S : 0.0;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const double Ap = __shfl_up(A, d, kWave);
+    const double Bp = __shfl_up(B, d, kWave);
+    if (lane >= d) {
+      B = fma(A, Bp, B);
+      A *= Ap;
+    }
+  }
+  if (lane == kWave - 1) {
+    sm.A[wid] = A;
+    sm.B[wid] = B;
+  }
   __syncthreads();
-  return r;
+  const double P_in = chas ? carry.S : 0.0;
+  double P0 = P_in;   // P entering this wave
+  for (int w = 0; w < wid; ++w) P0 = fma(sm.A[w], P0, sm.B[w]);
+  double Pt = P_in;
+  int th = chas ? 1 : 0;
+  float tu = carry.u;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    Pt = fma(sm.A[w], Pt, sm.B[w]);
+    if (sm.ah[w]) {
+      th = 1;
+      tu = sm.au[w];
+    }
+  }
+  const double Pi = fma(A, P0, B);
+  double Pe = __shfl_up(Pi, 1, kWave);
+  if (lane == 0) Pe = P0;
+  *total = th ? Pre{tu, Pt} : pre_empty();
+  __syncthreads();
+  return ph ? Pre{pu, Pe} : pre_empty();
 }
 
 // Exclusive block scan of Suf from the right, seeded with carry (groups
-// after the block).  *total gets all (+) carry.
+// after the block).  *total gets all (+) carry.  Empty groups (T == 0) are
+// skipped.
 template <int WAVES>
 __device__ Suf block_excl_suf(Suf x, Suf carry, double inv_t, ScanSmem<WAVES>& sm, Suf* total) {
   const int lane = lane_id();
   const int wid = threadIdx.x / kWave;
-  Suf incl = wave_incl_suf(x, inv_t);
-  float ev = __shfl_down(incl.v, 1, kWave);
-  double eT = __shfl_down(incl.T, 1, kWave);
-  Suf lane_excl = (lane == kWave - 1) ? suf_empty() : Suf{ev, eT};
-  if (lane == 0) sm.suf[wid] = incl;
-  __syncthreads();
-  if (wid == 0) {
-    Suf wv = (lane < WAVES) ? sm.suf[lane] : suf_empty();
-    Suf wi = wave_incl_suf(wv, inv_t);
-    float nv = __shfl_down(wi.v, 1, kWave);
-    double nT = __shfl_down(wi.T, 1, kWave);
-    Suf we = (lane == kWave - 1) ? suf_empty() : Suf{nv, nT};
-    if (lane < WAVES) sm.suf[lane] = suf_combine(we, carry, inv_t);
-    if (lane == 0) sm.suf[WAVES] = suf_combine(wi, carry, inv_t);
+  const bool has = x.T != 0.0;
+  const bool chas = carry.T != 0.0;
+  // 1. anchor of the first non-empty group from each thread on
+  int lh = has ? 1 : 0;
+  float lv = x.v;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int oh = __shfl_down(lh, d, kWave);
+    const float ov = __shfl_down(lv, d, kWave);
+    if (lane + d < kWave && !lh && oh) {
+      lh = 1;
+      lv = ov;
+    }
+  }
+  if (lane == 0) {
+    sm.ah[wid] = lh;
+    sm.au[wid] = lv;
   }
   __syncthreads();
-  Suf r = suf_combine(lane_excl, sm.suf[wid], inv_t);
-  *total = sm.suf[WAVES];
+  int wh = chas ? 1 : 0;   // the anchor following this wave
+  float wv = carry.v;
+  for (int w = WAVES - 1; w > wid; --w)
+    if (sm.ah[w]) {
+      wh = 1;
+      wv = sm.au[w];
+    }
+  int nh = __shfl_down(lh, 1, kWave);
+  float nv = __shfl_down(lv, 1, kWave);
+  if (lane == kWave - 1 || !nh) {
+    nh = wh;
+    nv = wv;
+  }
+  // 2. T_i = B_i + A_i T_{i+1}
+  double A = has ? (nh ? wexp_f64(static_cast<double>(x.v) - static_cast<double>(nv), inv_t) : 0.0) : 1.0;
+  double B = has ? x.T : 0.0;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const double An = __shfl_down(A, d, kWave);
+    const double Bn = __shfl_down(B, d, kWave);
+    if (lane + d < kWave) {
+      B = fma(A, Bn, B);
+      A *= An;
+    }
+  }
+  if (lane == 0) {
+    sm.A[wid] = A;
+    sm.B[wid] = B;
+  }
   __syncthreads();
-  return r;
+  const double T_in = chas ? carry.T : 0.0;
+  double T0 = T_in;   // T following this wave
+  for (int w = WAVES - 1; w > wid; --w) T0 = fma(sm.A[w], T0, sm.B[w]);
+  double Tt = T_in;
+  int th = chas ? 1 : 0;
+  float tv = carry.v;
+#pragma unroll
+  for (int w = WAVES - 1; w >= 0; --w) {
+    Tt = fma(sm.A[w], Tt, sm.B[w]);
+    if (sm.ah[w]) {
+      th = 1;
+      tv = sm.au[w];
+    }
+  }
+  const double Ti = fma(A, T0, B);
+  double Te = __shfl_down(Ti, 1, kWave);
+  if (lane == kWave - 1) Te = T0;
+  *total = th ? Suf{tv, Tt} : suf_empty();
+  __syncthreads();
+  return nh ? Suf{nv, Te} : suf_empty();
 }
 
 // Number of threads in the block with flag set.

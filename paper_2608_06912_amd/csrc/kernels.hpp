@@ -185,10 +185,11 @@ int band_wave_cap(int64_t chunk);
 size_t band_ctx_bytes(int64_t n);
 BandCtx band_ctx_view(void* base, int64_t n);
 // ones: [ceil(n/32)] bit set where r >= hi (written only when a_R is finite).
+// Also launches the totals: *tot and each block's offset into M.
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
                             float aR, double t, int nblocks, int64_t chunk, float* stage_v,
                             int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
-                            hipStream_t s);
+                            int64_t* offsets, PartTotals* tot, hipStream_t s);
 // Emit after a certified bracket (skipped when rec->ok == 0): p from the band
 // lists and the ones bits, dense from r for blocks without usable lists; the
 // band entries get p in place; b_out[0] = rec->b; the context header is set.
@@ -202,9 +203,6 @@ hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s);
 hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const BandCtx& band,
                            float* gstash, double* partials, double* coef, double t, float* grad,
                            hipStream_t s);
-hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const SelectRec* sel,
-                                   int use_sel, float aL, float aR, int64_t* offsets,
-                                   PartTotals* tot, hipStream_t s);
 hipError_t launch_gather(const float* r, int64_t n, const PartTotals* tot, const PartBlock* blk,
                          const int64_t* offsets, int nblocks, int64_t chunk, const float* stage_v,
                          const int32_t* stage_i, int64_t m_capacity, uint32_t* m_keys,
@@ -214,6 +212,22 @@ hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, in
                                 bool with_idx, const PartTotals* tot, double k, double t,
                                 int64_t n_total, SolveRec* out, int32_t* m_idx_sorted,
                                 hipStream_t s);
+// Middle set solved by buckets of keys (only the bucket holding the root is
+// sorted).  acc: bucket accumulators, zero on entry and left zero.  The
+// record reports side = 2 (not ok) when that bucket exceeds kBucketSortCap
+// keys; the caller then solves M by the full sort.
+constexpr int kBucketCount = 2048;
+constexpr int kBucketSortCap = 4096;
+struct BucketAcc {
+  uint32_t* n;              // [kBucketCount]
+  unsigned long long* u;    // [kBucketCount]
+  unsigned long long* d;    // [kBucketCount]
+};
+constexpr int64_t kBucketAccWords = kBucketCount * 5;   // u32 words of n, u, d
+hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m, float mmin, float mmax,
+                               uint32_t kmin, uint32_t kmax, BucketAcc acc, const PartTotals* tot,
+                               double k, double t, int64_t n_total, SolveRec* out, hipStream_t s);
+
 // Copy sorted M indices to the caller's [m_capacity] row, -1 padded.
 hipError_t launch_write_m_idx(const int32_t* sorted_idx, int64_t m_len, int64_t m_capacity,
                               int32_t* out, hipStream_t s);

@@ -171,6 +171,7 @@ size_t forward_ws(int64_t n, bool with_perm) {
 struct BracketWs {
   uint32_t* ykeys;
   uint32_t* hist;
+  BucketAcc acc;
   SelectRec* sel;
   PartBlock* blk;
   int64_t* offsets;
@@ -195,7 +196,11 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
   BracketWs w{};
   w.nblocks = partition_blocks(n, &w.chunk);
   w.ykeys = c.take<uint32_t>(K);
-  w.hist = c.take<uint32_t>(kSelectBins);
+  // one zero-filled region: the sample histogram, then the bucket accumulators
+  w.hist = c.take<uint32_t>(kSelectBins + kBucketAccWords);
+  w.acc.n = w.hist + kSelectBins;
+  w.acc.u = reinterpret_cast<unsigned long long*>(w.hist + kSelectBins + kBucketCount);
+  w.acc.d = reinterpret_cast<unsigned long long*>(w.hist + kSelectBins + 3 * kBucketCount);
   w.sel = c.take<SelectRec>(1);
   w.blk = c.take<PartBlock>(w.nblocks);
   w.offsets = c.take<int64_t>(w.nblocks);
@@ -337,15 +342,14 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
   if (st != LAPSUM_OK) return st;
 
   if (!(flags & LAPSUM_FLAG_FULL_SORT)) {
-    LAPSUM_TRY(launch_fill_u32(w.hist, kSelectBins, 0u, s));
+    LAPSUM_TRY(launch_fill_u32(w.hist, kSelectBins + kBucketAccWords, 0u, s));
     LAPSUM_TRY(launch_sample(r, n, noise, K, w.ykeys, w.hist, s));
     LAPSUM_TRY(launch_select(w.ykeys, K, w.hist, j, l, w.sel, s));
     float aL = 0.0f, aR = 0.0f;
     for (int attempt = 1; attempt <= 3 && !solved; ++attempt) {
       const int use_sel = attempt == 1 ? 1 : 0;
       LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR, t, w.nblocks, w.chunk, w.stage_v,
-                                  w.stage_i, w.blk, band, w.ones, s));
-      LAPSUM_TRY(launch_partition_totals(w.blk, w.nblocks, w.sel, use_sel, aL, aR, w.offsets, w.tot, s));
+                                  w.stage_i, w.blk, band, w.ones, w.offsets, w.tot, s));
       LAPSUM_TRY(launch_gather(r, n, w.tot, w.blk, w.offsets, w.nblocks, w.chunk, w.stage_v,
                                w.stage_i, mcap, w.m_keys, w.m_idx, s));
       st = copy_back(&hs->tot, w.tot, ev, s);
@@ -371,39 +375,63 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
       }
       const bool want_idx = midx_row != nullptr;
       const int32_t* sorted_idx = nullptr;
-      if (tot.nM <= kRowOnChipMax) {
-        LAPSUM_TRY(launch_small_m_solve(w.m_keys, w.m_idx, tot.nM, want_idx, w.tot, k, t, n, w.rec,
-                                        w.m_idx_sorted, s));
-        sorted_idx = w.m_idx_sorted;
-      } else {
-        const uint32_t* mk = nullptr;
-        const int32_t* mv = nullptr;
-        LAPSUM_TRY(launch_sort(nullptr, w.m_keys, w.m_idx, want_idx, tot.nM, nullptr, w.msb,
-                               sort_pass_mask(tot.mmin, tot.mmax), &mk, &mv, s));
-        SolveArgs a{};
-        a.keys = mk;
-        a.len = tot.nM;
-        a.len_dev = nullptr;
-        a.k = k;
-        a.t = t;
-        a.n_total = n;
-        a.tails = w.tot;
-        a.tile_buf = w.m_tile_buf;
-        a.max_tiles = w.m_solve_tiles;
-        a.out = w.rec;
-        a.b_out = nullptr;
-        LAPSUM_TRY(launch_sorted_solve(a, s));
-        sorted_idx = want_idx ? mv : nullptr;
-      }
+      // M by sorting all of it (needed for the sorted indices, or when the
+      // bucket holding the root is too large for the on-chip sort)
+      auto solve_sorted = [&]() -> int {
+        if (tot.nM <= kRowOnChipMax) {
+          LAPSUM_TRY(launch_small_m_solve(w.m_keys, w.m_idx, tot.nM, want_idx, w.tot, k, t, n,
+                                          w.rec, w.m_idx_sorted, s));
+          sorted_idx = w.m_idx_sorted;
+        } else {
+          const uint32_t* mk = nullptr;
+          const int32_t* mv = nullptr;
+          LAPSUM_TRY(launch_sort(nullptr, w.m_keys, w.m_idx, want_idx, tot.nM, nullptr, w.msb,
+                                 sort_pass_mask(tot.mmin, tot.mmax), &mk, &mv, s));
+          SolveArgs a{};
+          a.keys = mk;
+          a.len = tot.nM;
+          a.len_dev = nullptr;
+          a.k = k;
+          a.t = t;
+          a.n_total = n;
+          a.tails = w.tot;
+          a.tile_buf = w.m_tile_buf;
+          a.max_tiles = w.m_solve_tiles;
+          a.out = w.rec;
+          a.b_out = nullptr;
+          LAPSUM_TRY(launch_sorted_solve(a, s));
+          sorted_idx = want_idx ? mv : nullptr;
+        }
+        return LAPSUM_OK;
+      };
       // the record goes back to the host while the emit runs; the emit (and
       // its write of b) happens only if this bracket was certified
-      st = copy_back(&hs->rec, w.rec, ev, s);
+      auto emit_and_read = [&](SolveRec* out) -> int {
+        int e = copy_back(&hs->rec, w.rec, ev, s);
+        if (e != LAPSUM_OK) return e;
+        LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, tot.aR < INFINITY ? 1 : 0,
+                                    p_row, b_row, s));
+        e = wait_back(ev);
+        if (e != LAPSUM_OK) return e;
+        *out = hs->rec;
+        return LAPSUM_OK;
+      };
+      const bool bucketed = !want_idx && tot.nM > 0;
+      if (bucketed) {
+        LAPSUM_TRY(launch_bucket_solve(w.m_keys, tot.nM, tot.mmin, tot.mmax, host_desc_key(tot.mmax),
+                                       host_desc_key(tot.mmin), w.acc, w.tot, k, t, n, w.rec, s));
+      } else {
+        st = solve_sorted();
+        if (st != LAPSUM_OK) return st;
+      }
+      SolveRec rec;
+      st = emit_and_read(&rec);
       if (st != LAPSUM_OK) return st;
-      LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, tot.aR < INFINITY ? 1 : 0, p_row,
-                                  b_row, s));
-      st = wait_back(ev);
-      if (st != LAPSUM_OK) return st;
-      const SolveRec rec = hs->rec;
+      if (bucketed && rec.side == 2) {
+        st = solve_sorted();
+        if (st == LAPSUM_OK) st = emit_and_read(&rec);
+        if (st != LAPSUM_OK) return st;
+      }
       rec_info.lap_aL = rec.lap_aL;
       rec_info.lap_aR = rec.lap_aR;
       if (rec.ok) {

@@ -151,17 +151,7 @@ def test_devicewide_backward(lib, n, alpha):
 
 
 # -------------------------------------------------------------- bracketed --
-def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label="", g=None):
-    """Bracketed forward (with a saved band) against the oracle's bracketed
-    model; with an upstream gradient g also the backward from the band,
-    against Eq. (5) and against the p-form backward."""
-    import torch
-    band = lib.new_band(1, len(r32), "cuda")
-    p, b, infos, midx = lib.lapsum_forward_bracketed(_t(r32[None, :]), k, alpha, _t(noise), z=z,
-                                                     m_capacity=m_capacity, m_idx=True, band=band)
-    info = infos[0]
-    po, bo, oinfo, oms = O.bracketed_forward(r32, k, alpha, noise, z=z,
-                                             m_capacity=m_capacity or len(r32))
+def _check_info(info, oinfo, label):
     assert (info["j"], info["l"]) == (oinfo.j, oinfo.l), (label, info, oinfo)
     assert (info["attempts"], info["fell_back"], info["m_overflow"]) == \
         (oinfo.attempts, oinfo.fell_back, oinfo.m_overflow), (label, info, oinfo)
@@ -182,7 +172,29 @@ def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label="
             assert math.isnan(info[f]) and math.isnan(ref)
         else:
             assert abs(info[f] - ref) <= 1e-6 * scale, (label, f, info[f], ref)
+
+
+def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label="", g=None):
+    """Bracketed forward against the oracle's bracketed model, twice: with a
+    saved band and no M indices (M solved by buckets, the benchmark's
+    configuration), then with the sorted M indices (M sorted in full).
+    With an upstream gradient g also the backward from the band, against
+    Eq. (5) and against the p-form backward."""
+    import torch
+    band = lib.new_band(1, len(r32), "cuda")
+    po, bo, oinfo, oms = O.bracketed_forward(r32, k, alpha, noise, z=z,
+                                             m_capacity=m_capacity or len(r32))
     t = -alpha
+    pb, bb, infos_b, _ = lib.lapsum_forward_bracketed(_t(r32[None, :]), k, alpha, _t(noise), z=z,
+                                                      m_capacity=m_capacity, band=band)
+    _check_info(infos_b[0], oinfo, label + " (buckets)")
+    assert abs(float(_np(bb)[0]) - bo) <= 2e-6 * t, (label, float(_np(bb)[0]), bo)
+    pbn = _np(pb)[0]
+    assert O.budget_error(pbn, k) <= sum_tol(k), label
+    p, b, infos, midx = lib.lapsum_forward_bracketed(_t(r32[None, :]), k, alpha, _t(noise), z=z,
+                                                     m_capacity=m_capacity, m_idx=True)
+    info = infos[0]
+    _check_info(info, oinfo, label + " (sorted)")
     b_gpu = float(_np(b)[0])
     assert abs(b_gpu - bo) <= 2e-6 * t, (label, b_gpu, bo)
     m = _np(midx)[0]
@@ -192,15 +204,17 @@ def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label="
         assert np.all(m[nm:] == -1)
     else:
         assert np.all(m == -1)
+    # both forwards emit p of the same closed form from b's within 2e-6 t
+    assert np.max(np.abs(pbn.astype(np.float64) - _np(p)[0].astype(np.float64))) <= 2 * P_TOL, label
     if g is not None:
         gt = _t(g[None, :])
-        gb = _np(lib.lapsum_backward_band(gt, p, band, alpha))[0]
-        gp = _np(lib.lapsum_backward(gt, p, b, alpha))[0]
+        gb = _np(lib.lapsum_backward_band(gt, pb, band, alpha))[0]
+        gp = _np(lib.lapsum_backward(gt, pb, bb, alpha))[0]
         assert grad_rel(gb, O.vjp(r32, bo, alpha, g)) <= G_TOL, (label, "band backward")
         # same f from the same p; only the summation order differs
         assert grad_rel(gb, gp.astype(np.float64)) <= 1e-6, (label, "band vs p-form")
         assert np.all(gb[gp == 0.0] == 0.0), label
-    return _np(p)[0], b_gpu, bo, info
+    return pbn, float(_np(bb)[0]), bo, infos_b[0]
 
 
 @pytest.mark.parametrize("case", range(6))
@@ -270,6 +284,24 @@ def test_bracketed_band_with_scores_above_it(lib):
     assert np.max(np.abs(p.astype(np.float64) - p_ref)) <= P_TOL
     assert np.count_nonzero(p == 1.0) > n // 4
     assert O.budget_error(p, k) <= sum_tol(k)
+
+
+def test_bracketed_root_in_a_large_tie(lib):
+    # 20000 copies of one value at the target quantile put more keys into
+    # the bucket holding the root than the on-chip sort takes: the middle set
+    # is then solved by the full sort
+    n = 200_000
+    r = W.random_case(28, n, dist="normal")[0]
+    v = np.float32(np.quantile(r, 0.9))
+    r[np.random.default_rng(29).choice(n, 20_000, replace=False)] = v
+    alpha = -0.05
+    k = O.lapsum(r, float(v), 0.05)   # the root is the tied value itself
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([83], K, 0.05)
+    g = W.random_case(30, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label="tie", g=g)
+    assert info["n_M"] > 20_000 and not info["fell_back"]
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
 
 
 @pytest.mark.timeout(300)
