@@ -65,10 +65,17 @@ __device__ __forceinline__ bool block_dense(const BandCtx& c, int64_t n) {
   return !lists_usable(c);
 }
 
-// Build the map of this block's band.  value(rank, entry, slot) gives the
-// float stored for each member.  Ends with a barrier.
+// Build the map of this block's band.  Entries come either as the
+// partition left them (four wave segments, each in the order its members
+// were met; `from_segments`) or as the emit leaves them (one list in index
+// order at the start of the block's region).  value(entry, rank) gives the
+// float stored for each member; with `writeback` the members are written
+// back as one list in index order, each carrying its value.  Ends with a
+// barrier.
 template <typename Value>
-__device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L, Value&& value) {
+__device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L,
+                          bool from_segments, bool writeback, Value&& value) {
+  constexpr int EPT = kMaxEnt / BT;   // entries per thread
   const int tid = threadIdx.x;
   if (tid == 0) {
     int acc = 0;
@@ -84,15 +91,28 @@ __device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L,
   for (int w = tid; w < nwords; w += BT) L.bits[w] = 0u;
   __syncthreads();
   const int total = L.seg[BW];
-  for (int e = tid; e < total; e += BT) {
-    int w = 0;
+  BandEntry* base = c.ent + static_cast<int64_t>(blockIdx.x) * BW * c.cap;
+  BandEntry en[EPT];
+  int off[EPT];
 #pragma unroll
-    for (int q = 1; q < BW; ++q) w += (e >= L.seg[q]) ? 1 : 0;
-    const int64_t slot = (static_cast<int64_t>(blockIdx.x) * BW + w) * c.cap + (e - L.seg[w]);
-    const BandEntry en = c.ent[slot];
-    const int64_t o = static_cast<int64_t>(en.idx) - b0;
-    if (o >= 0 && o < len) atomicOr(&L.bits[o >> 5], 1u << (o & 31));
-    L.vals[e] = value(e, en, slot);
+  for (int q = 0; q < EPT; ++q) {
+    const int e = tid + q * BT;
+    off[q] = -1;
+    if (e < total) {
+      int j = e;
+      if (from_segments) {
+        int w = 0;
+#pragma unroll
+        for (int x = 1; x < BW; ++x) w += (e >= L.seg[x]) ? 1 : 0;
+        j = w * c.cap + (e - L.seg[w]);
+      }
+      en[q] = base[j];
+      const int64_t o = static_cast<int64_t>(en[q].idx) - b0;
+      if (o >= 0 && o < len) {
+        off[q] = static_cast<int>(o);
+        atomicOr(&L.bits[o >> 5], 1u << (o & 31));
+      }
+    }
   }
   __syncthreads();
   // exclusive prefix of the members per word: each thread owns a run of words
@@ -120,6 +140,24 @@ __device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L,
     if (w0 + q < nwords) {
       L.pre[w0 + q] = run;
       run += static_cast<uint32_t>(__popc(L.bits[w0 + q]));
+    }
+  }
+  __syncthreads();
+  // each member's rank in index order
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    if (off[q] >= 0) {
+      const int o = off[q];
+      const uint32_t word = L.bits[o >> 5];
+      const int rank = static_cast<int>(L.pre[o >> 5] + __popc(word & ((1u << (o & 31)) - 1u)));
+      const float val = value(en[q], rank);
+      L.vals[rank] = val;
+      if (writeback) {
+        BandEntry w;
+        w.idx = en[q].idx;
+        w.bits = __float_as_uint(val);
+        base[rank] = w;
+      }
     }
   }
   __syncthreads();
@@ -206,13 +244,8 @@ __global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__
     dense_emit(r, br.b0, br.b1, b, inv_t, p);
     return;
   }
-  build_map(c, br.b0, br.b1 - br.b0, L, [&](int, const BandEntry& en, int64_t slot) {
-    const float pv = laplace_p(__uint_as_float(en.bits), b, inv_t);
-    BandEntry o;
-    o.idx = en.idx;
-    o.bits = __float_as_uint(pv);
-    c.ent[slot] = o;
-    return pv;
+  build_map(c, br.b0, br.b1 - br.b0, L, true, true, [&](const BandEntry& en, int) {
+    return laplace_p(__uint_as_float(en.bits), b, inv_t);
   });
   write_dense(br.b0, br.b1, L, ones, p);
 }
@@ -250,7 +283,6 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
                                                              float* __restrict__ gstash,
                                                              double* __restrict__ partials) {
   __shared__ double red[2][BW];
-  __shared__ int seg[BW + 1];
   const int tid = threadIdx.x;
   const BlockRange br = block_range(n, c.chunk);
   double F = 0.0, G = 0.0;
@@ -264,23 +296,11 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
       }
     }
   } else {
-    if (tid == 0) {
-      int acc = 0;
-      const BandBlock& bb = c.blk[blockIdx.x];
-#pragma unroll
-      for (int w = 0; w < BW; ++w) {
-        seg[w] = acc;
-        acc += bb.cnt[w];
-      }
-      seg[BW] = acc;
-    }
-    __syncthreads();
-    const int total = seg[BW];
+    // after the emit the block's members form one list in index order
+    const BandBlock& bb = c.blk[blockIdx.x];
+    const int total = bb.cnt[0] + bb.cnt[1] + bb.cnt[2] + bb.cnt[3];
     for (int e = tid; e < total; e += BT) {
-      int w = 0;
-#pragma unroll
-      for (int q = 1; q < BW; ++q) w += (e >= seg[q]) ? 1 : 0;
-      const int64_t slot = (static_cast<int64_t>(blockIdx.x) * BW + w) * c.cap + (e - seg[w]);
+      const int64_t slot = static_cast<int64_t>(blockIdx.x) * BW * c.cap + e;
       const BandEntry en = c.ent[slot];
       const float pv = __uint_as_float(en.bits);
       const float f = fminf(pv, 1.0f - pv);
@@ -330,10 +350,11 @@ __global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restri
     }
     return;
   }
-  build_map(c, br.b0, br.b1 - br.b0, L, [&](int, const BandEntry& en, int64_t slot) {
+  const float* gs = gstash + static_cast<int64_t>(blockIdx.x) * BW * c.cap;
+  build_map(c, br.b0, br.b1 - br.b0, L, false, false, [&](const BandEntry& en, int rank) {
     const float pv = __uint_as_float(en.bits);
     const float f = fminf(pv, 1.0f - pv);
-    return (f != 0.0f) ? f * scale * (gstash[slot] - coef) : 0.0f;
+    return (f != 0.0f) ? f * scale * (gs[rank] - coef) : 0.0f;
   });
   write_dense(br.b0, br.b1, L, nullptr, grad);
 }

@@ -233,7 +233,7 @@ struct PartState {
   int64_t nL, nR;
   int64_t nM;   // M count of this wave (uniform across the wave)
   float mmin, mmax;
-  int64_t nB;   // band count of this wave (uniform across the wave)
+  int64_t nB;   // unused by the pass (the band count is the wave's LDS counter)
 };
 
 // Where a wave stages its band members and its bits of r >= hi.  Both go
@@ -244,6 +244,7 @@ constexpr int kOnesWaveWords = static_cast<int>(kBandMaxChunk / 4 / 32);   // 51
 
 struct BandWave {
   BandEntry* sbuf;   // LDS, cap entries
+  uint32_t* scnt;    // LDS counter of the wave's band members
   uint32_t* sones;   // LDS, kOnesWaveWords words: bit i of the wave's range
   int cap;
   bool stage;        // false when the block's range is too long for the band passes
@@ -323,29 +324,21 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       x |= __shfl_xor(x, 4, kWave);
       if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
     }
-    if (!__ballot(bb != 0u)) return;   // no lane holds a band member
-    {
-      uint32_t before = 0, total = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint64_t bal = __ballot((bb >> e) & 1u);
-        before += lanes_below(bal);
-        total += static_cast<uint32_t>(__popcll(bal));
-      }
-      int64_t slot = st.nB + before;
+    // band members are appended through the wave's LDS counter (in any
+    // order; the list is put in index order once, at the end of the range)
+    if (bb) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if ((bb >> e) & 1u) {
-          if (slot < bw.cap) {
+          const uint32_t slot = atomicAdd(bw.scnt, 1u);
+          if (slot < static_cast<uint32_t>(bw.cap)) {
             BandEntry en;
             en.idx = static_cast<int32_t>(i0 + e);
             en.bits = __float_as_uint(v[e]);
             bw.sbuf[slot] = en;
           }
-          ++slot;
         }
       }
-      st.nB += total;
     }
     if (__ballot(mb != 0u)) {   // rare: some lane holds an M member
       uint32_t before = 0, total = 0;
@@ -577,9 +570,12 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   const int64_t w0 = b0 + wid * wq < n ? b0 + wid * wq : n;
   const int64_t w1 = w0 + wq < n ? w0 + wq : n;
   const bool vec = (reinterpret_cast<uintptr_t>(r) & 15) == 0;
+  __shared__ uint32_t scnt[PW];
   BandWave bw;
   bw.sbuf = sband[wid];
   bw.sones = sones[wid];
+  bw.scnt = &scnt[wid];
+  if (lane == 0) scnt[wid] = 0u;   // wave-private: the wave's LDS accesses stay in order
   bw.stage = chunk <= kBandMaxChunk;
   bw.cap = bw.stage ? (bcap < kBandWaveCapMax ? bcap : kBandWaveCapMax) : 0;
   // rounded outwards so that the float comparisons imply the float64 bounds
@@ -592,14 +588,17 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
     partition_range<true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
   else
     partition_range<false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
-  // this wave's band list and bits out of LDS
+  st.nB = *bw.scnt;
+  // this wave's bits and band list (in the order the members were met) out
+  // of LDS; the emit puts the block's list in index order
   if (bw.stage) {
-    BandEntry* out = bent + (static_cast<int64_t>(blockIdx.x) * PW + wid) * bcap;
-    const int64_t nb = st.nB < bw.cap ? st.nB : bw.cap;
-    for (int64_t q = lane; q < nb; q += kWave) out[q] = bw.sbuf[q];
     if (has_r) {
-      const int64_t nw = (w1 - w0 + 31) / 32;
-      for (int64_t q = lane; q < nw; q += kWave) ones[(w0 >> 5) + q] = bw.sones[q];
+      const int nw = static_cast<int>((w1 - w0 + 31) / 32);   // <= kOnesWaveWords
+      for (int q = lane; q < nw; q += kWave) ones[(w0 >> 5) + q] = bw.sones[q];
+    }
+    if (st.nB <= bw.cap) {
+      BandEntry* out = bent + (static_cast<int64_t>(blockIdx.x) * PW + wid) * bcap;
+      for (int q = lane; q < static_cast<int>(st.nB); q += kWave) out[q] = bw.sbuf[q];
     }
   }
   if (lane == 0) {
