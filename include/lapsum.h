@@ -127,10 +127,13 @@ int lapsum_backward(const float* grad_p, const float* p, const double* b,
  *  3. one pass over r: L = {r < a_L}, M = {a_L <= r < a_R}, R = {r >= a_R},
  *     the tail sums of Eq. (7) S_L = sum_L e^{-(a_L - r)/t},
  *     S_R = sum_R e^{-(r - a_R)/t}, the counts, and M gathered in index order;
- *  4. M sorted descending; the scan of Suppl. A on sorted M with the tails as
+ *  4. the scan of Suppl. A over M in descending order with the tails as
  *     carries gives LapSum(a_L) and LapSum(a_R); the bracket is certified when
- *     LapSum(a_R) <= k <= LapSum(a_L);
- *  5. certified: b by the closed-form root on sorted M (Suppl. B).  Not
+ *     LapSum(a_R) <= k <= LapSum(a_L).  M is scanned in 2048 buckets of
+ *     consecutive keys and only the bucket holding the root is sorted (all of
+ *     M is sorted when m_idx_out is requested, or when that bucket holds more
+ *     than 4096 scores); both give the same b;
+ *  5. certified: b by the closed-form root (Suppl. B).  Not
  *     certified: the failing side is widened by one-sided doubling
  *     (LapSum(a_R) > k: a_L <- a_R, a_R <- a_R + 2 (a_R - a_L); LapSum(a_L) < k:
  *     a_R <- a_L, a_L <- a_L - 2 (a_R - a_L); float64 arithmetic on the
@@ -169,8 +172,9 @@ int lapsum_backward(const float* grad_p, const float* p, const double* b,
  *   band        NULL, or device memory of at least lapsum_band_size(batch, n)
  *               bytes, 256-byte aligned (band_bytes its size): receives the
  *               band of each row with its p, for lapsum_backward_band.  Its
- *               content is private to the library; it stays valid until the
- *               caller reuses the memory.
+ *               content is private to the library; it is valid once the
+ *               call's work on `stream` has completed and until the caller
+ *               reuses the memory.
  * ------------------------------------------------------------------------ */
 #define LAPSUM_FLAG_FULL_SORT 1u
 
