@@ -222,11 +222,13 @@ __device__ void dense_emit(const float* __restrict__ r, int64_t b0, int64_t b1, 
 __global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__ r, int64_t n,
                                                        const SolveRec* __restrict__ rec,
                                                        double inv_t, BandCtx c,
-                                                       const uint32_t* __restrict__ ones,
+                                                       const uint32_t* __restrict__ ones_all,
+                                                       const PartTotals* __restrict__ tot,
                                                        float* __restrict__ p,
                                                        double* __restrict__ b_out) {
   __shared__ BandLds L;
   if (!rec->ok) return;
+  const uint32_t* ones = tot->aR < INFINITY ? ones_all : nullptr;
   const double b = rec->b;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     b_out[0] = b;
@@ -251,11 +253,11 @@ __global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__
 }
 
 hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, double t,
-                            const BandCtx& band, const uint32_t* ones, int has_ones, float* p,
-                            double* b_out, hipStream_t s) {
+                            const BandCtx& band, const uint32_t* ones, const PartTotals* tot,
+                            float* p, double* b_out, hipStream_t s) {
   { ProfScope ps_("band_emit", s);
   hipLaunchKernelGGL(band_emit_kernel, dim3(band.nblocks), dim3(BT), 0, s, r, n, rec, 1.0 / t, band,
-                     has_ones ? ones : nullptr, p, b_out); }
+                     ones, tot, p, b_out); }
   return hipGetLastError();
 }
 

@@ -25,9 +25,11 @@
 // sum that enters LapSum with weight 1/2.
 //
 // Two launches: bucket_count (one block per 4096 keys of M) and
-// bucket_solve (one workgroup).  When bucket d* holds more keys than the
-// workgroup can sort (kBucketSortCap) the record reports side = 2 and the
-// caller solves M by the full sort instead.
+// bucket_solve (one workgroup).  Both read |M| and its range from the
+// partition totals on the device, so the host need not wait for them.  When
+// bucket d* holds more keys than the workgroup can sort (kBucketSortCap) the
+// record reports side = 2, and when |M| exceeds what the launch covers (or M
+// was not gathered) side = 3; the caller then solves M by the full sort.
 #include <math.h>
 
 #include "block_sort.hpp"
@@ -67,13 +69,34 @@ __device__ __forceinline__ float bucket_lo(const BucketGeom& g, int d) {
   return fmaxf(key_float(key), g.mmin);
 }
 
+// Bucket geometry from the range of M, the same in every block.
+__device__ __forceinline__ BucketGeom geom_of(const PartTotals& T) {
+  BucketGeom g;
+  g.mmin = T.mmin;
+  g.mmax = T.mmax;
+  g.kmin = desc_key(T.mmax);
+  g.kmax = desc_key(T.mmin);
+  const uint32_t span = g.kmax - g.kmin;
+  const int bits = span ? 32 - __clz(static_cast<int>(span)) : 0;
+  g.shift = bits > 11 ? bits - 11 : 0;
+  return g;
+}
+
+// |M| terms of at most 2^F each fit in 62 bits.
+__device__ __forceinline__ int fixed_bits(int64_t m) {
+  const int mbits = m > 0 ? 64 - __clzll(static_cast<long long>(m)) : 0;
+  return 62 - mbits;
+}
+
 }  // namespace
 
 // acc: [kBuckets] u32 counts, then [kBuckets] u64 U, then [kBuckets] u64 D;
-// zero on entry (bucket_solve clears it again).
+// zero on entry (bucket_solve clears it again).  |M| and its range come from
+// the partition totals; nothing is counted when |M| exceeds m_cap (M was not
+// gathered) or the keys this grid covers.
 __global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __restrict__ keys,
-                                                          int64_t m, BucketGeom g, double c2,
-                                                          double fscale,
+                                                          const PartTotals* __restrict__ tot,
+                                                          int64_t m_cap, double c2,
                                                           uint32_t* __restrict__ acc_n,
                                                           unsigned long long* __restrict__ acc_u,
                                                           unsigned long long* __restrict__ acc_d) {
@@ -81,13 +104,19 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __rest
   __shared__ unsigned long long cu[kBuckets];
   __shared__ unsigned long long cd[kBuckets];
   const int tid = threadIdx.x;
+  const PartTotals T = *tot;
+  const int64_t m = T.nM;
+  if (m < 1 || m > m_cap || m > static_cast<int64_t>(gridDim.x) * CT * CI) return;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * CT * CI;
+  if (base >= m) return;   // the launch is sized for the largest expected |M|
+  const BucketGeom g = geom_of(T);
+  const double fscale = ldexp(1.0, fixed_bits(m));
   for (int e = tid; e < kBuckets; e += CT) {
     cn[e] = 0u;
     cu[e] = 0ull;
     cd[e] = 0ull;
   }
   __syncthreads();
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * CT * CI;
 #pragma unroll
   for (int i = 0; i < CI; ++i) {
     const int64_t pos = base + i * CT + tid;
@@ -152,8 +181,7 @@ __device__ double sort_and_solve(uint32_t* buf, int c, const BucketGeom& g, doub
 // folds need one exponential per bucket and no search for the previous
 // non-empty bucket; the block scans then join the threads.
 __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __restrict__ keys,
-                                                          int64_t m, BucketGeom g,
-                                                          double inv_fscale,
+                                                          int64_t m_cap, int64_t m_grid,
                                                           uint32_t* __restrict__ acc_n,
                                                           unsigned long long* __restrict__ acc_u,
                                                           unsigned long long* __restrict__ acc_d,
@@ -176,6 +204,34 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
   const double inv_t = 1.0 / t;
   const Tails x = load_tails(tot);
   const int d0 = BPT * tid;
+  const int64_t m = tot->nM;
+  if (m > m_cap || m > m_grid) {
+    // M was not gathered, or not counted: the caller solves with |M| known
+    if (tid == 0) {
+      SolveRec rec;
+      rec.b = 0.0;
+      rec.lap_aL = NAN;
+      rec.lap_aR = NAN;
+      rec.ok = 0;
+      rec.side = 3;
+      *out = rec;
+    }
+    return;
+  }
+  if (m == 0) {
+    // every score is in a tail
+    if (tid == 0) {
+      SolveRec rec;
+      rec.ok = 1;
+      rec.side = 0;
+      certify(x, 0.0, static_cast<double>(n_total), k, t, x.pre, x.suf, rec);
+      rec.b = root_above(x, x.suf, k, t);
+      *out = rec;
+    }
+    return;
+  }
+  const BucketGeom g = geom_of(*tot);
+  const double inv_fscale = ldexp(1.0, -fixed_bits(m));
 
   // 1. this thread's buckets, cleared behind us for the next attempt
   uint32_t cnt[BPT];
@@ -366,36 +422,20 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
   }
 }
 
-int bucket_shift(uint32_t kmin, uint32_t kmax) {
-  const uint32_t span = kmax - kmin;
-  int bits = 0;
-  while (bits < 32 && (span >> bits) != 0u) ++bits;
-  return bits > 11 ? bits - 11 : 0;
-}
-
-hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m, float mmin, float mmax,
-                               uint32_t kmin, uint32_t kmax, BucketAcc acc, const PartTotals* tot,
-                               double k, double t, int64_t n_total, SolveRec* out, hipStream_t s) {
-  if (m < 1 || !(mmin <= mmax)) return hipErrorInvalidValue;
-  BucketGeom g;
-  g.kmin = kmin;
-  g.kmax = kmax;
-  g.shift = bucket_shift(kmin, kmax);
-  g.mmin = mmin;
-  g.mmax = mmax;
-  int mbits = 0;
-  while (mbits < 63 && (static_cast<uint64_t>(m) >> mbits) != 0u) ++mbits;
-  const int F = 62 - mbits;   // |M| terms of at most 2^F each fit in 62 bits
-  const double fscale = ldexp(1.0, F);
-  const int64_t blocks = (m + CT * CI - 1) / (CT * CI);
+hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m_cap, int64_t m_grid, BucketAcc acc,
+                               const PartTotals* tot, double k, double t, int64_t n_total,
+                               SolveRec* out, hipStream_t s) {
+  if (m_grid < 1) m_grid = 1;
+  const int64_t blocks = (m_grid + CT * CI - 1) / (CT * CI);
+  const int64_t covered = blocks * CT * CI;
   { ProfScope ps_("bucket_count", s);
   hipLaunchKernelGGL(bucket_count_kernel, dim3(static_cast<unsigned>(blocks)), dim3(CT), 0, s,
-                     m_keys, m, g, kLog2e / t, fscale, acc.n, acc.u, acc.d); }
+                     m_keys, tot, m_cap, kLog2e / t, acc.n, acc.u, acc.d); }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("bucket_solve", s);
-  hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, m_keys, m, g, 1.0 / fscale,
-                     acc.n, acc.u, acc.d, tot, k, t, n_total, out); }
+  hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, m_keys, m_cap, covered, acc.n,
+                     acc.u, acc.d, tot, k, t, n_total, out); }
   return hipGetLastError();
 }
 

@@ -191,11 +191,12 @@ hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int
                             int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
                             int64_t* offsets, PartTotals* tot, hipStream_t s);
 // Emit after a certified bracket (skipped when rec->ok == 0): p from the band
-// lists and the ones bits, dense from r for blocks without usable lists; the
-// band entries get p in place; b_out[0] = rec->b; the context header is set.
+// lists and the ones bits (used when tot->aR is finite), dense from r for
+// blocks without usable lists; each block's list is written back in index
+// order with p; b_out[0] = rec->b; the context header is set.
 hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, double t,
-                            const BandCtx& band, const uint32_t* ones, int has_ones, float* p,
-                            double* b_out, hipStream_t s);
+                            const BandCtx& band, const uint32_t* ones, const PartTotals* tot,
+                            float* p, double* b_out, hipStream_t s);
 // Mark a context as dense (rows solved by the full sort).
 hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s);
 // Backward from a saved band: partial (sum f, sum f g) per block, the
@@ -213,9 +214,12 @@ hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, in
                                 int64_t n_total, SolveRec* out, int32_t* m_idx_sorted,
                                 hipStream_t s);
 // Middle set solved by buckets of keys (only the bucket holding the root is
-// sorted).  acc: bucket accumulators, zero on entry and left zero.  The
-// record reports side = 2 (not ok) when that bucket exceeds kBucketSortCap
-// keys; the caller then solves M by the full sort.
+// sorted), reading |M| and its range from *tot on the device.  acc: bucket
+// accumulators, zero on entry and left zero.  m_cap: the capacity of M;
+// m_grid: the largest |M| the launch is sized for.  The record reports
+// ok = 0 with side = 2 when the root's bucket exceeds kBucketSortCap keys and
+// side = 3 when |M| exceeds m_cap or m_grid; the caller then solves M by the
+// full sort.
 constexpr int kBucketCount = 2048;
 constexpr int kBucketSortCap = 4096;
 struct BucketAcc {
@@ -224,9 +228,9 @@ struct BucketAcc {
   unsigned long long* d;    // [kBucketCount]
 };
 constexpr int64_t kBucketAccWords = kBucketCount * 5;   // u32 words of n, u, d
-hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m, float mmin, float mmax,
-                               uint32_t kmin, uint32_t kmax, BucketAcc acc, const PartTotals* tot,
-                               double k, double t, int64_t n_total, SolveRec* out, hipStream_t s);
+hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m_cap, int64_t m_grid, BucketAcc acc,
+                               const PartTotals* tot, double k, double t, int64_t n_total,
+                               SolveRec* out, hipStream_t s);
 
 // Copy sorted M indices to the caller's [m_capacity] row, -1 padded.
 hipError_t launch_write_m_idx(const int32_t* sorted_idx, int64_t m_len, int64_t m_capacity,

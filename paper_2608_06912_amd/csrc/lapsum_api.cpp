@@ -168,6 +168,13 @@ size_t forward_ws(int64_t n, bool with_perm) {
 }
 
 // --------------------------------------------------------------- bracket --
+// The totals of a partition and the record of its solve, next to each other
+// so that one copy brings both back to the host.
+struct AttemptRec {
+  PartTotals tot;
+  SolveRec rec;
+};
+
 struct BracketWs {
   uint32_t* ykeys;
   uint32_t* hist;
@@ -175,7 +182,8 @@ struct BracketWs {
   SelectRec* sel;
   PartBlock* blk;
   int64_t* offsets;
-  PartTotals* tot;
+  AttemptRec* att;
+  PartTotals* tot;     // &att->tot
   float* stage_v;
   int32_t* stage_i;
   uint32_t* m_keys;
@@ -184,7 +192,7 @@ struct BracketWs {
   SortBuffers msb;     // device-wide sort of M (|M| > on-chip limit)
   int64_t m_solve_tiles;
   double* m_tile_buf;
-  SolveRec* rec;
+  SolveRec* rec;       // &att->rec
   FullWs fall;         // full-sort fallback
   uint32_t* ones;      // [ceil(n/32)] scores at or above the band (finite a_R)
   void* band;          // one row's band when the caller keeps none
@@ -204,7 +212,8 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
   w.sel = c.take<SelectRec>(1);
   w.blk = c.take<PartBlock>(w.nblocks);
   w.offsets = c.take<int64_t>(w.nblocks);
-  w.tot = c.take<PartTotals>(1);
+  w.att = c.take<AttemptRec>(1);
+  w.tot = w.att ? &w.att->tot : nullptr;
   w.stage_v = c.take<float>(static_cast<size_t>(w.nblocks) * kPartStageCap);
   w.stage_i = c.take<int32_t>(static_cast<size_t>(w.nblocks) * kPartStageCap);
   w.m_keys = c.take<uint32_t>(mcap);
@@ -222,7 +231,7 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
     w.m_solve_tiles = mt;
     w.m_tile_buf = c.take<double>(static_cast<size_t>(mt) * kSolveTileDoubles);
   }
-  w.rec = c.take<SolveRec>(1);
+  w.rec = w.att ? &w.att->rec : nullptr;
   if (n > kRowOnChipMax) w.fall = carve_full(c, n, false);
   w.ones = c.take<uint32_t>(static_cast<size_t>((n + 31) / 32));
   w.band = c.take<char>(band_ctx_bytes(n));
@@ -284,8 +293,7 @@ void widen(float* aL, float* aR, int side) {
 // thread, allocated on its first use and kept), and the event that tells
 // the host a copy has landed while later work proceeds on the stream.
 struct HostStage {
-  PartTotals tot;
-  SolveRec rec;
+  AttemptRec att;
 };
 struct ThreadStage {
   HostStage* h = nullptr;
@@ -346,37 +354,18 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
     LAPSUM_TRY(launch_sample(r, n, noise, K, w.ykeys, w.hist, s));
     LAPSUM_TRY(launch_select(w.ykeys, K, w.hist, j, l, w.sel, s));
     float aL = 0.0f, aR = 0.0f;
+    const bool want_idx = midx_row != nullptr;
+    int64_t prev_m = -1;
     for (int attempt = 1; attempt <= 3 && !solved; ++attempt) {
       const int use_sel = attempt == 1 ? 1 : 0;
       LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR, t, w.nblocks, w.chunk, w.stage_v,
                                   w.stage_i, w.blk, band, w.ones, w.offsets, w.tot, s));
       LAPSUM_TRY(launch_gather(r, n, w.tot, w.blk, w.offsets, w.nblocks, w.chunk, w.stage_v,
                                w.stage_i, mcap, w.m_keys, w.m_idx, s));
-      st = copy_back(&hs->tot, w.tot, ev, s);
-      if (st == LAPSUM_OK) st = wait_back(ev);
-      if (st != LAPSUM_OK) return st;
-      const PartTotals tot = hs->tot;
-      aL = tot.aL;
-      aR = tot.aR;
-      rec_info.attempts = attempt;
-      rec_info.a_L = tot.aL;
-      rec_info.a_R = tot.aR;
-      rec_info.n_L = tot.nL;
-      rec_info.n_M = tot.nM;
-      rec_info.n_R = tot.nR;
-      rec_info.T_L = tot.TL;
-      rec_info.T_R = tot.TR;
-      if (tot.nM > mcap) {
-        // no room for M: the certificate is never evaluated
-        rec_info.m_overflow = 1;
-        rec_info.lap_aL = NAN;
-        rec_info.lap_aR = NAN;
-        break;
-      }
-      const bool want_idx = midx_row != nullptr;
       const int32_t* sorted_idx = nullptr;
+      PartTotals tot;
       // M by sorting all of it (needed for the sorted indices, or when the
-      // bucket holding the root is too large for the on-chip sort)
+      // buckets cannot take it); |M| known on the host
       auto solve_sorted = [&]() -> int {
         if (tot.nM <= kRowOnChipMax) {
           LAPSUM_TRY(launch_small_m_solve(w.m_keys, w.m_idx, tot.nM, want_idx, w.tot, k, t, n,
@@ -404,34 +393,64 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
         }
         return LAPSUM_OK;
       };
-      // the record goes back to the host while the emit runs; the emit (and
+      // the records come back to the host while the emit runs; the emit (and
       // its write of b) happens only if this bracket was certified
-      auto emit_and_read = [&](SolveRec* out) -> int {
-        int e = copy_back(&hs->rec, w.rec, ev, s);
+      auto emit_and_read = [&]() -> int {
+        int e = copy_back(&hs->att, w.att, ev, s);
         if (e != LAPSUM_OK) return e;
-        LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, tot.aR < INFINITY ? 1 : 0,
-                                    p_row, b_row, s));
-        e = wait_back(ev);
-        if (e != LAPSUM_OK) return e;
-        *out = hs->rec;
-        return LAPSUM_OK;
+        LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, w.tot, p_row, b_row, s));
+        return wait_back(ev);
       };
-      const bool bucketed = !want_idx && tot.nM > 0;
-      if (bucketed) {
-        LAPSUM_TRY(launch_bucket_solve(w.m_keys, tot.nM, tot.mmin, tot.mmax, host_desc_key(tot.mmax),
-                                       host_desc_key(tot.mmin), w.acc, w.tot, k, t, n, w.rec, s));
+      bool have_rec = false;
+      if (!want_idx) {
+        // buckets, sized from the expected |M|, with no wait for the totals:
+        // the first bracket holds about n (l - j) / K scores, a widened one
+        // about three times the previous middle set
+        int64_t expect;
+        if (attempt == 1) {
+          const double lo = static_cast<double>(j < 0 ? 0 : j);
+          const double hi = static_cast<double>(l > K + 1 ? K + 1 : l);
+          expect = static_cast<int64_t>(static_cast<double>(n) * ((hi - lo) / static_cast<double>(K)));
+        } else {
+          expect = 3 * prev_m;
+        }
+        int64_t grid_m = 2 * expect + 65536;
+        if (grid_m > mcap) grid_m = mcap;
+        LAPSUM_TRY(launch_bucket_solve(w.m_keys, mcap, grid_m, w.acc, w.tot, k, t, n, w.rec, s));
+        st = emit_and_read();
+        if (st != LAPSUM_OK) return st;
+        tot = hs->att.tot;
+        have_rec = true;
       } else {
+        st = copy_back(&hs->att, w.att, ev, s);
+        if (st == LAPSUM_OK) st = wait_back(ev);
+        if (st != LAPSUM_OK) return st;
+        tot = hs->att.tot;
+      }
+      prev_m = tot.nM;
+      aL = tot.aL;
+      aR = tot.aR;
+      rec_info.attempts = attempt;
+      rec_info.a_L = tot.aL;
+      rec_info.a_R = tot.aR;
+      rec_info.n_L = tot.nL;
+      rec_info.n_M = tot.nM;
+      rec_info.n_R = tot.nR;
+      rec_info.T_L = tot.TL;
+      rec_info.T_R = tot.TR;
+      if (tot.nM > mcap) {
+        // no room for M: the certificate is never evaluated
+        rec_info.m_overflow = 1;
+        rec_info.lap_aL = NAN;
+        rec_info.lap_aR = NAN;
+        break;
+      }
+      if (!have_rec || (!hs->att.rec.ok && hs->att.rec.side >= 2)) {
         st = solve_sorted();
+        if (st == LAPSUM_OK) st = emit_and_read();
         if (st != LAPSUM_OK) return st;
       }
-      SolveRec rec;
-      st = emit_and_read(&rec);
-      if (st != LAPSUM_OK) return st;
-      if (bucketed && rec.side == 2) {
-        st = solve_sorted();
-        if (st == LAPSUM_OK) st = emit_and_read(&rec);
-        if (st != LAPSUM_OK) return st;
-      }
+      const SolveRec rec = hs->att.rec;
       rec_info.lap_aL = rec.lap_aL;
       rec_info.lap_aR = rec.lap_aR;
       if (rec.ok) {
