@@ -7,9 +7,10 @@
 //                  plus 8 B per band member.  The entries then hold p, the
 //                  forward's context for the backward.
 //   band_vjp       Eq. (5) from the context: sums of f = min(p, 1 - p) and
-//                  f g over the band (g read only where f != 0), the
-//                  fixed-order finalize, and grad_r written densely (zero
-//                  outside the band): 4 B/score plus the band.
+//                  f g over the band (g read only where f != 0), then
+//                  grad_r written densely (zero outside the band), each emit
+//                  block summing the partials in a fixed order: 4 B/score
+//                  plus the band.
 // A block whose lists overflowed (or whose range is too long for the LDS
 // map) takes the dense form of each pass over its own range.
 #include "common.hpp"
@@ -46,9 +47,16 @@ __device__ __forceinline__ BlockRange block_range(int64_t n, int64_t chunk) {
   return br;
 }
 
-// This block's lists are complete and consistent with the layout.
-__device__ __forceinline__ bool lists_usable(const BandCtx& c) {
-  const BandBlock& bb = c.blk[blockIdx.x];
+__device__ __forceinline__ BlockRange range_of(int64_t n, int64_t chunk, int pb) {
+  BlockRange br;
+  br.b0 = static_cast<int64_t>(pb) * chunk;
+  br.b1 = br.b0 + chunk < n ? br.b0 + chunk : n;
+  return br;
+}
+
+// The lists of partition block pb are complete and consistent with the layout.
+__device__ __forceinline__ bool lists_usable(const BandCtx& c, int pb) {
+  const BandBlock& bb = c.blk[pb];
   bool ok = bb.dense == 0 && c.chunk <= kBandMaxChunk && c.cap <= kBandWaveCapMax;
 #pragma unroll
   for (int w = 0; w < BW; ++w) ok = ok && bb.cnt[w] >= 0 && bb.cnt[w] <= c.cap;
@@ -58,11 +66,11 @@ __device__ __forceinline__ bool lists_usable(const BandCtx& c) {
 // Backward: the saved header must describe this row (a band saved for
 // another length, or a forward that fell back to the full sort, makes every
 // pass dense).
-__device__ __forceinline__ bool block_dense(const BandCtx& c, int64_t n) {
+__device__ __forceinline__ bool block_dense(const BandCtx& c, int64_t n, int pb) {
   const CtxHeader h = *c.hdr;
   if (h.mode != 0 || h.n != n || h.nblocks != c.nblocks || h.chunk != c.chunk || h.cap != c.cap)
     return true;
-  return !lists_usable(c);
+  return !lists_usable(c, pb);
 }
 
 // Build the map of this block's band.  Entries come either as the
@@ -242,7 +250,7 @@ __global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__
     *c.hdr = h;
   }
   const BlockRange br = block_range(n, c.chunk);
-  if (!lists_usable(c)) {
+  if (!lists_usable(c, static_cast<int>(blockIdx.x))) {
     dense_emit(r, br.b0, br.b1, b, inv_t, p);
     return;
   }
@@ -279,6 +287,11 @@ hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------- backward --
+// One wave of a reduce block per partition block; the emit blocks sum the
+// reduce partials themselves (fixed order), so no launch sits between.
+constexpr int kVjpWaveBlocks = BW;             // partition blocks per reduce block
+constexpr int kVjpMaxParts = 4 * BT;           // partials an emit block sums
+
 __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __restrict__ g,
                                                              const float* __restrict__ p,
                                                              int64_t n, BandCtx c,
@@ -286,38 +299,42 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
                                                              double* __restrict__ partials) {
   __shared__ double red[2][BW];
   const int tid = threadIdx.x;
-  const BlockRange br = block_range(n, c.chunk);
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  const int pb = static_cast<int>(blockIdx.x) * kVjpWaveBlocks + wid;
   double F = 0.0, G = 0.0;
-  if (block_dense(c, n)) {
-    for (int64_t i = br.b0 + tid; i < br.b1; i += BT) {
-      const float pv = p[i];
-      const float f = fminf(pv, 1.0f - pv);
-      if (f != 0.0f) {
-        F += static_cast<double>(f);
-        G += static_cast<double>(f) * static_cast<double>(g[i]);
+  if (pb < c.nblocks) {
+    const BlockRange br = range_of(n, c.chunk, pb);
+    if (block_dense(c, n, pb)) {
+      for (int64_t i = br.b0 + lane; i < br.b1; i += kWave) {
+        const float pv = p[i];
+        const float f = fminf(pv, 1.0f - pv);
+        if (f != 0.0f) {
+          F += static_cast<double>(f);
+          G += static_cast<double>(f) * static_cast<double>(g[i]);
+        }
       }
-    }
-  } else {
-    // after the emit the block's members form one list in index order
-    const BandBlock& bb = c.blk[blockIdx.x];
-    const int total = bb.cnt[0] + bb.cnt[1] + bb.cnt[2] + bb.cnt[3];
-    for (int e = tid; e < total; e += BT) {
-      const int64_t slot = static_cast<int64_t>(blockIdx.x) * BW * c.cap + e;
-      const BandEntry en = c.ent[slot];
-      const float pv = __uint_as_float(en.bits);
-      const float f = fminf(pv, 1.0f - pv);
-      if (f != 0.0f && en.idx >= br.b0 && en.idx < br.b1) {
-        const float gv = g[en.idx];
-        gstash[slot] = gv;
-        F += static_cast<double>(f);
-        G += static_cast<double>(f) * static_cast<double>(gv);
+    } else {
+      // after the emit the block's members form one list in index order
+      const BandBlock& bb = c.blk[pb];
+      const int total = bb.cnt[0] + bb.cnt[1] + bb.cnt[2] + bb.cnt[3];
+      for (int e = lane; e < total; e += kWave) {
+        const int64_t slot = static_cast<int64_t>(pb) * BW * c.cap + e;
+        const BandEntry en = c.ent[slot];
+        const float pv = __uint_as_float(en.bits);
+        const float f = fminf(pv, 1.0f - pv);
+        if (f != 0.0f && en.idx >= br.b0 && en.idx < br.b1) {
+          const float gv = g[en.idx];
+          gstash[slot] = gv;
+          F += static_cast<double>(f);
+          G += static_cast<double>(f) * static_cast<double>(gv);
+        }
       }
     }
   }
   F = wave_sum(F);
   G = wave_sum(G);
-  const int wid = tid / kWave;
-  if (lane_id() == 0) {
+  if (lane == 0) {
     red[0][wid] = F;
     red[1][wid] = G;
   }
@@ -334,18 +351,45 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
   }
 }
 
+// grad_r = (f/t)(g - <g,q>); <g,q> = sum f g / sum f from the partials, 0
+// (and grad_r = 0) when sum f == 0.
 __global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restrict__ g,
                                                            const float* __restrict__ p,
                                                            int64_t n, BandCtx c,
                                                            const float* __restrict__ gstash,
-                                                           const double* __restrict__ coef2,
+                                                           const double* __restrict__ partials,
+                                                           int nparts, double inv_t,
                                                            float* __restrict__ grad) {
   __shared__ BandLds L;
-  const float coef = static_cast<float>(coef2[0]);
-  const float scale = static_cast<float>(coef2[1]);
+  __shared__ double red[2][BW];
+  const int tid = threadIdx.x;
+  double F = 0.0, G = 0.0;
+#pragma unroll
+  for (int q = 0; q < kVjpMaxParts / BT; ++q) {
+    const int i = q * BT + tid;
+    if (i < nparts) {
+      F += partials[2 * i];
+      G += partials[2 * i + 1];
+    }
+  }
+  F = wave_sum(F);
+  G = wave_sum(G);
+  if (lane_id() == 0) {
+    red[0][tid / kWave] = F;
+    red[1][tid / kWave] = G;
+  }
+  __syncthreads();
+  double fs = 0.0, gsum = 0.0;
+#pragma unroll
+  for (int w = 0; w < BW; ++w) {
+    fs += red[0][w];
+    gsum += red[1][w];
+  }
+  const float coef = static_cast<float>(fs > 0.0 ? gsum / fs : 0.0);
+  const float scale = static_cast<float>(fs > 0.0 ? inv_t : 0.0);
   const BlockRange br = block_range(n, c.chunk);
-  if (block_dense(c, n)) {
-    for (int64_t i = br.b0 + threadIdx.x; i < br.b1; i += BT) {
+  if (block_dense(c, n, static_cast<int>(blockIdx.x))) {
+    for (int64_t i = br.b0 + tid; i < br.b1; i += BT) {
       const float pv = p[i];
       const float f = fminf(pv, 1.0f - pv);
       grad[i] = (f != 0.0f) ? f * scale * (g[i] - coef) : 0.0f;
@@ -361,17 +405,20 @@ __global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restri
   write_dense(br.b0, br.b1, L, nullptr, grad);
 }
 
+int band_vjp_parts(int nblocks) { return (nblocks + kVjpWaveBlocks - 1) / kVjpWaveBlocks; }
+
 hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const BandCtx& band,
-                           float* gstash, double* partials, double* coef, double t, float* grad,
+                           float* gstash, double* partials, double t, float* grad,
                            hipStream_t s) {
+  const int parts = band_vjp_parts(band.nblocks);
   { ProfScope ps_("band_vjp_reduce", s);
-  hipLaunchKernelGGL(band_vjp_reduce_kernel, dim3(band.nblocks), dim3(BT), 0, s, g, p, n, band,
-                     gstash, partials); }
-  hipError_t e = launch_vjp_finalize(partials, band.nblocks, t, coef, s);
+  hipLaunchKernelGGL(band_vjp_reduce_kernel, dim3(parts), dim3(BT), 0, s, g, p, n, band, gstash,
+                     partials); }
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("band_vjp_emit", s);
   hipLaunchKernelGGL(band_vjp_emit_kernel, dim3(band.nblocks), dim3(BT), 0, s, g, p, n, band,
-                     gstash, coef, grad); }
+                     gstash, partials, parts, 1.0 / t, grad); }
   return hipGetLastError();
 }
 

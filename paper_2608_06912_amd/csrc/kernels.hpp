@@ -199,10 +199,12 @@ hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, doub
                             float* p, double* b_out, hipStream_t s);
 // Mark a context as dense (rows solved by the full sort).
 hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s);
-// Backward from a saved band: partial (sum f, sum f g) per block, the
-// fixed-order finalize, then grad_r written densely (zero outside the band).
+// Backward from a saved band: partial (sum f, sum f g) per run of blocks,
+// then grad_r written densely (zero outside the band).  partials: 2 doubles
+// per part, band_vjp_parts(nblocks) parts.
+int band_vjp_parts(int nblocks);
 hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const BandCtx& band,
-                           float* gstash, double* partials, double* coef, double t, float* grad,
+                           float* gstash, double* partials, double t, float* grad,
                            hipStream_t s);
 hipError_t launch_gather(const float* r, int64_t n, const PartTotals* tot, const PartBlock* blk,
                          const int64_t* offsets, int nblocks, int64_t chunk, const float* stage_v,

@@ -650,8 +650,7 @@ size_t lapsum_backward_band_workspace_size(int64_t batch, int64_t n) {
   if (n < 1 || n > 2147483647LL) return 0;
   const BandCtx v = band_ctx_view(nullptr, n);
   Carve c(nullptr);
-  c.take<double>(2 * static_cast<size_t>(v.nblocks));
-  c.take<double>(2);
+  c.take<double>(2 * static_cast<size_t>(band_vjp_parts(v.nblocks)));
   c.take<float>(static_cast<size_t>(v.nblocks) * 4 * v.cap);
   return c.size();
 }
@@ -671,8 +670,7 @@ int lapsum_backward_band(const float* grad_p, const float* p, const void* band, 
   const double t = -alpha;
   const BandCtx v0 = band_ctx_view(nullptr, n);
   Carve c(workspace);
-  double* partials = c.take<double>(2 * static_cast<size_t>(v0.nblocks));
-  double* coef = c.take<double>(2);
+  double* partials = c.take<double>(2 * static_cast<size_t>(band_vjp_parts(v0.nblocks)));
   float* gstash = c.take<float>(static_cast<size_t>(v0.nblocks) * 4 * v0.cap);
   const size_t band_row_bytes = band_ctx_bytes(n);
   for (int64_t row = 0; row < batch; ++row) {
@@ -680,8 +678,7 @@ int lapsum_backward_band(const float* grad_p, const float* p, const void* band, 
     // the kernels only read the band
     void* band_row = const_cast<char*>(static_cast<const char*>(band)) + row * band_row_bytes;
     const BandCtx v = band_ctx_view(band_row, n);
-    LAPSUM_TRY(launch_band_vjp(grad_p + o, p + o, n, v, gstash, partials, coef, t, grad_r + o,
-                               stream));
+    LAPSUM_TRY(launch_band_vjp(grad_p + o, p + o, n, v, gstash, partials, t, grad_r + o, stream));
   }
   return LAPSUM_OK;
 }
