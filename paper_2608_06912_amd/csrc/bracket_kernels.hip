@@ -296,12 +296,11 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
   // it: first score of this wave's 256-score step (a multiple of 256)
   auto one = [&](const float (&v)[4], const bool (&ok)[4], int64_t it) {
     const int64_t i0 = it + 4 * lane;
-    float tl = 0.0f, tr = 0.0f;
+    float tr = 0.0f;
     uint32_t mb = 0, bb = 0, ob = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const bool L = v[e] < aL;
-      tl += (ok[e] && L) ? exp2_fast((v[e] - aL) * c2f) : 0.0f;
       if constexpr (HAS_R) {
         const bool R = v[e] >= aR;
         tr += (ok[e] && R) ? exp2_fast((aR - v[e]) * c2f) : 0.0f;
@@ -314,7 +313,6 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
         if (ok[e] && !(v[e] < bw.lo)) bb |= 1u << e;
       }
     }
-    st.TL += static_cast<double>(tl);
     if constexpr (HAS_R) {
       st.TR += static_cast<double>(tr);
       // 8 lanes hold the 32 bits of one word
@@ -325,8 +323,15 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
     }
     // band members are appended through the wave's LDS counter (in any
-    // order; the list is put in index order once, at the end of the range)
+    // order; the list is put in index order once, at the end of the range).
+    // The L tail's terms are formed here too: below the band's lower edge
+    // (a_L - 105 t) a term e^{(r - a_L)/t} is exactly 0 in float32.
     if (bb) {
+      float tl = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (((bb >> e) & 1u) && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
+      st.TL += static_cast<double>(tl);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if ((bb >> e) & 1u) {
