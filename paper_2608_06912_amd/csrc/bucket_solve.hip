@@ -99,10 +99,14 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __rest
                                                           int64_t m_cap, double c2,
                                                           uint32_t* __restrict__ acc_n,
                                                           unsigned long long* __restrict__ acc_u,
-                                                          unsigned long long* __restrict__ acc_d) {
+                                                          unsigned long long* __restrict__ acc_d,
+                                                          uint32_t* __restrict__ bkeys,
+                                                          uint32_t* __restrict__ boff) {
   __shared__ uint32_t cn[kBuckets];
   __shared__ unsigned long long cu[kBuckets];
   __shared__ unsigned long long cd[kBuckets];
+  __shared__ uint32_t cur[kBuckets];
+  __shared__ uint32_t wtot[CT / kWave];
   const int tid = threadIdx.x;
   const PartTotals T = *tot;
   const int64_t m = T.nM;
@@ -117,11 +121,17 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __rest
     cd[e] = 0ull;
   }
   __syncthreads();
+  uint32_t kv[CI];
+#pragma unroll
+  for (int i = 0; i < CI; ++i) {
+    const int64_t pos = base + i * CT + tid;
+    kv[i] = pos < m ? keys[pos] : 0u;
+  }
 #pragma unroll
   for (int i = 0; i < CI; ++i) {
     const int64_t pos = base + i * CT + tid;
     if (pos < m) {
-      const uint32_t key = keys[pos];
+      const uint32_t key = kv[i];
       const int d = static_cast<int>((key - g.kmin) >> g.shift);
       const double r = key_float(key);
       const double up = wexp_f32(static_cast<double>(bucket_hi(g, d)) - r, c2);   // e^{-(v_d - r)/t}
@@ -132,6 +142,47 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __rest
     }
   }
   __syncthreads();
+  // this block's keys in bucket order (any order inside a bucket), with the
+  // bucket offsets, so that the solve reads only the bucket it needs
+  {
+    constexpr int PER = kBuckets / CT;
+    const int b0 = PER * tid;
+    uint32_t loc = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) loc += cn[b0 + q];
+    uint32_t incl = loc;
+    const int lane = lane_id();
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t y = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += y;
+    }
+    const int wid = tid / kWave;
+    if (lane == kWave - 1) wtot[wid] = incl;
+    __syncthreads();
+    uint32_t run = incl - loc;
+#pragma unroll
+    for (int w = 0; w < CT / kWave; ++w)
+      if (w < wid) run += wtot[w];
+    uint32_t* bo = boff + static_cast<int64_t>(blockIdx.x) * (kBuckets + 1);
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      cur[b0 + q] = run;
+      bo[b0 + q] = run;
+      run += cn[b0 + q];
+    }
+    if (tid == CT - 1) bo[kBuckets] = run;
+  }
+  __syncthreads();
+  uint32_t* bk = bkeys + static_cast<int64_t>(blockIdx.x) * CT * CI;
+#pragma unroll
+  for (int i = 0; i < CI; ++i) {
+    const int64_t pos = base + i * CT + tid;
+    if (pos < m) {
+      const int d = static_cast<int>((kv[i] - g.kmin) >> g.shift);
+      bk[atomicAdd(&cur[d], 1u)] = kv[i];
+    }
+  }
   for (int e = tid; e < kBuckets; e += CT) {
     if (cn[e]) {
       atomicAdd(&acc_n[e], cn[e]);
@@ -180,7 +231,8 @@ __device__ double sort_and_solve(uint32_t* buf, int c, const BucketGeom& g, doub
 // buckets carry their geometric anchors and a zero sum), so the in-thread
 // folds need one exponential per bucket and no search for the previous
 // non-empty bucket; the block scans then join the threads.
-__global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __restrict__ keys,
+__global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __restrict__ bkeys,
+                                                          const uint32_t* __restrict__ boff,
                                                           int64_t m_cap, int64_t m_grid,
                                                           uint32_t* __restrict__ acc_n,
                                                           unsigned long long* __restrict__ acc_u,
@@ -379,33 +431,24 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     rec.ok = 0;
     rec.side = 2;   // the bucket is too large to sort here: solve M by the full sort
   } else {
-    // 4. gather bucket d* as keys relative to key(max M), whose low `shift`
-    //    bits order the bucket (its order in LDS is irrelevant: sorted next)
-    auto take = [&](uint32_t key) {
-      const uint32_t rel = key - g.kmin;
-      if (static_cast<int>(rel >> g.shift) == dstar) {
+    // 4. gather bucket d* from each count block's bucket-ordered keys, as
+    //    keys relative to key(max M), whose low `shift` bits order the
+    //    bucket (the order in LDS is irrelevant: it is sorted next)
+    const int nbl = static_cast<int>((m + CT * CI - 1) / (CT * CI));
+    for (int b0 = 0; b0 < nbl; b0 += ST) {
+      const int bl = b0 + tid;
+      uint32_t from = 0, cnt_b = 0;
+      if (bl < nbl) {
+        const uint32_t* bo = boff + static_cast<int64_t>(bl) * (kBuckets + 1);
+        from = bo[dstar];
+        cnt_b = bo[dstar + 1] - from;
+      }
+      const uint32_t* bk = bkeys + static_cast<int64_t>(bl) * CT * CI + from;
+      for (uint32_t j = 0; j < cnt_b; ++j) {
         const uint32_t at = atomicAdd(&gathered_s, 1u);
-        if (at < static_cast<uint32_t>(kBucketSortCap)) buf[buf_at(static_cast<int>(at))] = rel;
-      }
-    };
-    const int64_t m4 = (reinterpret_cast<uintptr_t>(keys) & 15) == 0 ? m / 4 : 0;
-    const uint4* k4 = reinterpret_cast<const uint4*>(keys);
-    for (int64_t q0 = tid; q0 < m4; q0 += 8 * ST) {   // eight loads in flight
-      uint4 vv[8];
-#pragma unroll
-      for (int uu = 0; uu < 8; ++uu) {
-        const int64_t q = q0 + static_cast<int64_t>(uu) * ST;
-        vv[uu] = q < m4 ? k4[q] : make_uint4(g.kmin - 1u, g.kmin - 1u, g.kmin - 1u, g.kmin - 1u);
-      }
-#pragma unroll
-      for (int uu = 0; uu < 8; ++uu) {
-        take(vv[uu].x);
-        take(vv[uu].y);
-        take(vv[uu].z);
-        take(vv[uu].w);
+        if (at < static_cast<uint32_t>(kBucketSortCap)) buf[buf_at(static_cast<int>(at))] = bk[j] - g.kmin;
       }
     }
-    for (int64_t i = m4 * 4 + tid; i < m; i += ST) take(keys[i]);
     __syncthreads();
     const int c = static_cast<int>(ccount_s);
     const double rank0 = x.nR + static_cast<double>(cabove_s);
@@ -426,17 +469,23 @@ hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m_cap, int64_t m_
                                const PartTotals* tot, double k, double t, int64_t n_total,
                                SolveRec* out, hipStream_t s) {
   if (m_grid < 1) m_grid = 1;
+  if (m_grid > kBucketMaxM) m_grid = kBucketMaxM;
   const int64_t blocks = (m_grid + CT * CI - 1) / (CT * CI);
   const int64_t covered = blocks * CT * CI;
   { ProfScope ps_("bucket_count", s);
   hipLaunchKernelGGL(bucket_count_kernel, dim3(static_cast<unsigned>(blocks)), dim3(CT), 0, s,
-                     m_keys, tot, m_cap, kLog2e / t, acc.n, acc.u, acc.d); }
+                     m_keys, tot, m_cap, kLog2e / t, acc.n, acc.u, acc.d, acc.keys, acc.offs); }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("bucket_solve", s);
-  hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, m_keys, m_cap, covered, acc.n,
-                     acc.u, acc.d, tot, k, t, n_total, out); }
+  hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, acc.keys, acc.offs, m_cap,
+                     covered, acc.n, acc.u, acc.d, tot, k, t, n_total, out); }
   return hipGetLastError();
+}
+
+size_t bucket_keys_words() { return static_cast<size_t>(kBucketMaxM); }
+size_t bucket_offs_words() {
+  return static_cast<size_t>((kBucketMaxM + CT * CI - 1) / (CT * CI)) * (kBuckets + 1);
 }
 
 }  // namespace lapsum

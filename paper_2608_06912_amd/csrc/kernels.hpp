@@ -217,19 +217,25 @@ hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, in
                                 hipStream_t s);
 // Middle set solved by buckets of keys (only the bucket holding the root is
 // sorted), reading |M| and its range from *tot on the device.  acc: bucket
-// accumulators, zero on entry and left zero.  m_cap: the capacity of M;
-// m_grid: the largest |M| the launch is sized for.  The record reports
+// accumulators, zero on entry and left zero (keys, offs: scratch).  m_cap:
+// the capacity of M; m_grid: the largest |M| the launch is sized for (at most
+// kBucketMaxM).  The record reports
 // ok = 0 with side = 2 when the root's bucket exceeds kBucketSortCap keys and
 // side = 3 when |M| exceeds m_cap or m_grid; the caller then solves M by the
 // full sort.
 constexpr int kBucketCount = 2048;
 constexpr int kBucketSortCap = 4096;
+constexpr int64_t kBucketMaxM = int64_t(1) << 23;   // largest |M| the buckets take
 struct BucketAcc {
   uint32_t* n;              // [kBucketCount]
   unsigned long long* u;    // [kBucketCount]
   unsigned long long* d;    // [kBucketCount]
+  uint32_t* keys;           // [bucket_keys_words()] M per count block in bucket order
+  uint32_t* offs;           // [bucket_offs_words()] bucket offsets per count block
 };
 constexpr int64_t kBucketAccWords = kBucketCount * 5;   // u32 words of n, u, d
+size_t bucket_keys_words();
+size_t bucket_offs_words();
 hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m_cap, int64_t m_grid, BucketAcc acc,
                                const PartTotals* tot, double k, double t, int64_t n_total,
                                SolveRec* out, hipStream_t s);

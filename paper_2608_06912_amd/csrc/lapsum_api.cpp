@@ -209,6 +209,10 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
   w.acc.n = w.hist + kSelectBins;
   w.acc.u = reinterpret_cast<unsigned long long*>(w.hist + kSelectBins + kBucketCount);
   w.acc.d = reinterpret_cast<unsigned long long*>(w.hist + kSelectBins + 3 * kBucketCount);
+  const size_t bkw = static_cast<size_t>(mcap) < bucket_keys_words() ? static_cast<size_t>(mcap)
+                                                                      : bucket_keys_words();
+  w.acc.keys = c.take<uint32_t>(bkw + 4096);
+  w.acc.offs = c.take<uint32_t>(bucket_offs_words());
   w.sel = c.take<SelectRec>(1);
   w.blk = c.take<PartBlock>(w.nblocks);
   w.offsets = c.take<int64_t>(w.nblocks);
@@ -416,6 +420,7 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
         }
         int64_t grid_m = 2 * expect + 65536;
         if (grid_m > mcap) grid_m = mcap;
+        if (grid_m > kBucketMaxM) grid_m = kBucketMaxM;
         LAPSUM_TRY(launch_bucket_solve(w.m_keys, mcap, grid_m, w.acc, w.tot, k, t, n, w.rec, s));
         st = emit_and_read();
         if (st != LAPSUM_OK) return st;
