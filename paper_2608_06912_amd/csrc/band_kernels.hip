@@ -78,11 +78,12 @@ __device__ __forceinline__ bool block_dense(const BandCtx& c, int64_t n, int pb)
 // were met; `from_segments`) or as the emit leaves them (one list in index
 // order at the start of the block's region).  value(entry, rank) gives the
 // float stored for each member; with `writeback` the members are written
-// back as one list in index order, each carrying its value.  Ends with a
-// barrier.
+// back as one list in index order, each carrying its value.  `aux` (or
+// null) is a float per slot of the block's region, loaded with the entries
+// and handed to value(entry, rank, aux of its slot).  Ends with a barrier.
 template <typename Value>
 __device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L,
-                          bool from_segments, bool writeback, Value&& value) {
+                          bool from_segments, bool writeback, const float* aux, Value&& value) {
   constexpr int EPT = kMaxEnt / BT;   // entries per thread
   const int tid = threadIdx.x;
   if (tid == 0) {
@@ -100,21 +101,33 @@ __device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L,
   __syncthreads();
   const int total = L.seg[BW];
   BandEntry* base = c.ent + static_cast<int64_t>(blockIdx.x) * BW * c.cap;
+  const float* abase = aux ? aux + static_cast<int64_t>(blockIdx.x) * BW * c.cap : nullptr;
   BandEntry en[EPT];
+  float av[EPT];
   int off[EPT];
+  // all loads first (slot 0 of the region stands in past the end), then
+  // the bits
 #pragma unroll
   for (int q = 0; q < EPT; ++q) {
     const int e = tid + q * BT;
-    off[q] = -1;
+    int j = 0;
     if (e < total) {
-      int j = e;
+      j = e;
       if (from_segments) {
         int w = 0;
 #pragma unroll
         for (int x = 1; x < BW; ++x) w += (e >= L.seg[x]) ? 1 : 0;
         j = w * c.cap + (e - L.seg[w]);
       }
-      en[q] = base[j];
+    }
+    en[q] = base[j];
+    av[q] = abase ? abase[j] : 0.0f;
+  }
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    const int e = tid + q * BT;
+    off[q] = -1;
+    if (e < total) {
       const int64_t o = static_cast<int64_t>(en[q].idx) - b0;
       if (o >= 0 && o < len) {
         off[q] = static_cast<int>(o);
@@ -158,7 +171,7 @@ __device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L,
       const int o = off[q];
       const uint32_t word = L.bits[o >> 5];
       const int rank = static_cast<int>(L.pre[o >> 5] + __popc(word & ((1u << (o & 31)) - 1u)));
-      const float val = value(en[q], rank);
+      const float val = value(en[q], rank, av[q]);
       L.vals[rank] = val;
       if (writeback) {
         BandEntry w;
@@ -254,7 +267,7 @@ __global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__
     dense_emit(r, br.b0, br.b1, b, inv_t, p);
     return;
   }
-  build_map(c, br.b0, br.b1 - br.b0, L, true, true, [&](const BandEntry& en, int) {
+  build_map(c, br.b0, br.b1 - br.b0, L, true, true, nullptr, [&](const BandEntry& en, int, float) {
     return laplace_p(__uint_as_float(en.bits), b, inv_t);
   });
   write_dense(br.b0, br.b1, L, ones, p);
@@ -315,19 +328,38 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
         }
       }
     } else {
-      // after the emit the block's members form one list in index order
+      // after the emit the block's members form one list in index order;
+      // VB entries per lane at a time, all their loads (then all the loads
+      // of g they select) in flight together; each lane still adds its
+      // entries in list order
       const BandBlock& bb = c.blk[pb];
       const int total = bb.cnt[0] + bb.cnt[1] + bb.cnt[2] + bb.cnt[3];
-      for (int e = lane; e < total; e += kWave) {
-        const int64_t slot = static_cast<int64_t>(pb) * BW * c.cap + e;
-        const BandEntry en = c.ent[slot];
-        const float pv = __uint_as_float(en.bits);
-        const float f = fminf(pv, 1.0f - pv);
-        if (f != 0.0f && en.idx >= br.b0 && en.idx < br.b1) {
-          const float gv = g[en.idx];
-          gstash[slot] = gv;
-          F += static_cast<double>(f);
-          G += static_cast<double>(f) * static_cast<double>(gv);
+      const int64_t base = static_cast<int64_t>(pb) * BW * c.cap;
+      constexpr int VB = 8;
+      for (int e0 = 0; e0 < total; e0 += VB * kWave) {
+        BandEntry en[VB];
+#pragma unroll
+        for (int u = 0; u < VB; ++u) {
+          const int e = e0 + u * kWave + lane;
+          en[u] = c.ent[base + (e < total ? e : 0)];
+        }
+        float fv[VB], gv[VB];
+        bool use[VB];
+#pragma unroll
+        for (int u = 0; u < VB; ++u) {
+          const int e = e0 + u * kWave + lane;
+          const float pv = __uint_as_float(en[u].bits);
+          fv[u] = fminf(pv, 1.0f - pv);
+          use[u] = e < total && fv[u] != 0.0f && en[u].idx >= br.b0 && en[u].idx < br.b1;
+          gv[u] = g[use[u] ? en[u].idx : br.b0];   // an index of this block either way
+        }
+#pragma unroll
+        for (int u = 0; u < VB; ++u) {
+          if (use[u]) {
+            gstash[base + e0 + u * kWave + lane] = gv[u];
+            F += static_cast<double>(fv[u]);
+            G += static_cast<double>(fv[u]) * static_cast<double>(gv[u]);
+          }
         }
       }
     }
@@ -364,12 +396,20 @@ __global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restri
   __shared__ double red[2][BW];
   const int tid = threadIdx.x;
   double F = 0.0, G = 0.0;
+  {
+    // every load issued before the first add (nparts >= 1)
+    double2 pr[kVjpMaxParts / BT];
 #pragma unroll
-  for (int q = 0; q < kVjpMaxParts / BT; ++q) {
-    const int i = q * BT + tid;
-    if (i < nparts) {
-      F += partials[2 * i];
-      G += partials[2 * i + 1];
+    for (int q = 0; q < kVjpMaxParts / BT; ++q) {
+      const int i = q * BT + tid;
+      pr[q] = reinterpret_cast<const double2*>(partials)[i < nparts ? i : 0];
+    }
+#pragma unroll
+    for (int q = 0; q < kVjpMaxParts / BT; ++q) {
+      if (q * BT + tid < nparts) {
+        F += pr[q].x;
+        G += pr[q].y;
+      }
     }
   }
   F = wave_sum(F);
@@ -396,12 +436,13 @@ __global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restri
     }
     return;
   }
-  const float* gs = gstash + static_cast<int64_t>(blockIdx.x) * BW * c.cap;
-  build_map(c, br.b0, br.b1 - br.b0, L, false, false, [&](const BandEntry& en, int rank) {
-    const float pv = __uint_as_float(en.bits);
-    const float f = fminf(pv, 1.0f - pv);
-    return (f != 0.0f) ? f * scale * (gs[rank] - coef) : 0.0f;
-  });
+  // g of each member was stashed at its slot by the reduce (where f != 0)
+  build_map(c, br.b0, br.b1 - br.b0, L, false, false, gstash,
+            [&](const BandEntry& en, int, float gv) {
+              const float pv = __uint_as_float(en.bits);
+              const float f = fminf(pv, 1.0f - pv);
+              return (f != 0.0f) ? f * scale * (gv - coef) : 0.0f;
+            });
   write_dense(br.b0, br.b1, L, nullptr, grad);
 }
 

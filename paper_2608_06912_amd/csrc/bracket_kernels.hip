@@ -24,6 +24,7 @@ __device__ __forceinline__ uint32_t asc_key(float f) { return ~desc_key(f); }
 __device__ __forceinline__ float asc_key_float(uint32_t k) { return key_float(~k); }
 
 constexpr int kSampleThreads = 256;
+constexpr int kSampleItems = 8;
 constexpr int kSelThreads = 1024;
 constexpr int PT = kPartThreads;               // 256
 constexpr int PW = PT / kWave;                 // 4 waves
@@ -39,13 +40,27 @@ __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __r
   __shared__ uint32_t h[kSelectBins];
   for (int e = threadIdx.x; e < kSelectBins; e += kSampleThreads) h[e] = 0u;
   __syncthreads();
-  const int64_t s = static_cast<int64_t>(blockIdx.x) * kSampleThreads + threadIdx.x;
+  // kSampleItems draws per thread, all loads in flight together; a block's
+  // histogram goes out once (few, larger blocks: fewer global atomics)
   const int64_t stride = n / K;
-  if (s < K) {
-    const float y = r[s * stride] + noise[s];   // float32 addition
-    const uint32_t key = asc_key(y);
-    ykeys[s] = key;
-    atomicAdd(&h[key >> 21], 1u);
+  const int64_t s0 = static_cast<int64_t>(blockIdx.x) * kSampleThreads * kSampleItems + threadIdx.x;
+  float rv[kSampleItems], ev[kSampleItems];
+#pragma unroll
+  for (int i = 0; i < kSampleItems; ++i) {
+    const int64_t s = s0 + static_cast<int64_t>(i) * kSampleThreads;
+    const int64_t sc = s < K ? s : K - 1;
+    rv[i] = r[sc * stride];
+    ev[i] = noise[sc];
+  }
+#pragma unroll
+  for (int i = 0; i < kSampleItems; ++i) {
+    const int64_t s = s0 + static_cast<int64_t>(i) * kSampleThreads;
+    if (s < K) {
+      const float y = rv[i] + ev[i];   // float32 addition
+      const uint32_t key = asc_key(y);
+      ykeys[s] = key;
+      atomicAdd(&h[key >> 21], 1u);
+    }
   }
   __syncthreads();
   for (int e = threadIdx.x; e < kSelectBins; e += kSampleThreads)
@@ -54,7 +69,8 @@ __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __r
 
 hipError_t launch_sample(const float* r, int64_t n, const float* noise, int64_t K,
                          uint32_t* ykeys, uint32_t* hist, hipStream_t s) {
-  const int64_t blocks = (K + kSampleThreads - 1) / kSampleThreads;
+  const int64_t per = static_cast<int64_t>(kSampleThreads) * kSampleItems;
+  const int64_t blocks = (K + per - 1) / per;
   { ProfScope ps_("sample", s);
   hipLaunchKernelGGL(sample_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kSampleThreads), 0,
                      s, r, n, noise, K, ykeys, hist); }
@@ -659,7 +675,7 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
     rec.TL = tl;
     rec.TR = tr;
     rec.nR = nr;
-    rec.nM = mtot;
+    rec.nM = static_cast<int32_t>(mtot);
     rec.nL = (b1 - b0) - mtot - nr;
     float mn2 = INFINITY, mx2 = -INFINITY;
 #pragma unroll
@@ -670,7 +686,8 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
     rec.mmin = mn2;
     rec.mmax = mx2;
     rec.overflow = over ? 1 : 0;
-    rec.pad = 0;
+    rec.pad[0] = 0;
+    rec.pad[1] = 0;
     blk[blockIdx.x] = rec;
     bool bover = chunk > kBandMaxChunk;
 #pragma unroll
@@ -682,15 +699,19 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
                             float aR, double t, int nblocks, int64_t chunk, float* stage_v,
                             int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
-                            int64_t* offsets, PartTotals* tot, hipStream_t s) {
+                            hipStream_t s) {
   if (band.nblocks != nblocks || band.chunk != chunk || nblocks > kPartMaxBlocks)
     return hipErrorInvalidValue;
   const float c2f = static_cast<float>(kLog2e / t);
   { ProfScope ps_("partition", s);
   hipLaunchKernelGGL(partition_kernel, dim3(nblocks), dim3(PT), 0, s, r, n, sel, use_sel, aL, aR,
                      c2f, chunk, stage_v, stage_i, blk, t, band.ent, band.blk, band.cap, ones); }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const SelectRec* sel,
+                                   int use_sel, float aL, float aR, int64_t* offsets,
+                                   PartTotals* tot, hipStream_t s) {
   { ProfScope ps_("partition_totals", s);
   hipLaunchKernelGGL(partition_totals_kernel, dim3(1), dim3(TOT_T), 0, s, blk, nblocks, sel, use_sel,
                      aL, aR, offsets, tot); }

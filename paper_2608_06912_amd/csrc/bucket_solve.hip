@@ -24,12 +24,16 @@
 // A term below 2^-F is dropped, an absolute error of at most |M| 2^-F in a
 // sum that enters LapSum with weight 1/2.
 //
-// Two launches: bucket_count (one block per 4096 keys of M) and
-// bucket_solve (one workgroup).  Both read |M| and its range from the
-// partition totals on the device, so the host need not wait for them.  When
-// bucket d* holds more keys than the workgroup can sort (kBucketSortCap) the
-// record reports side = 2, and when |M| exceeds what the launch covers (or M
-// was not gathered) side = 3; the caller then solves M by the full sort.
+// Two launches, straight from the partition's per-block staging (the
+// order of M within a bucket does not matter): bucket_count (one block per
+// kBucketGroup partition blocks) and bucket_solve (one workgroup).  Every
+// count block derives |M| and the range of M from the block records itself
+// (integer min / max of keys, so all agree exactly) and folds its group's
+// tails in a fixed order; bucket_solve folds those partials, so the host
+// need not wait for anything.  When bucket d* holds more keys than the
+// workgroup can sort (kBucketSortCap) the record reports side = 2, and when
+// a block's staging overflowed or |M| exceeds the capacity side = 3; the
+// caller then gathers M in index order and solves it by the full sort.
 #include <math.h>
 
 #include "block_sort.hpp"
@@ -42,7 +46,9 @@ namespace {
 
 constexpr int kBuckets = kBucketCount;
 constexpr int CT = 256;             // bucket_count threads
-constexpr int CI = 16;              // keys per thread
+constexpr int CG = kBucketGroup;    // partition blocks per count block
+constexpr int CU = 8;               // keys per thread per batch
+constexpr int64_t kGroupKeys = static_cast<int64_t>(CG) * kPartStageCap;   // a count block's region
 constexpr int ST = 256;             // bucket_solve threads
 constexpr int SW = ST / kWave;      // 4 waves
 constexpr int BPT = kBuckets / ST;  // buckets per thread
@@ -69,13 +75,14 @@ __device__ __forceinline__ float bucket_lo(const BucketGeom& g, int d) {
   return fmaxf(key_float(key), g.mmin);
 }
 
-// Bucket geometry from the range of M, the same in every block.
-__device__ __forceinline__ BucketGeom geom_of(const PartTotals& T) {
+// Bucket geometry from the keys of max M and min M, the same in every
+// block.
+__device__ __forceinline__ BucketGeom geom_of(uint32_t kmin, uint32_t kmax) {
   BucketGeom g;
-  g.mmin = T.mmin;
-  g.mmax = T.mmax;
-  g.kmin = desc_key(T.mmax);
-  g.kmax = desc_key(T.mmin);
+  g.kmin = kmin;
+  g.kmax = kmax;
+  g.mmin = key_float(kmax);
+  g.mmax = key_float(kmin);
   const uint32_t span = g.kmax - g.kmin;
   const int bits = span ? 32 - __clz(static_cast<int>(span)) : 0;
   g.shift = bits > 11 ? bits - 11 : 0;
@@ -91,29 +98,166 @@ __device__ __forceinline__ int fixed_bits(int64_t m) {
 }  // namespace
 
 // acc: [kBuckets] u32 counts, then [kBuckets] u64 U, then [kBuckets] u64 D;
-// zero on entry (bucket_solve clears it again).  |M| and its range come from
-// the partition totals; nothing is counted when |M| exceeds m_cap (M was not
-// gathered) or the keys this grid covers.
-__global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __restrict__ keys,
-                                                          const PartTotals* __restrict__ tot,
+// zero on entry (bucket_solve clears it again).  Count block c writes its
+// partial of the totals to parts[c] whatever happens; it counts nothing when
+// a block's staging overflowed or |M| exceeds m_cap (the solve then reports
+// side 3).
+__global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __restrict__ blk,
+                                                          int nblocks,
+                                                          const float* __restrict__ stage_v,
                                                           int64_t m_cap, double c2,
                                                           uint32_t* __restrict__ acc_n,
                                                           unsigned long long* __restrict__ acc_u,
                                                           unsigned long long* __restrict__ acc_d,
                                                           uint32_t* __restrict__ bkeys,
-                                                          uint32_t* __restrict__ boff) {
+                                                          uint32_t* __restrict__ boff,
+                                                          CountPart* __restrict__ parts) {
   __shared__ uint32_t cn[kBuckets];
   __shared__ unsigned long long cu[kBuckets];
   __shared__ unsigned long long cd[kBuckets];
   __shared__ uint32_t cur[kBuckets];
   __shared__ uint32_t wtot[CT / kWave];
+  __shared__ int32_t goff[CG + 1];   // start of each group block's staged M
+  __shared__ uint32_t rk[2][CT / kWave];
+  __shared__ unsigned long long rm[CT / kWave];
+  __shared__ uint32_t rov[CT / kWave];
+  __shared__ int32_t ro[CT / kWave];
+  __shared__ double rd[2][CT / kWave];
+  __shared__ int64_t ri[3][CT / kWave];
   const int tid = threadIdx.x;
-  const PartTotals T = *tot;
-  const int64_t m = T.nM;
-  if (m < 1 || m > m_cap || m > static_cast<int64_t>(gridDim.x) * CT * CI) return;
-  const int64_t base = static_cast<int64_t>(blockIdx.x) * CT * CI;
-  if (base >= m) return;   // the launch is sized for the largest expected |M|
-  const BucketGeom g = geom_of(T);
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  const int g0 = static_cast<int>(blockIdx.x) * CG;
+  // this thread's record of the group, loaded with the heads below
+  const bool own = tid < CG && g0 + tid < nblocks;
+  const PartBlock rec = blk[own ? g0 + tid : 0];
+
+  // 1. |M|, the range of M and any overflow over every block (the first 16
+  //    bytes of each record, all loads in flight together)
+  {
+    constexpr int Q = kPartMaxBlocks / CT;
+    uint4 hd[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int b = tid + CT * q;
+      hd[q] = *reinterpret_cast<const uint4*>(&blk[b < nblocks ? b : nblocks - 1]);
+    }
+    uint32_t kmin = 0xffffffffu, kmax = 0u, ov = 0u;
+    unsigned long long m = 0ull;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      if (tid + CT * q < nblocks) {
+        const uint32_t nm = hd[q].z;
+        if (nm > 0) {
+          kmin = min(kmin, desc_key(__uint_as_float(hd[q].y)));   // key of the block's max
+          kmax = max(kmax, desc_key(__uint_as_float(hd[q].x)));   // key of the block's min
+        }
+        m += nm;
+        ov |= hd[q].w;
+      }
+    }
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) {
+      kmin = min(kmin, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmin), o, kWave)));
+      kmax = max(kmax, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmax), o, kWave)));
+      ov |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(ov), o, kWave));
+    }
+    m = wave_sum(m);
+    if (lane == 0) {
+      rk[0][wid] = kmin;
+      rk[1][wid] = kmax;
+      rm[wid] = m;
+      rov[wid] = ov;
+    }
+  }
+  // 2. this group's records: tails folded in a fixed order, and the start of
+  //    each block's staged M within the group
+  {
+    double TL = 0.0, TR = 0.0;
+    int64_t nL = 0, nR = 0, nM = 0;
+    int32_t nm = 0, ov = 0;
+    if (own) {
+      TL = rec.TL;
+      TR = rec.TR;
+      nL = rec.nL;
+      nR = rec.nR;
+      nm = rec.nM;
+      ov = rec.overflow;
+    }
+    nM = nm;
+    int32_t incl = nm;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int32_t y = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += y;
+    }
+    TL = wave_sum(TL);
+    TR = wave_sum(TR);
+    nL = wave_sum(nL);
+    nR = wave_sum(nR);
+    nM = wave_sum(nM);
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) ov |= __shfl_xor(ov, o, kWave);
+    if (lane == kWave - 1) wtot[wid] = static_cast<uint32_t>(incl);
+    if (lane == 0) {
+      rd[0][wid] = TL;
+      rd[1][wid] = TR;
+      ri[0][wid] = nL;
+      ri[1][wid] = nR;
+      ri[2][wid] = nM;
+      ro[wid] = ov;
+    }
+    __syncthreads();
+    if (tid < CG) {
+      int32_t base = 0;
+#pragma unroll
+      for (int w = 0; w < CG / kWave; ++w)
+        if (w < wid) base += static_cast<int32_t>(wtot[w]);
+      goff[tid] = base + incl - nm;
+      if (tid == CG - 1) goff[CG] = base + incl;
+    }
+    __syncthreads();
+  }
+  uint32_t kmin = 0xffffffffu, kmax = 0u, aov = 0u;
+  int64_t m = 0;
+#pragma unroll
+  for (int w = 0; w < CT / kWave; ++w) {
+    kmin = min(kmin, rk[0][w]);
+    kmax = max(kmax, rk[1][w]);
+    m += static_cast<int64_t>(rm[w]);
+    aov |= rov[w];
+  }
+  const int32_t any_ov = aov != 0u ? 1 : 0;
+  int32_t grp_ov = 0;
+#pragma unroll
+  for (int w = 0; w < CG / kWave; ++w) grp_ov |= ro[w];
+  if (tid == 0) {
+    CountPart cp;
+    cp.TL = 0.0;
+    cp.TR = 0.0;
+    cp.nL = cp.nR = cp.nM = 0;
+#pragma unroll
+    for (int w = 0; w < CG / kWave; ++w) {
+      cp.TL += rd[0][w];
+      cp.TR += rd[1][w];
+      cp.nL += ri[0][w];
+      cp.nR += ri[1][w];
+      cp.nM += ri[2][w];
+    }
+    cp.overflow = grp_ov;
+    cp.kmin = kmin;
+    cp.kmax = kmax;
+    cp.any_overflow = any_ov;
+    cp.m_all = m;
+    parts[blockIdx.x] = cp;
+  }
+  if (any_ov != 0 || m < 1 || m > m_cap) return;
+  const int cb = goff[CG];   // this group's members of M (no staging overflowed)
+  if (cb == 0) return;       // the solve skips a group with no members
+
+  // 3. bucket sums of the group's members, CU keys per thread at a time;
+  //    member j of the group is found by a search over goff
+  const BucketGeom g = geom_of(kmin, kmax);
   const double fscale = ldexp(1.0, fixed_bits(m));
   for (int e = tid; e < kBuckets; e += CT) {
     cn[e] = 0u;
@@ -121,29 +265,45 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __rest
     cd[e] = 0ull;
   }
   __syncthreads();
-  uint32_t kv[CI];
+  auto member_key = [&](int j) -> uint32_t {
+    int lo = 0, hi = CG;   // goff[lo] <= j < goff[hi]
 #pragma unroll
-  for (int i = 0; i < CI; ++i) {
-    const int64_t pos = base + i * CT + tid;
-    kv[i] = pos < m ? keys[pos] : 0u;
-  }
+    for (int st = 0; st < 7; ++st) {   // CG = 2^7
+      const int mid = (lo + hi) >> 1;
+      if (goff[mid] <= j) lo = mid; else hi = mid;
+    }
+    return desc_key(stage_v[static_cast<int64_t>(g0 + lo) * kPartStageCap + (j - goff[lo])]);
+  };
+  // the first batch stays in registers for the scatter below
+  uint32_t kv0[CU];
+  for (int j0 = 0; j0 < cb; j0 += CT * CU) {
+    uint32_t kv[CU];
 #pragma unroll
-  for (int i = 0; i < CI; ++i) {
-    const int64_t pos = base + i * CT + tid;
-    if (pos < m) {
-      const uint32_t key = kv[i];
-      const int d = static_cast<int>((key - g.kmin) >> g.shift);
-      const double r = key_float(key);
-      const double up = wexp_f32(static_cast<double>(bucket_hi(g, d)) - r, c2);   // e^{-(v_d - r)/t}
-      const double dn = wexp_f32(r - static_cast<double>(bucket_lo(g, d)), c2);   // e^{-(r - u_d)/t}
-      atomicAdd(&cn[d], 1u);
-      atomicAdd(&cu[d], static_cast<unsigned long long>(__double2ull_rn(up * fscale)));
-      atomicAdd(&cd[d], static_cast<unsigned long long>(__double2ull_rn(dn * fscale)));
+    for (int u = 0; u < CU; ++u) {
+      const int j = j0 + u * CT + tid;
+      kv[u] = member_key(j < cb ? j : cb - 1);
+    }
+    if (j0 == 0) {
+#pragma unroll
+      for (int u = 0; u < CU; ++u) kv0[u] = kv[u];
+    }
+#pragma unroll
+    for (int u = 0; u < CU; ++u) {
+      if (j0 + u * CT + tid < cb) {
+        const uint32_t key = kv[u];
+        const int d = static_cast<int>((key - g.kmin) >> g.shift);
+        const double r = key_float(key);
+        const double up = wexp_f32(static_cast<double>(bucket_hi(g, d)) - r, c2);   // e^{-(v_d - r)/t}
+        const double dn = wexp_f32(r - static_cast<double>(bucket_lo(g, d)), c2);   // e^{-(r - u_d)/t}
+        atomicAdd(&cn[d], 1u);
+        atomicAdd(&cu[d], static_cast<unsigned long long>(__double2ull_rn(up * fscale)));
+        atomicAdd(&cd[d], static_cast<unsigned long long>(__double2ull_rn(dn * fscale)));
+      }
     }
   }
   __syncthreads();
-  // this block's keys in bucket order (any order inside a bucket), with the
-  // bucket offsets, so that the solve reads only the bucket it needs
+  // 4. the group's keys in bucket order (any order inside a bucket), with
+  //    the bucket offsets, so that the solve reads only the bucket it needs
   {
     constexpr int PER = kBuckets / CT;
     const int b0 = PER * tid;
@@ -151,14 +311,12 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __rest
 #pragma unroll
     for (int q = 0; q < PER; ++q) loc += cn[b0 + q];
     uint32_t incl = loc;
-    const int lane = lane_id();
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
       const uint32_t y = __shfl_up(incl, o, kWave);
       if (lane >= o) incl += y;
     }
-    const int wid = tid / kWave;
-    if (lane == kWave - 1) wtot[wid] = incl;
+    if (lane == kWave - 1) wtot[wid] = incl;   // (its last readers passed two barriers ago)
     __syncthreads();
     uint32_t run = incl - loc;
 #pragma unroll
@@ -174,13 +332,20 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const uint32_t* __rest
     if (tid == CT - 1) bo[kBuckets] = run;
   }
   __syncthreads();
-  uint32_t* bk = bkeys + static_cast<int64_t>(blockIdx.x) * CT * CI;
+  uint32_t* bk = bkeys + static_cast<int64_t>(blockIdx.x) * kGroupKeys;
+  for (int j0 = 0; j0 < cb; j0 += CT * CU) {
+    uint32_t kv[CU];
 #pragma unroll
-  for (int i = 0; i < CI; ++i) {
-    const int64_t pos = base + i * CT + tid;
-    if (pos < m) {
-      const int d = static_cast<int>((kv[i] - g.kmin) >> g.shift);
-      bk[atomicAdd(&cur[d], 1u)] = kv[i];
+    for (int u = 0; u < CU; ++u) {
+      const int j = j0 + u * CT + tid;
+      kv[u] = j0 == 0 ? kv0[u] : member_key(j < cb ? j : cb - 1);
+    }
+#pragma unroll
+    for (int u = 0; u < CU; ++u) {
+      if (j0 + u * CT + tid < cb) {
+        const int d = static_cast<int>((kv[u] - g.kmin) >> g.shift);
+        bk[atomicAdd(&cur[d], 1u)] = kv[u];
+      }
     }
   }
   for (int e = tid; e < kBuckets; e += CT) {
@@ -224,6 +389,142 @@ __device__ double sort_and_solve(uint32_t* buf, int c, const BucketGeom& g, doub
   Suf st;
   return block_solve<ST, ITEMS>(s, cnt, rank0, ext_pre, ext_suf, k, t, csm, &pt, &st);
 }
+
+// A small bucket (c <= kDirectMax keys) is solved without sorting it:
+// LapSum at each of its scores is formed term by term,
+//     N(s_i) = rank0 + #{s_j > s_i} + #{s_j = s_i}/2
+//              - (1/2) (sum_{s_j > s_i} e^{-(s_j - s_i)/t} + pre carry)
+//              + (1/2) (sum_{s_j < s_i} e^{-(s_i - s_j)/t} + suf carry),
+// which is what the scan gives at that score's positions; each key gets TPK
+// threads, each summing a fixed slice of the bucket in order.  The root is
+// then in the gap between u, the lowest score with N <= k, and v, the
+// highest with N > k (or a carry's anchor when either side is empty), as in
+// the sorted block solve.
+constexpr int kDirectMax = ST;
+struct DirectSmem {
+  float4 sv4[kDirectMax / 4 + 1];   // the keys' scores, NaN past the end
+  uint32_t ukey, vkey, has_u, has_v;
+  double uA, uc, vB;
+};
+
+__device__ double direct_solve(const uint32_t* buf, int c, const BucketGeom& g, double rank0,
+                               Pre ext_pre, Suf ext_suf, double k, double t, DirectSmem& ds) {
+  const int tid = threadIdx.x;
+  const double inv_t = 1.0 / t;
+  const double c2 = kLog2e / t;
+  float* sv = reinterpret_cast<float*>(ds.sv4);
+  // threads per key (adjacent lanes) and the slice of keys each sums, a
+  // multiple of 4 so that it is read as float4; the slices cover
+  // tpk * slice <= kDirectMax + 3 entries, NaN past c (a NaN difference
+  // counts nowhere)
+  const int tpk = c <= kDirectMax / 8 ? 8 : (c <= kDirectMax / 4 ? 4 : (c <= kDirectMax / 2 ? 2 : 1));
+  const int slice = ((c + tpk - 1) / tpk + 3) & ~3;
+  if (tid < c) sv[tid] = key_float(buf[buf_at(tid)] + g.kmin);
+  for (int e = c + tid; e < tpk * slice; e += ST) sv[e] = __int_as_float(0x7fc00000);
+  if (tid == 0) {
+    ds.ukey = 0u;
+    ds.vkey = 0xffffffffu;
+    ds.has_u = 0u;
+    ds.has_v = 0u;
+  }
+  __syncthreads();
+  const int i = tid / tpk;
+  const int q = tid - i * tpk;
+  const bool active = i < c;
+  const float si = sv[active ? i : 0];
+  const double sd = si;
+  // four independent chains (one per lane of a float4), joined in order
+  double Pg[4] = {0.0, 0.0, 0.0, 0.0}, El[4] = {0.0, 0.0, 0.0, 0.0};
+  int gt = 0, eq = 0;
+  for (int j = q * slice; j < (q + 1) * slice; j += 4) {
+    const float4 v = ds.sv4[j >> 2];
+    const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const double d = static_cast<double>(vv[e]) - sd;
+      const double w = wexp_f32(fabs(d), c2);
+      Pg[e] += d > 0.0 ? w : 0.0;
+      El[e] += d < 0.0 ? w : 0.0;
+      gt += d > 0.0 ? 1 : 0;
+      eq += d == 0.0 ? 1 : 0;
+    }
+  }
+  double Pgs = (Pg[0] + Pg[1]) + (Pg[2] + Pg[3]);
+  double Els = (El[0] + El[1]) + (El[2] + El[3]);
+  // the key's threads are adjacent lanes: join their slices
+  for (int o = 1; o < tpk; o <<= 1) {
+    Pgs += __shfl_xor(Pgs, o, kWave);
+    Els += __shfl_xor(Els, o, kWave);
+    gt += __shfl_xor(gt, o, kWave);
+    eq += __shfl_xor(eq, o, kWave);
+  }
+  const double Pc = ext_pre.S != 0.0 ? ext_pre.S * wexp_f64(static_cast<double>(ext_pre.u) - sd, inv_t) : 0.0;
+  const double Ec = ext_suf.T != 0.0 ? ext_suf.T * wexp_f64(sd - static_cast<double>(ext_suf.v), inv_t) : 0.0;
+  const double N = rank0 + gt + 0.5 * eq - 0.5 * (Pgs + Pc) + 0.5 * (Els + Ec);
+  const bool le = N <= k;
+  const uint32_t key = desc_key(si);
+  const bool lead = active && q == 0;
+  {
+    // the lowest score at or below k (largest key) and the highest above k
+    // (smallest key): reduced in the wave, then one atomic per wave
+    uint32_t uk = (lead && le) ? key : 0u;
+    uint32_t vk = (lead && !le) ? key : 0xffffffffu;
+    uint32_t hu = (lead && le) ? 1u : 0u, hv = (lead && !le) ? 1u : 0u;
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) {
+      uk = max(uk, static_cast<uint32_t>(__shfl_xor(static_cast<int>(uk), o, kWave)));
+      vk = min(vk, static_cast<uint32_t>(__shfl_xor(static_cast<int>(vk), o, kWave)));
+      hu |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(hu), o, kWave));
+      hv |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(hv), o, kWave));
+    }
+    if (lane_id() == 0) {
+      if (hu) {
+        atomicMax(&ds.ukey, uk);
+        atomicOr(&ds.has_u, 1u);
+      }
+      if (hv) {
+        atomicMin(&ds.vkey, vk);
+        atomicOr(&ds.has_v, 1u);
+      }
+    }
+  }
+  __syncthreads();
+  // equal scores give equal sums, so any holder of u (or v) may publish
+  if (lead && le && key == ds.ukey) {
+    ds.uA = Pgs + eq + Pc;
+    ds.uc = gt + eq;
+  }
+  if (lead && !le && key == ds.vkey) ds.vB = Els + eq + Ec;
+  __syncthreads();
+  double b = 0.0;
+  if (tid < 2) {
+    // the two logarithms of the gap's sums side by side (lanes 0 and 1)
+    const bool has_u = ds.has_u != 0u, has_v = ds.has_v != 0u;
+    const bool has_dn = ext_suf.T != 0.0;
+    double arg;
+    if (tid == 0)
+      arg = has_u ? ds.uA : (ext_pre.S > 0 ? ext_pre.S : 1.0);
+    else
+      arg = has_v ? ds.vB : (has_dn ? ext_suf.T : 1.0);
+    const double lg = log(arg);
+    const double lnB = __shfl(lg, 1, kWave);
+    if (tid == 0) {
+      const double lnA = lg;
+      const double v = key_float(ds.vkey);
+      if (!has_u) {
+        // b lies above every score of the bucket
+        b = gap_root(k, t, rank0, ext_pre.S != 0.0, ext_pre.u, lnA, true, v, lnB);
+      } else {
+        const double u = key_float(ds.ukey);
+        if (has_v)
+          b = gap_root(k, t, rank0 + ds.uc, true, u, lnA, true, v, lnB);
+        else
+          b = gap_root(k, t, rank0 + ds.uc, true, u, lnA, has_dn, ext_suf.v, lnB);
+      }
+    }
+  }
+  return b;   // thread 0's value
+}
 }  // namespace
 
 // One workgroup.  Thread tid owns buckets BPT tid .. BPT tid + BPT - 1.
@@ -233,11 +534,14 @@ __device__ double sort_and_solve(uint32_t* buf, int c, const BucketGeom& g, doub
 // non-empty bucket; the block scans then join the threads.
 __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __restrict__ bkeys,
                                                           const uint32_t* __restrict__ boff,
-                                                          int64_t m_cap, int64_t m_grid,
+                                                          const CountPart* __restrict__ parts,
+                                                          int ngroups, int64_t m_cap,
+                                                          const SelectRec* __restrict__ sel,
+                                                          int use_sel, float aL_arg, float aR_arg,
                                                           uint32_t* __restrict__ acc_n,
                                                           unsigned long long* __restrict__ acc_u,
                                                           unsigned long long* __restrict__ acc_d,
-                                                          const PartTotals* __restrict__ tot,
+                                                          PartTotals* __restrict__ tot,
                                                           double k, double t, int64_t n_total,
                                                           SolveRec* __restrict__ out) {
   __shared__ uint32_t buf[sort_buf_words<ST, SI>()];
@@ -250,15 +554,57 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
   __shared__ int64_t cabove_s;
   __shared__ uint32_t ccount_s;
   __shared__ uint32_t gathered_s;
+  __shared__ DirectSmem dsm;
+  __shared__ PartTotals tot_s;
+  __shared__ int64_t gcount_s[kPartMaxBlocks / CG];
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
   const double inv_t = 1.0 / t;
-  const Tails x = load_tails(tot);
   const int d0 = BPT * tid;
-  const int64_t m = tot->nM;
-  if (m > m_cap || m > m_grid) {
-    // M was not gathered, or not counted: the caller solves with |M| known
+  // this thread's buckets, loaded with the partials below (they are zero
+  // when nothing was counted)
+  uint32_t cnt[BPT];
+  unsigned long long Ur[BPT], Dr[BPT];
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    cnt[q] = acc_n[d0 + q];
+    Ur[q] = acc_u[d0 + q];
+    Dr[q] = acc_d[d0 + q];
+  }
+  // 0. the partition totals from the count blocks' partials (wave 0, in a
+  //    fixed order), for this solve, the host and the emit
+  if (wid == 0) {
+    const CountPart cp = parts[lane < ngroups ? lane : 0];
+    const bool on = lane < ngroups;
+    const double TL = wave_sum(on ? cp.TL : 0.0);
+    const double TR = wave_sum(on ? cp.TR : 0.0);
+    const int64_t nL = wave_sum(on ? cp.nL : int64_t(0));
+    const int64_t nR = wave_sum(on ? cp.nR : int64_t(0));
+    if (on) gcount_s[lane] = cp.nM;
+    if (lane == 0) {
+      // |M|, its range and the overflow flag are the same in every partial
+      PartTotals T;
+      T.TL = TL;
+      T.TR = TR;
+      T.nL = nL;
+      T.nR = nR;
+      T.nM = cp.m_all;
+      T.aL = use_sel ? sel->aL : aL_arg;
+      T.aR = use_sel ? sel->aR : aR_arg;
+      T.mmin = cp.m_all > 0 ? key_float(cp.kmax) : INFINITY;
+      T.mmax = cp.m_all > 0 ? key_float(cp.kmin) : -INFINITY;
+      T.any_block_overflow = cp.any_overflow;
+      T.pad = 0;
+      tot_s = T;
+      *tot = T;
+    }
+  }
+  __syncthreads();
+  const Tails x = load_tails(&tot_s);
+  const int64_t m = tot_s.nM;
+  if (m > m_cap || tot_s.any_block_overflow != 0) {
+    // M was not counted: the caller gathers it and solves with |M| known
     if (tid == 0) {
       SolveRec rec;
       rec.b = 0.0;
@@ -282,18 +628,16 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     }
     return;
   }
-  const BucketGeom g = geom_of(*tot);
+  const BucketGeom g = geom_of(parts[0].kmin, parts[0].kmax);
   const double inv_fscale = ldexp(1.0, -fixed_bits(m));
 
   // 1. this thread's buckets, cleared behind us for the next attempt
-  uint32_t cnt[BPT];
   double U[BPT], D[BPT];
   float v[BPT], u[BPT];
 #pragma unroll
   for (int q = 0; q < BPT; ++q) {
-    cnt[q] = acc_n[d0 + q];
-    U[q] = static_cast<double>(acc_u[d0 + q]) * inv_fscale;
-    D[q] = static_cast<double>(acc_d[d0 + q]) * inv_fscale;
+    U[q] = static_cast<double>(Ur[q]) * inv_fscale;
+    D[q] = static_cast<double>(Dr[q]) * inv_fscale;
     v[q] = bucket_hi(g, d0 + q);
     u[q] = bucket_lo(g, d0 + q);
   }
@@ -434,16 +778,12 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     // 4. gather bucket d* from each count block's bucket-ordered keys, as
     //    keys relative to key(max M), whose low `shift` bits order the
     //    bucket (the order in LDS is irrelevant: it is sorted next)
-    const int nbl = static_cast<int>((m + CT * CI - 1) / (CT * CI));
-    for (int b0 = 0; b0 < nbl; b0 += ST) {
-      const int bl = b0 + tid;
-      uint32_t from = 0, cnt_b = 0;
-      if (bl < nbl) {
-        const uint32_t* bo = boff + static_cast<int64_t>(bl) * (kBuckets + 1);
-        from = bo[dstar];
-        cnt_b = bo[dstar + 1] - from;
-      }
-      const uint32_t* bk = bkeys + static_cast<int64_t>(bl) * CT * CI + from;
+    //    (a group with no members wrote no offsets)
+    if (tid < ngroups && gcount_s[tid] > 0) {
+      const uint32_t* bo = boff + static_cast<int64_t>(tid) * (kBuckets + 1);
+      const uint32_t from = bo[dstar];
+      const uint32_t cnt_b = bo[dstar + 1] - from;
+      const uint32_t* bk = bkeys + static_cast<int64_t>(tid) * kGroupKeys + from;
       for (uint32_t j = 0; j < cnt_b; ++j) {
         const uint32_t at = atomicAdd(&gathered_s, 1u);
         if (at < static_cast<uint32_t>(kBucketSortCap)) buf[buf_at(static_cast<int>(at))] = bk[j] - g.kmin;
@@ -452,8 +792,8 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     __syncthreads();
     const int c = static_cast<int>(ccount_s);
     const double rank0 = x.nR + static_cast<double>(cabove_s);
-    if (c <= ST)
-      b = sort_and_solve<1>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
+    if (c <= kDirectMax)
+      b = direct_solve(buf, c, g, rank0, cpre_s, csuf_s, k, t, dsm);
     else if (c <= 4 * ST)
       b = sort_and_solve<4>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
     else
@@ -465,27 +805,29 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
   }
 }
 
-hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m_cap, int64_t m_grid, BucketAcc acc,
-                               const PartTotals* tot, double k, double t, int64_t n_total,
-                               SolveRec* out, hipStream_t s) {
-  if (m_grid < 1) m_grid = 1;
-  if (m_grid > kBucketMaxM) m_grid = kBucketMaxM;
-  const int64_t blocks = (m_grid + CT * CI - 1) / (CT * CI);
-  const int64_t covered = blocks * CT * CI;
+int bucket_groups(int nblocks) { return (nblocks + CG - 1) / CG; }
+size_t bucket_keys_words(int nblocks) {
+  return static_cast<size_t>(bucket_groups(nblocks)) * static_cast<size_t>(kGroupKeys);
+}
+size_t bucket_offs_words(int nblocks) {
+  return static_cast<size_t>(bucket_groups(nblocks)) * (kBuckets + 1);
+}
+
+hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc acc, PartTotals* tot,
+                               double k, double t, int64_t n_total, SolveRec* out, hipStream_t s) {
+  if (ps.nblocks < 1 || ps.nblocks > kPartMaxBlocks) return hipErrorInvalidValue;
+  const int groups = bucket_groups(ps.nblocks);   // <= 32: one lane each in the solve
   { ProfScope ps_("bucket_count", s);
-  hipLaunchKernelGGL(bucket_count_kernel, dim3(static_cast<unsigned>(blocks)), dim3(CT), 0, s,
-                     m_keys, tot, m_cap, kLog2e / t, acc.n, acc.u, acc.d, acc.keys, acc.offs); }
+  hipLaunchKernelGGL(bucket_count_kernel, dim3(static_cast<unsigned>(groups)), dim3(CT), 0, s,
+                     ps.blk, ps.nblocks, ps.stage_v, m_cap, kLog2e / t, acc.n, acc.u, acc.d,
+                     acc.keys, acc.offs, acc.parts); }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("bucket_solve", s);
-  hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, acc.keys, acc.offs, m_cap,
-                     covered, acc.n, acc.u, acc.d, tot, k, t, n_total, out); }
+  hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, acc.keys, acc.offs, acc.parts,
+                     groups, m_cap, ps.sel, ps.use_sel, ps.aL, ps.aR, acc.n, acc.u, acc.d, tot, k,
+                     t, n_total, out); }
   return hipGetLastError();
-}
-
-size_t bucket_keys_words() { return static_cast<size_t>(kBucketMaxM); }
-size_t bucket_offs_words() {
-  return static_cast<size_t>((kBucketMaxM + CT * CI - 1) / (CT * CI)) * (kBuckets + 1);
 }
 
 }  // namespace lapsum

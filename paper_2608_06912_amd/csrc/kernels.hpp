@@ -29,14 +29,17 @@ struct SolveRec {
   int32_t side;    // 0 certified, +1 b >= a_R (LapSum(a_R) > k), -1 b < a_L
 };
 
-// Per-block record of the streaming partition.
-struct PartBlock {
-  int64_t nL, nM, nR;
-  double TL, TR;
+// Per-block record of the streaming partition (64 bytes; the first 16 are
+// what the bucketed solve needs of every block: one aligned load).
+struct alignas(16) PartBlock {
   float mmin, mmax;   // smallest / largest member of M (+inf / -inf if none)
+  int32_t nM;
   int32_t overflow;   // this block's M did not fit its staging
-  int32_t pad;
+  int64_t nL, nR;
+  double TL, TR;
+  int64_t pad[2];
 };
+static_assert(sizeof(PartBlock) == 64, "PartBlock layout");
 
 // Totals of the streaming partition (one per attempt).
 struct PartTotals {
@@ -185,11 +188,15 @@ int band_wave_cap(int64_t chunk);
 size_t band_ctx_bytes(int64_t n);
 BandCtx band_ctx_view(void* base, int64_t n);
 // ones: [ceil(n/32)] bit set where r >= hi (written only when a_R is finite).
-// Also launches the totals: *tot and each block's offset into M.
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
                             float aR, double t, int nblocks, int64_t chunk, float* stage_v,
                             int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
-                            int64_t* offsets, PartTotals* tot, hipStream_t s);
+                            hipStream_t s);
+// Fixed-order totals of the block records (*tot) and each block's offset
+// into M (for launch_gather).
+hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const SelectRec* sel,
+                                   int use_sel, float aL, float aR, int64_t* offsets,
+                                   PartTotals* tot, hipStream_t s);
 // Emit after a certified bracket (skipped when rec->ok == 0): p from the band
 // lists and the ones bits (used when tot->aR is finite), dense from r for
 // blocks without usable lists; each block's list is written back in index
@@ -216,29 +223,49 @@ hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, in
                                 int64_t n_total, SolveRec* out, int32_t* m_idx_sorted,
                                 hipStream_t s);
 // Middle set solved by buckets of keys (only the bucket holding the root is
-// sorted), reading |M| and its range from *tot on the device.  acc: bucket
-// accumulators, zero on entry and left zero (keys, offs: scratch).  m_cap:
-// the capacity of M; m_grid: the largest |M| the launch is sized for (at most
-// kBucketMaxM).  The record reports
-// ok = 0 with side = 2 when the root's bucket exceeds kBucketSortCap keys and
-// side = 3 when |M| exceeds m_cap or m_grid; the caller then solves M by the
-// full sort.
+// sorted), straight from the partition's staging: count block c takes the
+// staged M of partition blocks [c kBucketGroup, (c+1) kBucketGroup), and the
+// solve also forms the partition totals (*tot) in a fixed order.  acc:
+// bucket accumulators, zero on entry and left zero (keys, offs, parts:
+// scratch).  The record reports ok = 0 with side = 2 when the root's bucket
+// exceeds kBucketSortCap keys and side = 3 when a block's staging
+// overflowed or |M| exceeds m_cap; the caller then gathers M in index order
+// and solves it by the full sort.
 constexpr int kBucketCount = 2048;
 constexpr int kBucketSortCap = 4096;
-constexpr int64_t kBucketMaxM = int64_t(1) << 23;   // largest |M| the buckets take
+constexpr int kBucketGroup = 128;   // partition blocks per count block
+// One count block's share of the partition totals, and the range and size
+// of all of M (the same in every count block).
+struct alignas(16) CountPart {
+  double TL, TR;
+  int64_t nL, nR, nM;
+  int32_t overflow;   // a block of this group overflowed its staging
+  uint32_t kmin, kmax;   // keys of max M and min M over every block
+  int32_t any_overflow;
+  int64_t m_all;
+};
 struct BucketAcc {
   uint32_t* n;              // [kBucketCount]
   unsigned long long* u;    // [kBucketCount]
   unsigned long long* d;    // [kBucketCount]
-  uint32_t* keys;           // [bucket_keys_words()] M per count block in bucket order
-  uint32_t* offs;           // [bucket_offs_words()] bucket offsets per count block
+  uint32_t* keys;           // [bucket_keys_words(nblocks)] M per count block in bucket order
+  uint32_t* offs;           // [bucket_offs_words(nblocks)] bucket offsets per count block
+  CountPart* parts;         // [bucket_groups(nblocks)]
 };
 constexpr int64_t kBucketAccWords = kBucketCount * 5;   // u32 words of n, u, d
-size_t bucket_keys_words();
-size_t bucket_offs_words();
-hipError_t launch_bucket_solve(const uint32_t* m_keys, int64_t m_cap, int64_t m_grid, BucketAcc acc,
-                               const PartTotals* tot, double k, double t, int64_t n_total,
-                               SolveRec* out, hipStream_t s);
+int bucket_groups(int nblocks);
+size_t bucket_keys_words(int nblocks);
+size_t bucket_offs_words(int nblocks);
+struct PartSource {
+  const PartBlock* blk;
+  int nblocks;
+  const float* stage_v;      // [nblocks * kPartStageCap]
+  const SelectRec* sel;      // the bracket: sel (use_sel) or aL, aR
+  int use_sel;
+  float aL, aR;
+};
+hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc acc, PartTotals* tot,
+                               double k, double t, int64_t n_total, SolveRec* out, hipStream_t s);
 
 // Copy sorted M indices to the caller's [m_capacity] row, -1 padded.
 hipError_t launch_write_m_idx(const int32_t* sorted_idx, int64_t m_len, int64_t m_capacity,

@@ -209,10 +209,9 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
   w.acc.n = w.hist + kSelectBins;
   w.acc.u = reinterpret_cast<unsigned long long*>(w.hist + kSelectBins + kBucketCount);
   w.acc.d = reinterpret_cast<unsigned long long*>(w.hist + kSelectBins + 3 * kBucketCount);
-  const size_t bkw = static_cast<size_t>(mcap) < bucket_keys_words() ? static_cast<size_t>(mcap)
-                                                                      : bucket_keys_words();
-  w.acc.keys = c.take<uint32_t>(bkw + 4096);
-  w.acc.offs = c.take<uint32_t>(bucket_offs_words());
+  w.acc.keys = c.take<uint32_t>(bucket_keys_words(w.nblocks));
+  w.acc.offs = c.take<uint32_t>(bucket_offs_words(w.nblocks));
+  w.acc.parts = c.take<CountPart>(static_cast<size_t>(bucket_groups(w.nblocks)));
   w.sel = c.take<SelectRec>(1);
   w.blk = c.take<PartBlock>(w.nblocks);
   w.offsets = c.take<int64_t>(w.nblocks);
@@ -359,13 +358,19 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
     LAPSUM_TRY(launch_select(w.ykeys, K, w.hist, j, l, w.sel, s));
     float aL = 0.0f, aR = 0.0f;
     const bool want_idx = midx_row != nullptr;
-    int64_t prev_m = -1;
     for (int attempt = 1; attempt <= 3 && !solved; ++attempt) {
       const int use_sel = attempt == 1 ? 1 : 0;
       LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR, t, w.nblocks, w.chunk, w.stage_v,
-                                  w.stage_i, w.blk, band, w.ones, w.offsets, w.tot, s));
-      LAPSUM_TRY(launch_gather(r, n, w.tot, w.blk, w.offsets, w.nblocks, w.chunk, w.stage_v,
-                               w.stage_i, mcap, w.m_keys, w.m_idx, s));
+                                  w.stage_i, w.blk, band, w.ones, s));
+      // M in index order, one contiguous array: needed for the sorted
+      // indices and for the full sort of M; the buckets read the staging
+      auto gather_in_order = [&]() -> int {
+        LAPSUM_TRY(launch_partition_totals(w.blk, w.nblocks, w.sel, use_sel, aL, aR, w.offsets,
+                                           w.tot, s));
+        LAPSUM_TRY(launch_gather(r, n, w.tot, w.blk, w.offsets, w.nblocks, w.chunk, w.stage_v,
+                                 w.stage_i, mcap, w.m_keys, w.m_idx, s));
+        return LAPSUM_OK;
+      };
       const int32_t* sorted_idx = nullptr;
       PartTotals tot;
       // M by sorting all of it (needed for the sorted indices, or when the
@@ -407,32 +412,20 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
       };
       bool have_rec = false;
       if (!want_idx) {
-        // buckets, sized from the expected |M|, with no wait for the totals:
-        // the first bracket holds about n (l - j) / K scores, a widened one
-        // about three times the previous middle set
-        int64_t expect;
-        if (attempt == 1) {
-          const double lo = static_cast<double>(j < 0 ? 0 : j);
-          const double hi = static_cast<double>(l > K + 1 ? K + 1 : l);
-          expect = static_cast<int64_t>(static_cast<double>(n) * ((hi - lo) / static_cast<double>(K)));
-        } else {
-          expect = 3 * prev_m;
-        }
-        int64_t grid_m = 2 * expect + 65536;
-        if (grid_m > mcap) grid_m = mcap;
-        if (grid_m > kBucketMaxM) grid_m = kBucketMaxM;
-        LAPSUM_TRY(launch_bucket_solve(w.m_keys, mcap, grid_m, w.acc, w.tot, k, t, n, w.rec, s));
+        // buckets straight from the staging, with no wait for the totals
+        const PartSource ps{w.blk, w.nblocks, w.stage_v, w.sel, use_sel, aL, aR};
+        LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec, s));
         st = emit_and_read();
         if (st != LAPSUM_OK) return st;
         tot = hs->att.tot;
         have_rec = true;
       } else {
-        st = copy_back(&hs->att, w.att, ev, s);
+        st = gather_in_order();
+        if (st == LAPSUM_OK) st = copy_back(&hs->att, w.att, ev, s);
         if (st == LAPSUM_OK) st = wait_back(ev);
         if (st != LAPSUM_OK) return st;
         tot = hs->att.tot;
       }
-      prev_m = tot.nM;
       aL = tot.aL;
       aR = tot.aR;
       rec_info.attempts = attempt;
@@ -451,7 +444,8 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
         break;
       }
       if (!have_rec || (!hs->att.rec.ok && hs->att.rec.side >= 2)) {
-        st = solve_sorted();
+        st = have_rec ? gather_in_order() : LAPSUM_OK;
+        if (st == LAPSUM_OK) st = solve_sorted();
         if (st == LAPSUM_OK) st = emit_and_read();
         if (st != LAPSUM_OK) return st;
       }
