@@ -1,10 +1,11 @@
 // The probabilistic bracket (§4, Suppl. B, Suppl. C, Algorithm 1):
 //   sample            y_s = fl32(r[s * floor(n/K)] + eps_s) (the systematic
 //                     sampler: strided view + cached kernel noise), stored as
-//                     ascending uint32 keys, plus a histogram of their top
-//                     11 bits
+//                     ascending uint32 keys grouped per block by their top
+//                     11 bits, with the bin offsets
 //   select            the j-th and l-th smallest y (Eq. (8)) by an 11/11/10
-//                     bit radix select in one workgroup
+//                     bit radix select in one workgroup (only the keys of the
+//                     target's top-11-bit bin are fetched)
 //   partition         the single streaming pass: L = {r < a_L},
 //                     M = {a_L <= r < a_R}, R = {r >= a_R}, the tail sums of
 //                     Eq. (7) and counts, M compacted in index order into the
@@ -25,6 +26,7 @@ __device__ __forceinline__ float asc_key_float(uint32_t k) { return key_float(~k
 
 constexpr int kSampleThreads = 256;
 constexpr int kSampleItems = 8;
+constexpr int64_t kSampleBlock = static_cast<int64_t>(kSampleThreads) * kSampleItems;   // 2048
 constexpr int kSelThreads = 1024;
 constexpr int PT = kPartThreads;               // 256
 constexpr int PW = PT / kWave;                 // 4 waves
@@ -32,59 +34,108 @@ constexpr int PW = PT / kWave;                 // 4 waves
 }  // namespace
 
 // ----------------------------------------------------------------- sample --
+// Block b draws samples [b SB, b SB + SB) (kSampleItems per thread, all loads
+// in flight together) and writes their keys grouped by the top 11 bits
+// (kSelectBins bins, any order inside a bin) into its own region of ykeys,
+// with the exclusive bin offsets soffs[b (kSelectBins + 1) + bin] and the bin
+// counts packed two to a word (16 bits each) in scnt[b kSelectBins / 2 + i];
+// nothing needs to be zero beforehand.  The blocks also clear `zero`
+// (zero_words u32), which later passes accumulate into.
 __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __restrict__ r,
                                                                 int64_t n,
                                                                 const float* __restrict__ noise,
                                                                 int64_t K, uint32_t* __restrict__ ykeys,
-                                                                uint32_t* __restrict__ hist) {
+                                                                uint32_t* __restrict__ soffs,
+                                                                uint32_t* __restrict__ scnt,
+                                                                uint32_t* __restrict__ zero,
+                                                                int64_t zero_words) {
   __shared__ uint32_t h[kSelectBins];
-  for (int e = threadIdx.x; e < kSelectBins; e += kSampleThreads) h[e] = 0u;
-  __syncthreads();
-  // kSampleItems draws per thread, all loads in flight together; a block's
-  // histogram goes out once (few, larger blocks: fewer global atomics)
+  __shared__ uint32_t wsum[kSampleThreads / kWave];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < kSelectBins; e += kSampleThreads) h[e] = 0u;
+  for (int64_t w = static_cast<int64_t>(blockIdx.x) * kSampleThreads + tid; w < zero_words;
+       w += static_cast<int64_t>(gridDim.x) * kSampleThreads)
+    zero[w] = 0u;
   const int64_t stride = n / K;
-  const int64_t s0 = static_cast<int64_t>(blockIdx.x) * kSampleThreads * kSampleItems + threadIdx.x;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kSampleBlock;
   float rv[kSampleItems], ev[kSampleItems];
 #pragma unroll
   for (int i = 0; i < kSampleItems; ++i) {
-    const int64_t s = s0 + static_cast<int64_t>(i) * kSampleThreads;
+    const int64_t s = base + static_cast<int64_t>(i) * kSampleThreads + tid;
     const int64_t sc = s < K ? s : K - 1;
     rv[i] = r[sc * stride];
     ev[i] = noise[sc];
   }
+  __syncthreads();
+  uint32_t key[kSampleItems], slot[kSampleItems];
 #pragma unroll
   for (int i = 0; i < kSampleItems; ++i) {
-    const int64_t s = s0 + static_cast<int64_t>(i) * kSampleThreads;
-    if (s < K) {
-      const float y = rv[i] + ev[i];   // float32 addition
-      const uint32_t key = asc_key(y);
-      ykeys[s] = key;
-      atomicAdd(&h[key >> 21], 1u);
-    }
+    const int64_t s = base + static_cast<int64_t>(i) * kSampleThreads + tid;
+    key[i] = asc_key(rv[i] + ev[i]);   // float32 addition
+    slot[i] = s < K ? atomicAdd(&h[key[i] >> 21], 1u) : 0u;
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < kSelectBins; e += kSampleThreads)
-    if (h[e]) atomicAdd(&hist[e], h[e]);
+  // exclusive offsets of the bins, PER consecutive bins per thread
+  constexpr int PER = kSelectBins / kSampleThreads;
+  uint32_t c[PER];
+  uint32_t loc = 0u;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    c[e] = h[PER * tid + e];
+    loc += c[e];
+  }
+  uint32_t incl = loc;
+  const int lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  const int wid = tid / kWave;
+  if (lane == kWave - 1) wsum[wid] = incl;
+  __syncthreads();
+  uint32_t run = incl - loc;
+  for (int w = 0; w < wid; ++w) run += wsum[w];
+  uint32_t* so = soffs + static_cast<int64_t>(blockIdx.x) * (kSelectBins + 1);
+  uint32_t* sc = scnt + static_cast<int64_t>(blockIdx.x) * (kSelectBins / 2);
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    h[PER * tid + e] = run;
+    so[PER * tid + e] = run;
+    run += c[e];
+  }
+#pragma unroll
+  for (int e = 0; e < PER / 2; ++e) sc[PER / 2 * tid + e] = c[2 * e] | (c[2 * e + 1] << 16);
+  if (tid == kSampleThreads - 1) so[kSelectBins] = run;
+  __syncthreads();
+  uint32_t* yk = ykeys + base;
+#pragma unroll
+  for (int i = 0; i < kSampleItems; ++i) {
+    const int64_t s = base + static_cast<int64_t>(i) * kSampleThreads + tid;
+    if (s < K) yk[h[key[i] >> 21] + slot[i]] = key[i];
+  }
 }
 
+int sample_blocks(int64_t K) { return static_cast<int>((K + kSampleBlock - 1) / kSampleBlock); }
+
 hipError_t launch_sample(const float* r, int64_t n, const float* noise, int64_t K,
-                         uint32_t* ykeys, uint32_t* hist, hipStream_t s) {
-  const int64_t per = static_cast<int64_t>(kSampleThreads) * kSampleItems;
-  const int64_t blocks = (K + per - 1) / per;
+                         uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,
+                         int64_t zero_words, hipStream_t s) {
   { ProfScope ps_("sample", s);
-  hipLaunchKernelGGL(sample_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kSampleThreads), 0,
-                     s, r, n, noise, K, ykeys, hist); }
+  hipLaunchKernelGGL(sample_kernel, dim3(static_cast<unsigned>(sample_blocks(K))),
+                     dim3(kSampleThreads), 0, s, r, n, noise, K, ykeys, soffs, scnt, zero,
+                     zero_words); }
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------------- select --
 namespace {
 
-// Find the bin of a histogram (nb bins in LDS) holding 1-based rank `rank`;
-// writes (bin, rank inside the bin) to *bin_out, *rank_out.
+// 1-based rank `rank` in the histogram h (nb bins in LDS, nb / kSelThreads
+// consecutive bins per thread): writes (bin, rank inside the bin).  Ends
+// with a barrier.
 __device__ void find_bin(const uint32_t* h, int nb, uint32_t rank, uint32_t* wsum, int* bin_out,
                          uint32_t* rank_out) {
-  // each thread owns nb / kSelThreads consecutive bins (nb = 1024 or 2048)
   const int tid = threadIdx.x;
   const int per = nb / kSelThreads;
   uint32_t loc = 0;
@@ -113,9 +164,6 @@ __device__ void find_bin(const uint32_t* h, int nb, uint32_t rank, uint32_t* wsu
   __syncthreads();
 }
 
-}  // namespace
-
-namespace {
 constexpr int kCand = 4096;   // candidates per target kept in LDS
 
 // Histogram (into h, nb bins) of (key >> lo) & mask over the keys whose
@@ -134,79 +182,113 @@ __device__ void prefix_hist(const uint32_t* keys, int64_t count, int hi, uint32_
 
 // One workgroup.  Targets are 1-based ranks among the K sample keys; a rank
 // outside 1..K gives -inf (below) or +inf (above).  Level 1 (top 11 bits)
-// comes from the sample kernel's histogram; one vectorized pass then copies
-// each target's bin into LDS, where bits 10..20 and 0..9 are resolved.  A
-// bin too large for LDS is resolved by passes over the keys in memory.
+// sums the sample blocks' bin counts; the keys of each target's bin are then
+// fetched from every block's region (only that bin) into LDS, where bits
+// 10..20 and 0..9 are resolved.  A bin too large for LDS is resolved by
+// passes over all keys in memory.
+constexpr int kSelBatch = 64;   // sample blocks whose counts one thread loads at once
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __restrict__ ykeys,
                                                              int64_t K,
-                                                             const uint32_t* __restrict__ hist,
-                                                             int64_t j, int64_t l,
+                                                             const uint32_t* __restrict__ soffs,
+                                                             const uint32_t* __restrict__ scnt,
+                                                             int nsb, int64_t j, int64_t l,
                                                              SelectRec* __restrict__ out) {
+  __shared__ uint32_t h1[kSelectBins];   // level-1 counts (kept for both targets)
   __shared__ uint32_t h[kSelectBins];
   __shared__ uint32_t wsum[kSelThreads / kWave];
   __shared__ int bin_s;
   __shared__ uint32_t rank_s;
-  __shared__ uint32_t cand[2][kCand];
-  __shared__ uint32_t ccnt[2];
+  __shared__ uint32_t cand[kCand];
+  __shared__ uint32_t bst[kSelThreads];    // per sample block: start of the bin in its region
+  __shared__ uint32_t bpre[kSelThreads + 1];   // exclusive prefix of the bin's counts over blocks
   const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
   const int64_t tgt[2] = {j, l};
   bool live[2];
-  uint32_t pre[2] = {0u, 0u}, rk[2] = {0u, 0u}, key_out[2] = {0u, 0u};
+  uint32_t key_out[2] = {0u, 0u};
   for (int q = 0; q < 2; ++q) live[q] = (tgt[q] >= 1 && tgt[q] <= K);
 
-  for (int q = 0; q < 2; ++q) {
-    if (!live[q]) continue;
-    for (int e = tid; e < kSelectBins; e += kSelThreads) h[e] = hist[e];
-    __syncthreads();
-    find_bin(h, kSelectBins, static_cast<uint32_t>(tgt[q]), wsum, &bin_s, &rank_s);
-    pre[q] = static_cast<uint32_t>(bin_s);
-    rk[q] = rank_s;
-    __syncthreads();
-  }
-  if (tid < 2) ccnt[tid] = 0u;
-  __syncthreads();
-  auto collect = [&](uint32_t key) {
+  // 1. bin counts summed over the sample blocks: thread tid takes bins 2 tid
+  //    and 2 tid + 1, one packed word per block (kSelBatch blocks' loads in
+  //    flight at a time)
+  {
+    static_assert(kSelectBins == 2 * kSelThreads, "two bins per select thread");
+    uint32_t c0 = 0u, c1 = 0u;
+    for (int b0 = 0; b0 < nsb; b0 += kSelBatch) {
+      uint32_t wv[kSelBatch];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      if (live[q] && (key >> 21) == pre[q]) {
-        const uint32_t c = atomicAdd(&ccnt[q], 1u);
-        if (c < static_cast<uint32_t>(kCand)) cand[q][c] = key;
+      for (int u = 0; u < kSelBatch; ++u) {
+        const int b = b0 + u < nsb ? b0 + u : nsb - 1;
+        wv[u] = scnt[static_cast<int64_t>(b) * (kSelectBins / 2) + tid];
       }
-    }
-  };
-  const int64_t K4 = K / 4;
-  const uint4* y4 = reinterpret_cast<const uint4*>(ykeys);
-  int64_t i4 = tid;
-  for (; i4 + 7 * kSelThreads < K4; i4 += 8 * kSelThreads) {   // eight loads in flight
-    uint4 v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = y4[i4 + u * kSelThreads];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      collect(v[u].x);
-      collect(v[u].y);
-      collect(v[u].z);
-      collect(v[u].w);
+      for (int u = 0; u < kSelBatch; ++u)
+        if (b0 + u < nsb) {
+          c0 += wv[u] & 0xffffu;
+          c1 += wv[u] >> 16;
+        }
     }
+    h1[2 * tid] = c0;
+    h1[2 * tid + 1] = c1;
   }
-  for (; i4 < K4; i4 += kSelThreads) {
-    const uint4 v = y4[i4];
-    collect(v.x);
-    collect(v.y);
-    collect(v.z);
-    collect(v.w);
-  }
-  for (int64_t i = K4 * 4 + tid; i < K; i += kSelThreads) collect(ykeys[i]);
   __syncthreads();
 
   for (int q = 0; q < 2; ++q) {
-    if (!live[q]) continue;
-    const bool in_lds = ccnt[q] <= static_cast<uint32_t>(kCand);
-    const uint32_t* src = in_lds ? cand[q] : ykeys;
-    const int64_t count = in_lds ? static_cast<int64_t>(ccnt[q]) : K;
-    prefix_hist(src, count, 21, pre[q], 10, 2047u, 2048, h);
-    find_bin(h, 2048, rk[q], wsum, &bin_s, &rank_s);
-    const uint32_t pre2 = (pre[q] << 11) | static_cast<uint32_t>(bin_s);
+    if (!live[q]) continue;   // the same in every thread
+    find_bin(h1, kSelectBins, static_cast<uint32_t>(tgt[q]), wsum, &bin_s, &rank_s);
+    const uint32_t pre = static_cast<uint32_t>(bin_s);
+    const uint32_t rk = rank_s;
+    const uint32_t total = h1[pre];
+    const uint32_t* src = ykeys;
+    int64_t count = K;
+    if (total <= static_cast<uint32_t>(kCand)) {
+      // 2. the bin's keys from every block's region, in block order
+      uint32_t run = 0u;   // keys fetched so far (same in every thread)
+      for (int b0 = 0; b0 < nsb; b0 += kSelThreads) {
+        const int b = b0 + tid;
+        uint32_t st = 0u, cnt = 0u;
+        if (b < nsb) {
+          const uint32_t* so = soffs + static_cast<int64_t>(b) * (kSelectBins + 1);
+          st = so[pre];
+          cnt = so[pre + 1] - st;
+        }
+        uint32_t incl = cnt;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+          const uint32_t y = __shfl_up(incl, o, kWave);
+          if (lane >= o) incl += y;
+        }
+        if (lane == kWave - 1) wsum[wid] = incl;
+        __syncthreads();
+        uint32_t wb = 0u, all = 0u;
+        for (int w = 0; w < kSelThreads / kWave; ++w) {
+          if (w < wid) wb += wsum[w];
+          all += wsum[w];
+        }
+        bst[tid] = st;
+        bpre[tid] = wb + incl - cnt;
+        if (tid == 0) bpre[kSelThreads] = all;
+        __syncthreads();
+        const int nb = nsb - b0 < kSelThreads ? nsb - b0 : kSelThreads;
+        for (uint32_t e = tid; e < all; e += kSelThreads) {
+          int lo = 0, hi = nb;   // bpre[lo] <= e < bpre[hi]
+          while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (bpre[mid] <= e) lo = mid; else hi = mid;
+          }
+          cand[run + e] = ykeys[static_cast<int64_t>(b0 + lo) * kSampleBlock + bst[lo] + (e - bpre[lo])];
+        }
+        run += all;
+        __syncthreads();
+      }
+      src = cand;
+      count = total;
+    }
+    // 3. bits 10..20, then 0..9, of the bin's keys
+    prefix_hist(src, count, 21, pre, 10, 2047u, 2048, h);
+    find_bin(h, 2048, rk, wsum, &bin_s, &rank_s);
+    const uint32_t pre2 = (pre << 11) | static_cast<uint32_t>(bin_s);
     const uint32_t rk2 = rank_s;
     __syncthreads();
     prefix_hist(src, count, 10, pre2, 0, 1023u, 1024, h);
@@ -224,10 +306,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __r
   }
 }
 
-hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* hist, int64_t j,
-                         int64_t l, SelectRec* out, hipStream_t s) {
+hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* soffs,
+                         const uint32_t* scnt, int64_t j, int64_t l, SelectRec* out,
+                         hipStream_t s) {
   { ProfScope ps_("select", s);
-  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kSelThreads), 0, s, ykeys, K, hist, j, l, out); }
+  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kSelThreads), 0, s, ykeys, K, soffs, scnt,
+                     sample_blocks(K), j, l, out); }
   return hipGetLastError();
 }
 

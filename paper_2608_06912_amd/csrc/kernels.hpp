@@ -178,10 +178,16 @@ constexpr int kSolveTileDoubles = 8;
 hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s);
 
 // Bracketed pipeline.
+// ykeys: [K]; soffs: [sample_blocks(K) * (kSelectBins + 1)]; scnt:
+// [sample_blocks(K) * kSelectBins / 2]; the sample also clears
+// zero[0 .. zero_words) for passes that accumulate later.
+int sample_blocks(int64_t K);
 hipError_t launch_sample(const float* r, int64_t n, const float* noise, int64_t K,
-                         uint32_t* ykeys, uint32_t* hist, hipStream_t s);
-hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* hist, int64_t j,
-                         int64_t l, SelectRec* out, hipStream_t s);
+                         uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,
+                         int64_t zero_words, hipStream_t s);
+hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* soffs,
+                         const uint32_t* scnt, int64_t j, int64_t l, SelectRec* out,
+                         hipStream_t s);
 int partition_blocks(int64_t n, int64_t* chunk);
 int band_wave_cap(int64_t chunk);
 // Bytes of one row's context and its layout at `base` (null base: sizes only).

@@ -177,7 +177,9 @@ struct AttemptRec {
 
 struct BracketWs {
   uint32_t* ykeys;
-  uint32_t* hist;
+  uint32_t* soffs;
+  uint32_t* scnt;
+  uint32_t* hist;      // the bucket accumulators' words
   BucketAcc acc;
   SelectRec* sel;
   PartBlock* blk;
@@ -204,11 +206,14 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
   BracketWs w{};
   w.nblocks = partition_blocks(n, &w.chunk);
   w.ykeys = c.take<uint32_t>(K);
-  // one zero-filled region: the sample histogram, then the bucket accumulators
-  w.hist = c.take<uint32_t>(kSelectBins + kBucketAccWords);
-  w.acc.n = w.hist + kSelectBins;
-  w.acc.u = reinterpret_cast<unsigned long long*>(w.hist + kSelectBins + kBucketCount);
-  w.acc.d = reinterpret_cast<unsigned long long*>(w.hist + kSelectBins + 3 * kBucketCount);
+  // the sample's bin offsets per block, and the bucket accumulators (which
+  // the sample clears)
+  w.soffs = c.take<uint32_t>(static_cast<size_t>(sample_blocks(K)) * (kSelectBins + 1));
+  w.scnt = c.take<uint32_t>(static_cast<size_t>(sample_blocks(K)) * (kSelectBins / 2));
+  w.hist = c.take<uint32_t>(kBucketAccWords);
+  w.acc.n = w.hist;
+  w.acc.u = reinterpret_cast<unsigned long long*>(w.hist + kBucketCount);
+  w.acc.d = reinterpret_cast<unsigned long long*>(w.hist + 3 * kBucketCount);
   w.acc.keys = c.take<uint32_t>(bucket_keys_words(w.nblocks));
   w.acc.offs = c.take<uint32_t>(bucket_offs_words(w.nblocks));
   w.acc.parts = c.take<CountPart>(static_cast<size_t>(bucket_groups(w.nblocks)));
@@ -353,9 +358,8 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
   if (st != LAPSUM_OK) return st;
 
   if (!(flags & LAPSUM_FLAG_FULL_SORT)) {
-    LAPSUM_TRY(launch_fill_u32(w.hist, kSelectBins + kBucketAccWords, 0u, s));
-    LAPSUM_TRY(launch_sample(r, n, noise, K, w.ykeys, w.hist, s));
-    LAPSUM_TRY(launch_select(w.ykeys, K, w.hist, j, l, w.sel, s));
+    LAPSUM_TRY(launch_sample(r, n, noise, K, w.ykeys, w.soffs, w.scnt, w.hist, kBucketAccWords, s));
+    LAPSUM_TRY(launch_select(w.ykeys, K, w.soffs, w.scnt, j, l, w.sel, s));
     float aL = 0.0f, aR = 0.0f;
     const bool want_idx = midx_row != nullptr;
     for (int attempt = 1; attempt <= 3 && !solved; ++attempt) {

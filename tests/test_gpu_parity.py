@@ -304,6 +304,32 @@ def test_bracketed_root_in_a_large_tie(lib):
     assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
 
 
+@pytest.mark.parametrize("distinct,copies", [(1, 100), (600, 1), (1500, 2)])
+def test_bracketed_root_bucket_sizes(lib, distinct, copies):
+    # scores packed at the root put about distinct * copies keys into the
+    # bucket (or two) holding it: a few tied keys are solved term by term,
+    # a few hundred to a few thousand are sorted on chip first
+    n = 200_000
+    r = W.random_case(31, n, dist="normal")[0]
+    v = np.float32(np.quantile(r, 0.9))
+    cluster = np.empty(distinct, dtype=np.float32)
+    x = v
+    for i in range(distinct):
+        cluster[i] = x
+        x = np.nextafter(x, np.float32(np.inf))
+    at = np.random.default_rng(32).choice(n, distinct * copies, replace=False)
+    r[at] = np.repeat(cluster, copies)
+    alpha = -0.05
+    k = O.lapsum(r, float(cluster[distinct // 2]), 0.05)   # the root is inside the pack
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([84, distinct], K, 0.05)
+    g = W.random_case(33, n, dist="normal")[0]
+    label = f"pack {distinct}x{copies}"
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=label, g=g)
+    assert not info["fell_back"], label
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL, label
+
+
 @pytest.mark.timeout(300)
 def test_bracketed_band_too_wide_for_the_lists(lib):
     # a temperature wide compared with the score spread puts every score in
