@@ -333,7 +333,7 @@ struct PartState {
   int64_t nL, nR;
   int64_t nM;   // M count of this wave (uniform across the wave)
   float mmin, mmax;
-  int64_t nB;   // unused by the pass (the band count is the wave's LDS counter)
+  int64_t nB;   // band members of this wave (uniform across the wave)
 };
 
 // Where a wave stages its band members and its bits of r >= hi.  Both go
@@ -344,7 +344,6 @@ constexpr int kOnesWaveWords = static_cast<int>(kBandMaxChunk / 4 / 32);   // 51
 
 struct BandWave {
   BandEntry* sbuf;   // LDS, cap entries
-  uint32_t* scnt;    // LDS counter of the wave's band members
   uint32_t* sones;   // LDS, kOnesWaveWords words: bit i of the wave's range
   int cap;
   bool stage;        // false when the block's range is too long for the band passes
@@ -383,11 +382,15 @@ __device__ __forceinline__ void classify4(const float (&v)[4], const bool (&ok)[
 constexpr int kWaveStage = kPartStageCap / PW;   // M entries staged per wave
 
 // Per-wave pass over [w0, w1): tails in float32 over one float4 and float64
-// across, R counted only when a_R is finite (HAS_R), band members and M
-// members (a subset of the band) staged in index order, and with a finite
-// a_R one bit per score for r >= hi.  L is not counted:
+// across, R counted only when a_R is finite (HAS_R), band members staged in
+// any order and M members (a subset of the band) in index order, and with a
+// finite a_R one bit per score for r >= hi.  L is not counted:
 // n_L = scores - n_M - n_R.
-template <bool HAS_R>
+// With STAGE the L tail is summed once at the end from the wave's staged
+// band (its members below a_L are the only nonzero terms), or from a second
+// read of the range if the list overflowed; without it (a range too long to
+// stage) each member's term is formed as it is met.
+template <bool HAS_R, bool STAGE>
 __device__ __forceinline__ void partition_range(const float* __restrict__ r, int64_t w0, int64_t w1,
                                                 bool vec, float aL, float aR, float c2f,
                                                 float* sv, int32_t* si, const BandWave& bw,
@@ -422,20 +425,25 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       x |= __shfl_xor(x, 4, kWave);
       if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
     }
-    // band members are appended through the wave's LDS counter (in any
-    // order; the list is put in index order once, at the end of the range).
-    // The L tail's terms are formed here too: below the band's lower edge
-    // (a_L - 105 t) a term e^{(r - a_L)/t} is exactly 0 in float32.
-    if (bb) {
-      float tl = 0.0f;
+    // band members take slots from ballots and the wave's running count
+    // (element-major, so not in index order; the emit puts each block's
+    // list in index order).  The L tail's terms are formed here too: below
+    // the band's lower edge (a_L - 105 t) a term e^{(r - a_L)/t} is exactly
+    // 0 in float32.
+    if (__ballot(bb != 0u)) {
+      if (!STAGE && bb) {
+        float tl = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (((bb >> e) & 1u) && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
-      st.TL += static_cast<double>(tl);
+        for (int e = 0; e < 4; ++e)
+          if (((bb >> e) & 1u) && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
+        st.TL += static_cast<double>(tl);
+      }
+      uint32_t nb = static_cast<uint32_t>(st.nB);   // uniform across the wave
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
+        const uint64_t bal = __ballot((bb >> e) & 1u);
         if ((bb >> e) & 1u) {
-          const uint32_t slot = atomicAdd(bw.scnt, 1u);
+          const uint32_t slot = nb + lanes_below(bal);
           if (slot < static_cast<uint32_t>(bw.cap)) {
             BandEntry en;
             en.idx = static_cast<int32_t>(i0 + e);
@@ -443,7 +451,9 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
             bw.sbuf[slot] = en;
           }
         }
+        nb += static_cast<uint32_t>(__popcll(bal));
       }
+      st.nB = nb;
     }
     if (__ballot(mb != 0u)) {   // rare: some lane holds an M member
       uint32_t before = 0, total = 0;
@@ -505,6 +515,23 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       v[e] = ok[e] ? r[i0 + e] : 0.0f;
     }
     one(v, ok, it);
+  }
+  if constexpr (STAGE) {
+    // the L tail: e^{(r - a_L)/t} over the band members below a_L, each
+    // term in float32 and summed per lane in float64
+    double tl = 0.0;
+    if (st.nB <= bw.cap) {
+      for (int q = lane; q < static_cast<int>(st.nB); q += kWave) {
+        const float x = __uint_as_float(bw.sbuf[q].bits);
+        if (x < aL) tl += static_cast<double>(exp2_fast((x - aL) * c2f));
+      }
+    } else {
+      for (int64_t i = w0 + lane; i < w1; i += kWave) {
+        const float x = r[i];
+        if (!(x < bw.lo) && x < aL) tl += static_cast<double>(exp2_fast((x - aL) * c2f));
+      }
+    }
+    st.TL += tl;
   }
 }
 
@@ -675,12 +702,9 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   const int64_t w0 = b0 + wid * wq < n ? b0 + wid * wq : n;
   const int64_t w1 = w0 + wq < n ? w0 + wq : n;
   const bool vec = (reinterpret_cast<uintptr_t>(r) & 15) == 0;
-  __shared__ uint32_t scnt[PW];
   BandWave bw;
   bw.sbuf = sband[wid];
   bw.sones = sones[wid];
-  bw.scnt = &scnt[wid];
-  if (lane == 0) scnt[wid] = 0u;   // wave-private: the wave's LDS accesses stay in order
   bw.stage = chunk <= kBandMaxChunk;
   bw.cap = bw.stage ? (bcap < kBandWaveCapMax ? bcap : kBandWaveCapMax) : 0;
   // rounded outwards so that the float comparisons imply the float64 bounds
@@ -690,10 +714,15 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY, 0};
   const bool has_r = aR < INFINITY;
   if (has_r)
-    partition_range<true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
+    if (bw.stage)
+      partition_range<true, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
+    else
+      partition_range<true, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
   else
-    partition_range<false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
-  st.nB = *bw.scnt;
+    if (bw.stage)
+      partition_range<false, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
+    else
+      partition_range<false, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
   // this wave's bits and band list (in the order the members were met) out
   // of LDS; the emit puts the block's list in index order
   if (bw.stage) {
