@@ -399,24 +399,28 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
   // it: first score of this wave's 256-score step (a multiple of 256)
   auto one = [&](const float (&v)[4], const bool (&ok)[4], int64_t it) {
     const int64_t i0 = it + 4 * lane;
-    float tr = 0.0f;
-    uint32_t mb = 0, bb = 0, ob = 0;
+    // membership as lane masks: a comparison is its own ballot
+    bool inB[4], inM[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const bool L = v[e] < aL;
       if constexpr (HAS_R) {
-        const bool R = v[e] >= aR;
-        tr += (ok[e] && R) ? exp2_fast((aR - v[e]) * c2f) : 0.0f;
-        st.nR += (ok[e] && R) ? 1 : 0;
-        if (ok[e] && !L && !R) mb |= 1u << e;
-        if (ok[e] && v[e] >= bw.hi) ob |= 1u << e;
-        if (ok[e] && !(v[e] < bw.lo) && !(v[e] >= bw.hi)) bb |= 1u << e;
+        inB[e] = ok[e] && !(v[e] < bw.lo) && !(v[e] >= bw.hi);
+        inM[e] = ok[e] && !(v[e] < aL) && !(v[e] >= aR);
       } else {
-        if (ok[e] && !L) mb |= 1u << e;
-        if (ok[e] && !(v[e] < bw.lo)) bb |= 1u << e;
+        inB[e] = ok[e] && !(v[e] < bw.lo);
+        inM[e] = ok[e] && !(v[e] < aL);
       }
     }
     if constexpr (HAS_R) {
+      float tr = 0.0f;
+      uint32_t ob = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool R = v[e] >= aR;
+        tr += (ok[e] && R) ? exp2_fast((aR - v[e]) * c2f) : 0.0f;
+        st.nR += (ok[e] && R) ? 1 : 0;
+        if (ok[e] && v[e] >= bw.hi) ob |= 1u << e;
+      }
       st.TR += static_cast<double>(tr);
       // 8 lanes hold the 32 bits of one word
       uint32_t x = ob << (4 * (lane & 7));
@@ -425,48 +429,55 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       x |= __shfl_xor(x, 4, kWave);
       if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
     }
-    // band members take slots from ballots and the wave's running count
+    // band members take slots from the masks and the wave's running count
     // (element-major, so not in index order; the emit puts each block's
-    // list in index order).  The L tail's terms are formed here too: below
-    // the band's lower edge (a_L - 105 t) a term e^{(r - a_L)/t} is exactly
-    // 0 in float32.
-    if (__ballot(bb != 0u)) {
-      if (!STAGE && bb) {
+    // list in index order)
+    uint64_t bm[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) bm[e] = __ballot(inB[e]);
+    if (bm[0] | bm[1] | bm[2] | bm[3]) {
+      if (!STAGE) {
+        // the L tail's terms as they are met: below the band's lower edge
+        // (a_L - 105 t) a term e^{(r - a_L)/t} is exactly 0 in float32
         float tl = 0.0f;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          if (((bb >> e) & 1u) && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
+          if (inB[e] && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
         st.TL += static_cast<double>(tl);
       }
-      uint32_t nb = static_cast<uint32_t>(st.nB);   // uniform across the wave
+      const uint32_t nb0 = static_cast<uint32_t>(st.nB);   // uniform across the wave
+      uint32_t tot = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) tot += static_cast<uint32_t>(__popcll(bm[e]));
+      const bool room = nb0 + tot <= static_cast<uint32_t>(bw.cap);   // uniform
+      uint32_t nb = nb0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const uint64_t bal = __ballot((bb >> e) & 1u);
-        if ((bb >> e) & 1u) {
-          const uint32_t slot = nb + lanes_below(bal);
-          if (slot < static_cast<uint32_t>(bw.cap)) {
+        if (inB[e]) {
+          const uint32_t slot = nb + lanes_below(bm[e]);
+          if (room || slot < static_cast<uint32_t>(bw.cap)) {
             BandEntry en;
             en.idx = static_cast<int32_t>(i0 + e);
             en.bits = __float_as_uint(v[e]);
             bw.sbuf[slot] = en;
           }
         }
-        nb += static_cast<uint32_t>(__popcll(bal));
+        nb += static_cast<uint32_t>(__popcll(bm[e]));
       }
-      st.nB = nb;
+      st.nB = nb0 + tot;
     }
-    if (__ballot(mb != 0u)) {   // rare: some lane holds an M member
+    if (__ballot(inM[0] || inM[1] || inM[2] || inM[3])) {   // rare: some lane holds an M member
       uint32_t before = 0, total = 0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const uint64_t bal = __ballot((mb >> e) & 1u);
+        const uint64_t bal = __ballot(inM[e]);
         before += lanes_below(bal);
         total += static_cast<uint32_t>(__popcll(bal));
       }
       uint32_t idx = static_cast<uint32_t>(st.nM) + before;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        if ((mb >> e) & 1u) {
+        if (inM[e]) {
           st.mmin = fminf(st.mmin, v[e]);
           st.mmax = fmaxf(st.mmax, v[e]);
           if (idx < static_cast<uint32_t>(kWaveStage)) {
@@ -482,27 +493,34 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
   constexpr int U = 4;   // float4 loads per lane per batch, two batches in flight
   int64_t it = w0;
   if (vec && it + U * 256 <= w1) {
-    float4 q[U];
+    // two buffers taking turns, so that no registers are copied per batch
+    auto load = [&](float4 (&q)[U], int64_t at) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) q[u] = load_stream4(r + it + u * 256 + 4 * lane);
-    while (true) {
-      const int64_t cur = it;
-      it += U * 256;
-      const bool more = it + U * 256 <= w1;
-      float4 qn[U];
-      if (more) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) qn[u] = load_stream4(r + it + u * 256 + 4 * lane);
-      }
+      for (int u = 0; u < U; ++u) q[u] = load_stream4(r + at + u * 256 + 4 * lane);
+    };
+    auto run = [&](const float4 (&q)[U], int64_t at) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const float v[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
         const bool ok[4] = {true, true, true, true};
-        one(v, ok, cur + u * 256);
+        one(v, ok, at + u * 256);
       }
-      if (!more) break;
-#pragma unroll
-      for (int u = 0; u < U; ++u) q[u] = qn[u];
+    };
+    float4 qa[U], qb[U];
+    load(qa, it);
+    while (true) {
+      const int64_t ca = it;
+      it += U * 256;
+      const bool more_a = it + U * 256 <= w1;
+      if (more_a) load(qb, it);
+      run(qa, ca);
+      if (!more_a) break;
+      const int64_t cb = it;
+      it += U * 256;
+      const bool more_b = it + U * 256 <= w1;
+      if (more_b) load(qa, it);
+      run(qb, cb);
+      if (!more_b) break;
     }
   }
   for (; it < w1; it += 256) {
