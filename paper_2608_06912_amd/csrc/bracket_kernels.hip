@@ -449,20 +449,40 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       uint32_t tot = 0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) tot += static_cast<uint32_t>(__popcll(bm[e]));
-      const bool room = nb0 + tot <= static_cast<uint32_t>(bw.cap);   // uniform
-      uint32_t nb = nb0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (inB[e]) {
-          const uint32_t slot = nb + lanes_below(bm[e]);
-          if (room || slot < static_cast<uint32_t>(bw.cap)) {
+      const uint32_t cap = static_cast<uint32_t>(bw.cap);
+      const uint64_t any = bm[0] | bm[1] | bm[2] | bm[3];
+      const uint64_t two = (bm[0] & (bm[1] | bm[2] | bm[3])) | (bm[1] & (bm[2] | bm[3])) |
+                           (bm[2] & bm[3]);   // lanes with two or more members
+      if (two == 0ull) {
+        // each lane holds at most one member: its slot is its rank among
+        // the lanes that hold one (scalar mask work, a few vector ops)
+        if (inB[0] || inB[1] || inB[2] || inB[3]) {
+          const uint32_t slot = nb0 + lanes_below(any);
+          const int e0 = inB[0] ? 0 : (inB[1] ? 1 : (inB[2] ? 2 : 3));
+          const float x0 = inB[0] ? v[0] : (inB[1] ? v[1] : (inB[2] ? v[2] : v[3]));
+          if (slot < cap) {
             BandEntry en;
-            en.idx = static_cast<int32_t>(i0 + e);
-            en.bits = __float_as_uint(v[e]);
+            en.idx = static_cast<int32_t>(i0 + e0);
+            en.bits = __float_as_uint(x0);
             bw.sbuf[slot] = en;
           }
         }
-        nb += static_cast<uint32_t>(__popcll(bm[e]));
+      } else {
+        // element-major: all members of element 0, then of element 1, ...
+        uint32_t nb = nb0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (inB[e]) {
+            const uint32_t slot = nb + lanes_below(bm[e]);
+            if (slot < cap) {
+              BandEntry en;
+              en.idx = static_cast<int32_t>(i0 + e);
+              en.bits = __float_as_uint(v[e]);
+              bw.sbuf[slot] = en;
+            }
+          }
+          nb += static_cast<uint32_t>(__popcll(bm[e]));
+        }
       }
       st.nB = nb0 + tot;
     }
@@ -493,10 +513,15 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
   constexpr int U = 4;   // float4 loads per lane per batch, two batches in flight
   int64_t it = w0;
   if (vec && it + U * 256 <= w1) {
-    // two buffers taking turns, so that no registers are copied per batch
-    auto load = [&](float4 (&q)[U], int64_t at) {
+    // two buffers taking turns, so that no registers are copied per batch.
+    // The loads are unconditional (past the last batch every lane reads the
+    // range's first float4 again, one line per wave): a conditional load
+    // would make the compiler merge the old and new values with copies that
+    // wait for the load right away.
+    auto load = [&](float4 (&q)[U], int64_t at, bool real) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) q[u] = load_stream4(r + at + u * 256 + 4 * lane);
+      for (int u = 0; u < U; ++u)
+        q[u] = load_stream4(real ? r + at + u * 256 + 4 * lane : r + w0);
     };
     auto run = [&](const float4 (&q)[U], int64_t at) {
 #pragma unroll
@@ -507,18 +532,18 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       }
     };
     float4 qa[U], qb[U];
-    load(qa, it);
+    load(qa, it, true);
     while (true) {
       const int64_t ca = it;
       it += U * 256;
       const bool more_a = it + U * 256 <= w1;
-      if (more_a) load(qb, it);
+      load(qb, it, more_a);
       run(qa, ca);
       if (!more_a) break;
       const int64_t cb = it;
       it += U * 256;
       const bool more_b = it + U * 256 <= w1;
-      if (more_b) load(qa, it);
+      load(qa, it, more_b);
       run(qb, cb);
       if (!more_b) break;
     }
