@@ -27,14 +27,34 @@ constexpr int kMaxWords = static_cast<int>(kBandMaxChunk / 32);
 constexpr int kMaxEnt = 4 * kBandWaveCapMax;
 constexpr int kWordsPerThread = kMaxWords / BT;
 
-// LDS map from a block-local offset to the rank of its band member.
+// LDS map from a block-local offset to the rank of its band member, sized
+// for the row's chunk and list capacity (dynamic LDS: a block of a shorter
+// chunk needs less, so that more blocks share a CU).
 struct BandLds {
-  uint32_t bits[kMaxWords];
-  uint32_t pre[kMaxWords];   // members in the words before
-  float vals[kMaxEnt];       // value of the member of each rank
-  int seg[BW + 1];           // rank of each wave segment's first entry
-  uint32_t wtot[BW];
+  uint32_t* bits;   // [words] one bit per score of the chunk
+  uint32_t* pre;    // [words] members in the words before
+  float* vals;      // [4 cap] value of the member of each rank
+  uint32_t* wtot;   // [BW]
 };
+
+__host__ __device__ inline int band_lds_words(int64_t chunk) {
+  const int64_t c = chunk < kBandMaxChunk ? chunk : kBandMaxChunk;
+  return static_cast<int>((c + 31) / 32);
+}
+__host__ __device__ inline size_t band_lds_bytes(int64_t chunk, int cap) {
+  const int e = 4 * (cap < kBandWaveCapMax ? cap : kBandWaveCapMax);
+  return static_cast<size_t>(2 * band_lds_words(chunk) + e + BW) * 4;
+}
+__device__ inline BandLds band_lds(uint32_t* base, int64_t chunk, int cap) {
+  const int w = band_lds_words(chunk);
+  const int e = 4 * (cap < kBandWaveCapMax ? cap : kBandWaveCapMax);
+  BandLds L;
+  L.bits = base;
+  L.pre = base + w;
+  L.vals = reinterpret_cast<float*>(base + 2 * w);
+  L.wtot = base + 2 * w + e;
+  return L;
+}
 
 struct BlockRange {
   int64_t b0, b1;
@@ -82,31 +102,28 @@ __device__ __forceinline__ bool block_dense(const BandCtx& c, int64_t n, int pb)
 // null) is a float per slot of the block's region, loaded with the entries
 // and handed to value(entry, rank, aux of its slot).  Ends with a barrier.
 template <typename Value>
-__device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L,
+__device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, const BandLds& L,
                           bool from_segments, bool writeback, const float* aux, Value&& value) {
   constexpr int EPT = kMaxEnt / BT;   // entries per thread
   const int tid = threadIdx.x;
-  if (tid == 0) {
-    int acc = 0;
-    const BandBlock& bb = c.blk[blockIdx.x];
-#pragma unroll
-    for (int w = 0; w < BW; ++w) {
-      L.seg[w] = acc;
-      acc += bb.cnt[w];
-    }
-    L.seg[BW] = acc;
+  // every thread reads the four segment counts (one broadcast load)
+  int seg[BW + 1];
+  {
+    const int4 cnt = *reinterpret_cast<const int4*>(c.blk[blockIdx.x].cnt);
+    seg[0] = 0;
+    seg[1] = cnt.x;
+    seg[2] = cnt.x + cnt.y;
+    seg[3] = cnt.x + cnt.y + cnt.z;
+    seg[4] = cnt.x + cnt.y + cnt.z + cnt.w;
   }
-  const int nwords = static_cast<int>((len + 31) / 32);
-  for (int w = tid; w < nwords; w += BT) L.bits[w] = 0u;
-  __syncthreads();
-  const int total = L.seg[BW];
+  const int total = seg[BW];
   BandEntry* base = c.ent + static_cast<int64_t>(blockIdx.x) * BW * c.cap;
   const float* abase = aux ? aux + static_cast<int64_t>(blockIdx.x) * BW * c.cap : nullptr;
   BandEntry en[EPT];
   float av[EPT];
   int off[EPT];
-  // all loads first (slot 0 of the region stands in past the end), then
-  // the bits
+  // all loads first (slot 0 of the region stands in past the end); the
+  // bits are cleared while they are in flight
 #pragma unroll
   for (int q = 0; q < EPT; ++q) {
     const int e = tid + q * BT;
@@ -116,13 +133,16 @@ __device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, BandLds& L,
       if (from_segments) {
         int w = 0;
 #pragma unroll
-        for (int x = 1; x < BW; ++x) w += (e >= L.seg[x]) ? 1 : 0;
-        j = w * c.cap + (e - L.seg[w]);
+        for (int x = 1; x < BW; ++x) w += (e >= seg[x]) ? 1 : 0;
+        j = w * c.cap + (e - seg[w]);
       }
     }
     en[q] = base[j];
     av[q] = abase ? abase[j] : 0.0f;
   }
+  const int nwords = static_cast<int>((len + 31) / 32);
+  for (int w = tid; w < nwords; w += BT) L.bits[w] = 0u;
+  __syncthreads();
 #pragma unroll
   for (int q = 0; q < EPT; ++q) {
     const int e = tid + q * BT;
@@ -198,11 +218,12 @@ __device__ void write_dense(int64_t b0, int64_t b1, const BandLds& L, const uint
   };
   if ((reinterpret_cast<uintptr_t>(out + b0) & 15) == 0) {
     const int64_t n4 = len / 4;
-    for (int64_t q = tid; q < n4; q += BT) {
-      const uint32_t word = L.bits[q >> 3];
+    // float4 q takes nibble q & 7 of word q >> 3; WB float4 per thread at
+    // a time, their words (and bits of `ones`) read before any store
+    auto one4 = [&](int64_t q, uint32_t word, uint32_t oword) {
       const int sh = static_cast<int>(q & 7) * 4;
       const uint32_t nib = (word >> sh) & 15u;
-      const uint32_t onib = ones ? (ones[(b0 >> 5) + (q >> 3)] >> sh) & 15u : 0u;
+      const uint32_t onib = (oword >> sh) & 15u;
       float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) v[e] = ((onib >> e) & 1u) ? 1.0f : 0.0f;
@@ -213,7 +234,22 @@ __device__ void write_dense(int64_t b0, int64_t b1, const BandLds& L, const uint
           if ((nib >> e) & 1u) v[e] = L.vals[rk++];
       }
       store_stream4(out + b0 + 4 * q, make_float4(v[0], v[1], v[2], v[3]));
+    };
+    constexpr int WB = 8;
+    int64_t q0 = 0;
+    for (; q0 + WB * BT <= n4; q0 += WB * BT) {
+      uint32_t wd[WB], ow[WB];
+#pragma unroll
+      for (int k = 0; k < WB; ++k) {
+        const int64_t q = q0 + k * BT + tid;
+        wd[k] = L.bits[q >> 3];
+        ow[k] = ones ? ones[(b0 >> 5) + (q >> 3)] : 0u;
+      }
+#pragma unroll
+      for (int k = 0; k < WB; ++k) one4(q0 + k * BT + tid, wd[k], ow[k]);
     }
+    for (int64_t q = q0 + tid; q < n4; q += BT)
+      one4(q, L.bits[q >> 3], ones ? ones[(b0 >> 5) + (q >> 3)] : 0u);
     for (int64_t o = n4 * 4 + tid; o < len; o += BT) out[b0 + o] = value(o);
   } else {
     for (int64_t o = tid; o < len; o += BT) out[b0 + o] = value(o);
@@ -247,7 +283,8 @@ __global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__
                                                        const PartTotals* __restrict__ tot,
                                                        float* __restrict__ p,
                                                        double* __restrict__ b_out) {
-  __shared__ BandLds L;
+  extern __shared__ uint32_t band_lds_mem[];
+  const BandLds L = band_lds(band_lds_mem, c.chunk, c.cap);
   if (!rec->ok) return;
   const uint32_t* ones = tot->aR < INFINITY ? ones_all : nullptr;
   const double b = rec->b;
@@ -277,7 +314,8 @@ hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, doub
                             const BandCtx& band, const uint32_t* ones, const PartTotals* tot,
                             float* p, double* b_out, hipStream_t s) {
   { ProfScope ps_("band_emit", s);
-  hipLaunchKernelGGL(band_emit_kernel, dim3(band.nblocks), dim3(BT), 0, s, r, n, rec, 1.0 / t, band,
+  hipLaunchKernelGGL(band_emit_kernel, dim3(band.nblocks), dim3(BT),
+                     static_cast<unsigned>(band_lds_bytes(band.chunk, band.cap)), s, r, n, rec, 1.0 / t, band,
                      ones, tot, p, b_out); }
   return hipGetLastError();
 }
@@ -392,7 +430,8 @@ __global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restri
                                                            const double* __restrict__ partials,
                                                            int nparts, double inv_t,
                                                            float* __restrict__ grad) {
-  __shared__ BandLds L;
+  extern __shared__ uint32_t band_lds_mem[];
+  const BandLds L = band_lds(band_lds_mem, c.chunk, c.cap);
   __shared__ double red[2][BW];
   const int tid = threadIdx.x;
   double F = 0.0, G = 0.0;
@@ -458,7 +497,8 @@ hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const Band
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("band_vjp_emit", s);
-  hipLaunchKernelGGL(band_vjp_emit_kernel, dim3(band.nblocks), dim3(BT), 0, s, g, p, n, band,
+  hipLaunchKernelGGL(band_vjp_emit_kernel, dim3(band.nblocks), dim3(BT),
+                     static_cast<unsigned>(band_lds_bytes(band.chunk, band.cap)), s, g, p, n, band,
                      gstash, partials, parts, 1.0 / t, grad); }
   return hipGetLastError();
 }
