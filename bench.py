@@ -36,15 +36,15 @@ HBM_PEAK_GBS = 8000.0
 
 # Measured HBM traffic per launch (bytes) at n = 1e8: rocprofv3 FETCH_SIZE and
 # WRITE_SIZE passes over this script with --copy-probe, scaled by what the same
-# counters read for a 4e8-byte device copy (FETCH_SIZE x 1.9998, WRITE_SIZE
+# counters read for a 4e8-byte device copy (FETCH_SIZE x 1.99981, WRITE_SIZE
 # x 1.0).  Each entry holds the SHA-1 of the kernel's source file at the time of
 # measurement; once that file changes the figure no longer describes the
 # kernel and is reported as null.
 MEASURED_TRAFFIC = {
-    "vjp_emit": ("stream_kernels.hip", "16775165a5c2d0a08c9b16c1f8c7ac508fba6bb3", 844.8e6),
-    "vjp_reduce": ("stream_kernels.hip", "16775165a5c2d0a08c9b16c1f8c7ac508fba6bb3", 445.0e6),
-    "emit": ("stream_kernels.hip", "16775165a5c2d0a08c9b16c1f8c7ac508fba6bb3", 800.0e6),
-    "partition": ("bracket_kernels.hip", "a3bfadc37daf9e92847a35bee6f445c0f41463c5", 400.9e6),
+    "band_emit": ("band_kernels.hip", "16de33e92a58549052e914223eac99bf151cc2c3", 422.0e6),
+    "band_vjp_emit": ("band_kernels.hip", "16de33e92a58549052e914223eac99bf151cc2c3", 416.6e6),
+    "band_vjp_reduce": ("band_kernels.hip", "16de33e92a58549052e914223eac99bf151cc2c3", 60.5e6),
+    "partition": ("bracket_kernels.hip", "5e1b71812ce2df80bcbffa768415d2326a9a27a2", 413.0e6),
 }
 METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
 
@@ -68,11 +68,11 @@ def kernel_bytes(name: str, n: int, active: int, band: int) -> float | None:
     if name == "partition":
         return 4.0 * n + 8.0 * band          # read r, stage the band
     if name == "band_emit":
-        return 4.0 * n + 12.0 * band         # write p; read the band, write its p
+        return 4.0 * n + 16.0 * band         # write p; read the band, write it back with p
     if name == "band_vjp_reduce":
         return 8.0 * band + 8.0 * active     # read the band; g and its copy where f != 0
     if name == "band_vjp_emit":
-        return 4.0 * n + 8.0 * band + 4.0 * active   # write grad; read the band and g copies
+        return 4.0 * n + 12.0 * band         # write grad; read the band and its g copies
     if name == "emit":
         return 8.0 * n                       # read r, write p
     if name == "vjp_reduce":
