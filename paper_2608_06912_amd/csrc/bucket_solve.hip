@@ -543,7 +543,8 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
                                                           unsigned long long* __restrict__ acc_d,
                                                           PartTotals* __restrict__ tot,
                                                           double k, double t, int64_t n_total,
-                                                          SolveRec* __restrict__ out) {
+                                                          SolveRec* __restrict__ out,
+                                                          AttemptRec* __restrict__ host) {
   __shared__ uint32_t buf[sort_buf_words<ST, SI>()];
   __shared__ SortSmem<ST> ssm;
   __shared__ ScanSmem<SW> csm;
@@ -601,6 +602,14 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     }
   }
   __syncthreads();
+  // thread 0: the record, for the emit, and with the totals for the host
+  auto publish = [&](const SolveRec& rec) {
+    *out = rec;
+    if (host) {
+      host->tot = tot_s;
+      host->rec = rec;
+    }
+  };
   const Tails x = load_tails(&tot_s);
   const int64_t m = tot_s.nM;
   if (m > m_cap || tot_s.any_block_overflow != 0) {
@@ -612,7 +621,7 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
       rec.lap_aR = NAN;
       rec.ok = 0;
       rec.side = 3;
-      *out = rec;
+      publish(rec);
     }
     return;
   }
@@ -624,7 +633,7 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
       rec.side = 0;
       certify(x, 0.0, static_cast<double>(n_total), k, t, x.pre, x.suf, rec);
       rec.b = root_above(x, x.suf, k, t);
-      *out = rec;
+      publish(rec);
     }
     return;
   }
@@ -801,7 +810,7 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
   }
   if (tid == 0) {
     rec.b = b;
-    *out = rec;
+    publish(rec);
   }
 }
 
@@ -814,7 +823,8 @@ size_t bucket_offs_words(int nblocks) {
 }
 
 hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc acc, PartTotals* tot,
-                               double k, double t, int64_t n_total, SolveRec* out, hipStream_t s) {
+                               double k, double t, int64_t n_total, SolveRec* out,
+                               AttemptRec* host, hipStream_t s) {
   if (ps.nblocks < 1 || ps.nblocks > kPartMaxBlocks) return hipErrorInvalidValue;
   const int groups = bucket_groups(ps.nblocks);   // <= 32: one lane each in the solve
   { ProfScope ps_("bucket_count", s);
@@ -826,7 +836,7 @@ hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc ac
   { ProfScope ps_("bucket_solve", s);
   hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, acc.keys, acc.offs, acc.parts,
                      groups, m_cap, ps.sel, ps.use_sel, ps.aL, ps.aR, acc.n, acc.u, acc.d, tot, k,
-                     t, n_total, out); }
+                     t, n_total, out, host); }
   return hipGetLastError();
 }
 

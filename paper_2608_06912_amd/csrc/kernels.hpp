@@ -270,8 +270,17 @@ struct PartSource {
   int use_sel;
   float aL, aR;
 };
+// The totals of a partition and the record of its solve, next to each other
+// so that one copy (or one write to host memory) brings both back.
+struct AttemptRec {
+  PartTotals tot;
+  SolveRec rec;
+};
+// host: null, or a device-visible pointer to host memory that also receives
+// the totals and the record (no copy needed on the stream).
 hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc acc, PartTotals* tot,
-                               double k, double t, int64_t n_total, SolveRec* out, hipStream_t s);
+                               double k, double t, int64_t n_total, SolveRec* out,
+                               AttemptRec* host, hipStream_t s);
 
 // Copy sorted M indices to the caller's [m_capacity] row, -1 padded.
 hipError_t launch_write_m_idx(const int32_t* sorted_idx, int64_t m_len, int64_t m_capacity,

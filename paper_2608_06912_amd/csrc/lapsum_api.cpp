@@ -168,13 +168,6 @@ size_t forward_ws(int64_t n, bool with_perm) {
 }
 
 // --------------------------------------------------------------- bracket --
-// The totals of a partition and the record of its solve, next to each other
-// so that one copy brings both back to the host.
-struct AttemptRec {
-  PartTotals tot;
-  SolveRec rec;
-};
-
 struct BracketWs {
   uint32_t* ykeys;
   uint32_t* soffs;
@@ -305,22 +298,30 @@ struct HostStage {
 };
 struct ThreadStage {
   HostStage* h = nullptr;
+  HostStage* dev = nullptr;   // the same memory as the device addresses it
   hipEvent_t ev = nullptr;
 };
 thread_local ThreadStage t_stage;
 
-int host_stage(HostStage** h, hipEvent_t* ev) {
+// Mapped, coherent pinned memory: the bucketed solve writes its record there
+// directly, so that no copy has to run on the stream before the emit.
+int host_stage(HostStage** h, HostStage** dev, hipEvent_t* ev) {
   if (!t_stage.h) {
     void* ptr = nullptr;
-    if (hipHostMalloc(&ptr, sizeof(HostStage), hipHostMallocPortable) != hipSuccess)
+    if (hipHostMalloc(&ptr, sizeof(HostStage),
+                      hipHostMallocPortable | hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
       return LAPSUM_ERR_HIP;
+    void* dptr = nullptr;
+    if (hipHostGetDevicePointer(&dptr, ptr, 0) != hipSuccess) return LAPSUM_ERR_HIP;
     t_stage.h = static_cast<HostStage*>(ptr);
+    t_stage.dev = static_cast<HostStage*>(dptr);
   }
   if (!t_stage.ev) {
     if (hipEventCreateWithFlags(&t_stage.ev, hipEventDisableTiming) != hipSuccess)
       return LAPSUM_ERR_HIP;
   }
   *h = t_stage.h;
+  *dev = t_stage.dev;
   *ev = t_stage.ev;
   return LAPSUM_OK;
 }
@@ -353,8 +354,9 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
   bool wrote_midx = false;
   const BandCtx band = band_ctx_view(band_row ? band_row : w.band, n);
   HostStage* hs = nullptr;
+  HostStage* hs_dev = nullptr;
   hipEvent_t ev = nullptr;
-  int st = host_stage(&hs, &ev);
+  int st = host_stage(&hs, &hs_dev, &ev);
   if (st != LAPSUM_OK) return st;
 
   if (!(flags & LAPSUM_FLAG_FULL_SORT)) {
@@ -417,9 +419,13 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
       bool have_rec = false;
       if (!want_idx) {
         // buckets straight from the staging, with no wait for the totals
+        // the solve writes its record to host memory as well; the emit (of
+        // a certified bracket only) runs while the host waits for it
         const PartSource ps{w.blk, w.nblocks, w.stage_v, w.sel, use_sel, aL, aR};
-        LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec, s));
-        st = emit_and_read();
+        LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec, &hs_dev->att, s));
+        if (hipEventRecord(ev, s) != hipSuccess) return LAPSUM_ERR_HIP;
+        LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, w.tot, p_row, b_row, s));
+        st = wait_back(ev);
         if (st != LAPSUM_OK) return st;
         tot = hs->att.tot;
         have_rec = true;
