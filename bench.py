@@ -158,9 +158,12 @@ def main():
     band = L.new_band(1, n, dev)
     grad = torch.empty_like(r)
 
+    p_buf = torch.empty_like(r)
+    b_buf = torch.empty(1, dtype=torch.float64, device=dev)
+
     def forward():
         return L.lapsum_forward_bracketed(r, w.k, w.alpha, noise, z=w.z, m_capacity=mcap,
-                                          band=band, workspace=ws_f)[:3]
+                                          band=band, workspace=ws_f, out=p_buf, b_out=b_buf)[:3]
 
     def backward(p):
         L.lapsum_backward_band(g, p, band, w.alpha, workspace=ws_b, out=grad)

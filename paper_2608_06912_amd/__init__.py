@@ -51,8 +51,13 @@ class BracketInfo(ctypes.Structure):
         ("m_overflow", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]
 
+    _names = None
+
     def as_dict(self) -> dict:
-        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+        names = BracketInfo._names
+        if names is None:
+            names = BracketInfo._names = tuple(nm for nm, _ in self._fields_ if nm != "reserved")
+        return {name: getattr(self, name) for name in names}
 
 
 def load():
@@ -106,9 +111,37 @@ def _check(status: int, where: str):
         raise LapsumError(status, where)
 
 
+_torch_mod = None
+
+
 def _torch():
-    import torch
-    return torch
+    global _torch_mod
+    if _torch_mod is None:
+        import torch
+        _torch_mod = torch
+    return _torch_mod
+
+
+class _on_device:
+    """Make `device` current for a call (a no-op when it already is)."""
+
+    __slots__ = ("dev", "prev")
+
+    def __init__(self, device):
+        self.dev = device.index if device.index is not None else _torch().cuda.current_device()
+        self.prev = None
+
+    def __enter__(self):
+        cur = _torch().cuda.current_device()
+        if cur != self.dev:
+            self.prev = cur
+            _torch().cuda.set_device(self.dev)
+        return self
+
+    def __exit__(self, *exc):
+        if self.prev is not None:
+            _torch().cuda.set_device(self.prev)
+        return False
 
 
 def _rows(x, name):
@@ -162,7 +195,7 @@ def lapsum_forward(scores, k: float, alpha: float, *, perm: bool = False, worksp
     b = torch.empty(batch, dtype=torch.float64, device=dev)
     pm = torch.empty(scores.shape, dtype=torch.int32, device=dev) if perm else None
     ws, nbytes = _workspace(lib.lapsum_forward_workspace_size(batch, n, int(perm)), dev, workspace)
-    with torch.cuda.device(dev):
+    with _on_device(dev):
         _check(lib.lapsum_forward(_ptr(scores), batch, n, float(k), float(alpha), _ptr(p), _ptr(b),
                                   _ptr(pm), _ptr(ws), nbytes, _stream(dev)), "lapsum_forward")
     return (p, b, pm) if perm else (p, b)
@@ -183,7 +216,7 @@ def lapsum_backward(grad_p, p, b, alpha: float, *, workspace=None, out=None):
     dev = p.device
     grad = out if out is not None else torch.empty_like(p)
     ws, nbytes = _workspace(lib.lapsum_backward_workspace_size(batch, n), dev, workspace)
-    with torch.cuda.device(dev):
+    with _on_device(dev):
         _check(lib.lapsum_backward(_ptr(grad_p), _ptr(p), _ptr(b), batch, n, float(alpha),
                                    _ptr(grad), _ptr(ws), nbytes, _stream(dev)), "lapsum_backward")
     return grad
@@ -222,11 +255,13 @@ def _band_arg(band, batch, n):
 
 def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float = 5.16,
                              m_capacity: int | None = None, flags: int = 0,
-                             m_idx: bool = False, band=None, workspace=None):
+                             m_idx: bool = False, band=None, workspace=None, out=None,
+                             b_out=None):
     """Bracketed forward.  noise: float32 CUDA tensor [K] of Laplace(0, |alpha|)
     draws.  band: None, or a buffer from new_band() that receives the band for
-    lapsum_backward_band.  Returns (p, b, infos, m_idx or None) with infos a
-    list of dicts."""
+    lapsum_backward_band.  out / b_out: optional buffers for p (float32, the
+    shape of scores) and b (float64, [batch]).  Returns (p, b, infos, m_idx or
+    None) with infos a list of dicts."""
     torch = _torch()
     lib = load()
     batch, n = _rows(scores, "scores")
@@ -237,14 +272,26 @@ def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float 
     if m_capacity is None:
         m_capacity = default_m_capacity(n, K)
     dev = scores.device
-    p = torch.empty_like(scores)
-    b = torch.empty(batch, dtype=torch.float64, device=dev)
+    if out is not None:
+        if (out.shape != scores.shape or out.dtype != torch.float32 or not out.is_contiguous()
+                or out.device != dev):
+            raise ValueError("out must be a contiguous float32 tensor shaped like scores")
+        p = out
+    else:
+        p = torch.empty_like(scores)
+    if b_out is not None:
+        if (b_out.numel() != batch or b_out.dtype != torch.float64 or not b_out.is_contiguous()
+                or b_out.device != dev):
+            raise ValueError("b_out must be a contiguous float64 tensor of [batch] elements")
+        b = b_out
+    else:
+        b = torch.empty(batch, dtype=torch.float64, device=dev)
     mi = torch.empty((batch, m_capacity), dtype=torch.int32, device=dev) if m_idx else None
     infos = (BracketInfo * batch)()
     ws, nbytes = _workspace(lib.lapsum_forward_bracketed_workspace_size(batch, n, K, m_capacity,
                                                                         int(m_idx)), dev, workspace)
     bp, bbytes = _band_arg(band, batch, n)
-    with torch.cuda.device(dev):
+    with _on_device(dev):
         _check(lib.lapsum_forward_bracketed(_ptr(scores), batch, n, float(k), float(alpha), K,
                                             float(z), _ptr(noise), int(m_capacity), int(flags),
                                             _ptr(p), _ptr(b), ctypes.cast(infos, ctypes.c_void_p),
@@ -271,7 +318,7 @@ def lapsum_backward_band(grad_p, p, band, alpha: float, *, workspace=None, out=N
     grad = out if out is not None else torch.empty_like(p)
     ws, nbytes = _workspace(lib.lapsum_backward_band_workspace_size(batch, n), dev, workspace)
     bp, bbytes = _band_arg(band, batch, n)
-    with torch.cuda.device(dev):
+    with _on_device(dev):
         _check(lib.lapsum_backward_band(_ptr(grad_p), _ptr(p), bp, bbytes, batch, n, float(alpha),
                                         _ptr(grad), _ptr(ws), nbytes, _stream(dev)),
                "lapsum_backward_band")

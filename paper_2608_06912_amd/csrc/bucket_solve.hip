@@ -544,7 +544,9 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
                                                           PartTotals* __restrict__ tot,
                                                           double k, double t, int64_t n_total,
                                                           SolveRec* __restrict__ out,
-                                                          AttemptRec* __restrict__ host) {
+                                                          AttemptRec* __restrict__ host,
+                                                          uint32_t* __restrict__ host_seq,
+                                                          uint32_t seq) {
   __shared__ uint32_t buf[sort_buf_words<ST, SI>()];
   __shared__ SortSmem<ST> ssm;
   __shared__ ScanSmem<SW> csm;
@@ -608,6 +610,8 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     if (host) {
       host->tot = tot_s;
       host->rec = rec;
+      __threadfence_system();   // the record lands before the sequence number
+      *reinterpret_cast<volatile uint32_t*>(host_seq) = seq;
     }
   };
   const Tails x = load_tails(&tot_s);
@@ -824,7 +828,7 @@ size_t bucket_offs_words(int nblocks) {
 
 hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc acc, PartTotals* tot,
                                double k, double t, int64_t n_total, SolveRec* out,
-                               AttemptRec* host, hipStream_t s) {
+                               AttemptRec* host, uint32_t* host_seq, uint32_t seq, hipStream_t s) {
   if (ps.nblocks < 1 || ps.nblocks > kPartMaxBlocks) return hipErrorInvalidValue;
   const int groups = bucket_groups(ps.nblocks);   // <= 32: one lane each in the solve
   { ProfScope ps_("bucket_count", s);
@@ -836,7 +840,7 @@ hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc ac
   { ProfScope ps_("bucket_solve", s);
   hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, acc.keys, acc.offs, acc.parts,
                      groups, m_cap, ps.sel, ps.use_sel, ps.aL, ps.aR, acc.n, acc.u, acc.d, tot, k,
-                     t, n_total, out, host); }
+                     t, n_total, out, host, host_seq, seq); }
   return hipGetLastError();
 }
 

@@ -277,10 +277,12 @@ struct AttemptRec {
   SolveRec rec;
 };
 // host: null, or a device-visible pointer to host memory that also receives
-// the totals and the record (no copy needed on the stream).
+// the totals and the record, after which host_seq (same memory) is set to
+// seq (a system-scope fence between): the host polls it, no event or copy
+// sits on the stream.
 hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc acc, PartTotals* tot,
                                double k, double t, int64_t n_total, SolveRec* out,
-                               AttemptRec* host, hipStream_t s);
+                               AttemptRec* host, uint32_t* host_seq, uint32_t seq, hipStream_t s);
 
 // Copy sorted M indices to the caller's [m_capacity] row, -1 padded.
 hipError_t launch_write_m_idx(const int32_t* sorted_idx, int64_t m_len, int64_t m_capacity,

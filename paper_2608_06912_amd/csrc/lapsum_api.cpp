@@ -4,6 +4,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <atomic>
+#include <chrono>
 #include <map>
 #include <mutex>
 #include <string>
@@ -295,11 +297,13 @@ void widen(float* aL, float* aR, int side) {
 // the host a copy has landed while later work proceeds on the stream.
 struct HostStage {
   AttemptRec att;
+  uint32_t seq;   // set by the bucketed solve after att
 };
 struct ThreadStage {
   HostStage* h = nullptr;
   HostStage* dev = nullptr;   // the same memory as the device addresses it
   hipEvent_t ev = nullptr;
+  uint32_t next_seq = 1;
 };
 thread_local ThreadStage t_stage;
 
@@ -315,6 +319,7 @@ int host_stage(HostStage** h, HostStage** dev, hipEvent_t* ev) {
     if (hipHostGetDevicePointer(&dptr, ptr, 0) != hipSuccess) return LAPSUM_ERR_HIP;
     t_stage.h = static_cast<HostStage*>(ptr);
     t_stage.dev = static_cast<HostStage*>(dptr);
+    t_stage.h->seq = 0u;
   }
   if (!t_stage.ev) {
     if (hipEventCreateWithFlags(&t_stage.ev, hipEventDisableTiming) != hipSuccess)
@@ -337,6 +342,39 @@ int copy_back(T* host, const T* dev, hipEvent_t ev, hipStream_t s) {
 
 int wait_back(hipEvent_t ev) {
   return hipEventSynchronize(ev) == hipSuccess ? LAPSUM_OK : LAPSUM_ERR_HIP;
+}
+
+// Poll the sequence number a kernel sets in mapped host memory after its
+// record.  The stream is queried only once the number has been missing for a
+// few milliseconds: a query on a stream whose last command is a kernel makes
+// the runtime enqueue a marker behind that kernel, and the marker's cache
+// writeback delays the next kernel by several microseconds.  If the stream
+// has finished (or failed) without the number appearing, the call fails
+// instead of waiting on.
+int wait_seq(const HostStage* h, uint32_t want, hipStream_t s) {
+  const volatile uint32_t* seq = &h->seq;
+  using clock = std::chrono::steady_clock;
+  const auto start = clock::now();
+  bool patient = true;
+  for (uint64_t i = 1;; ++i) {
+    if (*seq == want) {
+      std::atomic_thread_fence(std::memory_order_acquire);
+      return LAPSUM_OK;
+    }
+    if ((i & 255u) != 0u) continue;
+    if (patient) {
+      if (clock::now() - start < std::chrono::milliseconds(4)) continue;
+      patient = false;
+    }
+    if ((i & 1023u) != 0u) continue;
+    const hipError_t q = hipStreamQuery(s);
+    if (q == hipErrorNotReady) continue;
+    if (q == hipSuccess && *seq == want) {
+      std::atomic_thread_fence(std::memory_order_acquire);
+      return LAPSUM_OK;
+    }
+    return LAPSUM_ERR_HIP;
+  }
 }
 
 int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, double z,
@@ -422,10 +460,11 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
         // the solve writes its record to host memory as well; the emit (of
         // a certified bracket only) runs while the host waits for it
         const PartSource ps{w.blk, w.nblocks, w.stage_v, w.sel, use_sel, aL, aR};
-        LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec, &hs_dev->att, s));
-        if (hipEventRecord(ev, s) != hipSuccess) return LAPSUM_ERR_HIP;
+        const uint32_t seq = t_stage.next_seq++;
+        LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec, &hs_dev->att,
+                                       &hs_dev->seq, seq, s));
         LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, w.tot, p_row, b_row, s));
-        st = wait_back(ev);
+        st = wait_seq(hs, seq, s);
         if (st != LAPSUM_OK) return st;
         tot = hs->att.tot;
         have_rec = true;
