@@ -65,14 +65,17 @@ def parse():
 def kernel_bytes(name: str, n: int, active: int, band: int) -> float | None:
     """Algorithmic HBM bytes one launch of a streaming kernel must move
     (band: scores in the bracket's band; active: scores with 0 < p < 1)."""
+    tiles = 8.0 * ((n + 1023) // 1024)     # one 8-byte record per writer tile
     if name == "partition":
-        return 4.0 * n + 8.0 * band          # read r, stage the band
+        # read r; stage the band; one bit per score above it; the tile records
+        return 4.0 * n + 8.0 * band + n / 8.0 + tiles
     if name == "band_emit":
-        return 4.0 * n + 16.0 * band         # write p; read the band, write it back with p
+        # write p; read the band, the bits above it and the tile records
+        return 4.0 * n + 8.0 * band + n / 8.0 + tiles
     if name == "band_vjp_reduce":
         return 8.0 * band + 8.0 * active     # read the band; g and its copy where f != 0
     if name == "band_vjp_emit":
-        return 4.0 * n + 12.0 * band         # write grad; read the band and its g copies
+        return 4.0 * n + 12.0 * band + tiles  # write grad; read the band, its g copies, the records
     if name == "emit":
         return 8.0 * n                       # read r, write p
     if name == "vjp_reduce":

@@ -1,18 +1,29 @@
 // Passes over the band a bracket's partition staged (the scores whose p is
 // strictly between 0 and 1 can only lie there; see BandEntry):
-//   band_emit      p for one partition block's range: band members from
-//                  their staged score and b, every other score 0 or 1 from
-//                  the side it lies on (one bit per score when a_R is
-//                  finite).  Writes p densely without reading r: 4 B/score
-//                  plus 8 B per band member.  The entries then hold p, the
-//                  forward's context for the backward.
-//   band_vjp       Eq. (5) from the context: sums of f = min(p, 1 - p) and
-//                  f g over the band (g read only where f != 0), then
-//                  grad_r written densely (zero outside the band), each emit
-//                  block summing the partials in a fixed order: 4 B/score
-//                  plus the band.
-// A block whose lists overflowed (or whose range is too long for the LDS
-// map) takes the dense form of each pass over its own range.
+//   band_emit        p for every score: band members from their staged score
+//                    and b, every other score 0 or 1 from the side it lies
+//                    on (one bit per score when a_R is finite).  Writes p
+//                    without reading r: 4 B/score plus 8 B per band member.
+//   band_vjp_reduce  Eq. (5)'s sums of f = min(p, 1 - p) and f g over the
+//                    band, p recomputed from the staged score and the b the
+//                    emit saved, g read only where f != 0 (and stashed at the
+//                    member's list slot).
+//   band_vjp_write   grad_r for every score, zero outside the band, each
+//                    writer block summing the reduce partials in a fixed
+//                    order: 4 B/score plus 12 B per band member.
+// Both dense outputs are written by one persistent scheme (band_write): one
+// workgroup per CU, four waves that only store and one wave that only loads.
+// The row is cut into tiles of kBandTile scores and workgroup w writes tiles
+// w, w + G, w + 2G, ... (G workgroups), kRound of them per round: at any time
+// the device writes one contiguous window of G tiles, one tile per CU, which
+// is the write pattern the memory system takes at its full rate.  The
+// loading wave prefetches the tile records, member lists and ones bits of
+// the next round and lays the round's member values into an LDS tile; the
+// storing waves read LDS and store.  No wave both loads from and stores to
+// memory in the stream, so no wait for a load is also a wait for earlier
+// stores (one counter tracks both on this architecture).
+// A tile whose block's lists are incomplete takes the dense form: its
+// storing threads read r (forward) or p and g (backward) themselves.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -23,54 +34,17 @@ namespace {
 constexpr int BT = 256;
 constexpr int BW = BT / kWave;   // one list segment per wave of the partition
 static_assert(BW == 4, "the partition stages one list per wave of four");
-constexpr int kMaxWords = static_cast<int>(kBandMaxChunk / 32);
-constexpr int kMaxEnt = 4 * kBandWaveCapMax;
-constexpr int kWordsPerThread = kMaxWords / BT;
 
-// LDS map from a block-local offset to the rank of its band member, sized
-// for the row's chunk and list capacity (dynamic LDS: a block of a shorter
-// chunk needs less, so that more blocks share a CU).
-struct BandLds {
-  uint32_t* bits;   // [words] one bit per score of the chunk
-  uint32_t* pre;    // [words] members in the words before
-  float* vals;      // [4 cap] value of the member of each rank
-  uint32_t* wtot;   // [BW]
-};
-
-__host__ __device__ inline int band_lds_words(int64_t chunk) {
-  const int64_t c = chunk < kBandMaxChunk ? chunk : kBandMaxChunk;
-  return static_cast<int>((c + 31) / 32);
-}
-__host__ __device__ inline size_t band_lds_bytes(int64_t chunk, int cap) {
-  const int e = 4 * (cap < kBandWaveCapMax ? cap : kBandWaveCapMax);
-  return static_cast<size_t>(2 * band_lds_words(chunk) + e + BW) * 4;
-}
-__device__ inline BandLds band_lds(uint32_t* base, int64_t chunk, int cap) {
-  const int w = band_lds_words(chunk);
-  const int e = 4 * (cap < kBandWaveCapMax ? cap : kBandWaveCapMax);
-  BandLds L;
-  L.bits = base;
-  L.pre = base + w;
-  L.vals = reinterpret_cast<float*>(base + 2 * w);
-  L.wtot = base + 2 * w + e;
-  return L;
-}
+__device__ __forceinline__ int64_t clamp_end(int64_t a, int64_t n) { return a < n ? a : n; }
 
 struct BlockRange {
   int64_t b0, b1;
 };
 
-__device__ __forceinline__ BlockRange block_range(int64_t n, int64_t chunk) {
-  BlockRange br;
-  br.b0 = static_cast<int64_t>(blockIdx.x) * chunk;
-  br.b1 = br.b0 + chunk < n ? br.b0 + chunk : n;
-  return br;
-}
-
 __device__ __forceinline__ BlockRange range_of(int64_t n, int64_t chunk, int pb) {
   BlockRange br;
   br.b0 = static_cast<int64_t>(pb) * chunk;
-  br.b1 = br.b0 + chunk < n ? br.b0 + chunk : n;
+  br.b1 = clamp_end(br.b0 + chunk, n);
   return br;
 }
 
@@ -86,207 +60,307 @@ __device__ __forceinline__ bool lists_usable(const BandCtx& c, int pb) {
 // Backward: the saved header must describe this row (a band saved for
 // another length, or a forward that fell back to the full sort, makes every
 // pass dense).
-__device__ __forceinline__ bool block_dense(const BandCtx& c, int64_t n, int pb) {
-  const CtxHeader h = *c.hdr;
-  if (h.mode != 0 || h.n != n || h.nblocks != c.nblocks || h.chunk != c.chunk || h.cap != c.cap)
-    return true;
-  return !lists_usable(c, pb);
+__device__ __forceinline__ bool header_dense(const CtxHeader& h, const BandCtx& c, int64_t n) {
+  return h.mode != 0 || h.n != n || h.nblocks != c.nblocks || h.chunk != c.chunk || h.cap != c.cap;
 }
 
-// Build the map of this block's band.  Entries come either as the
-// partition left them (four wave segments, each in the order its members
-// were met; `from_segments`) or as the emit leaves them (one list in index
-// order at the start of the block's region).  value(entry, rank) gives the
-// float stored for each member; with `writeback` the members are written
-// back as one list in index order, each carrying its value.  `aux` (or
-// null) is a float per slot of the block's region, loaded with the entries
-// and handed to value(entry, rank, aux of its slot).  Ends with a barrier.
-template <typename Value>
-__device__ void build_map(const BandCtx& c, int64_t b0, int64_t len, const BandLds& L,
-                          bool from_segments, bool writeback, const float* aux, Value&& value) {
-  constexpr int EPT = kMaxEnt / BT;   // entries per thread
+// ------------------------------------------------------------ tile writer --
+constexpr int kRound = 8;          // tiles per round of a writer workgroup
+constexpr int kSlots = 3;          // member slots per loading lane and round
+constexpr int kStoreWaves = 4;
+constexpr int WT = (kStoreWaves + 1) * kWave;   // 320 threads
+constexpr int kTileF4 = static_cast<int>(kBandTile / 4);
+constexpr int kTileWords = static_cast<int>(kBandTile / 32);
+constexpr int kLanesPerTile = kWave / kRound;              // loading lanes per tile's ones words
+constexpr int kWriterBlocks = 256;                         // one per CU
+static_assert(kTileF4 == kStoreWaves * kWave, "one float4 of a tile per storing thread");
+static_assert(kTileWords == 4 * kLanesPerTile, "a tile's ones words are one uint4 per lane");
+
+struct WriterLds {
+  float4 tile[2][kRound][kTileF4];      // member values of a round (0 elsewhere)
+  uint32_t ow[2][kRound][kTileWords];   // ones bits of a round's tiles
+  uint32_t dense[2];                    // bit i: tile i of the round is dense
+  double red[2][kStoreWaves];
+};
+
+// Forward: p.
+struct EmitPass {
+  static constexpr bool kOnes = true;
+  const float* r;
+  const uint32_t* ones;   // null when a_R is infinite
+  double b, inv_t;
+  __device__ float member(const BandEntry& e, float) const {
+    return laplace_p(__uint_as_float(e.bits), b, inv_t);
+  }
+  __device__ float dense(float x, float) const { return laplace_p(x, b, inv_t); }
+  __device__ const float* in0() const { return r; }
+  __device__ const float* in1() const { return nullptr; }
+  __device__ const float* stash() const { return nullptr; }
+};
+
+// Backward: grad_r = (f/t)(g - <g,q>), f = min(p, 1 - p).
+struct VjpPass {
+  static constexpr bool kOnes = false;
+  const float* p;
+  const float* g;
+  const float* gstash;
+  double b, inv_t;
+  float coef, scale;
+  __device__ float member(const BandEntry& e, float gs) const {
+    const float pv = laplace_p(__uint_as_float(e.bits), b, inv_t);
+    const float f = fminf(pv, 1.0f - pv);
+    return (f != 0.0f) ? f * scale * (gs - coef) : 0.0f;
+  }
+  __device__ float dense(float pv, float gv) const {
+    const float f = fminf(pv, 1.0f - pv);
+    return (f != 0.0f) ? f * scale * (gv - coef) : 0.0f;
+  }
+  __device__ const float* in0() const { return p; }
+  __device__ const float* in1() const { return g; }
+  __device__ const float* stash() const { return gstash; }
+};
+
+__device__ __forceinline__ float4 load4_at(const float* x, int64_t o, int64_t n, bool vec) {
+  if (vec && o + 3 < n) return load_stream4(x + o);
+  float4 v;
+  v.x = o < n ? x[o] : 0.0f;
+  v.y = o + 1 < n ? x[o + 1] : 0.0f;
+  v.z = o + 2 < n ? x[o + 2] : 0.0f;
+  v.w = o + 3 < n ? x[o + 3] : 0.0f;
+  return v;
+}
+
+// Storing waves: one float4 of each tile per thread and round.
+template <class Pass>
+__device__ void writer_store(const Pass& P, WriterLds& S, float* __restrict__ out, int64_t n,
+                             int64_t nt, int64_t nr, bool vec_out, bool vec_in) {
   const int tid = threadIdx.x;
-  // every thread reads the four segment counts (one broadcast load)
-  int seg[BW + 1];
-  {
-    const int4 cnt = *reinterpret_cast<const int4*>(c.blk[blockIdx.x].cnt);
-    seg[0] = 0;
-    seg[1] = cnt.x;
-    seg[2] = cnt.x + cnt.y;
-    seg[3] = cnt.x + cnt.y + cnt.z;
-    seg[4] = cnt.x + cnt.y + cnt.z + cnt.w;
-  }
-  const int total = seg[BW];
-  BandEntry* base = c.ent + static_cast<int64_t>(blockIdx.x) * BW * c.cap;
-  const float* abase = aux ? aux + static_cast<int64_t>(blockIdx.x) * BW * c.cap : nullptr;
-  BandEntry en[EPT];
-  float av[EPT];
-  int off[EPT];
-  // all loads first (slot 0 of the region stands in past the end); the
-  // bits are cleared while they are in flight
+  const int64_t G = gridDim.x;
+  for (int64_t k = 0; k < nr; ++k) {
+    __syncthreads();
+    const int buf = static_cast<int>(k & 1);
+    const uint32_t dm = S.dense[buf];
+    float4 v[kRound];
+    uint32_t w[kRound];
 #pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    const int e = tid + q * BT;
-    int j = 0;
-    if (e < total) {
-      j = e;
-      if (from_segments) {
-        int w = 0;
+    for (int i = 0; i < kRound; ++i) {
+      v[i] = S.tile[buf][i][tid];
+      if constexpr (Pass::kOnes) w[i] = S.ow[buf][i][tid >> 3];
+      else w[i] = 0u;
+    }
+    if (dm) {
+      // dense tiles (rare): every load of the round first, then the values
+      float4 a[kRound], c[kRound];
 #pragma unroll
-        for (int x = 1; x < BW; ++x) w += (e >= seg[x]) ? 1 : 0;
-        j = w * c.cap + (e - seg[w]);
+      for (int i = 0; i < kRound; ++i) {
+        if ((dm >> i) & 1u) {
+          const int64_t o = ((blockIdx.x + (k * kRound + i) * G) * kTileF4 + tid) * 4;
+          a[i] = load4_at(P.in0(), o, n, vec_in);
+          if (P.in1()) c[i] = load4_at(P.in1(), o, n, vec_in);
+          else c[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kRound; ++i) {
+        if ((dm >> i) & 1u) {
+          v[i] = make_float4(P.dense(a[i].x, c[i].x), P.dense(a[i].y, c[i].y),
+                             P.dense(a[i].z, c[i].z), P.dense(a[i].w, c[i].w));
+          w[i] = 0u;
+        }
       }
     }
-    en[q] = base[j];
-    av[q] = abase ? abase[j] : 0.0f;
-  }
-  const int nwords = static_cast<int>((len + 31) / 32);
-  for (int w = tid; w < nwords; w += BT) L.bits[w] = 0u;
-  __syncthreads();
 #pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    const int e = tid + q * BT;
-    off[q] = -1;
-    if (e < total) {
-      const int64_t o = static_cast<int64_t>(en[q].idx) - b0;
-      if (o >= 0 && o < len) {
-        off[q] = static_cast<int>(o);
-        atomicOr(&L.bits[o >> 5], 1u << (o & 31));
+    for (int i = 0; i < kRound; ++i) {
+      const int64_t t = k * kRound + i;
+      if (t < nt) {
+        const uint32_t nib = (w[i] >> ((tid & 7) * 4)) & 15u;
+        float4 x;
+        x.x = (nib & 1u) ? 1.0f : v[i].x;
+        x.y = (nib & 2u) ? 1.0f : v[i].y;
+        x.z = (nib & 4u) ? 1.0f : v[i].z;
+        x.w = (nib & 8u) ? 1.0f : v[i].w;
+        const int64_t o = ((blockIdx.x + t * G) * kTileF4 + tid) * 4;
+        if (vec_out && o + 3 < n) {
+          store_stream4(out + o, x);
+        } else {
+          if (o < n) out[o] = x.x;
+          if (o + 1 < n) out[o + 1] = x.y;
+          if (o + 2 < n) out[o + 2] = x.z;
+          if (o + 3 < n) out[o + 3] = x.w;
+        }
       }
     }
-  }
-  __syncthreads();
-  // exclusive prefix of the members per word: each thread owns a run of words
-  const int w0 = tid * kWordsPerThread;
-  uint32_t loc = 0;
 #pragma unroll
-  for (int q = 0; q < kWordsPerThread; ++q)
-    loc += (w0 + q < nwords) ? static_cast<uint32_t>(__popc(L.bits[w0 + q])) : 0u;
-  uint32_t incl = loc;
+    for (int i = 0; i < kRound; ++i) S.tile[buf][i][tid] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
+}
+
+// The loading wave.  Round k's tile records are loaded two rounds ahead and
+// its lists and ones bits one round ahead; member slot s of a round (lane +
+// 64 q) takes the s-th member of the round's tiles taken in order.  A round's
+// bookkeeping stays in registers, lane i < kRound holding tile i (record and
+// count), and per-slot choices are made from scalars read out of those
+// lanes: no private array, so nothing of the loop goes through scratch
+// memory (whose loads would join the wait for the prefetched data).
+template <class Pass>
+__device__ void writer_load(const Pass& P, WriterLds& S, const BandTile* __restrict__ tiles,
+                            const BandEntry* __restrict__ ent, int64_t nt, int64_t nr,
+                            bool all_dense) {
   const int lane = lane_id();
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t x = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += x;
-  }
-  const int wid = tid / kWave;
-  if (lane == kWave - 1) L.wtot[wid] = incl;
-  __syncthreads();
-  uint32_t run = incl - loc;
-#pragma unroll
-  for (int w = 0; w < BW; ++w)
-    if (w < wid) run += L.wtot[w];
-#pragma unroll
-  for (int q = 0; q < kWordsPerThread; ++q) {
-    if (w0 + q < nwords) {
-      L.pre[w0 + q] = run;
-      run += static_cast<uint32_t>(__popc(L.bits[w0 + q]));
-    }
-  }
-  __syncthreads();
-  // each member's rank in index order
-#pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    if (off[q] >= 0) {
-      const int o = off[q];
-      const uint32_t word = L.bits[o >> 5];
-      const int rank = static_cast<int>(L.pre[o >> 5] + __popc(word & ((1u << (o & 31)) - 1u)));
-      const float val = value(en[q], rank, av[q]);
-      L.vals[rank] = val;
-      if (writeback) {
-        BandEntry w;
-        w.idx = en[q].idx;
-        w.bits = __float_as_uint(val);
-        base[rank] = w;
-      }
-    }
-  }
-  __syncthreads();
-}
-
-// Write out[b0 .. b1) from the map: members take their value, other scores
-// 0, or 1 where their bit in `ones` is set (ones may be null).
-__device__ void write_dense(int64_t b0, int64_t b1, const BandLds& L, const uint32_t* ones,
-                            float* __restrict__ out) {
-  const int tid = threadIdx.x;
-  const int64_t len = b1 - b0;
-  auto value = [&](int64_t o) -> float {   // o: block-local offset
-    const uint32_t word = L.bits[o >> 5];
-    const uint32_t bit = 1u << (o & 31);
-    if (word & bit) return L.vals[L.pre[o >> 5] + __popc(word & (bit - 1u))];
-    return (ones && ((ones[(b0 + o) >> 5] >> ((b0 + o) & 31)) & 1u)) ? 1.0f : 0.0f;
+  const int64_t G = gridDim.x;
+  // tile t of this workgroup (tile 0 stands in past the end)
+  auto tile_at = [&](int64_t t) -> int64_t { return t < nt ? blockIdx.x + t * G : 0; };
+  // lane i < kRound: the record of tile i of round k
+  auto ld_rec = [&](int64_t k) -> int2 {
+    const int64_t j = tile_at(k * kRound + (lane < kRound ? lane : 0));
+    return reinterpret_cast<const int2*>(tiles)[j];
   };
-  if ((reinterpret_cast<uintptr_t>(out + b0) & 15) == 0) {
-    const int64_t n4 = len / 4;
-    // float4 q takes nibble q & 7 of word q >> 3; WB float4 per thread at
-    // a time, their words (and bits of `ones`) read before any store
-    auto one4 = [&](int64_t q, uint32_t word, uint32_t oword) {
-      const int sh = static_cast<int>(q & 7) * 4;
-      const uint32_t nib = (word >> sh) & 15u;
-      const uint32_t onib = (oword >> sh) & 15u;
-      float v[4];
+  struct RoundInfo {
+    int32_t first;   // lane i < kRound: tile i's first list slot
+    int32_t cnt;     // lane i < kRound: its members in the lists (0 if dense or past the end)
+    int32_t total;   // members of the round
+    uint32_t dense;  // bit i: tile i is dense
+  };
+  auto info_of = [&](int64_t k, int2 rec) -> RoundInfo {
+    RoundInfo ri;
+    const bool valid = lane < kRound && k * kRound + lane < nt;
+    const bool dn = valid && (all_dense || rec.y < 0);
+    ri.first = rec.x;
+    ri.cnt = (valid && !dn) ? rec.y : 0;
+    ri.total = 0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = ((onib >> e) & 1u) ? 1.0f : 0.0f;
-      if (nib) {
-        uint32_t rk = L.pre[q >> 3] + static_cast<uint32_t>(__popc(word & ((1u << sh) - 1u)));
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if ((nib >> e) & 1u) v[e] = L.vals[rk++];
+    for (int x = 0; x < kRound; ++x) ri.total += __builtin_amdgcn_readlane(ri.cnt, x);
+    ri.dense = static_cast<uint32_t>(__ballot(dn));
+    return ri;
+  };
+  struct Data {
+    uint4 ov;
+    BandEntry e[kSlots];
+    float gs[kSlots];
+    int ti[kSlots];
+  };
+  auto ld_data = [&](int64_t k, const RoundInfo& ri, Data& d) {
+    if constexpr (Pass::kOnes) {
+      if (P.ones) {
+        const int64_t j = tile_at(k * kRound + lane / kLanesPerTile);
+        d.ov = reinterpret_cast<const uint4*>(P.ones)[j * (kTileWords / 4) + lane % kLanesPerTile];
+      } else {
+        d.ov = make_uint4(0u, 0u, 0u, 0u);
       }
-      store_stream4(out + b0 + 4 * q, make_float4(v[0], v[1], v[2], v[3]));
-    };
-    constexpr int WB = 8;
-    int64_t q0 = 0;
-    for (; q0 + WB * BT <= n4; q0 += WB * BT) {
-      uint32_t wd[WB], ow[WB];
-#pragma unroll
-      for (int k = 0; k < WB; ++k) {
-        const int64_t q = q0 + k * BT + tid;
-        wd[k] = L.bits[q >> 3];
-        ow[k] = ones ? ones[(b0 >> 5) + (q >> 3)] : 0u;
-      }
-#pragma unroll
-      for (int k = 0; k < WB; ++k) one4(q0 + k * BT + tid, wd[k], ow[k]);
     }
-    for (int64_t q = q0 + tid; q < n4; q += BT)
-      one4(q, L.bits[q >> 3], ones ? ones[(b0 >> 5) + (q >> 3)] : 0u);
-    for (int64_t o = n4 * 4 + tid; o < len; o += BT) out[b0 + o] = value(o);
-  } else {
-    for (int64_t o = tid; o < len; o += BT) out[b0 + o] = value(o);
+#pragma unroll
+    for (int q = 0; q < kSlots; ++q) {
+      const int32_t s = lane + kWave * q;
+      // tile of slot s: the last tile whose members start at or before s
+      int i = 0;
+      int32_t f = __builtin_amdgcn_readlane(ri.first, 0), p0 = 0;
+      int32_t run = __builtin_amdgcn_readlane(ri.cnt, 0);   // members of tiles 0 .. x-1
+#pragma unroll
+      for (int x = 1; x < kRound; ++x) {
+        const int32_t fx = __builtin_amdgcn_readlane(ri.first, x);
+        const bool at_or_past = s >= run;
+        i = at_or_past ? x : i;
+        f = at_or_past ? fx : f;
+        p0 = at_or_past ? run : p0;
+        run += __builtin_amdgcn_readlane(ri.cnt, x);
+      }
+      const bool valid = s < ri.total;
+      const int32_t at = valid ? f + (s - p0) : 0;
+      d.ti[q] = valid ? i : -1;
+      d.e[q] = ent[at];
+      d.gs[q] = P.stash() ? P.stash()[at] : 0.0f;
+    }
+  };
+  auto place = [&](int buf, int i, const BandEntry& e, float gs) {
+    float* tl = reinterpret_cast<float*>(S.tile[buf][i]);
+    tl[e.idx & static_cast<int32_t>(kBandTile - 1)] = P.member(e, gs);
+  };
+  int2 rec1 = ld_rec(1), rec2;
+  RoundInfo ri0 = info_of(0, ld_rec(0));
+  Data cur, nxt;
+  ld_data(0, ri0, cur);
+  // round 0's data in hand before the loop (an empty asm that reads it): the
+  // loop's own loads are then only waited for at its end (the copies into
+  // `cur`), never while the round's members are placed
+#pragma unroll
+  for (int q = 0; q < kSlots; ++q)
+    asm volatile("" ::"v"(cur.e[q].idx), "v"(cur.e[q].bits), "v"(cur.gs[q]), "v"(cur.ti[q]));
+  if constexpr (Pass::kOnes)
+    asm volatile("" ::"v"(cur.ov.x), "v"(cur.ov.y), "v"(cur.ov.z), "v"(cur.ov.w));
+  for (int64_t k = 0; k < nr; ++k) {
+    rec2 = ld_rec(k + 2);
+    const RoundInfo ri1 = info_of(k + 1, rec1);
+    ld_data(k + 1, ri1, nxt);
+    const int buf = static_cast<int>(k & 1);
+    if constexpr (Pass::kOnes)
+      reinterpret_cast<uint4*>(S.ow[buf][lane / kLanesPerTile])[lane % kLanesPerTile] = cur.ov;
+    if (lane == 0) S.dense[buf] = ri0.dense;
+#pragma unroll
+    for (int q = 0; q < kSlots; ++q)
+      if (cur.ti[q] >= 0) place(buf, cur.ti[q], cur.e[q], cur.gs[q]);
+    if (ri0.total > kWave * kSlots) {
+      // members past the slots (dense bands): read here, one at a time
+      int32_t pi = 0;   // members of the tiles before tile i
+      for (int i = 0; i < kRound; ++i) {
+        const int32_t fi = __builtin_amdgcn_readlane(ri0.first, i);
+        const int32_t ci = __builtin_amdgcn_readlane(ri0.cnt, i);
+        for (int32_t e = lane; e < ci; e += kWave) {
+          if (pi + e >= kWave * kSlots) {
+            const int32_t at = fi + e;
+            place(buf, i, ent[at], P.stash() ? P.stash()[at] : 0.0f);
+          }
+        }
+        pi += ci;
+      }
+    }
+    __syncthreads();
+    rec1 = rec2;
+    ri0 = ri1;
+    cur = nxt;
   }
 }
 
-// Dense emit of one block's range.
-__device__ void dense_emit(const float* __restrict__ r, int64_t b0, int64_t b1, double b,
-                           double inv_t, float* __restrict__ p) {
-  const int tid = threadIdx.x;
-  const bool vec = ((reinterpret_cast<uintptr_t>(r + b0) | reinterpret_cast<uintptr_t>(p + b0)) & 15) == 0;
-  int64_t i = b0 + tid;
-  if (vec) {
-    const int64_t n4 = (b1 - b0) / 4;
-    for (int64_t q = tid; q < n4; q += BT) {
-      const float4 v = load_stream4(r + b0 + 4 * q);
-      store_stream4(p + b0 + 4 * q, make_float4(laplace_p(v.x, b, inv_t), laplace_p(v.y, b, inv_t),
-                                                laplace_p(v.z, b, inv_t), laplace_p(v.w, b, inv_t)));
+template <class Pass>
+__device__ void band_write(const Pass& P, WriterLds& S, const BandCtx& c, int64_t n,
+                           float* __restrict__ out, bool all_dense) {
+  const int64_t ntiles = (n + kBandTile - 1) / kBandTile;
+  const int64_t nt = static_cast<int64_t>(blockIdx.x) < ntiles
+                         ? (ntiles - 1 - static_cast<int64_t>(blockIdx.x)) / gridDim.x + 1
+                         : 0;
+  const int64_t nr = (nt + kRound - 1) / kRound;
+  const bool vec_out = (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  const bool vec_in = ((reinterpret_cast<uintptr_t>(P.in0()) |
+                        reinterpret_cast<uintptr_t>(P.in1())) & 15) == 0;
+  if (threadIdx.x < kStoreWaves * kWave) {
+#pragma unroll
+    for (int i = 0; i < kRound; ++i) {
+      S.tile[0][i][threadIdx.x] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      S.tile[1][i][threadIdx.x] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     }
-    i = b0 + n4 * 4 + tid;
+    __syncthreads();
+    writer_store(P, S, out, n, nt, nr, vec_out, vec_in);
+  } else {
+    __syncthreads();
+    writer_load(P, S, c.tiles, c.ent, nt, nr, all_dense);
   }
-  for (; i < b1; i += BT) p[i] = laplace_p(r[i], b, inv_t);
+}
+
+int writer_blocks(int64_t n) {
+  const int64_t ntiles = (n + kBandTile - 1) / kBandTile;
+  return static_cast<int>(ntiles < kWriterBlocks ? ntiles : kWriterBlocks);
 }
 
 }  // namespace
 
-__global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__ r, int64_t n,
+__global__ __launch_bounds__(WT) void band_emit_kernel(const float* __restrict__ r, int64_t n,
                                                        const SolveRec* __restrict__ rec,
                                                        double inv_t, BandCtx c,
                                                        const uint32_t* __restrict__ ones_all,
                                                        const PartTotals* __restrict__ tot,
                                                        float* __restrict__ p,
                                                        double* __restrict__ b_out) {
-  extern __shared__ uint32_t band_lds_mem[];
-  const BandLds L = band_lds(band_lds_mem, c.chunk, c.cap);
+  __shared__ WriterLds S;
   if (!rec->ok) return;
-  const uint32_t* ones = tot->aR < INFINITY ? ones_all : nullptr;
   const double b = rec->b;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     b_out[0] = b;
@@ -297,26 +371,23 @@ __global__ __launch_bounds__(BT) void band_emit_kernel(const float* __restrict__
     h.cap = c.cap;
     h.pad = 0;
     h.n = n;
+    h.b = b;
     *c.hdr = h;
   }
-  const BlockRange br = block_range(n, c.chunk);
-  if (!lists_usable(c, static_cast<int>(blockIdx.x))) {
-    dense_emit(r, br.b0, br.b1, b, inv_t, p);
-    return;
-  }
-  build_map(c, br.b0, br.b1 - br.b0, L, true, true, nullptr, [&](const BandEntry& en, int, float) {
-    return laplace_p(__uint_as_float(en.bits), b, inv_t);
-  });
-  write_dense(br.b0, br.b1, L, ones, p);
+  EmitPass P;
+  P.r = r;
+  P.ones = tot->aR < INFINITY ? ones_all : nullptr;
+  P.b = b;
+  P.inv_t = inv_t;
+  band_write(P, S, c, n, p, false);
 }
 
 hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, double t,
                             const BandCtx& band, const uint32_t* ones, const PartTotals* tot,
                             float* p, double* b_out, hipStream_t s) {
   { ProfScope ps_("band_emit", s);
-  hipLaunchKernelGGL(band_emit_kernel, dim3(band.nblocks), dim3(BT),
-                     static_cast<unsigned>(band_lds_bytes(band.chunk, band.cap)), s, r, n, rec, 1.0 / t, band,
-                     ones, tot, p, b_out); }
+  hipLaunchKernelGGL(band_emit_kernel, dim3(writer_blocks(n)), dim3(WT), 0, s, r, n, rec, 1.0 / t,
+                     band, ones, tot, p, b_out); }
   return hipGetLastError();
 }
 
@@ -328,6 +399,7 @@ __global__ void ctx_dense_kernel(BandCtx c, int64_t n) {
   h.cap = c.cap;
   h.pad = 0;
   h.n = n;
+  h.b = 0.0;
   *c.hdr = h;
 }
 
@@ -338,14 +410,14 @@ hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------- backward --
-// One wave of a reduce block per partition block; the emit blocks sum the
+// One wave of a reduce block per partition block; the writer blocks sum the
 // reduce partials themselves (fixed order), so no launch sits between.
 constexpr int kVjpWaveBlocks = BW;             // partition blocks per reduce block
-constexpr int kVjpMaxParts = 4 * BT;           // partials an emit block sums
+constexpr int kVjpMaxParts = 4 * BT;           // partials a writer block sums
 
 __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __restrict__ g,
                                                              const float* __restrict__ p,
-                                                             int64_t n, BandCtx c,
+                                                             int64_t n, BandCtx c, double inv_t,
                                                              float* __restrict__ gstash,
                                                              double* __restrict__ partials) {
   __shared__ double red[2][BW];
@@ -353,10 +425,11 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
   const int lane = lane_id();
   const int wid = tid / kWave;
   const int pb = static_cast<int>(blockIdx.x) * kVjpWaveBlocks + wid;
+  const CtxHeader h = *c.hdr;
   double F = 0.0, G = 0.0;
   if (pb < c.nblocks) {
     const BlockRange br = range_of(n, c.chunk, pb);
-    if (block_dense(c, n, pb)) {
+    if (header_dense(h, c, n) || !lists_usable(c, pb)) {
       for (int64_t i = br.b0 + lane; i < br.b1; i += kWave) {
         const float pv = p[i];
         const float f = fminf(pv, 1.0f - pv);
@@ -366,27 +439,35 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
         }
       }
     } else {
-      // after the emit the block's members form one list in index order;
-      // VB entries per lane at a time, all their loads (then all the loads
-      // of g they select) in flight together; each lane still adds its
-      // entries in list order
-      const BandBlock& bb = c.blk[pb];
-      const int total = bb.cnt[0] + bb.cnt[1] + bb.cnt[2] + bb.cnt[3];
+      // the block's members in index order are the four wave segments one
+      // after the other; VB members per lane at a time, all their loads
+      // (then all the loads of g they select) in flight together; each lane
+      // still adds its members in list order
+      const int4 cnt = *reinterpret_cast<const int4*>(c.blk[pb].cnt);
+      const int s1 = cnt.x, s2 = cnt.x + cnt.y, s3 = cnt.x + cnt.y + cnt.z;
+      const int total = s3 + cnt.w;
       const int64_t base = static_cast<int64_t>(pb) * BW * c.cap;
+      auto slot_of = [&](int e) -> int64_t {
+        const int w = (e >= s1 ? 1 : 0) + (e >= s2 ? 1 : 0) + (e >= s3 ? 1 : 0);
+        const int sb = w == 0 ? 0 : (w == 1 ? s1 : (w == 2 ? s2 : s3));
+        return base + static_cast<int64_t>(w) * c.cap + (e - sb);
+      };
       constexpr int VB = 8;
       for (int e0 = 0; e0 < total; e0 += VB * kWave) {
         BandEntry en[VB];
+        int64_t at[VB];
 #pragma unroll
         for (int u = 0; u < VB; ++u) {
           const int e = e0 + u * kWave + lane;
-          en[u] = c.ent[base + (e < total ? e : 0)];
+          at[u] = slot_of(e < total ? e : 0);
+          en[u] = c.ent[at[u]];
         }
         float fv[VB], gv[VB];
         bool use[VB];
 #pragma unroll
         for (int u = 0; u < VB; ++u) {
           const int e = e0 + u * kWave + lane;
-          const float pv = __uint_as_float(en[u].bits);
+          const float pv = laplace_p(__uint_as_float(en[u].bits), h.b, inv_t);
           fv[u] = fminf(pv, 1.0f - pv);
           use[u] = e < total && fv[u] != 0.0f && en[u].idx >= br.b0 && en[u].idx < br.b1;
           gv[u] = g[use[u] ? en[u].idx : br.b0];   // an index of this block either way
@@ -394,7 +475,7 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
 #pragma unroll
         for (int u = 0; u < VB; ++u) {
           if (use[u]) {
-            gstash[base + e0 + u * kWave + lane] = gv[u];
+            gstash[at[u]] = gv[u];
             F += static_cast<double>(fv[u]);
             G += static_cast<double>(fv[u]) * static_cast<double>(gv[u]);
           }
@@ -423,20 +504,19 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
 
 // grad_r = (f/t)(g - <g,q>); <g,q> = sum f g / sum f from the partials, 0
 // (and grad_r = 0) when sum f == 0.
-__global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restrict__ g,
-                                                           const float* __restrict__ p,
-                                                           int64_t n, BandCtx c,
-                                                           const float* __restrict__ gstash,
-                                                           const double* __restrict__ partials,
-                                                           int nparts, double inv_t,
-                                                           float* __restrict__ grad) {
-  extern __shared__ uint32_t band_lds_mem[];
-  const BandLds L = band_lds(band_lds_mem, c.chunk, c.cap);
-  __shared__ double red[2][BW];
+__global__ __launch_bounds__(WT) void band_vjp_write_kernel(const float* __restrict__ g,
+                                                            const float* __restrict__ p,
+                                                            int64_t n, BandCtx c,
+                                                            const float* __restrict__ gstash,
+                                                            const double* __restrict__ partials,
+                                                            int nparts, double inv_t,
+                                                            float* __restrict__ grad) {
+  __shared__ WriterLds S;
   const int tid = threadIdx.x;
-  double F = 0.0, G = 0.0;
-  {
-    // every load issued before the first add (nparts >= 1)
+  const CtxHeader h = *c.hdr;
+  if (tid < BT) {
+    // the partials in a fixed order: thread tid adds parts tid, tid + BT, ...
+    double F = 0.0, G = 0.0;
     double2 pr[kVjpMaxParts / BT];
 #pragma unroll
     for (int q = 0; q < kVjpMaxParts / BT; ++q) {
@@ -450,39 +530,29 @@ __global__ __launch_bounds__(BT) void band_vjp_emit_kernel(const float* __restri
         G += pr[q].y;
       }
     }
-  }
-  F = wave_sum(F);
-  G = wave_sum(G);
-  if (lane_id() == 0) {
-    red[0][tid / kWave] = F;
-    red[1][tid / kWave] = G;
+    F = wave_sum(F);
+    G = wave_sum(G);
+    if (lane_id() == 0) {
+      S.red[0][tid / kWave] = F;
+      S.red[1][tid / kWave] = G;
+    }
   }
   __syncthreads();
   double fs = 0.0, gsum = 0.0;
 #pragma unroll
   for (int w = 0; w < BW; ++w) {
-    fs += red[0][w];
-    gsum += red[1][w];
+    fs += S.red[0][w];
+    gsum += S.red[1][w];
   }
-  const float coef = static_cast<float>(fs > 0.0 ? gsum / fs : 0.0);
-  const float scale = static_cast<float>(fs > 0.0 ? inv_t : 0.0);
-  const BlockRange br = block_range(n, c.chunk);
-  if (block_dense(c, n, static_cast<int>(blockIdx.x))) {
-    for (int64_t i = br.b0 + tid; i < br.b1; i += BT) {
-      const float pv = p[i];
-      const float f = fminf(pv, 1.0f - pv);
-      grad[i] = (f != 0.0f) ? f * scale * (g[i] - coef) : 0.0f;
-    }
-    return;
-  }
-  // g of each member was stashed at its slot by the reduce (where f != 0)
-  build_map(c, br.b0, br.b1 - br.b0, L, false, false, gstash,
-            [&](const BandEntry& en, int, float gv) {
-              const float pv = __uint_as_float(en.bits);
-              const float f = fminf(pv, 1.0f - pv);
-              return (f != 0.0f) ? f * scale * (gv - coef) : 0.0f;
-            });
-  write_dense(br.b0, br.b1, L, nullptr, grad);
+  VjpPass P;
+  P.p = p;
+  P.g = g;
+  P.gstash = gstash;
+  P.b = h.b;
+  P.inv_t = inv_t;
+  P.coef = static_cast<float>(fs > 0.0 ? gsum / fs : 0.0);
+  P.scale = static_cast<float>(fs > 0.0 ? inv_t : 0.0);
+  band_write(P, S, c, n, grad, header_dense(h, c, n));
 }
 
 int band_vjp_parts(int nblocks) { return (nblocks + kVjpWaveBlocks - 1) / kVjpWaveBlocks; }
@@ -491,14 +561,14 @@ hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const Band
                            float* gstash, double* partials, double t, float* grad,
                            hipStream_t s) {
   const int parts = band_vjp_parts(band.nblocks);
+  if (parts > kVjpMaxParts) return hipErrorInvalidValue;
   { ProfScope ps_("band_vjp_reduce", s);
-  hipLaunchKernelGGL(band_vjp_reduce_kernel, dim3(parts), dim3(BT), 0, s, g, p, n, band, gstash,
-                     partials); }
+  hipLaunchKernelGGL(band_vjp_reduce_kernel, dim3(parts), dim3(BT), 0, s, g, p, n, band, 1.0 / t,
+                     gstash, partials); }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("band_vjp_emit", s);
-  hipLaunchKernelGGL(band_vjp_emit_kernel, dim3(band.nblocks), dim3(BT),
-                     static_cast<unsigned>(band_lds_bytes(band.chunk, band.cap)), s, g, p, n, band,
+  hipLaunchKernelGGL(band_vjp_write_kernel, dim3(writer_blocks(n)), dim3(WT), 0, s, g, p, n, band,
                      gstash, partials, parts, 1.0 / t, grad); }
   return hipGetLastError();
 }

@@ -317,11 +317,12 @@ hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* soffs
 
 // -------------------------------------------------------------- partition --
 int partition_blocks(int64_t n, int64_t* chunk) {
-  // up to 4096 blocks; a block's chunk is a multiple of 1024 scores so that
-  // each wave owns a contiguous, float4-aligned quarter of it
+  // up to 4096 blocks; a block's chunk is a multiple of four writer tiles so
+  // that each wave owns a contiguous quarter of it made of whole tiles
+  constexpr int64_t q = PW * kBandTile;
   int64_t c = (n + kPartMaxBlocks - 1) / kPartMaxBlocks;
-  c = (c + 1023) / 1024 * 1024;
-  if (c < 1024) c = 1024;
+  c = (c + q - 1) / q * q;
+  if (c < q) c = q;
   *chunk = c;
   return static_cast<int>((n + c - 1) / c);
 }
@@ -382,20 +383,25 @@ __device__ __forceinline__ void classify4(const float (&v)[4], const bool (&ok)[
 constexpr int kWaveStage = kPartStageCap / PW;   // M entries staged per wave
 
 // Per-wave pass over [w0, w1): tails in float32 over one float4 and float64
-// across, R counted only when a_R is finite (HAS_R), band members staged in
-// any order and M members (a subset of the band) in index order, and with a
-// finite a_R one bit per score for r >= hi.  L is not counted:
+// across, R counted only when a_R is finite (HAS_R), band members and M
+// members (a subset of the band) staged in index order, and with a finite
+// a_R one bit per score for r >= hi.  L is not counted:
 // n_L = scores - n_M - n_R.
 // With STAGE the L tail is summed once at the end from the wave's staged
 // band (its members below a_L are the only nonzero terms), or from a second
 // read of the range if the list overflowed; without it (a range too long to
 // stage) each member's term is formed as it is met.
+// tb: lane q ends with the band members met before tile q of the range (the
+// range starts on a tile boundary; tiles are kBandTile scores).
 template <bool HAS_R, bool STAGE>
 __device__ __forceinline__ void partition_range(const float* __restrict__ r, int64_t w0, int64_t w1,
                                                 bool vec, float aL, float aR, float c2f,
                                                 float* sv, int32_t* si, const BandWave& bw,
-                                                PartState& st) {
+                                                PartState& st, int32_t& tb) {
   const int lane = lane_id();
+  auto tile_start = [&](int64_t at) {
+    if (lane == static_cast<int>((at - w0) / kBandTile)) tb = static_cast<int32_t>(st.nB);
+  };
   // it: first score of this wave's 256-score step (a multiple of 256)
   auto one = [&](const float (&v)[4], const bool (&ok)[4], int64_t it) {
     const int64_t i0 = it + 4 * lane;
@@ -429,9 +435,8 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       x |= __shfl_xor(x, 4, kWave);
       if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
     }
-    // band members take slots from the masks and the wave's running count
-    // (element-major, so not in index order; the emit puts each block's
-    // list in index order)
+    // band members take slots in index order from the masks and the wave's
+    // running count
     uint64_t bm[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) bm[e] = __ballot(inB[e]);
@@ -468,20 +473,21 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
           }
         }
       } else {
-        // element-major: all members of element 0, then of element 1, ...
-        uint32_t nb = nb0;
+        // a lane's members follow those of the lanes below it
+        uint32_t slot = nb0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) slot += lanes_below(bm[e]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if (inB[e]) {
-            const uint32_t slot = nb + lanes_below(bm[e]);
             if (slot < cap) {
               BandEntry en;
               en.idx = static_cast<int32_t>(i0 + e);
               en.bits = __float_as_uint(v[e]);
               bw.sbuf[slot] = en;
             }
+            ++slot;
           }
-          nb += static_cast<uint32_t>(__popcll(bm[e]));
         }
       }
       st.nB = nb0 + tot;
@@ -511,6 +517,7 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
     }
   };
   constexpr int U = 4;   // float4 loads per lane per batch, two batches in flight
+  static_assert(U * 256 == kBandTile, "a batch of the vector loop is one tile");
   int64_t it = w0;
   if (vec && it + U * 256 <= w1) {
     // two buffers taking turns, so that no registers are copied per batch.
@@ -538,17 +545,20 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       it += U * 256;
       const bool more_a = it + U * 256 <= w1;
       load(qb, it, more_a);
+      tile_start(ca);
       run(qa, ca);
       if (!more_a) break;
       const int64_t cb = it;
       it += U * 256;
       const bool more_b = it + U * 256 <= w1;
       load(qa, it, more_b);
+      tile_start(cb);
       run(qb, cb);
       if (!more_b) break;
     }
   }
   for (; it < w1; it += 256) {
+    if (((it - w0) & (kBandTile - 1)) == 0) tile_start(it);
     const int64_t i0 = it + 4 * lane;
     float v[4];
     bool ok[4];
@@ -725,7 +735,8 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
                                                        int32_t* __restrict__ stage_i,
                                                        PartBlock* __restrict__ blk, double t,
                                                        BandEntry* __restrict__ bent,
-                                                       BandBlock* __restrict__ bblk, int bcap,
+                                                       BandBlock* __restrict__ bblk,
+                                                       BandTile* __restrict__ btile, int bcap,
                                                        uint32_t* __restrict__ ones) {
   __shared__ float sv[PW][kWaveStage];
   __shared__ int32_t si[PW][kWaveStage];
@@ -755,19 +766,19 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   bw.hi = __double2float_ru(static_cast<double>(aR) + kBandHighT * t);
   bw.w0 = w0;
   PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY, 0};
+  int32_t tb = 0;
   const bool has_r = aR < INFINITY;
   if (has_r)
     if (bw.stage)
-      partition_range<true, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
+      partition_range<true, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
     else
-      partition_range<true, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
+      partition_range<true, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
   else
     if (bw.stage)
-      partition_range<false, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
+      partition_range<false, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
     else
-      partition_range<false, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st);
-  // this wave's bits and band list (in the order the members were met) out
-  // of LDS; the emit puts the block's list in index order
+      partition_range<false, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
+  // this wave's bits and band list out of LDS
   if (bw.stage) {
     if (has_r) {
       const int nw = static_cast<int>((w1 - w0 + 31) / 32);   // <= kOnesWaveWords
@@ -801,6 +812,28 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
     red_f[1][wid] = mx;
   }
   __syncthreads();
+  // per tile of this wave's range: its members' place in the lists, or -1
+  // when the block's lists are incomplete
+  {
+    bool bdense = !bw.stage;
+#pragma unroll
+    for (int w = 0; w < PW; ++w) bdense |= red_b[w] > bcap;
+    const int ntw = static_cast<int>((w1 - w0 + kBandTile - 1) / kBandTile);
+    const int32_t nb = static_cast<int32_t>(st.nB);
+    const int32_t next = __shfl_down(tb, 1, kWave);   // tile q + 1's start
+    const int32_t seg = (static_cast<int32_t>(blockIdx.x) * PW + wid) * bcap;
+    for (int q = lane; q < ntw; q += kWave) {
+      BandTile tr;
+      if (bdense) {
+        tr.first = 0;
+        tr.count = -1;
+      } else {
+        tr.first = seg + tb;
+        tr.count = (q + 1 < ntw ? next : nb) - tb;
+      }
+      btile[w0 / kBandTile + q] = tr;
+    }
+  }
   int64_t off = 0, mtot = 0;
   bool over = false;
 #pragma unroll
@@ -861,7 +894,8 @@ hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int
   const float c2f = static_cast<float>(kLog2e / t);
   { ProfScope ps_("partition", s);
   hipLaunchKernelGGL(partition_kernel, dim3(nblocks), dim3(PT), 0, s, r, n, sel, use_sel, aL, aR,
-                     c2f, chunk, stage_v, stage_i, blk, t, band.ent, band.blk, band.cap, ones); }
+                     c2f, chunk, stage_v, stage_i, blk, t, band.ent, band.blk, band.tiles, band.cap,
+                     ones); }
   return hipGetLastError();
 }
 
@@ -885,14 +919,16 @@ struct CtxLayout {
   int nblocks;
   int64_t chunk;
   int cap;
-  size_t blk_off, ent_off, bytes;
+  size_t blk_off, tile_off, ent_off, bytes;
 };
 CtxLayout ctx_layout(int64_t n) {
   CtxLayout L{};
   L.nblocks = partition_blocks(n, &L.chunk);
   L.cap = band_wave_cap(L.chunk);
+  const size_t ntiles = static_cast<size_t>((n + kBandTile - 1) / kBandTile);
   L.blk_off = 256;
-  L.ent_off = L.blk_off + (static_cast<size_t>(L.nblocks) * sizeof(BandBlock) + 255) / 256 * 256;
+  L.tile_off = L.blk_off + (static_cast<size_t>(L.nblocks) * sizeof(BandBlock) + 255) / 256 * 256;
+  L.ent_off = L.tile_off + (ntiles * sizeof(BandTile) + 255) / 256 * 256;
   L.bytes = (L.ent_off + static_cast<size_t>(L.nblocks) * PW * L.cap * sizeof(BandEntry) + 255) /
             256 * 256;
   return L;
@@ -910,6 +946,7 @@ BandCtx band_ctx_view(void* base, int64_t n) {
   char* b = static_cast<char*>(base);
   v.hdr = reinterpret_cast<CtxHeader*>(b);
   v.blk = b ? reinterpret_cast<BandBlock*>(b + L.blk_off) : nullptr;
+  v.tiles = b ? reinterpret_cast<BandTile*>(b + L.tile_off) : nullptr;
   v.ent = b ? reinterpret_cast<BandEntry*>(b + L.ent_off) : nullptr;
   return v;
 }

@@ -56,16 +56,19 @@ struct PartTotals {
 // float32) and hi = a_R + 18 t (rounded up), every score below lo has
 // (r - b)/t < -104 and p exactly 0 in float32, and every score at or above
 // hi has (r - b)/t > 17 and p exactly 1, for any b in the bracket.  The
-// partition stages the band in index order, the emit then writes p without
-// re-reading r, and the backward visits only the band.
+// partition stages the band in index order and records, per tile of
+// kBandTile scores, where the tile's members sit in the lists; the dense
+// writers then fill p (and grad_r) tile by tile without re-reading r, and
+// the backward visits only the band.
 constexpr double kBandLowT = 105.0;
 constexpr double kBandHighT = 18.0;
 constexpr int kBandWaveCapMax = 512;        // band entries a partition wave stages
 constexpr int64_t kBandMaxChunk = 65536;    // longer block ranges take the dense passes
+constexpr int64_t kBandTile = 1024;         // scores per tile of the dense writers
 
 struct alignas(8) BandEntry {
   int32_t idx;     // index in the row
-  uint32_t bits;   // float32 score after the partition, p after the emit
+  uint32_t bits;   // float32 score
 };
 
 // Per partition block.
@@ -73,6 +76,14 @@ struct BandBlock {
   int32_t cnt[4];   // band members met by each wave (can exceed the capacity)
   int32_t dense;    // 1: the lists of this block are incomplete; passes read it densely
   int32_t pad[3];
+};
+
+// Where the members of one tile are: entries [first, first + count) of the
+// list array, in index order; count -1 when the tile takes the dense form
+// (its block's lists are incomplete).
+struct BandTile {
+  int32_t first;
+  int32_t count;
 };
 
 // Saved band of one row (the forward's context for the backward).
@@ -83,11 +94,13 @@ struct CtxHeader {
   int32_t cap;      // entries per wave segment
   int32_t pad;
   int64_t n;
+  double b;         // the forward's root (mode 0)
 };
 
 struct BandCtx {
   CtxHeader* hdr;
   BandBlock* blk;    // [nblocks]
+  BandTile* tiles;   // [ceil(n / kBandTile)]
   BandEntry* ent;    // [nblocks][4][cap]
   int nblocks;
   int64_t chunk;
@@ -193,7 +206,8 @@ int band_wave_cap(int64_t chunk);
 // Bytes of one row's context and its layout at `base` (null base: sizes only).
 size_t band_ctx_bytes(int64_t n);
 BandCtx band_ctx_view(void* base, int64_t n);
-// ones: [ceil(n/32)] bit set where r >= hi (written only when a_R is finite).
+// ones: [ceil(n / kBandTile) * kBandTile / 32] bit set where r >= hi (written
+// only when a_R is finite; the words past n are never written).
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
                             float aR, double t, int nblocks, int64_t chunk, float* stage_v,
                             int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
@@ -203,10 +217,10 @@ hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int
 hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const SelectRec* sel,
                                    int use_sel, float aL, float aR, int64_t* offsets,
                                    PartTotals* tot, hipStream_t s);
-// Emit after a certified bracket (skipped when rec->ok == 0): p from the band
-// lists and the ones bits (used when tot->aR is finite), dense from r for
-// blocks without usable lists; each block's list is written back in index
-// order with p; b_out[0] = rec->b; the context header is set.
+// Emit after a certified bracket (skipped when rec->ok == 0): p of every
+// score, from the band lists and the ones bits (used when tot->aR is
+// finite), and from r for tiles without usable lists; b_out[0] = rec->b; the
+// context header is set (with b).
 hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, double t,
                             const BandCtx& band, const uint32_t* ones, const PartTotals* tot,
                             float* p, double* b_out, hipStream_t s);
@@ -214,7 +228,7 @@ hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, doub
 hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s);
 // Backward from a saved band: partial (sum f, sum f g) per run of blocks,
 // then grad_r written densely (zero outside the band).  partials: 2 doubles
-// per part, band_vjp_parts(nblocks) parts.
+// per part, band_vjp_parts(nblocks) parts; gstash: one float per list slot.
 int band_vjp_parts(int nblocks);
 hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const BandCtx& band,
                            float* gstash, double* partials, double t, float* grad,

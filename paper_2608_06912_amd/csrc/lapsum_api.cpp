@@ -191,7 +191,7 @@ struct BracketWs {
   double* m_tile_buf;
   SolveRec* rec;       // &att->rec
   FullWs fall;         // full-sort fallback
-  uint32_t* ones;      // [ceil(n/32)] scores at or above the band (finite a_R)
+  uint32_t* ones;      // [ceil(n/kBandTile) kBandTile/32] scores at or above the band (finite a_R)
   void* band;          // one row's band when the caller keeps none
   int nblocks;
   int64_t chunk;
@@ -236,7 +236,7 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
   }
   w.rec = w.att ? &w.att->rec : nullptr;
   if (n > kRowOnChipMax) w.fall = carve_full(c, n, false);
-  w.ones = c.take<uint32_t>(static_cast<size_t>((n + 31) / 32));
+  w.ones = c.take<uint32_t>(static_cast<size_t>((n + kBandTile - 1) / kBandTile * (kBandTile / 32)));
   w.band = c.take<char>(band_ctx_bytes(n));
   return w;
 }
