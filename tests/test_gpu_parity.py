@@ -347,6 +347,76 @@ def test_bracketed_band_too_wide_for_the_lists(lib):
     assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
 
 
+def test_bracketed_band_past_the_writer_slots(lib):
+    # a band of about 2.5% of the scores puts some 200 members into a
+    # writer round (eight tiles of 1024) and often more: the loading wave
+    # places those past its slots one at a time; no block overflows its lists
+    n = 2_000_003
+    r = W.random_case(34, n, dist="normal")[0]
+    k, alpha = n / 2.0, -0.0005
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([85], K, 0.0005)
+    g = W.random_case(35, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label="slots", g=g)
+    assert not info["fell_back"]
+    t = -alpha
+    lo = np.float32(info["a_L"]) - 105.0 * t
+    hi = np.float32(info["a_R"]) + 18.0 * t
+    assert np.count_nonzero((r >= lo) & (r < hi)) > 0.02 * n
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
+
+
+def test_bracketed_dense_and_listed_blocks_in_one_row(lib):
+    # 40000 scores packed at the root fill the band lists of the blocks that
+    # hold them (those blocks take the dense form); the rest of the row keeps
+    # its lists, so one writer round mixes dense and listed tiles
+    n = 1_000_000
+    r = W.random_case(36, n, dist="normal")[0]
+    k, alpha = n / 4.0, -0.0004
+    v = np.float32(np.quantile(r, 1.0 - k / n))
+    seg = slice(300_000, 340_000)
+    r[seg] = v + np.float32(1e-4) * W.random_case(37, 40_000, dist="normal")[0]
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([86], K, 0.0004)
+    g = W.random_case(38, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label="mixed", g=g)
+    assert not info["fell_back"]
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
+
+
+def test_bracketed_batched_rows_of_odd_length(lib):
+    # rows of a batch start 4 n bytes apart: with n odd they are not 16-byte
+    # aligned, and the passes take their scalar paths
+    batch, n = 3, 100_003
+    rows = W.random_case(39, n, dist="normal", batch=batch)
+    k, alpha = n / 8.0, -0.01
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([87], K, 0.01)
+    gs = W.random_case(40, n, dist="normal", batch=batch)
+    band = lib.new_band(batch, n, "cuda")
+    p, b, infos, _ = lib.lapsum_forward_bracketed(_t(rows), k, alpha, _t(noise), band=band)
+    grad = _np(lib.lapsum_backward_band(_t(gs), p, band, alpha))
+    pn, bn = _np(p), _np(b)
+    for i in range(batch):
+        po, bo, oinfo, _ = O.bracketed_forward(rows[i], k, alpha, noise)
+        _check_info(infos[i], oinfo, f"row {i}")
+        assert abs(float(bn[i]) - bo) <= 2e-6 * -alpha, i
+        assert np.max(np.abs(pn[i].astype(np.float64) - O.probs(rows[i], bo, alpha))) <= P_TOL, i
+        assert grad_rel(grad[i], O.vjp(rows[i], bo, alpha, gs[i])) <= G_TOL, i
+
+
+@pytest.mark.parametrize("n", [700, 1024, 1025])
+def test_bracketed_rows_of_about_one_tile(lib, n):
+    # one writer workgroup; the last tile whole, partial, or a single score
+    r = W.random_case(41, n, dist="normal")[0]
+    k, alpha = n / 10.0, -0.05
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([88, n], K, 0.05)
+    g = W.random_case(42, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=f"n={n}", g=g)
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
+
+
 def test_backward_band_saved_for_another_length(lib):
     # a band whose header names another row length is not used: the
     # backward takes the dense form from p
