@@ -41,10 +41,10 @@ HBM_PEAK_GBS = 8000.0
 # measurement; once that file changes the figure no longer describes the
 # kernel and is reported as null.
 MEASURED_TRAFFIC = {
-    "band_emit": ("band_kernels.hip", "16de33e92a58549052e914223eac99bf151cc2c3", 422.0e6),
-    "band_vjp_emit": ("band_kernels.hip", "16de33e92a58549052e914223eac99bf151cc2c3", 416.6e6),
-    "band_vjp_reduce": ("band_kernels.hip", "16de33e92a58549052e914223eac99bf151cc2c3", 60.5e6),
-    "partition": ("bracket_kernels.hip", "5e1b71812ce2df80bcbffa768415d2326a9a27a2", 413.0e6),
+    "band_emit": ("band_kernels.hip", "283a3cddadfd71026920a615b48d8f90b747c3fa", 427.2e6),
+    "band_vjp_emit": ("band_kernels.hip", "283a3cddadfd71026920a615b48d8f90b747c3fa", 443.6e6),
+    "band_vjp_reduce": ("band_kernels.hip", "283a3cddadfd71026920a615b48d8f90b747c3fa", 61.3e6),
+    "partition": ("bracket_kernels.hip", "d923efb3ca4b3562671a1eee0dc2017c323bbb0e", 413.8e6),
 }
 METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
 
@@ -62,16 +62,18 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_bytes(name: str, n: int, active: int, band: int) -> float | None:
+def kernel_bytes(name: str, n: int, active: int, band: int, ones: bool) -> float | None:
     """Algorithmic HBM bytes one launch of a streaming kernel must move
-    (band: scores in the bracket's band; active: scores with 0 < p < 1)."""
+    (band: scores in the bracket's band; active: scores with 0 < p < 1;
+    ones: a_R is finite, so one bit per score marks the scores above the band)."""
     tiles = 8.0 * ((n + 1023) // 1024)     # one 8-byte record per writer tile
+    bits = n / 8.0 if ones else 0.0
     if name == "partition":
-        # read r; stage the band; one bit per score above it; the tile records
-        return 4.0 * n + 8.0 * band + n / 8.0 + tiles
+        # read r; stage the band; the bits above it; the tile records
+        return 4.0 * n + 8.0 * band + bits + tiles
     if name == "band_emit":
         # write p; read the band, the bits above it and the tile records
-        return 4.0 * n + 8.0 * band + n / 8.0 + tiles
+        return 4.0 * n + 8.0 * band + bits + tiles
     if name == "band_vjp_reduce":
         return 8.0 * band + 8.0 * active     # read the band; g and its copy where f != 0
     if name == "band_vjp_emit":
@@ -215,11 +217,12 @@ def main():
     lo = np.float32(inf0["a_L"]) - np.float64(105.0 * w.t)
     hi = np.float32(inf0["a_R"]) + np.float64(18.0 * w.t)
     band_n = int(((r >= float(lo)) & (r < float(hi))).sum().item())
-    dom = max((kname for kname in prof if kernel_bytes(kname, n, active, band_n) is not None),
+    ones = math.isfinite(inf0["a_R"])
+    dom = max((kname for kname in prof if kernel_bytes(kname, n, active, band_n, ones) is not None),
               key=lambda kname: prof[kname][1])
     launches, total_ms = prof[dom]
     avg_s = total_ms / launches / 1e3
-    achieved = kernel_bytes(dom, n, active, band_n) / avg_s / 1e9
+    achieved = kernel_bytes(dom, n, active, band_n, ones) / avg_s / 1e9
     kernels = {kname: {"launches": c, "avg_us": 1e3 * ms / c} for kname, (c, ms) in sorted(prof.items())}
 
     model_bytes = 32.0 * n
@@ -249,7 +252,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(dom),
-                     "algorithmic_bytes": kernel_bytes(dom, n, active, band_n)},
+                     "algorithmic_bytes": kernel_bytes(dom, n, active, band_n, ones)},
         "kernels": kernels,
         "bracket": {key: infos[0][key] for key in ("attempts", "fell_back", "n_M", "n_L", "n_R")},
         "active_scores": active,
