@@ -84,13 +84,8 @@ __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __r
     c[e] = h[PER * tid + e];
     loc += c[e];
   }
-  uint32_t incl = loc;
+  uint32_t incl = wave_incl_add<uint32_t>(loc);
   const int lane = lane_id();
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t y = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += y;
-  }
   const int wid = tid / kWave;
   if (lane == kWave - 1) wsum[wid] = incl;
   __syncthreads();
@@ -140,13 +135,8 @@ __device__ void find_bin(const uint32_t* h, int nb, uint32_t rank, uint32_t* wsu
   const int per = nb / kSelThreads;
   uint32_t loc = 0;
   for (int q = 0; q < per; ++q) loc += h[tid * per + q];
-  uint32_t incl = loc;
+  uint32_t incl = wave_incl_add<uint32_t>(loc);
   const int lane = lane_id();
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t x = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += x;
-  }
   const int wid = tid / kWave;
   if (lane == kWave - 1) wsum[wid] = incl;
   __syncthreads();
@@ -253,12 +243,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __r
           st = so[pre];
           cnt = so[pre + 1] - st;
         }
-        uint32_t incl = cnt;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-          const uint32_t y = __shfl_up(incl, o, kWave);
-          if (lane >= o) incl += y;
-        }
+        uint32_t incl = wave_incl_add<uint32_t>(cnt);
         if (lane == kWave - 1) wsum[wid] = incl;
         __syncthreads();
         uint32_t wb = 0u, all = 0u;
@@ -635,20 +620,12 @@ __device__ void partition_totals_block(const PartBlock* __restrict__ blk, int nb
     const int b = Q * tid + q;
     loc += (b < nblocks) ? nm[b] : 0;
   }
-  int64_t incl = loc;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int64_t x = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += x;
-  }
+  int64_t incl = wave_incl_add<int64_t>(loc);
   TL = wave_sum(TL);
   TR = wave_sum(TR);
   const int64_t sL = wave_sum(nL), sR = wave_sum(nR), sO = wave_sum(ov);
-#pragma unroll
-  for (int o = kWave / 2; o >= 1; o >>= 1) {
-    mn = fminf(mn, __shfl_xor(mn, o, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
-  }
+mn = wave_min(mn, INFINITY);
+mx = wave_max(mx, -INFINITY);
   if (lane == kWave - 1) ri[3][wid] = incl;
   if (lane == 0) {
     rd[0][wid] = TL;
@@ -798,11 +775,8 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   const double TR = wave_sum(st.TR);
   const int64_t nR = wave_sum(st.nR);
   float mn = st.mmin, mx = st.mmax;
-#pragma unroll
-  for (int o = kWave / 2; o >= 1; o >>= 1) {
-    mn = fminf(mn, __shfl_xor(mn, o, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
-  }
+mn = wave_min(mn, INFINITY);
+mx = wave_max(mx, -INFINITY);
   if (lane == 0) {
     red_d[0][wid] = TL;
     red_d[1][wid] = TR;

@@ -4,15 +4,18 @@
 //
 // M is cut into 2048 buckets of consecutive order-preserving keys (bucket
 // d = (key - key(max M)) >> shift, so bucket 0 holds the largest scores).
-// Bucket d covers the score interval [u_d, v_d] (its lowest and highest
-// possible float, clamped to the range of M) and is summarised by its count
-// and the two sums
-//     D_d = sum_{r in d} e^{-(r - u_d)/t}    (a prefix pair anchored at u_d)
-//     U_d = sum_{r in d} e^{-(v_d - r)/t}    (a suffix pair anchored at v_d).
-// The shift-carrying scans over the buckets, seeded with the bracket tails,
-// give LapSum at every bucket's upper edge,
-//     LapSum(v_d) = n_above - (1/2) e^{-(u - v_d)/t} S_above
-//                   + (1/2) (U_d + e^{-(v_d - v')/t} T_below),
+// Bucket d covers the scores up to v_d, the highest float it can hold
+// (clamped to the range of M); v_{d+1}, the highest the next bucket can
+// hold, lies below every score of bucket d.  Bucket d is summarised by its
+// count and the two sums
+//     U_d = sum_{r in d} e^{-(v_d - r)/t}       (a suffix pair anchored at v_d)
+//     D_d = sum_{r in d} e^{-(r - v_{d+1})/t}   (a prefix pair anchored at v_{d+1}),
+// so the prefix and the suffix chains move between the same anchors by the
+// same links e^{-(v_d - v_{d+1})/t}, one exponential per bucket.  The
+// shift-carrying scans over the buckets, seeded with the bracket tails, give
+// LapSum at every bucket's upper edge,
+//     LapSum(v_d) = n_above - (1/2) S_above + (1/2) (U_d + e^{-(v_d - v')/t} T_below),
+// with S_above (the buckets before d and the upper tail) anchored at v_d,
 // which is non-decreasing in d; the root lies in the last bucket d* with
 // LapSum(v_d*) <= k (or above every bucket).  Only bucket d* is then sorted
 // (on chip) and solved by block_solve with the scans as carries; the scan
@@ -49,8 +52,9 @@ constexpr int CT = 256;             // bucket_count threads
 constexpr int CG = kBucketGroup;    // partition blocks per count block
 constexpr int CU = 8;               // keys per thread per batch
 constexpr int64_t kGroupKeys = static_cast<int64_t>(CG) * kPartStageCap;   // a count block's region
-constexpr int ST = 256;             // bucket_solve threads
-constexpr int SW = ST / kWave;      // 4 waves
+constexpr int ST = 512;             // bucket_solve threads: two waves per SIMD hide
+                                    // the latency of each other's float64 chains
+constexpr int SW = ST / kWave;      // 8 waves
 constexpr int BPT = kBuckets / ST;  // buckets per thread
 constexpr int SI = kBucketSortCap / ST;   // keys per thread in the largest on-chip sort
 
@@ -68,13 +72,6 @@ __device__ __forceinline__ float bucket_hi(const BucketGeom& g, int d) {
   if (first > g.kmax) return g.mmin;
   return fminf(key_float(static_cast<uint32_t>(first)), g.mmax);
 }
-__device__ __forceinline__ float bucket_lo(const BucketGeom& g, int d) {
-  // lowest score bucket d can hold (its largest key, at most key(min M))
-  const uint64_t last = static_cast<uint64_t>(g.kmin) + ((static_cast<uint64_t>(d) + 1) << g.shift) - 1;
-  const uint32_t key = last < g.kmax ? static_cast<uint32_t>(last) : g.kmax;
-  return fmaxf(key_float(key), g.mmin);
-}
-
 // Bucket geometry from the keys of max M and min M, the same in every
 // block.
 __device__ __forceinline__ BucketGeom geom_of(uint32_t kmin, uint32_t kmax) {
@@ -156,12 +153,9 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
         ov |= hd[q].w;
       }
     }
-#pragma unroll
-    for (int o = kWave / 2; o >= 1; o >>= 1) {
-      kmin = min(kmin, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmin), o, kWave)));
-      kmax = max(kmax, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmax), o, kWave)));
-      ov |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(ov), o, kWave));
-    }
+    kmin = wave_min(kmin, 0xffffffffu);
+    kmax = wave_max(kmax, 0u);
+    ov = wave_or(ov);
     m = wave_sum(m);
     if (lane == 0) {
       rk[0][wid] = kmin;
@@ -185,19 +179,13 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
       ov = rec.overflow;
     }
     nM = nm;
-    int32_t incl = nm;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int32_t y = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += y;
-    }
+    const int32_t incl = wave_incl_add(nm);
     TL = wave_sum(TL);
     TR = wave_sum(TR);
     nL = wave_sum(nL);
     nR = wave_sum(nR);
     nM = wave_sum(nM);
-#pragma unroll
-    for (int o = kWave / 2; o >= 1; o >>= 1) ov |= __shfl_xor(ov, o, kWave);
+    ov = wave_or(ov);
     if (lane == kWave - 1) wtot[wid] = static_cast<uint32_t>(incl);
     if (lane == 0) {
       rd[0][wid] = TL;
@@ -293,8 +281,10 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
         const uint32_t key = kv[u];
         const int d = static_cast<int>((key - g.kmin) >> g.shift);
         const double r = key_float(key);
-        const double up = wexp_f32(static_cast<double>(bucket_hi(g, d)) - r, c2);   // e^{-(v_d - r)/t}
-        const double dn = wexp_f32(r - static_cast<double>(bucket_lo(g, d)), c2);   // e^{-(r - u_d)/t}
+        // e^{-(v_d - r)/t}, and e^{-(r - v_{d+1})/t} anchored at the next
+        // bucket's upper edge (the highest score below bucket d)
+        const double up = wexp_f32(static_cast<double>(bucket_hi(g, d)) - r, c2);
+        const double dn = wexp_f32(r - static_cast<double>(bucket_hi(g, d + 1)), c2);
         atomicAdd(&cn[d], 1u);
         atomicAdd(&cu[d], static_cast<unsigned long long>(__double2ull_rn(up * fscale)));
         atomicAdd(&cd[d], static_cast<unsigned long long>(__double2ull_rn(dn * fscale)));
@@ -310,12 +300,7 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
     uint32_t loc = 0;
 #pragma unroll
     for (int q = 0; q < PER; ++q) loc += cn[b0 + q];
-    uint32_t incl = loc;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const uint32_t y = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += y;
-    }
+    uint32_t incl = wave_incl_add<uint32_t>(loc);
     if (lane == kWave - 1) wtot[wid] = incl;   // (its last readers passed two barriers ago)
     __syncthreads();
     uint32_t run = incl - loc;
@@ -400,9 +385,12 @@ __device__ double sort_and_solve(uint32_t* buf, int c, const BucketGeom& g, doub
 // then in the gap between u, the lowest score with N <= k, and v, the
 // highest with N > k (or a carry's anchor when either side is empty), as in
 // the sorted block solve.
-constexpr int kDirectMax = ST;
+constexpr int kDirectMax = 256;
+constexpr int kDirectTpk = 16;          // at most this many threads per key
+constexpr int kGatherLanes = ST / 32;   // threads per count group in the gather (<= 32 groups)
+constexpr int kGatherBatch = 4;         // keys a gather thread loads at a time
 struct DirectSmem {
-  float4 sv4[kDirectMax / 4 + 1];   // the keys' scores, NaN past the end
+  float4 sv4[(kDirectMax + 4 * kDirectTpk) / 4];   // the keys' scores, NaN past the end
   uint32_t ukey, vkey, has_u, has_v;
   double uA, uc, vB;
 };
@@ -413,11 +401,12 @@ __device__ double direct_solve(const uint32_t* buf, int c, const BucketGeom& g, 
   const double inv_t = 1.0 / t;
   const double c2 = kLog2e / t;
   float* sv = reinterpret_cast<float*>(ds.sv4);
-  // threads per key (adjacent lanes) and the slice of keys each sums, a
-  // multiple of 4 so that it is read as float4; the slices cover
-  // tpk * slice <= kDirectMax + 3 entries, NaN past c (a NaN difference
-  // counts nowhere)
-  const int tpk = c <= kDirectMax / 8 ? 8 : (c <= kDirectMax / 4 ? 4 : (c <= kDirectMax / 2 ? 2 : 1));
+  // threads per key (adjacent lanes, as many as the block holds, at most
+  // kDirectTpk) and the slice of keys each sums, a multiple of 4 so that it
+  // is read as float4; the slices cover tpk * slice < c + 4 tpk entries,
+  // NaN past c (a NaN difference counts nowhere)
+  int tpk = kDirectTpk;
+  while (tpk > 1 && c * tpk > ST) tpk >>= 1;
   const int slice = ((c + tpk - 1) / tpk + 3) & ~3;
   if (tid < c) sv[tid] = key_float(buf[buf_at(tid)] + g.kmin);
   for (int e = c + tid; e < tpk * slice; e += ST) sv[e] = __int_as_float(0x7fc00000);
@@ -467,16 +456,9 @@ __device__ double direct_solve(const uint32_t* buf, int c, const BucketGeom& g, 
   {
     // the lowest score at or below k (largest key) and the highest above k
     // (smallest key): reduced in the wave, then one atomic per wave
-    uint32_t uk = (lead && le) ? key : 0u;
-    uint32_t vk = (lead && !le) ? key : 0xffffffffu;
-    uint32_t hu = (lead && le) ? 1u : 0u, hv = (lead && !le) ? 1u : 0u;
-#pragma unroll
-    for (int o = kWave / 2; o >= 1; o >>= 1) {
-      uk = max(uk, static_cast<uint32_t>(__shfl_xor(static_cast<int>(uk), o, kWave)));
-      vk = min(vk, static_cast<uint32_t>(__shfl_xor(static_cast<int>(vk), o, kWave)));
-      hu |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(hu), o, kWave));
-      hv |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(hv), o, kWave));
-    }
+    const uint32_t uk = wave_max_u32((lead && le) ? key : 0u);
+    const uint32_t vk = wave_min_u32((lead && !le) ? key : 0xffffffffu);
+    const bool hu = __ballot(lead && le) != 0ull, hv = __ballot(lead && !le) != 0ull;
     if (lane_id() == 0) {
       if (hu) {
         atomicMax(&ds.ukey, uk);
@@ -644,44 +626,45 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
   const BucketGeom g = geom_of(parts[0].kmin, parts[0].kmax);
   const double inv_fscale = ldexp(1.0, -fixed_bits(m));
 
-  // 1. this thread's buckets, cleared behind us for the next attempt
+  // 1. this thread's buckets, cleared behind us for the next attempt.  The
+  //    suffix sum of bucket q is anchored at its upper edge v_q and the
+  //    prefix sum at v_{q+1}, the upper edge of the bucket after it, so both
+  //    chains move between anchors by the same links
+  //    wv[q] = e^{-(v_q - v_{q+1})/t}, one exponential per bucket.
   double U[BPT], D[BPT];
-  float v[BPT], u[BPT];
+  float v[BPT + 1];   // v[BPT]: the upper edge of the next thread's first bucket
 #pragma unroll
   for (int q = 0; q < BPT; ++q) {
     U[q] = static_cast<double>(Ur[q]) * inv_fscale;
     D[q] = static_cast<double>(Dr[q]) * inv_fscale;
     v[q] = bucket_hi(g, d0 + q);
-    u[q] = bucket_lo(g, d0 + q);
   }
+  v[BPT] = bucket_hi(g, d0 + BPT);
 #pragma unroll
   for (int q = 0; q < BPT; ++q) {
     acc_n[d0 + q] = 0u;
     acc_u[d0 + q] = 0ull;
     acc_d[d0 + q] = 0ull;
   }
-  // links between consecutive anchors of this thread (all independent)
-  double wu[BPT], wv[BPT];   // wu[q] = e^{-(u_{q-1} - u_q)/t}, wv[q] = e^{-(v_q - v_{q+1})/t}
+  // links between consecutive anchors (all independent)
+  double wv[BPT];
 #pragma unroll
-  for (int q = 0; q < BPT; ++q) {
-    wu[q] = q > 0 ? wexp_f64(static_cast<double>(u[q - 1]) - u[q], inv_t) : 0.0;
-    wv[q] = q + 1 < BPT ? wexp_f64(static_cast<double>(v[q]) - v[q + 1], inv_t) : 0.0;
-  }
+  for (int q = 0; q < BPT; ++q) wv[q] = wexp_f64(static_cast<double>(v[q]) - v[q + 1], inv_t);
   // The prefix pair may sit at any anchor at or above the root, so it
   // chains through the geometric anchors of empty buckets.  A suffix pair
   // is anchored at the upper edge of a non-empty bucket: the root lies above
   // the upper edge of the first non-empty bucket after the crossing, but can
   // lie below the edge of an empty bucket in between.
-  double Pm = 0.0;   // prefix pair of the thread, anchored at u[BPT-1]
+  double Pm = 0.0;   // prefix pair of the thread, anchored at v[BPT]
   int64_t mine = 0;
 #pragma unroll
   for (int q = 0; q < BPT; ++q) {
-    Pm = fma(wu[q], Pm, D[q]);
+    Pm = fma(wv[q], Pm, D[q]);
     mine += cnt[q];
   }
   double Tl[BPT];    // suffix within the thread from bucket q, anchored at v[q]
 #pragma unroll
-  for (int q = BPT - 1; q >= 0; --q) Tl[q] = fma(wv[q], q + 1 < BPT ? Tl[q + 1] : 0.0, U[q]);
+  for (int q = BPT - 1; q >= 0; --q) Tl[q] = q + 1 < BPT ? fma(wv[q], Tl[q + 1], U[q]) : U[q];
   Suf mys = suf_empty();   // anchored at the first non-empty bucket of the thread
 #pragma unroll
   for (int q = BPT - 1; q >= 0; --q)
@@ -690,14 +673,10 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
   // 2. block scans, seeded with the tails
   Pre pre_all;
   Suf suf_all;
-  const Pre pre_in = block_excl_pre<SW>(Pre{u[BPT - 1], Pm}, x.pre, inv_t, csm, &pre_all);
+  const Pre pre_in = block_excl_pre<SW>(Pre{v[BPT], Pm}, x.pre, inv_t, csm, &pre_all);
   const Suf suf_in = block_excl_suf<SW>(mys, x.suf, inv_t, csm, &suf_all);
-  int64_t incl = mine;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int64_t y = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += y;
-  }
+  // |M| < 2^31, so the counts scan in 32 bits
+  const int64_t incl = static_cast<int64_t>(wave_incl_add(static_cast<uint32_t>(mine)));
   if (lane == kWave - 1) cw[wid] = incl;
   __syncthreads();
   int64_t above = incl - mine;
@@ -707,7 +686,10 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
 
   // 3. suffix sums from each bucket on (anchored at its v), right to left,
   //    then LapSum at each non-empty bucket's upper edge, left to right:
-  //    LapSum(v_q) = n_R + above_q - (1/2) e^{-(u_prev - v_q)/t} P_before + (1/2) T_q
+  //    LapSum(v_q) = n_R + above_q - (1/2) e^{-(a - v_q)/t} P_before + (1/2) T_q
+  //    with P_before anchored at a, which is v_q itself (weight 1) unless
+  //    the prefix still sits on the seed's anchor.  Moving P past bucket q
+  //    takes the link wv[q] in the same case.
   double T[BPT];
   {
     double tn = suf_in.T;
@@ -726,22 +708,20 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     int64_t ab = above;
 #pragma unroll
     for (int q = 0; q < BPT; ++q) {
+      const bool at_v = pu == v[q];
       if (cnt[q]) {
         double lap = x.nR + static_cast<double>(ab) + 0.5 * T[q];
-        if (P != 0.0) lap -= 0.5 * wexp_f64(static_cast<double>(pu) - v[q], inv_t) * P;
+        if (P != 0.0) lap -= 0.5 * (at_v ? P : wexp_f64(static_cast<double>(pu) - v[q], inv_t) * P);
         if (lap <= k) below = d0 + q + 1;
       }
-      const double w = (P != 0.0) ? wexp_f64(static_cast<double>(pu) - u[q], inv_t) : 0.0;
+      const double w = (P != 0.0) ? (at_v ? wv[q] : wexp_f64(static_cast<double>(pu) - v[q + 1], inv_t))
+                                  : 0.0;
       P = fma(w, P, D[q]);
-      pu = u[q];
+      pu = v[q + 1];
       ab += cnt[q];
     }
   }
-#pragma unroll
-  for (int o = kWave / 2; o >= 1; o >>= 1) {
-    const int64_t y = __shfl_xor(below, o, kWave);
-    below = y > below ? y : below;
-  }
+  below = static_cast<int64_t>(wave_max_u32(static_cast<uint32_t>(below)));
   if (lane == 0) red_i[wid] = below;
   if (tid == 0) gathered_s = 0u;
   __syncthreads();
@@ -767,9 +747,11 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
         cabove_s = ab;
         ccount_s = cnt[q];
       }
-      const double w = (P != 0.0) ? wexp_f64(static_cast<double>(pu) - u[q], inv_t) : 0.0;
+      const double w = (P != 0.0) ? (pu == v[q] ? wv[q]
+                                                : wexp_f64(static_cast<double>(pu) - v[q + 1], inv_t))
+                                  : 0.0;
       P = fma(w, P, D[q]);
-      pu = u[q];
+      pu = v[q + 1];
       ab += cnt[q];
     }
   }
@@ -792,14 +774,31 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     //    keys relative to key(max M), whose low `shift` bits order the
     //    bucket (the order in LDS is irrelevant: it is sorted next)
     //    (a group with no members wrote no offsets)
-    if (tid < ngroups && gcount_s[tid] > 0) {
-      const uint32_t* bo = boff + static_cast<int64_t>(tid) * (kBuckets + 1);
-      const uint32_t from = bo[dstar];
-      const uint32_t cnt_b = bo[dstar + 1] - from;
-      const uint32_t* bk = bkeys + static_cast<int64_t>(tid) * kGroupKeys + from;
-      for (uint32_t j = 0; j < cnt_b; ++j) {
-        const uint32_t at = atomicAdd(&gathered_s, 1u);
-        if (at < static_cast<uint32_t>(kBucketSortCap)) buf[buf_at(static_cast<int>(at))] = bk[j] - g.kmin;
+    //    (kGatherLanes threads per group, each loading its keys before
+    //    placing any)
+    {
+      const int grp = tid / kGatherLanes;
+      const int sub = tid % kGatherLanes;
+      if (grp < ngroups && gcount_s[grp] > 0) {
+        const uint32_t* bo = boff + static_cast<int64_t>(grp) * (kBuckets + 1);
+        const uint32_t from = bo[dstar];
+        const uint32_t cnt_b = bo[dstar + 1] - from;
+        const uint32_t* bk = bkeys + static_cast<int64_t>(grp) * kGroupKeys + from;
+        for (uint32_t j0 = 0; j0 < cnt_b; j0 += kGatherLanes * kGatherBatch) {
+          uint32_t kv[kGatherBatch];
+#pragma unroll
+          for (int u = 0; u < kGatherBatch; ++u) {
+            const uint32_t j = j0 + static_cast<uint32_t>(u * kGatherLanes + sub);
+            kv[u] = bk[j < cnt_b ? j : 0];
+          }
+#pragma unroll
+          for (int u = 0; u < kGatherBatch; ++u) {
+            if (j0 + static_cast<uint32_t>(u * kGatherLanes + sub) < cnt_b) {
+              const uint32_t at = atomicAdd(&gathered_s, 1u);
+              if (at < static_cast<uint32_t>(kBucketSortCap)) buf[buf_at(static_cast<int>(at))] = kv[u] - g.kmin;
+            }
+          }
+        }
       }
     }
     __syncthreads();
@@ -807,8 +806,8 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     const double rank0 = x.nR + static_cast<double>(cabove_s);
     if (c <= kDirectMax)
       b = direct_solve(buf, c, g, rank0, cpre_s, csuf_s, k, t, dsm);
-    else if (c <= 4 * ST)
-      b = sort_and_solve<4>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
+    else if (c <= 2 * ST)
+      b = sort_and_solve<2>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
     else
       b = sort_and_solve<SI>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
   }

@@ -108,36 +108,130 @@ __device__ __forceinline__ Suf suf_combine(Suf a, Suf b, double inv_t) {
 // ------------------------------------------------------------ wave scans ---
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
-// inclusive, left to right: lane l gets x_0 (+) ... (+) x_l
-__device__ __forceinline__ Pre wave_incl_pre(Pre x, double inv_t) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    float ou = __shfl_up(x.u, d, kWave);
-    double oS = __shfl_up(x.S, d, kWave);
-    if (lane >= d) x = pre_combine(Pre{ou, oS}, x, inv_t);
+// Cross-lane moves within rows of 16 lanes (DPP): lane l takes the value of
+// the lane the control names in its row; a lane whose source lies outside
+// the row keeps `id`.  Controls used: row_shr:d = 0x110 + d (source l - d),
+// row_shl:d = 0x100 + d (source l + d).  No LDS traffic, unlike a shuffle.
+// Every helper below needs the whole wave active.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x, uint32_t id) {
+  return static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(static_cast<int>(id), static_cast<int>(x), CTRL, 0xf, 0xf, false));
+}
+template <int CTRL, typename T>
+__device__ __forceinline__ T dpp_move(T x, T id) {
+  static_assert(sizeof(T) == 4 || sizeof(T) == 8, "32- or 64-bit values");
+  if constexpr (sizeof(T) == 4) {
+    return __builtin_bit_cast(T, dpp_u32<CTRL>(__builtin_bit_cast(uint32_t, x),
+                                               __builtin_bit_cast(uint32_t, id)));
+  } else {
+    const uint64_t xb = __builtin_bit_cast(uint64_t, x);
+    const uint64_t ib = __builtin_bit_cast(uint64_t, id);
+    const uint32_t lo = dpp_u32<CTRL>(static_cast<uint32_t>(xb), static_cast<uint32_t>(ib));
+    const uint32_t hi = dpp_u32<CTRL>(static_cast<uint32_t>(xb >> 32), static_cast<uint32_t>(ib >> 32));
+    return __builtin_bit_cast(T, (static_cast<uint64_t>(hi) << 32) | lo);
   }
-  return x;
+}
+template <typename T>
+__device__ __forceinline__ T readlane_as(T x, int l) {
+  static_assert(sizeof(T) == 4 || sizeof(T) == 8, "32- or 64-bit values");
+  if constexpr (sizeof(T) == 4) {
+    return __builtin_bit_cast(
+        T, static_cast<uint32_t>(__builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l)));
+  } else {
+    const uint64_t xb = __builtin_bit_cast(uint64_t, x);
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(xb), l));
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(xb >> 32), l));
+    return __builtin_bit_cast(T, (static_cast<uint64_t>(hi) << 32) | lo);
+  }
 }
 
-// inclusive, right to left: lane l gets x_l (+) ... (+) x_63
-__device__ __forceinline__ Suf wave_incl_suf(Suf x, double inv_t) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    float ov = __shfl_down(x.v, d, kWave);
-    double oT = __shfl_down(x.T, d, kWave);
-    if (lane + d < kWave) x = suf_combine(x, Suf{ov, oT}, inv_t);
-  }
-  return x;
+// Reduction over the wave in a fixed order, the result in every lane:
+// partial results inside each row of 16 lanes, then the four rows as
+// (r0 op r1) op (r2 op r3).
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, T id, Op op) {
+  v = op(v, dpp_move<0x111>(v, id));
+  v = op(v, dpp_move<0x112>(v, id));
+  v = op(v, dpp_move<0x114>(v, id));
+  v = op(v, dpp_move<0x118>(v, id));
+  return op(op(readlane_as(v, 15), readlane_as(v, 31)), op(readlane_as(v, 47), readlane_as(v, 63)));
 }
-
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
-#pragma unroll
-  for (int d = kWave / 2; d >= 1; d >>= 1) v += __shfl_xor(v, d, kWave);
-  return v;
+  return wave_reduce(v, T(0), [](T a, T b) { return a + b; });
 }
+template <typename T>
+__device__ __forceinline__ T wave_max(T v, T id) {
+  return wave_reduce(v, id, [](T a, T b) { return a > b ? a : b; });
+}
+template <typename T>
+__device__ __forceinline__ T wave_min(T v, T id) {
+  return wave_reduce(v, id, [](T a, T b) { return a < b ? a : b; });
+}
+template <typename T>
+__device__ __forceinline__ T wave_or(T v) {
+  return wave_reduce(v, T(0), [](T a, T b) { return a | b; });
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) { return wave_max(x, 0u); }
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) { return wave_min(x, 0xffffffffu); }
+
+// Inclusive sum over lanes 0 .. l.
+template <typename T>
+__device__ __forceinline__ T wave_incl_add(T x) {
+  x += dpp_move<0x111>(x, T(0));
+  x += dpp_move<0x112>(x, T(0));
+  x += dpp_move<0x114>(x, T(0));
+  x += dpp_move<0x118>(x, T(0));
+  const T r0 = readlane_as(x, 15), r1 = readlane_as(x, 31), r2 = readlane_as(x, 47);
+  const int row = lane_id() >> 4;
+  return x + (row == 0 ? T(0) : (row == 1 ? r0 : (row == 2 ? r0 + r1 : r0 + r1 + r2)));
+}
+
+// Affine maps x -> A x + B composed along the wave.  Left to right, lane l
+// ends with x_l o ... o x_0 (apply lane 0's map first); right to left, with
+// x_l o ... o x_63.  Hillis-Steele inside each row of 16, then every row
+// takes the composition of the rows before (after) it from lanes read out
+// as scalars.
+#define LAPSUM_AFFINE_STEP(C)                                                  \
+  {                                                                            \
+    const double eA = dpp_move<C>(A, 1.0), eB = dpp_move<C>(B, 0.0);           \
+    B = fma(A, eB, B);                                                         \
+    A *= eA;                                                                   \
+  }
+__device__ __forceinline__ void wave_affine_up(double& A, double& B) {
+  LAPSUM_AFFINE_STEP(0x111)
+  LAPSUM_AFFINE_STEP(0x112)
+  LAPSUM_AFFINE_STEP(0x114)
+  LAPSUM_AFFINE_STEP(0x118)
+  const double a0 = readlane_as(A, 15), b0 = readlane_as(B, 15);
+  const double a1 = readlane_as(A, 31), b1 = readlane_as(B, 31);
+  const double a2 = readlane_as(A, 47), b2 = readlane_as(B, 47);
+  const double e2A = a1 * a0, e2B = fma(a1, b0, b1);
+  const double e3A = a2 * e2A, e3B = fma(a2, e2B, b2);
+  const int row = lane_id() >> 4;
+  const double eA = row == 0 ? 1.0 : (row == 1 ? a0 : (row == 2 ? e2A : e3A));
+  const double eB = row == 0 ? 0.0 : (row == 1 ? b0 : (row == 2 ? e2B : e3B));
+  B = fma(A, eB, B);
+  A *= eA;
+}
+__device__ __forceinline__ void wave_affine_down(double& A, double& B) {
+  LAPSUM_AFFINE_STEP(0x101)
+  LAPSUM_AFFINE_STEP(0x102)
+  LAPSUM_AFFINE_STEP(0x104)
+  LAPSUM_AFFINE_STEP(0x108)
+  const double a1 = readlane_as(A, 16), b1 = readlane_as(B, 16);
+  const double a2 = readlane_as(A, 32), b2 = readlane_as(B, 32);
+  const double a3 = readlane_as(A, 48), b3 = readlane_as(B, 48);
+  const double e1A = a2 * a3, e1B = fma(a2, b3, b2);
+  const double e0A = a1 * e1A, e0B = fma(a1, e1B, b1);
+  const int row = lane_id() >> 4;
+  const double eA = row == 3 ? 1.0 : (row == 2 ? a3 : (row == 1 ? e1A : e0A));
+  const double eB = row == 3 ? 0.0 : (row == 2 ? b3 : (row == 1 ? e1B : e0B));
+  B = fma(A, eB, B);
+  A *= eA;
+}
+#undef LAPSUM_AFFINE_STEP
 
 // Scratch for the block-level scans and the crossing search.
 template <int WAVES>
@@ -173,48 +267,34 @@ __device__ Pre block_excl_pre(Pre x, Pre carry, double inv_t, ScanSmem<WAVES>& s
   const int wid = threadIdx.x / kWave;
   const bool has = x.S != 0.0;
   const bool chas = carry.S != 0.0;
-  // 1. anchor of the last non-empty group up to each thread
-  int lh = has ? 1 : 0;
-  float lu = x.u;
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const int oh = __shfl_up(lh, d, kWave);
-    const float ou = __shfl_up(lu, d, kWave);
-    if (lane >= d && !lh && oh) {
-      lh = 1;
-      lu = ou;
-    }
-  }
-  if (lane == kWave - 1) {
-    sm.ah[wid] = lh;
+  // 1. anchor of the last non-empty group before each thread (ballot)
+  const uint64_t hm = __ballot(has);
+  const float lu = __shfl(x.u, hm != 0ull ? 63 - __clzll(hm) : 0, kWave);
+  if (lane == 0) {
+    sm.ah[wid] = hm != 0ull ? 1 : 0;
     sm.au[wid] = lu;
   }
+  const uint64_t before = hm & ((1ull << lane) - 1ull);
+  const float bu = __shfl(x.u, before ? 63 - __clzll(before) : 0, kWave);
   __syncthreads();
-  int wh = chas ? 1 : 0;   // the anchor entering this wave
-  float wu = carry.u;
-  for (int w = 0; w < wid; ++w)
-    if (sm.ah[w]) {
-      wh = 1;
-      wu = sm.au[w];
+  // the anchor entering this wave (every wave's record read at once)
+  int eh = chas ? 1 : 0;
+  float eu = carry.u;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    const int h = sm.ah[w];
+    const float a = sm.au[w];
+    if (w < wid && h) {
+      eh = 1;
+      eu = a;
     }
-  int ph = __shfl_up(lh, 1, kWave);
-  float pu = __shfl_up(lu, 1, kWave);
-  if (lane == 0 || !ph) {
-    ph = wh;
-    pu = wu;
   }
+  const int ph = before != 0ull ? 1 : eh;
+  const float pu = before != 0ull ? bu : eu;
   // 2. P_i = A_i P_{i-1} + B_i
   double A = has ? (ph ? wexp_f64(static_cast<double>(pu) - static_cast<double>(x.u), inv_t) : 0.0) : 1.0;
   double B = has ? x.S : 0.0;
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const double Ap = __shfl_up(A, d, kWave);
-    const double Bp = __shfl_up(B, d, kWave);
-    if (lane >= d) {
-      B = fma(A, Bp, B);
-      A *= Ap;
-    }
-  }
+  wave_affine_up(A, B);
   if (lane == kWave - 1) {
     sm.A[wid] = A;
     sm.B[wid] = B;
@@ -222,7 +302,11 @@ __device__ Pre block_excl_pre(Pre x, Pre carry, double inv_t, ScanSmem<WAVES>& s
   __syncthreads();
   const double P_in = chas ? carry.S : 0.0;
   double P0 = P_in;   // P entering this wave
-  for (int w = 0; w < wid; ++w) P0 = fma(sm.A[w], P0, sm.B[w]);
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    const double Aw = sm.A[w], Bw = sm.B[w];
+    if (w < wid) P0 = fma(Aw, P0, Bw);
+  }
   double Pt = P_in;
   int th = chas ? 1 : 0;
   float tu = carry.u;
@@ -251,48 +335,34 @@ __device__ Suf block_excl_suf(Suf x, Suf carry, double inv_t, ScanSmem<WAVES>& s
   const int wid = threadIdx.x / kWave;
   const bool has = x.T != 0.0;
   const bool chas = carry.T != 0.0;
-  // 1. anchor of the first non-empty group from each thread on
-  int lh = has ? 1 : 0;
-  float lv = x.v;
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const int oh = __shfl_down(lh, d, kWave);
-    const float ov = __shfl_down(lv, d, kWave);
-    if (lane + d < kWave && !lh && oh) {
-      lh = 1;
-      lv = ov;
-    }
-  }
+  // 1. anchor of the first non-empty group after each thread (ballot)
+  const uint64_t hm = __ballot(has);
+  const float fv = __shfl(x.v, hm != 0ull ? __ffsll(static_cast<long long>(hm)) - 1 : 0, kWave);
   if (lane == 0) {
-    sm.ah[wid] = lh;
-    sm.au[wid] = lv;
+    sm.ah[wid] = hm != 0ull ? 1 : 0;
+    sm.au[wid] = fv;
   }
+  const uint64_t after = lane == kWave - 1 ? 0ull : hm & (~0ull << (lane + 1));
+  const float av = __shfl(x.v, after ? __ffsll(static_cast<long long>(after)) - 1 : 0, kWave);
   __syncthreads();
-  int wh = chas ? 1 : 0;   // the anchor following this wave
-  float wv = carry.v;
-  for (int w = WAVES - 1; w > wid; --w)
-    if (sm.ah[w]) {
-      wh = 1;
-      wv = sm.au[w];
+  // the anchor following this wave (every wave's record read at once)
+  int fh = chas ? 1 : 0;
+  float fv2 = carry.v;
+#pragma unroll
+  for (int w = WAVES - 1; w >= 0; --w) {
+    const int h = sm.ah[w];
+    const float a = sm.au[w];
+    if (w > wid && h) {
+      fh = 1;
+      fv2 = a;
     }
-  int nh = __shfl_down(lh, 1, kWave);
-  float nv = __shfl_down(lv, 1, kWave);
-  if (lane == kWave - 1 || !nh) {
-    nh = wh;
-    nv = wv;
   }
+  const int nh = after != 0ull ? 1 : fh;
+  const float nv = after != 0ull ? av : fv2;
   // 2. T_i = B_i + A_i T_{i+1}
   double A = has ? (nh ? wexp_f64(static_cast<double>(x.v) - static_cast<double>(nv), inv_t) : 0.0) : 1.0;
   double B = has ? x.T : 0.0;
-#pragma unroll
-  for (int d = 1; d < kWave; d <<= 1) {
-    const double An = __shfl_down(A, d, kWave);
-    const double Bn = __shfl_down(B, d, kWave);
-    if (lane + d < kWave) {
-      B = fma(A, Bn, B);
-      A *= An;
-    }
-  }
+  wave_affine_down(A, B);
   if (lane == 0) {
     sm.A[wid] = A;
     sm.B[wid] = B;
@@ -300,7 +370,11 @@ __device__ Suf block_excl_suf(Suf x, Suf carry, double inv_t, ScanSmem<WAVES>& s
   __syncthreads();
   const double T_in = chas ? carry.T : 0.0;
   double T0 = T_in;   // T following this wave
-  for (int w = WAVES - 1; w > wid; --w) T0 = fma(sm.A[w], T0, sm.B[w]);
+#pragma unroll
+  for (int w = WAVES - 1; w >= 0; --w) {
+    const double Aw = sm.A[w], Bw = sm.B[w];
+    if (w > wid) T0 = fma(Aw, T0, Bw);
+  }
   double Tt = T_in;
   int th = chas ? 1 : 0;
   float tv = carry.v;
