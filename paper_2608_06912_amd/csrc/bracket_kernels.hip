@@ -37,8 +37,9 @@ constexpr int PW = PT / kWave;                 // 4 waves
 // Block b draws samples [b SB, b SB + SB) (kSampleItems per thread, all loads
 // in flight together) and writes their keys grouped by the top 11 bits
 // (kSelectBins bins, any order inside a bin) into its own region of ykeys,
-// with the exclusive bin offsets soffs[b (kSelectBins + 1) + bin] and the bin
-// counts packed two to a word (16 bits each) in scnt[b kSelectBins / 2 + i];
+// with the exclusive bin offsets soffs[b (kSelectBins + 1) + bin], the bin
+// counts packed two to a word (16 bits each) in scnt[b kSampleCntWords + i]
+// and after them the counts of the kSelectGroups groups of consecutive bins;
 // nothing needs to be zero beforehand.  The blocks also clear `zero`
 // (zero_words u32), which later passes accumulate into.
 __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __restrict__ r,
@@ -90,9 +91,23 @@ __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __r
   if (lane == kWave - 1) wsum[wid] = incl;
   __syncthreads();
   uint32_t run = incl - loc;
-  for (int w = 0; w < wid; ++w) run += wsum[w];
+#pragma unroll
+  for (int w = 0; w < kSampleThreads / kWave; ++w) {
+    const uint32_t x = wsum[w];
+    run += w < wid ? x : 0u;
+  }
   uint32_t* so = soffs + static_cast<int64_t>(blockIdx.x) * (kSelectBins + 1);
-  uint32_t* sc = scnt + static_cast<int64_t>(blockIdx.x) * (kSelectBins / 2);
+  uint32_t* sc = scnt + static_cast<int64_t>(blockIdx.x) * kSampleCntWords;
+  {
+    // the count of each group of kSelectBins / kSelectGroups bins (the
+    // bins of TPG adjacent threads)
+    constexpr int TPG = kSelectBins / kSelectGroups / PER;
+    static_assert(TPG >= 1 && TPG <= 4 && (TPG & (TPG - 1)) == 0, "a group is 1, 2 or 4 threads' bins");
+    uint32_t gsum = loc;
+    if (TPG >= 2) gsum += __shfl_xor(gsum, 1, kWave);
+    if (TPG >= 4) gsum += __shfl_xor(gsum, 2, kWave);
+    if (tid % TPG == 0) sc[kSelectBins / 2 + tid / TPG] = gsum;
+  }
 #pragma unroll
   for (int e = 0; e < PER; ++e) {
     h[PER * tid + e] = run;
@@ -141,7 +156,11 @@ __device__ void find_bin(const uint32_t* h, int nb, uint32_t rank, uint32_t* wsu
   if (lane == kWave - 1) wsum[wid] = incl;
   __syncthreads();
   uint32_t base = 0;
-  for (int w = 0; w < wid; ++w) base += wsum[w];
+#pragma unroll
+  for (int w = 0; w < kSelThreads / kWave; ++w) {
+    const uint32_t x = wsum[w];
+    base += w < wid ? x : 0u;
+  }
   uint32_t c = base + incl - loc;   // exclusive count before my first bin
   for (int q = 0; q < per; ++q) {
     const uint32_t v = h[tid * per + q];
@@ -155,6 +174,7 @@ __device__ void find_bin(const uint32_t* h, int nb, uint32_t rank, uint32_t* wsu
 }
 
 constexpr int kCand = 4096;   // candidates per target kept in LDS
+constexpr int kFewCand = 256;   // a bin this small is ranked directly
 
 // Histogram (into h, nb bins) of (key >> lo) & mask over the keys whose
 // bits above `hi` equal `prefix`.
@@ -172,23 +192,30 @@ __device__ void prefix_hist(const uint32_t* keys, int64_t count, int hi, uint32_
 
 // One workgroup.  Targets are 1-based ranks among the K sample keys; a rank
 // outside 1..K gives -inf (below) or +inf (above).  Level 1 (top 11 bits)
-// sums the sample blocks' bin counts; the keys of each target's bin are then
-// fetched from every block's region (only that bin) into LDS, where bits
-// 10..20 and 0..9 are resolved.  A bin too large for LDS is resolved by
-// passes over all keys in memory.
-constexpr int kSelBatch = 64;   // sample blocks whose counts one thread loads at once
+// locates each target's group of bins from the sample blocks' group counts,
+// then its bin from the bin counts of that group only.  A bin of at most
+// kFewCand keys is
+// gathered into LDS in any order and its key of the target rank found by
+// counting; otherwise the bin's keys are fetched from every block's region
+// (only that bin) into LDS, where bits 10..20 and 0..9 are resolved, and a
+// bin too large for LDS is resolved by passes over all keys in memory.
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __restrict__ ykeys,
                                                              int64_t K,
                                                              const uint32_t* __restrict__ soffs,
                                                              const uint32_t* __restrict__ scnt,
                                                              int nsb, int64_t j, int64_t l,
                                                              SelectRec* __restrict__ out) {
-  __shared__ uint32_t h1[kSelectBins];   // level-1 counts (kept for both targets)
+  __shared__ uint32_t hc[kSelectGroups];   // group counts over all blocks
+  __shared__ uint32_t hf[2][kSelectBins / kSelectGroups];   // bin counts of each target's group
+  __shared__ int grp_s[2], pre_s[2];
+  __shared__ uint32_t grank_s[2], rk_s[2], tot_s[2];
   __shared__ uint32_t h[kSelectBins];
   __shared__ uint32_t wsum[kSelThreads / kWave];
   __shared__ int bin_s;
   __shared__ uint32_t rank_s;
-  __shared__ uint32_t cand[kCand];
+  __shared__ uint32_t ncand_s;
+  __shared__ uint32_t key_s;
+  __shared__ __align__(16) uint32_t cand[kCand];
   __shared__ uint32_t bst[kSelThreads];    // per sample block: start of the bin in its region
   __shared__ uint32_t bpre[kSelThreads + 1];   // exclusive prefix of the bin's counts over blocks
   const int tid = threadIdx.x;
@@ -199,39 +226,130 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __r
   uint32_t key_out[2] = {0u, 0u};
   for (int q = 0; q < 2; ++q) live[q] = (tgt[q] >= 1 && tgt[q] <= K);
 
-  // 1. bin counts summed over the sample blocks: thread tid takes bins 2 tid
-  //    and 2 tid + 1, one packed word per block (kSelBatch blocks' loads in
-  //    flight at a time)
+  // 1. each live target's bin and its rank inside the bin: the group counts
+  //    summed over the sample blocks locate the group, then the bin counts
+  //    of that group only
   {
-    static_assert(kSelectBins == 2 * kSelThreads, "two bins per select thread");
-    uint32_t c0 = 0u, c1 = 0u;
-    for (int b0 = 0; b0 < nsb; b0 += kSelBatch) {
-      uint32_t wv[kSelBatch];
-#pragma unroll
-      for (int u = 0; u < kSelBatch; ++u) {
-        const int b = b0 + u < nsb ? b0 + u : nsb - 1;
-        wv[u] = scnt[static_cast<int64_t>(b) * (kSelectBins / 2) + tid];
-      }
-#pragma unroll
-      for (int u = 0; u < kSelBatch; ++u)
-        if (b0 + u < nsb) {
-          c0 += wv[u] & 0xffffu;
-          c1 += wv[u] >> 16;
-        }
+    constexpr int GB = kSelectBins / kSelectGroups;   // bins per group
+    static_assert(kSelectGroups == kWave && GB <= kWave && GB % 2 == 0, "one lane per group or bin");
+    if (tid < kSelectGroups) hc[tid] = 0u;
+    if (tid < 2 * GB) hf[tid / GB][tid % GB] = 0u;
+    __syncthreads();
+    {
+      const int gi = tid % kSelectGroups;
+      uint32_t sum = 0u;
+      for (int b = tid / kSelectGroups; b < nsb; b += kSelThreads / kSelectGroups)
+        sum += scnt[static_cast<int64_t>(b) * kSampleCntWords + kSelectBins / 2 + gi];
+      if (sum) atomicAdd(&hc[gi], sum);
     }
-    h1[2 * tid] = c0;
-    h1[2 * tid + 1] = c1;
+    __syncthreads();
+    if (wid == 0) {
+      const uint32_t v = hc[lane];
+      const uint32_t incl = wave_incl_add<uint32_t>(v);
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const uint32_t t = static_cast<uint32_t>(live[q] ? tgt[q] : 1);
+        if (incl - v < t && t <= incl) {
+          grp_s[q] = lane;
+          grank_s[q] = t - (incl - v);
+        }
+      }
+    }
+    __syncthreads();
+    {
+      // GB / 2 packed words of the group per block, both targets at once
+      constexpr int WPG = GB / 2;
+      const int wi = tid % WPG;
+      for (int b = tid / WPG; b < nsb; b += kSelThreads / WPG) {
+        const uint32_t* sc = scnt + static_cast<int64_t>(b) * kSampleCntWords;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          if (!live[q]) continue;
+          const uint32_t wv = sc[grp_s[q] * WPG + wi];
+          if (wv & 0xffffu) atomicAdd(&hf[q][2 * wi], wv & 0xffffu);
+          if (wv >> 16) atomicAdd(&hf[q][2 * wi + 1], wv >> 16);
+        }
+      }
+    }
+    __syncthreads();
+    if (wid == 0) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        if (!live[q]) continue;
+        const uint32_t v = lane < GB ? hf[q][lane] : 0u;
+        const uint32_t incl = wave_incl_add<uint32_t>(v);
+        const uint32_t t = grank_s[q];
+        if (lane < GB && incl - v < t && t <= incl) {
+          pre_s[q] = grp_s[q] * GB + lane;
+          rk_s[q] = t - (incl - v);
+          tot_s[q] = v;
+        }
+      }
+    }
+    __syncthreads();
   }
-  __syncthreads();
 
   for (int q = 0; q < 2; ++q) {
     if (!live[q]) continue;   // the same in every thread
-    find_bin(h1, kSelectBins, static_cast<uint32_t>(tgt[q]), wsum, &bin_s, &rank_s);
-    const uint32_t pre = static_cast<uint32_t>(bin_s);
-    const uint32_t rk = rank_s;
-    const uint32_t total = h1[pre];
+    const uint32_t pre = static_cast<uint32_t>(pre_s[q]);
+    const uint32_t rk = rk_s[q];
+    const uint32_t total = tot_s[q];
     const uint32_t* src = ykeys;
     int64_t count = K;
+    if (total <= static_cast<uint32_t>(kFewCand)) {
+      // 2'. a small bin: its keys from every block's region in any order,
+      //     then the key of rank rk among them by counting (ties share a
+      //     value, so any holder of the rank may write it)
+      if (tid == 0) ncand_s = 0u;
+      // tpb threads per sample block (a power of two), each taking every
+      // tpb-th key of the block's part of the bin
+      int tpb = kSelThreads;
+      while (tpb > 1 && tpb * nsb > kSelThreads) tpb >>= 1;
+      __syncthreads();
+      for (int b = tid / tpb; b < nsb; b += kSelThreads / tpb) {
+        const uint32_t* so = soffs + static_cast<int64_t>(b) * (kSelectBins + 1);
+        const uint32_t st = so[pre];
+        const uint32_t cnt = so[pre + 1] - st;
+        const uint32_t* yk = ykeys + static_cast<int64_t>(b) * kSampleBlock + st;
+        for (uint32_t e = static_cast<uint32_t>(tid % tpb); e < cnt; e += static_cast<uint32_t>(tpb)) {
+          const uint32_t key = yk[e];
+          const uint32_t at = atomicAdd(&ncand_s, 1u);
+          if (at < static_cast<uint32_t>(kFewCand)) cand[at] = key;
+        }
+      }
+      __syncthreads();
+      {
+        // tpc adjacent threads per candidate, each counting a slice of the
+        // candidates (a multiple of 4, read four at a time; slots past
+        // `total` never count), joined across the candidate's threads
+        int tpc = kWave / 4;
+        while (tpc > 1 && tpc * static_cast<int>(total) > kSelThreads) tpc >>= 1;
+        const int slice = ((static_cast<int>(total) + tpc - 1) / tpc + 3) & ~3;
+        const int ci = tid / tpc;
+        const int part = tid % tpc;
+        const uint32_t x = cand[ci < static_cast<int>(total) ? ci : 0];
+        uint32_t below = 0u, same = 0u;
+        for (int e0 = part * slice; e0 < (part + 1) * slice; e0 += 4) {
+          const uint4 y4 = *reinterpret_cast<const uint4*>(&cand[e0]);
+          const uint32_t y[4] = {y4.x, y4.y, y4.z, y4.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const bool in = e0 + u < static_cast<int>(total);
+            below += (in && y[u] < x) ? 1u : 0u;
+            same += (in && y[u] == x) ? 1u : 0u;
+          }
+        }
+        for (int o = 1; o < tpc; o <<= 1) {
+          below += __shfl_xor(below, o, kWave);
+          same += __shfl_xor(same, o, kWave);
+        }
+        if (ci < static_cast<int>(total) && part == 0 && below < rk && rk <= below + same) key_s = x;
+      }
+      __syncthreads();
+      key_out[q] = key_s;
+      __syncthreads();
+      continue;
+    }
     if (total <= static_cast<uint32_t>(kCand)) {
       // 2. the bin's keys from every block's region, in block order
       uint32_t run = 0u;   // keys fetched so far (same in every thread)

@@ -19,6 +19,8 @@ constexpr int kPartThreads = 256;
 constexpr int kPartMaxBlocks = 4096;   // blocks of the streaming partition
 constexpr int kPartStageCap = 960;     // M entries a partition block stages (LDS: 5 blocks per CU)
 constexpr int kSelectBins = 2048;      // 11-bit digits of the order-statistic select
+constexpr int kSelectGroups = 64;      // coarse groups of kSelectBins / kSelectGroups bins
+constexpr int kSampleCntWords = kSelectBins / 2 + kSelectGroups;   // scnt words per sample block
 
 // Threshold record written by the device-wide solve (one per row).
 struct SolveRec {
@@ -192,8 +194,9 @@ hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s);
 
 // Bracketed pipeline.
 // ykeys: [K]; soffs: [sample_blocks(K) * (kSelectBins + 1)]; scnt:
-// [sample_blocks(K) * kSelectBins / 2]; the sample also clears
-// zero[0 .. zero_words) for passes that accumulate later.
+// [sample_blocks(K) * kSampleCntWords] (per block the bin counts packed two
+// to a word, then the counts of the kSelectGroups groups of bins); the
+// sample also clears zero[0 .. zero_words) for passes that accumulate later.
 int sample_blocks(int64_t K);
 hipError_t launch_sample(const float* r, int64_t n, const float* noise, int64_t K,
                          uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,

@@ -204,7 +204,7 @@ BracketWs carve_bracket(Carve& c, int64_t n, int64_t K, int64_t mcap, bool with_
   // the sample's bin offsets per block, and the bucket accumulators (which
   // the sample clears)
   w.soffs = c.take<uint32_t>(static_cast<size_t>(sample_blocks(K)) * (kSelectBins + 1));
-  w.scnt = c.take<uint32_t>(static_cast<size_t>(sample_blocks(K)) * (kSelectBins / 2));
+  w.scnt = c.take<uint32_t>(static_cast<size_t>(sample_blocks(K)) * kSampleCntWords);
   w.hist = c.take<uint32_t>(kBucketAccWords);
   w.acc.n = w.hist;
   w.acc.u = reinterpret_cast<unsigned long long*>(w.hist + kBucketCount);
