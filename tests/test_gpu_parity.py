@@ -417,6 +417,24 @@ def test_bracketed_rows_of_about_one_tile(lib, n):
     assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
 
 
+@pytest.mark.parametrize("n", [200_000, 3_000_000])
+def test_bracketed_select_bin_sizes(lib, n):
+    # half of the scores in [1, 1.25), one bin of the select's top 11 bits,
+    # with the budget's quantile inside it: that bin holds about K/2 sample
+    # keys (n = 2e5: about 1700, ranked in LDS; n = 3e6: about 10000, ranked
+    # by passes over all sample keys)
+    rng = np.random.default_rng([43, n])
+    r = rng.standard_normal(n).astype(np.float32)
+    inside = rng.random(n) < 0.5
+    r[inside] = (1.0 + 0.25 * rng.random(np.count_nonzero(inside))).astype(np.float32)
+    k, alpha = float(np.count_nonzero(r >= np.float32(1.1))), -0.01
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([89, n], K, 0.01)
+    g = W.random_case(44, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=f"select n={n}", g=g)
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
+
+
 def test_backward_band_saved_for_another_length(lib):
     # a band whose header names another row length is not used: the
     # backward takes the dense form from p
