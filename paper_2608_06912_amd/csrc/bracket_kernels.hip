@@ -539,11 +539,14 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
     }
     // band members take slots in index order from the masks and the wave's
-    // running count
+    // running count.  M lies inside the band (lo <= a_L, hi >= a_R, both
+    // rounded outwards), so a step without band members has no M members
+    // either, and a lane's one band member is its only possible M member.
     uint64_t bm[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) bm[e] = __ballot(inB[e]);
-    if (bm[0] | bm[1] | bm[2] | bm[3]) {
+    const uint64_t any = bm[0] | bm[1] | bm[2] | bm[3];
+    if (any) {
       if (!STAGE) {
         // the L tail's terms as they are met: below the band's lower edge
         // (a_L - 105 t) a term e^{(r - a_L)/t} is exactly 0 in float32
@@ -554,20 +557,26 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
         st.TL += static_cast<double>(tl);
       }
       const uint32_t nb0 = static_cast<uint32_t>(st.nB);   // uniform across the wave
-      uint32_t tot = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) tot += static_cast<uint32_t>(__popcll(bm[e]));
       const uint32_t cap = static_cast<uint32_t>(bw.cap);
-      const uint64_t any = bm[0] | bm[1] | bm[2] | bm[3];
       const uint64_t two = (bm[0] & (bm[1] | bm[2] | bm[3])) | (bm[1] & (bm[2] | bm[3])) |
                            (bm[2] & bm[3]);   // lanes with two or more members
+      // M members of the step: staged in index order, with the range of M
+      auto stage_m = [&](float x, int64_t i, uint32_t at) {
+        st.mmin = fminf(st.mmin, x);
+        st.mmax = fmaxf(st.mmax, x);
+        if (at < static_cast<uint32_t>(kWaveStage)) {
+          sv[at] = x;
+          si[at] = static_cast<int32_t>(i);
+        }
+      };
       if (two == 0ull) {
         // each lane holds at most one member: its slot is its rank among
         // the lanes that hold one (scalar mask work, a few vector ops)
-        if (inB[0] || inB[1] || inB[2] || inB[3]) {
+        const bool mine = inB[0] || inB[1] || inB[2] || inB[3];
+        const int e0 = inB[0] ? 0 : (inB[1] ? 1 : (inB[2] ? 2 : 3));
+        const float x0 = inB[0] ? v[0] : (inB[1] ? v[1] : (inB[2] ? v[2] : v[3]));
+        if (mine) {
           const uint32_t slot = nb0 + lanes_below(any);
-          const int e0 = inB[0] ? 0 : (inB[1] ? 1 : (inB[2] ? 2 : 3));
-          const float x0 = inB[0] ? v[0] : (inB[1] ? v[1] : (inB[2] ? v[2] : v[3]));
           if (slot < cap) {
             BandEntry en;
             en.idx = static_cast<int32_t>(i0 + e0);
@@ -575,11 +584,22 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
             bw.sbuf[slot] = en;
           }
         }
+        st.nB = nb0 + static_cast<uint32_t>(__popcll(any));
+        bool m0 = mine && !(x0 < aL);
+        if constexpr (HAS_R) m0 = m0 && !(x0 >= aR);
+        const uint64_t mm = __ballot(m0);
+        if (mm) {   // rare: some lane holds an M member
+          if (m0) stage_m(x0, i0 + e0, static_cast<uint32_t>(st.nM) + lanes_below(mm));
+          st.nM += static_cast<uint32_t>(__popcll(mm));
+        }
       } else {
         // a lane's members follow those of the lanes below it
-        uint32_t slot = nb0;
+        uint32_t slot = nb0, tot = 0;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) slot += lanes_below(bm[e]);
+        for (int e = 0; e < 4; ++e) {
+          slot += lanes_below(bm[e]);
+          tot += static_cast<uint32_t>(__popcll(bm[e]));
+        }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if (inB[e]) {
@@ -592,31 +612,26 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
             ++slot;
           }
         }
-      }
-      st.nB = nb0 + tot;
-    }
-    if (__ballot(inM[0] || inM[1] || inM[2] || inM[3])) {   // rare: some lane holds an M member
-      uint32_t before = 0, total = 0;
+        st.nB = nb0 + tot;
+        if (__ballot(inM[0] || inM[1] || inM[2] || inM[3])) {
+          uint32_t before = 0, total = 0;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint64_t bal = __ballot(inM[e]);
-        before += lanes_below(bal);
-        total += static_cast<uint32_t>(__popcll(bal));
-      }
-      uint32_t idx = static_cast<uint32_t>(st.nM) + before;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (inM[e]) {
-          st.mmin = fminf(st.mmin, v[e]);
-          st.mmax = fmaxf(st.mmax, v[e]);
-          if (idx < static_cast<uint32_t>(kWaveStage)) {
-            sv[idx] = v[e];
-            si[idx] = static_cast<int32_t>(i0 + e);
+          for (int e = 0; e < 4; ++e) {
+            const uint64_t bal = __ballot(inM[e]);
+            before += lanes_below(bal);
+            total += static_cast<uint32_t>(__popcll(bal));
           }
-          ++idx;
+          uint32_t at = static_cast<uint32_t>(st.nM) + before;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (inM[e]) {
+              stage_m(v[e], i0 + e, at);
+              ++at;
+            }
+          }
+          st.nM += total;
         }
       }
-      st.nM += total;
     }
   };
   constexpr int U = 4;   // float4 loads per lane per batch, two batches in flight
