@@ -31,6 +31,10 @@ probs                  Eq. (1): p_i = sigma((b - r_i)/alpha).
 vjp                    Eq. (5): (grad_r p)^T g = f * (g - <g, q>).
 fd_vjp                 centred finite differences (Suppl. F, Table gradcheck
                        protocol).
+vjp_params             §5 (the attack trains k and alpha): dL/dk and dL/dalpha
+                       by implicit differentiation of Eq. (1) (a reading; the
+                       paper gives no formula).
+fd_params              centred finite differences of <g, p> in k and alpha.
 bracket_ranks          Eq. (8): j = floor(Kq - z sqrt(Kq(1-q))),
                        l = ceil(Kq + z sqrt(Kq(1-q))), q = (n-k)/n.
 systematic_sample      §4 / Suppl. C remark (iii): strided view plus cached
@@ -65,7 +69,7 @@ F64 = np.float64
 __all__ = [
     "laplace_cdf", "lapsum", "initial_bracket", "solve_bisect", "solve_brent",
     "certify_root", "desc_keys", "desc_order", "solve_sorted_scan", "probs",
-    "vjp", "forward", "fd_vjp", "bracket_ranks", "systematic_sample",
+    "vjp", "vjp_params", "forward", "fd_vjp", "fd_params", "bracket_ranks", "systematic_sample",
     "order_statistic", "partition", "solve_in_bracket", "widen",
     "BracketInfo", "bracketed_forward", "zero_temperature_threshold",
     "budget_error",
@@ -373,6 +377,44 @@ def fd_vjp(r, k: float, alpha: float, g, eps: float = 1e-5) -> np.ndarray:
         r[i] = x
         out[i] = (fp - fm) / (2.0 * eps)
     return out
+
+
+def vjp_params(r, b: float, alpha: float, g) -> tuple[float, float]:
+    """(dL/dk, dL/dalpha) for L = <g, p> with b tied to (k, alpha) by Eq. (1).
+
+    §5 (exact-budget adversarial examples) trains both the budget k and the
+    temperature alpha; the paper states no formula, so this is a reading:
+    implicit differentiation of sum_i sigma((r_i - b)/t) = k, t = -alpha.
+    With s_i = exp(-|r_i - b|/t)/2 (so that dp_i/db = -s_i/t, the f of
+    Eq. (5) times t) and u_i = (r_i - b)/t:
+        db/dk = -t / sum s,   dp_i/dk = s_i / sum s,
+        db/dt = -t sum s u / sum s,   dp_i/dt = -(s_i/t)(u_i - sum s u / sum s),
+    so with F = sum s, G = sum s g, U = sum s u, H = sum s g u
+        dL/dk = G / F,   dL/dalpha = -dL/dt = (H - (U/F) G) / t.
+    Both are taken as zero when F is zero in float64 (as in `vjp`)."""
+    t = -float(alpha)
+    r = _as_f64(r)
+    g = _as_f64(g)
+    u = (r - b) / t
+    s = 0.5 * np.exp(-np.abs(u))
+    F = math.fsum(s)
+    if F == 0.0:
+        return 0.0, 0.0
+    G = math.fsum(s * g)
+    U = math.fsum(s * u)
+    H = math.fsum(s * g * u)
+    return G / F, (H - (U / F) * G) / t
+
+
+def fd_params(r, k: float, alpha: float, g, eps: float = 1e-6) -> tuple[float, float]:
+    """Centred finite differences of <g, p(k, alpha)> in k and in alpha, each
+    re-solving the threshold by its definition."""
+    def loss(kk, aa):
+        return float(np.dot(_as_f64(g), probs(r, solve_bisect(r, kk, aa), aa)))
+
+    dk = (loss(k + eps, alpha) - loss(k - eps, alpha)) / (2.0 * eps)
+    da = (loss(k, alpha + eps) - loss(k, alpha - eps)) / (2.0 * eps)
+    return dk, da
 
 
 def budget_error(p, k: float) -> float:

@@ -218,6 +218,65 @@ def check_vjp_invariants():
         assert abs(np.dot(u, O.vjp(x, b, a, g)) - np.dot(g, O.vjp(x, b, a, u))) <= 1e-12
 
 
+def check_params_fd(cases=((24, 6.0, -1.0), (40, 13.5, -0.3), (64, 3.25, -2.0)), tol=1e-6):
+    """dL/dk and dL/dalpha against centred finite differences of <g, p> in k
+    and alpha, each threshold re-solved by its definition."""
+    worst = 0.0
+    for ci, (n, k, a) in enumerate(cases):
+        rg = np.random.default_rng([91, ci])
+        x = rg.standard_normal(n)
+        g = rg.standard_normal(n)
+        b = O.solve_bisect(x, k, a)
+        got = O.vjp_params(x, b, a, g)
+        fd = O.fd_params(x, k, a, g)
+        for an, nu in zip(got, fd):
+            rel = abs(an - nu) / max(abs(nu), 1e-3)
+            worst = max(worst, rel)
+    assert worst <= tol, worst
+    return worst
+
+
+def check_params_closed_forms():
+    """Cases with closed forms: one score (p = k whatever alpha), all scores
+    equal (p = k/n), and a constant cotangent c (<c, p> = c k): the gradients
+    are (mean g, 0), (mean g, 0) and (c, 0)."""
+    rg = np.random.default_rng(17)
+    gk, ga = O.vjp_params(np.array([0.7]), O.solve_bisect(np.array([0.7]), 0.3, -0.5), -0.5,
+                          np.array([2.5]))
+    assert abs(gk - 2.5) <= 1e-15 and abs(ga) <= 1e-15
+    for n in (2, 9, 50):
+        x = np.full(n, -1.25)
+        g = rg.standard_normal(n)
+        k = 0.37 * n
+        gk, ga = O.vjp_params(x, O.solve_bisect(x, k, -0.8), -0.8, g)
+        assert abs(gk - g.mean()) <= 1e-14 * (1 + np.abs(g).max()) and abs(ga) <= 1e-14
+    for _ in range(5):
+        n = int(rg.integers(3, 60))
+        x = rg.standard_normal(n)
+        a = -float(rg.uniform(0.05, 3.0))
+        k = float(rg.uniform(0.5, n - 0.5))
+        gk, ga = O.vjp_params(x, O.solve_bisect(x, k, a), a, np.full(n, -1.5))
+        assert abs(gk + 1.5) <= 1e-14 and abs(ga) <= 1e-12
+
+
+def check_params_scale_identity():
+    """p(c r, k, c alpha) = p(r, k, alpha) for c > 0 (Eq. (1) depends on
+    (r - b)/alpha only), so d/dc at c = 1 gives
+    alpha dL/dalpha = -<r, grad_r L>, tying dL/dalpha to Eq. (5)."""
+    rg = np.random.default_rng(23)
+    for _ in range(6):
+        n = int(rg.integers(2, 90))
+        x = rg.standard_normal(n) * rg.uniform(0.5, 4.0) + rg.uniform(-3, 3)
+        a = -float(rg.uniform(0.05, 3.0))
+        k = float(rg.uniform(0.5, n - 0.5))
+        g = rg.standard_normal(n)
+        b = O.solve_bisect(x, k, a)
+        _, ga = O.vjp_params(x, b, a, g)
+        rhs = -float(np.dot(x, O.vjp(x, b, a, g)))
+        scale = float(np.dot(np.abs(x), np.abs(O.vjp(x, b, a, np.abs(g))))) + 1e-300
+        assert abs(a * ga - rhs) <= 1e-12 * max(scale, abs(rhs), 1.0), (a * ga, rhs)
+
+
 def check_desc_order():
     """Descending by value; equal values keep ascending index; -0.0 after +0.0."""
     rg = np.random.default_rng(1)

@@ -71,6 +71,35 @@ def _bad_vjp_scale(r, b, alpha, g):
     return 2.0 * _orig_vjp(r, b, alpha, g)    # f without the 1/(2t)... off by 2
 
 
+def _params_sums(r, b, alpha, g):
+    t = -float(alpha)
+    r = np.asarray(r, _F64)
+    g = np.asarray(g, _F64)
+    u = (r - b) / t
+    s = 0.5 * np.exp(-np.abs(u))
+    return t, s.sum(), (s * g).sum(), (s * u).sum(), (s * g * u).sum()
+
+
+def _bad_params_mean_sign(r, b, alpha, g):
+    t, F, G, U, H = _params_sums(r, b, alpha, g)
+    return G / F, (H + (U / F) * G) / t       # wrong sign of the centring term
+
+
+def _bad_params_no_centre(r, b, alpha, g):
+    t, F, G, U, H = _params_sums(r, b, alpha, g)
+    return G / F, H / t                        # db/dalpha dropped
+
+
+def _bad_params_t(r, b, alpha, g):
+    t, F, G, U, H = _params_sums(r, b, alpha, g)
+    return G / F, (H - (U / F) * G) / (t * t)  # u differentiated as r/t
+
+
+def _bad_params_k_unnormalised(r, b, alpha, g):
+    t, F, G, U, H = _params_sums(r, b, alpha, g)
+    return G / t, (H - (U / F) * G) / t        # dp/dk taken as s/t
+
+
 def _bad_ranks_sd(n, k, K, z):
     q = (n - k) / n
     sd = math.sqrt(K * q)                     # dropped (1 - q)
@@ -138,6 +167,10 @@ MUTANTS = {
     "gap_root_sign": ("_gap_root", _bad_gap_sign),
     "vjp_unnormalised_q": ("vjp", _bad_vjp_unnormalised),
     "vjp_scale": ("vjp", _bad_vjp_scale),
+    "params_mean_sign": ("vjp_params", _bad_params_mean_sign),
+    "params_no_centre": ("vjp_params", _bad_params_no_centre),
+    "params_t": ("vjp_params", _bad_params_t),
+    "params_k_unnormalised": ("vjp_params", _bad_params_k_unnormalised),
     "ranks_sd": ("bracket_ranks", _bad_ranks_sd),
     "ranks_q": ("bracket_ranks", _bad_ranks_q),
     "partition_boundary": ("partition", _bad_partition_closed),
@@ -154,6 +187,8 @@ CHECKS = [
     pins.check_decimal_bruteforce,
     lambda: pins.check_vjp_fd(((1, 16, 4, -1.0),), tol=1e-8),
     pins.check_vjp_invariants,
+    lambda: pins.check_params_fd(((24, 6.0, -1.0), (40, 13.5, -0.3)), tol=1e-6),
+    pins.check_params_closed_forms, pins.check_params_scale_identity,
     pins.check_bracket_ranks, pins.check_partition_definition,
     pins.check_sampler_and_order_statistic, pins.check_widen_rule,
     pins.check_bracket_equals_full, pins.check_forced_widening,

@@ -69,6 +69,19 @@ def test_vjp_invariants():
     pins.check_vjp_invariants()
 
 
+def test_budget_and_temperature_gradients_match_finite_differences():
+    worst = pins.check_params_fd()
+    assert worst < 1e-6
+
+
+def test_budget_and_temperature_gradients_closed_forms():
+    pins.check_params_closed_forms()
+
+
+def test_temperature_gradient_scale_identity():
+    pins.check_params_scale_identity()
+
+
 def test_descending_order_and_ties():
     pins.check_desc_order()
 
