@@ -107,11 +107,25 @@ int lapsum_forward(const float* scores, int64_t batch, int64_t n, double k,
  *           that callers can pass the forward's outputs unchanged).
  *   alpha   the forward's temperature.
  *   grad_r  [batch, n] float32, output dL/dr.
+ *   grad_k, grad_alpha
+ *           [batch] float64 device memory each, or NULL: the gradients of
+ *           L with respect to the budget k and the temperature alpha, which
+ *           the adversarial attack of §5 trains along with the input (the
+ *           paper gives no formula; these follow from differentiating
+ *           Eq. (1) implicitly).  With s_i = min(p_i, 1 - p_i) and
+ *           u_i = (r_i - b)/t (recovered from p_i: |u_i| = -ln(2 s_i),
+ *           negative where p_i <= 1/2),
+ *             dL/dk     = sum s g / sum s  (= <g, q>),
+ *             dL/dalpha = (sum s g u - (sum s u / sum s) sum s g) / t,
+ *           both 0 when sum s is zero.  Requesting either adds the two
+ *           extra sums to the same reduction; NULL for both leaves the pass
+ *           as it is.
  * ------------------------------------------------------------------------ */
 size_t lapsum_backward_workspace_size(int64_t batch, int64_t n);
 
 int lapsum_backward(const float* grad_p, const float* p, const double* b,
                     int64_t batch, int64_t n, double alpha, float* grad_r,
+                    double* grad_k, double* grad_alpha,
                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
@@ -215,6 +229,9 @@ int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n,
  * that fell back to the full sort, are computed from p and grad_p directly.
  *
  *   grad_p, p, alpha, grad_r   as in lapsum_backward (p: the forward's output)
+ *   grad_k, grad_alpha         as in lapsum_backward; u_i is taken from the
+ *                              saved score for band members and from p_i in
+ *                              blocks computed from p
  *   band, band_bytes           the forward's band, unchanged since; a band
  *                              saved for another row length is detected and
  *                              the dense form used instead
@@ -225,7 +242,8 @@ size_t lapsum_backward_band_workspace_size(int64_t batch, int64_t n);
 
 int lapsum_backward_band(const float* grad_p, const float* p, const void* band,
                          size_t band_bytes, int64_t batch, int64_t n,
-                         double alpha, float* grad_r, void* workspace,
+                         double alpha, float* grad_r, double* grad_k,
+                         double* grad_alpha, void* workspace,
                          size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------

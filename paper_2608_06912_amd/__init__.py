@@ -78,7 +78,7 @@ def load():
     lib.lapsum_forward.restype = i32
     lib.lapsum_backward_workspace_size.argtypes = [i64, i64]
     lib.lapsum_backward_workspace_size.restype = sz
-    lib.lapsum_backward.argtypes = [vp, vp, vp, i64, i64, f64, vp, vp, sz, vp]
+    lib.lapsum_backward.argtypes = [vp, vp, vp, i64, i64, f64, vp, vp, vp, vp, sz, vp]
     lib.lapsum_backward.restype = i32
     lib.lapsum_forward_bracketed_workspace_size.argtypes = [i64, i64, i64, i64, i32]
     lib.lapsum_forward_bracketed_workspace_size.restype = sz
@@ -89,7 +89,7 @@ def load():
     lib.lapsum_band_size.restype = sz
     lib.lapsum_backward_band_workspace_size.argtypes = [i64, i64]
     lib.lapsum_backward_band_workspace_size.restype = sz
-    lib.lapsum_backward_band.argtypes = [vp, vp, vp, sz, i64, i64, f64, vp, vp, sz, vp]
+    lib.lapsum_backward_band.argtypes = [vp, vp, vp, sz, i64, i64, f64, vp, vp, vp, vp, sz, vp]
     lib.lapsum_backward_band.restype = i32
     lib.lapsum_profile_start.argtypes = []
     lib.lapsum_profile_start.restype = i32
@@ -205,8 +205,22 @@ def lapsum_backward_workspace_size(batch: int, n: int) -> int:
     return int(load().lapsum_backward_workspace_size(batch, n))
 
 
-def lapsum_backward(grad_p, p, b, alpha: float, *, workspace=None, out=None):
-    """VJP of Eq. (5): grad_r = f * (g - <g, q>) with f from p."""
+def _param_grads(p, params: bool):
+    """float64 outputs for dL/dk and dL/dalpha, one per row (shape p.shape[:-1])."""
+    if not params:
+        return None, None
+    torch = _torch()
+    shape = tuple(p.shape[:-1])
+    return (torch.empty(shape, dtype=torch.float64, device=p.device),
+            torch.empty(shape, dtype=torch.float64, device=p.device))
+
+
+def lapsum_backward(grad_p, p, b, alpha: float, *, params: bool = False, workspace=None,
+                    out=None):
+    """VJP of Eq. (5): grad_r = f * (g - <g, q>) with f from p.  With
+    params=True returns (grad_r, grad_k, grad_alpha), the last two float64 of
+    shape p.shape[:-1]: the gradients with respect to the budget and the
+    temperature from the same reduction."""
     torch = _torch()
     lib = load()
     batch, n = _rows(p, "p")
@@ -215,11 +229,13 @@ def lapsum_backward(grad_p, p, b, alpha: float, *, workspace=None, out=None):
     _rows(grad_p, "grad_p")
     dev = p.device
     grad = out if out is not None else torch.empty_like(p)
+    gk, ga = _param_grads(p, params)
     ws, nbytes = _workspace(lib.lapsum_backward_workspace_size(batch, n), dev, workspace)
     with _on_device(dev):
         _check(lib.lapsum_backward(_ptr(grad_p), _ptr(p), _ptr(b), batch, n, float(alpha),
-                                   _ptr(grad), _ptr(ws), nbytes, _stream(dev)), "lapsum_backward")
-    return grad
+                                   _ptr(grad), _ptr(gk), _ptr(ga), _ptr(ws), nbytes, _stream(dev)),
+               "lapsum_backward")
+    return (grad, gk, ga) if params else grad
 
 
 def lapsum_forward_bracketed_workspace_size(batch: int, n: int, K: int, m_capacity: int,
@@ -304,8 +320,10 @@ def lapsum_backward_band_workspace_size(batch: int, n: int) -> int:
     return int(load().lapsum_backward_band_workspace_size(batch, n))
 
 
-def lapsum_backward_band(grad_p, p, band, alpha: float, *, workspace=None, out=None):
-    """Eq. (5) VJP from the band a bracketed forward saved (see new_band)."""
+def lapsum_backward_band(grad_p, p, band, alpha: float, *, params: bool = False, workspace=None,
+                         out=None):
+    """Eq. (5) VJP from the band a bracketed forward saved (see new_band);
+    params=True as in lapsum_backward."""
     torch = _torch()
     lib = load()
     batch, n = _rows(p, "p")
@@ -316,13 +334,15 @@ def lapsum_backward_band(grad_p, p, band, alpha: float, *, workspace=None, out=N
         raise ValueError("band is required")
     dev = p.device
     grad = out if out is not None else torch.empty_like(p)
+    gk, ga = _param_grads(p, params)
     ws, nbytes = _workspace(lib.lapsum_backward_band_workspace_size(batch, n), dev, workspace)
     bp, bbytes = _band_arg(band, batch, n)
     with _on_device(dev):
         _check(lib.lapsum_backward_band(_ptr(grad_p), _ptr(p), bp, bbytes, batch, n, float(alpha),
-                                        _ptr(grad), _ptr(ws), nbytes, _stream(dev)),
+                                        _ptr(grad), _ptr(gk), _ptr(ga), _ptr(ws), nbytes,
+                                        _stream(dev)),
                "lapsum_backward_band")
-    return grad
+    return (grad, gk, ga) if params else grad
 
 
 def lapsum_profile_start() -> None:

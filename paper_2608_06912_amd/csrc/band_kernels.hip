@@ -80,7 +80,7 @@ struct WriterLds {
   float4 tile[2][kRound][kTileF4];      // member values of a round (0 elsewhere)
   uint32_t ow[2][kRound][kTileWords];   // ones bits of a round's tiles
   uint32_t dense[2];                    // bit i: tile i of the round is dense
-  double red[2][kStoreWaves];
+  double red[4][kStoreWaves];
 };
 
 // Forward: p.
@@ -415,18 +415,23 @@ hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s) {
 constexpr int kVjpWaveBlocks = BW;             // partition blocks per reduce block
 constexpr int kVjpMaxParts = 4 * BT;           // partials a writer block sums
 
+// With PARAMS each part also carries sum s u and sum s g u (u = (r - b)/t:
+// from the score for list members, recovered from p for dense blocks), for
+// the budget and temperature gradients.
+template <bool PARAMS>
 __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __restrict__ g,
                                                              const float* __restrict__ p,
                                                              int64_t n, BandCtx c, double inv_t,
                                                              float* __restrict__ gstash,
                                                              double* __restrict__ partials) {
-  __shared__ double red[2][BW];
+  constexpr int NS = PARAMS ? 4 : 2;
+  __shared__ double red[NS][BW];
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
   const int pb = static_cast<int>(blockIdx.x) * kVjpWaveBlocks + wid;
   const CtxHeader h = *c.hdr;
-  double F = 0.0, G = 0.0;
+  double F = 0.0, G = 0.0, U = 0.0, H = 0.0;
   if (pb < c.nblocks) {
     const BlockRange br = range_of(n, c.chunk, pb);
     if (header_dense(h, c, n) || !lists_usable(c, pb)) {
@@ -434,8 +439,14 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
         const float pv = p[i];
         const float f = fminf(pv, 1.0f - pv);
         if (f != 0.0f) {
+          const double fg = static_cast<double>(f) * static_cast<double>(g[i]);
           F += static_cast<double>(f);
-          G += static_cast<double>(f) * static_cast<double>(g[i]);
+          G += fg;
+          if constexpr (PARAMS) {
+            const double u = static_cast<double>(laplace_u_from_p(pv, f));
+            U += static_cast<double>(f) * u;
+            H += fg * u;
+          }
         }
       }
     } else {
@@ -476,8 +487,15 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
         for (int u = 0; u < VB; ++u) {
           if (use[u]) {
             gstash[at[u]] = gv[u];
+            const double fg = static_cast<double>(fv[u]) * static_cast<double>(gv[u]);
             F += static_cast<double>(fv[u]);
-            G += static_cast<double>(fv[u]) * static_cast<double>(gv[u]);
+            G += fg;
+            if constexpr (PARAMS) {
+              const double uu =
+                  (static_cast<double>(__uint_as_float(en[u].bits)) - h.b) * inv_t;
+              U += static_cast<double>(fv[u]) * uu;
+              H += fg * uu;
+            }
           }
         }
       }
@@ -485,64 +503,88 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
   }
   F = wave_sum(F);
   G = wave_sum(G);
+  if constexpr (PARAMS) {
+    U = wave_sum(U);
+    H = wave_sum(H);
+  }
   if (lane == 0) {
     red[0][wid] = F;
     red[1][wid] = G;
+    if constexpr (PARAMS) {
+      red[2][wid] = U;
+      red[3][wid] = H;
+    }
   }
   __syncthreads();
-  if (tid == 0) {
-    double fs = 0.0, gs = 0.0;
+  if (tid < NS) {
+    double acc = 0.0;
 #pragma unroll
-    for (int w = 0; w < BW; ++w) {
-      fs += red[0][w];
-      gs += red[1][w];
-    }
-    partials[2 * blockIdx.x] = fs;
-    partials[2 * blockIdx.x + 1] = gs;
+    for (int w = 0; w < BW; ++w) acc += red[tid][w];
+    partials[NS * blockIdx.x + tid] = acc;
   }
 }
 
 // grad_r = (f/t)(g - <g,q>); <g,q> = sum f g / sum f from the partials, 0
-// (and grad_r = 0) when sum f == 0.
+// (and grad_r = 0) when sum f == 0.  With PARAMS block 0 also stores
+// dL/dk = <g,q> and dL/dalpha = (H - (U/F) G)/t (0 when F == 0).
+template <bool PARAMS>
 __global__ __launch_bounds__(WT) void band_vjp_write_kernel(const float* __restrict__ g,
                                                             const float* __restrict__ p,
                                                             int64_t n, BandCtx c,
                                                             const float* __restrict__ gstash,
                                                             const double* __restrict__ partials,
                                                             int nparts, double inv_t,
-                                                            float* __restrict__ grad) {
+                                                            float* __restrict__ grad,
+                                                            double* __restrict__ grad_k,
+                                                            double* __restrict__ grad_alpha) {
+  constexpr int NS = PARAMS ? 4 : 2;
   __shared__ WriterLds S;
   const int tid = threadIdx.x;
   const CtxHeader h = *c.hdr;
   if (tid < BT) {
     // the partials in a fixed order: thread tid adds parts tid, tid + BT, ...
-    double F = 0.0, G = 0.0;
-    double2 pr[kVjpMaxParts / BT];
+    double acc[NS];
+#pragma unroll
+    for (int q = 0; q < NS; ++q) acc[q] = 0.0;
+    double2 pr[kVjpMaxParts / BT][NS / 2];
 #pragma unroll
     for (int q = 0; q < kVjpMaxParts / BT; ++q) {
       const int i = q * BT + tid;
-      pr[q] = reinterpret_cast<const double2*>(partials)[i < nparts ? i : 0];
+#pragma unroll
+      for (int h2 = 0; h2 < NS / 2; ++h2)
+        pr[q][h2] = reinterpret_cast<const double2*>(partials)[(i < nparts ? i : 0) * (NS / 2) + h2];
     }
 #pragma unroll
     for (int q = 0; q < kVjpMaxParts / BT; ++q) {
       if (q * BT + tid < nparts) {
-        F += pr[q].x;
-        G += pr[q].y;
+#pragma unroll
+        for (int h2 = 0; h2 < NS / 2; ++h2) {
+          acc[2 * h2] += pr[q][h2].x;
+          acc[2 * h2 + 1] += pr[q][h2].y;
+        }
       }
     }
-    F = wave_sum(F);
-    G = wave_sum(G);
+#pragma unroll
+    for (int q = 0; q < NS; ++q) acc[q] = wave_sum(acc[q]);
     if (lane_id() == 0) {
-      S.red[0][tid / kWave] = F;
-      S.red[1][tid / kWave] = G;
+#pragma unroll
+      for (int q = 0; q < NS; ++q) S.red[q][tid / kWave] = acc[q];
     }
   }
   __syncthreads();
-  double fs = 0.0, gsum = 0.0;
+  double tot[NS];
 #pragma unroll
-  for (int w = 0; w < BW; ++w) {
-    fs += S.red[0][w];
-    gsum += S.red[1][w];
+  for (int q = 0; q < NS; ++q) {
+    tot[q] = 0.0;
+#pragma unroll
+    for (int w = 0; w < BW; ++w) tot[q] += S.red[q][w];
+  }
+  const double fs = tot[0], gsum = tot[1];
+  if constexpr (PARAMS) {
+    if (blockIdx.x == 0 && tid == 0) {
+      if (grad_k) *grad_k = fs > 0.0 ? gsum / fs : 0.0;
+      if (grad_alpha) *grad_alpha = fs > 0.0 ? (tot[3] - (tot[2] / fs) * gsum) * inv_t : 0.0;
+    }
   }
   VjpPass P;
   P.p = p;
@@ -559,17 +601,26 @@ int band_vjp_parts(int nblocks) { return (nblocks + kVjpWaveBlocks - 1) / kVjpWa
 
 hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const BandCtx& band,
                            float* gstash, double* partials, double t, float* grad,
-                           hipStream_t s) {
+                           double* grad_k, double* grad_alpha, hipStream_t s) {
   const int parts = band_vjp_parts(band.nblocks);
   if (parts > kVjpMaxParts) return hipErrorInvalidValue;
+  const bool params = grad_k || grad_alpha;
   { ProfScope ps_("band_vjp_reduce", s);
-  hipLaunchKernelGGL(band_vjp_reduce_kernel, dim3(parts), dim3(BT), 0, s, g, p, n, band, 1.0 / t,
-                     gstash, partials); }
+  if (params)
+    hipLaunchKernelGGL(band_vjp_reduce_kernel<true>, dim3(parts), dim3(BT), 0, s, g, p, n, band,
+                       1.0 / t, gstash, partials);
+  else
+    hipLaunchKernelGGL(band_vjp_reduce_kernel<false>, dim3(parts), dim3(BT), 0, s, g, p, n, band,
+                       1.0 / t, gstash, partials); }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("band_vjp_emit", s);
-  hipLaunchKernelGGL(band_vjp_write_kernel, dim3(writer_blocks(n)), dim3(WT), 0, s, g, p, n, band,
-                     gstash, partials, parts, 1.0 / t, grad); }
+  if (params)
+    hipLaunchKernelGGL(band_vjp_write_kernel<true>, dim3(writer_blocks(n)), dim3(WT), 0, s, g, p,
+                       n, band, gstash, partials, parts, 1.0 / t, grad, grad_k, grad_alpha);
+  else
+    hipLaunchKernelGGL(band_vjp_write_kernel<false>, dim3(writer_blocks(n)), dim3(WT), 0, s, g, p,
+                       n, band, gstash, partials, parts, 1.0 / t, grad, grad_k, grad_alpha); }
   return hipGetLastError();
 }
 

@@ -571,4 +571,12 @@ __device__ __forceinline__ float laplace_p(float r, double b, double inv_t) {
   return (u <= 0.0f) ? 0.5f * e : 1.0f - 0.5f * e;
 }
 
+// u = (r - b)/t recovered from p = sigma(u) by inverting Eq. (3): with
+// s = min(p, 1 - p) = e^{-|u|}/2, |u| = -ln(2s), and u <= 0 exactly where
+// p <= 1/2.  Called only where s > 0.
+__device__ __forceinline__ float laplace_u_from_p(float p, float s) {
+  const float a = logf(2.0f * s);
+  return p > 0.5f ? -a : a;
+}
+
 }  // namespace lapsum

@@ -130,24 +130,26 @@ hipError_t launch_fill_u32(uint32_t* dst, int64_t count, uint32_t value, hipStre
 // Full-sort forward for rows with n <= kRowOnChipMax (one workgroup per row).
 hipError_t launch_row_forward(const float* scores, int64_t batch, int64_t n, double k, double t,
                               float* p, double* b, int32_t* perm, hipStream_t s);
-// Backward for rows with n <= kRowOnChipMax.
+// Backward for rows with n <= kRowOnChipMax; grad_k / grad_alpha ([batch]
+// float64, each may be null) receive the budget and temperature gradients.
 hipError_t launch_row_backward(const float* grad_p, const float* p, int64_t batch, int64_t n,
-                               double t, float* grad_r, hipStream_t s);
+                               double t, float* grad_r, double* grad_k, double* grad_alpha,
+                               hipStream_t s);
 
 // Laplace-CDF emit p = sigma((r - b)/t) for one row, b read from device.
 hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t, float* p,
                        hipStream_t s);
 
-// Device-wide backward for one row: partial (sum f, sum f g) per 4096-score
-// tile, one block reducing them in a fixed order to coef[0] = <g, q> and
-// coef[1] = 1/t (0 when sum f == 0), then the emit.
+// Device-wide backward for one row: partial sums per block, one block
+// reducing them in a fixed order to coef[0] = <g, q> and coef[1] = 1/t (0 when
+// sum f == 0), then the emit.  The partials are (sum s, sum s g), or with
+// grad_k / grad_alpha requested (sum s, sum s g, sum s u, sum s g u) with
+// s = min(p, 1 - p), u = (r - b)/t; partials holds 4 doubles per block.
+// grad_k / grad_alpha: one float64 each (may be null).
 int vjp_reduce_blocks(int64_t n);
 hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
-                             int nblocks, double t, double* coef, hipStream_t s);
-// coef[0] = sum f g / sum f, coef[1] = 1/t (both 0 when sum f == 0) from
-// nparts (sum f, sum f g) pairs, summed in a fixed order.
-hipError_t launch_vjp_finalize(const double* partials, int nparts, double t, double* coef,
-                               hipStream_t s);
+                             int nblocks, double t, double* coef, double* grad_k,
+                             double* grad_alpha, hipStream_t s);
 hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* coef,
                            float* grad, hipStream_t s);
 
@@ -230,12 +232,15 @@ hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, doub
 // Mark a context as dense (rows solved by the full sort).
 hipError_t launch_ctx_dense(const BandCtx& band, int64_t n, hipStream_t s);
 // Backward from a saved band: partial (sum f, sum f g) per run of blocks,
-// then grad_r written densely (zero outside the band).  partials: 2 doubles
+// then grad_r written densely (zero outside the band).  partials: 4 doubles
 // per part, band_vjp_parts(nblocks) parts; gstash: one float per list slot.
+// grad_k / grad_alpha (one float64 each, may be null) receive the budget and
+// temperature gradients; requesting either adds sum s u and sum s g u to the
+// partials.
 int band_vjp_parts(int nblocks);
 hipError_t launch_band_vjp(const float* g, const float* p, int64_t n, const BandCtx& band,
                            float* gstash, double* partials, double t, float* grad,
-                           hipStream_t s);
+                           double* grad_k, double* grad_alpha, hipStream_t s);
 hipError_t launch_gather(const float* r, int64_t n, const PartTotals* tot, const PartBlock* blk,
                          const int64_t* offsets, int nblocks, int64_t chunk, const float* stage_v,
                          const int32_t* stage_i, int64_t m_capacity, uint32_t* m_keys,

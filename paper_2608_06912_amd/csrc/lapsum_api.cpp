@@ -618,14 +618,14 @@ size_t lapsum_backward_workspace_size(int64_t batch, int64_t n) {
   (void)batch;
   if (n <= kRowOnChipMax) return 0;
   Carve c(nullptr);
-  c.take<double>(2 * static_cast<size_t>(vjp_reduce_blocks(n)));
+  c.take<double>(4 * static_cast<size_t>(vjp_reduce_blocks(n)));
   c.take<double>(2);
   return c.size();
 }
 
 int lapsum_backward(const float* grad_p, const float* p, const double* b, int64_t batch, int64_t n,
-                    double alpha, float* grad_r, void* workspace, size_t workspace_bytes,
-                    hipStream_t stream) {
+                    double alpha, float* grad_r, double* grad_k, double* grad_alpha,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
   (void)b;
   if (!grad_p || !p || !grad_r) return LAPSUM_ERR_INVALID_ARG;
   if (batch < 1 || n < 1 || n > 2147483647LL || !isfinite(alpha) || !(alpha < 0.0))
@@ -636,16 +636,18 @@ int lapsum_backward(const float* grad_p, const float* p, const double* b, int64_
   if (dst != LAPSUM_OK) return dst;
   const double t = -alpha;
   if (n <= kRowOnChipMax) {
-    LAPSUM_TRY(launch_row_backward(grad_p, p, batch, n, t, grad_r, stream));
+    LAPSUM_TRY(launch_row_backward(grad_p, p, batch, n, t, grad_r, grad_k, grad_alpha, stream));
     return LAPSUM_OK;
   }
   Carve c(workspace);
   const int nb = vjp_reduce_blocks(n);
-  double* partials = c.take<double>(2 * static_cast<size_t>(nb));
+  double* partials = c.take<double>(4 * static_cast<size_t>(nb));
   double* coef = c.take<double>(2);
   for (int64_t row = 0; row < batch; ++row) {
     const int64_t o = row * n;
-    LAPSUM_TRY(launch_vjp_reduce(grad_p + o, p + o, n, partials, nb, t, coef, stream));
+    LAPSUM_TRY(launch_vjp_reduce(grad_p + o, p + o, n, partials, nb, t, coef,
+                                 grad_k ? grad_k + row : nullptr,
+                                 grad_alpha ? grad_alpha + row : nullptr, stream));
     LAPSUM_TRY(launch_vjp_emit(grad_p + o, p + o, n, coef, grad_r + o, stream));
   }
   return LAPSUM_OK;
@@ -698,14 +700,15 @@ size_t lapsum_backward_band_workspace_size(int64_t batch, int64_t n) {
   if (n < 1 || n > 2147483647LL) return 0;
   const BandCtx v = band_ctx_view(nullptr, n);
   Carve c(nullptr);
-  c.take<double>(2 * static_cast<size_t>(band_vjp_parts(v.nblocks)));
+  c.take<double>(4 * static_cast<size_t>(band_vjp_parts(v.nblocks)));
   c.take<float>(static_cast<size_t>(v.nblocks) * 4 * v.cap);
   return c.size();
 }
 
 int lapsum_backward_band(const float* grad_p, const float* p, const void* band, size_t band_bytes,
-                         int64_t batch, int64_t n, double alpha, float* grad_r, void* workspace,
-                         size_t workspace_bytes, hipStream_t stream) {
+                         int64_t batch, int64_t n, double alpha, float* grad_r, double* grad_k,
+                         double* grad_alpha, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream) {
   if (!grad_p || !p || !band || !grad_r) return LAPSUM_ERR_INVALID_ARG;
   if (batch < 1 || n < 1 || n > 2147483647LL || !isfinite(alpha) || !(alpha < 0.0))
     return LAPSUM_ERR_INVALID_ARG;
@@ -718,7 +721,7 @@ int lapsum_backward_band(const float* grad_p, const float* p, const void* band, 
   const double t = -alpha;
   const BandCtx v0 = band_ctx_view(nullptr, n);
   Carve c(workspace);
-  double* partials = c.take<double>(2 * static_cast<size_t>(band_vjp_parts(v0.nblocks)));
+  double* partials = c.take<double>(4 * static_cast<size_t>(band_vjp_parts(v0.nblocks)));
   float* gstash = c.take<float>(static_cast<size_t>(v0.nblocks) * 4 * v0.cap);
   const size_t band_row_bytes = band_ctx_bytes(n);
   for (int64_t row = 0; row < batch; ++row) {
@@ -726,7 +729,9 @@ int lapsum_backward_band(const float* grad_p, const float* p, const void* band, 
     // the kernels only read the band
     void* band_row = const_cast<char*>(static_cast<const char*>(band)) + row * band_row_bytes;
     const BandCtx v = band_ctx_view(band_row, n);
-    LAPSUM_TRY(launch_band_vjp(grad_p + o, p + o, n, v, gstash, partials, t, grad_r + o, stream));
+    LAPSUM_TRY(launch_band_vjp(grad_p + o, p + o, n, v, gstash, partials, t, grad_r + o,
+                               grad_k ? grad_k + row : nullptr,
+                               grad_alpha ? grad_alpha + row : nullptr, stream));
   }
   return LAPSUM_OK;
 }

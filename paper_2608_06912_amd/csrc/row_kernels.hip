@@ -80,17 +80,24 @@ __global__ __launch_bounds__(BLOCK) void row_forward_kernel(const float* __restr
   }
 }
 
-template <int BLOCK, int ITEMS>
+// Eq. (5) for one row; with PARAMS also the budget and temperature gradients
+// dL/dk = G/F and dL/dalpha = (H - (U/F) G)/t, from F = sum s, G = sum s g,
+// U = sum s u, H = sum s g u over s = min(p, 1 - p), u = (r - b)/t (implicit
+// differentiation of Eq. (1)); both 0 when F == 0.
+template <int BLOCK, int ITEMS, bool PARAMS>
 __global__ __launch_bounds__(BLOCK) void row_backward_kernel(const float* __restrict__ g,
                                                              const float* __restrict__ p, int n,
-                                                             double t, float* __restrict__ grad) {
+                                                             double t, float* __restrict__ grad,
+                                                             double* __restrict__ grad_k,
+                                                             double* __restrict__ grad_alpha) {
   constexpr int WAVES = BLOCK / kWave;
-  __shared__ double red[2 * WAVES];
+  constexpr int NS = PARAMS ? 4 : 2;
+  __shared__ double red[NS * WAVES];
   const int tid = threadIdx.x;
   const int64_t row = blockIdx.x;
   const float* pr = p + row * n;
   const float* gr = g + row * n;
-  double F = 0.0, G = 0.0;
+  double F = 0.0, G = 0.0, U = 0.0, H = 0.0;
 #pragma unroll
   for (int i = 0; i < ITEMS; ++i) {
     const int j = i * BLOCK + tid;
@@ -98,15 +105,31 @@ __global__ __launch_bounds__(BLOCK) void row_backward_kernel(const float* __rest
       const float pp = pr[j];
       const float f = fminf(pp, 1.0f - pp);   // e^{-|b-r|/t} / 2, exact from p
       F += static_cast<double>(f);
-      if (f != 0.0f) G += static_cast<double>(f) * static_cast<double>(gr[j]);
+      if (f != 0.0f) {
+        const double fg = static_cast<double>(f) * static_cast<double>(gr[j]);
+        G += fg;
+        if constexpr (PARAMS) {
+          const double u = static_cast<double>(laplace_u_from_p(pp, f));
+          U += static_cast<double>(f) * u;
+          H += fg * u;
+        }
+      }
     }
   }
   F = wave_sum(F);
   G = wave_sum(G);
+  if constexpr (PARAMS) {
+    U = wave_sum(U);
+    H = wave_sum(H);
+  }
   const int wid = tid / kWave;
   if (lane_id() == 0) {
     red[wid] = F;
     red[WAVES + wid] = G;
+    if constexpr (PARAMS) {
+      red[2 * WAVES + wid] = U;
+      red[3 * WAVES + wid] = H;
+    }
   }
   __syncthreads();
   F = 0.0;
@@ -120,6 +143,19 @@ __global__ __launch_bounds__(BLOCK) void row_backward_kernel(const float* __rest
   // second read of p and g hits L2 (the row is at most 256 KB).
   const double coef = (F > 0.0) ? G / F : 0.0;
   const double scale = (F > 0.0) ? 1.0 / t : 0.0;
+  if constexpr (PARAMS) {
+    if (tid == 0) {
+      U = 0.0;
+      H = 0.0;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) {
+        U += red[2 * WAVES + w];
+        H += red[3 * WAVES + w];
+      }
+      if (grad_k) grad_k[row] = coef;
+      if (grad_alpha) grad_alpha[row] = (F > 0.0) ? (H - (U / F) * G) / t : 0.0;
+    }
+  }
   float* out = grad + row * n;
 #pragma unroll
   for (int i = 0; i < ITEMS; ++i) {
@@ -152,10 +188,14 @@ hipError_t fwd_items(const float* scores, int64_t batch, int64_t n, double k, do
 
 template <int BLOCK, int ITEMS>
 hipError_t bwd_items(const float* g, const float* p, int64_t batch, int64_t n, double t,
-                     float* grad, hipStream_t s) {
+                     float* grad, double* grad_k, double* grad_alpha, hipStream_t s) {
   { ProfScope ps_("row_backward", s);
-  hipLaunchKernelGGL((row_backward_kernel<BLOCK, ITEMS>), dim3(batch), dim3(BLOCK), 0, s, g, p,
-                     static_cast<int>(n), t, grad); }
+  if (grad_k || grad_alpha)
+    hipLaunchKernelGGL((row_backward_kernel<BLOCK, ITEMS, true>), dim3(batch), dim3(BLOCK), 0, s,
+                       g, p, static_cast<int>(n), t, grad, grad_k, grad_alpha);
+  else
+    hipLaunchKernelGGL((row_backward_kernel<BLOCK, ITEMS, false>), dim3(batch), dim3(BLOCK), 0, s,
+                       g, p, static_cast<int>(n), t, grad, grad_k, grad_alpha); }
   return hipGetLastError();
 }
 
@@ -175,12 +215,14 @@ hipError_t launch_row_forward(const float* scores, int64_t batch, int64_t n, dou
 }
 
 hipError_t launch_row_backward(const float* grad_p, const float* p, int64_t batch, int64_t n,
-                               double t, float* grad_r, hipStream_t s) {
-  if (n <= 1024) return bwd_items<256, 4>(grad_p, p, batch, n, t, grad_r, s);
-  if (n <= 4096) return bwd_items<1024, 4>(grad_p, p, batch, n, t, grad_r, s);
-  if (n <= 8192) return bwd_items<1024, 8>(grad_p, p, batch, n, t, grad_r, s);
-  if (n <= 16384) return bwd_items<1024, 16>(grad_p, p, batch, n, t, grad_r, s);
-  if (n <= kRowOnChipMax) return bwd_items<1024, 32>(grad_p, p, batch, n, t, grad_r, s);
+                               double t, float* grad_r, double* grad_k, double* grad_alpha,
+                               hipStream_t s) {
+  if (n <= 1024) return bwd_items<256, 4>(grad_p, p, batch, n, t, grad_r, grad_k, grad_alpha, s);
+  if (n <= 4096) return bwd_items<1024, 4>(grad_p, p, batch, n, t, grad_r, grad_k, grad_alpha, s);
+  if (n <= 8192) return bwd_items<1024, 8>(grad_p, p, batch, n, t, grad_r, grad_k, grad_alpha, s);
+  if (n <= 16384) return bwd_items<1024, 16>(grad_p, p, batch, n, t, grad_r, grad_k, grad_alpha, s);
+  if (n <= kRowOnChipMax)
+    return bwd_items<1024, 32>(grad_p, p, batch, n, t, grad_r, grad_k, grad_alpha, s);
   return hipErrorInvalidValue;
 }
 

@@ -83,12 +83,15 @@ int vjp_reduce_blocks(int64_t n) {
 // Block b sums f = min(p, 1-p) and f g over a contiguous range of float4s,
 // four per lane in flight; g is read only for float4s with some f != 0.
 // float32 within a float4, float64 across, then a fixed-order block
-// reduction (butterfly within a wave, waves in order).
+// reduction (DPP within a wave, waves in order).  With PARAMS also sum s u
+// and sum s g u, u recovered from p.
+template <bool PARAMS>
 __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float* __restrict__ g,
                                                                     const float* __restrict__ p,
                                                                     int64_t n,
                                                                     double* __restrict__ partials) {
-  __shared__ double red[2][kStreamThreads / kWave];
+  constexpr int NS = PARAMS ? 4 : 2;
+  __shared__ double red[NS][kStreamThreads / kWave];
   const int tid = threadIdx.x;
   const bool vec = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(p)) & 15) == 0;
   const int64_t n4 = vec ? n / 4 : 0;
@@ -97,7 +100,21 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float*
   const int64_t hi = (lo + per < n4) ? lo + per : n4;
   const float4* p4 = reinterpret_cast<const float4*>(p);
   const float4* g4 = reinterpret_cast<const float4*>(g);
-  double F = 0.0, G = 0.0;
+  double F = 0.0, G = 0.0, Us = 0.0, H = 0.0;
+  // sum s u and sum s g u of four scores (float32; s == 0 terms skipped)
+  auto su4 = [&](const float4& pv, const float (&f)[4], const float4& gv) {
+    const float pw[4] = {pv.x, pv.y, pv.z, pv.w};
+    const float gw[4] = {gv.x, gv.y, gv.z, gv.w};
+    float a = 0.0f, c = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float fu = f[q] != 0.0f ? f[q] * laplace_u_from_p(pw[q], f[q]) : 0.0f;
+      a += fu;
+      c += fu * gw[q];
+    }
+    Us += static_cast<double>(a);
+    H += static_cast<double>(c);
+  };
   constexpr int U = 4;   // float4 of p per lane per batch, two batches in flight
   int64_t i = lo + tid;
   auto batch = [&](const float4 (&pv)[U], int64_t at) {
@@ -121,6 +138,7 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float*
         F += static_cast<double>((f[u][0] + f[u][1]) + (f[u][2] + f[u][3]));
         G += static_cast<double>((f[u][0] * gv[u].x + f[u][1] * gv[u].y) +
                                  (f[u][2] * gv[u].z + f[u][3] * gv[u].w));
+        if constexpr (PARAMS) su4(pv[u], f[u], gv[u]);
       }
     }
   };
@@ -145,13 +163,14 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float*
   }
   for (; i < hi; i += kStreamThreads) {
     const float4 pv = p4[i];
-    const float fx = fminf(pv.x, 1.0f - pv.x), fy = fminf(pv.y, 1.0f - pv.y);
-    const float fz = fminf(pv.z, 1.0f - pv.z), fw = fminf(pv.w, 1.0f - pv.w);
-    const float fs = (fx + fy) + (fz + fw);
+    const float f[4] = {fminf(pv.x, 1.0f - pv.x), fminf(pv.y, 1.0f - pv.y),
+                        fminf(pv.z, 1.0f - pv.z), fminf(pv.w, 1.0f - pv.w)};
+    const float fs = (f[0] + f[1]) + (f[2] + f[3]);
     if (fs != 0.0f) {
       const float4 gq = g4[i];
       F += static_cast<double>(fs);
-      G += static_cast<double>((fx * gq.x + fy * gq.y) + (fz * gq.z + fw * gq.w));
+      G += static_cast<double>((f[0] * gq.x + f[1] * gq.y) + (f[2] * gq.z + f[3] * gq.w));
+      if constexpr (PARAMS) su4(pv, f, gq);
     }
   }
   if (blockIdx.x == gridDim.x - 1) {   // scalar tail (all of it when unaligned)
@@ -159,80 +178,108 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float*
       const float pp = p[j];
       const float f1 = fminf(pp, 1.0f - pp);
       if (f1 != 0.0f) {
+        const double gj = static_cast<double>(g[j]);
         F += static_cast<double>(f1);
-        G += static_cast<double>(f1) * static_cast<double>(g[j]);
+        G += static_cast<double>(f1) * gj;
+        if constexpr (PARAMS) {
+          const double fu = static_cast<double>(f1) * static_cast<double>(laplace_u_from_p(pp, f1));
+          Us += fu;
+          H += fu * gj;
+        }
       }
     }
   }
   F = wave_sum(F);
   G = wave_sum(G);
+  if constexpr (PARAMS) {
+    Us = wave_sum(Us);
+    H = wave_sum(H);
+  }
   const int wid = tid / kWave;
   if (lane_id() == 0) {
     red[0][wid] = F;
     red[1][wid] = G;
+    if constexpr (PARAMS) {
+      red[2][wid] = Us;
+      red[3][wid] = H;
+    }
   }
   __syncthreads();
-  if (tid == 0) {
-    double fsum = 0.0, gsum = 0.0;
+  if (tid < NS) {
+    double acc = 0.0;
 #pragma unroll
-    for (int w = 0; w < kStreamThreads / kWave; ++w) {
-      fsum += red[0][w];
-      gsum += red[1][w];
-    }
-    partials[2 * blockIdx.x] = fsum;
-    partials[2 * blockIdx.x + 1] = gsum;
+    for (int w = 0; w < kStreamThreads / kWave; ++w) acc += red[tid][w];
+    partials[NS * blockIdx.x + tid] = acc;
   }
 }
 
 // One block: sum the partials in a fixed order and store
-// coef = <g, q> = sum f g / sum f and scale = 1/t (both 0 when sum f == 0).
+// coef = <g, q> = sum f g / sum f and scale = 1/t (both 0 when sum f == 0);
+// with PARAMS also dL/dk = <g, q> and dL/dalpha = (H - (U/F) G)/t.
+template <bool PARAMS>
 __global__ __launch_bounds__(1024) void vjp_finalize_kernel(const double* __restrict__ partials,
                                                             int nparts, double inv_t,
-                                                            double* __restrict__ coef) {
+                                                            double* __restrict__ coef,
+                                                            double* __restrict__ grad_k,
+                                                            double* __restrict__ grad_alpha) {
   constexpr int T = 1024;
-  __shared__ double red[2][T / kWave];
+  constexpr int NS = PARAMS ? 4 : 2;
+  __shared__ double red[NS][T / kWave];
   const int tid = threadIdx.x;
-  double F = 0.0, G = 0.0;
+  double acc[NS];
+#pragma unroll
+  for (int q = 0; q < NS; ++q) acc[q] = 0.0;
   for (int j = tid; j < nparts; j += T) {
-    F += partials[2 * j];
-    G += partials[2 * j + 1];
+#pragma unroll
+    for (int q = 0; q < NS; ++q) acc[q] += partials[NS * j + q];
   }
-  F = wave_sum(F);
-  G = wave_sum(G);
+#pragma unroll
+  for (int q = 0; q < NS; ++q) acc[q] = wave_sum(acc[q]);
   const int wid = tid / kWave;
   if (lane_id() == 0) {
-    red[0][wid] = F;
-    red[1][wid] = G;
+#pragma unroll
+    for (int q = 0; q < NS; ++q) red[q][wid] = acc[q];
   }
   __syncthreads();
   if (tid == 0) {
-    double f = 0.0, gg = 0.0;
+    double tot[NS];
 #pragma unroll
-    for (int w = 0; w < T / kWave; ++w) {
-      f += red[0][w];
-      gg += red[1][w];
+    for (int q = 0; q < NS; ++q) {
+      tot[q] = 0.0;
+#pragma unroll
+      for (int w = 0; w < T / kWave; ++w) tot[q] += red[q][w];
     }
+    const double f = tot[0], gg = tot[1];
     coef[0] = (f > 0.0) ? gg / f : 0.0;
     coef[1] = (f > 0.0) ? inv_t : 0.0;
+    if constexpr (PARAMS) {
+      if (grad_k) *grad_k = coef[0];
+      if (grad_alpha) *grad_alpha = (f > 0.0) ? (tot[3] - (tot[2] / f) * gg) * inv_t : 0.0;
+    }
   }
 }
 
-hipError_t launch_vjp_finalize(const double* partials, int nparts, double t, double* coef,
-                               hipStream_t s) {
-  { ProfScope ps_("vjp_finalize", s);
-  hipLaunchKernelGGL(vjp_finalize_kernel, dim3(1), dim3(1024), 0, s, partials, nparts, 1.0 / t,
-                     coef); }
-  return hipGetLastError();
-}
-
 hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
-                             int nblocks, double t, double* coef, hipStream_t s) {
+                             int nblocks, double t, double* coef, double* grad_k,
+                             double* grad_alpha, hipStream_t s) {
+  const bool params = grad_k || grad_alpha;
   { ProfScope ps_("vjp_reduce", s);
-  hipLaunchKernelGGL(vjp_reduce_kernel, dim3(nblocks), dim3(kStreamThreads), 0, s, g, p, n,
-                     partials); }
+  if (params)
+    hipLaunchKernelGGL(vjp_reduce_kernel<true>, dim3(nblocks), dim3(kStreamThreads), 0, s, g, p,
+                       n, partials);
+  else
+    hipLaunchKernelGGL(vjp_reduce_kernel<false>, dim3(nblocks), dim3(kStreamThreads), 0, s, g, p,
+                       n, partials); }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_vjp_finalize(partials, nblocks, t, coef, s);
+  { ProfScope ps_("vjp_finalize", s);
+  if (params)
+    hipLaunchKernelGGL(vjp_finalize_kernel<true>, dim3(1), dim3(1024), 0, s, partials, nblocks,
+                       1.0 / t, coef, grad_k, grad_alpha);
+  else
+    hipLaunchKernelGGL(vjp_finalize_kernel<false>, dim3(1), dim3(1024), 0, s, partials, nblocks,
+                       1.0 / t, coef, grad_k, grad_alpha); }
+  return hipGetLastError();
 }
 
 // -------------------------------------------------------------- vjp emit ---

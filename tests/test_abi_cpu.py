@@ -91,10 +91,13 @@ def test_forward_rejects_missing_workspace():
 def test_backward_rejects_invalid_arguments():
     lib = L.load()
     v = ctypes.c_void_p
-    assert lib.lapsum_backward(v(0), v(1), v(0), 1, 8, -1.0, v(1), v(0), 0, v(0)) == 1
-    assert lib.lapsum_backward(v(1), v(1), v(0), 1, 8, 0.5, v(1), v(0), 0, v(0)) == 1
-    assert lib.lapsum_backward(v(1), v(1), v(0), 0, 8, -1.0, v(1), v(0), 0, v(0)) == 1
-    assert lib.lapsum_backward(v(1), v(1), v(0), 1, 10**6, -1.0, v(1), v(0), 0, v(0)) == 2
+    z = (v(0), v(0))   # no budget / temperature gradients
+    assert lib.lapsum_backward(v(0), v(1), v(0), 1, 8, -1.0, v(1), *z, v(0), 0, v(0)) == 1
+    assert lib.lapsum_backward(v(1), v(1), v(0), 1, 8, 0.5, v(1), *z, v(0), 0, v(0)) == 1
+    assert lib.lapsum_backward(v(1), v(1), v(0), 0, 8, -1.0, v(1), *z, v(0), 0, v(0)) == 1
+    assert lib.lapsum_backward(v(1), v(1), v(0), 1, 10**6, -1.0, v(1), *z, v(0), 0, v(0)) == 2
+    assert lib.lapsum_backward(v(1), v(1), v(0), 1, 10**6, -1.0, v(1), v(8), v(8), v(0), 0,
+                               v(0)) == 2
 
 
 @pytest.mark.parametrize("kw", [
@@ -140,7 +143,7 @@ def test_backward_band_rejects_invalid_arguments():
     need = L.lapsum_band_size(1, 1000)
     ws = L.lapsum_backward_band_workspace_size(1, 1000)
     args = lambda band, bb, alpha=-1.0, wsp=256, wsb=ws: lib.lapsum_backward_band(
-        v(1), v(1), v(band), bb, 1, 1000, alpha, v(1), v(wsp), wsb, v(0))
+        v(1), v(1), v(band), bb, 1, 1000, alpha, v(1), v(0), v(0), v(wsp), wsb, v(0))
     assert args(0, need) == 1            # no band
     assert args(256, need - 1) == 1      # band too small
     assert args(128, need) == 1          # misaligned

@@ -5,6 +5,8 @@ Tolerances (applied in float32):
   sum p   |sum p - k| <= 1e-6 max(1, k) + 1e-3        (sum taken in float64)
   b       |b - b_oracle| <= 2e-6 t   (keeps the p error below 1e-6)
   grad_r  ||grad - grad_oracle||_2 / ||grad_oracle||_2 <= 1e-4
+  dL/dk, dL/dalpha   the error bound of `params_tol` (below), against the
+                     oracle at the forward's b
   permutation, bracket endpoints, set sizes and M membership: bit-exact
 """
 import math
@@ -49,6 +51,48 @@ def grad_rel(g_gpu, g_ref):
     num = np.linalg.norm(g_gpu.astype(np.float64) - g_ref)
     den = np.linalg.norm(g_ref)
     return num / den if den > 0 else num
+
+
+def params_tol(r32, b, alpha, g, gk_ref):
+    """Error bounds for dL/dk = sum s g / sum s and
+    dL/dalpha = sum s g (u - ubar) / t computed from the float32 p that the
+    forward emitted with threshold b (the oracle is evaluated at the same b;
+    b itself is checked against the oracle's root separately).
+
+    u_i = (r_i - b)/t is rounded to float32 (relative 6e-8) before the
+    exponential, so s_i = min(p_i, 1 - p_i) is off by s_i |u_i| 6e-8, plus a
+    few float32 ulps for the exponential, the rounding of p_i and the float32
+    partial sums: w_i = 3e-7 s_i (1 + |u_i|); where p_i > 1/2 add the absolute
+    rounding of p_i, up to 6e-8 (s_i below it is dropped entirely).  u_i,
+    recovered as -ln(2 s_i) or taken from the score, is then off by
+    w_i / s_i.  To first order
+      |d dL/dk|     <= sum w_i (|g_i| + |dL/dk|) / F
+      |d dL/dalpha| <= sum w_i (|g_i| + |dL/dk|)(1 + |u_i| + |u_i - ubar|) / t."""
+    t = -alpha
+    u = (np.asarray(r32, np.float64) - b) / t
+    s = 0.5 * np.exp(-np.abs(u))
+    F = float(s.sum())
+    if F == 0.0:
+        return 1e-12, 1e-12
+    ubar = float((s * u).sum()) / F
+    w = 3e-7 * s * (1.0 + np.abs(u)) + np.where(u > 0, np.minimum(6e-8, 2.0 * s), 0.0)
+    ga = np.abs(np.asarray(g, np.float64)) + abs(gk_ref)
+    tol_k = float((w * ga).sum()) / F + 1e-12
+    tol_a = float((w * ga * (1.0 + np.abs(u) + np.abs(u - ubar))).sum()) / t + 1e-12
+    return tol_k, tol_a
+
+
+def check_params(gk, ga, r32, b, alpha, g, label=""):
+    """dL/dk, dL/dalpha against the oracle at the forward's own threshold b;
+    gk, ga: one value each, or lists of values from several backwards of the
+    same p."""
+    ref_k, ref_a = O.vjp_params(r32, b, alpha, g)
+    tol_k, tol_a = params_tol(r32, b, alpha, g, ref_k)
+    gks = gk if isinstance(gk, (list, tuple)) else [gk]
+    gas = ga if isinstance(ga, (list, tuple)) else [ga]
+    for i, (vk, va) in enumerate(zip(gks, gas)):
+        assert abs(vk - ref_k) <= tol_k, (label, i, "dL/dk", vk, ref_k, tol_k)
+        assert abs(va - ref_a) <= tol_a, (label, i, "dL/dalpha", va, ref_a, tol_a)
 
 
 # ------------------------------------------------------------ on-chip rows --
@@ -97,10 +141,17 @@ def test_row_backward_matches_oracle(lib, n, alpha):
     k = max(0.5, n / 16.0) if n > 1 else 0.25
     p, b = lib.lapsum_forward(_t(r), k, alpha)
     grad = _np(lib.lapsum_backward(_t(g), p, b, alpha))
+    grad2, gk, ga = lib.lapsum_backward(_t(g), p, b, alpha, params=True)
+    # the extra sums leave grad_r as it is
+    assert np.array_equal(_np(grad2), grad)
+    gk, ga = _np(gk), _np(ga)
+    assert gk.shape == (3,) and ga.shape == (3,)
     for row in range(3):
         b_ref = O.solve_sorted_scan(r[row], k, alpha)
         ref = O.vjp(r[row], b_ref, alpha, g[row])
         assert grad_rel(grad[row], ref) <= G_TOL, (n, row, grad_rel(grad[row], ref))
+        check_params(float(gk[row]), float(ga[row]), r[row], float(_np(b)[row]), alpha, g[row],
+                     f"n={n}")
 
 
 def test_forward_is_deterministic(lib):
@@ -146,8 +197,13 @@ def test_devicewide_backward(lib, n, alpha):
     k = n / 100.0
     p, b = lib.lapsum_forward(_t(r), k, alpha)
     grad = _np(lib.lapsum_backward(_t(g), p, b, alpha))[0]
-    ref = O.vjp(r[0], O.solve_sorted_scan(r[0], k, alpha), alpha, g[0])
+    b_ref = O.solve_sorted_scan(r[0], k, alpha)
+    ref = O.vjp(r[0], b_ref, alpha, g[0])
     assert grad_rel(grad, ref) <= G_TOL
+    grad2, gk, ga = lib.lapsum_backward(_t(g), p, b, alpha, params=True)
+    assert np.array_equal(_np(grad2)[0], grad)
+    check_params(float(_np(gk)[0]), float(_np(ga)[0]), r[0], float(_np(b)[0]), alpha, g[0],
+                 f"n={n}")
 
 
 # -------------------------------------------------------------- bracketed --
@@ -206,6 +262,7 @@ def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label="
         assert np.all(m == -1)
     # both forwards emit p of the same closed form from b's within 2e-6 t
     assert np.max(np.abs(pbn.astype(np.float64) - _np(p)[0].astype(np.float64))) <= 2 * P_TOL, label
+    print(f"{label}: forwards checked", flush=True)
     if g is not None:
         gt = _t(g[None, :])
         gb = _np(lib.lapsum_backward_band(gt, pb, band, alpha))[0]
@@ -214,6 +271,15 @@ def _check_bracketed(lib, r32, k, alpha, noise, z=5.16, m_capacity=None, label="
         # same f from the same p; only the summation order differs
         assert grad_rel(gb, gp.astype(np.float64)) <= 1e-6, (label, "band vs p-form")
         assert np.all(gb[gp == 0.0] == 0.0), label
+        print(f"{label}: grad_r checked", flush=True)
+        # budget and temperature gradients from both backwards; grad_r unchanged
+        gb2, gkb, gab = lib.lapsum_backward_band(gt, pb, band, alpha, params=True)
+        gp2, gkp, gap = lib.lapsum_backward(gt, pb, bb, alpha, params=True)
+        assert np.array_equal(_np(gb2)[0], gb) and np.array_equal(_np(gp2)[0], gp), label
+        # one oracle evaluation for both (band, then p-form)
+        check_params([float(_np(gkb)[0]), float(_np(gkp)[0])],
+                     [float(_np(gab)[0]), float(_np(gap)[0])], r32, float(_np(bb)[0]), alpha, g,
+                     label)
     return pbn, float(_np(bb)[0]), bo, infos_b[0]
 
 
@@ -396,6 +462,8 @@ def test_bracketed_batched_rows_of_odd_length(lib):
     band = lib.new_band(batch, n, "cuda")
     p, b, infos, _ = lib.lapsum_forward_bracketed(_t(rows), k, alpha, _t(noise), band=band)
     grad = _np(lib.lapsum_backward_band(_t(gs), p, band, alpha))
+    _, gk, ga = lib.lapsum_backward_band(_t(gs), p, band, alpha, params=True)
+    gk, ga = _np(gk), _np(ga)
     pn, bn = _np(p), _np(b)
     for i in range(batch):
         po, bo, oinfo, _ = O.bracketed_forward(rows[i], k, alpha, noise)
@@ -403,6 +471,7 @@ def test_bracketed_batched_rows_of_odd_length(lib):
         assert abs(float(bn[i]) - bo) <= 2e-6 * -alpha, i
         assert np.max(np.abs(pn[i].astype(np.float64) - O.probs(rows[i], bo, alpha))) <= P_TOL, i
         assert grad_rel(grad[i], O.vjp(rows[i], bo, alpha, gs[i])) <= G_TOL, i
+        check_params(float(gk[i]), float(ga[i]), rows[i], float(bn[i]), alpha, gs[i], f"row {i}")
 
 
 @pytest.mark.parametrize("n", [700, 1024, 1025])
