@@ -173,6 +173,14 @@ def main():
     def backward(p):
         L.lapsum_backward_band(g, p, band, w.alpha, workspace=ws_b, out=grad)
 
+    gk_buf = torch.empty(1, dtype=torch.float64, device=dev)
+    ga_buf = torch.empty(1, dtype=torch.float64, device=dev)
+
+    def backward_params(p):
+        # the same backward also reducing dL/dk and dL/dalpha
+        L.lapsum_backward_band(g, p, band, w.alpha, params=True, params_out=(gk_buf, ga_buf),
+                               workspace=ws_b, out=grad)
+
     def step():
         p, b, infos = forward()
         backward(p)
@@ -206,6 +214,14 @@ def main():
         backward(p)
     torch.cuda.synchronize()
     ms_bwd = (time.perf_counter() - t0) * 1e3 / args.steps
+    for _ in range(args.warmup):
+        backward_params(p)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        backward_params(p)
+    torch.cuda.synchronize()
+    ms_bwd_params = (time.perf_counter() - t0) * 1e3 / args.steps
 
     # per-kernel durations with HIP events over the same K steps
     L.lapsum_profile_start()
@@ -247,6 +263,7 @@ def main():
                    "m_capacity": mcap},
         "ms_fwd": ms_fwd,
         "ms_bwd": ms_bwd,
+        "ms_bwd_with_k_alpha_grads": ms_bwd_params,
         "path_roofline": {"model_bytes_per_score": 32, "frac": path_frac,
                           "note": "32 B/score required-traffic model at 8 TB/s"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,

@@ -81,8 +81,10 @@ const char* lapsum_status_string(int status);
  *            ordered by the order-preserving uint32 key of the float (so
  *            +0.0 precedes -0.0) and then by ascending original index.
  *            Asking for it makes the sort carry indices (slower).
- * Rows with n <= 32768 are solved by one workgroup per row entirely on chip;
- * longer rows use the device-wide sort and scan, one row after another.
+ * Rows with n <= 32768 are solved by one workgroup per row entirely on chip,
+ * except a batch of one row longer than 16384, which is faster through the
+ * device-wide sort and scan; longer rows use the device-wide path, one row
+ * after another.  The workspace size depends on batch for that reason.
  * ------------------------------------------------------------------------ */
 size_t lapsum_forward_workspace_size(int64_t batch, int64_t n, int with_perm);
 
@@ -127,6 +129,23 @@ int lapsum_backward(const float* grad_p, const float* p, const double* b,
                     int64_t batch, int64_t n, double alpha, float* grad_r,
                     double* grad_k, double* grad_alpha,
                     void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Hard top-k mask for the straight-through estimator of Suppl. "Straight-
+ * Through Estimator": m_i = 1 when r_i is among the k largest scores of its
+ * row, else 0, so that sum_i m_i = k.  It is formed from the descending
+ * order that lapsum_forward returns in perm_out (equal scores ordered by
+ * index, so exactly k ones even with ties).  The estimator itself,
+ * m^ = p + sg(m - p), is assembled by the caller's autodiff.
+ *
+ *   perm   [batch, n] int32, a descending order per row (lapsum_forward's
+ *          perm_out).  Entries outside [0, n) are skipped; positions that no
+ *          entry names are left unchanged.
+ *   k      integer count of ones per row, 0 <= k <= n.
+ *   mask   [batch, n] float32 output.
+ * ------------------------------------------------------------------------ */
+int lapsum_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64_t k,
+                     float* mask, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Bracketed forward for very long rows (paper §4, Suppl. B, Suppl. C,

@@ -25,6 +25,7 @@ __all__ = [
     "lapsum_forward_bracketed_workspace_size", "lapsum_forward_bracketed",
     "LAPSUM_FLAG_FULL_SORT", "LIB_PATH", "lapsum_profile_start", "lapsum_profile_stop",
     "lapsum_band_size", "new_band", "lapsum_backward_band_workspace_size", "lapsum_backward_band",
+    "lapsum_topk_mask",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapsum.so")
@@ -91,6 +92,8 @@ def load():
     lib.lapsum_backward_band_workspace_size.restype = sz
     lib.lapsum_backward_band.argtypes = [vp, vp, vp, sz, i64, i64, f64, vp, vp, vp, vp, sz, vp]
     lib.lapsum_backward_band.restype = i32
+    lib.lapsum_topk_mask.argtypes = [vp, i64, i64, i64, vp, vp]
+    lib.lapsum_topk_mask.restype = i32
     lib.lapsum_profile_start.argtypes = []
     lib.lapsum_profile_start.restype = i32
     lib.lapsum_profile_stop.argtypes = []
@@ -201,22 +204,51 @@ def lapsum_forward(scores, k: float, alpha: float, *, perm: bool = False, worksp
     return (p, b, pm) if perm else (p, b)
 
 
+def lapsum_topk_mask(perm, k: int, *, out=None):
+    """Hard top-k mask (1.0 for the k largest scores of each row, 0.0
+    elsewhere) from a descending order `perm` (int32, lapsum_forward's
+    perm)."""
+    torch = _torch()
+    lib = load()
+    if not isinstance(perm, torch.Tensor) or perm.device.type != "cuda" or \
+            perm.dtype != torch.int32 or perm.dim() not in (1, 2) or not perm.is_contiguous():
+        raise ValueError("perm must be a contiguous int32 CUDA tensor of shape [n] or [batch, n]")
+    batch, n = (1, perm.shape[0]) if perm.dim() == 1 else (perm.shape[0], perm.shape[1])
+    if int(k) != k:
+        raise ValueError("k must be an integer count")
+    dev = perm.device
+    mask = out if out is not None else torch.empty(perm.shape, dtype=torch.float32, device=dev)
+    if mask.shape != perm.shape or mask.dtype != torch.float32 or not mask.is_contiguous():
+        raise ValueError("out must be a contiguous float32 tensor shaped like perm")
+    with _on_device(dev):
+        _check(lib.lapsum_topk_mask(_ptr(perm), int(batch), int(n), int(k), _ptr(mask),
+                                    _stream(dev)), "lapsum_topk_mask")
+    return mask
+
+
 def lapsum_backward_workspace_size(batch: int, n: int) -> int:
     return int(load().lapsum_backward_workspace_size(batch, n))
 
 
-def _param_grads(p, params: bool):
-    """float64 outputs for dL/dk and dL/dalpha, one per row (shape p.shape[:-1])."""
+def _param_grads(p, params: bool, params_out=None):
+    """float64 outputs for dL/dk and dL/dalpha, one per row (shape
+    p.shape[:-1]); params_out, if given, is a pair of such tensors to fill."""
     if not params:
         return None, None
     torch = _torch()
     shape = tuple(p.shape[:-1])
+    if params_out is not None:
+        for x in params_out:
+            if x.dtype != torch.float64 or tuple(x.shape) != shape or x.device != p.device \
+                    or not x.is_contiguous():
+                raise ValueError(f"params_out: float64 tensors of shape {shape} on {p.device}")
+        return params_out
     return (torch.empty(shape, dtype=torch.float64, device=p.device),
             torch.empty(shape, dtype=torch.float64, device=p.device))
 
 
-def lapsum_backward(grad_p, p, b, alpha: float, *, params: bool = False, workspace=None,
-                    out=None):
+def lapsum_backward(grad_p, p, b, alpha: float, *, params: bool = False, params_out=None,
+                    workspace=None, out=None):
     """VJP of Eq. (5): grad_r = f * (g - <g, q>) with f from p.  With
     params=True returns (grad_r, grad_k, grad_alpha), the last two float64 of
     shape p.shape[:-1]: the gradients with respect to the budget and the
@@ -229,7 +261,7 @@ def lapsum_backward(grad_p, p, b, alpha: float, *, params: bool = False, workspa
     _rows(grad_p, "grad_p")
     dev = p.device
     grad = out if out is not None else torch.empty_like(p)
-    gk, ga = _param_grads(p, params)
+    gk, ga = _param_grads(p, params, params_out)
     ws, nbytes = _workspace(lib.lapsum_backward_workspace_size(batch, n), dev, workspace)
     with _on_device(dev):
         _check(lib.lapsum_backward(_ptr(grad_p), _ptr(p), _ptr(b), batch, n, float(alpha),
@@ -320,8 +352,8 @@ def lapsum_backward_band_workspace_size(batch: int, n: int) -> int:
     return int(load().lapsum_backward_band_workspace_size(batch, n))
 
 
-def lapsum_backward_band(grad_p, p, band, alpha: float, *, params: bool = False, workspace=None,
-                         out=None):
+def lapsum_backward_band(grad_p, p, band, alpha: float, *, params: bool = False,
+                         params_out=None, workspace=None, out=None):
     """Eq. (5) VJP from the band a bracketed forward saved (see new_band);
     params=True as in lapsum_backward."""
     torch = _torch()
@@ -334,7 +366,7 @@ def lapsum_backward_band(grad_p, p, band, alpha: float, *, params: bool = False,
         raise ValueError("band is required")
     dev = p.device
     grad = out if out is not None else torch.empty_like(p)
-    gk, ga = _param_grads(p, params)
+    gk, ga = _param_grads(p, params, params_out)
     ws, nbytes = _workspace(lib.lapsum_backward_band_workspace_size(batch, n), dev, workspace)
     bp, bbytes = _band_arg(band, batch, n)
     with _on_device(dev):

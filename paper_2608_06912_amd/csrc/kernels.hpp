@@ -136,6 +136,10 @@ hipError_t launch_row_backward(const float* grad_p, const float* p, int64_t batc
                                double t, float* grad_r, double* grad_k, double* grad_alpha,
                                hipStream_t s);
 
+// Hard top-k mask from a descending order: mask[row][perm[row][j]] = (j < k).
+hipError_t launch_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64_t k, float* mask,
+                            hipStream_t s);
+
 // Laplace-CDF emit p = sigma((r - b)/t) for one row, b read from device.
 hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t, float* p,
                        hipStream_t s);

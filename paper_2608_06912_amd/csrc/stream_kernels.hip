@@ -34,6 +34,32 @@ hipError_t launch_fill_u32(uint32_t* dst, int64_t count, uint32_t value, hipStre
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------ top-k mask ---
+// mask[row][perm[row][j]] = (j < k ? 1 : 0): one thread per position j of the
+// descending order; an index outside [0, n) is skipped.
+__global__ __launch_bounds__(256) void topk_mask_kernel(const int32_t* __restrict__ perm,
+                                                        int64_t n, int64_t k, int64_t total,
+                                                        float* __restrict__ mask) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < total; i += stride) {
+    const int64_t row = i / n;
+    const int64_t j = i - row * n;
+    const int32_t at = perm[i];
+    if (at >= 0 && at < n) mask[row * n + at] = j < k ? 1.0f : 0.0f;
+  }
+}
+
+hipError_t launch_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64_t k, float* mask,
+                            hipStream_t s) {
+  const int64_t total = batch * n;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  { ProfScope ps_("topk_mask", s);
+  hipLaunchKernelGGL(topk_mask_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, perm,
+                     n, k, total, mask); }
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ emit ---
 __global__ __launch_bounds__(kStreamThreads) void emit_kernel(const float* __restrict__ r,
                                                               int64_t n,

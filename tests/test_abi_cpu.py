@@ -49,6 +49,10 @@ def test_status_strings():
 def test_workspace_sizes():
     # rows that fit on chip need no workspace
     assert L.lapsum_forward_workspace_size(256, 32768) == 0
+    assert L.lapsum_forward_workspace_size(1, 16384) == 0
+    # one row longer than 16384 goes through the device-wide sort
+    assert L.lapsum_forward_workspace_size(1, 32768) > 0
+    assert L.lapsum_forward_workspace_size(2, 32768) == 0
     assert L.lapsum_backward_workspace_size(256, 32768) == 0
     a = L.lapsum_forward_workspace_size(1, 10**6, False)
     b = L.lapsum_forward_workspace_size(1, 10**6, True)
@@ -150,3 +154,13 @@ def test_backward_band_rejects_invalid_arguments():
     assert args(256, need, alpha=1.0) == 1
     assert args(256, need, wsp=0) == 2   # workspace missing
     assert args(256, need, wsb=ws - 1) == 2
+
+
+def test_topk_mask_rejects_invalid_arguments():
+    lib = L.load()
+    v = ctypes.c_void_p
+    assert lib.lapsum_topk_mask(v(0), 1, 8, 2, v(1), v(0)) == 1     # no perm
+    assert lib.lapsum_topk_mask(v(1), 1, 8, 2, v(0), v(0)) == 1     # no mask
+    assert lib.lapsum_topk_mask(v(1), 0, 8, 2, v(1), v(0)) == 1     # batch < 1
+    assert lib.lapsum_topk_mask(v(1), 1, 8, 9, v(1), v(0)) == 1     # k > n
+    assert lib.lapsum_topk_mask(v(1), 1, 8, -1, v(1), v(0)) == 1    # k < 0

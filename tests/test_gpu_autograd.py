@@ -1,0 +1,127 @@
+"""The autograd layer on the GPU: soft_topk's forward is the library's p,
+its backward matches Eq. (5) and the budget / temperature gradients of the
+oracle, and the straight-through estimator forwards the hard top-k mask
+while differentiating p (Suppl. "Straight-Through Estimator")."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.lapsum_oracle as O
+import workloads as W
+from test_gpu_parity import G_TOL, P_TOL, grad_rel, params_tol
+
+pytestmark = pytest.mark.gpu
+
+
+def _A():
+    import paper_2608_06912_amd.autograd as A
+    return A
+
+
+def _hard_mask_oracle(r32, k):
+    m = np.zeros(r32.shape[-1], np.float32)
+    m[O.desc_order(r32)[:k]] = 1.0
+    return m
+
+
+def _check_rows(r, w, b_rows, alpha, grad, gk, ga, label):
+    """grad_r per row against Eq. (5); dL/dk, dL/dalpha (one k and alpha for
+    the whole batch, so the per-row gradients add) against the oracle with
+    the per-row error bounds added."""
+    ref_k = ref_a = tol_k = tol_a = 0.0
+    for i in range(r.shape[0]):
+        b = float(b_rows[i])
+        assert grad_rel(grad[i], O.vjp(r[i], b, alpha, w[i])) <= G_TOL, (label, i)
+        rk, ra = O.vjp_params(r[i], b, alpha, w[i])
+        tk, ta = params_tol(r[i], b, alpha, w[i], rk)
+        ref_k, ref_a, tol_k, tol_a = ref_k + rk, ref_a + ra, tol_k + tk, tol_a + ta
+    assert abs(gk - ref_k) <= tol_k, (label, gk, ref_k, tol_k)
+    assert abs(ga - ref_a) <= tol_a, (label, ga, ref_a, tol_a)
+
+
+@pytest.mark.parametrize("path,n,batch", [("full", 5000, 3), ("full", 40000, 2),
+                                          ("bracketed", 200_000, 1), ("bracketed", 300_007, 2)])
+def test_soft_topk_forward_and_gradients(lib, path, n, batch):
+    A = _A()
+    rg = np.random.default_rng([61, n])
+    r = rg.standard_normal((batch, n)).astype(np.float32)
+    w = rg.standard_normal((batch, n)).astype(np.float32)
+    kv, av = n / 20.0, -0.05
+    x = torch.from_numpy(r).cuda().requires_grad_(True)
+    k = torch.tensor(kv, dtype=torch.float64, requires_grad=True)         # host tensor
+    a = torch.tensor(av, dtype=torch.float32, device="cuda", requires_grad=True)
+    av = float(a.item())        # the float32 temperature the forward sees
+    p = A.soft_topk(x, k, a, path=path)
+    assert p.shape == x.shape and p.requires_grad
+    (p * torch.from_numpy(w).cuda()).sum().backward()
+    # the forward is the library's forward of the same path
+    if path == "full":
+        p2, b2 = lib.lapsum_forward(torch.from_numpy(r).cuda(), kv, av)
+    else:
+        K = A.sample_size(n)
+        noise = A.bracket_noise(K, -av, "cuda")
+        p2, b2, infos, _ = lib.lapsum_forward_bracketed(torch.from_numpy(r).cuda(), kv, av, noise)
+    assert torch.equal(p.detach(), p2)
+    b2 = b2.cpu().numpy()
+    for i in range(batch):
+        assert abs(b2[i] - O.solve_brent(r[i], kv, av)) <= 2e-6 * -av
+    assert k.grad.dtype == torch.float64 and k.grad.shape == ()
+    assert a.grad.dtype == torch.float32 and a.grad.device.type == "cuda"
+    _check_rows(r, w, b2, av, x.grad.cpu().numpy(), float(k.grad), float(a.grad), path)
+
+
+def test_soft_topk_auto_path_and_leading_dims(lib):
+    A = _A()
+    rg = np.random.default_rng(62)
+    r = rg.standard_normal((2, 3, 1000)).astype(np.float32)
+    x = torch.from_numpy(r).cuda().requires_grad_(True)
+    p = A.soft_topk(x, 50.0, -0.1)                      # python k, alpha: no grads for them
+    assert p.shape == (2, 3, 1000)
+    p2, _ = lib.lapsum_forward(torch.from_numpy(r.reshape(6, 1000)).cuda(), 50.0, -0.1)
+    assert torch.equal(p.detach().reshape(6, 1000), p2)
+    w = torch.from_numpy(rg.standard_normal((2, 3, 1000)).astype(np.float32)).cuda()
+    (p * w).sum().backward()
+    rows = r.reshape(6, 1000)
+    wn = w.cpu().numpy().reshape(6, 1000)
+    gr = x.grad.cpu().numpy().reshape(6, 1000)
+    for i in range(6):
+        ref = O.vjp(rows[i], O.solve_sorted_scan(rows[i], 50.0, -0.1), -0.1, wn[i])
+        assert grad_rel(gr[i], ref) <= G_TOL
+    # a row longer than the switch takes the bracket
+    assert A.choose_path(A.FULL_SORT_MAX_N + 1) == "bracketed"
+
+
+@pytest.mark.parametrize("path,n,dist", [("full", 3000, "normal"), ("full", 50_000, "levels16"),
+                                         ("bracketed", 300_007, "normal")])
+def test_straight_through_forwards_the_hard_mask(lib, path, n, dist):
+    A = _A()
+    r = W.random_case(63, n, dist=dist, ties=0.05, batch=2)
+    k = n // 10
+    w = np.random.default_rng(64).standard_normal((2, n)).astype(np.float32)
+    x = torch.from_numpy(r).cuda().requires_grad_(True)
+    mh = A.soft_topk(x, float(k), -0.2, path=path, ste=True)
+    (mh * torch.from_numpy(w).cuda()).sum().backward()
+    got = mh.detach().cpu().numpy()
+    x2 = torch.from_numpy(r).cuda().requires_grad_(True)
+    p = A.soft_topk(x2, float(k), -0.2, path=path)
+    (p * torch.from_numpy(w).cuda()).sum().backward()
+    pn = p.detach().cpu().numpy()
+    for i in range(2):
+        # m^ = p + (m - p) is m exactly in float32 for p in [0, 1]: with m = 0
+        # the terms cancel; with m = 1, 1 - p is exact for p >= 1/2 and
+        # otherwise within 2^-25 of it, and p + fl(1 - p) rounds back to 1
+        assert np.array_equal(got[i], _hard_mask_oracle(r[i], k)), i
+        assert got[i].sum() == k
+        assert 0.0 <= pn[i].min() and pn[i].max() <= 1.0
+    # the gradient is the soft p's, computed by the same kernels
+    assert torch.equal(x.grad, x2.grad)
+
+
+@pytest.mark.parametrize("k", [0, 1, 7, 999, 1000])
+def test_hard_topk_mask_with_ties(lib, k):
+    A = _A()
+    r = W.random_case(65, 1000, dist="levels16", ties=0.2, batch=3)
+    m = A.hard_topk_mask(torch.from_numpy(r).cuda(), k).cpu().numpy()
+    for i in range(3):
+        assert np.array_equal(m[i], _hard_mask_oracle(r[i], k)), i
+        assert m[i].sum() == k
