@@ -39,6 +39,8 @@ bracket_ranks          Eq. (8): j = floor(Kq - z sqrt(Kq(1-q))),
                        l = ceil(Kq + z sqrt(Kq(1-q))), q = (n-k)/n.
 systematic_sample      §4 / Suppl. C remark (iii): strided view plus cached
                        kernel noise, y_s = r_{s*stride} + eps_s.
+iid_sample             Suppl. C, Theorem 2: uniform draws with replacement
+                       (indices given) plus kernel noise.
 partition              Suppl. B: L, M, R sets and the tail sums of Eq. (7).
 solve_in_bracket       Suppl. B: LapSum(b) = |R| + 1/2 S_L e^{(b-a_L)/alpha}
                        - 1/2 S_R e^{(a_R-b)/alpha} + sum_M sigma(.), solved on
@@ -70,6 +72,7 @@ __all__ = [
     "laplace_cdf", "lapsum", "initial_bracket", "solve_bisect", "solve_brent",
     "certify_root", "desc_keys", "desc_order", "solve_sorted_scan", "probs",
     "vjp", "vjp_params", "forward", "fd_vjp", "fd_params", "bracket_ranks", "systematic_sample",
+    "iid_sample",
     "order_statistic", "partition", "solve_in_bracket", "widen",
     "BracketInfo", "bracketed_forward", "zero_temperature_threshold",
     "budget_error",
@@ -459,6 +462,18 @@ def systematic_sample(r32, noise32) -> np.ndarray:
     return (r32[idx] + eps).astype(np.float32)
 
 
+def iid_sample(r32, idx, noise32) -> np.ndarray:
+    """The sampler the coverage theorem assumes (Suppl. C, Theorem 2): K
+    scores drawn uniformly with replacement, at indices idx that the caller
+    draws, plus the kernel noise, y_s = fl32(r[idx_s] + eps_s)."""
+    r32 = np.asarray(r32, dtype=np.float32).ravel()
+    eps = np.asarray(noise32, dtype=np.float32).ravel()
+    idx = np.asarray(idx, dtype=np.int64).ravel()
+    if idx.size != eps.size or np.any(idx < 0) or np.any(idx >= r32.size):
+        raise ValueError("need one index in [0, n) per noise draw")
+    return (r32[idx] + eps).astype(np.float32)
+
+
 def order_statistic(y32, j: int) -> float:
     """y_(j), the j-th smallest (1-based); -inf below 1 and +inf above K."""
     K = y32.size
@@ -560,10 +575,12 @@ class BracketInfo:
 
 
 def bracketed_forward(r32, k: float, alpha: float, noise32, z: float = 5.16,
-                      m_capacity: int | None = None, max_attempts: int = 3):
+                      m_capacity: int | None = None, max_attempts: int = 3,
+                      sample_idx=None):
     """Algorithm 1 with the validated path (§4, Suppl. C, Suppl. D).
 
-    1. K = len(noise) kernel-noised samples by the systematic sampler;
+    1. K = len(noise) kernel-noised samples by the systematic sampler, or by
+       the i.i.d. sampler at the indices sample_idx when they are given;
     2. ranks j, l of Eq. (8); a_L = y_(j), a_R = y_(l);
     3. one pass: tails, counts, the middle set M;
     4. when |M| exceeds m_capacity (no room to hold M; widening only grows
@@ -585,7 +602,7 @@ def bracketed_forward(r32, k: float, alpha: float, noise32, z: float = 5.16,
     if m_capacity is None:
         m_capacity = n
     j, l, _q = bracket_ranks(n, k, K, z)
-    y = systematic_sample(r32, eps)
+    y = systematic_sample(r32, eps) if sample_idx is None else iid_sample(r32, sample_idx, eps)
     a_L = order_statistic(y, j)
     a_R = order_statistic(y, l)
     info = BracketInfo(a_L, a_R, j, l, 0, 0, 0, 0.0, 0.0, 0.0, 0.0, 0, 0, 0)

@@ -378,6 +378,13 @@ def check_sampler_and_order_statistic():
     v = np.array([5.0, -1.0, 3.0, 3.0, 0.5], np.float32)
     assert [O.order_statistic(v, j) for j in (1, 2, 3, 4, 5)] == [-1.0, 0.5, 3.0, 3.0, 5.0]
     assert O.order_statistic(v, 0) == -math.inf and O.order_statistic(v, 6) == math.inf
+    # the i.i.d. sampler at the strided indices is the systematic one, and it
+    # reads the indices it is given, in their order
+    rg = np.random.default_rng(8)
+    x = rg.standard_normal(1000).astype(np.float32)
+    e = rg.laplace(0.0, 0.1, 7).astype(np.float32)
+    assert np.array_equal(O.iid_sample(x, np.arange(7) * 142, e), O.systematic_sample(x, e))
+    assert O.iid_sample(r, [999, 3, 3], np.zeros(3, np.float32)).tolist() == [999.0, 3.0, 3.0]
 
 
 def check_widen_rule():
@@ -402,11 +409,8 @@ def check_coverage_theorem(trials=1500):
         want = binom.cdf(l - 1, K, q) - binom.cdf(j - 1, K, q)
         hits = 0
         for _ in range(trials):
-            idx = rg.integers(0, n, K)
-            y = x[idx].astype(np.float64) + rg.laplace(0.0, t, K)
-            ys = np.sort(y)
-            aL = ys[j - 1] if j >= 1 else -math.inf
-            aR = ys[l - 1] if l <= K else math.inf
+            y = O.iid_sample(x, rg.integers(0, n, K), rg.laplace(0.0, t, K).astype(np.float32))
+            aL, aR = O.order_statistic(y, j), O.order_statistic(y, l)
             hits += (aL <= b < aR)
         freq = hits / trials
         sd = math.sqrt(want * (1 - want) / trials)

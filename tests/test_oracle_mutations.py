@@ -158,6 +158,10 @@ def _bad_sampler(r32, noise32):
     return (r32[idx] + eps).astype(np.float32)
 
 
+def _bad_iid_sample(r32, idx, noise32):
+    return O.systematic_sample(r32, noise32)  # the indices ignored
+
+
 MUTANTS = {
     "cdf_sign": ("laplace_cdf", _bad_cdf_sign),
     "cdf_branch": ("laplace_cdf", _bad_cdf_branch),
@@ -178,6 +182,7 @@ MUTANTS = {
     "widen_sequential": ("widen", _bad_widen),
     "order_stat_0based": ("order_statistic", _bad_order_stat),
     "sampler_stride": ("systematic_sample", _bad_sampler),
+    "iid_sampler_ignores_indices": ("iid_sample", _bad_iid_sample),
 }
 
 CHECKS = [
