@@ -152,7 +152,9 @@ int lapsum_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64_t k,
  * Algorithm 1, validated path of Suppl. D):
  *
  *  1. systematic sample of K kernel-noised scores,
- *     y_s = fl32(r[s * floor(n / K)] + noise[s]), s = 0..K-1;
+ *     y_s = fl32(r[s * floor(n / K)] + noise[s]), s = 0..K-1 (the deployed
+ *     sampler of §4), or with sample_idx the i.i.d. sample that the coverage
+ *     theorem of Suppl. C assumes, y_s = fl32(r[sample_idx[s]] + noise[s]);
  *  2. ranks of Eq. (8) in IEEE float64: q = (n - k) / n,
  *     j = floor(K q - z sqrt(K q (1 - q))), l = ceil(K q + z sqrt(K q (1 - q)));
  *     a_L = y_(j), a_R = y_(l) (1-based order statistics; j < 1 gives
@@ -191,6 +193,9 @@ int lapsum_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64_t k,
  *               5.16), finite and > 0.
  *   noise       [K] float32 Laplace(0, |alpha|) draws, shared by all rows
  *               (the cached kernel noise); required.
+ *   sample_idx  NULL (systematic sample), or [K] int32 indices drawn
+ *               uniformly from [0, n) by the caller, shared by all rows
+ *               (i.i.d. sample); entries outside [0, n) are clamped to it.
  *   m_capacity  largest |M| the workspace holds, >= 1.
  *   flags       0, or LAPSUM_FLAG_FULL_SORT to skip the bracket and solve
  *               by the full-sort path (same outputs; info->fell_back = 1).
@@ -231,8 +236,8 @@ size_t lapsum_band_size(int64_t batch, int64_t n);
 
 int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n,
                              double k, double alpha, int64_t K, double z,
-                             const float* noise, int64_t m_capacity,
-                             uint32_t flags, float* p, double* b,
+                             const float* noise, const int32_t* sample_idx,
+                             int64_t m_capacity, uint32_t flags, float* p, double* b,
                              lapsum_bracket_info* info, int32_t* m_idx_out,
                              void* band, size_t band_bytes,
                              void* workspace, size_t workspace_bytes,

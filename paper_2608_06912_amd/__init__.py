@@ -83,7 +83,7 @@ def load():
     lib.lapsum_backward.restype = i32
     lib.lapsum_forward_bracketed_workspace_size.argtypes = [i64, i64, i64, i64, i32]
     lib.lapsum_forward_bracketed_workspace_size.restype = sz
-    lib.lapsum_forward_bracketed.argtypes = [vp, i64, i64, f64, f64, i64, f64, vp, i64, u32,
+    lib.lapsum_forward_bracketed.argtypes = [vp, i64, i64, f64, f64, i64, f64, vp, vp, i64, u32,
                                              vp, vp, vp, vp, vp, sz, vp, sz, vp]
     lib.lapsum_forward_bracketed.restype = i32
     lib.lapsum_band_size.argtypes = [i64, i64]
@@ -304,9 +304,10 @@ def _band_arg(band, batch, n):
 def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float = 5.16,
                              m_capacity: int | None = None, flags: int = 0,
                              m_idx: bool = False, band=None, workspace=None, out=None,
-                             b_out=None):
+                             b_out=None, sample_idx=None):
     """Bracketed forward.  noise: float32 CUDA tensor [K] of Laplace(0, |alpha|)
-    draws.  band: None, or a buffer from new_band() that receives the band for
+    draws.  sample_idx: None (systematic sample) or an int32 CUDA tensor [K]
+    of indices in [0, n) for the i.i.d. sample.  band: None, or a buffer from new_band() that receives the band for
     lapsum_backward_band.  out / b_out: optional buffers for p (float32, the
     shape of scores) and b (float64, [batch]).  Returns (p, b, infos, m_idx or
     None) with infos a list of dicts."""
@@ -317,6 +318,11 @@ def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float 
         raise ValueError("noise must be 1-D [K]")
     _rows(noise, "noise")
     K = int(noise.shape[0])
+    if sample_idx is not None:
+        if (not isinstance(sample_idx, torch.Tensor) or sample_idx.dtype != torch.int32
+                or tuple(sample_idx.shape) != (K,) or sample_idx.device != scores.device
+                or not sample_idx.is_contiguous()):
+            raise ValueError("sample_idx must be a contiguous int32 tensor [K] on the scores' device")
     if m_capacity is None:
         m_capacity = default_m_capacity(n, K)
     dev = scores.device
@@ -341,7 +347,8 @@ def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float 
     bp, bbytes = _band_arg(band, batch, n)
     with _on_device(dev):
         _check(lib.lapsum_forward_bracketed(_ptr(scores), batch, n, float(k), float(alpha), K,
-                                            float(z), _ptr(noise), int(m_capacity), int(flags),
+                                            float(z), _ptr(noise), _ptr(sample_idx),
+                                            int(m_capacity), int(flags),
                                             _ptr(p), _ptr(b), ctypes.cast(infos, ctypes.c_void_p),
                                             _ptr(mi), bp, bbytes, _ptr(ws), nbytes, _stream(dev)),
                "lapsum_forward_bracketed")

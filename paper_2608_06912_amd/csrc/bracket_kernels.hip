@@ -35,7 +35,8 @@ constexpr int PW = PT / kWave;                 // 4 waves
 
 // ----------------------------------------------------------------- sample --
 // Block b draws samples [b SB, b SB + SB) (kSampleItems per thread, all loads
-// in flight together) and writes their keys grouped by the top 11 bits
+// in flight together; sample s reads r[s floor(n/K)], or r[idx[s]] when the
+// caller gives i.i.d. indices) and writes their keys grouped by the top 11 bits
 // (kSelectBins bins, any order inside a bin) into its own region of ykeys,
 // with the exclusive bin offsets soffs[b (kSelectBins + 1) + bin], the bin
 // counts packed two to a word (16 bits each) in scnt[b kSampleCntWords + i]
@@ -45,6 +46,7 @@ constexpr int PW = PT / kWave;                 // 4 waves
 __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __restrict__ r,
                                                                 int64_t n,
                                                                 const float* __restrict__ noise,
+                                                                const int32_t* __restrict__ idx,
                                                                 int64_t K, uint32_t* __restrict__ ykeys,
                                                                 uint32_t* __restrict__ soffs,
                                                                 uint32_t* __restrict__ scnt,
@@ -64,7 +66,12 @@ __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __r
   for (int i = 0; i < kSampleItems; ++i) {
     const int64_t s = base + static_cast<int64_t>(i) * kSampleThreads + tid;
     const int64_t sc = s < K ? s : K - 1;
-    rv[i] = r[sc * stride];
+    int64_t at = sc * stride;
+    if (idx) {   // i.i.d. sampler: the caller's indices, clamped to the row
+      const int32_t q = idx[sc];
+      at = q < 0 ? 0 : (q >= n ? n - 1 : q);
+    }
+    rv[i] = r[at];
     ev[i] = noise[sc];
   }
   __syncthreads();
@@ -128,12 +135,12 @@ __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __r
 
 int sample_blocks(int64_t K) { return static_cast<int>((K + kSampleBlock - 1) / kSampleBlock); }
 
-hipError_t launch_sample(const float* r, int64_t n, const float* noise, int64_t K,
-                         uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,
+hipError_t launch_sample(const float* r, int64_t n, const float* noise, const int32_t* idx,
+                         int64_t K, uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,
                          int64_t zero_words, hipStream_t s) {
   { ProfScope ps_("sample", s);
   hipLaunchKernelGGL(sample_kernel, dim3(static_cast<unsigned>(sample_blocks(K))),
-                     dim3(kSampleThreads), 0, s, r, n, noise, K, ykeys, soffs, scnt, zero,
+                     dim3(kSampleThreads), 0, s, r, n, noise, idx, K, ykeys, soffs, scnt, zero,
                      zero_words); }
   return hipGetLastError();
 }

@@ -204,8 +204,9 @@ hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s);
 // to a word, then the counts of the kSelectGroups groups of bins); the
 // sample also clears zero[0 .. zero_words) for passes that accumulate later.
 int sample_blocks(int64_t K);
-hipError_t launch_sample(const float* r, int64_t n, const float* noise, int64_t K,
-                         uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,
+// idx: null (systematic sample) or [K] indices of the i.i.d. sample.
+hipError_t launch_sample(const float* r, int64_t n, const float* noise, const int32_t* idx,
+                         int64_t K, uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,
                          int64_t zero_words, hipStream_t s);
 hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* soffs,
                          const uint32_t* scnt, int64_t j, int64_t l, SelectRec* out,

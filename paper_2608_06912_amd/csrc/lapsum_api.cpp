@@ -371,7 +371,7 @@ int wait_seq(const HostStage* h, uint32_t want, hipStream_t s) {
 }
 
 int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, double z,
-                  const float* noise, int64_t mcap, int64_t out_cap, uint32_t flags, float* p_row,
+                  const float* noise, const int32_t* sample_idx, int64_t mcap, int64_t out_cap, uint32_t flags, float* p_row,
                   double* b_row, lapsum_bracket_info* info, int32_t* midx_row, void* band_row,
                   BracketWs& w, hipStream_t s) {
   const double t = -alpha;
@@ -391,7 +391,7 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
   if (st != LAPSUM_OK) return st;
 
   if (!(flags & LAPSUM_FLAG_FULL_SORT)) {
-    LAPSUM_TRY(launch_sample(r, n, noise, K, w.ykeys, w.soffs, w.scnt, w.hist, kBucketAccWords, s));
+    LAPSUM_TRY(launch_sample(r, n, noise, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist, kBucketAccWords, s));
     LAPSUM_TRY(launch_select(w.ykeys, K, w.soffs, w.scnt, j, l, w.sel, s));
     float aL = 0.0f, aR = 0.0f;
     const bool want_idx = midx_row != nullptr;
@@ -683,7 +683,8 @@ size_t lapsum_band_size(int64_t batch, int64_t n) {
 }
 
 int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n, double k, double alpha,
-                             int64_t K, double z, const float* noise, int64_t m_capacity,
+                             int64_t K, double z, const float* noise,
+                             const int32_t* sample_idx, int64_t m_capacity,
                              uint32_t flags, float* p, double* b, lapsum_bracket_info* info,
                              int32_t* m_idx_out, void* band, size_t band_bytes, void* workspace,
                              size_t workspace_bytes, hipStream_t stream) {
@@ -704,7 +705,8 @@ int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n, doub
   const size_t band_row_bytes = band_ctx_bytes(n);
   for (int64_t row = 0; row < batch; ++row) {
     void* band_row = band ? static_cast<char*>(band) + row * band_row_bytes : nullptr;
-    int st = bracketed_row(scores + row * n, n, k, alpha, K, z, noise, mcap, m_capacity, flags,
+    int st = bracketed_row(scores + row * n, n, k, alpha, K, z, noise, sample_idx, mcap,
+                           m_capacity, flags,
                            p + row * n, b + row, info ? info + row : nullptr,
                            m_idx_out ? m_idx_out + row * m_capacity : nullptr, band_row, w, stream);
     if (st != LAPSUM_OK) return st;

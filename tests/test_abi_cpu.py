@@ -114,7 +114,7 @@ def test_bracketed_rejects_invalid_arguments(kw):
     a = dict(noise=1, K=100, z=5.16, m_capacity=64, flags=0, k=10.0)
     a.update(kw)
     st = lib.lapsum_forward_bracketed(v(1), 1, 1000, a["k"], -1.0, a["K"], a["z"], v(a["noise"]),
-                                      a["m_capacity"], a["flags"], v(1), v(1), v(0), v(0), v(0),
+                                      v(0), a["m_capacity"], a["flags"], v(1), v(1), v(0), v(0), v(0),
                                       0, v(0), 0, v(0))
     assert st == 1
 
@@ -124,7 +124,8 @@ def test_bracketed_rejects_a_short_or_misaligned_band():
     v = ctypes.c_void_p
     need = L.lapsum_band_size(1, 1000)
     for ptr, size in ((256, need - 1), (128, need)):
-        st = lib.lapsum_forward_bracketed(v(1), 1, 1000, 10.0, -1.0, 100, 5.16, v(1), 64, 0, v(1),
+        st = lib.lapsum_forward_bracketed(v(1), 1, 1000, 10.0, -1.0, 100, 5.16, v(1), v(0), 64, 0,
+                                          v(1),
                                           v(1), v(0), v(0), v(ptr), size, v(0), 0, v(0))
         assert st == 1
 

@@ -474,6 +474,37 @@ def test_bracketed_batched_rows_of_odd_length(lib):
         check_params(float(gk[i]), float(ga[i]), rows[i], float(bn[i]), alpha, gs[i], f"row {i}")
 
 
+@pytest.mark.parametrize("dist,n,kfrac,alpha,batch", [
+    ("normal", 200_000, 1 / 16, -1.0, 1), ("normal", 300_007, 1 / 3, -0.002, 1),
+    ("student2", 1_000_003, 1e-4, -0.05, 1), ("lognormal", 100_003, 1 / 8, -0.01, 3)])
+def test_bracketed_iid_sampler(lib, dist, n, kfrac, alpha, batch):
+    # the i.i.d. sample of the coverage theorem: y_s = r[idx_s] + eps_s at
+    # indices the caller draws (shared by the rows of a batch)
+    rows = W.random_case(45, n, dist=dist, batch=batch)
+    k = n * kfrac
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([92, n], K, -alpha)
+    idx = W.sample_indices([93, n], n, K)
+    band = lib.new_band(batch, n, "cuda")
+    p, b, infos, _ = lib.lapsum_forward_bracketed(_t(rows), k, alpha, _t(noise), band=band,
+                                                  sample_idx=_t(idx))
+    gs = W.random_case(46, n, dist="normal", batch=batch)
+    grad = _np(lib.lapsum_backward_band(_t(gs), p, band, alpha))
+    pn, bn = _np(p), _np(b)
+    for i in range(batch):
+        label = f"{dist} n={n} row {i}"
+        po, bo, oinfo, _ = O.bracketed_forward(rows[i], k, alpha, noise, sample_idx=idx)
+        _check_info(infos[i], oinfo, label)
+        assert abs(float(bn[i]) - bo) <= 2e-6 * -alpha, label
+        assert np.max(np.abs(pn[i].astype(np.float64) - O.probs(rows[i], bo, alpha))) <= P_TOL, label
+        assert O.budget_error(pn[i], k) <= sum_tol(k), label
+        assert grad_rel(grad[i], O.vjp(rows[i], bo, alpha, gs[i])) <= G_TOL, label
+        # the two samplers draw different brackets around the same root
+        if i == 0:
+            so = O.bracketed_forward(rows[i], k, alpha, noise)[2]
+            assert (so.a_L, so.a_R) != (oinfo.a_L, oinfo.a_R) or so.attempts != oinfo.attempts
+
+
 @pytest.mark.parametrize("n", [700, 1024, 1025])
 def test_bracketed_rows_of_about_one_tile(lib, n):
     # one writer workgroup; the last tile whole, partial, or a single score

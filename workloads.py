@@ -35,7 +35,7 @@ import math
 import numpy as np
 
 __all__ = ["Workload", "WORKLOADS", "get", "scores", "upstream_grad",
-           "bracket_noise", "default_sample_size", "laplace_noise"]
+           "bracket_noise", "default_sample_size", "laplace_noise", "sample_indices"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -141,6 +141,12 @@ def upstream_grad(name: str) -> np.ndarray:
 def laplace_noise(seed, count: int, scale: float) -> np.ndarray:
     """`count` float32 draws of Laplace(0, scale) from default_rng(seed)."""
     return np.random.default_rng(seed).laplace(0.0, scale, count).astype(np.float32)
+
+
+def sample_indices(seed, n: int, K: int) -> np.ndarray:
+    """K indices drawn uniformly from [0, n) with replacement (int32), the
+    draws of an i.i.d. bracket sample."""
+    return np.random.default_rng(seed).integers(0, n, K).astype(np.int32)
 
 
 def bracket_noise(name: str) -> np.ndarray:
