@@ -41,10 +41,10 @@ HBM_PEAK_GBS = 8000.0
 # measurement; once that file changes the figure no longer describes the
 # kernel and is reported as null.
 MEASURED_TRAFFIC = {
-    "band_emit": ("band_kernels.hip", "283a3cddadfd71026920a615b48d8f90b747c3fa", 427.2e6),
-    "band_vjp_emit": ("band_kernels.hip", "283a3cddadfd71026920a615b48d8f90b747c3fa", 443.6e6),
-    "band_vjp_reduce": ("band_kernels.hip", "283a3cddadfd71026920a615b48d8f90b747c3fa", 61.3e6),
-    "partition": ("bracket_kernels.hip", "d923efb3ca4b3562671a1eee0dc2017c323bbb0e", 413.8e6),
+    "band_emit": ("band_kernels.hip", "a61fa181fbae50e8681e6c0e83c8de8748b4135d", 427.2e6),
+    "band_vjp_emit": ("band_kernels.hip", "a61fa181fbae50e8681e6c0e83c8de8748b4135d", 443.6e6),
+    "band_vjp_reduce": ("band_kernels.hip", "a61fa181fbae50e8681e6c0e83c8de8748b4135d", 61.3e6),
+    "partition": ("bracket_kernels.hip", "6a0009ad98b16e5251c8423291f3af49c634ea6e", 413.8e6),
 }
 METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
 

@@ -25,7 +25,7 @@ from . import (lapsum_backward, lapsum_backward_band, lapsum_forward, lapsum_for
                lapsum_topk_mask, new_band)
 
 __all__ = ["soft_topk", "hard_topk_mask", "straight_through", "choose_path", "sample_size",
-           "bracket_noise", "LapSumFunction", "FULL_SORT_MAX_N"]
+           "bracket_noise", "bracket_indices", "LapSumFunction", "FULL_SORT_MAX_N"]
 
 # Rows up to this length take the full sort; longer rows the sample bracket.
 # §4 places the switch where the two paths cost the same; on MI355X the
@@ -78,6 +78,23 @@ def bracket_noise(K: int, t: float, device, seed: int = 0):
     return hit
 
 
+_index_cache: dict = {}
+
+
+def bracket_indices(K: int, n: int, device, seed: int = 0):
+    """K indices drawn uniformly from [0, n) with replacement (int32), for the
+    i.i.d. sampler of the coverage theorem (Suppl. C); cached like the noise."""
+    device = torch.device(device)
+    key = (int(K), int(n), str(device), int(seed))
+    hit = _index_cache.get(key)
+    if hit is None:
+        gen = torch.Generator(device="cpu").manual_seed(int(seed) + 0x5EED)
+        hit = torch.randint(0, int(n), (int(K),), generator=gen, dtype=torch.int64)
+        hit = hit.to(torch.int32).to(device)
+        _index_cache[key] = hit
+    return hit
+
+
 def _as_rows(scores):
     if scores.dim() < 1:
         raise ValueError("scores must have at least one dimension")
@@ -91,13 +108,14 @@ def _as_rows(scores):
 class LapSumFunction(torch.autograd.Function):
     """p = LapSum_k(scores; alpha) over the last dimension.
 
-    forward(scores, k, alpha, path, K, z, noise_seed, want_perm) returns p
+    forward(scores, k, alpha, path, K, z, noise_seed, want_perm, sampler)
+    returns p
     (and, with want_perm on the full path, the descending order as a
     non-differentiable int32 tensor).  k and alpha may be Python numbers or
     tensors; as tensors they receive dL/dk and dL/dalpha."""
 
     @staticmethod
-    def forward(ctx, scores, k, alpha, path, K, z, noise_seed, want_perm):
+    def forward(ctx, scores, k, alpha, path, K, z, noise_seed, want_perm, sampler="systematic"):
         kf = float(k)
         af = float(alpha)
         x, n = _as_rows(scores)
@@ -108,8 +126,15 @@ class LapSumFunction(torch.autograd.Function):
             band = None
         elif path == "bracketed":
             noise = bracket_noise(K, -af, x.device, noise_seed)
+            if sampler == "systematic":
+                idx = None
+            elif sampler == "iid":
+                idx = bracket_indices(K, n, x.device, noise_seed)
+            else:
+                raise ValueError(f"unknown sampler {sampler!r}")
             band = new_band(x.shape[0], n, x.device)
-            p, b, _, _ = lapsum_forward_bracketed(x, kf, af, noise, z=z, band=band)
+            p, b, _, _ = lapsum_forward_bracketed(x, kf, af, noise, z=z, band=band,
+                                                  sample_idx=idx)
             perm = None
         else:
             raise ValueError(f"unknown path {path!r}")
@@ -146,7 +171,7 @@ class LapSumFunction(torch.autograd.Function):
         if ctx.needs_input_grad[2]:
             like = ctx.alpha_like
             grad_alpha = ga.sum().to(device=like.device, dtype=like.dtype).reshape(like.shape)
-        return grad_scores, grad_k, grad_alpha, None, None, None, None, None
+        return grad_scores, grad_k, grad_alpha, None, None, None, None, None, None
 
 
 def straight_through(p, m):
@@ -167,26 +192,27 @@ def hard_topk_mask(scores, k: int):
 
 
 def soft_topk(scores, k, alpha, *, path: str = "auto", sample: str = "n23", z: float = 5.16,
-              noise_seed: int = 0, ste: bool = False):
+              noise_seed: int = 0, sampler: str = "systematic", ste: bool = False):
     """Differentiable exact-budget soft top-k over the last dimension.
 
     path: "full" (sort), "bracketed" (sample bracket, §4) or "auto"
     (choose_path by row length).  sample: the bracket's sample-size rule
-    (sample_size).  ste=True returns the hard mask with the soft p's
+    (sample_size); sampler: "systematic" (§4's strided view) or "iid"
+    (uniform indices, the coverage theorem's model).  ste=True returns the hard mask with the soft p's
     gradient; k must then be an integer."""
     n = scores.shape[-1]
     if path == "auto":
         path = choose_path(n)
     K = sample_size(n, sample) if path == "bracketed" else 0
     if not ste:
-        return LapSumFunction.apply(scores, k, alpha, path, K, z, noise_seed, False)
+        return LapSumFunction.apply(scores, k, alpha, path, K, z, noise_seed, False, sampler)
     kf = float(k)
     if int(kf) != kf:
         raise ValueError("ste=True needs an integer k")
     if path == "full":
-        p, perm = LapSumFunction.apply(scores, k, alpha, path, K, z, noise_seed, True)
+        p, perm = LapSumFunction.apply(scores, k, alpha, path, K, z, noise_seed, True, sampler)
         m = lapsum_topk_mask(perm.reshape(-1, n).contiguous(), int(kf)).reshape(scores.shape)
     else:
-        p = LapSumFunction.apply(scores, k, alpha, path, K, z, noise_seed, False)
+        p = LapSumFunction.apply(scores, k, alpha, path, K, z, noise_seed, False, sampler)
         m = hard_topk_mask(scores.detach(), int(kf))
     return straight_through(p, m)

@@ -201,9 +201,8 @@ __device__ void prefix_hist(const uint32_t* keys, int64_t count, int hi, uint32_
 // outside 1..K gives -inf (below) or +inf (above).  Level 1 (top 11 bits)
 // locates each target's group of bins from the sample blocks' group counts,
 // then its bin from the bin counts of that group only.  A bin of at most
-// kFewCand keys is
-// gathered into LDS in any order and its key of the target rank found by
-// counting; otherwise the bin's keys are fetched from every block's region
+// kFewCand keys is gathered into LDS in any order and its key of the target
+// rank found by counting; otherwise the bin's keys are fetched from every block's region
 // (only that bin) into LDS, where bits 10..20 and 0..9 are resolved, and a
 // bin too large for LDS is resolved by passes over all keys in memory.
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __restrict__ ykeys,

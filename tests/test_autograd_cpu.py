@@ -60,3 +60,13 @@ def test_no_cpu_fallback():
         A.soft_topk(x, 4.0, -1.0)
     with pytest.raises(ValueError):
         A.hard_topk_mask(x, 4)
+
+
+def test_bracket_indices_are_uniform_and_cached():
+    from scipy import stats
+    idx = A.bracket_indices(50000, 1000, "cpu", seed=3)
+    assert idx.dtype == torch.int32 and idx.shape == (50000,)
+    assert int(idx.min()) >= 0 and int(idx.max()) < 1000
+    assert A.bracket_indices(50000, 1000, "cpu", seed=3) is idx
+    counts = np.bincount(idx.numpy(), minlength=1000)
+    assert stats.chisquare(counts).pvalue > 1e-3

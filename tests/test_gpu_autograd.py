@@ -39,9 +39,11 @@ def _check_rows(r, w, b_rows, alpha, grad, gk, ga, label):
     assert abs(ga - ref_a) <= tol_a, (label, ga, ref_a, tol_a)
 
 
-@pytest.mark.parametrize("path,n,batch", [("full", 5000, 3), ("full", 40000, 2),
-                                          ("bracketed", 200_000, 1), ("bracketed", 300_007, 2)])
-def test_soft_topk_forward_and_gradients(lib, path, n, batch):
+@pytest.mark.parametrize("path,n,batch,sampler,sample", [
+    ("full", 5000, 3, "systematic", "n23"), ("full", 40000, 2, "systematic", "n23"),
+    ("bracketed", 200_000, 1, "systematic", "n23"), ("bracketed", 300_007, 2, "systematic", "n23"),
+    ("bracketed", 250_000, 2, "iid", "n23"), ("bracketed", 1_000_000, 1, "systematic", "sqrt")])
+def test_soft_topk_forward_and_gradients(lib, path, n, batch, sampler, sample):
     A = _A()
     rg = np.random.default_rng([61, n])
     r = rg.standard_normal((batch, n)).astype(np.float32)
@@ -51,16 +53,19 @@ def test_soft_topk_forward_and_gradients(lib, path, n, batch):
     k = torch.tensor(kv, dtype=torch.float64, requires_grad=True)         # host tensor
     a = torch.tensor(av, dtype=torch.float32, device="cuda", requires_grad=True)
     av = float(a.item())        # the float32 temperature the forward sees
-    p = A.soft_topk(x, k, a, path=path)
+    p = A.soft_topk(x, k, a, path=path, sampler=sampler, sample=sample)
     assert p.shape == x.shape and p.requires_grad
     (p * torch.from_numpy(w).cuda()).sum().backward()
     # the forward is the library's forward of the same path
     if path == "full":
         p2, b2 = lib.lapsum_forward(torch.from_numpy(r).cuda(), kv, av)
     else:
-        K = A.sample_size(n)
+        K = A.sample_size(n, sample)
         noise = A.bracket_noise(K, -av, "cuda")
-        p2, b2, infos, _ = lib.lapsum_forward_bracketed(torch.from_numpy(r).cuda(), kv, av, noise)
+        idx = A.bracket_indices(K, n, "cuda") if sampler == "iid" else None
+        p2, b2, infos, _ = lib.lapsum_forward_bracketed(torch.from_numpy(r).cuda(), kv, av, noise,
+                                                        sample_idx=idx)
+        assert all(not info["fell_back"] for info in infos)
     assert torch.equal(p.detach(), p2)
     b2 = b2.cpu().numpy()
     for i in range(batch):

@@ -505,6 +505,20 @@ def test_bracketed_iid_sampler(lib, dist, n, kfrac, alpha, batch):
             assert (so.a_L, so.a_R) != (oinfo.a_L, oinfo.a_R) or so.attempts != oinfo.attempts
 
 
+@pytest.mark.timeout(600)
+def test_bracketed_sqrt_sample_size(lib):
+    # the coarser sample K = ceil(2 sqrt(n)) on the n = 1e7 scores: a wider
+    # bracket, a larger middle set, the same b
+    w = W.get("n1e7")
+    r = W.scores("n1e7")[0]
+    K = int(np.ceil(2.0 * np.sqrt(w.n)))
+    noise = W.laplace_noise([94], K, w.t)
+    g = W.upstream_grad("n1e7")[0]
+    p, bg, bo, info = _check_bracketed(lib, r, w.k, w.alpha, noise, z=w.z, label="sqrt K", g=g)
+    assert not info["fell_back"] and info["n_M"] > 0
+    _sampled_p_check(p, r, bo, w.alpha)
+
+
 @pytest.mark.parametrize("n", [700, 1024, 1025])
 def test_bracketed_rows_of_about_one_tile(lib, n):
     # one writer workgroup; the last tile whole, partial, or a single score
