@@ -44,7 +44,7 @@ MEASURED_TRAFFIC = {
     "band_emit": ("band_kernels.hip", "a61fa181fbae50e8681e6c0e83c8de8748b4135d", 427.2e6),
     "band_vjp_emit": ("band_kernels.hip", "a61fa181fbae50e8681e6c0e83c8de8748b4135d", 443.6e6),
     "band_vjp_reduce": ("band_kernels.hip", "a61fa181fbae50e8681e6c0e83c8de8748b4135d", 61.3e6),
-    "partition": ("bracket_kernels.hip", "6a0009ad98b16e5251c8423291f3af49c634ea6e", 413.8e6),
+    "partition": ("bracket_kernels.hip", "7ef29aa11dc7e2a3c42411e98ce3ec5a8af81bf0", 413.8e6),
 }
 METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
 
