@@ -277,6 +277,56 @@ def check_params_scale_identity():
         assert abs(a * ga - rhs) <= 1e-12 * max(scale, abs(rhs), 1.0), (a * ga, rhs)
 
 
+def check_dftopk_fd(cases=((64, 8, -0.5), (48, 24, -0.05), (33, 1, -2.0), (33, 32, -1.0))):
+    """The DFTopK vector-Jacobian product against centred finite differences
+    of <g, p(r)>.  The operator reads float32 scores, so the scores are
+    float32 values in (-2, 2) and the step is 2^-14, exact in float32 there;
+    the scores are drawn until no two lie within 8 steps, so no pair swaps
+    and the boundary pair stays the same."""
+    eps = 2.0 ** -14
+    for ci, (n, k, a) in enumerate(cases):
+        rg = np.random.default_rng([31, ci])
+        while True:
+            x = rg.uniform(-2.0, 2.0, n).astype(np.float32).astype(np.float64)
+            if np.min(np.diff(np.sort(x))) > 8 * eps:
+                break
+        g = rg.standard_normal(n)
+        an = O.dftopk_vjp(x, k, a, g)
+        fd = np.empty(n)
+        for i in range(n):
+            xp = x.copy(); xp[i] += eps
+            xm = x.copy(); xm[i] -= eps
+            fd[i] = (np.dot(g, O.dftopk(xp, k, a)[0]) - np.dot(g, O.dftopk(xm, k, a)[0])) / (2 * eps)
+        rel = np.max(np.abs(an - fd)) / np.max(np.abs(fd))
+        # centred differences err by h^2/6 times the third derivative,
+        # at most 1/(8 t^2) of the first for the logistic step
+        assert rel <= 1e-6, (ci, rel)
+
+
+def check_dftopk_midpoint_is_the_zero_temperature_threshold():
+    """Theorem 1: LapSum's threshold tends to the midpoint of r_(k), r_(k+1)
+    as t -> 0; DFTopK fixes its threshold there at every t."""
+    rg = np.random.default_rng(41)
+    for _ in range(8):
+        n = int(rg.integers(2, 300))
+        k = int(rg.integers(1, n))
+        x = rg.standard_normal(n).astype(np.float32)
+        assert O.dftopk(x, k, -0.3)[1] == O.zero_temperature_threshold(x, k)
+
+
+def check_dftopk_budget_table(rows):
+    """Table budget, DFTopK row: the relative mass error |sum p - k|/k on
+    Gaussian scores with k = n/16, alpha = -1, within the sampling spread of
+    one draw (4 standard deviations of the mean of the logistic step, plus
+    the table's rounding)."""
+    for n, want in rows:
+        x = np.random.default_rng([51, n]).standard_normal(n).astype(np.float32)
+        p = O.dftopk(x, n // 16, -1.0)[0]
+        got = abs(math.fsum(p) - n // 16) / (n // 16)
+        spread = 16.0 * 0.3 / math.sqrt(n) * 4.0 + 0.005
+        assert abs(got - want) <= spread, (n, got, want, spread)
+
+
 def check_desc_order():
     """Descending by value; equal values keep ascending index; -0.0 after +0.0."""
     rg = np.random.default_rng(1)

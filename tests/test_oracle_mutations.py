@@ -162,6 +162,30 @@ def _bad_iid_sample(r32, idx, noise32):
     return O.systematic_sample(r32, noise32)  # the indices ignored
 
 
+_orig_dftopk = O.dftopk
+_orig_dftopk_vjp = O.dftopk_vjp
+
+
+def _bad_dftopk_step(r, k, alpha):
+    p, c, b = _orig_dftopk(r, k, alpha)
+    u = (np.asarray(r, np.float32).astype(_F64) - c) / -alpha
+    return np.where(u <= 0, 0.5 * np.exp(u), 1 - 0.5 * np.exp(-u)), c, b   # Laplace CDF step
+
+
+def _bad_dftopk_ranks(r, k, alpha):
+    r32 = np.asarray(r, np.float32).ravel()
+    o = O.desc_order(r32)
+    p, _, _ = _orig_dftopk(r, k, alpha)
+    c = 0.5 * (float(r32[o[k - 1]]) + float(r32[o[max(k - 2, 0)]]))   # r_(k-1), r_(k)
+    u = (r32.astype(_F64) - c) / -alpha
+    return 1.0 / (1.0 + np.exp(-u)), c, (int(o[k - 1]), int(o[max(k - 2, 0)]))
+
+
+def _bad_dftopk_vjp(r, k, alpha, g):
+    p = _orig_dftopk(r, k, alpha)[0]
+    return np.asarray(g, _F64) * p * (1 - p) / -alpha   # threshold held fixed
+
+
 MUTANTS = {
     "cdf_sign": ("laplace_cdf", _bad_cdf_sign),
     "cdf_branch": ("laplace_cdf", _bad_cdf_branch),
@@ -183,6 +207,9 @@ MUTANTS = {
     "order_stat_0based": ("order_statistic", _bad_order_stat),
     "sampler_stride": ("systematic_sample", _bad_sampler),
     "iid_sampler_ignores_indices": ("iid_sample", _bad_iid_sample),
+    "dftopk_laplace_step": ("dftopk", _bad_dftopk_step),
+    "dftopk_wrong_pair": ("dftopk", _bad_dftopk_ranks),
+    "dftopk_vjp_fixed_threshold": ("dftopk_vjp", _bad_dftopk_vjp),
 }
 
 CHECKS = [
@@ -194,6 +221,8 @@ CHECKS = [
     pins.check_vjp_invariants,
     lambda: pins.check_params_fd(((24, 6.0, -1.0), (40, 13.5, -0.3)), tol=1e-6),
     pins.check_params_closed_forms, pins.check_params_scale_identity,
+    pins.check_dftopk_fd, pins.check_dftopk_midpoint_is_the_zero_temperature_threshold,
+    lambda: pins.check_dftopk_budget_table([(10000, 2.46), (100000, 2.47)]),
     pins.check_bracket_ranks, pins.check_partition_definition,
     pins.check_sampler_and_order_statistic, pins.check_widen_rule,
     pins.check_bracket_equals_full, pins.check_forced_widening,

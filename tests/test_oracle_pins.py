@@ -141,3 +141,28 @@ def test_oracle_rejects_invalid_arguments():
             O.solve_bisect(x, k, a)
     with pytest.raises(ValueError):
         O.solve_bisect(np.array([np.inf], dtype=np.float32), 0.5, -1.0)
+
+
+def _dftopk_rows():
+    rows = []
+    with open(os.path.join(GOLDEN, "dftopk_budget_table.txt")) as fh:
+        for line in fh:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                n, v = line.split()
+                rows.append((int(n), float(v)))
+    return rows
+
+
+def test_dftopk_budget_error_matches_the_table():
+    rows = _dftopk_rows()
+    assert [n for n, _ in rows] == [1000, 10000, 100000, 1000000, 10000000]
+    pins.check_dftopk_budget_table([r for r in rows if r[0] <= 1000000])
+
+
+def test_dftopk_vjp_matches_finite_differences():
+    pins.check_dftopk_fd()
+
+
+def test_dftopk_midpoint_is_the_zero_temperature_threshold():
+    pins.check_dftopk_midpoint_is_the_zero_temperature_threshold()
