@@ -56,6 +56,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=20_000_000)
+    ap.add_argument("--comparators", action="store_true",
+                    help="also time the comparators (bisection baseline, DFTopK) against the "
+                         "operator in the paper's settings, outside the timed region")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 4e8-byte device copy (outside the timed region) so a "
                          "counter profile can calibrate its byte counters")
@@ -127,6 +130,82 @@ def cpu_baseline(r_full, noise_full, w, n_s: int):
                   f"workload), float64 bracketed model + Eq. (5) VJP, {dt:.1f} s "
                   f"(NumPy, single-threaded; host cores available: {len(os.sched_getaffinity(0))})",
     }
+
+
+def _timed_ms(fn, iters=20, warmup=3):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(iters):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / iters
+
+
+def comparators(dev):
+    """The paper's comparisons on this device: the per-query bisection
+    baseline at B = 256, n = 4096 (§5 "Speed"); DFTopK forward + backward at
+    k = floor(n/2), batch 1 (Suppl. "Comparison with DFTopK" protocol)
+    against the operator's forward + backward (sort up to 2^21 scores, the
+    bracket above); the realised budget error on Gaussian scores, k = n/16,
+    alpha = -1 (Table budget).  Synthetic Gaussian scores throughout."""
+    import numpy as np
+    import torch
+
+    import paper_2608_06912_amd as L
+    import paper_2608_06912_amd.autograd as A
+
+    out = {}
+    rg = np.random.default_rng(77)
+    r = torch.from_numpy(rg.standard_normal((256, 4096)).astype(np.float32)).to(dev)
+    bis = _timed_ms(lambda: L.lapsum_bisect_forward(r, 256.0, -1.0, 60), iters=5, warmup=1)
+    fast = _timed_ms(lambda: L.lapsum_forward(r, 256.0, -1.0))
+    out["bisection_b256_n4096"] = {"k": 256, "alpha": -1.0, "steps": 60, "bisect_fwd_ms": bis,
+                                   "lapsum_fwd_ms": fast, "speedup": bis / fast}
+    rows = []
+    for n in (10, 100, 1000, 10**4, 10**5, 10**6, 3 * 10**6):
+        x = torch.from_numpy(rg.standard_normal((1, n)).astype(np.float32)).to(dev)
+        g = torch.from_numpy(rg.standard_normal((1, n)).astype(np.float32)).to(dev)
+        k = n // 2
+        wsd = torch.empty(max(1, L.lapsum_dftopk_workspace_size(1, n)), dtype=torch.uint8,
+                          device=dev)
+
+        def dft():
+            p, _, pair = L.lapsum_dftopk_forward(x, k, -1.0, workspace=wsd)
+            L.lapsum_dftopk_backward(g, p, pair, -1.0, workspace=wsd)
+
+        path = A.choose_path(n)
+        if path == "full":
+            wsf = torch.empty(max(1, L.lapsum_forward_workspace_size(1, n)), dtype=torch.uint8,
+                              device=dev)
+            wsb = torch.empty(max(1, L.lapsum_backward_workspace_size(1, n)), dtype=torch.uint8,
+                              device=dev)
+
+            def fast_fb():
+                p, b = L.lapsum_forward(x, float(k), -1.0, workspace=wsf)
+                L.lapsum_backward(g, p, b, -1.0, workspace=wsb)
+        else:
+            K = A.sample_size(n)
+            noise = A.bracket_noise(K, 1.0, dev)
+            band = L.new_band(1, n, dev)
+
+            def fast_fb():
+                p, b, _, _ = L.lapsum_forward_bracketed(x, float(k), -1.0, noise, band=band)
+                L.lapsum_backward_band(g, p, band, -1.0)
+        rows.append({"n": n, "dftopk_fwd_bwd_ms": _timed_ms(dft),
+                     "lapsum_fwd_bwd_ms": _timed_ms(fast_fb), "lapsum_path": path})
+    out["dftopk_k_half_batch1"] = rows
+    n = 10**6
+    x = torch.from_numpy(rg.standard_normal((1, n)).astype(np.float32)).to(dev)
+    pd, _, _ = L.lapsum_dftopk_forward(x, n // 16, -1.0)
+    pf, _ = L.lapsum_forward(x, n / 16.0, -1.0)
+    k = n / 16.0
+    out["budget_rel_error_n1e6_k_n16_alpha_m1"] = {
+        "dftopk": abs(pd.double().sum().item() - k) / k,
+        "lapsum": abs(pf.double().sum().item() - k) / k}
+    return out
 
 
 def main():
@@ -275,6 +354,9 @@ def main():
         "active_scores": active,
         "band_scores": band_n,
     }
+    if args.comparators:
+        print("[bench] comparators", file=sys.stderr, flush=True)
+        out["comparators"] = comparators(dev)
     if not args.no_cpu_baseline:
         print(f"[bench] cpu baseline on {args.cpu_sample:.0e} scores", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(r_np[0], noise_np, w, args.cpu_sample)

@@ -148,6 +148,55 @@ int lapsum_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64_t k,
                      float* mask, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Comparators (not part of the operator): the two methods the paper measures
+ * Fast LapSum against, so that its speed and budget claims can be checked on
+ * this device.
+ *
+ * lapsum_bisect_forward: the per-query bisection baseline of §5 ("Speed"),
+ * the pattern of the original LapSum implementation: one thread per row runs
+ * `steps` bisection steps on LapSum(b) = k, each re-summing all n Laplace-CDF
+ * terms, in float32 throughout (scores, midpoints, terms and the running
+ * sum), from lo = min r - t (ln(n / (2(n - k)))^+ + 1) and
+ * hi = max r + t (ln(n / (2k))^+ + 1); b = the last midpoint, and p as in
+ * lapsum_forward.  The paper runs 60 steps.
+ *   scores, k, alpha, p, b   as in lapsum_forward (b: the float32 midpoint
+ *                            widened to float64)
+ *   steps                    0..200
+ *
+ * lapsum_dftopk_forward / _backward: DFTopK (§2; Suppl. "Comparison with
+ * DFTopK"): the threshold fixed at c = (r_(k) + r_(k+1)) / 2, the midpoint of
+ * the k-th and (k+1)-th largest scores of the row (equal scores ranked by
+ * index as in lapsum_forward's perm_out), and the logistic step
+ * p_i = 1 / (1 + e^{-(r_i - c)/t}) (the paper names a smooth step; its
+ * Table budget value for DFTopK, a mass 3.46 k at alpha = -1, is the
+ * logistic one).  The budget is not exact: sum p drifts from k.  The
+ * backward is the VJP of that map: grad_i = g_i s_i / t with
+ * s_i = p_i (1 - p_i), minus (1/(2t)) sum_j g_j s_j at the two boundary
+ * scores (c moves by 1/2 with each).  Rows are processed one after another
+ * (one device-wide sort each).
+ *   k       integer, 1 <= k < n (n >= 2)
+ *   c       [batch] float64 output: the thresholds
+ *   pair    [batch, 2] int32: forward output, backward input: the indices
+ *           of r_(k) and r_(k+1) in each row
+ *   workspace  lapsum_dftopk_workspace_size(batch, n) bytes, 256-aligned
+ * ------------------------------------------------------------------------ */
+int lapsum_bisect_forward(const float* scores, int64_t batch, int64_t n,
+                          double k, double alpha, int32_t steps, float* p,
+                          double* b, hipStream_t stream);
+
+size_t lapsum_dftopk_workspace_size(int64_t batch, int64_t n);
+
+int lapsum_dftopk_forward(const float* scores, int64_t batch, int64_t n,
+                          int64_t k, double alpha, float* p, double* c,
+                          int32_t* pair, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream);
+
+int lapsum_dftopk_backward(const float* grad_p, const float* p,
+                           const int32_t* pair, int64_t batch, int64_t n,
+                           double alpha, float* grad_r, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Bracketed forward for very long rows (paper §4, Suppl. B, Suppl. C,
  * Algorithm 1, validated path of Suppl. D):
  *

@@ -25,7 +25,8 @@ __all__ = [
     "lapsum_forward_bracketed_workspace_size", "lapsum_forward_bracketed",
     "LAPSUM_FLAG_FULL_SORT", "LIB_PATH", "lapsum_profile_start", "lapsum_profile_stop",
     "lapsum_band_size", "new_band", "lapsum_backward_band_workspace_size", "lapsum_backward_band",
-    "lapsum_topk_mask",
+    "lapsum_topk_mask", "lapsum_bisect_forward", "lapsum_dftopk_workspace_size",
+    "lapsum_dftopk_forward", "lapsum_dftopk_backward",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapsum.so")
@@ -92,6 +93,14 @@ def load():
     lib.lapsum_backward_band_workspace_size.restype = sz
     lib.lapsum_backward_band.argtypes = [vp, vp, vp, sz, i64, i64, f64, vp, vp, vp, vp, sz, vp]
     lib.lapsum_backward_band.restype = i32
+    lib.lapsum_bisect_forward.argtypes = [vp, i64, i64, f64, f64, i32, vp, vp, vp]
+    lib.lapsum_bisect_forward.restype = i32
+    lib.lapsum_dftopk_workspace_size.argtypes = [i64, i64]
+    lib.lapsum_dftopk_workspace_size.restype = sz
+    lib.lapsum_dftopk_forward.argtypes = [vp, i64, i64, i64, f64, vp, vp, vp, vp, sz, vp]
+    lib.lapsum_dftopk_forward.restype = i32
+    lib.lapsum_dftopk_backward.argtypes = [vp, vp, vp, i64, i64, f64, vp, vp, sz, vp]
+    lib.lapsum_dftopk_backward.restype = i32
     lib.lapsum_topk_mask.argtypes = [vp, i64, i64, i64, vp, vp]
     lib.lapsum_topk_mask.restype = i32
     lib.lapsum_profile_start.argtypes = []
@@ -224,6 +233,65 @@ def lapsum_topk_mask(perm, k: int, *, out=None):
         _check(lib.lapsum_topk_mask(_ptr(perm), int(batch), int(n), int(k), _ptr(mask),
                                     _stream(dev)), "lapsum_topk_mask")
     return mask
+
+
+def lapsum_bisect_forward(scores, k: float, alpha: float, steps: int = 60):
+    """Comparator: the per-query bisection baseline (one thread per row,
+    float32).  Returns (p, b)."""
+    torch = _torch()
+    lib = load()
+    batch, n = _rows(scores, "scores")
+    dev = scores.device
+    p = torch.empty_like(scores)
+    b = torch.empty(batch, dtype=torch.float64, device=dev)
+    with _on_device(dev):
+        _check(lib.lapsum_bisect_forward(_ptr(scores), batch, n, float(k), float(alpha), int(steps),
+                                         _ptr(p), _ptr(b), _stream(dev)), "lapsum_bisect_forward")
+    return p, b
+
+
+def lapsum_dftopk_workspace_size(batch: int, n: int) -> int:
+    return int(load().lapsum_dftopk_workspace_size(batch, n))
+
+
+def lapsum_dftopk_forward(scores, k: int, alpha: float, *, workspace=None):
+    """Comparator: DFTopK.  Returns (p, c, pair): c float64 [batch], pair
+    int32 [batch, 2] (indices of the k-th and (k+1)-th largest scores)."""
+    torch = _torch()
+    lib = load()
+    batch, n = _rows(scores, "scores")
+    if int(k) != k:
+        raise ValueError("k must be an integer")
+    dev = scores.device
+    p = torch.empty_like(scores)
+    c = torch.empty(batch, dtype=torch.float64, device=dev)
+    pair = torch.empty((batch, 2), dtype=torch.int32, device=dev)
+    ws, nbytes = _workspace(lib.lapsum_dftopk_workspace_size(batch, n), dev, workspace)
+    with _on_device(dev):
+        _check(lib.lapsum_dftopk_forward(_ptr(scores), batch, n, int(k), float(alpha), _ptr(p),
+                                         _ptr(c), _ptr(pair), _ptr(ws), nbytes, _stream(dev)),
+               "lapsum_dftopk_forward")
+    return p, c, pair
+
+
+def lapsum_dftopk_backward(grad_p, p, pair, alpha: float, *, workspace=None, out=None):
+    """Comparator: the DFTopK vector-Jacobian product."""
+    torch = _torch()
+    lib = load()
+    batch, n = _rows(p, "p")
+    if grad_p.shape != p.shape:
+        raise ValueError("grad_p and p must have the same shape")
+    _rows(grad_p, "grad_p")
+    if pair.dtype != torch.int32 or tuple(pair.shape) != (batch, 2) or not pair.is_contiguous():
+        raise ValueError("pair must be a contiguous int32 tensor [batch, 2]")
+    dev = p.device
+    grad = out if out is not None else torch.empty_like(p)
+    ws, nbytes = _workspace(lib.lapsum_dftopk_workspace_size(batch, n), dev, workspace)
+    with _on_device(dev):
+        _check(lib.lapsum_dftopk_backward(_ptr(grad_p), _ptr(p), _ptr(pair), batch, n,
+                                          float(alpha), _ptr(grad), _ptr(ws), nbytes,
+                                          _stream(dev)), "lapsum_dftopk_backward")
+    return grad
 
 
 def lapsum_backward_workspace_size(batch: int, n: int) -> int:

@@ -136,6 +136,21 @@ hipError_t launch_row_backward(const float* grad_p, const float* p, int64_t batc
                                double t, float* grad_r, double* grad_k, double* grad_alpha,
                                hipStream_t s);
 
+// Comparators (comparator_kernels.hip).  Bisection baseline: one thread per
+// row, `steps` float32 bisection steps on the plain sum, then p.
+hipError_t launch_bisect(const float* r, int64_t batch, int64_t n, double k, double t, int steps,
+                         float* p, double* b, hipStream_t s);
+// DFTopK on one row: c and the boundary pair from the descending sort
+// (keys, source positions), the logistic emit, and the backward (partials:
+// dftopk_blocks(n) doubles).
+int dftopk_blocks(int64_t n);
+hipError_t launch_dftopk_pick(const uint32_t* keys, const int32_t* vals, int64_t k, double* c,
+                              int32_t* pair, hipStream_t s);
+hipError_t launch_dftopk_emit(const float* r, int64_t n, const double* c, double t, float* p,
+                              hipStream_t s);
+hipError_t launch_dftopk_backward(const float* g, const float* p, int64_t n, const int32_t* pair,
+                                  double t, double* partials, float* grad, hipStream_t s);
+
 // Hard top-k mask from a descending order: mask[row][perm[row][j]] = (j < k).
 hipError_t launch_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64_t k, float* mask,
                             hipStream_t s);

@@ -522,6 +522,30 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
   return LAPSUM_OK;
 }
 
+
+struct DftopkWs {
+  SortBuffers sb;
+  double* partials;
+};
+
+DftopkWs carve_dftopk(Carve& c, int64_t n) {
+  DftopkWs w{};
+  w.sb.keys[0] = c.take<uint32_t>(n);
+  w.sb.keys[1] = c.take<uint32_t>(n);
+  w.sb.vals[0] = c.take<int32_t>(n);
+  w.sb.vals[1] = c.take<int32_t>(n);
+  w.sb.hist = c.take<uint32_t>(sort_hist_words(n));
+  w.sb.totals = c.take<uint32_t>(256);
+  w.sb.max_tiles = sort_max_tiles(n);
+  w.partials = c.take<double>(static_cast<size_t>(dftopk_blocks(n)));
+  return w;
+}
+
+bool dftopk_args(int64_t batch, int64_t n, int64_t k, double alpha) {
+  return batch >= 1 && n >= 2 && n <= 2147483647LL && k >= 1 && k < n && isfinite(alpha) &&
+         alpha < 0.0;
+}
+
 }  // namespace
 
 extern "C" {
@@ -667,6 +691,67 @@ int lapsum_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64_t k, f
   const int dst = check_device();
   if (dst != LAPSUM_OK) return dst;
   LAPSUM_TRY(launch_topk_mask(perm, batch, n, k, mask, stream));
+  return LAPSUM_OK;
+}
+
+int lapsum_bisect_forward(const float* scores, int64_t batch, int64_t n, double k, double alpha,
+                          int32_t steps, float* p, double* b, hipStream_t stream) {
+  if (!scores || !p || !b || !valid_common(batch, n, k, alpha) || steps < 0 || steps > 200)
+    return LAPSUM_ERR_INVALID_ARG;
+  const int dst = check_device();
+  if (dst != LAPSUM_OK) return dst;
+  LAPSUM_TRY(launch_bisect(scores, batch, n, k, -alpha, steps, p, b, stream));
+  return LAPSUM_OK;
+}
+
+
+size_t lapsum_dftopk_workspace_size(int64_t batch, int64_t n) {
+  (void)batch;
+  if (n < 2 || n > 2147483647LL) return 0;
+  Carve c(nullptr);
+  carve_dftopk(c, n);
+  return c.size();
+}
+
+int lapsum_dftopk_forward(const float* scores, int64_t batch, int64_t n, int64_t k, double alpha,
+                          float* p, double* c_out, int32_t* pair, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream) {
+  if (!scores || !p || !c_out || !pair || !dftopk_args(batch, n, k, alpha))
+    return LAPSUM_ERR_INVALID_ARG;
+  const int wst = check_ws(workspace, workspace_bytes, lapsum_dftopk_workspace_size(batch, n));
+  if (wst != LAPSUM_OK) return wst;
+  const int dst = check_device();
+  if (dst != LAPSUM_OK) return dst;
+  Carve c(workspace);
+  DftopkWs w = carve_dftopk(c, n);
+  for (int64_t row = 0; row < batch; ++row) {
+    const float* r = scores + row * n;
+    const uint32_t* keys = nullptr;
+    const int32_t* vals = nullptr;
+    LAPSUM_TRY(launch_sort(r, nullptr, nullptr, true, n, nullptr, w.sb, 0xfu, &keys, &vals,
+                           stream));
+    LAPSUM_TRY(launch_dftopk_pick(keys, vals, k, c_out + row, pair + 2 * row, stream));
+    LAPSUM_TRY(launch_dftopk_emit(r, n, c_out + row, -alpha, p + row * n, stream));
+  }
+  return LAPSUM_OK;
+}
+
+int lapsum_dftopk_backward(const float* grad_p, const float* p, const int32_t* pair, int64_t batch,
+                           int64_t n, double alpha, float* grad_r, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  if (!grad_p || !p || !pair || !grad_r || !dftopk_args(batch, n, 1, alpha))
+    return LAPSUM_ERR_INVALID_ARG;
+  const int wst = check_ws(workspace, workspace_bytes, lapsum_dftopk_workspace_size(batch, n));
+  if (wst != LAPSUM_OK) return wst;
+  const int dst = check_device();
+  if (dst != LAPSUM_OK) return dst;
+  Carve c(workspace);
+  DftopkWs w = carve_dftopk(c, n);
+  for (int64_t row = 0; row < batch; ++row) {
+    const int64_t o = row * n;
+    LAPSUM_TRY(launch_dftopk_backward(grad_p + o, p + o, n, pair + 2 * row, -alpha, w.partials,
+                                      grad_r + o, stream));
+  }
   return LAPSUM_OK;
 }
 

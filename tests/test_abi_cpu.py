@@ -165,3 +165,19 @@ def test_topk_mask_rejects_invalid_arguments():
     assert lib.lapsum_topk_mask(v(1), 0, 8, 2, v(1), v(0)) == 1     # batch < 1
     assert lib.lapsum_topk_mask(v(1), 1, 8, 9, v(1), v(0)) == 1     # k > n
     assert lib.lapsum_topk_mask(v(1), 1, 8, -1, v(1), v(0)) == 1    # k < 0
+
+
+def test_comparators_reject_invalid_arguments():
+    lib = L.load()
+    v = ctypes.c_void_p
+    assert lib.lapsum_bisect_forward(v(0), 1, 8, 2.0, -1.0, 60, v(1), v(1), v(0)) == 1
+    assert lib.lapsum_bisect_forward(v(1), 1, 8, 8.0, -1.0, 60, v(1), v(1), v(0)) == 1   # k = n
+    assert lib.lapsum_bisect_forward(v(1), 1, 8, 2.0, -1.0, 201, v(1), v(1), v(0)) == 1
+    ws = L.lapsum_dftopk_workspace_size(1, 1000)
+    assert ws > 0 and L.lapsum_dftopk_workspace_size(1, 1) == 0
+    f = lambda k, alpha=-1.0, n=1000, wsp=256, wsb=ws: lib.lapsum_dftopk_forward(
+        v(1), 1, n, k, alpha, v(1), v(1), v(1), v(wsp), wsb, v(0))
+    assert f(0) == 1 and f(1000) == 1 and f(10, alpha=0.5) == 1 and f(1, n=1) == 1
+    assert f(10, wsp=0) == 2 and f(10, wsb=ws - 1) == 2
+    assert lib.lapsum_dftopk_backward(v(1), v(1), v(0), 1, 1000, -1.0, v(1), v(256), ws,
+                                      v(0)) == 1
