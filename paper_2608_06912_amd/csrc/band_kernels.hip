@@ -320,6 +320,49 @@ __device__ void writer_load(const Pass& P, WriterLds& S, const BandTile* __restr
   }
 }
 
+// A row without usable lists, streamed: out[i] = P.dense(in0[i], in1[i])
+// for every score, by the first kStoreWaves waves of each workgroup, float4
+// grid-strided so that the workgroups write neighbouring 4 KB pieces of one
+// 1 MB window at a time (the pattern that reaches the full write rate), four
+// float4 loads per lane in flight.
+template <class Pass>
+__device__ void stream_row(const Pass& P, int64_t n, float* __restrict__ out) {
+  constexpr int T = kStoreWaves * kWave;
+  if (threadIdx.x >= T) return;
+  const float* a = P.in0();
+  const float* g = P.in1();
+  const bool vec = ((reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(g) |
+                     reinterpret_cast<uintptr_t>(out)) & 15) == 0;
+  const int64_t n4 = vec ? n / 4 : 0;
+  const int64_t G = static_cast<int64_t>(gridDim.x) * T;
+  int64_t i = static_cast<int64_t>(blockIdx.x) * T + threadIdx.x;
+  auto apply = [&](const float4& x, const float4& y) {
+    float4 o;
+    o.x = P.dense(x.x, y.x);
+    o.y = P.dense(x.y, y.y);
+    o.z = P.dense(x.z, y.z);
+    o.w = P.dense(x.w, y.w);
+    return o;
+  };
+  constexpr int U = 4;
+  for (; i + (U - 1) * G < n4; i += U * G) {
+    float4 x[U], y[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      x[u] = load_stream4(a + 4 * (i + u * G));
+      y[u] = g ? load_stream4(g + 4 * (i + u * G)) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) store_stream4(out + 4 * (i + u * G), apply(x[u], y[u]));
+  }
+  for (; i < n4; i += G) {
+    const float4 y = g ? load_stream4(g + 4 * i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    store_stream4(out + 4 * i, apply(load_stream4(a + 4 * i), y));
+  }
+  for (int64_t j = n4 * 4 + static_cast<int64_t>(blockIdx.x) * T + threadIdx.x; j < n; j += G)
+    out[j] = P.dense(a[j], g ? g[j] : 0.0f);
+}
+
 template <class Pass>
 __device__ void band_write(const Pass& P, WriterLds& S, const BandCtx& c, int64_t n,
                            float* __restrict__ out, bool all_dense) {
@@ -362,10 +405,14 @@ __global__ __launch_bounds__(WT) void band_emit_kernel(const float* __restrict__
   __shared__ WriterLds S;
   if (!rec->ok) return;
   const double b = rec->b;
+  // a band as wide as the scores (t large against their spread) leaves most
+  // blocks without lists: the whole row is then streamed, here and in the
+  // backward (the dense form gives the same values everywhere)
+  const bool dense_row = 4 * static_cast<int64_t>(tot->dense_blocks) >= c.nblocks;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     b_out[0] = b;
     CtxHeader h;
-    h.mode = 0;
+    h.mode = dense_row ? 1 : 0;
     h.nblocks = c.nblocks;
     h.chunk = c.chunk;
     h.cap = c.cap;
@@ -379,7 +426,10 @@ __global__ __launch_bounds__(WT) void band_emit_kernel(const float* __restrict__
   P.ones = tot->aR < INFINITY ? ones_all : nullptr;
   P.b = b;
   P.inv_t = inv_t;
-  band_write(P, S, c, n, p, false);
+  if (dense_row)
+    stream_row(P, n, p);
+  else
+    band_write(P, S, c, n, p, false);
 }
 
 hipError_t launch_band_emit(const float* r, int64_t n, const SolveRec* rec, double t,
@@ -435,11 +485,12 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
   if (pb < c.nblocks) {
     const BlockRange br = range_of(n, c.chunk, pb);
     if (header_dense(h, c, n) || !lists_usable(c, pb)) {
-      for (int64_t i = br.b0 + lane; i < br.b1; i += kWave) {
-        const float pv = p[i];
+      // the block's range from p (float4 loads, four per lane in flight; g
+      // only where some f != 0); a block starts on a multiple of 4096 scores
+      auto add = [&](float pv, float gv) {
         const float f = fminf(pv, 1.0f - pv);
         if (f != 0.0f) {
-          const double fg = static_cast<double>(f) * static_cast<double>(g[i]);
+          const double fg = static_cast<double>(f) * static_cast<double>(gv);
           F += static_cast<double>(f);
           G += fg;
           if constexpr (PARAMS) {
@@ -448,6 +499,41 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
             H += fg * u;
           }
         }
+      };
+      const bool vec = ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(g)) & 15) == 0;
+      int64_t i = br.b0 + 4 * lane;
+      if (vec) {
+        constexpr int VU = 4;
+        for (; i + 4 * kWave * (VU - 1) + 3 < br.b1; i += 4 * kWave * VU) {
+          float4 pv[VU];
+#pragma unroll
+          for (int u = 0; u < VU; ++u) pv[u] = load_stream4(p + i + 4 * kWave * u);
+#pragma unroll
+          for (int u = 0; u < VU; ++u) {
+            const float4 q = pv[u];
+            const bool need = (fminf(q.x, 1.0f - q.x) + fminf(q.y, 1.0f - q.y)) +
+                                  (fminf(q.z, 1.0f - q.z) + fminf(q.w, 1.0f - q.w)) != 0.0f;
+            if (need) {
+              const float4 gv = load_stream4(g + i + 4 * kWave * u);
+              add(q.x, gv.x);
+              add(q.y, gv.y);
+              add(q.z, gv.z);
+              add(q.w, gv.w);
+            }
+          }
+        }
+        for (; i + 3 < br.b1; i += 4 * kWave) {
+          const float4 q = load_stream4(p + i);
+          const float4 gv = load_stream4(g + i);
+          add(q.x, gv.x);
+          add(q.y, gv.y);
+          add(q.z, gv.z);
+          add(q.w, gv.w);
+        }
+        for (int e = 0; e < 4; ++e)
+          if (i + e < br.b1) add(p[i + e], g[i + e]);
+      } else {
+        for (int64_t j = br.b0 + lane; j < br.b1; j += kWave) add(p[j], g[j]);
       }
     } else {
       // the block's members in index order are the four wave segments one
@@ -594,7 +680,10 @@ __global__ __launch_bounds__(WT) void band_vjp_write_kernel(const float* __restr
   P.inv_t = inv_t;
   P.coef = static_cast<float>(fs > 0.0 ? gsum / fs : 0.0);
   P.scale = static_cast<float>(fs > 0.0 ? inv_t : 0.0);
-  band_write(P, S, c, n, grad, header_dense(h, c, n));
+  if (header_dense(h, c, n))
+    stream_row(P, n, grad);
+  else
+    band_write(P, S, c, n, grad, false);
 }
 
 int band_vjp_parts(int nblocks) { return (nblocks + kVjpWaveBlocks - 1) / kVjpWaveBlocks; }

@@ -180,7 +180,7 @@ __device__ void find_bin(const uint32_t* h, int nb, uint32_t rank, uint32_t* wsu
   __syncthreads();
 }
 
-constexpr int kCand = 4096;   // candidates per target kept in LDS
+constexpr int kCand = 16384;   // candidates per target kept in LDS (64 KB)
 constexpr int kFewCand = 256;   // a bin this small is ranked directly
 
 // Histogram (into h, nb bins) of (key >> lo) & mask over the keys whose
@@ -497,9 +497,12 @@ constexpr int kWaveStage = kPartStageCap / PW;   // M entries staged per wave
 // a_R one bit per score for r >= hi.  L is not counted:
 // n_L = scores - n_M - n_R.
 // With STAGE the L tail is summed once at the end from the wave's staged
-// band (its members below a_L are the only nonzero terms), or from a second
-// read of the range if the list overflowed; without it (a range too long to
-// stage) each member's term is formed as it is met.
+// band (its members below a_L are the only nonzero terms).  Once the list
+// could not take another step's members (a band as wide as the scores, when
+// t is large against their spread) the wave stops staging the band and
+// forms each later member's term as it is met; its block then takes the
+// dense passes.  Without STAGE (a range too long to stage) every term is
+// formed as it is met.
 // tb: lane q ends with the band members met before tile q of the range (the
 // range starts on a tile boundary; tiles are kBandTile scores).
 template <bool HAS_R, bool STAGE>
@@ -511,6 +514,10 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
   auto tile_start = [&](int64_t at) {
     if (lane == static_cast<int>((at - w0) / kBandTile)) tb = static_cast<int32_t>(st.nB);
   };
+  // staging stopped (uniform across the wave); the list then holds the
+  // members of the steps before, `listed` of them
+  bool spill = !STAGE;
+  int64_t listed = 0;
   // it: first score of this wave's 256-score step (a multiple of 256)
   auto one = [&](const float (&v)[4], const bool (&ok)[4], int64_t it) {
     const int64_t i0 = it + 4 * lane;
@@ -553,19 +560,12 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
     for (int e = 0; e < 4; ++e) bm[e] = __ballot(inB[e]);
     const uint64_t any = bm[0] | bm[1] | bm[2] | bm[3];
     if (any) {
-      if (!STAGE) {
-        // the L tail's terms as they are met: below the band's lower edge
-        // (a_L - 105 t) a term e^{(r - a_L)/t} is exactly 0 in float32
-        float tl = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (inB[e] && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
-        st.TL += static_cast<double>(tl);
-      }
       const uint32_t nb0 = static_cast<uint32_t>(st.nB);   // uniform across the wave
       const uint32_t cap = static_cast<uint32_t>(bw.cap);
-      const uint64_t two = (bm[0] & (bm[1] | bm[2] | bm[3])) | (bm[1] & (bm[2] | bm[3])) |
-                           (bm[2] & bm[3]);   // lanes with two or more members
+      if (STAGE && !spill && nb0 + 256u > cap) {
+        spill = true;   // a step adds at most 256 members
+        listed = nb0;
+      }
       // M members of the step: staged in index order, with the range of M
       auto stage_m = [&](float x, int64_t i, uint32_t at) {
         st.mmin = fminf(st.mmin, x);
@@ -575,6 +575,41 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
           si[at] = static_cast<int32_t>(i);
         }
       };
+      auto stage_all_m = [&]() {
+        if (__ballot(inM[0] || inM[1] || inM[2] || inM[3])) {
+          uint32_t before = 0, total = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint64_t bal = __ballot(inM[e]);
+            before += lanes_below(bal);
+            total += static_cast<uint32_t>(__popcll(bal));
+          }
+          uint32_t at = static_cast<uint32_t>(st.nM) + before;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (inM[e]) {
+              stage_m(v[e], i0 + e, at);
+              ++at;
+            }
+          }
+          st.nM += total;
+        }
+      };
+      if (spill) {
+        // the L tail's terms as they are met: below the band's lower edge
+        // (a_L - 105 t) a term e^{(r - a_L)/t} is exactly 0 in float32
+        float tl = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (inB[e] && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
+        st.TL += static_cast<double>(tl);
+        st.nB = nb0 + static_cast<uint32_t>(__popcll(bm[0]) + __popcll(bm[1]) + __popcll(bm[2]) +
+                                            __popcll(bm[3]));
+        stage_all_m();
+        return;
+      }
+      const uint64_t two = (bm[0] & (bm[1] | bm[2] | bm[3])) | (bm[1] & (bm[2] | bm[3])) |
+                           (bm[2] & bm[3]);   // lanes with two or more members
       if (two == 0ull) {
         // each lane holds at most one member: its slot is its rank among
         // the lanes that hold one (scalar mask work, a few vector ops)
@@ -619,24 +654,7 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
           }
         }
         st.nB = nb0 + tot;
-        if (__ballot(inM[0] || inM[1] || inM[2] || inM[3])) {
-          uint32_t before = 0, total = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint64_t bal = __ballot(inM[e]);
-            before += lanes_below(bal);
-            total += static_cast<uint32_t>(__popcll(bal));
-          }
-          uint32_t at = static_cast<uint32_t>(st.nM) + before;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (inM[e]) {
-              stage_m(v[e], i0 + e, at);
-              ++at;
-            }
-          }
-          st.nM += total;
-        }
+        stage_all_m();
       }
     }
   };
@@ -694,21 +712,18 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
     one(v, ok, it);
   }
   if constexpr (STAGE) {
-    // the L tail: e^{(r - a_L)/t} over the band members below a_L, each
-    // term in float32 and summed per lane in float64
+    // the L tail of the listed members: e^{(r - a_L)/t} over the band
+    // members below a_L, each term in float32 and summed per lane in float64
+    const int nl = static_cast<int>(spill ? listed : st.nB);
     double tl = 0.0;
-    if (st.nB <= bw.cap) {
-      for (int q = lane; q < static_cast<int>(st.nB); q += kWave) {
-        const float x = __uint_as_float(bw.sbuf[q].bits);
-        if (x < aL) tl += static_cast<double>(exp2_fast((x - aL) * c2f));
-      }
-    } else {
-      for (int64_t i = w0 + lane; i < w1; i += kWave) {
-        const float x = r[i];
-        if (!(x < bw.lo) && x < aL) tl += static_cast<double>(exp2_fast((x - aL) * c2f));
-      }
+    for (int q = lane; q < nl; q += kWave) {
+      const float x = __uint_as_float(bw.sbuf[q].bits);
+      if (x < aL) tl += static_cast<double>(exp2_fast((x - aL) * c2f));
     }
     st.TL += tl;
+    // an incomplete list reports more members than it can hold, so that
+    // the block takes the dense passes
+    if (spill && st.nB <= bw.cap) st.nB = bw.cap + 1;
   }
 }
 
@@ -728,13 +743,13 @@ __device__ void partition_totals_block(const PartBlock* __restrict__ blk, int nb
   constexpr int PT = TOT_T;
   constexpr int PW = TOT_W;
   __shared__ double rd[2][PW];
-  __shared__ int64_t ri[4][PW];
+  __shared__ int64_t ri[5][PW];
   __shared__ float rf[2][PW];
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
   double TL = 0.0, TR = 0.0;
-  int64_t nL = 0, nR = 0, ov = 0;
+  int64_t nL = 0, nR = 0, ov = 0, nd = 0;
   float mn = INFINITY, mx = -INFINITY;
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
@@ -746,6 +761,7 @@ __device__ void partition_totals_block(const PartBlock* __restrict__ blk, int nb
       nL += rec.nL;
       nR += rec.nR;
       ov += rec.overflow;
+      nd += rec.band_dense;
       mn = fminf(mn, rec.mmin);
       mx = fmaxf(mx, rec.mmax);
       nm[b] = static_cast<int32_t>(rec.nM);
@@ -762,7 +778,7 @@ __device__ void partition_totals_block(const PartBlock* __restrict__ blk, int nb
   int64_t incl = wave_incl_add<int64_t>(loc);
   TL = wave_sum(TL);
   TR = wave_sum(TR);
-  const int64_t sL = wave_sum(nL), sR = wave_sum(nR), sO = wave_sum(ov);
+  const int64_t sL = wave_sum(nL), sR = wave_sum(nR), sO = wave_sum(ov), sD = wave_sum(nd);
 mn = wave_min(mn, INFINITY);
 mx = wave_max(mx, -INFINITY);
   if (lane == kWave - 1) ri[3][wid] = incl;
@@ -772,6 +788,7 @@ mx = wave_max(mx, -INFINITY);
     ri[0][wid] = sL;
     ri[1][wid] = sR;
     ri[2][wid] = sO;
+    ri[4][wid] = sD;
     rf[0][wid] = mn;
     rf[1][wid] = mx;
   }
@@ -794,7 +811,7 @@ mx = wave_max(mx, -INFINITY);
   if (tid == 0) {
     PartTotals x;
     double tl = 0.0, tr = 0.0;
-    int64_t cl = 0, cr = 0, co = 0;
+    int64_t cl = 0, cr = 0, co = 0, cd = 0;
     float fmn = INFINITY, fmx = -INFINITY;
 #pragma unroll
     for (int w = 0; w < PW; ++w) {
@@ -803,6 +820,7 @@ mx = wave_max(mx, -INFINITY);
       cl += ri[0][w];
       cr += ri[1][w];
       co += ri[2][w];
+      cd += ri[4][w];
       fmn = fminf(fmn, rf[0][w]);
       fmx = fmaxf(fmx, rf[1][w]);
     }
@@ -816,7 +834,7 @@ mx = wave_max(mx, -INFINITY);
     x.mmin = fmn;
     x.mmax = fmx;
     x.any_block_overflow = co > 0 ? 1 : 0;
-    x.pad = 0;
+    x.dense_blocks = static_cast<int32_t>(cd);
     *tot = x;
   }
 }
@@ -988,12 +1006,12 @@ mx = wave_max(mx, -INFINITY);
     rec.mmin = mn2;
     rec.mmax = mx2;
     rec.overflow = over ? 1 : 0;
-    rec.pad[0] = 0;
-    rec.pad[1] = 0;
-    blk[blockIdx.x] = rec;
     bool bover = chunk > kBandMaxChunk;
 #pragma unroll
     for (int w = 0; w < PW; ++w) bover |= red_b[w] > bcap;
+    rec.band_dense = bover ? 1 : 0;
+    rec.pad = 0;
+    blk[blockIdx.x] = rec;
     bblk[blockIdx.x].dense = bover ? 1 : 0;
   }
 }

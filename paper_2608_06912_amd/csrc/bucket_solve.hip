@@ -119,6 +119,7 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
   __shared__ unsigned long long rm[CT / kWave];
   __shared__ uint32_t rov[CT / kWave];
   __shared__ int32_t ro[CT / kWave];
+  __shared__ int32_t rdn[CT / kWave];
   __shared__ double rd[2][CT / kWave];
   __shared__ int64_t ri[3][CT / kWave];
   const int tid = threadIdx.x;
@@ -169,7 +170,7 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
   {
     double TL = 0.0, TR = 0.0;
     int64_t nL = 0, nR = 0, nM = 0;
-    int32_t nm = 0, ov = 0;
+    int32_t nm = 0, ov = 0, nd = 0;
     if (own) {
       TL = rec.TL;
       TR = rec.TR;
@@ -177,6 +178,7 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
       nR = rec.nR;
       nm = rec.nM;
       ov = rec.overflow;
+      nd = static_cast<int32_t>(rec.band_dense);
     }
     nM = nm;
     const int32_t incl = wave_incl_add(nm);
@@ -186,8 +188,10 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
     nR = wave_sum(nR);
     nM = wave_sum(nM);
     ov = wave_or(ov);
+    nd = wave_sum(nd);
     if (lane == kWave - 1) wtot[wid] = static_cast<uint32_t>(incl);
     if (lane == 0) {
+      rdn[wid] = nd;
       rd[0][wid] = TL;
       rd[1][wid] = TR;
       ri[0][wid] = nL;
@@ -233,6 +237,10 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
       cp.nM += ri[2][w];
     }
     cp.overflow = grp_ov;
+    cp.ndense = 0;
+#pragma unroll
+    for (int w = 0; w < CG / kWave; ++w) cp.ndense += rdn[w];
+    cp.pad = 0;
     cp.kmin = kmin;
     cp.kmax = kmax;
     cp.any_overflow = any_ov;
@@ -566,6 +574,7 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
     const double TR = wave_sum(on ? cp.TR : 0.0);
     const int64_t nL = wave_sum(on ? cp.nL : int64_t(0));
     const int64_t nR = wave_sum(on ? cp.nR : int64_t(0));
+    const int32_t nd = wave_sum(on ? cp.ndense : 0);
     if (on) gcount_s[lane] = cp.nM;
     if (lane == 0) {
       // |M|, its range and the overflow flag are the same in every partial
@@ -580,7 +589,7 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
       T.mmin = cp.m_all > 0 ? key_float(cp.kmax) : INFINITY;
       T.mmax = cp.m_all > 0 ? key_float(cp.kmin) : -INFINITY;
       T.any_block_overflow = cp.any_overflow;
-      T.pad = 0;
+      T.dense_blocks = nd;
       tot_s = T;
       *tot = T;
     }

@@ -39,7 +39,8 @@ struct alignas(16) PartBlock {
   int32_t overflow;   // this block's M did not fit its staging
   int64_t nL, nR;
   double TL, TR;
-  int64_t pad[2];
+  int64_t band_dense;   // 1: this block's band lists are incomplete
+  int64_t pad;
 };
 static_assert(sizeof(PartBlock) == 64, "PartBlock layout");
 
@@ -50,7 +51,7 @@ struct PartTotals {
   float aL, aR;       // the bracket that was partitioned
   float mmin, mmax;   // range of M (+inf / -inf when M is empty)
   int32_t any_block_overflow;
-  int32_t pad;
+  int32_t dense_blocks;   // partition blocks whose band lists are incomplete
 };
 
 // Band of a bracket: the scores whose p depends on where b falls inside a
@@ -291,6 +292,8 @@ struct alignas(16) CountPart {
   uint32_t kmin, kmax;   // keys of max M and min M over every block
   int32_t any_overflow;
   int64_t m_all;
+  int32_t ndense;   // blocks of this group whose band lists are incomplete
+  int32_t pad;
 };
 struct BucketAcc {
   uint32_t* n;              // [kBucketCount]

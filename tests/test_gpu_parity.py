@@ -413,6 +413,31 @@ def test_bracketed_band_too_wide_for_the_lists(lib):
     assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
 
 
+def test_bracketed_wide_band_rows_of_odd_length(lib):
+    # every block without lists, so each row is streamed whole (emit, reduce,
+    # write); odd rows are not 16-byte aligned, so the streams take their
+    # scalar forms, and k = n/3 makes a_R finite
+    batch, n = 2, 1_000_003
+    rows = W.random_case(50, n, dist="normal", batch=batch)
+    k, alpha = n / 3.0, -1.5
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([95], K, 1.5)
+    gs = W.random_case(51, n, dist="normal", batch=batch)
+    band = lib.new_band(batch, n, "cuda")
+    p, b, infos, _ = lib.lapsum_forward_bracketed(_t(rows), k, alpha, _t(noise), band=band)
+    grad, gk, ga = lib.lapsum_backward_band(_t(gs), p, band, alpha, params=True)
+    pn, bn, grad, gk, ga = _np(p), _np(b), _np(grad), _np(gk), _np(ga)
+    for i in range(batch):
+        po, bo, oinfo, _ = O.bracketed_forward(rows[i], k, alpha, noise)
+        _check_info(infos[i], oinfo, f"row {i}")
+        assert not oinfo.fell_back and math.isfinite(oinfo.a_R)
+        assert abs(float(bn[i]) - bo) <= 2e-6 * -alpha, i
+        assert np.max(np.abs(pn[i].astype(np.float64) - O.probs(rows[i], bo, alpha))) <= P_TOL, i
+        assert O.budget_error(pn[i], k) <= sum_tol(k), i
+        assert grad_rel(grad[i], O.vjp(rows[i], bo, alpha, gs[i])) <= G_TOL, i
+        check_params(float(gk[i]), float(ga[i]), rows[i], float(bn[i]), alpha, gs[i], f"row {i}")
+
+
 def test_bracketed_band_past_the_writer_slots(lib):
     # a band of about 2.5% of the scores puts some 200 members into a
     # writer round (eight tiles of 1024) and often more: the loading wave
