@@ -14,6 +14,8 @@
 //   gather            M to one contiguous array of (key, index)
 #include <math.h>
 
+#include <type_traits>
+
 #include "block_sort.hpp"
 #include "kernels.hpp"
 
@@ -441,9 +443,9 @@ namespace {
 struct PartState {
   double TL, TR;
   int64_t nL, nR;
-  int64_t nM;   // M count of this wave (uniform across the wave)
+  int32_t nM;   // M count of this wave (uniform across the wave)
   float mmin, mmax;
-  int64_t nB;   // band members of this wave (uniform across the wave)
+  int32_t nB;   // band members of this wave (uniform across the wave)
 };
 
 // Where a wave stages its band members and its bits of r >= hi.  Both go
@@ -515,11 +517,24 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
     if (lane == static_cast<int>((at - w0) / kBandTile)) tb = static_cast<int32_t>(st.nB);
   };
   // staging stopped (uniform across the wave); the list then holds the
-  // members of the steps before, `listed` of them
+  // members met before, `listed` of them
   bool spill = !STAGE;
-  int64_t listed = 0;
-  // it: first score of this wave's 256-score step (a multiple of 256)
-  auto one = [&](const float (&v)[4], const bool (&ok)[4], int64_t it) {
+  int32_t listed = 0;
+  // the lower tail's terms of a step's band members, formed directly:
+  // below the band's lower edge (a_L - 105 t) a term e^{(r - a_L)/t} is
+  // exactly 0 in float32
+  auto direct_tl = [&](const float (&v)[4], const bool (&ok)[4]) {
+    float tl = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (ok[e] && !(v[e] < bw.lo) && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
+    st.TL += static_cast<double>(tl);
+  };
+  // it: first score of this wave's 256-score step (a multiple of 256).
+  // DIRECT: the band is not staged, each member's lower-tail term is formed
+  // as it is met
+  auto one = [&](auto direct, const float (&v)[4], const bool (&ok)[4], int64_t it) {
+    constexpr bool DIRECT = decltype(direct)::value;
     const int64_t i0 = it + 4 * lane;
     // membership as lane masks: a comparison is its own ballot
     bool inB[4], inM[4];
@@ -562,10 +577,6 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
     if (any) {
       const uint32_t nb0 = static_cast<uint32_t>(st.nB);   // uniform across the wave
       const uint32_t cap = static_cast<uint32_t>(bw.cap);
-      if (STAGE && !spill && nb0 + 256u > cap) {
-        spill = true;   // a step adds at most 256 members
-        listed = nb0;
-      }
       // M members of the step: staged in index order, with the range of M
       auto stage_m = [&](float x, int64_t i, uint32_t at) {
         st.mmin = fminf(st.mmin, x);
@@ -595,14 +606,8 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
           st.nM += total;
         }
       };
-      if (spill) {
-        // the L tail's terms as they are met: below the band's lower edge
-        // (a_L - 105 t) a term e^{(r - a_L)/t} is exactly 0 in float32
-        float tl = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (inB[e] && v[e] < aL) tl += exp2_fast((v[e] - aL) * c2f);
-        st.TL += static_cast<double>(tl);
+      if constexpr (DIRECT) {
+        direct_tl(v, ok);
         st.nB = nb0 + static_cast<uint32_t>(__popcll(bm[0]) + __popcll(bm[1]) + __popcll(bm[2]) +
                                             __popcll(bm[3]));
         stage_all_m();
@@ -672,32 +677,59 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       for (int u = 0; u < U; ++u)
         q[u] = load_stream4(real ? r + at + u * 256 + 4 * lane : r + w0);
     };
-    auto run = [&](const float4 (&q)[U], int64_t at) {
+    // one batch (tile).  A staged batch that overflows the list keeps its M
+    // and has its lower-tail terms formed again directly; the wave then
+    // stops staging (returns true)
+    auto run = [&](auto direct, const float4 (&q)[U], int64_t at) -> bool {
+      constexpr bool DIRECT = decltype(direct)::value;
+      const bool ok[4] = {true, true, true, true};
+      const int32_t nb_start = st.nB;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const float v[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
-        const bool ok[4] = {true, true, true, true};
-        one(v, ok, at + u * 256);
+        one(direct, v, ok, at + u * 256);
+      }
+      if constexpr (!DIRECT) {
+        if (st.nB > bw.cap) {
+          spill = true;
+          listed = nb_start;
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            const float v[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+            direct_tl(v, ok);
+          }
+          return true;
+        }
+      }
+      return false;
+    };
+    // the batches from `from` on, two buffers taking turns so that no
+    // registers are copied per batch; returns where it stopped (after the
+    // last whole batch, or after the batch where staging stopped).  The
+    // staged and the direct passes are separate loops, so that neither
+    // carries the other's registers
+    auto stream = [&](auto direct, int64_t from) -> int64_t {
+      int64_t at = from;
+      if (at + U * 256 > w1) return at;
+      float4 qa[U], qb[U];
+      load(qa, at, true);
+      while (true) {
+        const int64_t ca = at;
+        at += U * 256;
+        const bool more_a = at + U * 256 <= w1;
+        load(qb, at, more_a);
+        tile_start(ca);
+        if (run(direct, qa, ca) || !more_a) return at;
+        const int64_t cb = at;
+        at += U * 256;
+        const bool more_b = at + U * 256 <= w1;
+        load(qa, at, more_b);
+        tile_start(cb);
+        if (run(direct, qb, cb) || !more_b) return at;
       }
     };
-    float4 qa[U], qb[U];
-    load(qa, it, true);
-    while (true) {
-      const int64_t ca = it;
-      it += U * 256;
-      const bool more_a = it + U * 256 <= w1;
-      load(qb, it, more_a);
-      tile_start(ca);
-      run(qa, ca);
-      if (!more_a) break;
-      const int64_t cb = it;
-      it += U * 256;
-      const bool more_b = it + U * 256 <= w1;
-      load(qa, it, more_b);
-      tile_start(cb);
-      run(qb, cb);
-      if (!more_b) break;
-    }
+    if (!spill) it = stream(std::false_type{}, it);
+    if (spill) it = stream(std::true_type{}, it);
   }
   for (; it < w1; it += 256) {
     if (((it - w0) & (kBandTile - 1)) == 0) tile_start(it);
@@ -709,12 +741,22 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
       ok[e] = (i0 + e) < w1;
       v[e] = ok[e] ? r[i0 + e] : 0.0f;
     }
-    one(v, ok, it);
+    if (spill) {
+      one(std::true_type{}, v, ok, it);
+    } else {
+      const int32_t nb_start = st.nB;
+      one(std::false_type{}, v, ok, it);
+      if (st.nB > bw.cap) {
+        spill = true;
+        listed = nb_start;
+        direct_tl(v, ok);
+      }
+    }
   }
   if constexpr (STAGE) {
     // the L tail of the listed members: e^{(r - a_L)/t} over the band
     // members below a_L, each term in float32 and summed per lane in float64
-    const int nl = static_cast<int>(spill ? listed : st.nB);
+    const int nl = static_cast<int>(spill ? listed : st.nB);   // <= bw.cap
     double tl = 0.0;
     for (int q = lane; q < nl; q += kWave) {
       const float x = __uint_as_float(bw.sbuf[q].bits);
