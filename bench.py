@@ -56,6 +56,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample", type=int, default=20_000_000)
+    ap.add_argument("--no-tables", action="store_true",
+                    help="skip the per-config table and the paper-setting timings")
     ap.add_argument("--comparators", action="store_true",
                     help="also time the comparators (bisection baseline, DFTopK) against the "
                          "operator in the paper's settings, outside the timed region")
@@ -142,6 +144,92 @@ def _timed_ms(fn, iters=20, warmup=3):
         fn()
     torch.cuda.synchronize()
     return (time.perf_counter() - t0) * 1e3 / iters
+
+
+def _fwd_bwd_fns(L, A, x, g, k, alpha, path, noise=None, z=5.16):
+    """(forward, forward + backward) closures for one workload on one path,
+    with their workspaces allocated up front."""
+    import torch
+    dev = x.device
+    batch, n = x.shape
+    if path == "full":
+        wsf = torch.empty(max(1, L.lapsum_forward_workspace_size(batch, n)), dtype=torch.uint8,
+                          device=dev)
+        wsb = torch.empty(max(1, L.lapsum_backward_workspace_size(batch, n)), dtype=torch.uint8,
+                          device=dev)
+
+        def fwd():
+            return L.lapsum_forward(x, k, alpha, workspace=wsf)
+
+        def fb():
+            p, b = fwd()
+            L.lapsum_backward(g, p, b, alpha, workspace=wsb)
+        return fwd, fb
+    if noise is None:
+        noise = A.bracket_noise(A.sample_size(n), -alpha, dev)
+    K = int(noise.shape[0])
+    mcap = L.default_m_capacity(n, K)
+    wsf = torch.empty(L.lapsum_forward_bracketed_workspace_size(batch, n, K, mcap),
+                      dtype=torch.uint8, device=dev)
+    wsb = torch.empty(max(1, L.lapsum_backward_band_workspace_size(batch, n)), dtype=torch.uint8,
+                      device=dev)
+    band = L.new_band(batch, n, dev)
+
+    def fwd():
+        return L.lapsum_forward_bracketed(x, k, alpha, noise, z=z, m_capacity=mcap, band=band,
+                                          workspace=wsf)
+
+    def fb():
+        p = fwd()[0]
+        L.lapsum_backward_band(g, p, band, alpha, workspace=wsb)
+    return fwd, fb
+
+
+def config_table(dev, main_ms):
+    """Forward + backward per call and scores/s on every synthetic workload
+    (n1e8 is the timed step above)."""
+    import torch
+
+    import paper_2608_06912_amd as L
+    import paper_2608_06912_amd.autograd as A
+    import workloads as W
+    rows = []
+    for name, path in (("single4k", "full"), ("batch256", "full"), ("n1e6", "full"),
+                       ("n1e7", "full"), ("n1e7", "bracketed")):
+        w = W.get(name)
+        x = torch.from_numpy(W.scores(name)).to(dev)
+        g = torch.from_numpy(W.upstream_grad(name)).to(dev)
+        noise = torch.from_numpy(W.bracket_noise(name)).to(dev) if path == "bracketed" else None
+        _, fb = _fwd_bwd_fns(L, A, x, g, w.k, w.alpha, path, noise, w.z)
+        ms = _timed_ms(fb)
+        rows.append({"workload": name, "path": path, "batch": w.batch, "n": w.n,
+                     "fwd_bwd_ms": ms, "scores_per_s": w.batch * w.n / (ms / 1e3)})
+        del x, g
+    w = W.get("n1e8")
+    rows.append({"workload": "n1e8", "path": "bracketed", "batch": 1, "n": w.n,
+                 "fwd_bwd_ms": main_ms, "scores_per_s": w.n / (main_ms / 1e3)})
+    return rows
+
+
+def paper_setting(dev):
+    """The paper's headline setting (abstract, Table ks-main): one row of
+    Gaussian scores, k = n/16, alpha = -1, dispatched (sort up to 2^21
+    scores, the bracket above); forward alone and forward + backward.  The
+    paper's forward times on its laptop GPU are 0.41 / 1.15 / 5.23 ms."""
+    import torch
+
+    import paper_2608_06912_amd as L
+    import paper_2608_06912_amd.autograd as A
+    out = []
+    gen = torch.Generator(device=dev).manual_seed(16)
+    for n in (10**6, 10**7, 10**8):
+        x = torch.randn((1, n), generator=gen, device=dev, dtype=torch.float32)
+        g = torch.randn((1, n), generator=gen, device=dev, dtype=torch.float32)
+        path = A.choose_path(n)
+        fwd, fb = _fwd_bwd_fns(L, A, x, g, n / 16.0, -1.0, path)
+        out.append({"n": n, "path": path, "fwd_ms": _timed_ms(fwd), "fwd_bwd_ms": _timed_ms(fb)})
+        del x, g
+    return out
 
 
 def comparators(dev):
@@ -354,6 +442,10 @@ def main():
         "active_scores": active,
         "band_scores": band_n,
     }
+    if not args.no_tables:
+        print("[bench] per-config table and the paper's setting", file=sys.stderr, flush=True)
+        out["configs"] = config_table(dev, ms_step)
+        out["paper_setting_k_n16_alpha_m1"] = paper_setting(dev)
     if args.comparators:
         print("[bench] comparators", file=sys.stderr, flush=True)
         out["comparators"] = comparators(dev)
