@@ -86,6 +86,7 @@ struct WriterLds {
 // Forward: p.
 struct EmitPass {
   static constexpr bool kOnes = true;
+  static constexpr int kInputs = 1;   // arrays a dense score reads
   const float* r;
   const uint32_t* ones;   // null when a_R is infinite
   double b, inv_t;
@@ -101,6 +102,7 @@ struct EmitPass {
 // Backward: grad_r = (f/t)(g - <g,q>), f = min(p, 1 - p).
 struct VjpPass {
   static constexpr bool kOnes = false;
+  static constexpr int kInputs = 2;
   const float* p;
   const float* g;
   const float* gstash;
@@ -323,8 +325,7 @@ __device__ void writer_load(const Pass& P, WriterLds& S, const BandTile* __restr
 // A row without usable lists, streamed: out[i] = P.dense(in0[i], in1[i])
 // for every score, by the first kStoreWaves waves of each workgroup, float4
 // grid-strided so that the workgroups write neighbouring 4 KB pieces of one
-// 1 MB window at a time (the pattern that reaches the full write rate), four
-// float4 loads per lane in flight.
+// 1 MB window at a time (the pattern that reaches the full write rate).
 template <class Pass>
 __device__ void stream_row(const Pass& P, int64_t n, float* __restrict__ out) {
   constexpr int T = kStoreWaves * kWave;
@@ -344,7 +345,9 @@ __device__ void stream_row(const Pass& P, int64_t n, float* __restrict__ out) {
     o.w = P.dense(x.w, y.w);
     return o;
   };
-  constexpr int U = 4;
+  // eight float4 in flight per lane for one input stream, four for two
+  // (measured: the emit's single stream gains, the backward's two do not)
+  constexpr int U = Pass::kInputs == 1 ? 8 : 4;
   for (; i + (U - 1) * G < n4; i += U * G) {
     float4 x[U], y[U];
 #pragma unroll
