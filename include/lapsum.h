@@ -229,7 +229,10 @@ int lapsum_dftopk_backward(const float* grad_p, const float* p,
  *     hi = a_R + 18 t (rounded outwards to float32): for any b in a certified
  *     bracket, p is exactly 0 below the band and exactly 1 above it in
  *     float32, so step 6 writes p from the band and one bit per score
- *     without reading r again.
+ *     without reading r again.  When t is so large against the spread of
+ *     the scores that a quarter or more of the row's blocks cannot list
+ *     their band, step 6 (and the backward from the saved band) streams the
+ *     whole row instead; the values are the same.
  *
  * The result is the same b as lapsum_forward (the bracket only locates it).
  * The host waits on `stream` twice per bracket attempt to read the set sizes

@@ -62,7 +62,9 @@ struct PartTotals {
 // partition stages the band in index order and records, per tile of
 // kBandTile scores, where the tile's members sit in the lists; the dense
 // writers then fill p (and grad_r) tile by tile without re-reading r, and
-// the backward visits only the band.
+// the backward visits only the band.  A row where a quarter or more of the
+// blocks could not list their band is instead streamed whole by the emit
+// and the backward (the saved header then says mode 1).
 constexpr double kBandLowT = 105.0;
 constexpr double kBandHighT = 18.0;
 constexpr int kBandWaveCapMax = 512;        // band entries a partition wave stages
