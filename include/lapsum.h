@@ -235,10 +235,14 @@ int lapsum_dftopk_backward(const float* grad_p, const float* p,
  *     whole row instead; the values are the same.
  *
  * The result is the same b as lapsum_forward (the bracket only locates it).
- * The host waits on `stream` twice per bracket attempt to read the set sizes
- * and the certificate, so this call returns after the row's threshold is
- * known (the emit of step 6 may still be running).  The first call on a
- * host thread allocates a small pinned host buffer that the library keeps.
+ * The host waits on `stream` for each bracket attempt's record (set sizes
+ * and certificate), so this call returns after every row's threshold is
+ * known (the emit of step 6 may still be running).  In a batch without
+ * m_idx_out the first brackets of up to 4 rows are enqueued before the
+ * host waits for the first row's record, each with its own slice of the
+ * workspace (lapsum_forward_bracketed_workspace_size counts the slices).
+ * The first call on a host thread allocates a small pinned host buffer
+ * that the library keeps.
  *
  *   K           sample size, 2 <= K <= n.
  *   z           bracket half-width in standard deviations (the paper uses

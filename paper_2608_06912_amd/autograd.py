@@ -29,10 +29,11 @@ __all__ = ["soft_topk", "hard_topk_mask", "straight_through", "choose_path", "sa
 
 # Rows up to this length take the full sort; longer rows the sample bracket.
 # §4 places the switch where the two paths cost the same; on MI355X the
-# forward + backward of one row costs 0.114 ms (sort) against 0.140 ms
-# (bracket) at n = 2^20 and 0.161 against 0.157 ms at 2^21, and the same
-# holds per row in batches of 8.
-FULL_SORT_MAX_N = 1 << 21
+# forward + backward of one row costs 0.091 ms (sort) against 0.120 ms
+# (bracket) at n = 2^19, 0.114 against 0.111 ms at 2^20 and 0.162 against
+# 0.109 ms at 2^21; per row in batches of 8 the switch falls in the same
+# place.
+FULL_SORT_MAX_N = 1 << 20
 
 
 def choose_path(n: int) -> str:

@@ -286,12 +286,17 @@ void widen(float* aL, float* aR, int side) {
 }
 
 // Pinned host records the bracketed path reads back (one set per host
-// thread, allocated on its first use and kept), and the event that tells
-// the host a copy has landed while later work proceeds on the stream.
+// thread, allocated on its first use and kept; one slot per row in flight),
+// and the event that tells the host a copy has landed while later work
+// proceeds on the stream.
 struct HostStage {
   AttemptRec att;
   uint32_t seq;   // set by the bucketed solve after att
+  uint32_t pad[3];
 };
+// Rows of a batch whose first bracket is enqueued before the host reads
+// the first row's record (each with its own workspace slice and host slot).
+constexpr int kRowsInFlight = 4;
 struct ThreadStage {
   HostStage* h = nullptr;
   HostStage* dev = nullptr;   // the same memory as the device addresses it
@@ -305,14 +310,14 @@ thread_local ThreadStage t_stage;
 int host_stage(HostStage** h, HostStage** dev, hipEvent_t* ev) {
   if (!t_stage.h) {
     void* ptr = nullptr;
-    if (hipHostMalloc(&ptr, sizeof(HostStage),
+    if (hipHostMalloc(&ptr, kRowsInFlight * sizeof(HostStage),
                       hipHostMallocPortable | hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
       return LAPSUM_ERR_HIP;
     void* dptr = nullptr;
     if (hipHostGetDevicePointer(&dptr, ptr, 0) != hipSuccess) return LAPSUM_ERR_HIP;
     t_stage.h = static_cast<HostStage*>(ptr);
     t_stage.dev = static_cast<HostStage*>(dptr);
-    t_stage.h->seq = 0u;
+    for (int i = 0; i < kRowsInFlight; ++i) t_stage.h[i].seq = 0u;
   }
   if (!t_stage.ev) {
     if (hipEventCreateWithFlags(&t_stage.ev, hipEventDisableTiming) != hipSuccess)
@@ -370,10 +375,45 @@ int wait_seq(const HostStage* h, uint32_t want, hipStream_t s) {
   }
 }
 
+// The first bracket of a row without requested M indices: sample, select,
+// partition, bucketed solve (its record and then `seq` to host slot
+// `slot`), and the emit, which writes p only if the bracket was certified.
+// Nothing waits; bracketed_row takes the row from there.
+int launch_first_bracket(const float* r, int64_t n, double k, double alpha, int64_t K, double z,
+                         const float* noise, const int32_t* sample_idx, int64_t mcap,
+                         float* p_row, double* b_row, void* band_row, BracketWs& w, int slot,
+                         uint32_t seq, hipStream_t s) {
+  const double t = -alpha;
+  HostStage* hs = nullptr;
+  HostStage* hs_dev = nullptr;
+  hipEvent_t ev = nullptr;
+  const int st = host_stage(&hs, &hs_dev, &ev);
+  if (st != LAPSUM_OK) return st;
+  int64_t j = 0, l = 0;
+  bracket_ranks(n, k, K, z, &j, &l);
+  const BandCtx band = band_ctx_view(band_row ? band_row : w.band, n);
+  LAPSUM_TRY(launch_sample(r, n, noise, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist,
+                           kBucketAccWords, s));
+  LAPSUM_TRY(launch_select(w.ykeys, K, w.soffs, w.scnt, j, l, w.sel, s));
+  LAPSUM_TRY(launch_partition(r, n, w.sel, 1, 0.0f, 0.0f, t, w.nblocks, w.chunk, w.stage_v,
+                              w.stage_i, w.blk, band, w.ones, s));
+  const PartSource ps{w.blk, w.nblocks, w.stage_v, w.sel, 1, 0.0f, 0.0f};
+  LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec, &hs_dev[slot].att,
+                                 &hs_dev[slot].seq, seq, s));
+  LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, w.tot, p_row, b_row, s));
+  return LAPSUM_OK;
+}
+
+// A first bracket already enqueued by launch_first_bracket.
+struct FirstBracket {
+  int slot;
+  uint32_t seq;
+};
+
 int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, double z,
                   const float* noise, const int32_t* sample_idx, int64_t mcap, int64_t out_cap, uint32_t flags, float* p_row,
                   double* b_row, lapsum_bracket_info* info, int32_t* midx_row, void* band_row,
-                  BracketWs& w, hipStream_t s) {
+                  BracketWs& w, hipStream_t s, const FirstBracket* pre = nullptr) {
   const double t = -alpha;
   lapsum_bracket_info rec_info;
   memset(&rec_info, 0, sizeof(rec_info));
@@ -389,16 +429,22 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
   hipEvent_t ev = nullptr;
   int st = host_stage(&hs, &hs_dev, &ev);
   if (st != LAPSUM_OK) return st;
+  if (pre) hs += pre->slot;   // this row's record lands in its own slot
 
   if (!(flags & LAPSUM_FLAG_FULL_SORT)) {
-    LAPSUM_TRY(launch_sample(r, n, noise, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist, kBucketAccWords, s));
-    LAPSUM_TRY(launch_select(w.ykeys, K, w.soffs, w.scnt, j, l, w.sel, s));
+    if (!pre) {
+      LAPSUM_TRY(launch_sample(r, n, noise, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist,
+                               kBucketAccWords, s));
+      LAPSUM_TRY(launch_select(w.ykeys, K, w.soffs, w.scnt, j, l, w.sel, s));
+    }
     float aL = 0.0f, aR = 0.0f;
     const bool want_idx = midx_row != nullptr;
     for (int attempt = 1; attempt <= 3 && !solved; ++attempt) {
       const int use_sel = attempt == 1 ? 1 : 0;
-      LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR, t, w.nblocks, w.chunk, w.stage_v,
-                                  w.stage_i, w.blk, band, w.ones, s));
+      const bool prelaunched = pre && attempt == 1;   // partition, solve and emit enqueued
+      if (!prelaunched)
+        LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR, t, w.nblocks, w.chunk,
+                                    w.stage_v, w.stage_i, w.blk, band, w.ones, s));
       // M in index order, one contiguous array: needed for the sorted
       // indices and for the full sort of M; the buckets read the staging
       auto gather_in_order = [&]() -> int {
@@ -452,11 +498,17 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
         // buckets straight from the staging, with no wait for the totals
         // the solve writes its record to host memory as well; the emit (of
         // a certified bracket only) runs while the host waits for it
-        const PartSource ps{w.blk, w.nblocks, w.stage_v, w.sel, use_sel, aL, aR};
-        const uint32_t seq = t_stage.next_seq++;
-        LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec, &hs_dev->att,
-                                       &hs_dev->seq, seq, s));
-        LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, w.tot, p_row, b_row, s));
+        uint32_t seq = 0;
+        if (prelaunched) {
+          seq = pre->seq;
+        } else {
+          const int slot = pre ? pre->slot : 0;
+          const PartSource ps{w.blk, w.nblocks, w.stage_v, w.sel, use_sel, aL, aR};
+          seq = t_stage.next_seq++;
+          LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec,
+                                         &hs_dev[slot].att, &hs_dev[slot].seq, seq, s));
+          LAPSUM_TRY(launch_band_emit(r, n, w.rec, t, band, w.ones, w.tot, p_row, b_row, s));
+        }
         st = wait_seq(hs, seq, s);
         if (st != LAPSUM_OK) return st;
         tot = hs->att.tot;
@@ -755,11 +807,17 @@ int lapsum_dftopk_backward(const float* grad_p, const float* p, const int32_t* p
   return LAPSUM_OK;
 }
 
+// Workspace slices of a bracketed call: one per row in flight (rows of a
+// batch without requested M indices), each a whole row's workspace.
+int64_t bracket_slices(int64_t batch, bool with_idx) {
+  return with_idx ? 1 : (batch < kRowsInFlight ? (batch < 1 ? 1 : batch) : kRowsInFlight);
+}
+
 size_t lapsum_forward_bracketed_workspace_size(int64_t batch, int64_t n, int64_t K,
                                                int64_t m_capacity, int with_m_idx) {
-  (void)batch;
   if (n < 1 || K < 1 || m_capacity < 1) return 0;
-  return bracketed_ws(n, K, m_capacity < n ? m_capacity : n, with_m_idx != 0);
+  const size_t one = bracketed_ws(n, K, m_capacity < n ? m_capacity : n, with_m_idx != 0);
+  return static_cast<size_t>(bracket_slices(batch, with_m_idx != 0)) * one;
 }
 
 size_t lapsum_band_size(int64_t batch, int64_t n) {
@@ -781,19 +839,52 @@ int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n, doub
   // |M| <= n always, so capacity beyond n is never used internally; the
   // caller's m_idx_out rows keep their m_capacity stride.
   const int64_t mcap = m_capacity < n ? m_capacity : n;
-  const int wst = check_ws(workspace, workspace_bytes, bracketed_ws(n, K, mcap, m_idx_out != nullptr));
+  const bool with_idx = m_idx_out != nullptr;
+  const int wst = check_ws(workspace, workspace_bytes,
+                           lapsum_forward_bracketed_workspace_size(batch, n, K, m_capacity, with_idx));
   if (wst != LAPSUM_OK) return wst;
   const int dst = check_device();
   if (dst != LAPSUM_OK) return dst;
-  Carve c(workspace);
-  BracketWs w = carve_bracket(c, n, K, mcap, m_idx_out != nullptr);
   const size_t band_row_bytes = band_ctx_bytes(n);
+  auto band_of = [&](int64_t row) -> void* {
+    return band ? static_cast<char*>(band) + row * band_row_bytes : nullptr;
+  };
+  Carve c(workspace);
+  if (with_idx || (flags & LAPSUM_FLAG_FULL_SORT) || batch == 1) {
+    BracketWs w = carve_bracket(c, n, K, mcap, with_idx);
+    for (int64_t row = 0; row < batch; ++row) {
+      int st = bracketed_row(scores + row * n, n, k, alpha, K, z, noise, sample_idx, mcap,
+                             m_capacity, flags, p + row * n, b + row, info ? info + row : nullptr,
+                             m_idx_out ? m_idx_out + row * m_capacity : nullptr, band_of(row), w,
+                             stream);
+      if (st != LAPSUM_OK) return st;
+    }
+    return LAPSUM_OK;
+  }
+  // rows in flight: the first brackets of up to kRowsInFlight rows are
+  // enqueued before the host reads the first row's record, so the device
+  // runs the next rows while the host finishes the earlier ones
+  const int64_t P = bracket_slices(batch, false);
+  BracketWs ws[kRowsInFlight];
+  for (int64_t q = 0; q < P; ++q) ws[q] = carve_bracket(c, n, K, mcap, false);
+  FirstBracket pre[kRowsInFlight];
+  auto launch = [&](int64_t row) -> int {
+    const int q = static_cast<int>(row % P);
+    pre[q].slot = q;
+    pre[q].seq = t_stage.next_seq++;
+    return launch_first_bracket(scores + row * n, n, k, alpha, K, z, noise, sample_idx, mcap,
+                                p + row * n, b + row, band_of(row), ws[q], q, pre[q].seq, stream);
+  };
+  for (int64_t row = 0; row < P; ++row) {
+    const int st = launch(row);
+    if (st != LAPSUM_OK) return st;
+  }
   for (int64_t row = 0; row < batch; ++row) {
-    void* band_row = band ? static_cast<char*>(band) + row * band_row_bytes : nullptr;
+    const int q = static_cast<int>(row % P);
     int st = bracketed_row(scores + row * n, n, k, alpha, K, z, noise, sample_idx, mcap,
-                           m_capacity, flags,
-                           p + row * n, b + row, info ? info + row : nullptr,
-                           m_idx_out ? m_idx_out + row * m_capacity : nullptr, band_row, w, stream);
+                           m_capacity, flags, p + row * n, b + row, info ? info + row : nullptr,
+                           nullptr, band_of(row), ws[q], stream, &pre[q]);
+    if (st == LAPSUM_OK && row + P < batch) st = launch(row + P);
     if (st != LAPSUM_OK) return st;
   }
   return LAPSUM_OK;
