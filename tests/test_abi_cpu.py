@@ -181,3 +181,13 @@ def test_comparators_reject_invalid_arguments():
     assert f(10, wsp=0) == 2 and f(10, wsb=ws - 1) == 2
     assert lib.lapsum_dftopk_backward(v(1), v(1), v(0), 1, 1000, -1.0, v(1), v(256), ws,
                                       v(0)) == 1
+
+
+def test_bracketed_workspace_has_a_slice_per_row_in_flight():
+    one = L.lapsum_forward_bracketed_workspace_size(1, 100000, 2000, 5000)
+    assert one > 0
+    assert L.lapsum_forward_bracketed_workspace_size(3, 100000, 2000, 5000) == 3 * one
+    assert L.lapsum_forward_bracketed_workspace_size(9, 100000, 2000, 5000) == 4 * one
+    # with the M indices the rows go one after another through one slice
+    assert L.lapsum_forward_bracketed_workspace_size(9, 100000, 2000, 5000, True) == \
+        L.lapsum_forward_bracketed_workspace_size(1, 100000, 2000, 5000, True)

@@ -544,6 +544,32 @@ def test_bracketed_sqrt_sample_size(lib):
     _sampled_p_check(p, r, bo, w.alpha)
 
 
+@pytest.mark.parametrize("shift", [0.0, 3.0])
+def test_bracketed_batch_past_the_rows_in_flight(lib, shift):
+    # nine rows: the first brackets of four rows are in flight at a time,
+    # each workspace slice and host slot is reused by the row four later;
+    # with the noise shifted every row widens and falls back while later rows
+    # are already enqueued
+    batch, n = 9, 60_000
+    rows = W.random_case(52, n, dist="normal", batch=batch)
+    rows[4] *= np.float32(3.0)
+    k, alpha = n / 10.0, -0.05
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([96], K, 0.05) + np.float32(shift)
+    band = lib.new_band(batch, n, "cuda")
+    p, b, infos, _ = lib.lapsum_forward_bracketed(_t(rows), k, alpha, _t(noise), band=band)
+    gs = W.random_case(53, n, dist="normal", batch=batch)
+    grad = _np(lib.lapsum_backward_band(_t(gs), p, band, alpha))
+    pn, bn = _np(p), _np(b)
+    for i in range(batch):
+        po, bo, oinfo, _ = O.bracketed_forward(rows[i], k, alpha, noise)
+        _check_info(infos[i], oinfo, f"row {i}")
+        assert (oinfo.attempts > 1) == (shift != 0.0), (i, oinfo.attempts)
+        assert abs(float(bn[i]) - bo) <= 2e-6 * -alpha, i
+        assert np.max(np.abs(pn[i].astype(np.float64) - O.probs(rows[i], bo, alpha))) <= P_TOL, i
+        assert grad_rel(grad[i], O.vjp(rows[i], bo, alpha, gs[i])) <= G_TOL, i
+
+
 @pytest.mark.parametrize("n", [700, 1024, 1025])
 def test_bracketed_rows_of_about_one_tile(lib, n):
     # one writer workgroup; the last tile whole, partial, or a single score
