@@ -903,6 +903,10 @@ __global__ __launch_bounds__(TOT_T) void partition_totals_kernel(const PartBlock
 // M members in LDS with a wave-private counter; the block then writes them
 // to its slot of the global staging area (wave 0's first) and one record of
 // tails and counts.
+// HAS_R: a_R is finite (the host knows: for the first bracket from the rank
+// l <= K, afterwards from the endpoints it passes).  One instance per case
+// keeps the common one (a_R infinite) in fewer registers.
+template <bool HAS_R>
 __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__ r, int64_t n,
                                                        const SelectRec* __restrict__ sel,
                                                        int use_sel, float aL_arg, float aR_arg,
@@ -943,17 +947,11 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
   bw.w0 = w0;
   PartState st{0.0, 0.0, 0, 0, 0, INFINITY, -INFINITY, 0};
   int32_t tb = 0;
-  const bool has_r = aR < INFINITY;
-  if (has_r)
-    if (bw.stage)
-      partition_range<true, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
-    else
-      partition_range<true, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
+  const bool has_r = HAS_R;
+  if (bw.stage)
+    partition_range<HAS_R, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
   else
-    if (bw.stage)
-      partition_range<false, true>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
-    else
-      partition_range<false, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
+    partition_range<HAS_R, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
   // this wave's bits and band list out of LDS
   if (bw.stage) {
     if (has_r) {
@@ -1059,16 +1057,21 @@ mx = wave_max(mx, -INFINITY);
 }
 
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
-                            float aR, double t, int nblocks, int64_t chunk, float* stage_v,
-                            int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
-                            hipStream_t s) {
+                            float aR, bool has_r, double t, int nblocks, int64_t chunk,
+                            float* stage_v, int32_t* stage_i, PartBlock* blk, const BandCtx& band,
+                            uint32_t* ones, hipStream_t s) {
   if (band.nblocks != nblocks || band.chunk != chunk || nblocks > kPartMaxBlocks)
     return hipErrorInvalidValue;
   const float c2f = static_cast<float>(kLog2e / t);
   { ProfScope ps_("partition", s);
-  hipLaunchKernelGGL(partition_kernel, dim3(nblocks), dim3(PT), 0, s, r, n, sel, use_sel, aL, aR,
-                     c2f, chunk, stage_v, stage_i, blk, t, band.ent, band.blk, band.tiles, band.cap,
-                     ones); }
+  if (has_r)
+    hipLaunchKernelGGL(partition_kernel<true>, dim3(nblocks), dim3(PT), 0, s, r, n, sel, use_sel,
+                       aL, aR, c2f, chunk, stage_v, stage_i, blk, t, band.ent, band.blk,
+                       band.tiles, band.cap, ones);
+  else
+    hipLaunchKernelGGL(partition_kernel<false>, dim3(nblocks), dim3(PT), 0, s, r, n, sel, use_sel,
+                       aL, aR, c2f, chunk, stage_v, stage_i, blk, t, band.ent, band.blk,
+                       band.tiles, band.cap, ones); }
   return hipGetLastError();
 }
 

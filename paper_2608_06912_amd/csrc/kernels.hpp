@@ -235,11 +235,13 @@ int band_wave_cap(int64_t chunk);
 size_t band_ctx_bytes(int64_t n);
 BandCtx band_ctx_view(void* base, int64_t n);
 // ones: [ceil(n / kBandTile) * kBandTile / 32] bit set where r >= hi (written
-// only when a_R is finite; the words past n are never written).
+// only when a_R is finite; the words past n are never written).  has_r: a_R
+// is finite (with use_sel, the selected rank l is at most K); a false has_r
+// with a finite a_R would leave R uncounted.
 hipError_t launch_partition(const float* r, int64_t n, const SelectRec* sel, int use_sel, float aL,
-                            float aR, double t, int nblocks, int64_t chunk, float* stage_v,
-                            int32_t* stage_i, PartBlock* blk, const BandCtx& band, uint32_t* ones,
-                            hipStream_t s);
+                            float aR, bool has_r, double t, int nblocks, int64_t chunk,
+                            float* stage_v, int32_t* stage_i, PartBlock* blk, const BandCtx& band,
+                            uint32_t* ones, hipStream_t s);
 // Fixed-order totals of the block records (*tot) and each block's offset
 // into M (for launch_gather).
 hipError_t launch_partition_totals(const PartBlock* blk, int nblocks, const SelectRec* sel,

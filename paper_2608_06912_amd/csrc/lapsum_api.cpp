@@ -395,8 +395,8 @@ int launch_first_bracket(const float* r, int64_t n, double k, double alpha, int6
   LAPSUM_TRY(launch_sample(r, n, noise, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist,
                            kBucketAccWords, s));
   LAPSUM_TRY(launch_select(w.ykeys, K, w.soffs, w.scnt, j, l, w.sel, s));
-  LAPSUM_TRY(launch_partition(r, n, w.sel, 1, 0.0f, 0.0f, t, w.nblocks, w.chunk, w.stage_v,
-                              w.stage_i, w.blk, band, w.ones, s));
+  LAPSUM_TRY(launch_partition(r, n, w.sel, 1, 0.0f, 0.0f, l <= K, t, w.nblocks, w.chunk,
+                              w.stage_v, w.stage_i, w.blk, band, w.ones, s));
   const PartSource ps{w.blk, w.nblocks, w.stage_v, w.sel, 1, 0.0f, 0.0f};
   LAPSUM_TRY(launch_bucket_solve(ps, mcap, w.acc, w.tot, k, t, n, w.rec, &hs_dev[slot].att,
                                  &hs_dev[slot].seq, seq, s));
@@ -443,7 +443,8 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
       const int use_sel = attempt == 1 ? 1 : 0;
       const bool prelaunched = pre && attempt == 1;   // partition, solve and emit enqueued
       if (!prelaunched)
-        LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR, t, w.nblocks, w.chunk,
+        LAPSUM_TRY(launch_partition(r, n, w.sel, use_sel, aL, aR,
+                                    use_sel ? l <= K : aR < INFINITY, t, w.nblocks, w.chunk,
                                     w.stage_v, w.stage_i, w.blk, band, w.ones, s));
       // M in index order, one contiguous array: needed for the sorted
       // indices and for the full sort of M; the buckets read the staging
