@@ -544,13 +544,13 @@ def test_bracketed_sqrt_sample_size(lib):
     _sampled_p_check(p, r, bo, w.alpha)
 
 
-@pytest.mark.parametrize("shift", [0.0, 3.0])
-def test_bracketed_batch_past_the_rows_in_flight(lib, shift):
+@pytest.mark.parametrize("n,shift", [(60_000, 0.0), (60_000, 3.0), (1025, 3.0)])
+def test_bracketed_batch_past_the_rows_in_flight(lib, n, shift):
     # nine rows: the first brackets of four rows are in flight at a time,
     # each workspace slice and host slot is reused by the row four later;
-    # with the noise shifted every row widens and falls back while later rows
-    # are already enqueued
-    batch, n = 9, 60_000
+    # with the noise shifted every row widens, some fall back (on chip for
+    # n = 1025), while later rows are already enqueued
+    batch = 9
     rows = W.random_case(52, n, dist="normal", batch=batch)
     rows[4] *= np.float32(3.0)
     k, alpha = n / 10.0, -0.05
@@ -559,12 +559,14 @@ def test_bracketed_batch_past_the_rows_in_flight(lib, shift):
     band = lib.new_band(batch, n, "cuda")
     p, b, infos, _ = lib.lapsum_forward_bracketed(_t(rows), k, alpha, _t(noise), band=band)
     gs = W.random_case(53, n, dist="normal", batch=batch)
-    grad = _np(lib.lapsum_backward_band(_t(gs), p, band, alpha))
+    grad, gk, ga = lib.lapsum_backward_band(_t(gs), p, band, alpha, params=True)
+    grad, gk, ga = _np(grad), _np(gk), _np(ga)
     pn, bn = _np(p), _np(b)
     for i in range(batch):
         po, bo, oinfo, _ = O.bracketed_forward(rows[i], k, alpha, noise)
         _check_info(infos[i], oinfo, f"row {i}")
         assert (oinfo.attempts > 1) == (shift != 0.0), (i, oinfo.attempts)
+        check_params(float(gk[i]), float(ga[i]), rows[i], float(bn[i]), alpha, gs[i], f"row {i}")
         assert abs(float(bn[i]) - bo) <= 2e-6 * -alpha, i
         assert np.max(np.abs(pn[i].astype(np.float64) - O.probs(rows[i], bo, alpha))) <= P_TOL, i
         assert grad_rel(grad[i], O.vjp(rows[i], bo, alpha, gs[i])) <= G_TOL, i
