@@ -51,7 +51,8 @@ void prof_begin(const char* name, hipStream_t s) {
 }
 void prof_end(hipStream_t s) {
   if (!g_prof_on || g_prof_recs.empty()) return;
-  hipEventRecord(g_prof_recs.back().b, s);
+  // a launch whose end could not be marked is not reported
+  if (hipEventRecord(g_prof_recs.back().b, s) != hipSuccess) g_prof_recs.pop_back();
 }
 }  // namespace lapsum
 
