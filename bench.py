@@ -47,6 +47,9 @@ MEASURED_TRAFFIC = {
     "partition": ("bracket_kernels.hip", "34b446f5fbf6cfd72a920c1f3db02cb9ccd0fb57", 413.9e6),
 }
 METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
+# The paper's dispatched forward times in its headline setting (abstract,
+# Table ks-main; NVIDIA RTX 5060 Laptop GPU): context only, other hardware.
+PAPER_FWD_MS = {10**6: 0.41, 10**7: 1.15, 10**8: 5.23}
 
 
 def parse():
@@ -227,7 +230,8 @@ def paper_setting(dev):
         g = torch.randn((1, n), generator=gen, device=dev, dtype=torch.float32)
         path = A.choose_path(n)
         fwd, fb = _fwd_bwd_fns(L, A, x, g, n / 16.0, -1.0, path)
-        out.append({"n": n, "path": path, "fwd_ms": _timed_ms(fwd), "fwd_bwd_ms": _timed_ms(fb)})
+        out.append({"n": n, "path": path, "fwd_ms": _timed_ms(fwd), "fwd_bwd_ms": _timed_ms(fb),
+                    "paper_fwd_ms_rtx5060_laptop": PAPER_FWD_MS[n]})
         del x, g
     return out
 
