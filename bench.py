@@ -44,7 +44,7 @@ MEASURED_TRAFFIC = {
     "band_emit": ("band_kernels.hip", "971a0862c0f5a91fea8077dbc5e75929152da532", 427.2e6),
     "band_vjp_emit": ("band_kernels.hip", "971a0862c0f5a91fea8077dbc5e75929152da532", 443.6e6),
     "band_vjp_reduce": ("band_kernels.hip", "971a0862c0f5a91fea8077dbc5e75929152da532", 61.3e6),
-    "partition": ("bracket_kernels.hip", "7880541b7476504884cd0b31725e6b58250d0fcd", 413.9e6),
+    "partition": ("bracket_kernels.hip", "2efa96ac60bad2d48f9ed8e80819e8f7556f19d3", 413.8e6),
 }
 METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
 # The paper's dispatched forward times in its headline setting (abstract,

@@ -246,10 +246,20 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __r
     if (tid < 2 * GB) hf[tid / GB][tid % GB] = 0u;
     __syncthreads();
     {
+      // eight blocks' counts per thread in flight at a time
+      constexpr int BS = kSelThreads / kSelectGroups;   // blocks per sweep
       const int gi = tid % kSelectGroups;
       uint32_t sum = 0u;
-      for (int b = tid / kSelectGroups; b < nsb; b += kSelThreads / kSelectGroups)
-        sum += scnt[static_cast<int64_t>(b) * kSampleCntWords + kSelectBins / 2 + gi];
+      for (int b0 = tid / kSelectGroups; b0 < nsb; b0 += 8 * BS) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int b = b0 + u * BS;
+          v[u] = b < nsb ? scnt[static_cast<int64_t>(b) * kSampleCntWords + kSelectBins / 2 + gi] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) sum += v[u];
+      }
       if (sum) atomicAdd(&hc[gi], sum);
     }
     __syncthreads();
@@ -269,16 +279,31 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const uint32_t* __r
     {
       // GB / 2 packed words of the group per block, both targets at once
       constexpr int WPG = GB / 2;
+      constexpr int BS = kSelThreads / WPG;   // blocks per sweep
       const int wi = tid % WPG;
-      for (int b = tid / WPG; b < nsb; b += kSelThreads / WPG) {
-        const uint32_t* sc = scnt + static_cast<int64_t>(b) * kSampleCntWords;
+      uint32_t lo[2] = {0u, 0u}, hi[2] = {0u, 0u};
+      for (int b0 = tid / WPG; b0 < nsb; b0 += 4 * BS) {
+        uint32_t wv[4][2];
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          if (!live[q]) continue;
-          const uint32_t wv = sc[grp_s[q] * WPG + wi];
-          if (wv & 0xffffu) atomicAdd(&hf[q][2 * wi], wv & 0xffffu);
-          if (wv >> 16) atomicAdd(&hf[q][2 * wi + 1], wv >> 16);
+        for (int u = 0; u < 4; ++u) {
+          const int b = b0 + u * BS;
+          const uint32_t* sc = scnt + static_cast<int64_t>(b < nsb ? b : 0) * kSampleCntWords;
+#pragma unroll
+          for (int q = 0; q < 2; ++q) wv[u][q] = (b < nsb && live[q]) ? sc[grp_s[q] * WPG + wi] : 0u;
         }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            lo[q] += wv[u][q] & 0xffffu;
+            hi[q] += wv[u][q] >> 16;
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        if (lo[q]) atomicAdd(&hf[q][2 * wi], lo[q]);
+        if (hi[q]) atomicAdd(&hf[q][2 * wi + 1], hi[q]);
       }
     }
     __syncthreads();
