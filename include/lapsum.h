@@ -247,8 +247,12 @@ int lapsum_dftopk_backward(const float* grad_p, const float* p,
  *   K           sample size, 2 <= K <= n.
  *   z           bracket half-width in standard deviations (the paper uses
  *               5.16), finite and > 0.
- *   noise       [K] float32 Laplace(0, |alpha|) draws, shared by all rows
- *               (the cached kernel noise); required.
+ *   noise       NULL, or [K] float32 Laplace(0, |alpha|) draws shared by all
+ *               rows (the cached kernel noise of §4 and Algorithm 1).  NULL:
+ *               the library draws the table itself from `seed`, the same
+ *               draws lapsum_bracket_noise(seed, K, alpha) writes (they are
+ *               formed inside the sample pass, so no table is stored).
+ *   seed        the default noise's seed; ignored when noise is given.
  *   sample_idx  NULL (systematic sample), or [K] int32 indices drawn
  *               uniformly from [0, n) by the caller, shared by all rows
  *               (i.i.d. sample); entries outside [0, n) are clamped to it.
@@ -292,12 +296,35 @@ size_t lapsum_band_size(int64_t batch, int64_t n);
 
 int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n,
                              double k, double alpha, int64_t K, double z,
-                             const float* noise, const int32_t* sample_idx,
+                             const float* noise, uint64_t seed,
+                             const int32_t* sample_idx,
                              int64_t m_capacity, uint32_t flags, float* p, double* b,
                              lapsum_bracket_info* info, int32_t* m_idx_out,
                              void* band, size_t band_bytes,
                              void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * The bracket's default kernel noise (§4: the sample is a strided view plus
+ * cached Laplace kernel noise; Algorithm 1 draws it once): draw s of seed
+ * `seed`, s = 0..K-1, is
+ *
+ *   z = the (s+1)-th output of SplitMix64 started at state `seed` (Steele,
+ *       Lea and Flood, "Fast splittable pseudorandom number generators",
+ *       OOPSLA 2014): x = seed + (s+1) 0x9E3779B97F4A7C15 (mod 2^64),
+ *       z = (x ^ (x >> 30)) 0xBF58476D1CE4E5B9, z = (z ^ (z >> 27))
+ *       0x94D049BB133111EB, z = z ^ (z >> 31);
+ *   u = (2 (z >> 12) + 1) 2^-53, strictly inside (0, 1);
+ *   eps_s = t ln(2u) for u < 1/2, -t ln(2(1 - u)) otherwise (the Laplace
+ *       inverse CDF, t = -alpha), in float64, rounded to float32.
+ *
+ * A counter-based generator: the same (seed, s) gives the same draw on
+ * every call, so the table needs no storage.  This call writes the table
+ * that lapsum_forward_bracketed uses when it is given noise == NULL.
+ *   out   [K] float32 device memory, 1 <= K <= 2^31 - 1.
+ * ------------------------------------------------------------------------ */
+int lapsum_bracket_noise(uint64_t seed, int64_t K, double alpha, float* out,
+                         hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Backward from a saved band: the same vector-Jacobian product as

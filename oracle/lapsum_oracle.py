@@ -37,6 +37,10 @@ vjp_params             §5 (the attack trains k and alpha): dL/dk and dL/dalpha
 fd_params              centred finite differences of <g, p> in k and alpha.
 bracket_ranks          Eq. (8): j = floor(Kq - z sqrt(Kq(1-q))),
                        l = ceil(Kq + z sqrt(Kq(1-q))), q = (n-k)/n.
+splitmix64             the counter-based generator behind the default
+                       kernel noise (its published definition).
+counter_laplace_noise  the default kernel noise: Laplace(0, t) by the
+                       inverse CDF of SplitMix64 uniforms.
 systematic_sample      §4 / Suppl. C remark (iii): strided view plus cached
                        kernel noise, y_s = r_{s*stride} + eps_s.
 iid_sample             Suppl. C, Theorem 2: uniform draws with replacement
@@ -75,7 +79,7 @@ __all__ = [
     "laplace_cdf", "lapsum", "initial_bracket", "solve_bisect", "solve_brent",
     "certify_root", "desc_keys", "desc_order", "solve_sorted_scan", "probs",
     "vjp", "vjp_params", "forward", "fd_vjp", "fd_params", "bracket_ranks", "systematic_sample",
-    "iid_sample", "dftopk", "dftopk_vjp",
+    "iid_sample", "dftopk", "dftopk_vjp", "splitmix64", "counter_laplace_noise",
     "order_statistic", "partition", "solve_in_bracket", "widen",
     "BracketInfo", "bracketed_forward", "zero_temperature_threshold",
     "budget_error",
@@ -493,6 +497,42 @@ def bracket_ranks(n: int, k: float, K: int, z: float):
     j = math.floor(K * q - z * sd)
     l = math.ceil(K * q + z * sd)
     return int(j), int(l), q
+
+
+def splitmix64(seed: int, count: int) -> list[int]:
+    """The first `count` outputs of SplitMix64 from state `seed` (Steele, Lea
+    and Flood, "Fast splittable pseudorandom number generators", OOPSLA
+    2014): the state advances by the golden-ratio increment 0x9E3779B97F4A7C15
+    and each output is the state passed through the variant-13 mixing
+    function (xor-shift 30, multiply 0xBF58476D1CE4E5B9, xor-shift 27,
+    multiply 0x94D049BB133111EB, xor-shift 31), all modulo 2^64.  Python
+    integers, one output at a time."""
+    mask = (1 << 64) - 1
+    state = seed & mask
+    out = []
+    for _ in range(count):
+        state = (state + 0x9E3779B97F4A7C15) & mask
+        x = state
+        x = ((x ^ (x >> 30)) * 0xBF58476D1CE4E5B9) & mask
+        x = ((x ^ (x >> 27)) * 0x94D049BB133111EB) & mask
+        out.append(x ^ (x >> 31))
+    return out
+
+
+def counter_laplace_noise(seed: int, K: int, t: float) -> np.ndarray:
+    """The library's default kernel noise for the bracket's sample (§4: a
+    cached table of Laplace kernel noise; here drawn from a seed): draw s is
+    the (s+1)-th SplitMix64 output z of `seed`, u = (2 floor(z / 2^12) + 1)
+    / 2^53 (uniform, strictly inside (0, 1)), and the Laplace(0, t) inverse
+    CDF of u, t ln(2u) below 1/2 and -t ln(2(1 - u)) above, in float64,
+    rounded to float32."""
+    z = splitmix64(seed, K)
+    out = np.empty(K, dtype=np.float32)
+    for s, v in enumerate(z):
+        u = (2 * (v >> 12) + 1) / float(1 << 53)
+        e = t * math.log(2.0 * u) if u < 0.5 else -t * math.log(2.0 * (1.0 - u))
+        out[s] = np.float32(e)
+    return out
 
 
 def systematic_sample(r32, noise32) -> np.ndarray:

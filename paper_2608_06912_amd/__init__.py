@@ -22,7 +22,7 @@ __all__ = [
     "load", "LapsumError", "BracketInfo", "lapsum_status_string",
     "lapsum_forward_workspace_size", "lapsum_forward",
     "lapsum_backward_workspace_size", "lapsum_backward",
-    "lapsum_forward_bracketed_workspace_size", "lapsum_forward_bracketed",
+    "lapsum_forward_bracketed_workspace_size", "lapsum_forward_bracketed", "lapsum_bracket_noise",
     "LAPSUM_FLAG_FULL_SORT", "LIB_PATH", "lapsum_profile_start", "lapsum_profile_stop",
     "lapsum_band_size", "new_band", "lapsum_backward_band_workspace_size", "lapsum_backward_band",
     "lapsum_topk_mask", "lapsum_bisect_forward", "lapsum_dftopk_workspace_size",
@@ -70,8 +70,9 @@ def load():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_06912_amd.build`")
     lib = ctypes.CDLL(LIB_PATH)
-    vp, i64, f64, sz, u32, i32 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_double,
-                                  ctypes.c_size_t, ctypes.c_uint32, ctypes.c_int)
+    vp, i64, f64, sz, u32, i32, u64 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_double,
+                                       ctypes.c_size_t, ctypes.c_uint32, ctypes.c_int,
+                                       ctypes.c_uint64)
     lib.lapsum_status_string.argtypes = [i32]
     lib.lapsum_status_string.restype = ctypes.c_char_p
     lib.lapsum_forward_workspace_size.argtypes = [i64, i64, i32]
@@ -84,9 +85,11 @@ def load():
     lib.lapsum_backward.restype = i32
     lib.lapsum_forward_bracketed_workspace_size.argtypes = [i64, i64, i64, i64, i32]
     lib.lapsum_forward_bracketed_workspace_size.restype = sz
-    lib.lapsum_forward_bracketed.argtypes = [vp, i64, i64, f64, f64, i64, f64, vp, vp, i64, u32,
+    lib.lapsum_forward_bracketed.argtypes = [vp, i64, i64, f64, f64, i64, f64, vp, u64, vp, i64, u32,
                                              vp, vp, vp, vp, vp, sz, vp, sz, vp]
     lib.lapsum_forward_bracketed.restype = i32
+    lib.lapsum_bracket_noise.argtypes = [u64, i64, f64, vp, vp]
+    lib.lapsum_bracket_noise.restype = i32
     lib.lapsum_band_size.argtypes = [i64, i64]
     lib.lapsum_band_size.restype = sz
     lib.lapsum_backward_band_workspace_size.argtypes = [i64, i64]
@@ -369,12 +372,30 @@ def _band_arg(band, batch, n):
     return ctypes.c_void_p(band.data_ptr()), band.numel() * band.element_size()
 
 
-def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float = 5.16,
+def lapsum_bracket_noise(seed: int, K: int, alpha: float, device="cuda", *, out=None):
+    """The default kernel noise of the bracket: K float32 Laplace(0, |alpha|)
+    draws of the counter-based generator at `seed` (the table the bracketed
+    forward uses when given noise=None)."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty(int(K), dtype=torch.float32, device=device)
+    elif out.dtype != torch.float32 or out.numel() != int(K) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 tensor of K elements")
+    with _on_device(out.device):
+        _check(load().lapsum_bracket_noise(int(seed) & ((1 << 64) - 1), int(K), float(alpha),
+                                           _ptr(out), _stream(out.device)),
+               "lapsum_bracket_noise")
+    return out
+
+
+def lapsum_forward_bracketed(scores, k: float, alpha: float, noise=None, *, K: int | None = None,
+                             seed: int = 0, z: float = 5.16,
                              m_capacity: int | None = None, flags: int = 0,
                              m_idx: bool = False, band=None, workspace=None, out=None,
                              b_out=None, sample_idx=None):
     """Bracketed forward.  noise: float32 CUDA tensor [K] of Laplace(0, |alpha|)
-    draws.  sample_idx: None (systematic sample) or an int32 CUDA tensor [K]
+    draws, or None for the library's default noise of `seed` (then K must be
+    given).  sample_idx: None (systematic sample) or an int32 CUDA tensor [K]
     of indices in [0, n) for the i.i.d. sample.  band: None, or a buffer from new_band() that receives the band for
     lapsum_backward_band.  out / b_out: optional buffers for p (float32, the
     shape of scores) and b (float64, [batch]).  Returns (p, b, infos, m_idx or
@@ -382,10 +403,16 @@ def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float 
     torch = _torch()
     lib = load()
     batch, n = _rows(scores, "scores")
-    if noise.dim() != 1:
-        raise ValueError("noise must be 1-D [K]")
-    _rows(noise, "noise")
-    K = int(noise.shape[0])
+    if noise is not None:
+        if noise.dim() != 1:
+            raise ValueError("noise must be 1-D [K]")
+        _rows(noise, "noise")
+        if K is not None and int(K) != int(noise.shape[0]):
+            raise ValueError("K differs from the noise table's length")
+        K = int(noise.shape[0])
+    elif K is None:
+        raise ValueError("K is required when noise is None")
+    K = int(K)
     if sample_idx is not None:
         if (not isinstance(sample_idx, torch.Tensor) or sample_idx.dtype != torch.int32
                 or tuple(sample_idx.shape) != (K,) or sample_idx.device != scores.device
@@ -415,7 +442,8 @@ def lapsum_forward_bracketed(scores, k: float, alpha: float, noise, *, z: float 
     bp, bbytes = _band_arg(band, batch, n)
     with _on_device(dev):
         _check(lib.lapsum_forward_bracketed(_ptr(scores), batch, n, float(k), float(alpha), K,
-                                            float(z), _ptr(noise), _ptr(sample_idx),
+                                            float(z), _ptr(noise), int(seed) & ((1 << 64) - 1),
+                                            _ptr(sample_idx),
                                             int(m_capacity), int(flags),
                                             _ptr(p), _ptr(b), ctypes.cast(infos, ctypes.c_void_p),
                                             _ptr(mi), bp, bbytes, _ptr(ws), nbytes, _stream(dev)),

@@ -11,9 +11,10 @@ in the backward, m^ = p + sg(m - p).
 
 Everything here is orchestration over the C ABI: the threshold, p, the
 gradients and the hard mask are computed by the library's kernels.  The
-only tensor arithmetic done by torch is input preparation (the cached
-kernel noise of the bracket's sample, Suppl. C), reshaping, and summing the
-per-row dL/dk, dL/dalpha of a batch that shares one k and one alpha.
+only tensor arithmetic done by torch is input preparation (the i.i.d.
+sampler's indices, Suppl. C), reshaping, and summing the per-row dL/dk,
+dL/dalpha of a batch that shares one k and one alpha; the bracket's kernel
+noise is drawn by the library from the seed.
 """
 from __future__ import annotations
 
@@ -21,8 +22,8 @@ import math
 
 import torch
 
-from . import (lapsum_backward, lapsum_backward_band, lapsum_forward, lapsum_forward_bracketed,
-               lapsum_topk_mask, new_band)
+from . import (lapsum_backward, lapsum_backward_band, lapsum_bracket_noise, lapsum_forward,
+               lapsum_forward_bracketed, lapsum_topk_mask, new_band)
 
 __all__ = ["soft_topk", "hard_topk_mask", "straight_through", "choose_path", "sample_size",
            "bracket_noise", "bracket_indices", "LapSumFunction", "FULL_SORT_MAX_N"]
@@ -60,23 +61,12 @@ def sample_size(n: int, rule: str = "n23") -> int:
     return int(min(max(K, 2), n))
 
 
-_noise_cache: dict = {}
-
-
 def bracket_noise(K: int, t: float, device, seed: int = 0):
-    """K draws of Laplace(0, t) noise for the bracket's sample, drawn once per
-    (K, t, device, seed) and reused, as Suppl. C caches the kernel noise.
-    Inverse CDF of a uniform u in (-1/2, 1/2): -t sign(u) ln(1 - 2|u|)."""
-    device = torch.device(device)
-    key = (int(K), float(t), str(device), int(seed))
-    hit = _noise_cache.get(key)
-    if hit is None:
-        gen = torch.Generator(device="cpu").manual_seed(int(seed))
-        u = torch.rand(int(K), generator=gen, dtype=torch.float64) - 0.5
-        x = -float(t) * torch.sign(u) * torch.log1p(-2.0 * u.abs())
-        hit = x.to(torch.float32).to(device)
-        _noise_cache[key] = hit
-    return hit
+    """The K draws of Laplace(0, t) kernel noise the bracketed forward uses
+    for `seed` when given no table (Suppl. C caches its kernel noise; here
+    the library's counter-based generator gives the same draws on every
+    call, so nothing is cached)."""
+    return lapsum_bracket_noise(seed, K, -float(t), device)
 
 
 _index_cache: dict = {}
@@ -126,7 +116,6 @@ class LapSumFunction(torch.autograd.Function):
             perm = out[2] if want_perm else None
             band = None
         elif path == "bracketed":
-            noise = bracket_noise(K, -af, x.device, noise_seed)
             if sampler == "systematic":
                 idx = None
             elif sampler == "iid":
@@ -134,8 +123,8 @@ class LapSumFunction(torch.autograd.Function):
             else:
                 raise ValueError(f"unknown sampler {sampler!r}")
             band = new_band(x.shape[0], n, x.device)
-            p, b, _, _ = lapsum_forward_bracketed(x, kf, af, noise, z=z, band=band,
-                                                  sample_idx=idx)
+            p, b, _, _ = lapsum_forward_bracketed(x, kf, af, None, K=K, seed=noise_seed, z=z,
+                                                  band=band, sample_idx=idx)
             perm = None
         else:
             raise ValueError(f"unknown path {path!r}")

@@ -50,6 +50,7 @@ constexpr int PW = PT / kWave;                 // 4 waves
 __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __restrict__ r,
                                                                 int64_t n,
                                                                 const float* __restrict__ noise,
+                                                                uint64_t seed, double t,
                                                                 const int32_t* __restrict__ idx,
                                                                 int64_t K, uint32_t* __restrict__ ykeys,
                                                                 uint32_t* __restrict__ soffs,
@@ -76,7 +77,7 @@ __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __r
       at = q < 0 ? 0 : (q >= n ? n - 1 : q);
     }
     rv[i] = r[at];
-    ev[i] = noise[sc];
+    ev[i] = noise ? noise[sc] : counter_laplace(seed, sc, t);
   }
   __syncthreads();
   uint32_t key[kSampleItems], slot[kSampleItems];
@@ -139,13 +140,27 @@ __global__ __launch_bounds__(kSampleThreads) void sample_kernel(const float* __r
 
 int sample_blocks(int64_t K) { return static_cast<int>((K + kSampleBlock - 1) / kSampleBlock); }
 
-hipError_t launch_sample(const float* r, int64_t n, const float* noise, const int32_t* idx,
+hipError_t launch_sample(const float* r, int64_t n, NoiseSrc noise, double t, const int32_t* idx,
                          int64_t K, uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,
                          int64_t zero_words, hipStream_t s) {
   { ProfScope ps_("sample", s);
   hipLaunchKernelGGL(sample_kernel, dim3(static_cast<unsigned>(sample_blocks(K))),
-                     dim3(kSampleThreads), 0, s, r, n, noise, idx, K, ykeys, soffs, scnt, zero,
-                     zero_words); }
+                     dim3(kSampleThreads), 0, s, r, n, noise.table, noise.seed, t, idx, K, ykeys,
+                     soffs, scnt, zero, zero_words); }
+  return hipGetLastError();
+}
+
+// The draws the sample takes when it is given no table.
+__global__ __launch_bounds__(256) void noise_table_kernel(uint64_t seed, int64_t K, double t,
+                                                          float* __restrict__ out) {
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (s < K) out[s] = counter_laplace(seed, s, t);
+}
+
+hipError_t launch_noise_table(uint64_t seed, int64_t K, double t, float* out, hipStream_t s) {
+  { ProfScope ps_("noise_table", s);
+  hipLaunchKernelGGL(noise_table_kernel, dim3(static_cast<unsigned>((K + 255) / 256)), dim3(256),
+                     0, s, seed, K, t, out); }
   return hipGetLastError();
 }
 

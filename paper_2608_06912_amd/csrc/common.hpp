@@ -74,6 +74,26 @@ __device__ __forceinline__ double wexp_f32(double d, double c2) {
   return static_cast<double>(exp2_fast(static_cast<float>(-d * c2)));
 }
 
+// Laplace(0, t) draw number s of the bracket's default kernel noise (the
+// sample takes it when the caller passes no table).  A counter-based
+// generator, so the same (seed, s) always gives the same draw and no state
+// is kept: z is the (s+1)-th output of SplitMix64 started at `seed` (Steele,
+// Lea and Flood, "Fast splittable pseudorandom number generators", 2014),
+// its top 52 bits m give u = (2m + 1) 2^-53, strictly inside (0, 1) and
+// never 1/2 (1 - u is exact), and the Laplace inverse CDF gives
+// t ln(2u) for u < 1/2 and -t ln(2(1 - u)) above, in float64, rounded to
+// float32.
+__device__ __forceinline__ float counter_laplace(uint64_t seed, int64_t s, double t) {
+  uint64_t z = seed + static_cast<uint64_t>(s + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  z ^= z >> 31;
+  const uint64_t m = z >> 12;
+  const double u = static_cast<double>(2 * m + 1) * 0x1p-53;
+  const double e = u < 0.5 ? t * log(2.0 * u) : -t * log(2.0 * (1.0 - u));
+  return static_cast<float>(e);
+}
+
 // e^{-d/t} in float64, for scan combines and the root.
 __device__ __forceinline__ double wexp_f64(double d, double inv_t) { return exp(-d * inv_t); }
 

@@ -223,9 +223,17 @@ hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s);
 // sample also clears zero[0 .. zero_words) for passes that accumulate later.
 int sample_blocks(int64_t K);
 // idx: null (systematic sample) or [K] indices of the i.i.d. sample.
-hipError_t launch_sample(const float* r, int64_t n, const float* noise, const int32_t* idx,
+// The sample's noise: the caller's table, or (table null) the counter-based
+// Laplace(0, t) draws of `seed` (counter_laplace).
+struct NoiseSrc {
+  const float* table;
+  uint64_t seed;
+};
+hipError_t launch_sample(const float* r, int64_t n, NoiseSrc noise, double t, const int32_t* idx,
                          int64_t K, uint32_t* ykeys, uint32_t* soffs, uint32_t* scnt, uint32_t* zero,
                          int64_t zero_words, hipStream_t s);
+// The table counter_laplace gives for draws 0..K-1 of `seed`.
+hipError_t launch_noise_table(uint64_t seed, int64_t K, double t, float* out, hipStream_t s);
 hipError_t launch_select(const uint32_t* ykeys, int64_t K, const uint32_t* soffs,
                          const uint32_t* scnt, int64_t j, int64_t l, SelectRec* out,
                          hipStream_t s);

@@ -349,7 +349,11 @@ int wait_back(hipEvent_t ev) {
 // the runtime enqueue a marker behind that kernel, and the marker's cache
 // writeback delays the next kernel by several microseconds.  If the stream
 // has finished (or failed) without the number appearing, the call fails
-// instead of waiting on.
+// instead of waiting on; so does a wait longer than kSeqWaitLimit (a bracket
+// attempt takes well under a millisecond per 1e8 scores, so only work that
+// can no longer finish, or a stream held up by other work, reaches it).
+constexpr std::chrono::seconds kSeqWaitLimit(30);
+
 int wait_seq(const HostStage* h, uint32_t want, hipStream_t s) {
   const volatile uint32_t* seq = &h->seq;
   using clock = std::chrono::steady_clock;
@@ -367,7 +371,10 @@ int wait_seq(const HostStage* h, uint32_t want, hipStream_t s) {
     }
     if ((i & 1023u) != 0u) continue;
     const hipError_t q = hipStreamQuery(s);
-    if (q == hipErrorNotReady) continue;
+    if (q == hipErrorNotReady) {
+      if (clock::now() - start > kSeqWaitLimit) return LAPSUM_ERR_HIP;
+      continue;
+    }
     if (q == hipSuccess && *seq == want) {
       std::atomic_thread_fence(std::memory_order_acquire);
       return LAPSUM_OK;
@@ -381,7 +388,7 @@ int wait_seq(const HostStage* h, uint32_t want, hipStream_t s) {
 // `slot`), and the emit, which writes p only if the bracket was certified.
 // Nothing waits; bracketed_row takes the row from there.
 int launch_first_bracket(const float* r, int64_t n, double k, double alpha, int64_t K, double z,
-                         const float* noise, const int32_t* sample_idx, int64_t mcap,
+                         NoiseSrc noise, const int32_t* sample_idx, int64_t mcap,
                          float* p_row, double* b_row, void* band_row, BracketWs& w, int slot,
                          uint32_t seq, hipStream_t s) {
   const double t = -alpha;
@@ -393,7 +400,7 @@ int launch_first_bracket(const float* r, int64_t n, double k, double alpha, int6
   int64_t j = 0, l = 0;
   bracket_ranks(n, k, K, z, &j, &l);
   const BandCtx band = band_ctx_view(band_row ? band_row : w.band, n);
-  LAPSUM_TRY(launch_sample(r, n, noise, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist,
+  LAPSUM_TRY(launch_sample(r, n, noise, t, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist,
                            kBucketAccWords, s));
   LAPSUM_TRY(launch_select(w.ykeys, K, w.soffs, w.scnt, j, l, w.sel, s));
   LAPSUM_TRY(launch_partition(r, n, w.sel, 1, 0.0f, 0.0f, l <= K, t, w.nblocks, w.chunk,
@@ -412,7 +419,7 @@ struct FirstBracket {
 };
 
 int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, double z,
-                  const float* noise, const int32_t* sample_idx, int64_t mcap, int64_t out_cap, uint32_t flags, float* p_row,
+                  NoiseSrc noise, const int32_t* sample_idx, int64_t mcap, int64_t out_cap, uint32_t flags, float* p_row,
                   double* b_row, lapsum_bracket_info* info, int32_t* midx_row, void* band_row,
                   BracketWs& w, hipStream_t s, const FirstBracket* pre = nullptr) {
   const double t = -alpha;
@@ -434,7 +441,7 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
 
   if (!(flags & LAPSUM_FLAG_FULL_SORT)) {
     if (!pre) {
-      LAPSUM_TRY(launch_sample(r, n, noise, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist,
+      LAPSUM_TRY(launch_sample(r, n, noise, t, sample_idx, K, w.ykeys, w.soffs, w.scnt, w.hist,
                                kBucketAccWords, s));
       LAPSUM_TRY(launch_select(w.ykeys, K, w.soffs, w.scnt, j, l, w.sel, s));
     }
@@ -828,12 +835,13 @@ size_t lapsum_band_size(int64_t batch, int64_t n) {
 }
 
 int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n, double k, double alpha,
-                             int64_t K, double z, const float* noise,
+                             int64_t K, double z, const float* noise_table, uint64_t seed,
                              const int32_t* sample_idx, int64_t m_capacity,
                              uint32_t flags, float* p, double* b, lapsum_bracket_info* info,
                              int32_t* m_idx_out, void* band, size_t band_bytes, void* workspace,
                              size_t workspace_bytes, hipStream_t stream) {
-  if (!scores || !p || !b || !noise || !valid_common(batch, n, k, alpha)) return LAPSUM_ERR_INVALID_ARG;
+  if (!scores || !p || !b || !valid_common(batch, n, k, alpha)) return LAPSUM_ERR_INVALID_ARG;
+  const NoiseSrc noise{noise_table, seed};
   if (K < 2 || K > n || !isfinite(z) || !(z > 0.0) || m_capacity < 1 || (flags & ~LAPSUM_FLAG_FULL_SORT))
     return LAPSUM_ERR_INVALID_ARG;
   if (band && (band_bytes < lapsum_band_size(batch, n) || reinterpret_cast<uintptr_t>(band) % kAlign))
@@ -889,6 +897,15 @@ int lapsum_forward_bracketed(const float* scores, int64_t batch, int64_t n, doub
     if (st == LAPSUM_OK && row + P < batch) st = launch(row + P);
     if (st != LAPSUM_OK) return st;
   }
+  return LAPSUM_OK;
+}
+
+int lapsum_bracket_noise(uint64_t seed, int64_t K, double alpha, float* out, hipStream_t stream) {
+  if (!out || K < 1 || K > 2147483647LL || !isfinite(alpha) || !(alpha < 0.0))
+    return LAPSUM_ERR_INVALID_ARG;
+  const int dst = check_device();
+  if (dst != LAPSUM_OK) return dst;
+  LAPSUM_TRY(launch_noise_table(seed, K, -alpha, out, stream));
   return LAPSUM_OK;
 }
 

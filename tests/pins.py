@@ -178,9 +178,47 @@ def check_decimal_bruteforce():
         k = float(rg.uniform(0.05, n - 0.05))
         t = float(rg.choice([0.01, 0.5, 3.0]))
         want = _decimal_b(x, k, t)
-        for f in (O.solve_bisect, O.solve_sorted_scan):
+        for f in (O.solve_bisect, O.solve_sorted_scan, O.solve_brent):
             got = f(x, k, -t)
             assert abs(got - want) <= 1e-12 * (1 + abs(want)) + 1e-13 * t, (f.__name__, got, want)
+
+
+def check_brent(seed_count=12):
+    """The library root finder on the plain sum against the two independent
+    roots: the 40-digit `decimal` bisection on tiny rows (in
+    check_decimal_bruteforce) and, here, float64 bisection of the same sum on
+    the mixed rows (ties, heavy tails, t from 1e-3 to 7), and the closed form
+    of one score (b = r - t ln(2k) for k <= 1/2, r + t ln(2(1 - k)) above)."""
+    for x, k, a in _rows(seed_count):
+        b1 = O.solve_bisect(x, k, a)
+        b2 = O.solve_brent(x, k, a)
+        assert abs(b1 - b2) <= 1e-9 * -a + 1e-12 * abs(b1), (k, a, b1, b2)
+    for r0, k, t in ((0.25, 0.3, 0.01), (-3.5, 0.7, 5.0), (7.0, 0.999, 1.0)):
+        want = r0 - t * math.log(2 * k) if k <= 0.5 else r0 + t * math.log(2 * (1 - k))
+        got = O.solve_brent(np.array([r0], np.float32), k, -t)
+        assert abs(got - want) <= 1e-12 * (1 + abs(want)), (r0, k, t, got, want)
+
+
+def check_certify_root():
+    """The sign-change certificate at roots known in closed form: true at the
+    root with a margin delta, false when the claimed root is 3 delta off on
+    either side (LapSum is strictly decreasing, so then both evaluations sit
+    on one side of k).  Roots: one score (b = r - t ln(2k)), the symmetric
+    row {x, -x} at k = n/2 (b = 0), and n equal scores c (b = c - t ln(2k/n)
+    for k <= n/2)."""
+    rg = np.random.default_rng(4)
+    x = rg.standard_normal(500).astype(np.float32)
+    cases = [
+        (np.array([0.5], np.float32), 0.2, -0.3, 0.5 - 0.3 * math.log(0.4)),
+        (np.concatenate([x, -x]), 500.0, -0.05, 0.0),
+        (np.full(64, 1.25, np.float32), 8.0, -2.0, 1.25 - 2.0 * math.log(2 * 8.0 / 64)),
+    ]
+    for r, k, a, b in cases:
+        t = -a
+        for delta in (1e-6 * t, 1e-3 * t):
+            assert O.certify_root(r, k, a, b, delta), (k, a, b, delta)
+            assert not O.certify_root(r, k, a, b + 3 * delta, delta), (k, a, b, delta, "+")
+            assert not O.certify_root(r, k, a, b - 3 * delta, delta), (k, a, b, delta, "-")
 
 
 def check_vjp_fd(configs=((2, 32, 4, -1.0), (1, 64, 8, -0.5), (2, 64, 16, -2.0)), tol=1e-8):
@@ -477,3 +515,29 @@ def check_budget_table(sizes=(1000, 10000, 100000)):
         b = O.solve_sorted_scan(x, k, -1.0)
         p32 = O.probs(x, b, -1.0).astype(np.float32)
         assert O.budget_error(p32, k) / k < 1e-5
+
+
+def check_splitmix64(rows):
+    """The generator against its published outputs (tests/golden)."""
+    for seed, want in rows:
+        assert O.splitmix64(seed, len(want)) == list(want), seed
+
+
+def check_counter_noise():
+    """The default kernel noise is Laplace(0, t): a Kolmogorov-Smirnov test
+    against scipy's Laplace distribution (a wrong scale, sign or branch
+    fails it at these sizes), its sign follows the top bit of the generator
+    output (u >= 1/2 exactly when bit 63 is set), and the draws are the
+    generator's in order (a different seed or a shifted counter gives
+    different draws)."""
+    from scipy import stats
+    for seed, t in ((0, 0.01), (7, 1.0), ((1 << 64) - 1, 0.05)):
+        x = O.counter_laplace_noise(seed, 20000, t)
+        assert x.dtype == np.float32 and x.shape == (20000,)
+        ks = stats.kstest(x.astype(np.float64), stats.laplace(loc=0.0, scale=t).cdf)
+        assert ks.pvalue > 1e-3, (seed, t, ks)
+        top = np.array([v >> 63 for v in O.splitmix64(seed, 20000)])
+        assert np.array_equal(top == 1, x >= 0), seed
+    a = O.counter_laplace_noise(3, 100, 0.5)
+    assert np.array_equal(O.counter_laplace_noise(3, 50, 0.5), a[:50])
+    assert not np.array_equal(O.counter_laplace_noise(4, 100, 0.5), a)

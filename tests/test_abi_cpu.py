@@ -105,7 +105,7 @@ def test_backward_rejects_invalid_arguments():
 
 
 @pytest.mark.parametrize("kw", [
-    dict(noise=0), dict(K=1), dict(K=1001), dict(z=0.0), dict(z=float("nan")),
+    dict(K=1), dict(K=1001), dict(z=0.0), dict(z=float("nan")),
     dict(m_capacity=0), dict(flags=2), dict(k=1000.0),
 ])
 def test_bracketed_rejects_invalid_arguments(kw):
@@ -114,9 +114,18 @@ def test_bracketed_rejects_invalid_arguments(kw):
     a = dict(noise=1, K=100, z=5.16, m_capacity=64, flags=0, k=10.0)
     a.update(kw)
     st = lib.lapsum_forward_bracketed(v(1), 1, 1000, a["k"], -1.0, a["K"], a["z"], v(a["noise"]),
-                                      v(0), a["m_capacity"], a["flags"], v(1), v(1), v(0), v(0), v(0),
-                                      0, v(0), 0, v(0))
+                                      7, v(0), a["m_capacity"], a["flags"], v(1), v(1), v(0), v(0),
+                                      v(0), 0, v(0), 0, v(0))
     assert st == 1
+
+
+def test_bracket_noise_rejects_invalid_arguments():
+    lib = L.load()
+    v = ctypes.c_void_p
+    assert lib.lapsum_bracket_noise(3, 100, -1.0, v(0), v(0)) == 1      # no output
+    assert lib.lapsum_bracket_noise(3, 0, -1.0, v(1), v(0)) == 1        # K < 1
+    assert lib.lapsum_bracket_noise(3, 100, 0.0, v(1), v(0)) == 1       # alpha not < 0
+    assert lib.lapsum_bracket_noise(3, 100, float("inf"), v(1), v(0)) == 1
 
 
 def test_bracketed_rejects_a_short_or_misaligned_band():
@@ -124,7 +133,7 @@ def test_bracketed_rejects_a_short_or_misaligned_band():
     v = ctypes.c_void_p
     need = L.lapsum_band_size(1, 1000)
     for ptr, size in ((256, need - 1), (128, need)):
-        st = lib.lapsum_forward_bracketed(v(1), 1, 1000, 10.0, -1.0, 100, 5.16, v(1), v(0), 64, 0,
+        st = lib.lapsum_forward_bracketed(v(1), 1, 1000, 10.0, -1.0, 100, 5.16, v(1), 0, v(0), 64, 0,
                                           v(1),
                                           v(1), v(0), v(0), v(ptr), size, v(0), 0, v(0))
         assert st == 1

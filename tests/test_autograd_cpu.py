@@ -43,17 +43,6 @@ def test_path_switch():
     assert A.choose_path(A.FULL_SORT_MAX_N + 1) == "bracketed"
 
 
-def test_bracket_noise_is_laplace_and_cached():
-    from scipy import stats
-    t = 0.05
-    x = A.bracket_noise(20000, t, "cpu", seed=4)
-    assert x.dtype == torch.float32 and x.shape == (20000,)
-    assert A.bracket_noise(20000, t, "cpu", seed=4) is x
-    assert not torch.equal(A.bracket_noise(20000, t, "cpu", seed=5), x)
-    ks = stats.kstest(x.double().numpy(), stats.laplace(loc=0.0, scale=t).cdf)
-    assert ks.pvalue > 1e-3, ks
-
-
 def test_no_cpu_fallback():
     x = torch.zeros(16, dtype=torch.float32)
     with pytest.raises(ValueError):

@@ -35,6 +35,9 @@ _orig_gap_root = O._gap_root
 _orig_bracket_ranks = O.bracket_ranks
 _orig_partition = O.partition
 _orig_vjp = O.vjp
+_orig_lapsum = O.lapsum
+_orig_counter_noise = O.counter_laplace_noise
+_orig_initial_bracket = O.initial_bracket
 
 
 def _bad_node_full_E(s, t, n_above, above, below):
@@ -57,6 +60,53 @@ def _bad_node_rank(s, t, n_above, above, below):
 
 def _bad_gap_sign(k, t, c_up, up, down):
     return _orig_gap_root(2.0 * c_up - k if up is not None and down is not None else k, t, c_up, up, down)
+
+
+def _bad_brent_budget(r, k, alpha):
+    from scipy.optimize import brentq
+    t = -float(alpha)
+    lo, hi = O.initial_bracket(r, k, t)
+    n = np.asarray(r).size
+    # root of LapSum(b) = n - k: the budget counted from the wrong end
+    return float(brentq(lambda b: _orig_lapsum(r, b, t) - (n - k), lo - 50 * t, hi + 50 * t,
+                        xtol=1e-14 * t))
+
+
+def _bad_brent_tolerance(r, k, alpha):
+    from scipy.optimize import brentq
+    t = -float(alpha)
+    lo, hi = O.initial_bracket(r, k, t)
+    return float(brentq(lambda b: _orig_lapsum(r, b, t) - k, lo, hi, xtol=1e-3 * t))  # loose
+
+
+def _bad_certify_swapped(r, k, alpha, b, delta):
+    t = -float(alpha)
+    return _orig_lapsum(r, b + delta, t) > k > _orig_lapsum(r, b - delta, t)   # wrong sides
+
+
+def _bad_certify_one_sided(r, k, alpha, b, delta):
+    t = -float(alpha)
+    return _orig_lapsum(r, b - delta, t) > k                  # upper side never checked
+
+
+def _bad_splitmix_shift(seed, count):
+    mask = (1 << 64) - 1
+    state, out = seed & mask, []
+    for _ in range(count):
+        state = (state + 0x9E3779B97F4A7C15) & mask
+        x = state
+        x = ((x ^ (x >> 31)) * 0xBF58476D1CE4E5B9) & mask     # 31 for 30
+        x = ((x ^ (x >> 27)) * 0x94D049BB133111EB) & mask
+        out.append(x ^ (x >> 31))
+    return out
+
+
+def _bad_noise_scale(seed, K, t):
+    return _orig_counter_noise(seed, K, 2.0 * t)              # Laplace(0, 2t)
+
+
+def _bad_noise_branch(seed, K, t):
+    return -_orig_counter_noise(seed, K, t)                   # branches swapped
 
 
 def _bad_vjp_unnormalised(r, b, alpha, g):
@@ -193,6 +243,13 @@ MUTANTS = {
     "node_E_inclusive": ("_node_curve", _bad_node_inclusive_E),
     "node_rank_off_by_one": ("_node_curve", _bad_node_rank),
     "gap_root_sign": ("_gap_root", _bad_gap_sign),
+    "brent_budget_from_wrong_end": ("solve_brent", _bad_brent_budget),
+    "brent_loose_tolerance": ("solve_brent", _bad_brent_tolerance),
+    "certify_swapped_sides": ("certify_root", _bad_certify_swapped),
+    "certify_one_sided": ("certify_root", _bad_certify_one_sided),
+    "splitmix_shift": ("splitmix64", _bad_splitmix_shift),
+    "noise_scale": ("counter_laplace_noise", _bad_noise_scale),
+    "noise_branch": ("counter_laplace_noise", _bad_noise_branch),
     "vjp_unnormalised_q": ("vjp", _bad_vjp_unnormalised),
     "vjp_scale": ("vjp", _bad_vjp_scale),
     "params_mean_sign": ("vjp_params", _bad_params_mean_sign),
@@ -217,6 +274,9 @@ CHECKS = [
     pins.check_symmetric_half_budget, pins.check_invariants,
     lambda: pins.check_bisect_matches_scan(6),
     pins.check_decimal_bruteforce,
+    lambda: pins.check_brent(4), pins.check_certify_root,
+    lambda: pins.check_splitmix64([(1234567, (6457827717110365317, 3203168211198807973))]),
+    pins.check_counter_noise,
     lambda: pins.check_vjp_fd(((1, 16, 4, -1.0),), tol=1e-8),
     pins.check_vjp_invariants,
     lambda: pins.check_params_fd(((24, 6.0, -1.0), (40, 13.5, -0.3)), tol=1e-6),

@@ -43,6 +43,14 @@ def test_decimal_bruteforce_tiny():
     pins.check_decimal_bruteforce()
 
 
+def test_brent_matches_bisection_and_closed_form():
+    pins.check_brent()
+
+
+def test_certificate_at_known_roots():
+    pins.check_certify_root()
+
+
 def _gradcheck_rows():
     rows, thr = [], None
     with open(os.path.join(GOLDEN, "gradcheck_table.txt")) as fh:
@@ -166,3 +174,24 @@ def test_dftopk_vjp_matches_finite_differences():
 
 def test_dftopk_midpoint_is_the_zero_temperature_threshold():
     pins.check_dftopk_midpoint_is_the_zero_temperature_threshold()
+
+
+def _splitmix_rows():
+    rows = []
+    with open(os.path.join(GOLDEN, "splitmix64_vectors.txt")) as fh:
+        for line in fh:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                v = [int(x) for x in line.split()]
+                rows.append((v[0], tuple(v[1:])))
+    return rows
+
+
+def test_splitmix64_published_outputs():
+    rows = _splitmix_rows()
+    assert rows and len(rows[0][1]) == 5
+    pins.check_splitmix64(rows)
+
+
+def test_counter_noise_is_laplace():
+    pins.check_counter_noise()
