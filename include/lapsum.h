@@ -93,6 +93,29 @@ int lapsum_forward(const float* scores, int64_t batch, int64_t n, double k,
                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * lapsum_forward_noalloc: lapsum_forward for callers that cannot allocate
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels and outputs, with the workspace taken from a
+ * device array of LAPSUM_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends.  The call makes no
+ * allocation (its first call on a device only looks the array's address
+ * up).  The caller still passes scores and outputs.
+ *
+ *   arguments as lapsum_forward, without workspace
+ *   LAPSUM_ERR_WORKSPACE when lapsum_forward_workspace_size(batch, n,
+ *   perm_out != NULL) exceeds LAPSUM_NOALLOC_SCRATCH_BYTES (rows of up to
+ *   32768 scores need none; one long row fits up to 3,943,808 scores with
+ *   perm_out and 7,443,456 without).
+ * All calls on one GPU share its array: calls that overlap in time on one
+ * GPU (different streams, or host threads) race and must not be issued.
+ * ------------------------------------------------------------------------ */
+#define LAPSUM_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+
+int lapsum_forward_noalloc(const float* scores, int64_t batch, int64_t n,
+                           double k, double alpha, float* p, double* b,
+                           int32_t* perm_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Backward: the analytical vector-Jacobian product of Eq. (5),
  *
  *   grad_r = f * (g - <g, q>),  q = f / sum_j f_j,

@@ -20,7 +20,8 @@ import os
 
 __all__ = [
     "load", "LapsumError", "BracketInfo", "lapsum_status_string",
-    "lapsum_forward_workspace_size", "lapsum_forward",
+    "lapsum_forward_workspace_size", "lapsum_forward", "lapsum_forward_noalloc",
+    "NOALLOC_SCRATCH_BYTES",
     "lapsum_backward_workspace_size", "lapsum_backward",
     "lapsum_forward_bracketed_workspace_size", "lapsum_forward_bracketed", "lapsum_bracket_noise",
     "LAPSUM_FLAG_FULL_SORT", "LIB_PATH", "lapsum_profile_start", "lapsum_profile_stop",
@@ -31,6 +32,7 @@ __all__ = [
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblapsum.so")
 LAPSUM_FLAG_FULL_SORT = 1
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024   # LAPSUM_NOALLOC_SCRATCH_BYTES
 
 _lib = None
 
@@ -79,6 +81,8 @@ def load():
     lib.lapsum_forward_workspace_size.restype = sz
     lib.lapsum_forward.argtypes = [vp, i64, i64, f64, f64, vp, vp, vp, vp, sz, vp]
     lib.lapsum_forward.restype = i32
+    lib.lapsum_forward_noalloc.argtypes = [vp, i64, i64, f64, f64, vp, vp, vp, vp]
+    lib.lapsum_forward_noalloc.restype = i32
     lib.lapsum_backward_workspace_size.argtypes = [i64, i64]
     lib.lapsum_backward_workspace_size.restype = sz
     lib.lapsum_backward.argtypes = [vp, vp, vp, i64, i64, f64, vp, vp, vp, vp, sz, vp]
@@ -213,6 +217,36 @@ def lapsum_forward(scores, k: float, alpha: float, *, perm: bool = False, worksp
     with _on_device(dev):
         _check(lib.lapsum_forward(_ptr(scores), batch, n, float(k), float(alpha), _ptr(p), _ptr(b),
                                   _ptr(pm), _ptr(ws), nbytes, _stream(dev)), "lapsum_forward")
+    return (p, b, pm) if perm else (p, b)
+
+
+def lapsum_forward_noalloc(scores, k: float, alpha: float, *, perm: bool = False, out=None,
+                           b_out=None, perm_out=None):
+    """lapsum_forward with the library's own device scratch (no workspace,
+    no allocation inside the call).  out / b_out / perm_out: optional
+    preallocated outputs (float32 like scores, float64 [batch], int32 like
+    scores), so that a caller under graph capture allocates nothing either.
+    Returns (p, b) or (p, b, perm)."""
+    torch = _torch()
+    lib = load()
+    batch, n = _rows(scores, "scores")
+    dev = scores.device
+    p = torch.empty_like(scores) if out is None else out
+    b = torch.empty(batch, dtype=torch.float64, device=dev) if b_out is None else b_out
+    if perm:
+        pm = torch.empty(scores.shape, dtype=torch.int32, device=dev) if perm_out is None else perm_out
+    else:
+        pm = None
+    for name, buf, dt, numel in (("out", p, torch.float32, batch * n), ("b_out", b, torch.float64, batch),
+                                 ("perm_out", pm, torch.int32, batch * n)):
+        if buf is not None and (buf.dtype != dt or buf.numel() != numel or not buf.is_contiguous()
+                                or buf.device != dev):
+            raise ValueError(f"{name} must be a contiguous {dt} tensor of {numel} elements on "
+                             f"the scores' device")
+    with _on_device(dev):
+        _check(lib.lapsum_forward_noalloc(_ptr(scores), batch, n, float(k), float(alpha), _ptr(p),
+                                          _ptr(b), _ptr(pm), _stream(dev)),
+               "lapsum_forward_noalloc")
     return (p, b, pm) if perm else (p, b)
 
 

@@ -24,7 +24,7 @@ INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 
 HIP_SOURCES = ["row_kernels.hip", "stream_kernels.hip", "sort_kernels.hip",
                "solve_kernels.hip", "bracket_kernels.hip", "band_kernels.hip", "bucket_solve.hip",
-               "comparator_kernels.hip"]
+               "comparator_kernels.hip", "noalloc.hip"]
 HOST_SOURCES = ["lapsum_api.cpp"]
 
 ARCH = "gfx950"
