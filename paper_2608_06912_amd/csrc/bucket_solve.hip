@@ -515,13 +515,194 @@ __device__ double direct_solve(const uint32_t* buf, int c, const BucketGeom& g, 
   }
   return b;   // thread 0's value
 }
+
+// Shared memory of the bucketed solve (one workgroup of ST threads).
+struct BucketSolveSmem {
+  uint32_t buf[sort_buf_words<ST, SI>()];
+  SortSmem<ST> ssm;
+  ScanSmem<SW> csm;
+  int64_t cw[SW];
+  int64_t red_i[SW];
+  Pre cpre_s;
+  Suf csuf_s;
+  int64_t cabove_s;
+  uint32_t ccount_s;
+  uint32_t gathered_s;
+  DirectSmem dsm;
+};
+
+// The scans over the buckets, the lookup of the bucket holding the root, the
+// certificate and the root, by one workgroup of ST threads.  Thread tid owns
+// buckets BPT tid .. BPT tid + BPT - 1 with their counts and the two sums
+// (U anchored at the bucket's upper edge, D at the next bucket's upper
+// edge).  Inside a thread the pairs chain through every bucket's own anchors
+// (empty buckets carry their geometric anchors and a zero sum), so the
+// in-thread folds need one exponential per bucket and no search for the
+// previous non-empty bucket; the block scans then join the threads.
+// gather(dstar, S) appends the keys of bucket dstar, relative to g.kmin, to
+// S.buf (buf_at order, one atomicAdd on S.gathered_s per key, at most
+// kBucketSortCap kept); every thread calls it.  Returns b (valid in thread
+// 0) and fills rec (ok = 0, side = 2 when the root's bucket exceeds
+// kBucketSortCap keys).
+template <class Gather>
+__device__ double bucket_core(const uint32_t (&cnt)[BPT], const double (&U)[BPT],
+                              const double (&D)[BPT], const BucketGeom& g, int64_t m,
+                              const Tails& x, double k, double t, int64_t n_total,
+                              BucketSolveSmem& S, SolveRec& rec, Gather&& gather) {
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  const double inv_t = 1.0 / t;
+  const int d0 = BPT * tid;
+  // 1. the links between consecutive anchors: the suffix sum of bucket q is
+  //    anchored at its upper edge v_q and the prefix sum at v_{q+1}, the
+  //    upper edge of the bucket after it, so both chains move between
+  //    anchors by the same links wv[q] = e^{-(v_q - v_{q+1})/t}, one
+  //    exponential per bucket (all independent)
+  float v[BPT + 1];   // v[BPT]: the upper edge of the next thread's first bucket
+#pragma unroll
+  for (int q = 0; q <= BPT; ++q) v[q] = bucket_hi(g, d0 + q);
+  double wv[BPT];
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) wv[q] = wexp_f64(static_cast<double>(v[q]) - v[q + 1], inv_t);
+  // The prefix pair may sit at any anchor at or above the root, so it
+  // chains through the geometric anchors of empty buckets.  A suffix pair
+  // is anchored at the upper edge of a non-empty bucket: the root lies above
+  // the upper edge of the first non-empty bucket after the crossing, but can
+  // lie below the edge of an empty bucket in between.
+  double Pm = 0.0;   // prefix pair of the thread, anchored at v[BPT]
+  int64_t mine = 0;
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    Pm = fma(wv[q], Pm, D[q]);
+    mine += cnt[q];
+  }
+  double Tl[BPT];    // suffix within the thread from bucket q, anchored at v[q]
+#pragma unroll
+  for (int q = BPT - 1; q >= 0; --q) Tl[q] = q + 1 < BPT ? fma(wv[q], Tl[q + 1], U[q]) : U[q];
+  Suf mys = suf_empty();   // anchored at the first non-empty bucket of the thread
+#pragma unroll
+  for (int q = BPT - 1; q >= 0; --q)
+    if (cnt[q] && Tl[q] != 0.0) mys = Suf{v[q], Tl[q]};
+
+  // 2. block scans, seeded with the tails
+  Pre pre_all;
+  Suf suf_all;
+  const Pre pre_in = block_excl_pre<SW>(Pre{v[BPT], Pm}, x.pre, inv_t, S.csm, &pre_all);
+  const Suf suf_in = block_excl_suf<SW>(mys, x.suf, inv_t, S.csm, &suf_all);
+  // the counts scan in 32 bits (fewer than 2^31 keys)
+  const int64_t incl = static_cast<int64_t>(wave_incl_add(static_cast<uint32_t>(mine)));
+  if (lane == kWave - 1) S.cw[wid] = incl;
+  __syncthreads();
+  int64_t above = incl - mine;
+#pragma unroll
+  for (int w = 0; w < SW; ++w)
+    if (w < wid) above += S.cw[w];
+
+  // 3. suffix sums from each bucket on (anchored at its v), right to left,
+  //    then LapSum at each non-empty bucket's upper edge, left to right:
+  //    LapSum(v_q) = n_R + above_q - (1/2) e^{-(a - v_q)/t} P_before + (1/2) T_q
+  //    with P_before anchored at a, which is v_q itself (weight 1) unless
+  //    the prefix still sits on the seed's anchor.  Moving P past bucket q
+  //    takes the link wv[q] in the same case.
+  double T[BPT];
+  {
+    double tn = suf_in.T;
+    float vn = suf_in.v;
+#pragma unroll
+    for (int q = BPT - 1; q >= 0; --q) {
+      const double w = (q + 1 < BPT) ? wv[q]
+                       : (tn != 0.0 ? wexp_f64(static_cast<double>(v[q]) - vn, inv_t) : 0.0);
+      T[q] = fma(w, (q + 1 < BPT) ? T[q + 1] : tn, U[q]);
+    }
+  }
+  int64_t below = 0;   // 1 + the last bucket with LapSum(v_d) <= k
+  {
+    double P = pre_in.S;   // prefix before bucket q, anchored at pu
+    float pu = pre_in.u;
+    int64_t ab = above;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q) {
+      const bool at_v = pu == v[q];
+      if (cnt[q]) {
+        double lap = x.nR + static_cast<double>(ab) + 0.5 * T[q];
+        if (P != 0.0) lap -= 0.5 * (at_v ? P : wexp_f64(static_cast<double>(pu) - v[q], inv_t) * P);
+        if (lap <= k) below = d0 + q + 1;
+      }
+      const double w = (P != 0.0) ? (at_v ? wv[q] : wexp_f64(static_cast<double>(pu) - v[q + 1], inv_t))
+                                  : 0.0;
+      P = fma(w, P, D[q]);
+      pu = v[q + 1];
+      ab += cnt[q];
+    }
+  }
+  below = static_cast<int64_t>(wave_max_u32(static_cast<uint32_t>(below)));
+  if (lane == 0) S.red_i[wid] = below;
+  if (tid == 0) S.gathered_s = 0u;
+  __syncthreads();
+  below = 0;
+#pragma unroll
+  for (int w = 0; w < SW; ++w) below = S.red_i[w] > below ? S.red_i[w] : below;
+  const int dstar = static_cast<int>(below) - 1;
+  if (dstar >= d0 && dstar < d0 + BPT) {
+    // carries around bucket d*: the prefix of everything before it and the
+    // suffix of everything after it
+    double P = pre_in.S;
+    float pu = pre_in.u;
+    int64_t ab = above;
+#pragma unroll
+    for (int q = 0; q < BPT; ++q) {
+      if (d0 + q == dstar) {
+        S.cpre_s = (P != 0.0) ? Pre{pu, P} : pre_empty();
+        Suf after = suf_in;   // from the next non-empty bucket on
+#pragma unroll
+        for (int q2 = BPT - 1; q2 > q; --q2)
+          if (cnt[q2] && T[q2] != 0.0) after = Suf{v[q2], T[q2]};
+        S.csuf_s = after;
+        S.cabove_s = ab;
+        S.ccount_s = cnt[q];
+      }
+      const double w = (P != 0.0) ? (pu == v[q] ? wv[q]
+                                                : wexp_f64(static_cast<double>(pu) - v[q + 1], inv_t))
+                                  : 0.0;
+      P = fma(w, P, D[q]);
+      pu = v[q + 1];
+      ab += cnt[q];
+    }
+  }
+  __syncthreads();
+
+  rec.ok = 1;
+  rec.side = 0;
+  rec.lap_aL = 0.0;
+  rec.lap_aR = 0.0;
+  certify(x, static_cast<double>(m), static_cast<double>(n_total), k, t, pre_all, suf_all, rec);
+  double b = 0.0;
+  if (dstar < 0) {
+    b = root_above(x, suf_all, k, t);
+  } else if (S.ccount_s > static_cast<uint32_t>(kBucketSortCap)) {
+    rec.ok = 0;
+    rec.side = 2;   // the bucket is too large to sort here
+  } else {
+    // 4. bucket d*'s keys relative to g.kmin, whose low `shift` bits order
+    //    the bucket (the order in LDS is irrelevant: it is sorted next)
+    gather(dstar, S);
+    __syncthreads();
+    const int c = static_cast<int>(S.ccount_s);
+    const double rank0 = x.nR + static_cast<double>(S.cabove_s);
+    if (c <= kDirectMax)
+      b = direct_solve(S.buf, c, g, rank0, S.cpre_s, S.csuf_s, k, t, S.dsm);
+    else if (c <= 2 * ST)
+      b = sort_and_solve<2>(S.buf, c, g, rank0, S.cpre_s, S.csuf_s, k, t, S.ssm, S.csm);
+    else
+      b = sort_and_solve<SI>(S.buf, c, g, rank0, S.cpre_s, S.csuf_s, k, t, S.ssm, S.csm);
+  }
+  return b;
+}
 }  // namespace
 
-// One workgroup.  Thread tid owns buckets BPT tid .. BPT tid + BPT - 1.
-// Inside a thread the pairs chain through every bucket's own anchors (empty
-// buckets carry their geometric anchors and a zero sum), so the in-thread
-// folds need one exponential per bucket and no search for the previous
-// non-empty bucket; the block scans then join the threads.
+// One workgroup: the middle set's buckets from the count blocks, then
+// bucket_core.
 __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __restrict__ bkeys,
                                                           const uint32_t* __restrict__ boff,
                                                           const CountPart* __restrict__ parts,
@@ -537,26 +718,15 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
                                                           AttemptRec* __restrict__ host,
                                                           uint32_t* __restrict__ host_seq,
                                                           uint32_t seq) {
-  __shared__ uint32_t buf[sort_buf_words<ST, SI>()];
-  __shared__ SortSmem<ST> ssm;
-  __shared__ ScanSmem<SW> csm;
-  __shared__ int64_t cw[SW];
-  __shared__ int64_t red_i[SW];
-  __shared__ Pre cpre_s;
-  __shared__ Suf csuf_s;
-  __shared__ int64_t cabove_s;
-  __shared__ uint32_t ccount_s;
-  __shared__ uint32_t gathered_s;
-  __shared__ DirectSmem dsm;
+  __shared__ BucketSolveSmem S;
   __shared__ PartTotals tot_s;
   __shared__ int64_t gcount_s[kPartMaxBlocks / CG];
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
-  const double inv_t = 1.0 / t;
   const int d0 = BPT * tid;
   // this thread's buckets, loaded with the partials below (they are zero
-  // when nothing was counted)
+  // when nothing was counted), and cleared behind us for the next attempt
   uint32_t cnt[BPT];
   unsigned long long Ur[BPT], Dr[BPT];
 #pragma unroll
@@ -593,6 +763,12 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
       tot_s = T;
       *tot = T;
     }
+  }
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    acc_n[d0 + q] = 0u;
+    acc_u[d0 + q] = 0ull;
+    acc_d[d0 + q] = 0ull;
   }
   __syncthreads();
   // thread 0: the record, for the emit, and with the totals for the host
@@ -634,196 +810,247 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
   }
   const BucketGeom g = geom_of(parts[0].kmin, parts[0].kmax);
   const double inv_fscale = ldexp(1.0, -fixed_bits(m));
-
-  // 1. this thread's buckets, cleared behind us for the next attempt.  The
-  //    suffix sum of bucket q is anchored at its upper edge v_q and the
-  //    prefix sum at v_{q+1}, the upper edge of the bucket after it, so both
-  //    chains move between anchors by the same links
-  //    wv[q] = e^{-(v_q - v_{q+1})/t}, one exponential per bucket.
   double U[BPT], D[BPT];
-  float v[BPT + 1];   // v[BPT]: the upper edge of the next thread's first bucket
 #pragma unroll
   for (int q = 0; q < BPT; ++q) {
     U[q] = static_cast<double>(Ur[q]) * inv_fscale;
     D[q] = static_cast<double>(Dr[q]) * inv_fscale;
-    v[q] = bucket_hi(g, d0 + q);
   }
-  v[BPT] = bucket_hi(g, d0 + BPT);
+  // bucket d* from each count block's bucket-ordered keys (a group with no
+  // members wrote no offsets); kGatherLanes threads per group, each loading
+  // its keys before placing any
+  auto gather = [&](int dstar, BucketSolveSmem& Sm) {
+    const int grp = tid / kGatherLanes;
+    const int sub = tid % kGatherLanes;
+    if (grp < ngroups && gcount_s[grp] > 0) {
+      const uint32_t* bo = boff + static_cast<int64_t>(grp) * (kBuckets + 1);
+      const uint32_t from = bo[dstar];
+      const uint32_t cnt_b = bo[dstar + 1] - from;
+      const uint32_t* bk = bkeys + static_cast<int64_t>(grp) * kGroupKeys + from;
+      for (uint32_t j0 = 0; j0 < cnt_b; j0 += kGatherLanes * kGatherBatch) {
+        uint32_t kv[kGatherBatch];
 #pragma unroll
-  for (int q = 0; q < BPT; ++q) {
-    acc_n[d0 + q] = 0u;
-    acc_u[d0 + q] = 0ull;
-    acc_d[d0 + q] = 0ull;
-  }
-  // links between consecutive anchors (all independent)
-  double wv[BPT];
+        for (int u = 0; u < kGatherBatch; ++u) {
+          const uint32_t j = j0 + static_cast<uint32_t>(u * kGatherLanes + sub);
+          kv[u] = bk[j < cnt_b ? j : 0];
+        }
 #pragma unroll
-  for (int q = 0; q < BPT; ++q) wv[q] = wexp_f64(static_cast<double>(v[q]) - v[q + 1], inv_t);
-  // The prefix pair may sit at any anchor at or above the root, so it
-  // chains through the geometric anchors of empty buckets.  A suffix pair
-  // is anchored at the upper edge of a non-empty bucket: the root lies above
-  // the upper edge of the first non-empty bucket after the crossing, but can
-  // lie below the edge of an empty bucket in between.
-  double Pm = 0.0;   // prefix pair of the thread, anchored at v[BPT]
-  int64_t mine = 0;
-#pragma unroll
-  for (int q = 0; q < BPT; ++q) {
-    Pm = fma(wv[q], Pm, D[q]);
-    mine += cnt[q];
-  }
-  double Tl[BPT];    // suffix within the thread from bucket q, anchored at v[q]
-#pragma unroll
-  for (int q = BPT - 1; q >= 0; --q) Tl[q] = q + 1 < BPT ? fma(wv[q], Tl[q + 1], U[q]) : U[q];
-  Suf mys = suf_empty();   // anchored at the first non-empty bucket of the thread
-#pragma unroll
-  for (int q = BPT - 1; q >= 0; --q)
-    if (cnt[q] && Tl[q] != 0.0) mys = Suf{v[q], Tl[q]};
-
-  // 2. block scans, seeded with the tails
-  Pre pre_all;
-  Suf suf_all;
-  const Pre pre_in = block_excl_pre<SW>(Pre{v[BPT], Pm}, x.pre, inv_t, csm, &pre_all);
-  const Suf suf_in = block_excl_suf<SW>(mys, x.suf, inv_t, csm, &suf_all);
-  // |M| < 2^31, so the counts scan in 32 bits
-  const int64_t incl = static_cast<int64_t>(wave_incl_add(static_cast<uint32_t>(mine)));
-  if (lane == kWave - 1) cw[wid] = incl;
-  __syncthreads();
-  int64_t above = incl - mine;
-#pragma unroll
-  for (int w = 0; w < SW; ++w)
-    if (w < wid) above += cw[w];
-
-  // 3. suffix sums from each bucket on (anchored at its v), right to left,
-  //    then LapSum at each non-empty bucket's upper edge, left to right:
-  //    LapSum(v_q) = n_R + above_q - (1/2) e^{-(a - v_q)/t} P_before + (1/2) T_q
-  //    with P_before anchored at a, which is v_q itself (weight 1) unless
-  //    the prefix still sits on the seed's anchor.  Moving P past bucket q
-  //    takes the link wv[q] in the same case.
-  double T[BPT];
-  {
-    double tn = suf_in.T;
-    float vn = suf_in.v;
-#pragma unroll
-    for (int q = BPT - 1; q >= 0; --q) {
-      const double w = (q + 1 < BPT) ? wv[q]
-                       : (tn != 0.0 ? wexp_f64(static_cast<double>(v[q]) - vn, inv_t) : 0.0);
-      T[q] = fma(w, (q + 1 < BPT) ? T[q + 1] : tn, U[q]);
-    }
-  }
-  int64_t below = 0;   // 1 + the last bucket with LapSum(v_d) <= k
-  {
-    double P = pre_in.S;   // prefix before bucket q, anchored at pu
-    float pu = pre_in.u;
-    int64_t ab = above;
-#pragma unroll
-    for (int q = 0; q < BPT; ++q) {
-      const bool at_v = pu == v[q];
-      if (cnt[q]) {
-        double lap = x.nR + static_cast<double>(ab) + 0.5 * T[q];
-        if (P != 0.0) lap -= 0.5 * (at_v ? P : wexp_f64(static_cast<double>(pu) - v[q], inv_t) * P);
-        if (lap <= k) below = d0 + q + 1;
-      }
-      const double w = (P != 0.0) ? (at_v ? wv[q] : wexp_f64(static_cast<double>(pu) - v[q + 1], inv_t))
-                                  : 0.0;
-      P = fma(w, P, D[q]);
-      pu = v[q + 1];
-      ab += cnt[q];
-    }
-  }
-  below = static_cast<int64_t>(wave_max_u32(static_cast<uint32_t>(below)));
-  if (lane == 0) red_i[wid] = below;
-  if (tid == 0) gathered_s = 0u;
-  __syncthreads();
-  below = 0;
-#pragma unroll
-  for (int w = 0; w < SW; ++w) below = red_i[w] > below ? red_i[w] : below;
-  const int dstar = static_cast<int>(below) - 1;
-  if (dstar >= d0 && dstar < d0 + BPT) {
-    // carries around bucket d*: the prefix of everything before it and the
-    // suffix of everything after it
-    double P = pre_in.S;
-    float pu = pre_in.u;
-    int64_t ab = above;
-#pragma unroll
-    for (int q = 0; q < BPT; ++q) {
-      if (d0 + q == dstar) {
-        cpre_s = (P != 0.0) ? Pre{pu, P} : pre_empty();
-        Suf after = suf_in;   // from the next non-empty bucket on
-#pragma unroll
-        for (int q2 = BPT - 1; q2 > q; --q2)
-          if (cnt[q2] && T[q2] != 0.0) after = Suf{v[q2], T[q2]};
-        csuf_s = after;
-        cabove_s = ab;
-        ccount_s = cnt[q];
-      }
-      const double w = (P != 0.0) ? (pu == v[q] ? wv[q]
-                                                : wexp_f64(static_cast<double>(pu) - v[q + 1], inv_t))
-                                  : 0.0;
-      P = fma(w, P, D[q]);
-      pu = v[q + 1];
-      ab += cnt[q];
-    }
-  }
-  __syncthreads();
-
-  SolveRec rec;
-  rec.ok = 1;
-  rec.side = 0;
-  rec.lap_aL = 0.0;
-  rec.lap_aR = 0.0;
-  certify(x, static_cast<double>(m), static_cast<double>(n_total), k, t, pre_all, suf_all, rec);
-  double b = 0.0;
-  if (dstar < 0) {
-    b = root_above(x, suf_all, k, t);
-  } else if (ccount_s > static_cast<uint32_t>(kBucketSortCap)) {
-    rec.ok = 0;
-    rec.side = 2;   // the bucket is too large to sort here: solve M by the full sort
-  } else {
-    // 4. gather bucket d* from each count block's bucket-ordered keys, as
-    //    keys relative to key(max M), whose low `shift` bits order the
-    //    bucket (the order in LDS is irrelevant: it is sorted next)
-    //    (a group with no members wrote no offsets)
-    //    (kGatherLanes threads per group, each loading its keys before
-    //    placing any)
-    {
-      const int grp = tid / kGatherLanes;
-      const int sub = tid % kGatherLanes;
-      if (grp < ngroups && gcount_s[grp] > 0) {
-        const uint32_t* bo = boff + static_cast<int64_t>(grp) * (kBuckets + 1);
-        const uint32_t from = bo[dstar];
-        const uint32_t cnt_b = bo[dstar + 1] - from;
-        const uint32_t* bk = bkeys + static_cast<int64_t>(grp) * kGroupKeys + from;
-        for (uint32_t j0 = 0; j0 < cnt_b; j0 += kGatherLanes * kGatherBatch) {
-          uint32_t kv[kGatherBatch];
-#pragma unroll
-          for (int u = 0; u < kGatherBatch; ++u) {
-            const uint32_t j = j0 + static_cast<uint32_t>(u * kGatherLanes + sub);
-            kv[u] = bk[j < cnt_b ? j : 0];
-          }
-#pragma unroll
-          for (int u = 0; u < kGatherBatch; ++u) {
-            if (j0 + static_cast<uint32_t>(u * kGatherLanes + sub) < cnt_b) {
-              const uint32_t at = atomicAdd(&gathered_s, 1u);
-              if (at < static_cast<uint32_t>(kBucketSortCap)) buf[buf_at(static_cast<int>(at))] = kv[u] - g.kmin;
-            }
+        for (int u = 0; u < kGatherBatch; ++u) {
+          if (j0 + static_cast<uint32_t>(u * kGatherLanes + sub) < cnt_b) {
+            const uint32_t at = atomicAdd(&Sm.gathered_s, 1u);
+            if (at < static_cast<uint32_t>(kBucketSortCap)) Sm.buf[buf_at(static_cast<int>(at))] = kv[u] - g.kmin;
           }
         }
       }
     }
-    __syncthreads();
-    const int c = static_cast<int>(ccount_s);
-    const double rank0 = x.nR + static_cast<double>(cabove_s);
-    if (c <= kDirectMax)
-      b = direct_solve(buf, c, g, rank0, cpre_s, csuf_s, k, t, dsm);
-    else if (c <= 2 * ST)
-      b = sort_and_solve<2>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
-    else
-      b = sort_and_solve<SI>(buf, c, g, rank0, cpre_s, csuf_s, k, t, ssm, csm);
-  }
+  };
+  SolveRec rec;
+  const double b = bucket_core(cnt, U, D, g, m, x, k, t, n_total, S, rec, gather);
   if (tid == 0) {
     rec.b = b;
     publish(rec);
   }
+}
+
+// ------------------------------------------------------------ bucketed rows --
+// The full-sort forward's threshold for a row of n <= kRowOnChipMax scores
+// without sorting the row (used when no permutation is asked for): one
+// workgroup per row holds the row in registers, cuts it into kBuckets
+// buckets of consecutive keys over the row's own range, sums each bucket
+// as the middle-set solve does (count, and the two exponential sums in
+// 64-bit fixed point, by LDS atomics), and runs bucket_core without tails:
+// the scans give LapSum at every bucket edge, and only the bucket holding
+// the root is sorted (or solved term by term).  The same equation is solved
+// in the same interval as by the sort, so b agrees to rounding.  p is then
+// written from the registers: the row is read once and p written once.
+// A row whose root bucket holds more than kBucketSortCap scores (many equal
+// or near-equal scores) gets b = NaN and no p; row_forward_kernel, launched
+// behind this kernel in its gated form, then solves those rows by the full
+// sort.
+//
+// Item i of thread tid is score 4 (tid + ST (i/4)) + i%4 with float4 loads
+// (VEC, n a multiple of 4), else tid + ST i.
+template <int ITEMS, bool VEC>
+__device__ __forceinline__ int row_item_index(int tid, int i) {
+  return VEC ? 4 * (tid + ST * (i / 4)) + (i % 4) : tid + ST * i;
+}
+
+template <int ITEMS, bool VEC>
+__global__ __launch_bounds__(ST) void row_bucket_forward_kernel(const float* __restrict__ scores,
+                                                                int n, double k, double t,
+                                                                float* __restrict__ p,
+                                                                double* __restrict__ b_out) {
+  static_assert(!VEC || ITEMS % 4 == 0, "float4 items");
+  __shared__ BucketSolveSmem S;
+  __shared__ uint32_t cn[kBuckets];
+  __shared__ unsigned long long cu[kBuckets];
+  __shared__ unsigned long long cd[kBuckets];
+  __shared__ uint32_t rk[2][SW];
+  __shared__ double b_s;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
+  const int64_t row = blockIdx.x;
+  const float* r = scores + row * static_cast<int64_t>(n);
+
+  // 1. the row, all loads in flight together
+  float x[ITEMS];
+  if constexpr (VEC) {
+    const float4* r4 = reinterpret_cast<const float4*>(r);
+    const int n4 = n / 4;
+#pragma unroll
+    for (int j = 0; j < ITEMS / 4; ++j) {
+      const int q = tid + ST * j;
+      const float4 v = r4[q < n4 ? q : 0];
+      x[4 * j] = v.x;
+      x[4 * j + 1] = v.y;
+      x[4 * j + 2] = v.z;
+      x[4 * j + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      const int e = tid + ST * i;
+      x[i] = r[e < n ? e : 0];
+    }
+  }
+  // 2. the range of the row's keys (the bucket geometry) and clear the
+  //    bucket sums
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    if (row_item_index<ITEMS, VEC>(tid, i) < n) {
+      const uint32_t key = desc_key(x[i]);
+      kmin = min(kmin, key);
+      kmax = max(kmax, key);
+    }
+  }
+  kmin = wave_min(kmin, 0xffffffffu);
+  kmax = wave_max(kmax, 0u);
+  if (lane == 0) {
+    rk[0][wid] = kmin;
+    rk[1][wid] = kmax;
+  }
+  for (int e = tid; e < kBuckets; e += ST) {
+    cn[e] = 0u;
+    cu[e] = 0ull;
+    cd[e] = 0ull;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < SW; ++w) {
+    kmin = min(kmin, rk[0][w]);
+    kmax = max(kmax, rk[1][w]);
+  }
+  const BucketGeom g = geom_of(kmin, kmax);
+  const double fscale = ldexp(1.0, fixed_bits(n));
+  const double c2 = kLog2e / t;
+
+  // 3. bucket counts and sums: e^{-(v_d - r)/t} anchored at the bucket's
+  //    upper edge and e^{-(r - v_{d+1})/t} at the next bucket's
+#pragma unroll
+  for (int i = 0; i < ITEMS; ++i) {
+    if (row_item_index<ITEMS, VEC>(tid, i) < n) {
+      const uint32_t key = desc_key(x[i]);
+      const int d = static_cast<int>((key - g.kmin) >> g.shift);
+      const double rv = x[i];
+      const double up = wexp_f32(static_cast<double>(bucket_hi(g, d)) - rv, c2);
+      const double dn = wexp_f32(rv - static_cast<double>(bucket_hi(g, d + 1)), c2);
+      atomicAdd(&cn[d], 1u);
+      atomicAdd(&cu[d], static_cast<unsigned long long>(__double2ull_rn(up * fscale)));
+      atomicAdd(&cd[d], static_cast<unsigned long long>(__double2ull_rn(dn * fscale)));
+    }
+  }
+  __syncthreads();
+  const int d0 = BPT * tid;
+  const double inv_fscale = ldexp(1.0, -fixed_bits(n));
+  uint32_t cnt[BPT];
+  double U[BPT], D[BPT];
+#pragma unroll
+  for (int q = 0; q < BPT; ++q) {
+    cnt[q] = cn[d0 + q];
+    U[q] = static_cast<double>(cu[d0 + q]) * inv_fscale;
+    D[q] = static_cast<double>(cd[d0 + q]) * inv_fscale;
+  }
+  // 4. scans, lookup and root; the root's bucket gathered from registers
+  auto gather = [&](int dstar, BucketSolveSmem& Sm) {
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      if (row_item_index<ITEMS, VEC>(tid, i) < n) {
+        const uint32_t rel = desc_key(x[i]) - g.kmin;
+        if (static_cast<int>(rel >> g.shift) == dstar) {
+          const uint32_t at = atomicAdd(&Sm.gathered_s, 1u);
+          if (at < static_cast<uint32_t>(kBucketSortCap)) Sm.buf[buf_at(static_cast<int>(at))] = rel;
+        }
+      }
+    }
+  };
+  const Tails tails = load_tails(nullptr);
+  SolveRec rec;
+  const double b = bucket_core(cnt, U, D, g, static_cast<int64_t>(n), tails, k, t,
+                               static_cast<int64_t>(n), S, rec, gather);
+  if (tid == 0) {
+    b_s = rec.ok ? b : NAN;
+    b_out[row] = b_s;
+  }
+  __syncthreads();
+  const double bb = b_s;
+  if (!(bb == bb)) return;   // the gated full-sort kernel solves this row
+  // 5. p from the registers
+  const double inv_t = 1.0 / t;
+  float* pr = p + row * static_cast<int64_t>(n);
+  if constexpr (VEC) {
+    float4* p4 = reinterpret_cast<float4*>(pr);
+    const int n4 = n / 4;
+#pragma unroll
+    for (int j = 0; j < ITEMS / 4; ++j) {
+      const int q = tid + ST * j;
+      if (q < n4) {
+        float4 o;
+        o.x = laplace_p(x[4 * j], bb, inv_t);
+        o.y = laplace_p(x[4 * j + 1], bb, inv_t);
+        o.z = laplace_p(x[4 * j + 2], bb, inv_t);
+        o.w = laplace_p(x[4 * j + 3], bb, inv_t);
+        p4[q] = o;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      const int e = tid + ST * i;
+      if (e < n) pr[e] = laplace_p(x[i], bb, inv_t);
+    }
+  }
+}
+
+hipError_t launch_row_bucket_forward(const float* scores, int64_t batch, int64_t n, double k,
+                                     double t, float* p, double* b, hipStream_t s) {
+  if (n < 1 || n > kRowOnChipMax || batch < 1) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(batch)), block(ST);
+  const int ni = static_cast<int>(n);
+  const bool vec = (n % 4) == 0;
+  { ProfScope ps_("row_bucket_forward", s);
+#define LAPSUM_ROWB(IT)                                                                          \
+  if (vec)                                                                                       \
+    hipLaunchKernelGGL((row_bucket_forward_kernel<IT, true>), grid, block, 0, s, scores, ni, k,  \
+                       t, p, b);                                                                 \
+  else                                                                                           \
+    hipLaunchKernelGGL((row_bucket_forward_kernel<IT, false>), grid, block, 0, s, scores, ni, k, \
+                       t, p, b)
+  if (n <= ST * 4) {
+    LAPSUM_ROWB(4);
+  } else if (n <= ST * 8) {
+    LAPSUM_ROWB(8);
+  } else if (n <= ST * 16) {
+    LAPSUM_ROWB(16);
+  } else if (n <= ST * 32) {
+    LAPSUM_ROWB(32);
+  } else {
+    LAPSUM_ROWB(64);
+  }
+#undef LAPSUM_ROWB
+  }
+  return hipGetLastError();
 }
 
 int bucket_groups(int nblocks) { return (nblocks + CG - 1) / CG; }

@@ -131,8 +131,15 @@ struct ProfScope {
 hipError_t launch_fill_u32(uint32_t* dst, int64_t count, uint32_t value, hipStream_t s);
 
 // Full-sort forward for rows with n <= kRowOnChipMax (one workgroup per row).
+// gated: only rows whose b holds NaN (left by launch_row_bucket_forward) are
+// solved; the others exit at once.
 hipError_t launch_row_forward(const float* scores, int64_t batch, int64_t n, double k, double t,
-                              float* p, double* b, int32_t* perm, hipStream_t s);
+                              float* p, double* b, int32_t* perm, bool gated, hipStream_t s);
+// The same threshold and p for rows with n <= kRowOnChipMax without sorting
+// them (bucketed solve, bucket_solve.hip); a row it cannot finish gets
+// b = NaN and no p (the gated launch_row_forward completes it).
+hipError_t launch_row_bucket_forward(const float* scores, int64_t batch, int64_t n, double k,
+                                     double t, float* p, double* b, hipStream_t s);
 // Backward for rows with n <= kRowOnChipMax; grad_k / grad_alpha ([batch]
 // float64, each may be null) receive the budget and temperature gradients.
 hipError_t launch_row_backward(const float* grad_p, const float* p, int64_t batch, int64_t n,

@@ -570,7 +570,7 @@ int bracketed_row(const float* r, int64_t n, double k, double alpha, int64_t K, 
     rec_info.fell_back = 1;
     if (n <= kRowOnChipMax) {
       // the on-chip kernel also emits p
-      LAPSUM_TRY(launch_row_forward(r, 1, n, k, t, p_row, b_row, nullptr, s));
+      LAPSUM_TRY(launch_row_forward(r, 1, n, k, t, p_row, b_row, nullptr, false, s));
     } else {
       st = full_row_solve(r, n, k, t, b_row, nullptr, w.fall, s);
       if (st != LAPSUM_OK) return st;
@@ -692,7 +692,14 @@ int lapsum_forward(const float* scores, int64_t batch, int64_t n, double k, doub
   if (dst != LAPSUM_OK) return dst;
   const double t = -alpha;
   if (forward_on_chip(batch, n)) {
-    LAPSUM_TRY(launch_row_forward(scores, batch, n, k, t, p, b, perm_out, stream));
+    if (perm_out) {
+      LAPSUM_TRY(launch_row_forward(scores, batch, n, k, t, p, b, perm_out, false, stream));
+    } else {
+      // no order wanted: the bucketed solve, then the full sort only for
+      // rows it left unsolved
+      LAPSUM_TRY(launch_row_bucket_forward(scores, batch, n, k, t, p, b, stream));
+      LAPSUM_TRY(launch_row_forward(scores, batch, n, k, t, p, b, nullptr, true, stream));
+    }
     return LAPSUM_OK;
   }
   Carve c(workspace);

@@ -17,7 +17,8 @@ __global__ __launch_bounds__(BLOCK) void row_forward_kernel(const float* __restr
                                                             int n, double k, double t,
                                                             float* __restrict__ p,
                                                             double* __restrict__ b_out,
-                                                            int32_t* __restrict__ perm) {
+                                                            int32_t* __restrict__ perm,
+                                                            int gated) {
   constexpr int WAVES = BLOCK / kWave;
   __shared__ uint32_t buf[sort_buf_words<BLOCK, ITEMS>()];
   __shared__ SortSmem<BLOCK> ssm;
@@ -28,6 +29,11 @@ __global__ __launch_bounds__(BLOCK) void row_forward_kernel(const float* __restr
   const int wid = tid / kWave;
   const int64_t row = blockIdx.x;
   const float* r = scores + row * n;
+  // gated: only the rows the bucketed forward left unsolved (b = NaN)
+  if (gated) {
+    const double b0 = b_out[row];
+    if (b0 == b0) return;
+  }
 
   uint32_t key[ITEMS];
   int32_t val[ITEMS];
@@ -83,13 +89,17 @@ __global__ __launch_bounds__(BLOCK) void row_forward_kernel(const float* __restr
 // Eq. (5) for one row; with PARAMS also the budget and temperature gradients
 // dL/dk = G/F and dL/dalpha = (H - (U/F) G)/t, from F = sum s, G = sum s g,
 // U = sum s u, H = sum s g u over s = min(p, 1 - p), u = (r - b)/t (implicit
-// differentiation of Eq. (1)); both 0 when F == 0.
-template <int BLOCK, int ITEMS, bool PARAMS>
+// differentiation of Eq. (1)); both 0 when F == 0.  p and g stay in
+// registers between the reduction and the write, so each is read once
+// (float4 accesses when n is a multiple of 4: item i of thread tid is
+// element 4 (tid + BLOCK (i/4)) + i%4, else tid + BLOCK i).
+template <int BLOCK, int ITEMS, bool PARAMS, bool VEC>
 __global__ __launch_bounds__(BLOCK) void row_backward_kernel(const float* __restrict__ g,
                                                              const float* __restrict__ p, int n,
                                                              double t, float* __restrict__ grad,
                                                              double* __restrict__ grad_k,
                                                              double* __restrict__ grad_alpha) {
+  static_assert(!VEC || ITEMS % 4 == 0, "float4 items");
   constexpr int WAVES = BLOCK / kWave;
   constexpr int NS = PARAMS ? 4 : 2;
   __shared__ double red[NS * WAVES];
@@ -97,22 +107,43 @@ __global__ __launch_bounds__(BLOCK) void row_backward_kernel(const float* __rest
   const int64_t row = blockIdx.x;
   const float* pr = p + row * n;
   const float* gr = g + row * n;
+  auto index = [&](int i) { return VEC ? 4 * (tid + BLOCK * (i / 4)) + (i % 4) : tid + BLOCK * i; };
+  float pv[ITEMS], gv[ITEMS];
+  if constexpr (VEC) {
+    const float4* p4 = reinterpret_cast<const float4*>(pr);
+    const float4* g4 = reinterpret_cast<const float4*>(gr);
+    const int n4 = n / 4;
+#pragma unroll
+    for (int j = 0; j < ITEMS / 4; ++j) {
+      const int q = tid + BLOCK * j;
+      const bool in = q < n4;
+      const float4 a = in ? p4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 c = in ? g4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+      pv[4 * j] = a.x; pv[4 * j + 1] = a.y; pv[4 * j + 2] = a.z; pv[4 * j + 3] = a.w;
+      gv[4 * j] = c.x; gv[4 * j + 1] = c.y; gv[4 * j + 2] = c.z; gv[4 * j + 3] = c.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      const int j = index(i);
+      pv[i] = j < n ? pr[j] : 0.0f;
+      gv[i] = j < n ? gr[j] : 0.0f;
+    }
+  }
   double F = 0.0, G = 0.0, U = 0.0, H = 0.0;
 #pragma unroll
   for (int i = 0; i < ITEMS; ++i) {
-    const int j = i * BLOCK + tid;
-    if (j < n) {
-      const float pp = pr[j];
-      const float f = fminf(pp, 1.0f - pp);   // e^{-|b-r|/t} / 2, exact from p
-      F += static_cast<double>(f);
+    const float pp = pv[i];
+    const float f = fminf(pp, 1.0f - pp);   // e^{-|b-r|/t} / 2, exact from p (0 past n)
+    F += static_cast<double>(f);
+    // g is not used where f == 0 (p exactly 0 or 1)
+    const double fg = f != 0.0f ? static_cast<double>(f) * static_cast<double>(gv[i]) : 0.0;
+    G += fg;
+    if constexpr (PARAMS) {
       if (f != 0.0f) {
-        const double fg = static_cast<double>(f) * static_cast<double>(gr[j]);
-        G += fg;
-        if constexpr (PARAMS) {
-          const double u = static_cast<double>(laplace_u_from_p(pp, f));
-          U += static_cast<double>(f) * u;
-          H += fg * u;
-        }
+        const double u = static_cast<double>(laplace_u_from_p(pp, f));
+        U += static_cast<double>(f) * u;
+        H += fg * u;
       }
     }
   }
@@ -139,8 +170,7 @@ __global__ __launch_bounds__(BLOCK) void row_backward_kernel(const float* __rest
     F += red[w];
     G += red[WAVES + w];
   }
-  // grad_r = (f/t) (g - <g, q>), q = f / sum f; zero when sum f == 0.  The
-  // second read of p and g hits L2 (the row is at most 256 KB).
+  // grad_r = (f/t) (g - <g, q>), q = f / sum f; zero when sum f == 0
   const double coef = (F > 0.0) ? G / F : 0.0;
   const double scale = (F > 0.0) ? 1.0 / t : 0.0;
   if constexpr (PARAMS) {
@@ -156,16 +186,28 @@ __global__ __launch_bounds__(BLOCK) void row_backward_kernel(const float* __rest
       if (grad_alpha) grad_alpha[row] = (F > 0.0) ? (H - (U / F) * G) / t : 0.0;
     }
   }
+  // the write in float32 (the sums above are float64): each output carries
+  // a few float32 roundings, far below the VJP's tolerance
+  const float coef32 = static_cast<float>(coef);
+  const float scale32 = static_cast<float>(scale);
+  auto one = [&](int i) -> float {
+    const float f = fminf(pv[i], 1.0f - pv[i]);
+    return (f != 0.0f) ? (f * scale32) * (gv[i] - coef32) : 0.0f;
+  };
   float* out = grad + row * n;
+  if constexpr (VEC) {
+    float4* o4 = reinterpret_cast<float4*>(out);
+    const int n4 = n / 4;
 #pragma unroll
-  for (int i = 0; i < ITEMS; ++i) {
-    const int j = i * BLOCK + tid;
-    if (j < n) {
-      const float pp = pr[j];
-      const float f = fminf(pp, 1.0f - pp);
-      out[j] = (f != 0.0f)
-                   ? static_cast<float>(static_cast<double>(f) * scale * (static_cast<double>(gr[j]) - coef))
-                   : 0.0f;
+    for (int j = 0; j < ITEMS / 4; ++j) {
+      const int q = tid + BLOCK * j;
+      if (q < n4) o4[q] = make_float4(one(4 * j), one(4 * j + 1), one(4 * j + 2), one(4 * j + 3));
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < ITEMS; ++i) {
+      const int j = index(i);
+      if (j < n) out[j] = one(i);
     }
   }
 }
@@ -174,43 +216,49 @@ namespace {
 
 template <int BLOCK, int ITEMS>
 hipError_t fwd_items(const float* scores, int64_t batch, int64_t n, double k, double t, float* p,
-                     double* b, int32_t* perm, hipStream_t s) {
+                     double* b, int32_t* perm, bool gated, hipStream_t s) {
+  const char* name = gated ? "row_forward_gated" : "row_forward";
   if (perm)
-    { ProfScope ps_("row_forward", s);
+    { ProfScope ps_(name, s);
     hipLaunchKernelGGL((row_forward_kernel<BLOCK, ITEMS, true>), dim3(batch), dim3(BLOCK), 0, s,
-                       scores, static_cast<int>(n), k, t, p, b, perm); }
+                       scores, static_cast<int>(n), k, t, p, b, perm, gated ? 1 : 0); }
   else
-    { ProfScope ps_("row_forward", s);
+    { ProfScope ps_(name, s);
     hipLaunchKernelGGL((row_forward_kernel<BLOCK, ITEMS, false>), dim3(batch), dim3(BLOCK), 0, s,
-                       scores, static_cast<int>(n), k, t, p, b, perm); }
+                       scores, static_cast<int>(n), k, t, p, b, perm, gated ? 1 : 0); }
   return hipGetLastError();
 }
 
 template <int BLOCK, int ITEMS>
 hipError_t bwd_items(const float* g, const float* p, int64_t batch, int64_t n, double t,
                      float* grad, double* grad_k, double* grad_alpha, hipStream_t s) {
+  const bool vec = (n % 4) == 0 && ITEMS % 4 == 0;
   { ProfScope ps_("row_backward", s);
-  if (grad_k || grad_alpha)
-    hipLaunchKernelGGL((row_backward_kernel<BLOCK, ITEMS, true>), dim3(batch), dim3(BLOCK), 0, s,
-                       g, p, static_cast<int>(n), t, grad, grad_k, grad_alpha);
-  else
-    hipLaunchKernelGGL((row_backward_kernel<BLOCK, ITEMS, false>), dim3(batch), dim3(BLOCK), 0, s,
-                       g, p, static_cast<int>(n), t, grad, grad_k, grad_alpha); }
+#define LAPSUM_ROWBWD(P, V)                                                                      \
+  hipLaunchKernelGGL((row_backward_kernel<BLOCK, ITEMS, P, V>), dim3(batch), dim3(BLOCK), 0, s, g, \
+                     p, static_cast<int>(n), t, grad, grad_k, grad_alpha)
+  if (grad_k || grad_alpha) {
+    if (vec) LAPSUM_ROWBWD(true, ITEMS % 4 == 0); else LAPSUM_ROWBWD(true, false);
+  } else {
+    if (vec) LAPSUM_ROWBWD(false, ITEMS % 4 == 0); else LAPSUM_ROWBWD(false, false);
+  }
+#undef LAPSUM_ROWBWD
+  }
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_row_forward(const float* scores, int64_t batch, int64_t n, double k, double t,
-                              float* p, double* b, int32_t* perm, hipStream_t s) {
-  if (n <= 256) return fwd_items<256, 1>(scores, batch, n, k, t, p, b, perm, s);
-  if (n <= 512) return fwd_items<256, 2>(scores, batch, n, k, t, p, b, perm, s);
-  if (n <= 1024) return fwd_items<256, 4>(scores, batch, n, k, t, p, b, perm, s);
-  if (n <= 2048) return fwd_items<256, 8>(scores, batch, n, k, t, p, b, perm, s);
-  if (n <= 4096) return fwd_items<1024, 4>(scores, batch, n, k, t, p, b, perm, s);
-  if (n <= 8192) return fwd_items<1024, 8>(scores, batch, n, k, t, p, b, perm, s);
-  if (n <= 16384) return fwd_items<1024, 16>(scores, batch, n, k, t, p, b, perm, s);
-  if (n <= kRowOnChipMax) return fwd_items<1024, 32>(scores, batch, n, k, t, p, b, perm, s);
+                              float* p, double* b, int32_t* perm, bool gated, hipStream_t s) {
+  if (n <= 256) return fwd_items<256, 1>(scores, batch, n, k, t, p, b, perm, gated, s);
+  if (n <= 512) return fwd_items<256, 2>(scores, batch, n, k, t, p, b, perm, gated, s);
+  if (n <= 1024) return fwd_items<256, 4>(scores, batch, n, k, t, p, b, perm, gated, s);
+  if (n <= 2048) return fwd_items<256, 8>(scores, batch, n, k, t, p, b, perm, gated, s);
+  if (n <= 4096) return fwd_items<1024, 4>(scores, batch, n, k, t, p, b, perm, gated, s);
+  if (n <= 8192) return fwd_items<1024, 8>(scores, batch, n, k, t, p, b, perm, gated, s);
+  if (n <= 16384) return fwd_items<1024, 16>(scores, batch, n, k, t, p, b, perm, gated, s);
+  if (n <= kRowOnChipMax) return fwd_items<1024, 32>(scores, batch, n, k, t, p, b, perm, gated, s);
   return hipErrorInvalidValue;
 }
 

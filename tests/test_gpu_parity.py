@@ -114,6 +114,47 @@ def test_row_forward_matches_oracle(lib, n, dist, k, alpha):
     assert np.array_equal(_np(perm), O.desc_order(r)), "permutation"
 
 
+@pytest.mark.parametrize("n,dist,k,alpha", ROW_CASES)
+def test_row_bucketed_forward_matches_oracle(lib, n, dist, k, alpha):
+    """Without a permutation the on-chip rows are solved by buckets (only
+    the bucket holding the root is sorted); rows whose root bucket is too
+    large for that (the constant row) go to the full sort behind it."""
+    r = W.random_case(n, n, dist=dist, ties=0.05, batch=3)
+    p, b = lib.lapsum_forward(_t(r), k, alpha)
+    p, b = _np(p), _np(b)
+    for row in range(3):
+        check_row(r[row], k, alpha, p[row], float(b[row]), f"n={n} {dist} row {row}")
+
+
+def test_row_bucketed_batch_mixing_both_solves(lib):
+    """A batch whose rows alternate between the bucketed solve and the full
+    sort (constant rows and rows of four values fill a bucket past its
+    sort capacity)."""
+    n = 32768
+    rng = np.random.default_rng(31)
+    r = rng.standard_normal((6, n)).astype(np.float32)
+    r[1] = np.float32(0.75)
+    r[3] = rng.choice(np.array([-1.0, 0.0, 0.5, 2.0], np.float32), n)
+    r[5, : n // 2] = np.float32(1.5)
+    k, alpha = 300.0, -0.05
+    p, b = lib.lapsum_forward(_t(r), k, alpha)
+    p, b = _np(p), _np(b)
+    for row in range(6):
+        check_row(r[row], k, alpha, p[row], float(b[row]), f"row {row}")
+
+
+def test_row_bucketed_workloads(lib):
+    """single4k and all 256 rows of batch256 (the benchmark's forward) by
+    the bucketed solve."""
+    for name in ("single4k", "batch256"):
+        w = W.get(name)
+        r = W.scores(name)
+        p, b = lib.lapsum_forward(_t(r), w.k, w.alpha)
+        p, b = _np(p), _np(b)
+        for row in range(w.batch):
+            check_row(r[row], w.k, w.alpha, p[row], float(b[row]), f"{name} row {row}")
+
+
 def test_row_forward_single4k(lib):
     w = W.get("single4k")
     r = W.scores("single4k")
