@@ -256,6 +256,166 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
   }
 }
 
+// The same as solve_finalize_kernel for up to kFinPer * FT tiles, by FT =
+// 512 threads with each thread's run of at most kFinPer tiles in registers:
+// all tile records are loaded at once, every exponential (the links between
+// the run's anchors and the node terms) is formed independently, and the
+// chains along a run are fused multiply-adds only.  The crossing tile is
+// solved by block_solve with 512 threads of 8 keys.
+constexpr int FT = 512;
+constexpr int FW = FT / kWave;
+constexpr int kFinPer = 8;
+constexpr int FTI = static_cast<int>(TILE / FT);   // 8 keys per thread in the crossing tile
+
+__global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, double* b_out) {
+  __shared__ ScanSmem<FW> sm;
+  __shared__ int64_t cnt_s[FW];
+  __shared__ Pre tile_pre_s;
+  __shared__ Suf tile_suf_s;
+  const int tid = threadIdx.x;
+  const double t = a.t;
+  const double inv_t = 1.0 / t;
+  const double k = a.k;
+  const int64_t m = eff_len(a.len, a.len_dev);
+  const int64_t ntiles = (m + TILE - 1) / TILE;
+  const Tails x = load_tails(a.tails);
+  const double* tb = a.tile_buf;
+
+  // 1. this thread's run of tiles [t0, t0 + nr)
+  const int64_t per = (ntiles + FT - 1) / FT;   // <= kFinPer (checked by the launcher)
+  const int64_t t0 = static_cast<int64_t>(tid) * per;
+  int nr = static_cast<int>(ntiles - t0 < per ? ntiles - t0 : per);
+  nr = nr < 0 ? 0 : nr;
+  double S[kFinPer], X[kFinPer];
+  float fst[kFinPer], lst[kFinPer];
+#pragma unroll
+  for (int q = 0; q < kFinPer; ++q) {
+    const double* r = tb + (t0 + (q < nr ? q : 0)) * kTileRec;
+    const bool on = q < nr;
+    S[q] = on ? r[0] : 0.0;
+    X[q] = on ? r[1] : 0.0;
+    fst[q] = on ? static_cast<float>(r[2]) : 0.0f;
+    lst[q] = on ? static_cast<float>(r[3]) : 0.0f;
+  }
+  // links between the run's anchors: prefix pairs move from last_{q-1} to
+  // last_q, suffix pairs from first_{q+1} to first_q
+  double wp[kFinPer], ws[kFinPer];
+#pragma unroll
+  for (int q = 0; q < kFinPer; ++q) {
+    wp[q] = (q >= 1 && q < nr) ? wexp_f64(static_cast<double>(lst[q - 1]) - lst[q], inv_t) : 0.0;
+    ws[q] = (q + 1 < nr) ? wexp_f64(static_cast<double>(fst[q]) - fst[q + 1], inv_t) : 0.0;
+  }
+  // a tile's prefix sum anchored at its last score is S (>= 1), its suffix
+  // sum anchored at its first score 1 + X: no tile is empty
+  double Pm = 0.0, Tm = 0.0;
+#pragma unroll
+  for (int q = 0; q < kFinPer; ++q)
+    if (q < nr) Pm = fma(wp[q], Pm, S[q]);
+#pragma unroll
+  for (int q = kFinPer - 1; q >= 0; --q)
+    if (q < nr) Tm = fma(ws[q], Tm, 1.0 + X[q]);
+  const Pre mp = nr > 0 ? Pre{lst[nr - 1 < 0 ? 0 : nr - 1], Pm} : pre_empty();
+  const Suf ms = nr > 0 ? Suf{fst[0], Tm} : suf_empty();
+  Pre pre_all;
+  Suf suf_all;
+  const Pre pre_in = block_excl_pre<FW>(mp, x.pre, inv_t, sm, &pre_all);
+  const Suf suf_in = block_excl_suf<FW>(ms, x.suf, inv_t, sm, &suf_all);
+
+  // 2. the prefix before each tile (anchored at the previous tile's last
+  //    score, or the carry's anchor) and the suffix after it (anchored at
+  //    the next tile's first score, or the carry's), then the node value at
+  //    each tile's first score
+  const double pin_w = (nr > 0 && pre_in.S != 0.0)
+                           ? wexp_f64(static_cast<double>(pre_in.u) - lst[0], inv_t) * pre_in.S : 0.0;
+  double sin_w = 0.0;   // suffix after the run moved to the run's last tile's first score
+#pragma unroll
+  for (int q = 0; q < kFinPer; ++q)
+    if (q == nr - 1 && suf_in.T != 0.0)
+      sin_w = wexp_f64(static_cast<double>(fst[q]) - suf_in.v, inv_t) * suf_in.T;
+  Pre bef[kFinPer];
+  Suf aft[kFinPer];
+  {
+    Pre cur = pre_in;
+    double run = 0.0;   // prefix through tile q, anchored at lst[q]
+#pragma unroll
+    for (int q = 0; q < kFinPer; ++q) {
+      if (q < nr) {
+        bef[q] = cur;
+        run = (q == 0) ? S[0] + pin_w : fma(wp[q], run, S[q]);
+        cur = Pre{lst[q], run};
+      }
+    }
+  }
+  {
+    Suf cur = suf_in;
+    double run = 0.0;   // suffix from tile q on, anchored at fst[q]
+#pragma unroll
+    for (int q = kFinPer - 1; q >= 0; --q) {
+      if (q < nr) {
+        aft[q] = cur;
+        run = (q == nr - 1) ? (1.0 + X[q]) + sin_w : fma(ws[q], run, 1.0 + X[q]);
+        cur = Suf{fst[q], run};
+      }
+    }
+  }
+  int64_t below = 0;
+#pragma unroll
+  for (int q = 0; q < kFinPer; ++q) {
+    if (q < nr) {
+      double P = 1.0;
+      if (bef[q].S != 0.0) P += wexp_f64(static_cast<double>(bef[q].u) - fst[q], inv_t) * bef[q].S;
+      double E = X[q];
+      if (aft[q].T != 0.0) E += wexp_f64(static_cast<double>(fst[q]) - aft[q].v, inv_t) * aft[q].T;
+      const double N = x.nR + static_cast<double>((t0 + q) * TILE) + 1.0 - 0.5 * P + 0.5 * E;
+      if (N <= k) below = t0 + q + 1;   // non-decreasing: the last such tile
+    }
+  }
+  below = block_max_i64<FW>(below, cnt_s);
+  if (below > 0 && below - 1 >= t0 && below - 1 < t0 + nr) {
+#pragma unroll
+    for (int q = 0; q < kFinPer; ++q) {
+      if (t0 + q == below - 1) {
+        tile_pre_s = bef[q];
+        tile_suf_s = aft[q];
+      }
+    }
+  }
+  __syncthreads();
+
+  SolveRec rec;
+  rec.ok = 1;
+  rec.side = 0;
+  rec.lap_aL = 0.0;
+  rec.lap_aR = 0.0;
+  if (x.bracketed)
+    certify(x, static_cast<double>(m), static_cast<double>(a.n_total), k, t, pre_all, suf_all, rec);
+
+  double b;
+  if (m == 0 || below == 0) {
+    b = root_above(x, suf_all, k, t);
+  } else {
+    const int64_t ct = below - 1;
+    const Pre tp = tile_pre_s;
+    const Suf ts = tile_suf_s;
+    const int64_t base = ct * TILE;
+    const int64_t nv = (m - base) < TILE ? (m - base) : TILE;
+    float sv[FTI];
+    int cnt = static_cast<int>(nv - static_cast<int64_t>(tid) * FTI);
+    cnt = cnt < 0 ? 0 : (cnt > FTI ? FTI : cnt);
+#pragma unroll
+    for (int i = 0; i < FTI; ++i)
+      sv[i] = (i < cnt) ? key_float(a.keys[base + static_cast<int64_t>(tid) * FTI + i]) : 0.0f;
+    Pre pt;
+    Suf st;
+    b = block_solve<FT, FTI>(sv, cnt, x.nR + static_cast<double>(base), tp, ts, k, t, sm, &pt, &st);
+  }
+  if (tid == 0) {
+    rec.b = b;
+    *a.out = rec;
+    if (b_out) *b_out = b;
+  }
+}
+
 hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s) {
   const int64_t tiles = (a.len + TILE - 1) / TILE;
   if (tiles > a.max_tiles) return hipErrorInvalidValue;
@@ -263,8 +423,13 @@ hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s) {
     { ProfScope ps_("solve_tiles", s);
     hipLaunchKernelGGL(solve_tiles_kernel, dim3(static_cast<unsigned>(tiles)), dim3(TT), 0, s,
                        a.keys, a.len, a.len_dev, a.t, a.tile_buf); }
-  { ProfScope ps_("solve_finalize", s);
-  hipLaunchKernelGGL(solve_finalize_kernel, dim3(1), dim3(TT), 0, s, a, a.b_out); }
+  if (tiles > TT && tiles <= static_cast<int64_t>(kFinPer) * FT) {
+    { ProfScope ps_("solve_finalize", s);
+    hipLaunchKernelGGL(solve_finalize_wide_kernel, dim3(1), dim3(FT), 0, s, a, a.b_out); }
+  } else {
+    { ProfScope ps_("solve_finalize", s);
+    hipLaunchKernelGGL(solve_finalize_kernel, dim3(1), dim3(TT), 0, s, a, a.b_out); }
+  }
   return hipGetLastError();
 }
 
