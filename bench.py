@@ -50,7 +50,7 @@ HBM_PEAK_GBS = 8000.0
 
 # Measured HBM traffic per launch (bytes) at n = 1e8: rocprofv3 FETCH_SIZE and
 # WRITE_SIZE passes over this script with --copy-probe, scaled by what the same
-# counters read for a 4e8-byte device copy (FETCH_SIZE x 1.99981, WRITE_SIZE
+# counters read for a 4e8-byte device copy (FETCH_SIZE x 1.99987, WRITE_SIZE
 # x 1.0).  Each entry holds the SHA-1 of the kernel's source file at the time of
 # measurement; once that file changes the figure no longer describes the
 # kernel and is reported as null.
@@ -58,7 +58,7 @@ MEASURED_TRAFFIC = {
     "band_emit": ("band_kernels.hip", "971a0862c0f5a91fea8077dbc5e75929152da532", 427.2e6),
     "band_vjp_emit": ("band_kernels.hip", "971a0862c0f5a91fea8077dbc5e75929152da532", 443.6e6),
     "band_vjp_reduce": ("band_kernels.hip", "971a0862c0f5a91fea8077dbc5e75929152da532", 61.3e6),
-    "partition": ("bracket_kernels.hip", "2efa96ac60bad2d48f9ed8e80819e8f7556f19d3", 413.8e6),
+    "partition": ("bracket_kernels.hip", "2d4849e3a043cdb571200d39658c4d4087386a01", 413.9e6),
 }
 METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
 # The paper's dispatched forward times in its headline setting (abstract,
