@@ -864,9 +864,9 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
 // in the same interval as by the sort, so b agrees to rounding.  p is then
 // written from the registers: the row is read once and p written once.
 // A row whose root bucket holds more than kBucketSortCap scores (many equal
-// or near-equal scores) gets b = NaN and no p; row_forward_kernel, launched
-// behind this kernel in its gated form, then solves those rows by the full
-// sort.
+// or near-equal scores; only a row longer than that can) gets b = NaN and no
+// p; row_forward_kernel, launched behind this kernel in its gated form for
+// such row lengths, then solves those rows by the full sort.
 //
 // Item i of thread tid is score 4 (tid + ST (i/4)) + i%4 with float4 loads
 // (VEC, n a multiple of 4), else tid + ST i.

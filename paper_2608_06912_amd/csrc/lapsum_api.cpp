@@ -696,9 +696,12 @@ int lapsum_forward(const float* scores, int64_t batch, int64_t n, double k, doub
       LAPSUM_TRY(launch_row_forward(scores, batch, n, k, t, p, b, perm_out, false, stream));
     } else {
       // no order wanted: the bucketed solve, then the full sort only for
-      // rows it left unsolved
+      // rows it left unsolved.  It leaves a row only when the root's bucket
+      // holds more than kBucketSortCap scores, which a shorter row cannot
+      // have, so short rows need no second launch.
       LAPSUM_TRY(launch_row_bucket_forward(scores, batch, n, k, t, p, b, stream));
-      LAPSUM_TRY(launch_row_forward(scores, batch, n, k, t, p, b, nullptr, true, stream));
+      if (n > kBucketSortCap)
+        LAPSUM_TRY(launch_row_forward(scores, batch, n, k, t, p, b, nullptr, true, stream));
     }
     return LAPSUM_OK;
   }

@@ -143,6 +143,24 @@ def test_row_bucketed_batch_mixing_both_solves(lib):
         check_row(r[row], k, alpha, p[row], float(b[row]), f"row {row}")
 
 
+@pytest.mark.parametrize("n", [4000, 4096, 4097])
+def test_row_bucketed_root_bucket_at_the_sort_capacity(lib, n):
+    """Rows of one repeated value put every score into the root's bucket.
+    Up to 4096 scores (the on-chip sort capacity of the bucketed solve) the
+    bucketed kernel finishes such a row by itself, and no completion launch
+    follows for rows that short; at 4097 the gated full sort finishes it."""
+    rng = np.random.default_rng(n)
+    r = np.full((3, n), np.float32(0.3), np.float32)
+    r[1, ::3] = np.float32(-1.25)
+    r[2] = rng.standard_normal(n).astype(np.float32)
+    k, alpha = n / 5.0, -0.2
+    p, b = lib.lapsum_forward(_t(r), k, alpha)
+    p, b = _np(p), _np(b)
+    for row in range(3):
+        assert np.isfinite(b[row]), f"row {row} left unsolved"
+        check_row(r[row], k, alpha, p[row], float(b[row]), f"n {n} row {row}")
+
+
 def test_row_bucketed_workloads(lib):
     """single4k and all 256 rows of batch256 (the benchmark's forward) by
     the bucketed solve."""
