@@ -101,119 +101,146 @@ hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t,
 }
 
 // ------------------------------------------------------------ vjp reduce ---
+// Wave tiles of 256 float4 (1024 scores); wave w of the grid's G waves takes
+// tiles w, w + G, w + 2G, ..., so that the waves of the chip read
+// neighbouring tiles at any time, and the grid is at most kVjpBlocks
+// workgroups (about one round of resident ones) so that each wave streams
+// many tiles.  (Each workgroup streaming its own contiguous range read the
+// 400 MB of p at n = 1e8 at 3.6 TB/s.)
+constexpr int kVjpBlocks = 1280;
+
 int vjp_reduce_blocks(int64_t n) {
-  const int64_t b = (n + kStreamTile - 1) / kStreamTile;
-  return static_cast<int>(b < 1 ? 1 : (b > 4096 ? 4096 : b));
+  const int64_t tiles = n / 1024;   // whole wave tiles
+  int64_t b = (tiles + 3) / 4;
+  return static_cast<int>(b < 1 ? 1 : (b > kVjpBlocks ? kVjpBlocks : b));
 }
 
-// Block b sums f = min(p, 1-p) and f g over a contiguous range of float4s,
-// four per lane in flight; g is read only for float4s with some f != 0.
-// float32 within a float4, float64 across, then a fixed-order block
-// reduction (DPP within a wave, waves in order).  With PARAMS also sum s u
-// and sum s g u, u recovered from p.
+// Sums of f = min(p, 1-p) and f g over the row, g read only for float4s with
+// some f != 0: float32 within a float4, float64 across, then a fixed-order
+// block reduction (DPP within a wave, waves in order) to partials[block].
+// With PARAMS also sum s u and sum s g u, u recovered from p.
+//
+// Software pipeline per wave, one tile per step: step s issues the p loads
+// of tile s + 2 into the buffer tile s - 1 freed, then the g loads tile s
+// needs, then adds tile s; so the next two p tiles are in flight while a
+// tile's g is read, and no loaded register is copied (three p buffers rotate
+// through an unrolled period of three).  Loads past a wave's last tile read
+// one line of its first tile instead; a lane that needs no g reads one line
+// of it too.  The float4s past the whole tiles and the scalar tail go to the
+// last workgroup.
 template <bool PARAMS>
-__global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float* __restrict__ g,
+__global__ __launch_bounds__(kStreamThreads, 4) void vjp_reduce_kernel(const float* __restrict__ g,
                                                                     const float* __restrict__ p,
                                                                     int64_t n,
                                                                     double* __restrict__ partials) {
   constexpr int NS = PARAMS ? 4 : 2;
-  __shared__ double red[NS][kStreamThreads / kWave];
+  constexpr int W = kStreamThreads / kWave;
+  __shared__ double red[NS][W];
   const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = tid / kWave;
   const bool vec = ((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(p)) & 15) == 0;
-  const int64_t n4 = vec ? n / 4 : 0;
-  const int64_t per = (n4 + gridDim.x - 1) / gridDim.x;
-  const int64_t lo = static_cast<int64_t>(blockIdx.x) * per;
-  const int64_t hi = (lo + per < n4) ? lo + per : n4;
   const float4* p4 = reinterpret_cast<const float4*>(p);
   const float4* g4 = reinterpret_cast<const float4*>(g);
   double F = 0.0, G = 0.0, Us = 0.0, H = 0.0;
-  // sum s u and sum s g u of four scores (float32; s == 0 terms skipped)
-  auto su4 = [&](const float4& pv, const float (&f)[4], const float4& gv) {
-    const float pw[4] = {pv.x, pv.y, pv.z, pv.w};
-    const float gw[4] = {gv.x, gv.y, gv.z, gv.w};
-    float a = 0.0f, c = 0.0f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float fu = f[q] != 0.0f ? f[q] * laplace_u_from_p(pw[q], f[q]) : 0.0f;
-      a += fu;
-      c += fu * gw[q];
-    }
-    Us += static_cast<double>(a);
-    H += static_cast<double>(c);
-  };
-  constexpr int U = 4;   // float4 of p per lane per batch, two batches in flight
-  int64_t i = lo + tid;
-  auto batch = [&](const float4 (&pv)[U], int64_t at) {
-    float f[U][4];
-    bool need[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      f[u][0] = fminf(pv[u].x, 1.0f - pv[u].x);
-      f[u][1] = fminf(pv[u].y, 1.0f - pv[u].y);
-      f[u][2] = fminf(pv[u].z, 1.0f - pv[u].z);
-      f[u][3] = fminf(pv[u].w, 1.0f - pv[u].w);
-      need[u] = ((f[u][0] + f[u][1]) + (f[u][2] + f[u][3])) != 0.0f;
-    }
-    float4 gv[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      gv[u] = need[u] ? g4[at + u * kStreamThreads] : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (need[u]) {
-        F += static_cast<double>((f[u][0] + f[u][1]) + (f[u][2] + f[u][3]));
-        G += static_cast<double>((f[u][0] * gv[u].x + f[u][1] * gv[u].y) +
-                                 (f[u][2] * gv[u].z + f[u][3] * gv[u].w));
-        if constexpr (PARAMS) su4(pv[u], f[u], gv[u]);
-      }
-    }
-  };
-  if (i + (U - 1) * kStreamThreads < hi) {
-    float4 pv[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) pv[u] = p4[i + u * kStreamThreads];
-    while (true) {
-      const int64_t cur = i;
-      i += U * kStreamThreads;
-      const bool more = i + (U - 1) * kStreamThreads < hi;
-      float4 pn[U];
-      if (more) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) pn[u] = p4[i + u * kStreamThreads];
-      }
-      batch(pv, cur);
-      if (!more) break;
-#pragma unroll
-      for (int u = 0; u < U; ++u) pv[u] = pn[u];
-    }
-  }
-  for (; i < hi; i += kStreamThreads) {
-    const float4 pv = p4[i];
+  // one float4 of p with its g (g meaningful only where some f != 0).  No
+  // contraction into fused multiply-adds, so that both instances (with and
+  // without the parameter sums) round the same sums the same way.
+  auto add4 = [&](const float4& pv, const float4& gv) {
+#pragma clang fp contract(off)
     const float f[4] = {fminf(pv.x, 1.0f - pv.x), fminf(pv.y, 1.0f - pv.y),
                         fminf(pv.z, 1.0f - pv.z), fminf(pv.w, 1.0f - pv.w)};
     const float fs = (f[0] + f[1]) + (f[2] + f[3]);
     if (fs != 0.0f) {
-      const float4 gq = g4[i];
       F += static_cast<double>(fs);
-      G += static_cast<double>((f[0] * gq.x + f[1] * gq.y) + (f[2] * gq.z + f[3] * gq.w));
-      if constexpr (PARAMS) su4(pv, f, gq);
-    }
-  }
-  if (blockIdx.x == gridDim.x - 1) {   // scalar tail (all of it when unaligned)
-    for (int64_t j = n4 * 4 + tid; j < n; j += kStreamThreads) {
-      const float pp = p[j];
-      const float f1 = fminf(pp, 1.0f - pp);
-      if (f1 != 0.0f) {
-        const double gj = static_cast<double>(g[j]);
-        F += static_cast<double>(f1);
-        G += static_cast<double>(f1) * gj;
-        if constexpr (PARAMS) {
-          const double fu = static_cast<double>(f1) * static_cast<double>(laplace_u_from_p(pp, f1));
-          Us += fu;
-          H += fu * gj;
+      G += static_cast<double>((f[0] * gv.x + f[1] * gv.y) + (f[2] * gv.z + f[3] * gv.w));
+      if constexpr (PARAMS) {
+        const float pw[4] = {pv.x, pv.y, pv.z, pv.w};
+        const float gw[4] = {gv.x, gv.y, gv.z, gv.w};
+        float a = 0.0f, c = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float fu = f[q] != 0.0f ? f[q] * laplace_u_from_p(pw[q], f[q]) : 0.0f;
+          a += fu;
+          c += fu * gw[q];
         }
+        Us += static_cast<double>(a);
+        H += static_cast<double>(c);
       }
     }
+  };
+  auto add1 = [&](float pp, float gg) {
+#pragma clang fp contract(off)
+    const float f1 = fminf(pp, 1.0f - pp);
+    if (f1 != 0.0f) {
+      const double gj = static_cast<double>(gg);
+      F += static_cast<double>(f1);
+      G += static_cast<double>(f1) * gj;
+      if constexpr (PARAMS) {
+        const double fu = static_cast<double>(f1) * static_cast<double>(laplace_u_from_p(pp, f1));
+        Us += fu;
+        H += fu * gj;
+      }
+    }
+  };
+
+  if (vec) {
+    const int64_t n4 = n / 4;
+    const int64_t nt = n / 1024;   // whole wave tiles
+    const int64_t GW = static_cast<int64_t>(gridDim.x) * W;
+    const int64_t w0 = static_cast<int64_t>(blockIdx.x) * W + wid;
+    const int cnt = w0 < nt ? static_cast<int>((nt - w0 + GW - 1) / GW) : 0;
+    if (cnt > 0) {
+      const float4* pd = p4 + w0 * 256;   // the line loads past the end read
+      const float4* gd = g4 + w0 * 256;
+      auto base_of = [&](int j) { return (w0 + static_cast<int64_t>(j) * GW) * 256 + lane; };
+      auto load_p = [&](float4 (&q)[4], int j) {
+        const bool real = j < cnt;
+        const int64_t b = base_of(j);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) q[u] = load_stream4(reinterpret_cast<const float*>(real ? p4 + b + 64 * u : pd));
+      };
+      // tile s: its p loaded, the p of tiles s + 1 and s + 2 issued, then
+      // its g (issued after them, so waiting for g waits for tile s + 1's p
+      // as well, which the next step needs anyway; tile s + 2 stays in
+      // flight), then the sums
+      auto step = [&](const float4 (&pc)[4], float4 (&pn2)[4], int st) {
+        load_p(pn2, st + 2);
+        const int64_t b = base_of(st);
+        float4 gq[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const bool need = (fminf(pc[u].x, 1.0f - pc[u].x) + fminf(pc[u].y, 1.0f - pc[u].y)) +
+                                (fminf(pc[u].z, 1.0f - pc[u].z) + fminf(pc[u].w, 1.0f - pc[u].w)) != 0.0f;
+          gq[u] = *(need ? g4 + b + 64 * u : gd);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) add4(pc[u], gq[u]);
+      };
+      float4 P0[4], P1[4], P2[4];   // tile s sits in P[s % 3]
+      load_p(P0, 0);
+      load_p(P1, 1);
+      for (int s0 = 0;; s0 += 3) {
+        step(P0, P2, s0);
+        if (s0 + 1 >= cnt) break;
+        step(P1, P0, s0 + 1);
+        if (s0 + 2 >= cnt) break;
+        step(P2, P1, s0 + 2);
+        if (s0 + 3 >= cnt) break;
+      }
+    }
+    if (blockIdx.x == gridDim.x - 1) {
+      // the float4s past the whole tiles, then the scalars past them
+      for (int64_t i = nt * 256 + tid; i < n4; i += kStreamThreads) {
+        const float4 pv = p4[i];
+        add4(pv, g4[i]);
+      }
+      for (int64_t j = n4 * 4 + tid; j < n; j += kStreamThreads) add1(p[j], g[j]);
+    }
+  } else {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kStreamThreads;
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kStreamThreads + tid; j < n; j += stride)
+      add1(p[j], g[j]);
   }
   F = wave_sum(F);
   G = wave_sum(G);
@@ -221,8 +248,7 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float*
     Us = wave_sum(Us);
     H = wave_sum(H);
   }
-  const int wid = tid / kWave;
-  if (lane_id() == 0) {
+  if (lane == 0) {
     red[0][wid] = F;
     red[1][wid] = G;
     if constexpr (PARAMS) {
@@ -234,7 +260,7 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_reduce_kernel(const float*
   if (tid < NS) {
     double acc = 0.0;
 #pragma unroll
-    for (int w = 0; w < kStreamThreads / kWave; ++w) acc += red[tid][w];
+    for (int w = 0; w < W; ++w) acc += red[tid][w];
     partials[NS * blockIdx.x + tid] = acc;
   }
 }
@@ -309,7 +335,9 @@ hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* 
 }
 
 // -------------------------------------------------------------- vjp emit ---
-// grad_r = (f/t)(g - <g,q>), q = f / sum f; zero where f == 0
+// grad_r = (f/t)(g - <g,q>), q = f / sum f; zero where f == 0.  grad_r is
+// stored non-temporally: with ordinary stores its dirty lines are written
+// back while the next pass reads.
 __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* __restrict__ g,
                                                                   const float* __restrict__ p,
                                                                   int64_t n,
@@ -340,7 +368,7 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* _
         o.z = fz * scale * (gv.z - coef);
         o.w = fw * scale * (gv.w - coef);
       }
-      o4[j * kStreamThreads + tid] = o;
+      store_stream4(reinterpret_cast<float*>(o4 + j * kStreamThreads + tid), o);
     }
   } else {
     for (int64_t i = base + tid; i < n && i < base + kStreamTile; i += kStreamThreads) {
