@@ -213,6 +213,32 @@ def test_row_backward_matches_oracle(lib, n, alpha):
                      f"n={n}")
 
 
+@pytest.mark.parametrize("batch,n", [
+    (3, 40001),                  # odd length: rows 1 and 2 misaligned (scalar grid-stride form)
+    (2, (1 << 20) + 4),          # whole tiles, one wave tile each, one float4 past them
+    (1, 5120 * 1024 * 3 + 777),  # three tiles per wave, float4s and scalars past the tiles
+])
+def test_pform_backward_tile_layouts(lib, batch, n):
+    """The p-form backward's reduce over interleaved wave tiles of 1024
+    scores: whole tiles, the float4s and scalars past them, and rows that
+    are not 16-byte aligned; grad_r against Eq. (5) and the budget and
+    temperature gradients against the oracle."""
+    rg = np.random.default_rng([17, n])
+    r = rg.standard_normal((batch, n)).astype(np.float32)
+    g = rg.standard_normal((batch, n)).astype(np.float32)
+    k, alpha = n / 64.0, -0.05
+    p, b = lib.lapsum_forward(_t(r), k, alpha)
+    grad = _np(lib.lapsum_backward(_t(g), p, b, alpha))
+    grad2, gk, ga = lib.lapsum_backward(_t(g), p, b, alpha, params=True)
+    assert np.array_equal(_np(grad2), grad)
+    bn, gk, ga = _np(b), _np(gk), _np(ga)
+    for row in range(batch):
+        ref = O.vjp(r[row], O.solve_sorted_scan(r[row], k, alpha), alpha, g[row])
+        assert grad_rel(grad[row], ref) <= G_TOL, (n, row, grad_rel(grad[row], ref))
+        check_params(float(gk[row]), float(ga[row]), r[row], float(bn[row]), alpha, g[row],
+                     f"n={n} row {row}")
+
+
 def test_forward_is_deterministic(lib):
     r = W.random_case(3, 32768, dist="normal", ties=0.01, batch=4)
     x = _t(r)
