@@ -68,15 +68,42 @@ __global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
   for (int e = tid; e < cnt_words<TW>(); e += TT) cnt[e] = 0u;
   __syncthreads();
   const int64_t base = tile * TILE;
+  // counts only (the order is the downsweep's): one LDS atomic per key on
+  // the wave's own counters is cheaper than matching the digit across the
+  // wave (measured: 36 -> 22 us per pass over 1e7 keys).  Counting does not
+  // depend on which thread holds which key, so the keys are read four at a
+  // time (16-byte loads: 17 -> 12 us per pass over 1e7 keys in a probe)
+  const void* src = a.src_f ? static_cast<const void*>(a.src_f) : static_cast<const void*>(a.src_k);
+  const bool vec = (reinterpret_cast<uintptr_t>(src) & 15) == 0;
+  auto count = [&](uint32_t key) { atomicAdd(&cnt[cnt_at<TW>((key >> a.shift) & 255u, wid)], 1u); };
+  if (vec) {
+    constexpr int V = TI / 4;
+    static_assert(TI % 4 == 0, "four keys per load");
+    uint4 q[V];
 #pragma unroll
-  for (int i = 0; i < TI; ++i) {
-    const int64_t pos = base + tile_pos<TI>(i);
-    const bool valid = pos < len;
-    const uint32_t d = valid ? (load_key(a, pos) >> a.shift) & 255u : 0u;
-    // counts only (the order is the downsweep's): one LDS atomic per key on
-    // the wave's own counters is cheaper than matching the digit across the
-    // wave (measured: 36 -> 22 us per pass over 1e7 keys)
-    if (valid) atomicAdd(&cnt[cnt_at<TW>(d, wid)], 1u);
+    for (int j = 0; j < V; ++j) {
+      const int64_t at = base + 4 * (static_cast<int64_t>(j) * TT + tid);
+      q[j] = at + 3 < len ? *reinterpret_cast<const uint4*>(static_cast<const uint32_t*>(src) + at)
+                          : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int64_t at = base + 4 * (static_cast<int64_t>(j) * TT + tid);
+      if (at + 3 < len) {
+        const uint32_t w[4] = {q[j].x, q[j].y, q[j].z, q[j].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) count(a.src_f ? desc_key(__uint_as_float(w[e])) : w[e]);
+      } else {
+        for (int e = 0; e < 4; ++e)
+          if (at + e < len) count(load_key(a, at + e));
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TI; ++i) {
+      const int64_t pos = base + tile_pos<TI>(i);
+      if (pos < len) count(load_key(a, pos));
+    }
   }
   __syncthreads();
   uint32_t sum = 0;

@@ -107,12 +107,17 @@ hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t,
 // workgroups (about one round of resident ones) so that each wave streams
 // many tiles.  (Each workgroup streaming its own contiguous range read the
 // 400 MB of p at n = 1e8 at 3.6 TB/s.)
+// Rows up to 2^24 scores take one tile per wave (all of a wave's loads in
+// flight at once, up to 4096 workgroups): there the row sits in the
+// last-level cache and a short pipeline only adds steps.
 constexpr int kVjpBlocks = 1280;
+constexpr int kVjpOneTileBlocks = 4096;
 
 int vjp_reduce_blocks(int64_t n) {
   const int64_t tiles = n / 1024;   // whole wave tiles
-  int64_t b = (tiles + 3) / 4;
-  return static_cast<int>(b < 1 ? 1 : (b > kVjpBlocks ? kVjpBlocks : b));
+  const int64_t b = (tiles + 3) / 4;
+  const int64_t cap = b <= kVjpOneTileBlocks ? kVjpOneTileBlocks : kVjpBlocks;
+  return static_cast<int>(b < 1 ? 1 : (b > cap ? cap : b));
 }
 
 // Sums of f = min(p, 1-p) and f g over the row, g read only for float4s with
@@ -125,9 +130,8 @@ int vjp_reduce_blocks(int64_t n) {
 // needs, then adds tile s; so the next two p tiles are in flight while a
 // tile's g is read, and no loaded register is copied (three p buffers rotate
 // through an unrolled period of three).  Loads past a wave's last tile read
-// one line of its first tile instead; a lane that needs no g reads one line
-// of it too.  The float4s past the whole tiles and the scalar tail go to the
-// last workgroup.
+// one line of its first tile instead; only lanes that need g load it.  The
+// float4s past the whole tiles and the scalar tail go to the last workgroup.
 template <bool PARAMS>
 __global__ __launch_bounds__(kStreamThreads, 4) void vjp_reduce_kernel(const float* __restrict__ g,
                                                                     const float* __restrict__ p,
@@ -192,7 +196,6 @@ __global__ __launch_bounds__(kStreamThreads, 4) void vjp_reduce_kernel(const flo
     const int cnt = w0 < nt ? static_cast<int>((nt - w0 + GW - 1) / GW) : 0;
     if (cnt > 0) {
       const float4* pd = p4 + w0 * 256;   // the line loads past the end read
-      const float4* gd = g4 + w0 * 256;
       auto base_of = [&](int j) { return (w0 + static_cast<int64_t>(j) * GW) * 256 + lane; };
       auto load_p = [&](float4 (&q)[4], int j) {
         const bool real = j < cnt;
@@ -212,7 +215,10 @@ __global__ __launch_bounds__(kStreamThreads, 4) void vjp_reduce_kernel(const flo
         for (int u = 0; u < 4; ++u) {
           const bool need = (fminf(pc[u].x, 1.0f - pc[u].x) + fminf(pc[u].y, 1.0f - pc[u].y)) +
                                 (fminf(pc[u].z, 1.0f - pc[u].z) + fminf(pc[u].w, 1.0f - pc[u].w)) != 0.0f;
-          gq[u] = *(need ? g4 + b + 64 * u : gd);
+          // only lanes that need g load it (a lane that needs none issues no
+          // request); g is used within this step, so no register is copied
+          gq[u] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+          if (need) gq[u] = g4[b + 64 * u];
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) add4(pc[u], gq[u]);
@@ -335,9 +341,13 @@ hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* 
 }
 
 // -------------------------------------------------------------- vjp emit ---
-// grad_r = (f/t)(g - <g,q>), q = f / sum f; zero where f == 0.  grad_r is
-// stored non-temporally: with ordinary stores its dirty lines are written
-// back while the next pass reads.
+// grad_r = (f/t)(g - <g,q>), q = f / sum f; zero where f == 0.  NT: grad_r
+// is stored non-temporally (rows of kNtStoreMin scores and more): with
+// ordinary stores the dirty lines of such a row are written back while the
+// next pass reads, while a shorter row's stay in the last-level cache.
+constexpr int64_t kNtStoreMin = int64_t(1) << 24;
+
+template <bool NT>
 __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* __restrict__ g,
                                                                   const float* __restrict__ p,
                                                                   int64_t n,
@@ -368,7 +378,10 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* _
         o.z = fz * scale * (gv.z - coef);
         o.w = fw * scale * (gv.w - coef);
       }
-      store_stream4(reinterpret_cast<float*>(o4 + j * kStreamThreads + tid), o);
+      if constexpr (NT)
+        store_stream4(reinterpret_cast<float*>(o4 + j * kStreamThreads + tid), o);
+      else
+        o4[j * kStreamThreads + tid] = o;
     }
   } else {
     for (int64_t i = base + tid; i < n && i < base + kStreamTile; i += kStreamThreads) {
@@ -383,8 +396,12 @@ hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const doub
                            float* grad, hipStream_t s) {
   const int64_t blocks = (n + kStreamTile - 1) / kStreamTile;
   { ProfScope ps_("vjp_emit", s);
-  hipLaunchKernelGGL(vjp_emit_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kStreamThreads), 0,
-                     s, g, p, n, coef, grad); }
+  if (n >= kNtStoreMin)
+    hipLaunchKernelGGL(vjp_emit_kernel<true>, dim3(static_cast<unsigned>(blocks)),
+                       dim3(kStreamThreads), 0, s, g, p, n, coef, grad);
+  else
+    hipLaunchKernelGGL(vjp_emit_kernel<false>, dim3(static_cast<unsigned>(blocks)),
+                       dim3(kStreamThreads), 0, s, g, p, n, coef, grad); }
   return hipGetLastError();
 }
 
