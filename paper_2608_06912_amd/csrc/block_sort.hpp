@@ -24,15 +24,24 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
 }
 
 // Lanes of this wave whose 8-bit digit equals mine (all 64 lanes active).
+// A lane differs from me in bit b exactly where the ballot of bit b differs
+// from my bit broadcast to all 64 positions (m = 0 or ~0), so the peers are
+// the complement of the OR over the eight bits of (ballot ^ m).  Each bit
+// costs one bit-field extract, one compare for the ballot and one
+// three-input bit operation per 32-bit half, acc | (ballot ^ m) (truth table
+// 0xf6 over the inputs acc, ballot, m), taking the ballot straight from
+// scalar registers: 34 vector instructions per match instead of 71 for the
+// per-lane select of ballot or its complement.
 __device__ __forceinline__ uint64_t match_digit8(uint32_t d) {
-  uint64_t peers = ~0ull;
+  uint32_t lo = 0u, hi = 0u;
 #pragma unroll
   for (int b = 0; b < 8; ++b) {
-    const bool bit = (d >> b) & 1u;
-    const uint64_t bal = __ballot(bit);
-    peers &= bit ? bal : ~bal;
+    const uint32_t m = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(d), b, 1));
+    const uint64_t bal = __builtin_amdgcn_uicmp(m, 0u, 33);   // 33: integer "not equal"
+    lo = __builtin_amdgcn_bitop3_b32(lo, static_cast<uint32_t>(bal), m, 0xf6);
+    hi = __builtin_amdgcn_bitop3_b32(hi, static_cast<uint32_t>(bal >> 32), m, 0xf6);
   }
-  return peers;
+  return (static_cast<uint64_t>(~hi) << 32) | ~lo;
 }
 
 // Per-(digit, wave) counters, digit-major.  Each digit's row is padded to an

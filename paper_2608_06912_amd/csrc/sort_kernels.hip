@@ -160,6 +160,61 @@ __global__ __launch_bounds__(TT) void sort_scan_kernel(PassArgs a) {
   if (tid == 0) a.totals[d] = carry;
 }
 
+// Stable ranks of one tile's keys and their scatter: keys (and values) in
+// registers, wave-striped; `gbase` holds each digit's first output position
+// for this tile.  FULL tiles (every position valid) skip the validity masks.
+template <int TI, bool PAIRS, bool FULL>
+__device__ __forceinline__ void downsweep_tile(const PassArgs& a, int64_t base, int64_t len,
+                                               uint32_t (&key)[TI], int32_t (&val)[TI],
+                                               uint32_t* cnt, uint32_t* wave_tot, uint32_t* off,
+                                               uint32_t* buf, uint8_t* dg) {
+  constexpr int64_t TILE = static_cast<int64_t>(TT) * TI;
+  const int tid = threadIdx.x;
+  const int wid = tid / kWave;
+  const int lane = lane_id();
+  uint32_t pos[TI];
+  uint64_t validm[TI];
+#pragma unroll
+  for (int i = 0; i < TI; ++i) validm[i] = FULL ? ~0ull : __ballot(base + tile_pos<TI>(i) < len);
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const uint32_t d = (key[i] >> a.shift) & 255u;
+    const uint64_t peers = FULL ? match_digit8(d) : (match_digit8(d) & validm[i]);
+    const uint32_t below = lanes_below(peers);
+    uint32_t* slot = &cnt[cnt_at<TW>(d, wid)];
+    const uint32_t c = *slot;
+    pos[i] = c + below;
+    const bool valid = FULL || ((validm[i] >> lane) & 1ull);
+    if (valid && below == 0u) *slot = c + static_cast<uint32_t>(__popcll(peers));
+  }
+  __syncthreads();
+  block_excl_scan_u32x4<TT>(cnt, wave_tot);
+  // output position of tile-local position q with digit d: off[d] + q
+  off[tid] -= cnt[cnt_at<TW>(tid, 0)];
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    pos[i] += cnt[cnt_at<TW>((key[i] >> a.shift) & 255u, wid)];
+    if (FULL || ((validm[i] >> lane) & 1ull)) buf[pos[i]] = key[i];
+  }
+  __syncthreads();
+  const int nvalid = FULL ? static_cast<int>(TILE) : static_cast<int>(len - base);
+  for (int q = tid; q < nvalid; q += TT) {
+    const uint32_t k = buf[q];
+    const uint32_t d = (k >> a.shift) & 255u;
+    a.dst_k[off[d] + static_cast<uint32_t>(q)] = k;
+    if constexpr (PAIRS) dg[q] = static_cast<uint8_t>(d);
+  }
+  if constexpr (PAIRS) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+      if (FULL || ((validm[i] >> lane) & 1ull)) buf[pos[i]] = static_cast<uint32_t>(val[i]);
+    __syncthreads();
+    for (int q = tid; q < nvalid; q += TT)
+      a.dst_v[off[dg[q]] + static_cast<uint32_t>(q)] = static_cast<int32_t>(buf[q]);
+  }
+}
+
 template <int TI, bool PAIRS, bool FUSED>
 __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
   constexpr int64_t TILE = static_cast<int64_t>(TT) * TI;
@@ -169,13 +224,25 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
   if (tile >= ntiles) return;
   __shared__ uint32_t cnt[cnt_words<TW>()];
   __shared__ uint32_t wave_tot[TW];
-  __shared__ uint32_t gbase[256];    // first output position of each digit for this tile
-  __shared__ uint32_t dstart[256];   // first tile-local position of each digit
+  __shared__ uint32_t off[256];      // first output position of each digit for this tile
   __shared__ uint32_t buf[TILE];
   __shared__ uint8_t dg[PAIRS ? TILE : 1];   // digit of each tile-local position
   const int tid = threadIdx.x;
   const int wid = tid / kWave;
   const int lane = lane_id();
+  const int64_t base = tile * TILE;
+  const bool full = base + TILE <= len;
+
+  // the tile's keys first, so that their latency overlaps the digit bases
+  uint32_t key[TI];
+  int32_t val[TI];
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const int64_t gp = base + tile_pos<TI>(i);
+    const bool valid = gp < len;
+    key[i] = valid ? load_key(a, gp) : 0xffffffffu;
+    if constexpr (PAIRS) val[i] = valid ? (a.src_v ? a.src_v[gp] : static_cast<int32_t>(gp)) : -1;
+  }
 
   // digit base over the whole array: exclusive prefix of totals over digits
   {
@@ -211,62 +278,14 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
 #pragma unroll
     for (int w = 0; w < TW; ++w)
       if (w < wid) wbase += wave_tot[w];
-    gbase[tid] = wbase + incl - tot + before_tile;
+    off[tid] = wbase + incl - tot + before_tile;
   }
   for (int e = tid; e < cnt_words<TW>(); e += TT) cnt[e] = 0u;
   __syncthreads();
-
-  const int64_t base = tile * TILE;
-  uint32_t key[TI];
-  int32_t val[TI];
-  uint32_t pos[TI];
-  uint64_t validm[TI];
-#pragma unroll
-  for (int i = 0; i < TI; ++i) {
-    const int64_t gp = base + tile_pos<TI>(i);
-    const bool valid = gp < len;
-    key[i] = valid ? load_key(a, gp) : 0xffffffffu;
-    if constexpr (PAIRS) val[i] = valid ? (a.src_v ? a.src_v[gp] : static_cast<int32_t>(gp)) : -1;
-    validm[i] = __ballot(valid);
-  }
-#pragma unroll
-  for (int i = 0; i < TI; ++i) {
-    const uint32_t d = (key[i] >> a.shift) & 255u;
-    const uint64_t peers = match_digit8(d) & validm[i];
-    const uint32_t below = lanes_below(peers);
-    uint32_t* slot = &cnt[cnt_at<TW>(d, wid)];
-    const uint32_t c = *slot;
-    pos[i] = c + below;
-    const bool valid = (validm[i] >> lane) & 1ull;
-    if (valid && below == 0u) *slot = c + static_cast<uint32_t>(__popcll(peers));
-  }
-  __syncthreads();
-  block_excl_scan_u32x4<TT>(cnt, wave_tot);
-  dstart[tid] = cnt[cnt_at<TW>(tid, 0)];
-#pragma unroll
-  for (int i = 0; i < TI; ++i) {
-    pos[i] += cnt[cnt_at<TW>((key[i] >> a.shift) & 255u, wid)];
-    if ((validm[i] >> lane) & 1ull) buf[pos[i]] = key[i];
-  }
-  __syncthreads();
-  const int nvalid = static_cast<int>((len - base) < TILE ? (len - base) : TILE);
-  for (int q = tid; q < nvalid; q += TT) {
-    const uint32_t k = buf[q];
-    const uint32_t d = (k >> a.shift) & 255u;
-    a.dst_k[gbase[d] + (q - dstart[d])] = k;
-    if constexpr (PAIRS) dg[q] = static_cast<uint8_t>(d);
-  }
-  if constexpr (PAIRS) {
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < TI; ++i)
-      if ((validm[i] >> lane) & 1ull) buf[pos[i]] = static_cast<uint32_t>(val[i]);
-    __syncthreads();
-    for (int q = tid; q < nvalid; q += TT) {
-      const uint32_t d = dg[q];
-      a.dst_v[gbase[d] + (q - dstart[d])] = static_cast<int32_t>(buf[q]);
-    }
-  }
+  if (full)
+    downsweep_tile<TI, PAIRS, true>(a, base, len, key, val, cnt, wave_tot, off, buf, dg);
+  else
+    downsweep_tile<TI, PAIRS, false>(a, base, len, key, val, cnt, wave_tot, off, buf, dg);
 }
 
 size_t sort_hist_words(int64_t len) {
