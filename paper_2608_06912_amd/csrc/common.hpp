@@ -547,29 +547,48 @@ __device__ double block_solve(const float (&s)[ITEMS], int cnt, double rank0, Pr
       double P = 1.0, E = 0.0;
       if (pc.S != 0.0) P += wexp_f64(static_cast<double>(pc.u) - si, inv_t) * pc.S;
       if (sc.T != 0.0) E += wexp_f64(si - static_cast<double>(sc.v), inv_t) * sc.T;
-      for (int j = 0; j < oc; ++j) {
-        const double sj = sm.sv[j];
-        if (j < tid) P += wexp_f64(sj - si, inv_t);
-        else if (j > tid) E += wexp_f64(si - sj, inv_t);
+      // the run's own terms are per-score terms like those of the group
+      // summaries (float32 exponentials of float64 differences), unrolled
+      // over the run's capacity so that they are all independent (runs of
+      // 32 keep the loop: their kernels are short of registers already)
+      double Pt = 0.0, Et = 0.0;
+      if constexpr (ITEMS <= 16) {
+#pragma unroll
+        for (int j = 0; j < ITEMS; ++j) {
+          if (j < oc) {
+            const double sj = sm.sv[j];
+            if (j < tid) Pt += wexp_f32(sj - si, c2);
+            else if (j > tid) Et += wexp_f32(si - sj, c2);
+          }
+        }
+      } else {
+        for (int j = 0; j < oc; ++j) {
+          const double sj = sm.sv[j];
+          if (j < tid) Pt += wexp_f32(sj - si, c2);
+          else if (j > tid) Et += wexp_f32(si - sj, c2);
+        }
       }
+      P += Pt;
+      E += Et;
       sm.P[tid] = P;
       sm.Q[tid] = 1.0 + E;
       le = (base + static_cast<double>(tid) + 1.0 - 0.5 * P + 0.5 * E) <= k;
     }
     int m = block_count<WAVES>(le, sm);   // node values are non-decreasing
     if (m == 0) m = 1;                    // the first position was found at or below k
-    if (tid == 0) {
-      const double c_up = base + m;
-      const double u = sm.sv[m - 1];
-      const double lnA = log(sm.P[m - 1]);
-      double bb;
-      if (m < oc) {
-        bb = gap_root(k, t, c_up, true, u, lnA, true, sm.sv[m], log(sm.Q[m]));
-      } else {
-        const bool has_dn = sc.T != 0.0;
-        bb = gap_root(k, t, c_up, true, u, lnA, has_dn, sc.v, has_dn ? log(sc.T) : 0.0);
+    if (tid < 2) {
+      // the logarithms of the gap's two sums side by side (lanes 0 and 1);
+      // without a lower side gap_root does not use the second
+      const bool has_dn = m < oc || sc.T != 0.0;
+      const double arg = tid == 0 ? sm.P[m - 1] : (m < oc ? sm.Q[m] : (has_dn ? sc.T : 1.0));
+      const double lg = log(arg);
+      const double lnB = __shfl(lg, 1, kWave);
+      if (tid == 0) {
+        const double c_up = base + m;
+        const double u = sm.sv[m - 1];
+        sm.b = (m < oc) ? gap_root(k, t, c_up, true, u, lg, true, sm.sv[m], lnB)
+                        : gap_root(k, t, c_up, true, u, lg, has_dn, sc.v, lnB);
       }
-      sm.b = bb;
     }
     __syncthreads();
   }

@@ -29,7 +29,9 @@ namespace {
 constexpr int TT = kTileThreads;
 constexpr int TI = kTileItems;
 constexpr int64_t TILE = kTile;
-constexpr int kTileRec = 8;   // doubles per tile: S, X, first, last, suffix after (v, T), prefix before (u, S)
+constexpr int kTileRec = 8;   // doubles per tile: S, X, first, last, then e^{-(first - last)/t}
+                              // (the wide finalize) or the suffix after (v, T) and the prefix
+                              // before (u, S) (the finalize of longer rows)
 
 __device__ __forceinline__ int64_t eff_len(int64_t len, const int64_t* len_dev) {
   if (len_dev == nullptr) return len;
@@ -115,6 +117,7 @@ __global__ __launch_bounds__(TT) void solve_tiles_kernel(const uint32_t* __restr
     rec[1] = x;
     rec[2] = first;
     rec[3] = last;
+    rec[4] = wexp_f64(first - last, 1.0 / t);   // the link across the tile
   }
 }
 
@@ -286,24 +289,35 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
   const int64_t t0 = static_cast<int64_t>(tid) * per;
   int nr = static_cast<int>(ntiles - t0 < per ? ntiles - t0 : per);
   nr = nr < 0 ? 0 : nr;
-  double S[kFinPer], X[kFinPer];
+  double S[kFinPer], X[kFinPer], span[kFinPer];
   float fst[kFinPer], lst[kFinPer];
 #pragma unroll
   for (int q = 0; q < kFinPer; ++q) {
-    const double* r = tb + (t0 + (q < nr ? q : 0)) * kTileRec;
     const bool on = q < nr;
-    S[q] = on ? r[0] : 0.0;
-    X[q] = on ? r[1] : 0.0;
-    fst[q] = on ? static_cast<float>(r[2]) : 0.0f;
-    lst[q] = on ? static_cast<float>(r[3]) : 0.0f;
+    const double* r = tb + (on ? t0 + q : 0) * kTileRec;   // always a record of the buffer
+    const double2 sx = *reinterpret_cast<const double2*>(r);
+    const double2 fl = *reinterpret_cast<const double2*>(r + 2);
+    S[q] = on ? sx.x : 0.0;
+    X[q] = on ? sx.y : 0.0;
+    fst[q] = on ? static_cast<float>(fl.x) : 0.0f;
+    lst[q] = on ? static_cast<float>(fl.y) : 0.0f;
+    span[q] = on ? r[4] : 0.0;
   }
-  // links between the run's anchors: prefix pairs move from last_{q-1} to
-  // last_q, suffix pairs from first_{q+1} to first_q
+  // links between the run's anchors.  With span_q = e^{-(first_q - last_q)/t}
+  // from the tile pass and the gaps L_q = e^{-(last_{q-1} - first_q)/t}
+  // between tiles (one exponential per tile, all independent), the prefix
+  // pairs move from last_{q-1} to last_q by wp = L_q span_q and the suffix
+  // pairs from first_{q+1} to first_q by ws = span_q L_{q+1}; L_q itself
+  // moves a prefix pair to the tile's first score
+  double L[kFinPer];
+#pragma unroll
+  for (int q = 0; q < kFinPer; ++q)
+    L[q] = (q >= 1 && q < nr) ? wexp_f64(static_cast<double>(lst[q - 1]) - fst[q], inv_t) : 0.0;
   double wp[kFinPer], ws[kFinPer];
 #pragma unroll
   for (int q = 0; q < kFinPer; ++q) {
-    wp[q] = (q >= 1 && q < nr) ? wexp_f64(static_cast<double>(lst[q - 1]) - lst[q], inv_t) : 0.0;
-    ws[q] = (q + 1 < nr) ? wexp_f64(static_cast<double>(fst[q]) - fst[q + 1], inv_t) : 0.0;
+    wp[q] = (q >= 1 && q < nr) ? L[q] * span[q] : 0.0;
+    ws[q] = (q + 1 < nr) ? span[q] * L[q + 1] : 0.0;
   }
   // a tile's prefix sum anchored at its last score is S (>= 1), its suffix
   // sum anchored at its first score 1 + X: no tile is empty
@@ -324,9 +338,11 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
   // 2. the prefix before each tile (anchored at the previous tile's last
   //    score, or the carry's anchor) and the suffix after it (anchored at
   //    the next tile's first score, or the carry's), then the node value at
-  //    each tile's first score
-  const double pin_w = (nr > 0 && pre_in.S != 0.0)
-                           ? wexp_f64(static_cast<double>(pre_in.u) - lst[0], inv_t) * pre_in.S : 0.0;
+  //    each tile's first score: the carry into the run is moved to the first
+  //    tile's first score (pin0) and on to its last (pin_w = pin0 span_0)
+  const double pin0 = (nr > 0 && pre_in.S != 0.0)
+                          ? wexp_f64(static_cast<double>(pre_in.u) - fst[0], inv_t) * pre_in.S : 0.0;
+  const double pin_w = pin0 * span[0];
   double sin_w = 0.0;   // suffix after the run moved to the run's last tile's first score
 #pragma unroll
   for (int q = 0; q < kFinPer; ++q)
@@ -334,6 +350,7 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
       sin_w = wexp_f64(static_cast<double>(fst[q]) - suf_in.v, inv_t) * suf_in.T;
   Pre bef[kFinPer];
   Suf aft[kFinPer];
+  double Pin[kFinPer];   // the prefix before tile q moved to its first score
   {
     Pre cur = pre_in;
     double run = 0.0;   // prefix through tile q, anchored at lst[q]
@@ -341,11 +358,13 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
     for (int q = 0; q < kFinPer; ++q) {
       if (q < nr) {
         bef[q] = cur;
+        Pin[q] = (q == 0) ? pin0 : L[q] * run;
         run = (q == 0) ? S[0] + pin_w : fma(wp[q], run, S[q]);
         cur = Pre{lst[q], run};
       }
     }
   }
+  double Ein[kFinPer];   // the suffix after tile q moved to its first score
   {
     Suf cur = suf_in;
     double run = 0.0;   // suffix from tile q on, anchored at fst[q]
@@ -353,6 +372,7 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
     for (int q = kFinPer - 1; q >= 0; --q) {
       if (q < nr) {
         aft[q] = cur;
+        Ein[q] = (q == nr - 1) ? sin_w : ws[q] * run;
         run = (q == nr - 1) ? (1.0 + X[q]) + sin_w : fma(ws[q], run, 1.0 + X[q]);
         cur = Suf{fst[q], run};
       }
@@ -362,10 +382,8 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
 #pragma unroll
   for (int q = 0; q < kFinPer; ++q) {
     if (q < nr) {
-      double P = 1.0;
-      if (bef[q].S != 0.0) P += wexp_f64(static_cast<double>(bef[q].u) - fst[q], inv_t) * bef[q].S;
-      double E = X[q];
-      if (aft[q].T != 0.0) E += wexp_f64(static_cast<double>(fst[q]) - aft[q].v, inv_t) * aft[q].T;
+      const double P = 1.0 + Pin[q];
+      const double E = X[q] + Ein[q];
       const double N = x.nR + static_cast<double>((t0 + q) * TILE) + 1.0 - 0.5 * P + 0.5 * E;
       if (N <= k) below = t0 + q + 1;   // non-decreasing: the last such tile
     }
