@@ -588,8 +588,10 @@ __device__ double bucket_core(const uint32_t (&cnt)[BPT], const double (&U)[BPT]
   // 2. block scans, seeded with the tails
   Pre pre_all;
   Suf suf_all;
-  const Pre pre_in = block_excl_pre<SW>(Pre{v[BPT], Pm}, x.pre, inv_t, S.csm, &pre_all);
-  const Suf suf_in = block_excl_suf<SW>(mys, x.suf, inv_t, S.csm, &suf_all);
+  Pre pre_in;
+  Suf suf_in;
+  block_excl_pre_suf<SW>(Pre{v[BPT], Pm}, x.pre, mys, x.suf, inv_t, S.csm, &pre_in, &pre_all, &suf_in,
+                         &suf_all);
   // the counts scan in 32 bits (fewer than 2^31 keys)
   const int64_t incl = static_cast<int64_t>(wave_incl_add(static_cast<uint32_t>(mine)));
   if (lane == kWave - 1) S.cw[wid] = incl;

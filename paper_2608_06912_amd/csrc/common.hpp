@@ -259,6 +259,9 @@ struct ScanSmem {
   double A[WAVES], B[WAVES];   // per-wave affine maps
   float au[WAVES];             // per-wave anchor of the last (first) non-empty group
   int ah[WAVES];
+  double A2[WAVES], B2[WAVES];   // the suffix scan's, when both run together
+  float au2[WAVES];
+  int ah2[WAVES];
   int cnt[WAVES];
   double b;
   double P[64];   // crossing refinement (at most 64 items per thread)
@@ -278,28 +281,40 @@ struct ScanSmem {
 // non-increasing along the order), so products only underflow, when the
 // carried terms are negligible.
 
-// Exclusive block scan of Pre in thread order, seeded with carry (groups
-// before the block).  Returns this thread's exclusive prefix; *total gets
-// carry (+) all.  Empty groups (S == 0) are skipped.
+// Exclusive block scans of the prefix pairs xp in thread order, seeded
+// with pc (the groups before the block), and of the suffix pairs xs from
+// the right, seeded with sc (the groups after it), run together on three
+// barriers.  *pre_in / *suf_in get this thread's exclusive prefix / suffix,
+// *pre_total = pc (+) all and *suf_total = all (+) sc.  Empty groups (S == 0,
+// T == 0) are skipped.  The two exponentials and the two wave scans of a
+// thread are independent of each other.
 template <int WAVES>
-__device__ Pre block_excl_pre(Pre x, Pre carry, double inv_t, ScanSmem<WAVES>& sm, Pre* total) {
+__device__ void block_excl_pre_suf(Pre xp, Pre pc, Suf xs, Suf sc, double inv_t,
+                                   ScanSmem<WAVES>& sm, Pre* pre_in, Pre* pre_total, Suf* suf_in,
+                                   Suf* suf_total) {
   const int lane = lane_id();
   const int wid = threadIdx.x / kWave;
-  const bool has = x.S != 0.0;
-  const bool chas = carry.S != 0.0;
-  // 1. anchor of the last non-empty group before each thread (ballot)
-  const uint64_t hm = __ballot(has);
-  const float lu = __shfl(x.u, hm != 0ull ? 63 - __clzll(hm) : 0, kWave);
+  const bool phas = xp.S != 0.0, shas = xs.T != 0.0;
+  const bool pchas = pc.S != 0.0, schas = sc.T != 0.0;
+  // 1. anchors of the nearest non-empty groups before (prefix) and after
+  //    (suffix) each thread
+  const uint64_t phm = __ballot(phas);
+  const uint64_t shm = __ballot(shas);
+  const float lu = __shfl(xp.u, phm != 0ull ? 63 - __clzll(phm) : 0, kWave);
+  const float fv = __shfl(xs.v, shm != 0ull ? __ffsll(static_cast<long long>(shm)) - 1 : 0, kWave);
   if (lane == 0) {
-    sm.ah[wid] = hm != 0ull ? 1 : 0;
+    sm.ah[wid] = phm != 0ull ? 1 : 0;
     sm.au[wid] = lu;
+    sm.ah2[wid] = shm != 0ull ? 1 : 0;
+    sm.au2[wid] = fv;
   }
-  const uint64_t before = hm & ((1ull << lane) - 1ull);
-  const float bu = __shfl(x.u, before ? 63 - __clzll(before) : 0, kWave);
+  const uint64_t before = phm & ((1ull << lane) - 1ull);
+  const float bu = __shfl(xp.u, before ? 63 - __clzll(before) : 0, kWave);
+  const uint64_t after = lane == kWave - 1 ? 0ull : shm & (~0ull << (lane + 1));
+  const float av = __shfl(xs.v, after ? __ffsll(static_cast<long long>(after)) - 1 : 0, kWave);
   __syncthreads();
-  // the anchor entering this wave (every wave's record read at once)
-  int eh = chas ? 1 : 0;
-  float eu = carry.u;
+  int eh = pchas ? 1 : 0;
+  float eu = pc.u;
 #pragma unroll
   for (int w = 0; w < WAVES; ++w) {
     const int h = sm.ah[w];
@@ -309,109 +324,78 @@ __device__ Pre block_excl_pre(Pre x, Pre carry, double inv_t, ScanSmem<WAVES>& s
       eu = a;
     }
   }
-  const int ph = before != 0ull ? 1 : eh;
-  const float pu = before != 0ull ? bu : eu;
-  // 2. P_i = A_i P_{i-1} + B_i
-  double A = has ? (ph ? wexp_f64(static_cast<double>(pu) - static_cast<double>(x.u), inv_t) : 0.0) : 1.0;
-  double B = has ? x.S : 0.0;
-  wave_affine_up(A, B);
-  if (lane == kWave - 1) {
-    sm.A[wid] = A;
-    sm.B[wid] = B;
-  }
-  __syncthreads();
-  const double P_in = chas ? carry.S : 0.0;
-  double P0 = P_in;   // P entering this wave
-#pragma unroll
-  for (int w = 0; w < WAVES; ++w) {
-    const double Aw = sm.A[w], Bw = sm.B[w];
-    if (w < wid) P0 = fma(Aw, P0, Bw);
-  }
-  double Pt = P_in;
-  int th = chas ? 1 : 0;
-  float tu = carry.u;
-#pragma unroll
-  for (int w = 0; w < WAVES; ++w) {
-    Pt = fma(sm.A[w], Pt, sm.B[w]);
-    if (sm.ah[w]) {
-      th = 1;
-      tu = sm.au[w];
-    }
-  }
-  const double Pi = fma(A, P0, B);
-  double Pe = __shfl_up(Pi, 1, kWave);
-  if (lane == 0) Pe = P0;
-  *total = th ? Pre{tu, Pt} : pre_empty();
-  __syncthreads();
-  return ph ? Pre{pu, Pe} : pre_empty();
-}
-
-// Exclusive block scan of Suf from the right, seeded with carry (groups
-// after the block).  *total gets all (+) carry.  Empty groups (T == 0) are
-// skipped.
-template <int WAVES>
-__device__ Suf block_excl_suf(Suf x, Suf carry, double inv_t, ScanSmem<WAVES>& sm, Suf* total) {
-  const int lane = lane_id();
-  const int wid = threadIdx.x / kWave;
-  const bool has = x.T != 0.0;
-  const bool chas = carry.T != 0.0;
-  // 1. anchor of the first non-empty group after each thread (ballot)
-  const uint64_t hm = __ballot(has);
-  const float fv = __shfl(x.v, hm != 0ull ? __ffsll(static_cast<long long>(hm)) - 1 : 0, kWave);
-  if (lane == 0) {
-    sm.ah[wid] = hm != 0ull ? 1 : 0;
-    sm.au[wid] = fv;
-  }
-  const uint64_t after = lane == kWave - 1 ? 0ull : hm & (~0ull << (lane + 1));
-  const float av = __shfl(x.v, after ? __ffsll(static_cast<long long>(after)) - 1 : 0, kWave);
-  __syncthreads();
-  // the anchor following this wave (every wave's record read at once)
-  int fh = chas ? 1 : 0;
-  float fv2 = carry.v;
+  int fh = schas ? 1 : 0;
+  float fv2 = sc.v;
 #pragma unroll
   for (int w = WAVES - 1; w >= 0; --w) {
-    const int h = sm.ah[w];
-    const float a = sm.au[w];
+    const int h = sm.ah2[w];
+    const float a = sm.au2[w];
     if (w > wid && h) {
       fh = 1;
       fv2 = a;
     }
   }
+  const int ph = before != 0ull ? 1 : eh;
+  const float pu = before != 0ull ? bu : eu;
   const int nh = after != 0ull ? 1 : fh;
   const float nv = after != 0ull ? av : fv2;
-  // 2. T_i = B_i + A_i T_{i+1}
-  double A = has ? (nh ? wexp_f64(static_cast<double>(x.v) - static_cast<double>(nv), inv_t) : 0.0) : 1.0;
-  double B = has ? x.T : 0.0;
-  wave_affine_down(A, B);
+  // 2. P_i = A_i P_{i-1} + B_i and T_i = B_i + A_i T_{i+1}
+  double Ap = phas ? (ph ? wexp_f64(static_cast<double>(pu) - static_cast<double>(xp.u), inv_t) : 0.0) : 1.0;
+  double Bp = phas ? xp.S : 0.0;
+  double As = shas ? (nh ? wexp_f64(static_cast<double>(xs.v) - static_cast<double>(nv), inv_t) : 0.0) : 1.0;
+  double Bs = shas ? xs.T : 0.0;
+  wave_affine_up(Ap, Bp);
+  wave_affine_down(As, Bs);
+  if (lane == kWave - 1) {
+    sm.A[wid] = Ap;
+    sm.B[wid] = Bp;
+  }
   if (lane == 0) {
-    sm.A[wid] = A;
-    sm.B[wid] = B;
+    sm.A2[wid] = As;
+    sm.B2[wid] = Bs;
   }
   __syncthreads();
-  const double T_in = chas ? carry.T : 0.0;
-  double T0 = T_in;   // T following this wave
+  const double P_in = pchas ? pc.S : 0.0;
+  double P0 = P_in;   // P entering this wave
+  double Pt = P_in;
+  int pth = pchas ? 1 : 0;
+  float ptu = pc.u;
 #pragma unroll
-  for (int w = WAVES - 1; w >= 0; --w) {
+  for (int w = 0; w < WAVES; ++w) {
     const double Aw = sm.A[w], Bw = sm.B[w];
-    if (w > wid) T0 = fma(Aw, T0, Bw);
-  }
-  double Tt = T_in;
-  int th = chas ? 1 : 0;
-  float tv = carry.v;
-#pragma unroll
-  for (int w = WAVES - 1; w >= 0; --w) {
-    Tt = fma(sm.A[w], Tt, sm.B[w]);
+    if (w < wid) P0 = fma(Aw, P0, Bw);
+    Pt = fma(Aw, Pt, Bw);
     if (sm.ah[w]) {
-      th = 1;
-      tv = sm.au[w];
+      pth = 1;
+      ptu = sm.au[w];
     }
   }
-  const double Ti = fma(A, T0, B);
+  const double T_in = schas ? sc.T : 0.0;
+  double T0 = T_in;   // T following this wave
+  double Tt = T_in;
+  int sth = schas ? 1 : 0;
+  float stv = sc.v;
+#pragma unroll
+  for (int w = WAVES - 1; w >= 0; --w) {
+    const double Aw = sm.A2[w], Bw = sm.B2[w];
+    if (w > wid) T0 = fma(Aw, T0, Bw);
+    Tt = fma(Aw, Tt, Bw);
+    if (sm.ah2[w]) {
+      sth = 1;
+      stv = sm.au2[w];
+    }
+  }
+  const double Pi = fma(Ap, P0, Bp);
+  double Pe = __shfl_up(Pi, 1, kWave);
+  if (lane == 0) Pe = P0;
+  const double Ti = fma(As, T0, Bs);
   double Te = __shfl_down(Ti, 1, kWave);
   if (lane == kWave - 1) Te = T0;
-  *total = th ? Suf{tv, Tt} : suf_empty();
+  *pre_total = pth ? Pre{ptu, Pt} : pre_empty();
+  *suf_total = sth ? Suf{stv, Tt} : suf_empty();
+  *pre_in = ph ? Pre{pu, Pe} : pre_empty();
+  *suf_in = nh ? Suf{nv, Te} : suf_empty();
   __syncthreads();
-  return nh ? Suf{nv, Te} : suf_empty();
 }
 
 // Number of threads in the block with flag set.
@@ -499,8 +483,10 @@ __device__ double block_solve(const float (&s)[ITEMS], int cnt, double rank0, Pr
   }
 
   // 2. carries into this thread from both sides
-  Pre pre_in = block_excl_pre<WAVES>(mine_pre, ext_pre, inv_t, sm, pre_total);
-  Suf suf_in = block_excl_suf<WAVES>(mine_suf, ext_suf, inv_t, sm, suf_total);
+  Pre pre_in;
+  Suf suf_in;
+  block_excl_pre_suf<WAVES>(mine_pre, ext_pre, mine_suf, ext_suf, inv_t, sm, &pre_in, pre_total,
+                            &suf_in, suf_total);
 
   // 3. node value at this thread's first position
   bool below_k = false;

@@ -152,8 +152,9 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
     }
     const Pre mp = has ? Pre{static_cast<float>(last), S} : pre_empty();
     const Suf ms = has ? Suf{static_cast<float>(first), 1.0 + X} : suf_empty();
-    const Pre pre_in = block_excl_pre<WAVES>(mp, x.pre, inv_t, sm, &pre_all);
-    const Suf suf_in = block_excl_suf<WAVES>(ms, x.suf, inv_t, sm, &suf_all);
+    Pre pre_in;
+    Suf suf_in;
+    block_excl_pre_suf<WAVES>(mp, x.pre, ms, x.suf, inv_t, sm, &pre_in, &pre_all, &suf_in, &suf_all);
     if (has) {
       double P = 1.0;
       if (pre_in.S != 0.0) P += wexp_f64(static_cast<double>(pre_in.u) - first, inv_t) * pre_in.S;
@@ -183,8 +184,9 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
       const double* r = tb + q * kTileRec;
       ms = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, ms, inv_t);
     }
-    const Pre pre_in = block_excl_pre<WAVES>(mp, x.pre, inv_t, sm, &pre_all);
-    const Suf suf_in = block_excl_suf<WAVES>(ms, x.suf, inv_t, sm, &suf_all);
+    Pre pre_in;
+    Suf suf_in;
+    block_excl_pre_suf<WAVES>(mp, x.pre, ms, x.suf, inv_t, sm, &pre_in, &pre_all, &suf_in, &suf_all);
 
     // 2. suffix carried into each tile from the right (stored), then the
     //    node value at each tile's first score walking left to right
@@ -332,8 +334,9 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
   const Suf ms = nr > 0 ? Suf{fst[0], Tm} : suf_empty();
   Pre pre_all;
   Suf suf_all;
-  const Pre pre_in = block_excl_pre<FW>(mp, x.pre, inv_t, sm, &pre_all);
-  const Suf suf_in = block_excl_suf<FW>(ms, x.suf, inv_t, sm, &suf_all);
+  Pre pre_in;
+  Suf suf_in;
+  block_excl_pre_suf<FW>(mp, x.pre, ms, x.suf, inv_t, sm, &pre_in, &pre_all, &suf_in, &suf_all);
 
   // 2. the prefix before each tile (anchored at the previous tile's last
   //    score, or the carry's anchor) and the suffix after it (anchored at
