@@ -889,6 +889,7 @@ __global__ __launch_bounds__(ST) void row_bucket_forward_kernel(const float* __r
   __shared__ unsigned long long cd[kBuckets];
   __shared__ uint32_t rk[2][SW];
   __shared__ double b_s;
+  __shared__ float edge[kBuckets + 1];   // bucket_hi of every bucket edge, read twice per score
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
@@ -947,6 +948,8 @@ __global__ __launch_bounds__(ST) void row_bucket_forward_kernel(const float* __r
   const BucketGeom g = geom_of(kmin, kmax);
   const double fscale = ldexp(1.0, fixed_bits(n));
   const double c2 = kLog2e / t;
+  for (int e = tid; e <= kBuckets; e += ST) edge[e] = bucket_hi(g, e);
+  __syncthreads();
 
   // 3. bucket counts and sums: e^{-(v_d - r)/t} anchored at the bucket's
   //    upper edge and e^{-(r - v_{d+1})/t} at the next bucket's
@@ -956,8 +959,8 @@ __global__ __launch_bounds__(ST) void row_bucket_forward_kernel(const float* __r
       const uint32_t key = desc_key(x[i]);
       const int d = static_cast<int>((key - g.kmin) >> g.shift);
       const double rv = x[i];
-      const double up = wexp_f32(static_cast<double>(bucket_hi(g, d)) - rv, c2);
-      const double dn = wexp_f32(rv - static_cast<double>(bucket_hi(g, d + 1)), c2);
+      const double up = wexp_f32(static_cast<double>(edge[d]) - rv, c2);
+      const double dn = wexp_f32(rv - static_cast<double>(edge[d + 1]), c2);
       atomicAdd(&cn[d], 1u);
       atomicAdd(&cu[d], static_cast<unsigned long long>(__double2ull_rn(up * fscale)));
       atomicAdd(&cd[d], static_cast<unsigned long long>(__double2ull_rn(dn * fscale)));
