@@ -20,9 +20,12 @@ is reported on the bytes its kernels must move (path_roofline), against the
 
 Per workload (configs): forward, backward and forward + backward per call
 (median and mean over 30 calls timed with events after 3 warm-ups), scores/s
-and the fraction of the HBM peak for the bytes the survey's pass model says
-each path must move (20 B/score on chip, 100 B/score by the device-wide
-sort, 32 B/score + 8 K + 72 |M| bracketed).
+and the fraction of the HBM peak for the bytes the path's kernels must move
+(roofline_frac: every streaming kernel that runs, counted from the event
+profiler, times its algorithmic bytes per launch); model_equivalent_frac
+puts the survey's pass model over the same time (20 B/score on chip,
+100 B/score by the device-wide sort with indices, 32 B/score + 8 K + 72 |M|
+bracketed), which the band path and the keys-only sort beat.
 
 CPU baseline: the float64 oracle's closed form (sort + scan + root) and its
 Eq. (5) VJP on a bounded sample of the same row (its first 5e7 scores, k
@@ -92,8 +95,10 @@ def parse():
 
 def kernel_bytes(name: str, n: int, active: int, band: int, ones: bool) -> float | None:
     """Algorithmic HBM bytes one launch of a streaming kernel must move
-    (band: scores in the bracket's band; active: scores with 0 < p < 1;
-    ones: a_R is finite, so one bit per score marks the scores above the band)."""
+    (n: scores the launch covers; band: scores in the bracket's band; active:
+    scores with 0 < p < 1; ones: a_R is finite, so one bit per score marks
+    the scores above the band).  None for the latency-bound kernels (sample,
+    select, scans, solves, finalizes), whose bytes are under 1% of a call's."""
     tiles = 8.0 * ((n + 1023) // 1024)     # one 8-byte record per writer tile
     bits = n / 8.0 if ones else 0.0
     if name == "partition":
@@ -106,6 +111,16 @@ def kernel_bytes(name: str, n: int, active: int, band: int, ones: bool) -> float
         return 8.0 * band + 8.0 * active     # read the band; g and its copy where f != 0
     if name == "band_vjp_emit":
         return 4.0 * n + 12.0 * band + tiles  # write grad; read the band, its g copies, the records
+    if name == "sort_upsweep":
+        return 4.0 * n                       # read the keys (digit counts)
+    if name == "sort_downsweep":
+        return 8.0 * n                       # read and write the keys (no permutation asked for)
+    if name == "solve_tiles":
+        return 4.0 * n                       # read the sorted keys once
+    if name in ("row_bucket_forward", "row_forward"):
+        return 8.0 * n                       # read r, write p (n: every score of the batch)
+    if name == "row_backward":
+        return 12.0 * n                      # read g and p, write grad
     if name == "emit":
         return 8.0 * n                       # read r, write p
     if name == "vjp_reduce":
@@ -297,16 +312,47 @@ def run_workload(dev, name, path, iters=30):
     n_M = 0
     if path == "bracketed":
         n_M = int(out[2][0]["n_M"])
+    pb = path_bytes(L, fb, out, x, w, path)
     mb = model_bytes(w, path, n_M)
     med = _stats(t_fb)["median"]
     row = {"workload": name, "path": path, "batch": w.batch, "n": w.n,
            "fwd_ms": _stats(t_f), "bwd_ms": _stats(t_b), "fwd_bwd_ms": _stats(t_fb),
            "scores_per_s": w.batch * w.n / (med / 1e3),
-           "model_bytes": mb, "roofline_frac": mb / (med / 1e3) / 1e9 / HBM_PEAK_GBS}
+           "path_bytes": pb, "roofline_frac": pb / (med / 1e3) / 1e9 / HBM_PEAK_GBS,
+           "model_bytes": mb, "model_equivalent_frac": mb / (med / 1e3) / 1e9 / HBM_PEAK_GBS}
     if path == "bracketed":
         row["n_M"] = n_M
     del x, g
     return row
+
+
+def path_bytes(L, fb, out, x, w, path, calls=5):
+    """Bytes one forward + backward's kernels must move: the kernels that
+    run (event profiler over a few calls) times kernel_bytes for each."""
+    import numpy as np
+    import torch
+    N = w.batch * w.n
+    p = out[0]
+    active = int(((p > 0) & (p < 1)).sum().item())
+    band_n, ones = 0, False
+    if path == "bracketed":
+        inf0 = out[2][0]
+        lo = np.float32(inf0["a_L"]) - np.float64(105.0 * w.t)
+        hi = np.float32(inf0["a_R"]) + np.float64(18.0 * w.t)
+        band_n = int(((x >= float(lo)) & (x < float(hi))).sum().item())
+        ones = math.isfinite(inf0["a_R"])
+    torch.cuda.synchronize()
+    L.lapsum_profile_start()
+    for _ in range(calls):
+        fb()
+    torch.cuda.synchronize()
+    prof = L.lapsum_profile_stop()
+    total = 0.0
+    for kname, (c, _) in prof.items():
+        kb = kernel_bytes(kname, N, active, band_n, ones)
+        if kb is not None:
+            total += kb * c / calls
+    return total
 
 
 def config_table(dev, main):
@@ -571,12 +617,15 @@ def main():
     step_gbs = step_bytes / (ms_step / 1e3) / 1e9
 
     mb = model_bytes(w, "bracketed", int(inf0["n_M"]))
+    med_step = _stats(t_step)["median"] / 1e3
     main_row = {"workload": "n1e8", "path": "bracketed", "batch": 1, "n": n,
                 "fwd_ms": _stats(t_fwd), "bwd_ms": _stats(t_bwd), "fwd_bwd_ms": _stats(t_step),
                 "bwd_pform_ms": _stats(t_bwd_p),
-                "scores_per_s": n / (_stats(t_step)["median"] / 1e3),
+                "scores_per_s": n / med_step,
+                "path_bytes": step_bytes,
+                "roofline_frac": step_bytes / med_step / 1e9 / HBM_PEAK_GBS,
                 "model_bytes": mb,
-                "roofline_frac": mb / (_stats(t_step)["median"] / 1e3) / 1e9 / HBM_PEAK_GBS,
+                "model_equivalent_frac": mb / med_step / 1e9 / HBM_PEAK_GBS,
                 "n_M": int(inf0["n_M"])}
 
     out = {
