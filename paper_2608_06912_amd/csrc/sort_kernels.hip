@@ -161,8 +161,10 @@ __global__ __launch_bounds__(TT) void sort_scan_kernel(PassArgs a) {
 }
 
 // Stable ranks of one tile's keys and their scatter: keys (and values) in
-// registers, wave-striped; `gbase` holds each digit's first output position
-// for this tile.  FULL tiles (every position valid) skip the validity masks.
+// registers, wave-striped; `off` holds each digit's first output position
+// for this tile on entry and becomes the offset from a tile-local position
+// to its output position (unsigned arithmetic, so the difference may wrap).
+// FULL tiles (every position valid) skip the validity masks.
 template <int TI, bool PAIRS, bool FULL>
 __device__ __forceinline__ void downsweep_tile(const PassArgs& a, int64_t base, int64_t len,
                                                uint32_t (&key)[TI], int32_t (&val)[TI],
