@@ -29,9 +29,14 @@ namespace {
 constexpr int TT = kTileThreads;
 constexpr int TI = kTileItems;
 constexpr int64_t TILE = kTile;
-constexpr int kTileRec = 8;   // doubles per tile: S, X, first, last, then e^{-(first - last)/t}
-                              // (the wide finalize) or the suffix after (v, T) and the prefix
-                              // before (u, S) (the finalize of longer rows)
+// The tile records are stored field by field (kTileRec arrays of max_tiles
+// doubles), so that the lanes of a wave reading the records of neighbouring
+// tiles read neighbouring words: S, X, first, last, then e^{-(first - last)/t}
+// (the wide finalize) or the suffix after (v, T) and the prefix before (u, S)
+// (the finalize of longer rows).
+constexpr int kTileRec = 8;
+static_assert(kTileRec == kSolveTileDoubles, "the caller's tile buffer holds kTileRec arrays");
+enum TileField { kFS = 0, kFX, kFFirst, kFLast, kFSpan, kFAfterV = 4, kFAfterT, kFBeforeU, kFBeforeS };
 
 __device__ __forceinline__ int64_t eff_len(int64_t len, const int64_t* len_dev) {
   if (len_dev == nullptr) return len;
@@ -59,7 +64,8 @@ __device__ int64_t block_max_i64(int64_t v, int64_t* scratch) {
 
 __global__ __launch_bounds__(TT) void solve_tiles_kernel(const uint32_t* __restrict__ keys,
                                                          int64_t len, const int64_t* len_dev,
-                                                         double t, double* __restrict__ tiles) {
+                                                         double t, double* __restrict__ tiles,
+                                                         int64_t mt) {
   const int64_t m = eff_len(len, len_dev);
   const int64_t ntiles = (m + TILE - 1) / TILE;
   const int64_t tile = blockIdx.x;
@@ -112,12 +118,11 @@ __global__ __launch_bounds__(TT) void solve_tiles_kernel(const uint32_t* __restr
       s += red[0][w];
       x += red[1][w];
     }
-    double* rec = tiles + tile * kTileRec;
-    rec[0] = s;
-    rec[1] = x;
-    rec[2] = first;
-    rec[3] = last;
-    rec[4] = wexp_f64(first - last, 1.0 / t);   // the link across the tile
+    tiles[kFS * mt + tile] = s;
+    tiles[kFX * mt + tile] = x;
+    tiles[kFFirst * mt + tile] = first;
+    tiles[kFLast * mt + tile] = last;
+    tiles[kFSpan * mt + tile] = wexp_f64(first - last, 1.0 / t);   // the link across the tile
   }
 }
 
@@ -135,6 +140,8 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
   const int64_t ntiles = (m + TILE - 1) / TILE;
   const Tails x = load_tails(a.tails);
   double* tb = a.tile_buf;
+  const int64_t mt = a.max_tiles;
+  auto F = [&](int f, int64_t q) -> double& { return tb[f * mt + q]; };
 
   Pre pre_all;
   Suf suf_all;
@@ -144,11 +151,10 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
     const bool has = tid < ntiles;
     double S = 0.0, X = 0.0, first = 0.0, last = 0.0;
     if (has) {
-      const double* r = tb + static_cast<int64_t>(tid) * kTileRec;
-      S = r[0];
-      X = r[1];
-      first = r[2];
-      last = r[3];
+      S = F(kFS, tid);
+      X = F(kFX, tid);
+      first = F(kFFirst, tid);
+      last = F(kFLast, tid);
     }
     const Pre mp = has ? Pre{static_cast<float>(last), S} : pre_empty();
     const Suf ms = has ? Suf{static_cast<float>(first), 1.0 + X} : suf_empty();
@@ -177,12 +183,10 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
     Pre mp = pre_empty();
     Suf ms = suf_empty();
     for (int64_t q = t0; q < t1; ++q) {
-      const double* r = tb + q * kTileRec;
-      mp = pre_combine(mp, Pre{static_cast<float>(r[3]), r[0]}, inv_t);
+      mp = pre_combine(mp, Pre{static_cast<float>(F(kFLast, q)), F(kFS, q)}, inv_t);
     }
     for (int64_t q = t1 - 1; q >= t0; --q) {
-      const double* r = tb + q * kTileRec;
-      ms = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, ms, inv_t);
+      ms = suf_combine(Suf{static_cast<float>(F(kFFirst, q)), 1.0 + F(kFX, q)}, ms, inv_t);
     }
     Pre pre_in;
     Suf suf_in;
@@ -193,33 +197,30 @@ __global__ __launch_bounds__(TT) void solve_finalize_kernel(SolveArgs a, double*
     {
       Suf after = suf_in;
       for (int64_t q = t1 - 1; q >= t0; --q) {
-        double* r = tb + q * kTileRec;
-        r[4] = after.v;
-        r[5] = after.T;
-        after = suf_combine(Suf{static_cast<float>(r[2]), 1.0 + r[1]}, after, inv_t);
+        F(kFAfterV, q) = after.v;
+        F(kFAfterT, q) = after.T;
+        after = suf_combine(Suf{static_cast<float>(F(kFFirst, q)), 1.0 + F(kFX, q)}, after, inv_t);
       }
     }
     {
       Pre before = pre_in;
       for (int64_t q = t0; q < t1; ++q) {
-        double* r = tb + q * kTileRec;
-        r[6] = before.u;
-        r[7] = before.S;
-        const double first = r[2];
+        F(kFBeforeU, q) = before.u;
+        F(kFBeforeS, q) = before.S;
+        const double first = F(kFFirst, q);
         double P = 1.0;
         if (before.S != 0.0) P += wexp_f64(static_cast<double>(before.u) - first, inv_t) * before.S;
-        double E = r[1];
-        if (r[5] != 0.0) E += wexp_f64(first - r[4], inv_t) * r[5];
+        double E = F(kFX, q);
+        if (F(kFAfterT, q) != 0.0) E += wexp_f64(first - F(kFAfterV, q), inv_t) * F(kFAfterT, q);
         const double N = x.nR + static_cast<double>(q * TILE) + 1.0 - 0.5 * P + 0.5 * E;
         if (N <= k) below = q + 1;   // non-decreasing: the last such tile
-        before = pre_combine(before, Pre{static_cast<float>(r[3]), r[0]}, inv_t);
+        before = pre_combine(before, Pre{static_cast<float>(F(kFLast, q)), F(kFS, q)}, inv_t);
       }
     }
     below = block_max_i64<WAVES>(below, cnt_s);
     if (below > 0 && tid == 0) {
-      const double* r = tb + (below - 1) * kTileRec;
-      tile_pre_s = Pre{static_cast<float>(r[6]), r[7]};
-      tile_suf_s = Suf{static_cast<float>(r[4]), r[5]};
+      tile_pre_s = Pre{static_cast<float>(F(kFBeforeU, below - 1)), F(kFBeforeS, below - 1)};
+      tile_suf_s = Suf{static_cast<float>(F(kFAfterV, below - 1)), F(kFAfterT, below - 1)};
     }
     __syncthreads();
   }
@@ -285,6 +286,7 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
   const int64_t ntiles = (m + TILE - 1) / TILE;
   const Tails x = load_tails(a.tails);
   const double* tb = a.tile_buf;
+  const int64_t mt = a.max_tiles;
 
   // 1. this thread's run of tiles [t0, t0 + nr)
   const int64_t per = (ntiles + FT - 1) / FT;   // <= kFinPer (checked by the launcher)
@@ -296,14 +298,12 @@ __global__ __launch_bounds__(FT) void solve_finalize_wide_kernel(SolveArgs a, do
 #pragma unroll
   for (int q = 0; q < kFinPer; ++q) {
     const bool on = q < nr;
-    const double* r = tb + (on ? t0 + q : 0) * kTileRec;   // always a record of the buffer
-    const double2 sx = *reinterpret_cast<const double2*>(r);
-    const double2 fl = *reinterpret_cast<const double2*>(r + 2);
-    S[q] = on ? sx.x : 0.0;
-    X[q] = on ? sx.y : 0.0;
-    fst[q] = on ? static_cast<float>(fl.x) : 0.0f;
-    lst[q] = on ? static_cast<float>(fl.y) : 0.0f;
-    span[q] = on ? r[4] : 0.0;
+    const int64_t at = on ? t0 + q : 0;   // always a record of the buffer
+    S[q] = on ? tb[kFS * mt + at] : 0.0;
+    X[q] = on ? tb[kFX * mt + at] : 0.0;
+    fst[q] = on ? static_cast<float>(tb[kFFirst * mt + at]) : 0.0f;
+    lst[q] = on ? static_cast<float>(tb[kFLast * mt + at]) : 0.0f;
+    span[q] = on ? tb[kFSpan * mt + at] : 0.0;
   }
   // links between the run's anchors.  With span_q = e^{-(first_q - last_q)/t}
   // from the tile pass and the gaps L_q = e^{-(last_{q-1} - first_q)/t}
@@ -443,7 +443,7 @@ hipError_t launch_sorted_solve(const SolveArgs& a, hipStream_t s) {
   if (tiles > 0)
     { ProfScope ps_("solve_tiles", s);
     hipLaunchKernelGGL(solve_tiles_kernel, dim3(static_cast<unsigned>(tiles)), dim3(TT), 0, s,
-                       a.keys, a.len, a.len_dev, a.t, a.tile_buf); }
+                       a.keys, a.len, a.len_dev, a.t, a.tile_buf, a.max_tiles); }
   if (tiles > TT && tiles <= static_cast<int64_t>(kFinPer) * FT) {
     { ProfScope ps_("solve_finalize", s);
     hipLaunchKernelGGL(solve_finalize_wide_kernel, dim3(1), dim3(FT), 0, s, a, a.b_out); }
