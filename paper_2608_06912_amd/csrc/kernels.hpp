@@ -169,18 +169,22 @@ hipError_t launch_topk_mask(const int32_t* perm, int64_t batch, int64_t n, int64
 hipError_t launch_emit(const float* r, int64_t n, const double* b_dev, double t, float* p,
                        hipStream_t s);
 
-// Device-wide backward for one row: partial sums per block, one block
-// reducing them in a fixed order to coef[0] = <g, q> and coef[1] = 1/t (0 when
-// sum f == 0), then the emit.  The partials are (sum s, sum s g), or with
-// grad_k / grad_alpha requested (sum s, sum s g, sum s u, sum s g u) with
+// Device-wide backward for one row: partial sums per block, reduced in a
+// fixed order to coef[0] = <g, q> and coef[1] = 1/t (0 when sum f == 0),
+// then the emit.  The partials are (sum s, sum s g), or with grad_k /
+// grad_alpha requested (sum s, sum s g, sum s u, sum s g u) with
 // s = min(p, 1 - p), u = (r - b)/t; partials holds 4 doubles per block.
-// grad_k / grad_alpha: one float64 each (may be null).
+// grad_k / grad_alpha: one float64 each (may be null).  With many partials
+// one block combines them into coef (launched by launch_vjp_reduce); with
+// few, every emit block combines them itself and coef is not used.  Both
+// calls take the same nblocks / nparts and grad_k / grad_alpha.
 int vjp_reduce_blocks(int64_t n);
 hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
                              int nblocks, double t, double* coef, double* grad_k,
                              double* grad_alpha, hipStream_t s);
 hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* coef,
-                           float* grad, hipStream_t s);
+                           const double* partials, int nparts, double t, double* grad_k,
+                           double* grad_alpha, float* grad, hipStream_t s);
 
 // Device-wide stable LSD radix sort (descending float order) of one array.
 // Source: floats (converted to keys) or keys; values: none, the source

@@ -750,7 +750,9 @@ int lapsum_backward(const float* grad_p, const float* p, const double* b, int64_
     LAPSUM_TRY(launch_vjp_reduce(grad_p + o, p + o, n, partials, nb, t, coef,
                                  grad_k ? grad_k + row : nullptr,
                                  grad_alpha ? grad_alpha + row : nullptr, stream));
-    LAPSUM_TRY(launch_vjp_emit(grad_p + o, p + o, n, coef, grad_r + o, stream));
+    LAPSUM_TRY(launch_vjp_emit(grad_p + o, p + o, n, coef, partials, nb, t,
+                               grad_k ? grad_k + row : nullptr,
+                               grad_alpha ? grad_alpha + row : nullptr, grad_r + o, stream));
   }
   return LAPSUM_OK;
 }

@@ -271,18 +271,12 @@ __global__ __launch_bounds__(kStreamThreads, 4) void vjp_reduce_kernel(const flo
   }
 }
 
-// One block: sum the partials in a fixed order and store
-// coef = <g, q> = sum f g / sum f and scale = 1/t (both 0 when sum f == 0);
-// with PARAMS also dL/dk = <g, q> and dL/dalpha = (H - (U/F) G)/t.
-template <bool PARAMS>
-__global__ __launch_bounds__(1024) void vjp_finalize_kernel(const double* __restrict__ partials,
-                                                            int nparts, double inv_t,
-                                                            double* __restrict__ coef,
-                                                            double* __restrict__ grad_k,
-                                                            double* __restrict__ grad_alpha) {
-  constexpr int T = 1024;
-  constexpr int NS = PARAMS ? 4 : 2;
-  __shared__ double red[NS][T / kWave];
+// The partials summed in a fixed order by one block of T threads (thread
+// tid takes partials tid, tid + T, ..., then the waves in order); thread 0
+// returns the totals.
+template <int NS, int T>
+__device__ void vjp_totals(const double* __restrict__ partials, int nparts,
+                           double (&red)[NS][T / kWave], double (&tot)[NS]) {
   const int tid = threadIdx.x;
   double acc[NS];
 #pragma unroll
@@ -299,23 +293,47 @@ __global__ __launch_bounds__(1024) void vjp_finalize_kernel(const double* __rest
     for (int q = 0; q < NS; ++q) red[q][wid] = acc[q];
   }
   __syncthreads();
-  if (tid == 0) {
-    double tot[NS];
 #pragma unroll
-    for (int q = 0; q < NS; ++q) {
-      tot[q] = 0.0;
+  for (int q = 0; q < NS; ++q) {
+    tot[q] = 0.0;
 #pragma unroll
-      for (int w = 0; w < T / kWave; ++w) tot[q] += red[q][w];
-    }
-    const double f = tot[0], gg = tot[1];
-    coef[0] = (f > 0.0) ? gg / f : 0.0;
-    coef[1] = (f > 0.0) ? inv_t : 0.0;
-    if constexpr (PARAMS) {
-      if (grad_k) *grad_k = coef[0];
-      if (grad_alpha) *grad_alpha = (f > 0.0) ? (tot[3] - (tot[2] / f) * gg) * inv_t : 0.0;
-    }
+    for (int w = 0; w < T / kWave; ++w) tot[q] += red[q][w];
   }
 }
+
+// From the totals: coef = <g, q> = sum f g / sum f and scale = 1/t (both 0
+// when sum f == 0); with PARAMS also dL/dk = <g, q> and
+// dL/dalpha = (H - (U/F) G)/t (either output may be null).
+template <bool PARAMS, int NS>
+__device__ void vjp_coefs(const double (&tot)[NS], double inv_t, double* coef, double* grad_k,
+                          double* grad_alpha) {
+  const double f = tot[0], gg = tot[1];
+  coef[0] = (f > 0.0) ? gg / f : 0.0;
+  coef[1] = (f > 0.0) ? inv_t : 0.0;
+  if constexpr (PARAMS) {
+    if (grad_k) *grad_k = coef[0];
+    if (grad_alpha) *grad_alpha = (f > 0.0) ? (tot[3] - (tot[2] / f) * gg) * inv_t : 0.0;
+  }
+}
+
+// One block: the coefficients of the emit from the partials of a long row.
+template <bool PARAMS>
+__global__ __launch_bounds__(1024) void vjp_finalize_kernel(const double* __restrict__ partials,
+                                                            int nparts, double inv_t,
+                                                            double* __restrict__ coef,
+                                                            double* __restrict__ grad_k,
+                                                            double* __restrict__ grad_alpha) {
+  constexpr int T = 1024;
+  constexpr int NS = PARAMS ? 4 : 2;
+  __shared__ double red[NS][T / kWave];
+  double tot[NS];
+  vjp_totals<NS, T>(partials, nparts, red, tot);
+  if (threadIdx.x == 0) vjp_coefs<PARAMS, NS>(tot, inv_t, coef, grad_k, grad_alpha);
+}
+
+// Rows whose reduce leaves at most this many partials skip the finalize:
+// every emit block sums them itself (at most 4 KB each).
+constexpr int kFoldParts = 256;
 
 hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* partials,
                              int nblocks, double t, double* coef, double* grad_k,
@@ -330,6 +348,7 @@ hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* 
                        n, partials); }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (nblocks <= kFoldParts) return hipSuccess;   // the emit combines the partials
   { ProfScope ps_("vjp_finalize", s);
   if (params)
     hipLaunchKernelGGL(vjp_finalize_kernel<true>, dim3(1), dim3(1024), 0, s, partials, nblocks,
@@ -347,14 +366,34 @@ hipError_t launch_vjp_reduce(const float* g, const float* p, int64_t n, double* 
 // next pass reads, while a shorter row's stay in the last-level cache.
 constexpr int64_t kNtStoreMin = int64_t(1) << 24;
 
-template <bool NT>
+// FOLD: coef comes from the reduce partials, summed by every block in the
+// same order (block 0 also stores the parameter gradients); otherwise from
+// the finalize.
+template <bool NT, bool FOLD, bool PARAMS>
 __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* __restrict__ g,
                                                                   const float* __restrict__ p,
                                                                   int64_t n,
                                                                   const double* __restrict__ coef2,
+                                                                  const double* __restrict__ partials,
+                                                                  int nparts, double inv_t,
+                                                                  double* __restrict__ grad_k,
+                                                                  double* __restrict__ grad_alpha,
                                                                   float* __restrict__ grad) {
-  const float coef = static_cast<float>(coef2[0]);
-  const float scale = static_cast<float>(coef2[1]);
+  float coef, scale;
+  if constexpr (FOLD) {
+    constexpr int NS = PARAMS ? 4 : 2;
+    __shared__ double red[NS][kStreamThreads / kWave];
+    double tot[NS];
+    vjp_totals<NS, kStreamThreads>(partials, nparts, red, tot);
+    double c[2];
+    vjp_coefs<PARAMS, NS>(tot, inv_t, c, blockIdx.x == 0 && threadIdx.x == 0 ? grad_k : nullptr,
+                          blockIdx.x == 0 && threadIdx.x == 0 ? grad_alpha : nullptr);
+    coef = static_cast<float>(c[0]);
+    scale = static_cast<float>(c[1]);
+  } else {
+    coef = static_cast<float>(coef2[0]);
+    scale = static_cast<float>(coef2[1]);
+  }
   const int tid = threadIdx.x;
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kStreamTile;
   const bool vec =
@@ -393,15 +432,27 @@ __global__ __launch_bounds__(kStreamThreads) void vjp_emit_kernel(const float* _
 }
 
 hipError_t launch_vjp_emit(const float* g, const float* p, int64_t n, const double* coef,
-                           float* grad, hipStream_t s) {
+                           const double* partials, int nparts, double t, double* grad_k,
+                           double* grad_alpha, float* grad, hipStream_t s) {
   const int64_t blocks = (n + kStreamTile - 1) / kStreamTile;
+  const dim3 grid(static_cast<unsigned>(blocks)), block(kStreamThreads);
+  const double inv_t = 1.0 / t;
+  const bool params = grad_k || grad_alpha;
   { ProfScope ps_("vjp_emit", s);
-  if (n >= kNtStoreMin)
-    hipLaunchKernelGGL(vjp_emit_kernel<true>, dim3(static_cast<unsigned>(blocks)),
-                       dim3(kStreamThreads), 0, s, g, p, n, coef, grad);
-  else
-    hipLaunchKernelGGL(vjp_emit_kernel<false>, dim3(static_cast<unsigned>(blocks)),
-                       dim3(kStreamThreads), 0, s, g, p, n, coef, grad); }
+  if (nparts > kFoldParts) {
+    if (n >= kNtStoreMin)
+      hipLaunchKernelGGL((vjp_emit_kernel<true, false, false>), grid, block, 0, s, g, p, n, coef,
+                         partials, nparts, inv_t, grad_k, grad_alpha, grad);
+    else
+      hipLaunchKernelGGL((vjp_emit_kernel<false, false, false>), grid, block, 0, s, g, p, n, coef,
+                         partials, nparts, inv_t, grad_k, grad_alpha, grad);
+  } else if (params) {
+    hipLaunchKernelGGL((vjp_emit_kernel<false, true, true>), grid, block, 0, s, g, p, n, coef,
+                       partials, nparts, inv_t, grad_k, grad_alpha, grad);
+  } else {
+    hipLaunchKernelGGL((vjp_emit_kernel<false, true, false>), grid, block, 0, s, g, p, n, coef,
+                       partials, nparts, inv_t, grad_k, grad_alpha, grad);
+  } }
   return hipGetLastError();
 }
 
