@@ -819,11 +819,13 @@ def test_workload_n1e7_full_sort(lib):
     assert grad_rel(grad, O.vjp(r[0], b_ref, w.alpha, g[0])) <= G_TOL
 
 
-@pytest.mark.parametrize("n,dup", [((1 << 20) + 1, 0.01), (3_000_000, 0.02)])
+@pytest.mark.parametrize("n,dup", [(384 * 1024, 0.01), (384 * 1024 + 1, 0.01), (1 << 20, 0.01),
+                                   ((1 << 20) + 1, 0.01), (3_000_000, 0.02)])
 def test_devicewide_permutation_above_on_chip_tiles(lib, n, dup):
-    """Rows past 2^20 keys take the sort's 4096-key tiles; with indices and
-    injected duplicates (equal keys ordered by ascending index) the order
-    must equal the oracle's stable argsort exactly."""
+    """The device-wide sort's tiles grow with the row: 1024 keys up to
+    393216, 2048 up to 2^20, 4096 above (both sides of each switch here).
+    With indices and injected duplicates (equal keys ordered by ascending
+    index) the order must equal the oracle's stable argsort exactly."""
     rng = np.random.default_rng([61, n])
     r = rng.standard_normal(n).astype(np.float32)
     nd = int(dup * n)
