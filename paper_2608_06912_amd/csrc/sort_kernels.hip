@@ -236,15 +236,34 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
   const int64_t base = tile * TILE;
   const bool full = base + TILE <= len;
 
-  // the tile's keys first, so that their latency overlaps the digit bases
+  // the tile's raw words first, so that their latency overlaps the digit
+  // bases; keys are formed from them (floats, and the sentinel past the end)
+  // only after that.  Forming each key right after its own load made every
+  // load wait for the previous one in the pass from floats.  Full tiles need
+  // no bounds.
+  const bool from_f = a.src_f != nullptr;
   uint32_t key[TI];
   int32_t val[TI];
+  {
+    const uint32_t* src = from_f ? reinterpret_cast<const uint32_t*>(a.src_f) : a.src_k;
+    if (full) {
+      const uint32_t* ts = src + base;
 #pragma unroll
-  for (int i = 0; i < TI; ++i) {
-    const int64_t gp = base + tile_pos<TI>(i);
-    const bool valid = gp < len;
-    key[i] = valid ? load_key(a, gp) : 0xffffffffu;
-    if constexpr (PAIRS) val[i] = valid ? (a.src_v ? a.src_v[gp] : static_cast<int32_t>(gp)) : -1;
+      for (int i = 0; i < TI; ++i) key[i] = ts[tile_pos<TI>(i)];
+    } else {
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const int64_t gp = base + tile_pos<TI>(i);
+        key[i] = gp < len ? src[gp] : 0u;
+      }
+    }
+    if constexpr (PAIRS) {
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const int64_t gp = base + tile_pos<TI>(i);
+        val[i] = gp < len ? (a.src_v ? a.src_v[gp] : static_cast<int32_t>(gp)) : -1;
+      }
+    }
   }
 
   // digit base over the whole array: exclusive prefix of totals over digits
@@ -284,6 +303,18 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
     off[tid] = wbase + incl - tot + before_tile;
   }
   for (int e = tid; e < cnt_words<TW>(); e += TT) cnt[e] = 0u;
+  if (full) {
+    if (from_f) {
+#pragma unroll
+      for (int i = 0; i < TI; ++i) key[i] = desc_key(__uint_as_float(key[i]));
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TI; ++i) {
+      const bool valid = base + tile_pos<TI>(i) < len;
+      key[i] = !valid ? 0xffffffffu : (from_f ? desc_key(__uint_as_float(key[i])) : key[i]);
+    }
+  }
   __syncthreads();
   if (full)
     downsweep_tile<TI, PAIRS, true>(a, base, len, key, val, cnt, wave_tot, off, buf, dg);
