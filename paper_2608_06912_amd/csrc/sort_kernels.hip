@@ -100,10 +100,18 @@ __global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
       }
     }
   } else {
+    // a source not 16-byte aligned (a row of a batch whose length is not a
+    // multiple of 4): one word per load, all issued before any key is formed
+    const uint32_t* sw = static_cast<const uint32_t*>(src);
+    uint32_t w[TI];
 #pragma unroll
     for (int i = 0; i < TI; ++i) {
       const int64_t pos = base + tile_pos<TI>(i);
-      if (pos < len) count(load_key(a, pos));
+      w[i] = sw[pos < len ? pos : base];
+    }
+#pragma unroll
+    for (int i = 0; i < TI; ++i) {
+      if (base + tile_pos<TI>(i) < len) count(a.src_f ? desc_key(__uint_as_float(w[i])) : w[i]);
     }
   }
   __syncthreads();

@@ -259,6 +259,25 @@ def test_devicewide_forward_matches_oracle(lib, n, dist, k, alpha):
     assert np.array_equal(_np(perm), O.desc_order(r))
 
 
+@pytest.mark.parametrize("n", [40001, 400003])
+def test_devicewide_batch_of_unaligned_rows(lib, n):
+    """A batch of long rows of odd length: every row after the first starts
+    off the 16-byte alignment the sort's counting pass reads with, so those
+    rows take its one-word path; each row's permutation, p, b and backward
+    against the oracle."""
+    batch = 3
+    r = np.stack([W.random_case(n % 89 + i, n, dist="normal", ties=0.02)[0] for i in range(batch)])
+    g = np.random.default_rng([11, n]).standard_normal((batch, n)).astype(np.float32)
+    k, alpha = n / 50.0, -0.1
+    p, b, perm = lib.lapsum_forward(_t(r), k, alpha, perm=True)
+    grad = _np(lib.lapsum_backward(_t(g), p, b, alpha))
+    for i in range(batch):
+        assert np.array_equal(_np(perm)[i], O.desc_order(r[i])), f"row {i} permutation"
+        check_row(r[i], k, alpha, _np(p)[i], float(_np(b)[i]), f"row {i}")
+        ref = O.vjp(r[i], O.solve_sorted_scan(r[i], k, alpha), alpha, g[i])
+        assert grad_rel(grad[i], ref) <= G_TOL, f"row {i} grad"
+
+
 def test_devicewide_n1e6(lib):
     w = W.get("n1e6")
     r = W.scores("n1e6")
