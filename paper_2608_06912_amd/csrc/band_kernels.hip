@@ -511,17 +511,27 @@ __global__ __launch_bounds__(BT) void band_vjp_reduce_kernel(const float* __rest
           float4 pv[VU];
 #pragma unroll
           for (int u = 0; u < VU; ++u) pv[u] = load_stream4(p + i + 4 * kWave * u);
+          // every g load of the batch is issued before any is used: a lane
+          // that needs none reads the block's first float4 instead (one
+          // line for all such lanes), so that no load sits in a branch that
+          // the compiler would fill with its use (a load followed by its use
+          // made the next load wait for it)
+          float4 gv[VU];
+          bool need[VU];
 #pragma unroll
           for (int u = 0; u < VU; ++u) {
             const float4 q = pv[u];
-            const bool need = (fminf(q.x, 1.0f - q.x) + fminf(q.y, 1.0f - q.y)) +
-                                  (fminf(q.z, 1.0f - q.z) + fminf(q.w, 1.0f - q.w)) != 0.0f;
-            if (need) {
-              const float4 gv = load_stream4(g + i + 4 * kWave * u);
-              add(q.x, gv.x);
-              add(q.y, gv.y);
-              add(q.z, gv.z);
-              add(q.w, gv.w);
+            need[u] = (fminf(q.x, 1.0f - q.x) + fminf(q.y, 1.0f - q.y)) +
+                          (fminf(q.z, 1.0f - q.z) + fminf(q.w, 1.0f - q.w)) != 0.0f;
+            gv[u] = load_stream4(need[u] ? g + i + 4 * kWave * u : g + br.b0);
+          }
+#pragma unroll
+          for (int u = 0; u < VU; ++u) {
+            if (need[u]) {
+              add(pv[u].x, gv[u].x);
+              add(pv[u].y, gv[u].y);
+              add(pv[u].z, gv[u].z);
+              add(pv[u].w, gv[u].w);
             }
           }
         }
