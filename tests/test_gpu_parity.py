@@ -838,6 +838,31 @@ def test_workload_n1e7_full_sort(lib):
     assert grad_rel(grad, O.vjp(r[0], b_ref, w.alpha, g[0])) <= G_TOL
 
 
+@pytest.mark.timeout(600)
+def test_devicewide_rows_past_the_wide_finalize(lib):
+    """A full-sort row of more than 4096 sorted tiles (17M keys: the size a
+    bracketed row of the n1e8 kind reaches when it falls back to the full
+    sort) takes the finalize that walks each thread's run of tile records
+    field by field: b against the oracle's closed form (certified by sign
+    change), every p, the budget and the backward."""
+    n = 17_000_003
+    rg = np.random.default_rng([77, n])
+    r = (rg.standard_normal(n) + rg.laplace(0.0, 0.05, n)).astype(np.float32)[None, :]
+    k, alpha = 3400.0, -0.01
+    p, b = lib.lapsum_forward(_t(r), k, alpha)
+    b_ref = O.solve_sorted_scan(r[0], k, alpha)
+    assert O.certify_root(r[0], k, alpha, b_ref, 1e-7 * 0.01)
+    bg = float(_np(b)[0])
+    assert abs(bg - b_ref) <= 2e-6 * 0.01, (bg, b_ref)
+    pg = _np(p)[0]
+    _full_p_check(pg, r[0], b_ref, alpha, "17M full")
+    assert O.budget_error(pg, k) <= sum_tol(k)
+    g = rg.standard_normal((1, n)).astype(np.float32)
+    grad = _np(lib.lapsum_backward(_t(g), p, b, alpha))[0]
+    assert grad_rel(grad, O.vjp(r[0], b_ref, alpha, g[0])) <= G_TOL
+    print("17M full sort: b, p and grad checked", flush=True)
+
+
 @pytest.mark.parametrize("n,dup", [(384 * 1024, 0.01), (384 * 1024 + 1, 0.01), (1 << 20, 0.01),
                                    ((1 << 20) + 1, 0.01), (3_000_000, 0.02)])
 def test_devicewide_permutation_above_on_chip_tiles(lib, n, dup):
