@@ -105,7 +105,7 @@ int lapsum_forward(const float* scores, int64_t batch, int64_t n, double k,
  *   LAPSUM_ERR_WORKSPACE when lapsum_forward_workspace_size(batch, n,
  *   perm_out != NULL) exceeds LAPSUM_NOALLOC_SCRATCH_BYTES (rows of up to
  *   32768 scores need none; one long row fits up to 3,943,808 scores with
- *   perm_out and 7,443,456 without).
+ *   perm_out and 7,443,072 without).
  * All calls on one GPU share its array: calls that overlap in time on one
  * GPU (different streams, or host threads) race and must not be issued.
  * ------------------------------------------------------------------------ */

@@ -56,69 +56,97 @@ __device__ __forceinline__ int tile_pos(int i) {
 
 }  // namespace
 
-template <int TI>
-__global__ __launch_bounds__(TT) void sort_upsweep_kernel(PassArgs a) {
+// Per-tile digit counts (the order is the downsweep's): one LDS atomic per
+// key on counters of its own wave, cheaper than matching the digit across
+// the wave (36 -> 22 us per pass over 1e7 keys).  Counting does not depend on
+// which thread holds which key, so the keys are read four at a time (16-byte
+// loads: 17 -> 12 us per pass over 1e7 keys in a probe).
+//   TPB  tiles per block, one group of TT threads each.  With four, each
+//        digit's four counts leave as one 16-byte store: the histogram is
+//        digit-major, so one count per tile is a scattered 4-byte store
+//        (14.1 -> 11.5 us per pass over 1e7 spread digits).
+//   QS   counter sets per wave.  The leading digit of float keys takes few
+//        values, and lanes adding to one LDS address are served one after
+//        another; with a set per quarter wave a hot digit spreads over four
+//        addresses (25.1 -> 19.2 us on the leading digit of 1e7 exponential
+//        keys, +0.6 us on spread digits).
+template <int TI, int TPB, int QS>
+__global__ __launch_bounds__(TT * TPB) void sort_upsweep_kernel(PassArgs a) {
   constexpr int64_t TILE = static_cast<int64_t>(TT) * TI;
+  constexpr int SETS = TW * QS;
   const int64_t len = eff_len(a);
   const int64_t ntiles = (len + TILE - 1) / TILE;
-  const int64_t tile = blockIdx.x;
-  if (tile >= ntiles) return;
-  __shared__ uint32_t cnt[cnt_words<TW>()];
+  const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * TPB;
+  if (tile0 >= ntiles) return;
+  __shared__ uint32_t cnt[TPB][cnt_words<SETS>()];
   const int tid = threadIdx.x;
-  const int wid = tid / kWave;
-  for (int e = tid; e < cnt_words<TW>(); e += TT) cnt[e] = 0u;
+  const int grp = tid / TT;
+  const int gt = tid % TT;
+  const int lane = lane_id();
+  const int set = (gt / kWave) * QS + lane / (kWave / QS);
+  for (int e = tid; e < TPB * cnt_words<SETS>(); e += TT * TPB) (&cnt[0][0])[e] = 0u;
   __syncthreads();
+  const int64_t tile = tile0 + grp;
   const int64_t base = tile * TILE;
-  // counts only (the order is the downsweep's): one LDS atomic per key on
-  // the wave's own counters is cheaper than matching the digit across the
-  // wave (measured: 36 -> 22 us per pass over 1e7 keys).  Counting does not
-  // depend on which thread holds which key, so the keys are read four at a
-  // time (16-byte loads: 17 -> 12 us per pass over 1e7 keys in a probe)
   const void* src = a.src_f ? static_cast<const void*>(a.src_f) : static_cast<const void*>(a.src_k);
-  const bool vec = (reinterpret_cast<uintptr_t>(src) & 15) == 0;
-  auto count = [&](uint32_t key) { atomicAdd(&cnt[cnt_at<TW>((key >> a.shift) & 255u, wid)], 1u); };
-  if (vec) {
-    constexpr int V = TI / 4;
-    static_assert(TI % 4 == 0, "four keys per load");
-    uint4 q[V];
+  uint32_t* c = cnt[grp];
+  auto count = [&](uint32_t key) { atomicAdd(&c[cnt_at<SETS>((key >> a.shift) & 255u, set)], 1u); };
+  if (tile < ntiles) {
+    const bool vec = (reinterpret_cast<uintptr_t>(src) & 15) == 0;
+    if (vec) {
+      constexpr int V = TI / 4;
+      static_assert(TI % 4 == 0, "four keys per load");
+      uint4 q[V];
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
-      const int64_t at = base + 4 * (static_cast<int64_t>(j) * TT + tid);
-      q[j] = at + 3 < len ? *reinterpret_cast<const uint4*>(static_cast<const uint32_t*>(src) + at)
-                          : make_uint4(0u, 0u, 0u, 0u);
-    }
-#pragma unroll
-    for (int j = 0; j < V; ++j) {
-      const int64_t at = base + 4 * (static_cast<int64_t>(j) * TT + tid);
-      if (at + 3 < len) {
-        const uint32_t w[4] = {q[j].x, q[j].y, q[j].z, q[j].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) count(a.src_f ? desc_key(__uint_as_float(w[e])) : w[e]);
-      } else {
-        for (int e = 0; e < 4; ++e)
-          if (at + e < len) count(load_key(a, at + e));
+      for (int j = 0; j < V; ++j) {
+        const int64_t at = base + 4 * (static_cast<int64_t>(j) * TT + gt);
+        q[j] = at + 3 < len ? *reinterpret_cast<const uint4*>(static_cast<const uint32_t*>(src) + at)
+                            : make_uint4(0u, 0u, 0u, 0u);
       }
-    }
-  } else {
-    // a source not 16-byte aligned (a row of a batch whose length is not a
-    // multiple of 4): one word per load, all issued before any key is formed
-    const uint32_t* sw = static_cast<const uint32_t*>(src);
-    uint32_t w[TI];
 #pragma unroll
-    for (int i = 0; i < TI; ++i) {
-      const int64_t pos = base + tile_pos<TI>(i);
-      w[i] = sw[pos < len ? pos : base];
-    }
+      for (int j = 0; j < V; ++j) {
+        const int64_t at = base + 4 * (static_cast<int64_t>(j) * TT + gt);
+        if (at + 3 < len) {
+          const uint32_t w[4] = {q[j].x, q[j].y, q[j].z, q[j].w};
 #pragma unroll
-    for (int i = 0; i < TI; ++i) {
-      if (base + tile_pos<TI>(i) < len) count(a.src_f ? desc_key(__uint_as_float(w[i])) : w[i]);
+          for (int e = 0; e < 4; ++e) count(a.src_f ? desc_key(__uint_as_float(w[e])) : w[e]);
+        } else {
+          for (int e = 0; e < 4; ++e)
+            if (at + e < len) count(load_key(a, at + e));
+        }
+      }
+    } else {
+      // a source not 16-byte aligned (a row of a batch whose length is not
+      // a multiple of 4): one word per load, all issued before any key is
+      // formed
+      const uint32_t* sw = static_cast<const uint32_t*>(src);
+      uint32_t w[TI];
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const int64_t pos = base + i * TT + gt;
+        w[i] = sw[pos < len ? pos : base];
+      }
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        if (base + i * TT + gt < len) count(a.src_f ? desc_key(__uint_as_float(w[i])) : w[i]);
+      }
     }
   }
   __syncthreads();
-  uint32_t sum = 0;
+  if (tid < 256) {
+    uint32_t sum[TPB];
 #pragma unroll
-  for (int w = 0; w < TW; ++w) sum += cnt[cnt_at<TW>(tid, w)];
-  a.hist[static_cast<int64_t>(tid) * a.max_tiles + tile] = sum;
+    for (int g = 0; g < TPB; ++g) {
+      sum[g] = 0u;
+#pragma unroll
+      for (int w = 0; w < SETS; ++w) sum[g] += cnt[g][cnt_at<SETS>(tid, w)];
+    }
+    uint32_t* h = a.hist + static_cast<int64_t>(tid) * a.max_tiles + tile0;
+    if constexpr (TPB == 4)
+      *reinterpret_cast<uint4*>(h) = make_uint4(sum[0], sum[1], sum[2], sum[3]);   // max_tiles % 4 == 0
+    else
+      h[0] = sum[0];
+  }
 }
 
 // One block per digit: exclusive prefix of hist[d][0..ntiles) in place.
@@ -330,15 +358,15 @@ __global__ __launch_bounds__(TT) void sort_downsweep_kernel(PassArgs a) {
     downsweep_tile<TI, PAIRS, false>(a, base, len, key, val, cnt, wave_tot, off, buf, dg);
 }
 
-size_t sort_hist_words(int64_t len) {
-  // sized for the smaller tile
+int64_t sort_max_tiles(int64_t len) {
+  // sized for the smallest tile, a multiple of 4 so that every histogram row
+  // is 16-byte aligned for the four-tile counting blocks
   const int64_t tiles = (len + 1023) / 1024;
-  return static_cast<size_t>(256) * static_cast<size_t>(tiles < 1 ? 1 : tiles);
+  return ((tiles < 1 ? 1 : tiles) + 3) / 4 * 4;
 }
 
-int64_t sort_max_tiles(int64_t len) {
-  const int64_t tiles = (len + 1023) / 1024;
-  return tiles < 1 ? 1 : tiles;
+size_t sort_hist_words(int64_t len) {
+  return static_cast<size_t>(256) * static_cast<size_t>(sort_max_tiles(len));
 }
 
 namespace {
@@ -356,6 +384,11 @@ hipError_t sort_passes(const float* src_f, const uint32_t* src_k, const int32_t*
   const int32_t* cur_v = src_v;
   const float* cur_f = src_f;
   int nxt = 0;
+  // the leading digit that varies: the one whose values crowd onto a few
+  // counters (the sign and exponent bits of float keys)
+  int lead = 0;
+  for (int pass = 1; pass < 4; ++pass)
+    if (pass_mask & (1u << pass)) lead = pass;
   for (int pass = 0; pass < 4; ++pass) {
     if (!(pass_mask & (1u << pass)) && cur_f == nullptr) continue;   // digit shared by all keys
     PassArgs a{};
@@ -370,8 +403,19 @@ hipError_t sort_passes(const float* src_f, const uint32_t* src_k, const int32_t*
     a.src_v = cur_v;
     a.dst_k = sb.keys[nxt];
     a.dst_v = with_vals ? sb.vals[nxt] : nullptr;
-    { ProfScope ps_("sort_upsweep", s);
-    hipLaunchKernelGGL((sort_upsweep_kernel<TI>), dim3(grid), dim3(TT), 0, s, a); }
+    {
+      ProfScope ps_("sort_upsweep", s);
+      bool four = false;   // four tiles per block: only with enough blocks to fill the device
+      if constexpr (TI == 16) four = pass != lead && tiles >= 1024;
+      if (pass == lead)
+        hipLaunchKernelGGL((sort_upsweep_kernel<TI, 1, 4>), dim3(grid), dim3(TT), 0, s, a);
+      else if (four) {
+        if constexpr (TI == 16)
+          hipLaunchKernelGGL((sort_upsweep_kernel<TI, 4, 1>), dim3(static_cast<unsigned>((tiles + 3) / 4)),
+                             dim3(4 * TT), 0, s, a);
+      } else
+        hipLaunchKernelGGL((sort_upsweep_kernel<TI, 1, 1>), dim3(grid), dim3(TT), 0, s, a);
+    }
     if (!fused) {
       ProfScope ps_("sort_scan", s);
       hipLaunchKernelGGL((sort_scan_kernel<TI>), dim3(256), dim3(TT), 0, s, a);
