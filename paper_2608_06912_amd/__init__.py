@@ -141,20 +141,36 @@ def _torch():
     return _torch_mod
 
 
+_get_device = None
+
+
+def _current_device() -> int:
+    """The current HIP device index.  torch's raw query skips the lazy-init
+    check of torch.cuda.current_device(); every caller already holds a
+    tensor on the device, so initialisation has happened."""
+    global _get_device
+    if _get_device is None:
+        torch = _torch()
+        _get_device = getattr(torch._C, "_cuda_getDevice", None) or torch.cuda.current_device
+    return _get_device()
+
+
 class _on_device:
-    """Make `device` current for a call (a no-op when it already is)."""
+    """Make `device` current for a call (a no-op when it already is, or when
+    the device names no index, which means the current one)."""
 
     __slots__ = ("dev", "prev")
 
     def __init__(self, device):
-        self.dev = device.index if device.index is not None else _torch().cuda.current_device()
+        self.dev = device.index
         self.prev = None
 
     def __enter__(self):
-        cur = _torch().cuda.current_device()
-        if cur != self.dev:
-            self.prev = cur
-            _torch().cuda.set_device(self.dev)
+        if self.dev is not None:
+            cur = _current_device()
+            if cur != self.dev:
+                self.prev = cur
+                _torch().cuda.set_device(self.dev)
         return self
 
     def __exit__(self, *exc):
@@ -165,6 +181,13 @@ class _on_device:
 
 def _rows(x, name):
     torch = _torch()
+    # the common case in one test; the checks below say what is wrong
+    if type(x) is torch.Tensor and x.is_cuda and x.dtype is torch.float32 and x.is_contiguous():
+        shape = x.shape
+        if len(shape) == 2:
+            return shape[0], shape[1]
+        if len(shape) == 1:
+            return 1, shape[0]
     if not isinstance(x, torch.Tensor) or x.device.type != "cuda":
         raise ValueError(f"{name} must be a CUDA (HIP) tensor")
     if x.dtype != torch.float32:
@@ -181,18 +204,19 @@ _raw_stream = None
 
 
 def _stream(device):
-    """The caller's current HIP stream on `device` as a raw handle.  torch's
-    raw-handle query (0.14 us a call on MI355X) skips building a Stream
-    object (2.0 us), which shows on short rows; the public query is the
-    fallback where the raw one is missing."""
+    """The caller's current HIP stream on `device` as a raw handle (an int,
+    which ctypes passes as a pointer).  torch's raw-handle query (0.14 us a
+    call on MI355X) skips building a Stream object (2.0 us), which shows on
+    short rows; the public query is the fallback where the raw one is
+    missing."""
     global _raw_stream
     torch = _torch()
     if _raw_stream is None:
         _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", False)
     if _raw_stream:
-        idx = device.index if device.index is not None else torch.cuda.current_device()
-        return ctypes.c_void_p(_raw_stream(idx))
-    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+        idx = device.index
+        return _raw_stream(idx if idx is not None else _current_device())
+    return torch.cuda.current_stream(device).cuda_stream
 
 
 def _workspace(nbytes, device, workspace):
@@ -209,7 +233,9 @@ def _workspace(nbytes, device, workspace):
 
 
 def _ptr(t):
-    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+    # an int (or None for NULL): ctypes converts both for a c_void_p argument
+    # without building a c_void_p object per pointer
+    return t.data_ptr() if t is not None else None
 
 
 def lapsum_forward_workspace_size(batch: int, n: int, with_perm: bool = False) -> int:
