@@ -259,12 +259,15 @@ def test_devicewide_forward_matches_oracle(lib, n, dist, k, alpha):
     assert np.array_equal(_np(perm), O.desc_order(r))
 
 
-@pytest.mark.parametrize("n", [40001, 400003])
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("n", [40001, 400003, 4_200_003])
 def test_devicewide_batch_of_unaligned_rows(lib, n):
     """A batch of long rows of odd length: every row after the first starts
     off the 16-byte alignment the sort's counting pass reads with, so those
     rows take its one-word path; each row's permutation, p, b and backward
-    against the oracle."""
+    against the oracle.  At 4.2e6 keys a row has 1026 tiles of 4096: the
+    counting pass then takes four tiles per block (a last block with two)
+    and the scan over tiles holds eight counts per thread."""
     batch = 3
     r = np.stack([W.random_case(n % 89 + i, n, dist="normal", ties=0.02)[0] for i in range(batch)])
     g = np.random.default_rng([11, n]).standard_normal((batch, n)).astype(np.float32)
