@@ -64,12 +64,13 @@ __device__ __forceinline__ int tile_pos(int i) {
 //   TPB  tiles per block, one group of TT threads each.  With four, each
 //        digit's four counts leave as one 16-byte store: the histogram is
 //        digit-major, so one count per tile is a scattered 4-byte store
-//        (14.1 -> 11.5 us per pass over 1e7 spread digits).
+//        (12.1 -> 11.4 us per pass over 1e7 spread digits; 60 -> 45 MB of
+//        HBM traffic).
 //   QS   counter sets per wave.  The leading digit of float keys takes few
 //        values, and lanes adding to one LDS address are served one after
 //        another; with a set per quarter wave a hot digit spreads over four
-//        addresses (25.1 -> 19.2 us on the leading digit of 1e7 exponential
-//        keys, +0.6 us on spread digits).
+//        addresses (22.9 -> 17.2 us on the leading digit of 1e7 |Laplace|
+//        keys; on spread digits it costs 0.6 us, so only that pass uses it).
 template <int TI, int TPB, int QS>
 __global__ __launch_bounds__(TT * TPB) void sort_upsweep_kernel(PassArgs a) {
   constexpr int64_t TILE = static_cast<int64_t>(TT) * TI;
@@ -201,8 +202,8 @@ __global__ __launch_bounds__(TT) void sort_scan_kernel(PassArgs a) {
 // holds tiles C tid .. C tid + C - 1, read and written as 16-byte groups
 // (histogram rows are 16-byte aligned and padded to a multiple of 4 tiles;
 // entries past ntiles are read as zero and written with values nobody
-// reads).  Looping over rounds of 1024 tiles made each round wait for its
-// loads: 5.1 us per pass at 2442 tiles.
+// reads), instead of rounds of 1024 tiles that each wait for their loads:
+// 4.9 against 5.0 us per pass at 2442 tiles, 2.6 against 3.0 at 489.
 template <int TI, int C>
 __global__ __launch_bounds__(TT) void sort_scan1_kernel(PassArgs a) {
   static_assert(C % 4 == 0, "16-byte groups");
