@@ -49,9 +49,8 @@ namespace {
 
 constexpr int kBuckets = kBucketCount;
 constexpr int CT = 256;             // bucket_count threads
-constexpr int CG = kBucketGroup;    // partition blocks per count block
+constexpr int CG = kBucketGroup;    // most partition blocks per count block
 constexpr int CU = 8;               // keys per thread per batch
-constexpr int64_t kGroupKeys = static_cast<int64_t>(CG) * kPartStageCap;   // a count block's region
 constexpr int ST = 512;             // bucket_solve threads: two waves per SIMD hide
                                     // the latency of each other's float64 chains
 constexpr int SW = ST / kWave;      // 8 waves
@@ -100,7 +99,7 @@ __device__ __forceinline__ int fixed_bits(int64_t m) {
 // a block's staging overflowed or |M| exceeds m_cap (the solve then reports
 // side 3).
 __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __restrict__ blk,
-                                                          int nblocks,
+                                                          int nblocks, int cg,
                                                           const float* __restrict__ stage_v,
                                                           int64_t m_cap, double c2,
                                                           uint32_t* __restrict__ acc_n,
@@ -125,9 +124,10 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wid = tid / kWave;
-  const int g0 = static_cast<int>(blockIdx.x) * CG;
+  const int g0 = static_cast<int>(blockIdx.x) * cg;
+  const int gw = (cg + kWave - 1) / kWave;   // waves holding the group's records
   // this thread's record of the group, loaded with the heads below
-  const bool own = tid < CG && g0 + tid < nblocks;
+  const bool own = tid < cg && g0 + tid < nblocks;
   const PartBlock rec = blk[own ? g0 + tid : 0];
 
   // 1. |M|, the range of M and any overflow over every block (the first 16
@@ -200,13 +200,13 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
       ro[wid] = ov;
     }
     __syncthreads();
-    if (tid < CG) {
+    if (tid < cg) {
       int32_t base = 0;
 #pragma unroll
       for (int w = 0; w < CG / kWave; ++w)
         if (w < wid) base += static_cast<int32_t>(wtot[w]);
       goff[tid] = base + incl - nm;
-      if (tid == CG - 1) goff[CG] = base + incl;
+      if (tid == cg - 1) goff[cg] = base + incl;
     }
     __syncthreads();
   }
@@ -222,7 +222,8 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
   const int32_t any_ov = aov != 0u ? 1 : 0;
   int32_t grp_ov = 0;
 #pragma unroll
-  for (int w = 0; w < CG / kWave; ++w) grp_ov |= ro[w];
+  for (int w = 0; w < CG / kWave; ++w)
+    if (w < gw) grp_ov |= ro[w];
   if (tid == 0) {
     CountPart cp;
     cp.TL = 0.0;
@@ -230,16 +231,19 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
     cp.nL = cp.nR = cp.nM = 0;
 #pragma unroll
     for (int w = 0; w < CG / kWave; ++w) {
-      cp.TL += rd[0][w];
-      cp.TR += rd[1][w];
-      cp.nL += ri[0][w];
-      cp.nR += ri[1][w];
-      cp.nM += ri[2][w];
+      if (w < gw) {
+        cp.TL += rd[0][w];
+        cp.TR += rd[1][w];
+        cp.nL += ri[0][w];
+        cp.nR += ri[1][w];
+        cp.nM += ri[2][w];
+      }
     }
     cp.overflow = grp_ov;
     cp.ndense = 0;
 #pragma unroll
-    for (int w = 0; w < CG / kWave; ++w) cp.ndense += rdn[w];
+    for (int w = 0; w < CG / kWave; ++w)
+      if (w < gw) cp.ndense += rdn[w];
     cp.pad = 0;
     cp.kmin = kmin;
     cp.kmax = kmax;
@@ -248,7 +252,7 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
     parts[blockIdx.x] = cp;
   }
   if (any_ov != 0 || m < 1 || m > m_cap) return;
-  const int cb = goff[CG];   // this group's members of M (no staging overflowed)
+  const int cb = goff[cg];   // this group's members of M (no staging overflowed)
   if (cb == 0) return;       // the solve skips a group with no members
 
   // 3. bucket sums of the group's members, CU keys per thread at a time;
@@ -262,11 +266,13 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
   }
   __syncthreads();
   auto member_key = [&](int j) -> uint32_t {
-    int lo = 0, hi = CG;   // goff[lo] <= j < goff[hi]
+    int lo = 0, hi = cg;   // goff[lo] <= j < goff[hi]
 #pragma unroll
-    for (int st = 0; st < 7; ++st) {   // CG = 2^7
-      const int mid = (lo + hi) >> 1;
-      if (goff[mid] <= j) lo = mid; else hi = mid;
+    for (int st = 0; st < 7; ++st) {   // cg <= CG = 2^7
+      if (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (goff[mid] <= j) lo = mid; else hi = mid;
+      }
     }
     return desc_key(stage_v[static_cast<int64_t>(g0 + lo) * kPartStageCap + (j - goff[lo])]);
   };
@@ -325,7 +331,7 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
     if (tid == CT - 1) bo[kBuckets] = run;
   }
   __syncthreads();
-  uint32_t* bk = bkeys + static_cast<int64_t>(blockIdx.x) * kGroupKeys;
+  uint32_t* bk = bkeys + static_cast<int64_t>(blockIdx.x) * cg * kPartStageCap;
   for (int j0 = 0; j0 < cb; j0 += CT * CU) {
     uint32_t kv[CU];
 #pragma unroll
@@ -708,7 +714,7 @@ __device__ double bucket_core(const uint32_t (&cnt)[BPT], const double (&U)[BPT]
 __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __restrict__ bkeys,
                                                           const uint32_t* __restrict__ boff,
                                                           const CountPart* __restrict__ parts,
-                                                          int ngroups, int64_t m_cap,
+                                                          int ngroups, int cg, int64_t m_cap,
                                                           const SelectRec* __restrict__ sel,
                                                           int use_sel, float aL_arg, float aR_arg,
                                                           uint32_t* __restrict__ acc_n,
@@ -828,7 +834,7 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
       const uint32_t* bo = boff + static_cast<int64_t>(grp) * (kBuckets + 1);
       const uint32_t from = bo[dstar];
       const uint32_t cnt_b = bo[dstar + 1] - from;
-      const uint32_t* bk = bkeys + static_cast<int64_t>(grp) * kGroupKeys + from;
+      const uint32_t* bk = bkeys + static_cast<int64_t>(grp) * cg * kPartStageCap + from;
       for (uint32_t j0 = 0; j0 < cnt_b; j0 += kGatherLanes * kGatherBatch) {
         uint32_t kv[kGatherBatch];
 #pragma unroll
@@ -1058,9 +1064,23 @@ hipError_t launch_row_bucket_forward(const float* scores, int64_t batch, int64_t
   return hipGetLastError();
 }
 
-int bucket_groups(int nblocks) { return (nblocks + CG - 1) / CG; }
+// Partition blocks per count block: the smallest power of two from 8 to CG
+// that keeps the groups within 32 (one lane each in the solve), so that a
+// short row with a wide middle set still spreads its counting over up to 32
+// blocks (a row of 2^20 scores with |M| = 1e5 gave its two count blocks of
+// 128 partition blocks 38.7 us).
+int bucket_group_size(int nblocks) {
+  int cg = CG;
+  while (cg > 8 && (nblocks + cg / 2 - 1) / (cg / 2) <= 32) cg /= 2;
+  return cg;
+}
+int bucket_groups(int nblocks) {
+  const int cg = bucket_group_size(nblocks);
+  return (nblocks + cg - 1) / cg;
+}
 size_t bucket_keys_words(int nblocks) {
-  return static_cast<size_t>(bucket_groups(nblocks)) * static_cast<size_t>(kGroupKeys);
+  return static_cast<size_t>(bucket_groups(nblocks)) * static_cast<size_t>(bucket_group_size(nblocks)) *
+         static_cast<size_t>(kPartStageCap);
 }
 size_t bucket_offs_words(int nblocks) {
   return static_cast<size_t>(bucket_groups(nblocks)) * (kBuckets + 1);
@@ -1071,15 +1091,16 @@ hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc ac
                                AttemptRec* host, uint32_t* host_seq, uint32_t seq, hipStream_t s) {
   if (ps.nblocks < 1 || ps.nblocks > kPartMaxBlocks) return hipErrorInvalidValue;
   const int groups = bucket_groups(ps.nblocks);   // <= 32: one lane each in the solve
+  const int cg = bucket_group_size(ps.nblocks);
   { ProfScope ps_("bucket_count", s);
   hipLaunchKernelGGL(bucket_count_kernel, dim3(static_cast<unsigned>(groups)), dim3(CT), 0, s,
-                     ps.blk, ps.nblocks, ps.stage_v, m_cap, kLog2e / t, acc.n, acc.u, acc.d,
+                     ps.blk, ps.nblocks, cg, ps.stage_v, m_cap, kLog2e / t, acc.n, acc.u, acc.d,
                      acc.keys, acc.offs, acc.parts); }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("bucket_solve", s);
   hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, acc.keys, acc.offs, acc.parts,
-                     groups, m_cap, ps.sel, ps.use_sel, ps.aL, ps.aR, acc.n, acc.u, acc.d, tot, k,
+                     groups, cg, m_cap, ps.sel, ps.use_sel, ps.aL, ps.aR, acc.n, acc.u, acc.d, tot, k,
                      t, n_total, out, host, host_seq, seq); }
   return hipGetLastError();
 }

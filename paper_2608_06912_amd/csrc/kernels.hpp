@@ -296,7 +296,8 @@ hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, in
                                 hipStream_t s);
 // Middle set solved by buckets of keys (only the bucket holding the root is
 // sorted), straight from the partition's staging: count block c takes the
-// staged M of partition blocks [c kBucketGroup, (c+1) kBucketGroup), and the
+// staged M of partition blocks [c g, (c+1) g) with g =
+// bucket_group_size(nblocks) (at most kBucketGroup), and the
 // solve also forms the partition totals (*tot) in a fixed order.  acc:
 // bucket accumulators, zero on entry and left zero (keys, offs, parts:
 // scratch).  The record reports ok = 0 with side = 2 when the root's bucket
@@ -305,7 +306,7 @@ hipError_t launch_small_m_solve(const uint32_t* m_keys, const int32_t* m_idx, in
 // and solves it by the full sort.
 constexpr int kBucketCount = 2048;
 constexpr int kBucketSortCap = 4096;
-constexpr int kBucketGroup = 128;   // partition blocks per count block
+constexpr int kBucketGroup = 128;   // most partition blocks per count block
 // One count block's share of the partition totals, and the range and size
 // of all of M (the same in every count block).
 struct alignas(16) CountPart {
@@ -327,6 +328,7 @@ struct BucketAcc {
   CountPart* parts;         // [bucket_groups(nblocks)]
 };
 constexpr int64_t kBucketAccWords = kBucketCount * 5;   // u32 words of n, u, d
+int bucket_group_size(int nblocks);
 int bucket_groups(int nblocks);
 size_t bucket_keys_words(int nblocks);
 size_t bucket_offs_words(int nblocks);

@@ -517,6 +517,22 @@ def test_bracketed_large_middle_set(lib):
     assert np.max(np.abs(p[idx].astype(np.float64) - O.probs(r[idx], bo, alpha))) <= P_TOL
 
 
+def test_bracketed_wide_middle_set_in_a_short_row(lib):
+    """A row of 2^20 scores with a wide middle set (k = n/20, alpha = -0.05:
+    about 24000 scores, against 5400 in a row of 1e7 at k = 2000, alpha =
+    -0.01): 256 partition blocks counted in 32 groups of 8.  b, p, the
+    bracket and the backward against the oracle."""
+    n = 1 << 20
+    r = W.random_case(23, n, dist="normal")[0]
+    k, alpha, K = n / 20.0, -0.05, W.default_sample_size(n)
+    noise = W.laplace_noise([79], K, 0.05)
+    g = W.random_case(123, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label="wide M, 2^20", g=g)
+    assert info["n_M"] > 20_000 and not info["fell_back"]
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
+    assert O.budget_error(p, k) <= sum_tol(k)
+
+
 def test_bracketed_band_with_scores_above_it(lib):
     # k = n/3 puts a_R inside the sample, so scores at or above a_R + 18 t
     # are written as 1 from their bits; a ragged length exercises the last
