@@ -368,7 +368,7 @@ def config_table(dev, main):
 
 def paper_setting(dev):
     """The paper's headline setting (abstract, Table ks-main): one row of
-    Gaussian scores, k = n/16, alpha = -1, dispatched (sort up to 2^20
+    Gaussian scores, k = n/16, alpha = -1, dispatched (sort up to 2^18
     scores, the bracket above); forward alone and forward + backward.  The
     paper's forward times on its laptop GPU are 0.41 / 1.15 / 5.23 ms."""
     import torch
@@ -392,7 +392,7 @@ def comparators(dev):
     """The paper's comparisons on this device: the per-query bisection
     baseline at B = 256, n = 4096 (§5 "Speed"); DFTopK forward + backward at
     k = floor(n/2), batch 1 (Suppl. "Comparison with DFTopK" protocol)
-    against the operator's forward + backward (sort up to 2^20 scores, the
+    against the operator's forward + backward (sort up to 2^18 scores, the
     bracket above); the realised budget error on Gaussian scores, k = n/16,
     alpha = -1 (Table budget).  Synthetic Gaussian scores throughout."""
     import numpy as np

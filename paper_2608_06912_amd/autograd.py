@@ -29,12 +29,13 @@ __all__ = ["soft_topk", "hard_topk_mask", "straight_through", "choose_path", "sa
            "bracket_noise", "bracket_indices", "LapSumFunction", "FULL_SORT_MAX_N"]
 
 # Rows up to this length take the full sort; longer rows the sample bracket.
-# §4 places the switch where the two paths cost the same; on MI355X the
-# forward + backward of one row costs 0.091 ms (sort) against 0.120 ms
-# (bracket) at n = 2^19, 0.114 against 0.111 ms at 2^20 and 0.162 against
-# 0.109 ms at 2^21; per row in batches of 8 the switch falls in the same
-# place.
-FULL_SORT_MAX_N = 1 << 20
+# §4 places the switch where the two paths cost the same.  On MI355X, one
+# Gaussian row, forward + backward, sort against bracket: 0.065 / 0.072 ms
+# at n = 2^17, 0.069 / 0.072 at 2^18, 0.076 / 0.074 at 4e5 and 0.088 / 0.072
+# at 2^20 with k = n/20, alpha = -0.05; 0.069 / 0.069 at 2^18 and 0.075 /
+# 0.071 at 4e5 with k = n/16, alpha = -1; with k = 1000, alpha = -0.05 the
+# bracket is ahead from 2^17 on.  Batches of 8 rows of 2^18: 0.533 / 0.487.
+FULL_SORT_MAX_N = 1 << 18
 
 
 def choose_path(n: int) -> str:
