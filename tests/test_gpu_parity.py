@@ -783,12 +783,12 @@ def test_bracketed_rows_of_about_one_tile(lib, n):
     assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
 
 
-@pytest.mark.parametrize("n", [200_000, 3_000_000])
+@pytest.mark.parametrize("n", [60_000, 200_000, 3_000_000])
 def test_bracketed_select_bin_sizes(lib, n):
     # half of the scores in [1, 1.25), one bin of the select's top 11 bits,
     # with the budget's quantile inside it: that bin holds about K/2 sample
-    # keys (n = 2e5: about 1700, ranked in LDS; n = 3e6: about 10000, ranked
-    # by passes over all sample keys)
+    # keys (n = 6e4: about 770 and n = 2e5: about 1700, ranked in LDS; n =
+    # 3e6: about 10000, ranked by passes over all sample keys)
     rng = np.random.default_rng([43, n])
     r = rng.standard_normal(n).astype(np.float32)
     inside = rng.random(n) < 0.5
