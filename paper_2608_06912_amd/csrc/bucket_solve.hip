@@ -29,7 +29,8 @@
 //
 // Two launches, straight from the partition's per-block staging (the
 // order of M within a bucket does not matter): bucket_count (one block per
-// kBucketGroup partition blocks) and bucket_solve (one workgroup).  Every
+// group of 8 to kBucketGroup partition blocks, at most 32 groups) and
+// bucket_solve (one workgroup).  Every
 // count block derives |M| and the range of M from the block records itself
 // (integer min / max of keys, so all agree exactly) and folds its group's
 // tails in a fixed order; bucket_solve folds those partials, so the host
