@@ -99,8 +99,9 @@ __device__ __forceinline__ int fixed_bits(int64_t m) {
 // partial of the totals to parts[c] whatever happens; it counts nothing when
 // a block's staging overflowed or |M| exceeds m_cap (the solve then reports
 // side 3).
+template <int cg>
 __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __restrict__ blk,
-                                                          int nblocks, int cg,
+                                                          int nblocks,
                                                           const float* __restrict__ stage_v,
                                                           int64_t m_cap, double c2,
                                                           uint32_t* __restrict__ acc_n,
@@ -126,7 +127,8 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
   const int lane = lane_id();
   const int wid = tid / kWave;
   const int g0 = static_cast<int>(blockIdx.x) * cg;
-  const int gw = (cg + kWave - 1) / kWave;   // waves holding the group's records
+  constexpr int gw = (cg + kWave - 1) / kWave;   // waves holding the group's records
+  static_assert(cg >= 1 && cg <= CG && (cg & (cg - 1)) == 0, "a power of two up to CG");
   // this thread's record of the group, loaded with the heads below
   const bool own = tid < cg && g0 + tid < nblocks;
   const PartBlock rec = blk[own ? g0 + tid : 0];
@@ -269,11 +271,9 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
   auto member_key = [&](int j) -> uint32_t {
     int lo = 0, hi = cg;   // goff[lo] <= j < goff[hi]
 #pragma unroll
-    for (int st = 0; st < 7; ++st) {   // cg <= CG = 2^7
-      if (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (goff[mid] <= j) lo = mid; else hi = mid;
-      }
+    for (int w = cg; w > 1; w >>= 1) {
+      const int mid = (lo + hi) >> 1;
+      if (goff[mid] <= j) lo = mid; else hi = mid;
     }
     return desc_key(stage_v[static_cast<int64_t>(g0 + lo) * kPartStageCap + (j - goff[lo])]);
   };
@@ -332,7 +332,7 @@ __global__ __launch_bounds__(CT) void bucket_count_kernel(const PartBlock* __res
     if (tid == CT - 1) bo[kBuckets] = run;
   }
   __syncthreads();
-  uint32_t* bk = bkeys + static_cast<int64_t>(blockIdx.x) * cg * kPartStageCap;
+  uint32_t* bk = bkeys + static_cast<int64_t>(blockIdx.x) * (static_cast<int64_t>(cg) * kPartStageCap);
   for (int j0 = 0; j0 < cb; j0 += CT * CU) {
     uint32_t kv[CU];
 #pragma unroll
@@ -715,7 +715,8 @@ __device__ double bucket_core(const uint32_t (&cnt)[BPT], const double (&U)[BPT]
 __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __restrict__ bkeys,
                                                           const uint32_t* __restrict__ boff,
                                                           const CountPart* __restrict__ parts,
-                                                          int ngroups, int cg, int64_t m_cap,
+                                                          int ngroups, int64_t gstride,
+                                                          int64_t m_cap,
                                                           const SelectRec* __restrict__ sel,
                                                           int use_sel, float aL_arg, float aR_arg,
                                                           uint32_t* __restrict__ acc_n,
@@ -835,7 +836,7 @@ __global__ __launch_bounds__(ST) void bucket_solve_kernel(const uint32_t* __rest
       const uint32_t* bo = boff + static_cast<int64_t>(grp) * (kBuckets + 1);
       const uint32_t from = bo[dstar];
       const uint32_t cnt_b = bo[dstar + 1] - from;
-      const uint32_t* bk = bkeys + static_cast<int64_t>(grp) * cg * kPartStageCap + from;
+      const uint32_t* bk = bkeys + static_cast<int64_t>(grp) * gstride + from;
       for (uint32_t j0 = 0; j0 < cnt_b; j0 += kGatherLanes * kGatherBatch) {
         uint32_t kv[kGatherBatch];
 #pragma unroll
@@ -1094,15 +1095,26 @@ hipError_t launch_bucket_solve(const PartSource& ps, int64_t m_cap, BucketAcc ac
   const int groups = bucket_groups(ps.nblocks);   // <= 32: one lane each in the solve
   const int cg = bucket_group_size(ps.nblocks);
   { ProfScope ps_("bucket_count", s);
-  hipLaunchKernelGGL(bucket_count_kernel, dim3(static_cast<unsigned>(groups)), dim3(CT), 0, s,
-                     ps.blk, ps.nblocks, cg, ps.stage_v, m_cap, kLog2e / t, acc.n, acc.u, acc.d,
-                     acc.keys, acc.offs, acc.parts); }
+#define LAPSUM_COUNT(G)                                                                          \
+  hipLaunchKernelGGL(bucket_count_kernel<G>, dim3(static_cast<unsigned>(groups)), dim3(CT), 0, s, \
+                     ps.blk, ps.nblocks, ps.stage_v, m_cap, kLog2e / t, acc.n, acc.u, acc.d,      \
+                     acc.keys, acc.offs, acc.parts)
+  switch (cg) {
+    case 8: LAPSUM_COUNT(8); break;
+    case 16: LAPSUM_COUNT(16); break;
+    case 32: LAPSUM_COUNT(32); break;
+    case 64: LAPSUM_COUNT(64); break;
+    default: LAPSUM_COUNT(CG); break;
+  }
+#undef LAPSUM_COUNT
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   { ProfScope ps_("bucket_solve", s);
   hipLaunchKernelGGL(bucket_solve_kernel, dim3(1), dim3(ST), 0, s, acc.keys, acc.offs, acc.parts,
-                     groups, cg, m_cap, ps.sel, ps.use_sel, ps.aL, ps.aR, acc.n, acc.u, acc.d, tot, k,
-                     t, n_total, out, host, host_seq, seq); }
+                     groups, static_cast<int64_t>(cg) * kPartStageCap, m_cap, ps.sel, ps.use_sel,
+                     ps.aL, ps.aR, acc.n, acc.u, acc.d, tot, k, t, n_total, out, host, host_seq,
+                     seq); }
   return hipGetLastError();
 }
 
