@@ -533,6 +533,22 @@ def test_bracketed_wide_middle_set_in_a_short_row(lib):
     assert O.budget_error(p, k) <= sum_tol(k)
 
 
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("n", [1_500_000, 6_000_000])
+def test_bracketed_count_group_sizes(lib, n):
+    """Rows whose partition grids give the middle-set count blocks groups of
+    16 (367 partition blocks) and of 64 (1465): b, p, the bracket and the
+    backward against the oracle."""
+    r = W.random_case(29, n, dist="normal")[0]
+    k, alpha, K = n / 20.0, -0.05, W.default_sample_size(n)
+    noise = W.laplace_noise([81, n], K, 0.05)
+    g = W.random_case(129, n, dist="normal")[0]
+    p, b, bo, info = _check_bracketed(lib, r, k, alpha, noise, label=f"groups n={n}", g=g)
+    assert not info["fell_back"]
+    assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
+    assert O.budget_error(p, k) <= sum_tol(k)
+
+
 def test_bracketed_band_with_scores_above_it(lib):
     # k = n/3 puts a_R inside the sample, so scores at or above a_R + 18 t
     # are written as 1 from their bits; a ragged length exercises the last
