@@ -607,13 +607,23 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
         inM[e] = ok[e] && !(v[e] < aL);
       }
     }
+    // formed directly with both tails: a score lies in at most one of them,
+    // so one exponential per score serves both (the lower tail's below)
+    float ex[4];
+    if constexpr (DIRECT && HAS_R) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ex[e] = exp2_fast((v[e] < aL ? v[e] - aL : aR - v[e]) * c2f);
+    }
     if constexpr (HAS_R) {
       float tr = 0.0f;
       uint32_t ob = 0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const bool R = v[e] >= aR;
-        tr += (ok[e] && R) ? exp2_fast((aR - v[e]) * c2f) : 0.0f;
+        if constexpr (DIRECT)
+          tr += (ok[e] && R) ? ex[e] : 0.0f;
+        else
+          tr += (ok[e] && R) ? exp2_fast((aR - v[e]) * c2f) : 0.0f;
         st.nR += (ok[e] && R) ? 1 : 0;
         if (ok[e] && v[e] >= bw.hi) ob |= 1u << e;
       }
@@ -666,7 +676,15 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
         }
       };
       if constexpr (DIRECT) {
-        direct_tl(v, ok);
+        if constexpr (HAS_R) {
+          float tl = 0.0f;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (ok[e] && !(v[e] < bw.lo) && v[e] < aL) tl += ex[e];
+          st.TL += static_cast<double>(tl);
+        } else {
+          direct_tl(v, ok);
+        }
         st.nB = nb0 + static_cast<uint32_t>(__popcll(bm[0]) + __popcll(bm[1]) + __popcll(bm[2]) +
                                             __popcll(bm[3]));
         stage_all_m();
