@@ -19,7 +19,7 @@ is reported on the bytes its kernels must move (path_roofline), against the
 8 TB/s peak and against a device copy measured in the same run.
 
 Per workload (configs): forward, backward and forward + backward per call
-(median and mean over 30 calls timed with events after 3 warm-ups), scores/s
+(median and mean over 50 calls timed with events after 3 warm-ups), scores/s
 and the fraction of the HBM peak for the bytes the path's kernels must move
 (roofline_frac: every streaming kernel that runs, counted from the event
 profiler, times its algorithmic bytes per launch); model_equivalent_frac
@@ -293,7 +293,7 @@ def model_bytes(w, path, n_M=0):
     return 32.0 * N + 8.0 * (w.sample_size or 0) + 72.0 * n_M
 
 
-def run_workload(dev, name, path, iters=30):
+def run_workload(dev, name, path, iters=50):
     """fwd, bwd and fwd + bwd per call of one synthetic workload."""
     import torch
 
