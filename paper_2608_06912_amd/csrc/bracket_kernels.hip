@@ -591,7 +591,10 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
   };
   // it: first score of this wave's 256-score step (a multiple of 256).
   // DIRECT: the band is not staged, each member's lower-tail term is formed
-  // as it is met
+  // as it is met.  The wave's list is then incomplete and its block takes
+  // the dense passes, which read neither the band count nor the bits of
+  // r >= hi: DIRECT leaves nB as it was when staging stopped (above the
+  // list's capacity) and forms no bits.
   auto one = [&](auto direct, const float (&v)[4], const bool (&ok)[4], int64_t it) {
     constexpr bool DIRECT = decltype(direct)::value;
     const int64_t i0 = it + 4 * lane;
@@ -607,6 +610,35 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
         inM[e] = ok[e] && !(v[e] < aL);
       }
     }
+    // M members of the step: staged in index order, with the range of M
+    auto stage_m = [&](float x, int64_t i, uint32_t at) {
+      st.mmin = fminf(st.mmin, x);
+      st.mmax = fmaxf(st.mmax, x);
+      if (at < static_cast<uint32_t>(kWaveStage)) {
+        sv[at] = x;
+        si[at] = static_cast<int32_t>(i);
+      }
+    };
+    auto stage_all_m = [&]() {
+      if (__ballot(inM[0] || inM[1] || inM[2] || inM[3])) {
+        uint32_t before = 0, total = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint64_t bal = __ballot(inM[e]);
+          before += lanes_below(bal);
+          total += static_cast<uint32_t>(__popcll(bal));
+        }
+        uint32_t at = static_cast<uint32_t>(st.nM) + before;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (inM[e]) {
+            stage_m(v[e], i0 + e, at);
+            ++at;
+          }
+        }
+        st.nM += total;
+      }
+    };
     // formed directly with both tails: a score lies in at most one of them,
     // so one exponential per score serves both (the lower tail's below)
     float ex[4];
@@ -625,15 +657,32 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
         else
           tr += (ok[e] && R) ? exp2_fast((aR - v[e]) * c2f) : 0.0f;
         st.nR += (ok[e] && R) ? 1 : 0;
-        if (ok[e] && v[e] >= bw.hi) ob |= 1u << e;
+        if constexpr (!DIRECT)
+          if (ok[e] && v[e] >= bw.hi) ob |= 1u << e;
       }
       st.TR += static_cast<double>(tr);
-      // 8 lanes hold the 32 bits of one word
-      uint32_t x = ob << (4 * (lane & 7));
-      x |= __shfl_xor(x, 1, kWave);
-      x |= __shfl_xor(x, 2, kWave);
-      x |= __shfl_xor(x, 4, kWave);
-      if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
+      if constexpr (!DIRECT) {
+        // 8 lanes hold the 32 bits of one word
+        uint32_t x = ob << (4 * (lane & 7));
+        x |= __shfl_xor(x, 1, kWave);
+        x |= __shfl_xor(x, 2, kWave);
+        x |= __shfl_xor(x, 4, kWave);
+        if (bw.stage && (lane & 7) == 0) bw.sones[((it - bw.w0) >> 5) + (lane >> 3)] = x;
+      }
+    }
+    if constexpr (DIRECT) {
+      // a lower-tail term lies in the band (lo <= r < a_L <= hi)
+      if constexpr (HAS_R) {
+        float tl = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (ok[e] && !(v[e] < bw.lo) && v[e] < aL) tl += ex[e];
+        st.TL += static_cast<double>(tl);
+      } else {
+        direct_tl(v, ok);
+      }
+      stage_all_m();
+      return;
     }
     // band members take slots in index order from the masks and the wave's
     // running count.  M lies inside the band (lo <= a_L, hi >= a_R, both
@@ -646,50 +695,6 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
     if (any) {
       const uint32_t nb0 = static_cast<uint32_t>(st.nB);   // uniform across the wave
       const uint32_t cap = static_cast<uint32_t>(bw.cap);
-      // M members of the step: staged in index order, with the range of M
-      auto stage_m = [&](float x, int64_t i, uint32_t at) {
-        st.mmin = fminf(st.mmin, x);
-        st.mmax = fmaxf(st.mmax, x);
-        if (at < static_cast<uint32_t>(kWaveStage)) {
-          sv[at] = x;
-          si[at] = static_cast<int32_t>(i);
-        }
-      };
-      auto stage_all_m = [&]() {
-        if (__ballot(inM[0] || inM[1] || inM[2] || inM[3])) {
-          uint32_t before = 0, total = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const uint64_t bal = __ballot(inM[e]);
-            before += lanes_below(bal);
-            total += static_cast<uint32_t>(__popcll(bal));
-          }
-          uint32_t at = static_cast<uint32_t>(st.nM) + before;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (inM[e]) {
-              stage_m(v[e], i0 + e, at);
-              ++at;
-            }
-          }
-          st.nM += total;
-        }
-      };
-      if constexpr (DIRECT) {
-        if constexpr (HAS_R) {
-          float tl = 0.0f;
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (ok[e] && !(v[e] < bw.lo) && v[e] < aL) tl += ex[e];
-          st.TL += static_cast<double>(tl);
-        } else {
-          direct_tl(v, ok);
-        }
-        st.nB = nb0 + static_cast<uint32_t>(__popcll(bm[0]) + __popcll(bm[1]) + __popcll(bm[2]) +
-                                            __popcll(bm[3]));
-        stage_all_m();
-        return;
-      }
       const uint64_t two = (bm[0] & (bm[1] | bm[2] | bm[3])) | (bm[1] & (bm[2] | bm[3])) |
                            (bm[2] & bm[3]);   // lanes with two or more members
       if (two == 0ull) {
@@ -785,11 +790,42 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
     // last whole batch, or after the batch where staging stopped).  The
     // staged and the direct passes are separate loops, so that neither
     // carries the other's registers
+    // the wave's first batch says its list will overflow: it holds more
+    // band members than the list, or, counted over all the wave's batches
+    // at its rate, more than twice as many.  A wrong guess (a row whose
+    // band members bunch at the start of a wave) only costs speed: the
+    // block takes the dense passes, which are exact for every score.
+    auto crowded = [&](const float4 (&q)[U]) -> bool {
+      uint32_t c = 0;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float v[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          bool in = !(v[e] < bw.lo);
+          if constexpr (HAS_R) in = in && !(v[e] >= bw.hi);
+          c += static_cast<uint32_t>(__popcll(__ballot(in)));
+        }
+      }
+      const int64_t nb = (w1 - w0) / (U * 256);
+      const int64_t cap = bw.cap;
+      return c > cap || static_cast<int64_t>(c) * nb > 2 * cap;
+    };
     auto stream = [&](auto direct, int64_t from) -> int64_t {
+      constexpr bool DIRECT = decltype(direct)::value;
       int64_t at = from;
       if (at + U * 256 > w1) return at;
       float4 qa[U], qb[U];
       load(qa, at, true);
+      if constexpr (!DIRECT) {
+        if (at == w0 && crowded(qa)) {
+          // no list: every batch, this one included (read again, from
+          // the L2 as a rule), is formed by the direct loop
+          spill = true;
+          listed = 0;
+          return at;
+        }
+      }
       while (true) {
         const int64_t ca = at;
         at += U * 256;
@@ -1031,7 +1067,9 @@ __global__ __launch_bounds__(PT) void partition_kernel(const float* __restrict__
     partition_range<HAS_R, false>(r, w0, w1, vec, aL, aR, c2f, sv[wid], si[wid], bw, st, tb);
   // this wave's bits and band list out of LDS
   if (bw.stage) {
-    if (has_r) {
+    // a wave whose list is incomplete formed no bits once staging stopped;
+    // its block takes the dense passes, which do not read them
+    if (has_r && st.nB <= bw.cap) {
       const int nw = static_cast<int>((w1 - w0 + 31) / 32);   // <= kOnesWaveWords
       for (int q = lane; q < nw; q += kWave) ones[(w0 >> 5) + q] = bw.sones[q];
     }

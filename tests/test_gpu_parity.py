@@ -690,6 +690,45 @@ def test_bracketed_dense_and_listed_blocks_in_one_row(lib):
     assert np.max(np.abs(p.astype(np.float64) - O.probs(r, bo, alpha))) <= P_TOL
 
 
+@pytest.mark.timeout(600)
+def test_bracketed_band_bunched_at_wave_starts(lib):
+    # A partition wave of three or more 1024-score batches guesses from its
+    # first batch whether its band list (512 entries) will overflow.  Here
+    # the first batch of every wave of 100 partition blocks holds 360 scores
+    # inside the band just below a_L and the rest of the wave about 60 more:
+    # 3 x ~390 > 2 x 512 makes those 400 waves skip their lists although
+    # at most ~470 members would have fitted.  Their blocks take the dense
+    # form (tiles written from r); the values must be the oracle's all the
+    # same.  n = 3 * 2^24 gives 4096 blocks of 12288 scores (waves of 3072).
+    import torch
+    n, chunk, wave, P = 3 * 2**24, 12288, 3072, 360
+    r = W.random_case(41, n, dist="normal")[0]
+    k, alpha = n / 4.0, -0.0004
+    v = np.float32(np.quantile(r, 1.0 - k / n))
+    extra = W.random_case(42, 100 * 4 * P, dist="normal")[0].reshape(100, 4, P)
+    for bi, blk in enumerate(range(100, 200)):
+        for w in range(4):
+            s = blk * chunk + w * wave
+            r[s:s + P] = v - np.float32(0.03) + np.float32(0.002) * extra[bi, w]
+    K = W.default_sample_size(n)
+    noise = W.laplace_noise([88], K, -alpha)
+    g = W.random_case(43, n, dist="normal")[0]
+    p, _, bo, info = _check_bracketed(lib, r, k, alpha, noise, label="bunched", g=g)
+    assert not info["fell_back"]
+    _full_p_check(p, r, bo, alpha, "bunched")
+    # the saved context: its header (mode, blocks, chunk, capacity) and one
+    # 32-byte record per partition block (four wave counts, dense flag)
+    band = lib.new_band(1, n, "cuda")
+    lib.lapsum_forward_bracketed(_t(r[None, :]), k, alpha, _t(noise), band=band)
+    torch.cuda.synchronize()
+    head = band[:256].cpu().numpy()
+    mode, nblocks = head[:8].view(np.int32)
+    assert (mode, nblocks, int(head[8:16].view(np.int64)[0])) == (0, 4096, chunk)
+    recs = band[256:256 + 32 * nblocks].cpu().numpy().view(np.int32).reshape(nblocks, 8)
+    dense = recs[:, 4]
+    assert np.all(dense[100:200] == 1) and dense.sum() == 100
+
+
 def test_bracketed_batched_rows_of_odd_length(lib):
     # rows of a batch start 4 n bytes apart: with n odd they are not 16-byte
     # aligned, and the passes take their scalar paths
