@@ -61,7 +61,7 @@ MEASURED_TRAFFIC = {
     "band_emit": ("band_kernels.hip", "a2cc89e2dda7261606ca50608c3385980b6a5be5", 427.2e6),
     "band_vjp_emit": ("band_kernels.hip", "a2cc89e2dda7261606ca50608c3385980b6a5be5", 443.6e6),
     "band_vjp_reduce": ("band_kernels.hip", "a2cc89e2dda7261606ca50608c3385980b6a5be5", 61.3e6),
-    "partition": ("bracket_kernels.hip", "784985dc929bf118eed8f22540ff5f4be70f5d9c", 413.9e6),
+    "partition": ("bracket_kernels.hip", "c4bd1de42484ac9b4ef40873dca4b3ad95445e69", 413.7e6),
 }
 METRIC = "fwd+bwd ms/call and scores/sec at n=1e6/1e7/1e8; % HBM roofline"
 # The paper's dispatched forward times in its headline setting (abstract,

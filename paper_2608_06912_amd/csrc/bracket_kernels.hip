@@ -790,23 +790,22 @@ __device__ __forceinline__ void partition_range(const float* __restrict__ r, int
     // last whole batch, or after the batch where staging stopped).  The
     // staged and the direct passes are separate loops, so that neither
     // carries the other's registers
-    // the wave's first batch says its list will overflow: it holds more
-    // band members than the list, or, counted over all the wave's batches
-    // at its rate, more than twice as many.  A wrong guess (a row whose
-    // band members bunch at the start of a wave) only costs speed: the
-    // block takes the dense passes, which are exact for every score.
+    // the start of the wave's first batch says its list will overflow: the
+    // band members among the batch's first 256 scores, times U, exceed the
+    // list, or, counted over all the wave's batches at that rate, twice the
+    // list.  A wrong guess (a row whose band members bunch at the start of
+    // a wave) only costs speed: the block takes the dense passes, which are
+    // exact for every score.
     auto crowded = [&](const float4 (&q)[U]) -> bool {
+      const float v[4] = {q[0].x, q[0].y, q[0].z, q[0].w};
       uint32_t c = 0;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float v[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          bool in = !(v[e] < bw.lo);
-          if constexpr (HAS_R) in = in && !(v[e] >= bw.hi);
-          c += static_cast<uint32_t>(__popcll(__ballot(in)));
-        }
+      for (int e = 0; e < 4; ++e) {
+        bool in = !(v[e] < bw.lo);
+        if constexpr (HAS_R) in = in && !(v[e] >= bw.hi);
+        c += static_cast<uint32_t>(__popcll(__ballot(in)));
       }
+      c *= U;
       const int64_t nb = (w1 - w0) / (U * 256);
       const int64_t cap = bw.cap;
       return c > cap || static_cast<int64_t>(c) * nb > 2 * cap;

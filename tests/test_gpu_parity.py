@@ -692,12 +692,12 @@ def test_bracketed_dense_and_listed_blocks_in_one_row(lib):
 
 @pytest.mark.timeout(600)
 def test_bracketed_band_bunched_at_wave_starts(lib):
-    # A partition wave of three or more 1024-score batches guesses from its
-    # first batch whether its band list (512 entries) will overflow.  Here
-    # the first batch of every wave of 100 partition blocks holds 360 scores
-    # inside the band just below a_L and the rest of the wave about 60 more:
-    # 3 x ~390 > 2 x 512 makes those 400 waves skip their lists although
-    # at most ~470 members would have fitted.  Their blocks take the dense
+    # A partition wave of three or more 1024-score batches guesses from the
+    # first 256 scores of its first batch whether its band list (512
+    # entries) will overflow.  Here each wave of 100 partition blocks starts
+    # with 360 scores inside the band just below a_L and holds about 100
+    # more: 256 x 4 x 3 > 2 x 512 makes those 400 waves skip their lists
+    # although at most ~470 members would have fitted.  Their blocks take the dense
     # form (tiles written from r); the values must be the oracle's all the
     # same.  n = 3 * 2^24 gives 4096 blocks of 12288 scores (waves of 3072).
     import torch
